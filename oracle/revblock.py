@@ -1,0 +1,106 @@
+"""Residual functions and the reversible block (Sec. 3.2, Fig. 2; Eqs. 4-5).
+
+A residual function is a chain of conv -> BN(train) layers with a ReLU after
+every BN except the last:
+  basic      : conv3x3 - BN - ReLU - conv3x3 - BN
+  bottleneck : conv1x1 - BN - ReLU - conv3x3 - BN - ReLU - conv1x1 - BN
+It has no skip connection of its own: the skip lives in the coupling.
+
+The activation is split along channels into two equal streams {x1, x2}
+(Sec. 3.2 and the caption of Fig. 2).  The primitive is the additive
+half-coupling (a, b) -> (a + Phi(b), b), whose inverse subtracts Phi(b)
+instead of adding it (Sec. 3.2, "reverse forward").  A block is two
+half-couplings, F on x2 then G on the updated first stream:
+    y1 = x1 + F(x2)          x2~ = y2 - G(y1)
+    y2 = x2 + G(y1)          x1~ = y1 - F(x2~)
+(reading: the two-function coupling of the RevNet the paper builds on; the
+single-function form of Sec. 3.2 is one half-coupling.)
+
+Backward of a block (Eq. 4 and Eq. 5, Alg. 1 "reconstruct and keep the
+computational graph"): the graph of each function is rebuilt while its input
+is reconstructed, and the VJP runs through that rebuilt graph, so no separate
+forward pass is needed (Sec. 4.2).
+"""
+from __future__ import annotations
+
+from typing import List, Sequence, Tuple
+
+import numpy as np
+
+from . import bn, conv
+
+Layer = Tuple[np.ndarray, np.ndarray, np.ndarray]   # (W [O,R,S,I], gamma [O], beta [O])
+
+
+def function_forward(u: np.ndarray, layers: Sequence[Layer], eps: float):
+    """Returns (output, graph); graph keeps what the VJP needs."""
+    graph = []
+    a = u
+    for l, (w, g, b) in enumerate(layers):
+        h = conv.forward(a, w)
+        o, cache = bn.forward(h, g, b, eps)
+        graph.append((a, h, o, cache))
+        a = o if l == len(layers) - 1 else np.maximum(o, 0.0)
+    return a, graph
+
+
+def function_vjp(d: np.ndarray, layers: Sequence[Layer], graph):
+    """VJP through a rebuilt graph.  Returns (d_input, [(dW, dgamma, dbeta)...])."""
+    grads: List = [None] * len(layers)
+    for l in reversed(range(len(layers))):
+        w, g, _ = layers[l]
+        a, _, o, cache = graph[l]
+        if l != len(layers) - 1:
+            d = d * (o > 0.0)          # ReLU; derivative taken as 0 at 0
+        dh, dg, db = bn.backward(d, cache, g)
+        grads[l] = (conv.wgrad(a, dh, w.shape), dg, db)
+        d = conv.dgrad(dh, w, a.shape)
+    return d, grads
+
+
+def batch_stats(graph):
+    """(mean, var, m) of every BN of a rebuilt graph, for the running statistics."""
+    out = []
+    for (_, h, _, cache) in graph:
+        m = h.shape[0] * h.shape[1] * h.shape[2]
+        out.append((cache, m))
+    return out
+
+
+def couple(a: np.ndarray, b: np.ndarray, layers: Sequence[Layer], eps: float) -> np.ndarray:
+    """Additive half-coupling: a + Phi(b)."""
+    f, _ = function_forward(b, layers, eps)
+    return a + f
+
+
+def block_forward(x1, x2, f_layers, g_layers, eps):
+    """y1 = x1 + F(x2); y2 = x2 + G(y1)."""
+    y1 = couple(x1, x2, f_layers, eps)
+    y2 = couple(x2, y1, g_layers, eps)
+    return y1, y2
+
+
+def block_inverse(y1, y2, f_layers, g_layers, eps):
+    """Reconstruction only: x2 = y2 - G(y1); x1 = y1 - F(x2)."""
+    g, _ = function_forward(y1, g_layers, eps)
+    x2 = y2 - g
+    f, _ = function_forward(x2, f_layers, eps)
+    return y1 - f, x2
+
+
+def block_reconstruct_vjp(y1, y2, g1, g2, f_layers, g_layers, eps):
+    """Reconstruct the block input from its output and take the VJP.
+
+    g1, g2 are the gradients with respect to y1, y2.  Returns a dict with the
+    reconstructed inputs x1, x2, the input gradients dx1, dx2, the parameter
+    gradients of F and G, and the BN statistics observed while rebuilding.
+    """
+    gout, g_graph = function_forward(y1, g_layers, eps)
+    x2 = y2 - gout
+    u, dG = function_vjp(g2, g_layers, g_graph)
+    z1 = g1 + u                       # total gradient reaching y1
+    fout, f_graph = function_forward(x2, f_layers, eps)
+    x1 = y1 - fout
+    w, dF = function_vjp(z1, f_layers, f_graph)
+    return dict(x1=x1, x2=x2, dx1=z1, dx2=g2 + w, dF=dF, dG=dG,
+                stats_F=batch_stats(f_graph), stats_G=batch_stats(g_graph))
