@@ -1,0 +1,246 @@
+"""Multi-stage PETRA schedule on a RevNet-shaped network (Alg. 1, Eq. 5,
+Sec. 3.2 "Non-reversible stages", App. B delays).
+
+Network (CIFAR-style RevNet, Sec. 4.1 "Model adaptations"): a 3x3 stem
+(conv-BN-ReLU, no max-pool), then J stages of reversible blocks whose width
+doubles from stage to stage; between stages a non-reversible downsampling
+(conv1x1 stride 2 + BN) opens the next stage; the last stage ends with global
+average pooling, a linear layer with bias and softmax cross-entropy averaged
+over the micro-batch.  Readings: stage 0 = stem + blocks, stage j > 0 =
+downsampling + blocks, the last stage also owns the head; the stem has a ReLU
+after its BN, the downsampling has none; the downsampling convolves the two
+streams as one tensor (x1 first) and its output is split into halves again.
+
+Schedule (0-based stage index j, J stages, one hop per tick): at tick t stage j
+runs the forward of micro-batch t - j and the backward of micro-batch
+t - (2J - 2 - j), so the delay between a stage's forward and backward of the
+same micro-batch is 2(J - 1 - j), i.e. 2(J - j) with the paper's 1-based j.
+Every forward and backward of a tick reads the stage's current parameters and
+the update follows both (Eq. 5).  The last stage computes the loss and its own
+backward in the same tick.  Non-reversible front layers keep their input in a
+buffer and recompute it on the backward, discarding the reconstructed input
+that arrives from above; stage 0 re-reads its images from the dataset
+(Alg. 1; Sec. 4.2).  A reversible stage sends back its reconstructed input; a
+stage with a buffer sends back the buffered input (Alg. 1, reading of the
+backward send).
+"""
+from __future__ import annotations
+
+from typing import Callable, Dict, List, Optional, Sequence
+
+import numpy as np
+
+from . import bn, conv, revblock, sgd
+
+
+def nonrev_forward(x, w, g, b, eps, stride, relu):
+    h = conv.forward(x, w, stride=stride, pad=(w.shape[1] - 1) // 2)
+    o, cache = bn.forward(h, g, b, eps)
+    a = np.maximum(o, 0.0) if relu else o
+    return a, (x, h, o, cache)
+
+
+def nonrev_vjp(d, w, g, graph, stride, relu):
+    x, _, o, cache = graph
+    if relu:
+        d = d * (o > 0.0)
+    dh, dg, db = bn.backward(d, cache, g)
+    pad = (w.shape[1] - 1) // 2
+    return conv.dgrad(dh, w, x.shape, stride=stride, pad=pad), (
+        conv.wgrad(x, dh, w.shape, stride=stride, pad=pad), dg, db)
+
+
+def head_loss(x, wfc, bfc, labels):
+    """Global average pool -> linear -> softmax cross-entropy (batch mean)."""
+    pooled = x.mean(axis=(1, 2))                      # [N, C]
+    logits = pooled @ wfc.T + bfc                     # [N, K]
+    z = logits - logits.max(axis=1, keepdims=True)
+    lse = np.log(np.exp(z).sum(axis=1))
+    n = x.shape[0]
+    loss = float(np.mean(lse - z[np.arange(n), labels]))
+    return loss, (x.shape, pooled, z, lse)
+
+
+def head_vjp(wfc, labels, cache):
+    shape, pooled, z, lse = cache
+    n = shape[0]
+    p = np.exp(z - lse[:, None])
+    p[np.arange(n), labels] -= 1.0
+    dlogits = p / n
+    dw = dlogits.T @ pooled
+    db = dlogits.sum(axis=0)
+    dpooled = dlogits @ wfc
+    dx = np.broadcast_to(dpooled[:, None, None, :] / (shape[1] * shape[2]), shape).copy()
+    return dx, dw, db
+
+
+class NetStage:
+    """One stage: a non-reversible front layer, reversible blocks, optional head."""
+
+    def __init__(self, params, names, first: bool, last: bool, blocks: int, eps: float,
+                 bn_momentum: float, dtype, weight_view):
+        self.params = [np.array(p, dtype=dtype) for p in params]
+        self.names = list(names)
+        self.first, self.last, self.blocks = first, last, blocks
+        self.eps, self.bn_momentum, self.dtype = eps, bn_momentum, dtype
+        self.weight_view = weight_view
+        self.accum = [np.zeros_like(p) for p in self.params]
+        self.buf = [np.zeros_like(p) for p in self.params]
+        nbn = 1 + blocks * 4
+        self.run_mean = [np.zeros(self.params[3 * i + 1].shape, dtype) for i in range(nbn)]
+        self.run_var = [np.ones(self.params[3 * i + 1].shape, dtype) for i in range(nbn)]
+        self.t = 0
+        self.buffer: Dict[int, tuple] = {}
+
+    def _w(self, i):
+        w = self.params[i]
+        if self.weight_view is not None:
+            w = np.asarray(self.weight_view(w.astype(np.float32)), dtype=self.dtype)
+        return w
+
+    def _layers(self, b, f):
+        base = 3 + (2 * b + f) * 6
+        return [(self._w(base + 3 * l), self.params[base + 3 * l + 1], self.params[base + 3 * l + 2])
+                for l in range(2)]
+
+    def _front(self, x1, x2):
+        x = x1 if self.first else np.concatenate([x1, x2], axis=-1)
+        stride = 1 if self.first else 2
+        a, graph = nonrev_forward(x, self._w(0), self.params[1], self.params[2], self.eps,
+                                  stride, relu=self.first)
+        c = a.shape[-1] // 2
+        return a[..., :c], a[..., c:], graph
+
+    def forward(self, x1, x2):
+        y1, y2, _ = self._front(x1, x2)
+        for b in range(self.blocks):
+            y1, y2 = revblock.block_forward(y1, y2, self._layers(b, 0), self._layers(b, 1), self.eps)
+        return y1, y2
+
+    def backward(self, y1, y2, g1, g2, x1, x2, k):
+        """Blocks: reconstruct + VJP from (y, g).  Front: recompute from the
+        buffered input (x1, x2) and VJP.  Returns the input gradient halves."""
+        grads: List[Optional[np.ndarray]] = [None] * len(self.params)
+        for b in reversed(range(self.blocks)):
+            r = revblock.block_reconstruct_vjp(y1, y2, g1, g2, self._layers(b, 0),
+                                               self._layers(b, 1), self.eps)
+            for f, key in ((0, "dF"), (1, "dG")):
+                base = 3 + (2 * b + f) * 6
+                stats = r["stats_F" if f == 0 else "stats_G"]
+                for l, (dw, dg, db) in enumerate(r[key]):
+                    grads[base + 3 * l: base + 3 * l + 3] = [dw, dg, db]
+                    slot = (base + 3 * l) // 3
+                    cache, m = stats[l]
+                    self.run_mean[slot], self.run_var[slot] = bn.running_update(
+                        self.run_mean[slot], self.run_var[slot], cache, m, self.bn_momentum)
+            y1, y2, g1, g2 = r["x1"], r["x2"], r["dx1"], r["dx2"]
+        # non-reversible front: recompute from the buffered input
+        _, _, graph = self._front(x1, x2)
+        stride = 1 if self.first else 2
+        dx, (dw, dg, db) = nonrev_vjp(np.concatenate([g1, g2], axis=-1), self._w(0),
+                                      self.params[1], graph, stride, relu=self.first)
+        grads[0:3] = [dw, dg, db]
+        h = graph[1]
+        self.run_mean[0], self.run_var[0] = bn.running_update(
+            self.run_mean[0], self.run_var[0], graph[3], h.shape[0] * h.shape[1] * h.shape[2],
+            self.bn_momentum)
+        return dx, grads
+
+    def accumulate(self, grads, k):
+        for a, g in zip(self.accum, grads):
+            a += g / k
+        self.t += 1
+
+    def update(self, lr, mu, wd, nesterov, k):
+        if self.t == 0 or self.t % k != 0:
+            return False
+        for i, name in enumerate(self.names):
+            wdp = wd if name.endswith("weight") else 0.0
+            self.params[i], self.buf[i] = sgd.step(self.params[i], self.accum[i], self.buf[i],
+                                                   lr, mu, wdp, nesterov)
+            self.accum[i] = np.zeros_like(self.accum[i])
+        return True
+
+
+def split_params(names: Sequence[str], params: Sequence[np.ndarray], stages: int):
+    out = [([], []) for _ in range(stages)]
+    for nm, p in zip(names, params):
+        j = int(nm.split(".")[0][1:])
+        out[j][0].append(p)
+        out[j][1].append(nm)
+    return out
+
+
+class PetraNet:
+    """Tick-level simulation of the PETRA schedule over J stages."""
+
+    def __init__(self, params, names, stages: int, blocks_per_stage: int, eps=1e-5,
+                 bn_momentum=0.1, dtype=np.float64, weight_view=None):
+        self.J = stages
+        self.stages = []
+        for j, (ps, ns) in enumerate(split_params(names, params, stages)):
+            self.stages.append(NetStage(ps, ns, j == 0, j == stages - 1, blocks_per_stage,
+                                        eps, bn_momentum, dtype, weight_view))
+        self.dtype = dtype
+        self.fwd_msg: List[Optional[tuple]] = [None] * stages
+        self.bwd_msg: List[Optional[tuple]] = [None] * stages
+        self.trace: List[tuple] = []
+
+    def fwd_batch(self, t: int, j: int) -> int:
+        return t - j
+
+    def bwd_batch(self, t: int, j: int) -> int:
+        return t - (2 * self.J - 2 - j)
+
+    def tick(self, t: int, images: Callable[[int], np.ndarray], labels: Callable[[int], np.ndarray],
+             n_micro: int, lr: float, mu: float, wd: float, nesterov=True, k=1):
+        """One tick of every stage; returns the loss computed this tick (or None)."""
+        J = self.J
+        new_fwd: List[Optional[tuple]] = [None] * J
+        new_bwd: List[Optional[tuple]] = [None] * J
+        loss = None
+        did_bwd = [False] * J
+        for j, st in enumerate(self.stages):
+            m = self.fwd_batch(t, j)
+            last_out = None
+            if 0 <= m < n_micro:
+                if j == 0:
+                    x1, x2 = np.asarray(images(m), self.dtype), None
+                else:
+                    x1, x2 = self.fwd_msg[j - 1]
+                    st.buffer[m] = (x1, x2)
+                y1, y2 = st.forward(x1, x2)
+                if st.last:
+                    last_out = (y1, y2)
+                else:
+                    new_fwd[j] = (y1, y2)
+            mb = self.bwd_batch(t, j)
+            if 0 <= mb < n_micro:
+                if st.last:
+                    y1, y2 = last_out
+                    lab = labels(mb)
+                    loss, hc = head_loss(np.concatenate([y1, y2], -1), st.params[-2], st.params[-1], lab)
+                    dx, dwfc, dbfc = head_vjp(st._w(len(st.params) - 2), lab, hc)
+                    c = y1.shape[-1]
+                    g1, g2 = dx[..., :c], dx[..., c:]
+                else:
+                    y1, y2, g1, g2 = self.bwd_msg[j + 1]
+                if j == 0:
+                    bx1, bx2 = np.asarray(images(mb), self.dtype), None
+                else:
+                    bx1, bx2 = st.buffer.pop(mb)
+                dx, grads = st.backward(y1, y2, g1, g2, bx1, bx2, k)
+                if st.last:
+                    grads[-2], grads[-1] = dwfc, dbfc
+                st.accumulate(grads, k)
+                did_bwd[j] = True
+                if j > 0:
+                    c = bx1.shape[-1]
+                    new_bwd[j] = (bx1, bx2, dx[..., :c], dx[..., c:])
+            self.trace.append((t, j, m if 0 <= m < n_micro else None,
+                               mb if 0 <= mb < n_micro else None))
+        for j, st in enumerate(self.stages):
+            if did_bwd[j]:
+                st.update(lr, mu, wd, nesterov, k)
+        self.fwd_msg, self.bwd_msg = new_fwd, new_bwd
+        return loss
