@@ -1,0 +1,194 @@
+/*
+ * petra.h -- C ABI of the MI355X (gfx950) PETRA reversible-stage library.
+ *
+ * PETRA trains a network split into stages; each stage keeps one copy of its
+ * parameters and, per time step, runs the forward of one micro-batch and the
+ * backward of another with the same current parameters, then updates them in
+ * place (paper: Sec. 3.3, Eq. 5 and Alg. 1).  For a reversible stage the
+ * backward first rebuilds the stage input from its output (Sec. 3.2, Eq. 4),
+ * so no activation is kept between the two passes.
+ *
+ * Conventions shared by every call below
+ *  - All tensors are device pointers into memory the caller owns.  The library
+ *    owns only the host-side handle and the HIP streams/events it creates for
+ *    itself; no call allocates or frees device memory.
+ *  - Activations are NHWC.  A stage activation with C channels is passed as two
+ *    contiguous half-tensors x1 (channels [0, C/2)) and x2 (channels [C/2, C)),
+ *    each [N][H][W][C/2], of the stage's storage type (fp32 or bf16).
+ *  - Parameters live in flat fp32 buffers whose layout the library defines and
+ *    reports through petra_stage_param_info(): conv weights are KRSC
+ *    ([C_out][R][S][C_in]).  Gradient accumulator and momentum buffers use the
+ *    same layout.  BN running statistics are two fp32 arrays (mean, variance)
+ *    of petra_stage_query()'s n_bn_channels entries.
+ *  - `stream` is a hipStream_t (NULL = the null stream).  Compute calls only
+ *    enqueue work and return; buffers must stay alive until the stream has
+ *    drained them.
+ *  - Argument, shape, alignment and state errors are detected on the host
+ *    before anything is enqueued and return a non-zero status; nothing is
+ *    launched in that case.  An asynchronous HIP error is reported as
+ *    PETRA_ERR_HIP by the call that observes it.  petra_last_error() gives
+ *    a readable message for the calling thread.  The library never aborts.
+ *  - Device pointers must be 16-byte aligned.  A handle must not be used by
+ *    two host threads at once.
+ */
+#ifndef PETRA_H
+#define PETRA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  PETRA_OK = 0,
+  PETRA_ERR_INVALID_ARG = 1, /* null pointer, bad enum, bad hyper-parameter   */
+  PETRA_ERR_SHAPE = 2,       /* unsupported or inconsistent sizes             */
+  PETRA_ERR_DTYPE = 3,       /* unsupported storage type                      */
+  PETRA_ERR_ALIGN = 4,       /* a device pointer is not 16-byte aligned       */
+  PETRA_ERR_WORKSPACE = 5,   /* workspace missing or too small                */
+  PETRA_ERR_STATE = 6,       /* call out of order (e.g. compute before bind)  */
+  PETRA_ERR_HIP = 7,         /* a HIP runtime call failed                     */
+  PETRA_ERR_ALIAS = 8        /* two buffers overlap where that is not allowed */
+} petra_status;
+
+typedef enum { PETRA_FP32 = 0, PETRA_BF16 = 1 } petra_dtype; /* storage; accumulation is fp32 */
+
+typedef enum {
+  PETRA_BLOCK_BASIC = 0,      /* conv3x3-BN-ReLU-conv3x3-BN                        */
+  PETRA_BLOCK_BOTTLENECK = 1  /* conv1x1-BN-ReLU-conv3x3-BN-ReLU-conv1x1-BN         */
+} petra_block_kind;
+
+typedef enum {
+  PETRA_ROLE_CONV_WEIGHT = 0,
+  PETRA_ROLE_BN_GAMMA = 1,
+  PETRA_ROLE_BN_BETA = 2,
+  PETRA_ROLE_FC_WEIGHT = 3,
+  PETRA_ROLE_FC_BIAS = 4
+} petra_param_role;
+
+/* One reversible stage: num_blocks reversible blocks y1 = x1 + F(x2),
+ * y2 = x2 + G(y1) (Sec. 3.2, Fig. 2) at a fixed activation shape.
+ * Each block has two residual functions F and G of the given kind, acting on
+ * one stream of c_half channels (c_mid = inner width of a bottleneck).
+ * BN runs in training mode with batch statistics over N*H*W (eps bn_eps);
+ * running statistics use momentum bn_momentum and move only during the
+ * backward recompute (Sec. 4.1, "Model adaptations").
+ * Limits: c_half and c_mid multiples of 16 (bf16) or 8 (fp32), at most 512;
+ * N*H*W < 2^31 / c_half. */
+typedef struct {
+  int32_t n, h, w;
+  int32_t c_half;
+  int32_t c_mid;
+  int32_t num_blocks;
+  int32_t kind;   /* petra_block_kind */
+  int32_t dtype;  /* petra_dtype      */
+  float bn_eps;
+  float bn_momentum;
+} petra_stage_desc;
+
+/* SGD with momentum (Nesterov when nesterov != 0) and gradient accumulation
+ * over accum_k backward steps with averaging (Sec. 4.1; Alg. 1).  Weight decay
+ * applies to conv/FC weights only, never to BN parameters or biases. */
+typedef struct {
+  float lr;
+  float momentum;
+  float weight_decay;
+  int32_t nesterov;
+  int32_t accum_k;
+} petra_sgd;
+
+/* Placement of one parameter tensor in the flat fp32 buffers.  Tensors are
+ * indexed in canonical order: block b, function F then G, conv l, and for
+ * each conv its weight, BN gamma, BN beta. */
+typedef struct {
+  int64_t offset;        /* element offset into the flat buffers           */
+  int64_t numel;
+  int32_t role;          /* petra_param_role                                */
+  int32_t ndim;
+  int32_t shape[4];      /* KRSC for conv weights, [C] for BN parameters    */
+  int32_t weight_decay;  /* 1 if weight decay applies                       */
+  int32_t bn_index;      /* BN layer index for gamma/beta (and the conv it follows), else -1 */
+} petra_param_info;
+
+typedef struct petra_stage petra_stage;
+
+/* Status name, e.g. "PETRA_ERR_SHAPE". */
+const char* petra_status_str(petra_status s);
+/* Message of the calling thread's last failed call ("" if none). */
+const char* petra_last_error(void);
+
+/* Build a handle from a description (host only, no device work). */
+petra_status petra_stage_create(const petra_stage_desc* desc, petra_stage** out);
+petra_status petra_stage_destroy(petra_stage* st);
+
+/* Sizes the caller must allocate: n_params fp32 elements for each of the
+ * parameter, gradient-accumulator and momentum buffers; n_tensors parameter
+ * tensors; n_bn_channels fp32 elements for each running-statistics array;
+ * workspace_bytes of device scratch (compute copies of the weights, one
+ * block's intermediates for the forward and for the backward, partial sums). */
+petra_status petra_stage_query(const petra_stage* st, int64_t* n_params, int32_t* n_tensors,
+                               int64_t* n_bn_channels, size_t* workspace_bytes);
+petra_status petra_stage_param_info(const petra_stage* st, int32_t index, petra_param_info* out);
+
+/* Attach caller-owned device buffers.  params: fp32 master weights theta;
+ * grad_accum: the accumulator Delta; momentum: optimizer state; run_mean /
+ * run_var: BN running statistics; workspace: scratch of at least
+ * workspace_bytes.  The caller initialises params, zeroes grad_accum and
+ * momentum, and sets run_mean = 0, run_var = 1; then calls
+ * petra_stage_sync_weights(). */
+petra_status petra_stage_bind(petra_stage* st, float* params, float* grad_accum, float* momentum,
+                              float* run_mean, float* run_var, void* workspace,
+                              size_t workspace_bytes);
+
+/* Optimizer settings used by petra_stage_update() and the (1/k) gradient
+ * scale of petra_stage_reconstruct_backward(). */
+petra_status petra_stage_set_optimizer(petra_stage* st, const petra_sgd* opt);
+
+/* Refresh the storage-type compute copies of the conv weights from the fp32
+ * master (needed once after the caller writes params directly). */
+petra_status petra_stage_sync_weights(petra_stage* st, void* stream);
+
+/* Forward of the stage with the current parameters (Eq. 5, first line):
+ * blocks 1..B in order.  Reads x1, x2; writes y1, y2.  In place is allowed
+ * (x1 == y1 and/or x2 == y2); no other overlap.  BN uses batch statistics and
+ * leaves the running statistics untouched. */
+petra_status petra_stage_forward(petra_stage* st, const void* x1, const void* x2, void* y1,
+                                 void* y2, void* stream);
+
+/* Backward of the stage with the current parameters (Eq. 5, lines 2-4;
+ * Alg. 1): blocks B..1, each rebuilding its input from its output
+ * (x2 = y2 - G(y1), x1 = y1 - F(x2), Eq. 4) while recomputing the graph of G
+ * and F, then taking the vector-Jacobian products through them.
+ * Inputs: the stage output y1, y2 and its gradient dy1, dy2.
+ * Outputs: the reconstructed input x1, x2 and the input gradient dx1, dx2.
+ * Adds (1/accum_k) of the parameter gradient to grad_accum and updates the BN
+ * running statistics.  In place is allowed for x1 == y1, x2 == y2,
+ * dx1 == dy1, dx2 == dy2; no other overlap. */
+petra_status petra_stage_reconstruct_backward(petra_stage* st, const void* y1, const void* y2,
+                                              const void* dy1, const void* dy2, void* x1,
+                                              void* x2, void* dx1, void* dx2, void* stream);
+
+/* Parameter update (Eq. 5, last line; Alg. 1): counts one backward step and,
+ * when the count is a multiple of accum_k, applies the optimizer to params
+ * from grad_accum, zeroes grad_accum and refreshes the compute copies.
+ * *updated (nullable) receives 1 if the update ran. */
+petra_status petra_stage_update(petra_stage* st, void* stream, int32_t* updated);
+
+/* One PETRA stage step (Eq. 5): the forward of one micro-batch (x -> y) and
+ * the backward of another (yb, dyb -> xb, dxb) run concurrently on two
+ * library-owned streams, both reading the current parameters; the update
+ * follows both.  All work is ordered after prior work on `stream`, and later
+ * work on `stream` is ordered after it.  Aliasing rules of the two calls
+ * apply; the forward and backward buffers must not overlap each other. */
+petra_status petra_stage_step(petra_stage* st, const void* x1, const void* x2, void* y1, void* y2,
+                              const void* yb1, const void* yb2, const void* dyb1,
+                              const void* dyb2, void* xb1, void* xb2, void* dxb1, void* dxb2,
+                              void* stream, int32_t* updated);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PETRA_H */

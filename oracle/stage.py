@@ -33,11 +33,15 @@ class StageState:
     n_convs: convs per residual function (2 basic, 3 bottleneck).
     weight_view: optional map applied to conv weights before use (e.g. the
     rounding of a lower-precision compute copy); defaults to identity.
+    store: optional map giving the values a lower-precision storage format
+    holds, applied where the method materialises activations and activation
+    gradients (see revblock); defaults to identity (plain fp64).
     """
 
     def __init__(self, params: Sequence[np.ndarray], names: Sequence[str], n_convs: int,
                  eps: float = 1e-5, bn_momentum: float = 0.1, dtype=np.float64,
-                 weight_view: Optional[Callable[[np.ndarray], np.ndarray]] = None):
+                 weight_view: Optional[Callable[[np.ndarray], np.ndarray]] = None,
+                 store: Optional[Callable[[np.ndarray], np.ndarray]] = None):
         self.dtype = dtype
         self.params = [np.array(p, dtype=dtype) for p in params]
         self.names = list(names)
@@ -45,6 +49,10 @@ class StageState:
         self.eps = eps
         self.bn_momentum = bn_momentum
         self.weight_view = weight_view
+        if store is None:
+            self.store = lambda a: a
+        else:
+            self.store = lambda a: np.asarray(store(np.asarray(a, np.float32)), dtype=dtype)
         self.accum = [np.zeros_like(p) for p in self.params]
         self.buf = [np.zeros_like(p) for p in self.params]
         per_fn = 3 * n_convs
@@ -76,14 +84,16 @@ class StageState:
         x1 = np.asarray(x1, self.dtype)
         x2 = np.asarray(x2, self.dtype)
         for b in range(self.blocks):
-            x1, x2 = revblock.block_forward(x1, x2, self._layers(b, 0), self._layers(b, 1), self.eps)
+            x1, x2 = revblock.block_forward(x1, x2, self._layers(b, 0), self._layers(b, 1), self.eps,
+                                            self.store)
         return x1, x2
 
     def inverse(self, y1: np.ndarray, y2: np.ndarray):
         y1 = np.asarray(y1, self.dtype)
         y2 = np.asarray(y2, self.dtype)
         for b in reversed(range(self.blocks)):
-            y1, y2 = revblock.block_inverse(y1, y2, self._layers(b, 0), self._layers(b, 1), self.eps)
+            y1, y2 = revblock.block_inverse(y1, y2, self._layers(b, 0), self._layers(b, 1), self.eps,
+                                            self.store)
         return y1, y2
 
     # -- Eq. (5), lines two to four; Alg. 1 accumulation -----------------------
@@ -102,7 +112,7 @@ class StageState:
         per_fn = 3 * self.n_convs
         for b in reversed(range(self.blocks)):
             r = revblock.block_reconstruct_vjp(y1, y2, g1, g2, self._layers(b, 0),
-                                               self._layers(b, 1), self.eps)
+                                               self._layers(b, 1), self.eps, self.store)
             for f, key in ((0, "dF"), (1, "dG")):
                 base = (2 * b + f) * per_fn
                 stats = r["stats_F" if f == 0 else "stats_G"]

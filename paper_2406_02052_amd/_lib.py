@@ -1,0 +1,194 @@
+"""ctypes binding of libpetra.so (argument marshalling only).
+
+Every function named petra_* here calls the C entry point of the same name
+declared in include/petra.h; all arithmetic runs in the library's HIP kernels.
+PyTorch is used only to own device memory and to supply the current stream.
+If the library is missing the import fails loudly: there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libpetra.so")
+
+PETRA_FP32, PETRA_BF16 = 0, 1
+PETRA_BLOCK_BASIC, PETRA_BLOCK_BOTTLENECK = 0, 1
+ROLE_CONV_WEIGHT, ROLE_BN_GAMMA, ROLE_BN_BETA, ROLE_FC_WEIGHT, ROLE_FC_BIAS = range(5)
+STATUS = ["PETRA_OK", "PETRA_ERR_INVALID_ARG", "PETRA_ERR_SHAPE", "PETRA_ERR_DTYPE",
+          "PETRA_ERR_ALIGN", "PETRA_ERR_WORKSPACE", "PETRA_ERR_STATE", "PETRA_ERR_HIP",
+          "PETRA_ERR_ALIAS"]
+
+
+class PetraError(RuntimeError):
+    def __init__(self, status: int, func: str, msg: str):
+        name = STATUS[status] if 0 <= status < len(STATUS) else str(status)
+        super().__init__(f"{func} -> {name}: {msg}")
+        self.status = status
+        self.name = name
+
+
+class StageDesc(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int32), ("h", ctypes.c_int32), ("w", ctypes.c_int32),
+                ("c_half", ctypes.c_int32), ("c_mid", ctypes.c_int32),
+                ("num_blocks", ctypes.c_int32), ("kind", ctypes.c_int32),
+                ("dtype", ctypes.c_int32), ("bn_eps", ctypes.c_float),
+                ("bn_momentum", ctypes.c_float)]
+
+
+class Sgd(ctypes.Structure):
+    _fields_ = [("lr", ctypes.c_float), ("momentum", ctypes.c_float),
+                ("weight_decay", ctypes.c_float), ("nesterov", ctypes.c_int32),
+                ("accum_k", ctypes.c_int32)]
+
+
+class ParamInfo(ctypes.Structure):
+    _fields_ = [("offset", ctypes.c_int64), ("numel", ctypes.c_int64), ("role", ctypes.c_int32),
+                ("ndim", ctypes.c_int32), ("shape", ctypes.c_int32 * 4),
+                ("weight_decay", ctypes.c_int32), ("bn_index", ctypes.c_int32)]
+
+
+_VP = ctypes.c_void_p
+_SIGS = {
+    "petra_status_str": (ctypes.c_char_p, [ctypes.c_int]),
+    "petra_last_error": (ctypes.c_char_p, []),
+    "petra_stage_create": (ctypes.c_int, [ctypes.POINTER(StageDesc), ctypes.POINTER(_VP)]),
+    "petra_stage_destroy": (ctypes.c_int, [_VP]),
+    "petra_stage_query": (ctypes.c_int, [_VP, ctypes.POINTER(ctypes.c_int64),
+                                          ctypes.POINTER(ctypes.c_int32),
+                                          ctypes.POINTER(ctypes.c_int64),
+                                          ctypes.POINTER(ctypes.c_size_t)]),
+    "petra_stage_param_info": (ctypes.c_int, [_VP, ctypes.c_int32, ctypes.POINTER(ParamInfo)]),
+    "petra_stage_bind": (ctypes.c_int, [_VP, _VP, _VP, _VP, _VP, _VP, _VP, ctypes.c_size_t]),
+    "petra_stage_set_optimizer": (ctypes.c_int, [_VP, ctypes.POINTER(Sgd)]),
+    "petra_stage_sync_weights": (ctypes.c_int, [_VP, _VP]),
+    "petra_stage_forward": (ctypes.c_int, [_VP, _VP, _VP, _VP, _VP, _VP]),
+    "petra_stage_reconstruct_backward": (ctypes.c_int, [_VP] * 10),
+    "petra_stage_update": (ctypes.c_int, [_VP, _VP, ctypes.POINTER(ctypes.c_int32)]),
+    "petra_stage_step": (ctypes.c_int, [_VP] * 14 + [ctypes.POINTER(ctypes.c_int32)]),
+}
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+def load() -> ctypes.CDLL:
+    """Load libpetra.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it first "
+                          "(python -c 'import __graft_entry__; __graft_entry__.build()')")
+    lib = ctypes.CDLL(LIB_PATH)
+    for name, (res, args) in _SIGS.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _check(status: int, func: str) -> None:
+    if status != 0:
+        raise PetraError(status, func, load().petra_last_error().decode())
+
+
+def _ptr(t) -> int:
+    """Device address of a tensor (or an int address, or None)."""
+    if t is None:
+        return 0
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+# ---------------------------------------------------------------------------
+# One wrapper per C entry point, same names and argument order.
+# ---------------------------------------------------------------------------
+
+def petra_status_str(status: int) -> str:
+    return load().petra_status_str(status).decode()
+
+
+def petra_last_error() -> str:
+    return load().petra_last_error().decode()
+
+
+def petra_stage_create(desc: StageDesc) -> int:
+    h = _VP()
+    _check(load().petra_stage_create(ctypes.byref(desc), ctypes.byref(h)), "petra_stage_create")
+    return h.value
+
+
+def petra_stage_destroy(handle: int) -> None:
+    _check(load().petra_stage_destroy(handle), "petra_stage_destroy")
+
+
+def petra_stage_query(handle: int):
+    n_params, n_tensors = ctypes.c_int64(), ctypes.c_int32()
+    n_bn, ws = ctypes.c_int64(), ctypes.c_size_t()
+    _check(load().petra_stage_query(handle, ctypes.byref(n_params), ctypes.byref(n_tensors),
+                                    ctypes.byref(n_bn), ctypes.byref(ws)), "petra_stage_query")
+    return n_params.value, n_tensors.value, n_bn.value, ws.value
+
+
+def petra_stage_param_info(handle: int, index: int) -> ParamInfo:
+    info = ParamInfo()
+    _check(load().petra_stage_param_info(handle, index, ctypes.byref(info)),
+           "petra_stage_param_info")
+    return info
+
+
+def petra_stage_bind(handle, params, grad_accum, momentum, run_mean, run_var, workspace,
+                     workspace_bytes: int) -> None:
+    _check(load().petra_stage_bind(handle, _ptr(params), _ptr(grad_accum), _ptr(momentum),
+                                   _ptr(run_mean), _ptr(run_var), _ptr(workspace),
+                                   workspace_bytes), "petra_stage_bind")
+
+
+def petra_stage_set_optimizer(handle: int, opt: Sgd) -> None:
+    _check(load().petra_stage_set_optimizer(handle, ctypes.byref(opt)), "petra_stage_set_optimizer")
+
+
+def petra_stage_sync_weights(handle: int, stream=None) -> None:
+    _check(load().petra_stage_sync_weights(handle, _stream(stream)), "petra_stage_sync_weights")
+
+
+def petra_stage_forward(handle, x1, x2, y1, y2, stream=None) -> None:
+    _check(load().petra_stage_forward(handle, _ptr(x1), _ptr(x2), _ptr(y1), _ptr(y2),
+                                      _stream(stream)), "petra_stage_forward")
+
+
+def petra_stage_reconstruct_backward(handle, y1, y2, dy1, dy2, x1, x2, dx1, dx2,
+                                     stream=None) -> None:
+    _check(load().petra_stage_reconstruct_backward(
+        handle, _ptr(y1), _ptr(y2), _ptr(dy1), _ptr(dy2), _ptr(x1), _ptr(x2), _ptr(dx1),
+        _ptr(dx2), _stream(stream)), "petra_stage_reconstruct_backward")
+
+
+def petra_stage_update(handle, stream=None) -> bool:
+    upd = ctypes.c_int32()
+    _check(load().petra_stage_update(handle, _stream(stream), ctypes.byref(upd)),
+           "petra_stage_update")
+    return bool(upd.value)
+
+
+def petra_stage_step(handle, x1, x2, y1, y2, yb1, yb2, dyb1, dyb2, xb1, xb2, dxb1, dxb2,
+                     stream=None) -> bool:
+    upd = ctypes.c_int32()
+    _check(load().petra_stage_step(handle, _ptr(x1), _ptr(x2), _ptr(y1), _ptr(y2), _ptr(yb1),
+                                   _ptr(yb2), _ptr(dyb1), _ptr(dyb2), _ptr(xb1), _ptr(xb2),
+                                   _ptr(dxb1), _ptr(dxb2), _stream(stream), ctypes.byref(upd)),
+           "petra_stage_step")
+    return bool(upd.value)

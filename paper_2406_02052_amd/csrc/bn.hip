@@ -1,0 +1,258 @@
+// Batch-normalisation statistics, BN backward coefficients and the fused
+// elementwise passes of the reversible coupling (gfx950).
+//
+// Statistics arrive as per-tile partial sums written by the producing kernel
+// (the conv epilogue or combine_bwd); the finalize kernels combine them in a
+// fixed order in fp64, so results are run-to-run deterministic.
+#include "common.h"
+#include "kernels.h"
+
+namespace petra {
+
+namespace {
+
+constexpr int FIN_TX = 32, FIN_TY = 16;
+
+// Fixed-order reduction of partials[tile][which][c] over tiles, in fp64.
+__device__ void reduce_partials(const float* partials, int tiles, int c, int ch, double& s1,
+                                double& s2) {
+  __shared__ double red[2][FIN_TY][FIN_TX];
+  const int tx = threadIdx.x, ty = threadIdx.y;
+  double a = 0.0, b = 0.0;
+  if (ch < c) {
+    for (int t = ty; t < tiles; t += FIN_TY) {
+      a += partials[(static_cast<long>(t) * 2 + 0) * c + ch];
+      b += partials[(static_cast<long>(t) * 2 + 1) * c + ch];
+    }
+  }
+  red[0][ty][tx] = a;
+  red[1][ty][tx] = b;
+  __syncthreads();
+  s1 = s2 = 0.0;
+  if (ty == 0) {
+    for (int i = 0; i < FIN_TY; ++i) {
+      s1 += red[0][i][tx];
+      s2 += red[1][i][tx];
+    }
+  }
+}
+
+__global__ void bn_stats_finalize_kernel(const float* partials, int tiles, int c, long m,
+                                         const float* gamma, const float* beta, float eps,
+                                         float* scale, float* shift, float* mean_out,
+                                         float* rstd_out, float* run_mean, float* run_var,
+                                         float momentum) {
+  const int ch = blockIdx.x * FIN_TX + threadIdx.x;
+  double s1, s2;
+  reduce_partials(partials, tiles, c, ch, s1, s2);
+  if (threadIdx.y != 0 || ch >= c) return;
+  const double mean = s1 / static_cast<double>(m);
+  double var = s2 / static_cast<double>(m) - mean * mean;
+  if (var < 0.0) var = 0.0;
+  const double rstd = 1.0 / sqrt(var + static_cast<double>(eps));
+  const double sc = static_cast<double>(gamma[ch]) * rstd;
+  scale[ch] = static_cast<float>(sc);
+  shift[ch] = static_cast<float>(static_cast<double>(beta[ch]) - mean * sc);
+  mean_out[ch] = static_cast<float>(mean);
+  rstd_out[ch] = static_cast<float>(rstd);
+  if (run_mean != nullptr) {
+    const double mom = momentum;
+    const double unbiased = m > 1 ? var * static_cast<double>(m) / static_cast<double>(m - 1) : var;
+    run_mean[ch] = static_cast<float>((1.0 - mom) * run_mean[ch] + mom * mean);
+    run_var[ch] = static_cast<float>((1.0 - mom) * run_var[ch] + mom * unbiased);
+  }
+}
+
+__global__ void bn_bwd_finalize_kernel(const float* partials, int tiles, int c, long m,
+                                       const float* gamma, const float* mean, const float* rstd,
+                                       float inv_k, float* dgamma, float* dbeta, float* ca,
+                                       float* cb, float* cc) {
+  const int ch = blockIdx.x * FIN_TX + threadIdx.x;
+  double sd, sdx;
+  reduce_partials(partials, tiles, c, ch, sd, sdx);
+  if (threadIdx.y != 0 || ch >= c) return;
+  (void)mean;
+  dbeta[ch] += inv_k * static_cast<float>(sd);
+  dgamma[ch] += inv_k * static_cast<float>(sdx);
+  const double g = gamma[ch], r = rstd[ch], md = static_cast<double>(m);
+  // dh = g*r*(d - sd/m - xhat*sdx/m), xhat = (h - mean)*r
+  ca[ch] = static_cast<float>(g * r);
+  cb[ch] = static_cast<float>(-g * r * r * sdx / md);
+  cc[ch] = static_cast<float>(-g * r * sd / md);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void combine_fwd_kernel(const T* r, const T* h,
+                                                          const float* scale, const float* shift,
+                                                          T* y, long total8, int c8) {
+  for (long i = static_cast<long>(blockIdx.x) * 256 + threadIdx.x; i < total8;
+       i += static_cast<long>(gridDim.x) * 256) {
+    const int ch = static_cast<int>(i % c8) * 8;
+    float rv[8], hv[8], o[8];
+    Vec8<T>::load(r + i * 8, rv);
+    Vec8<T>::load(h + i * 8, hv);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) o[j] = rv[j] + fmaf(scale[ch + j], hv[j], shift[ch + j]);
+    Vec8<T>::store(y + i * 8, o);
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void bn_bwd_apply_kernel(const T* d, const T* h,
+                                                           const float* ca, const float* cb,
+                                                           const float* cc, const float* mean,
+                                                           T* out, long total8, int c8) {
+  for (long i = static_cast<long>(blockIdx.x) * 256 + threadIdx.x; i < total8;
+       i += static_cast<long>(gridDim.x) * 256) {
+    const int ch = static_cast<int>(i % c8) * 8;
+    float dv[8], hv[8], o[8];
+    Vec8<T>::load(d + i * 8, dv);
+    Vec8<T>::load(h + i * 8, hv);
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      o[j] = fmaf(ca[ch + j], dv[j], fmaf(cb[ch + j], hv[j] - mean[ch + j], cc[ch + j]));
+    Vec8<T>::store(out + i * 8, o);
+  }
+}
+
+// Each block owns rows [tile*rows_per_tile, ...) and writes one partial row.
+template <typename T>
+__global__ __launch_bounds__(256) void combine_bwd_kernel(const T* v, const T* h, const T* d,
+                                                          const float* scale, const float* shift,
+                                                          const float* mean, const float* rstd,
+                                                          T* x, float* partials, long m, int c,
+                                                          int rows_per_tile) {
+  const int c8 = c / 8;
+  const int rows_per_pass = 256 / c8;
+  const int tid = threadIdx.x;
+  const int cg = tid % c8, rr = tid / c8;
+  const int ch = cg * 8;
+  const long row0 = static_cast<long>(blockIdx.x) * rows_per_tile;
+  const long row1 = min(m, row0 + rows_per_tile);
+  float s1[8], s2[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) s1[j] = s2[j] = 0.f;
+  if (rr < rows_per_pass) {
+    float sc[8], sh[8], mu[8], rs[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      sc[j] = scale[ch + j];
+      sh[j] = shift[ch + j];
+      mu[j] = mean[ch + j];
+      rs[j] = rstd[ch + j];
+    }
+    for (long row = row0 + rr; row < row1; row += rows_per_pass) {
+      const long off = row * c + ch;
+      float vv[8], hv[8], dv[8], o[8];
+      Vec8<T>::load(v + off, vv);
+      Vec8<T>::load(h + off, hv);
+      Vec8<T>::load(d + off, dv);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        o[j] = vv[j] - fmaf(sc[j], hv[j], sh[j]);
+        s1[j] += dv[j];
+        s2[j] += dv[j] * ((hv[j] - mu[j]) * rs[j]);
+      }
+      Vec8<T>::store(x + off, o);
+    }
+  }
+  // Fixed-order reduction over the rows_per_pass thread rows of each channel.
+  __shared__ float buf[2][256][9];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    buf[0][tid][j] = s1[j];
+    buf[1][tid][j] = s2[j];
+  }
+  __syncthreads();
+  for (int i = tid; i < 2 * c; i += 256) {
+    const int which = i / c, chh = i - which * c;
+    const int g = chh / 8, j = chh - g * 8;
+    float t = 0.f;
+    for (int q = 0; q < rows_per_pass; ++q) t += buf[which][q * c8 + g][j];
+    partials[(static_cast<long>(blockIdx.x) * 2 + which) * c + chh] = t;
+  }
+}
+
+int ew_rows_per_tile(long m, int c) {
+  const int rows_per_pass = 256 / (c / 8);
+  long want = (m + 1023) / 1024;
+  long rpt = ((want + rows_per_pass - 1) / rows_per_pass) * rows_per_pass;
+  if (rpt < rows_per_pass) rpt = rows_per_pass;
+  return static_cast<int>(rpt);
+}
+
+unsigned ew_grid(long total8) {
+  long b = (total8 + 255) / 256;
+  if (b > 65536) b = 65536;
+  if (b < 1) b = 1;
+  return static_cast<unsigned>(b);
+}
+
+}  // namespace
+
+int ew_tiles(long m, int c) {
+  const int rpt = ew_rows_per_tile(m, c);
+  return static_cast<int>((m + rpt - 1) / rpt);
+}
+
+void bn_stats_finalize(const float* partials, int tiles, int c, long m, const float* gamma,
+                       const float* beta, float eps, float* scale, float* shift, float* mean,
+                       float* rstd, float* run_mean, float* run_var, float momentum,
+                       hipStream_t st) {
+  dim3 grid((c + FIN_TX - 1) / FIN_TX), block(FIN_TX, FIN_TY);
+  hipLaunchKernelGGL(bn_stats_finalize_kernel, grid, block, 0, st, partials, tiles, c, m, gamma,
+                     beta, eps, scale, shift, mean, rstd, run_mean, run_var, momentum);
+}
+
+void bn_bwd_finalize(const float* partials, int tiles, int c, long m, const float* gamma,
+                     const float* mean, const float* rstd, float inv_k, float* dgamma,
+                     float* dbeta, float* ca, float* cb, float* cc, hipStream_t st) {
+  dim3 grid((c + FIN_TX - 1) / FIN_TX), block(FIN_TX, FIN_TY);
+  hipLaunchKernelGGL(bn_bwd_finalize_kernel, grid, block, 0, st, partials, tiles, c, m, gamma,
+                     mean, rstd, inv_k, dgamma, dbeta, ca, cb, cc);
+}
+
+void combine_fwd(int dtype, const void* r, const void* h, const float* scale, const float* shift,
+                 void* y, long m, int c, hipStream_t st) {
+  const long total8 = m * c / 8;
+  if (dtype == DT_BF16)
+    hipLaunchKernelGGL(combine_fwd_kernel<bf16_t>, dim3(ew_grid(total8)), dim3(256), 0, st,
+                       static_cast<const bf16_t*>(r), static_cast<const bf16_t*>(h), scale, shift,
+                       static_cast<bf16_t*>(y), total8, c / 8);
+  else
+    hipLaunchKernelGGL(combine_fwd_kernel<float>, dim3(ew_grid(total8)), dim3(256), 0, st,
+                       static_cast<const float*>(r), static_cast<const float*>(h), scale, shift,
+                       static_cast<float*>(y), total8, c / 8);
+}
+
+void bn_bwd_apply(int dtype, const void* d, const void* h, const float* ca, const float* cb,
+                  const float* cc, const float* mean, void* out, long m, int c, hipStream_t st) {
+  const long total8 = m * c / 8;
+  if (dtype == DT_BF16)
+    hipLaunchKernelGGL(bn_bwd_apply_kernel<bf16_t>, dim3(ew_grid(total8)), dim3(256), 0, st,
+                       static_cast<const bf16_t*>(d), static_cast<const bf16_t*>(h), ca, cb, cc,
+                       mean, static_cast<bf16_t*>(out), total8, c / 8);
+  else
+    hipLaunchKernelGGL(bn_bwd_apply_kernel<float>, dim3(ew_grid(total8)), dim3(256), 0, st,
+                       static_cast<const float*>(d), static_cast<const float*>(h), ca, cb, cc,
+                       mean, static_cast<float*>(out), total8, c / 8);
+}
+
+void combine_bwd(int dtype, const void* v, const void* h, const void* d, const float* scale,
+                 const float* shift, const float* mean, const float* rstd, void* x,
+                 float* partials, long m, int c, hipStream_t st) {
+  const int rpt = ew_rows_per_tile(m, c);
+  const int tiles = static_cast<int>((m + rpt - 1) / rpt);
+  if (dtype == DT_BF16)
+    hipLaunchKernelGGL(combine_bwd_kernel<bf16_t>, dim3(tiles), dim3(256), 0, st,
+                       static_cast<const bf16_t*>(v), static_cast<const bf16_t*>(h),
+                       static_cast<const bf16_t*>(d), scale, shift, mean, rstd,
+                       static_cast<bf16_t*>(x), partials, m, c, rpt);
+  else
+    hipLaunchKernelGGL(combine_bwd_kernel<float>, dim3(tiles), dim3(256), 0, st,
+                       static_cast<const float*>(v), static_cast<const float*>(h),
+                       static_cast<const float*>(d), scale, shift, mean, rstd,
+                       static_cast<float*>(x), partials, m, c, rpt);
+}
+
+}  // namespace petra

@@ -1,0 +1,287 @@
+// extern "C" entry points of petra.h: argument validation, error reporting
+// and dispatch to the stage program.  Nothing here allocates device memory.
+#include <cstdint>
+#include <cstdio>
+#include <new>
+#include <string>
+
+#include "stage.h"
+
+struct petra_stage {
+  petra::Stage* impl;
+};
+
+namespace {
+
+thread_local std::string g_last_error;
+
+petra_status fail(petra_status s, const std::string& msg) {
+  g_last_error = msg;
+  return s;
+}
+
+petra_status ok() { return PETRA_OK; }
+
+petra_status check_hip(const char* where) {
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess)
+    return fail(PETRA_ERR_HIP, std::string(where) + ": " + hipGetErrorString(e));
+  return PETRA_OK;
+}
+
+bool pow2_multiple_of_8(int c) {
+  if (c < 8 || c > 512 || c % 8 != 0) return false;
+  const int g = c / 8;
+  return (g & (g - 1)) == 0;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// [a, a+n) and [b, b+n) overlap without being identical.
+bool partial_overlap(const void* a, const void* b, size_t n) {
+  const char* x = static_cast<const char*>(a);
+  const char* y = static_cast<const char*>(b);
+  if (x == y) return false;
+  return x < y + n && y < x + n;
+}
+
+bool any_overlap(const void* a, const void* b, size_t n) {
+  const char* x = static_cast<const char*>(a);
+  const char* y = static_cast<const char*>(b);
+  return x < y + n && y < x + n;
+}
+
+petra_status check_ready(const petra_stage* st) {
+  if (st == nullptr || st->impl == nullptr) return fail(PETRA_ERR_INVALID_ARG, "null stage handle");
+  if (!st->impl->bound()) return fail(PETRA_ERR_STATE, "stage buffers not bound");
+  return PETRA_OK;
+}
+
+petra_status check_act(const void* p, const char* name) {
+  if (p == nullptr) return fail(PETRA_ERR_INVALID_ARG, std::string("null pointer: ") + name);
+  if (!aligned16(p)) return fail(PETRA_ERR_ALIGN, std::string("misaligned pointer: ") + name);
+  return PETRA_OK;
+}
+
+petra_status check_fwd(const petra::Stage& s, const void* x1, const void* x2, const void* y1,
+                       const void* y2) {
+  petra_status r;
+  if ((r = check_act(x1, "x1")) || (r = check_act(x2, "x2")) || (r = check_act(y1, "y1")) ||
+      (r = check_act(y2, "y2")))
+    return r;
+  const size_t n = static_cast<size_t>(s.M) * s.desc.c_half * s.esz;
+  if (any_overlap(x1, x2, n) || any_overlap(y1, y2, n) || any_overlap(x1, y2, n) ||
+      any_overlap(x2, y1, n) || partial_overlap(x1, y1, n) || partial_overlap(x2, y2, n))
+    return fail(PETRA_ERR_ALIAS, "forward buffers overlap (only x1==y1, x2==y2 allowed)");
+  return PETRA_OK;
+}
+
+petra_status check_bwd(const petra::Stage& s, const void* y1, const void* y2, const void* dy1,
+                       const void* dy2, const void* x1, const void* x2, const void* dx1,
+                       const void* dx2) {
+  petra_status r;
+  if ((r = check_act(y1, "y1")) || (r = check_act(y2, "y2")) || (r = check_act(dy1, "dy1")) ||
+      (r = check_act(dy2, "dy2")) || (r = check_act(x1, "x1")) || (r = check_act(x2, "x2")) ||
+      (r = check_act(dx1, "dx1")) || (r = check_act(dx2, "dx2")))
+    return r;
+  const size_t n = static_cast<size_t>(s.M) * s.desc.c_half * s.esz;
+  const void* in[4] = {y1, y2, dy1, dy2};
+  const void* out[4] = {x1, x2, dx1, dx2};
+  for (int i = 0; i < 4; ++i)
+    for (int j = 0; j < 4; ++j) {
+      if (i < j && (any_overlap(in[i], in[j], n) || any_overlap(out[i], out[j], n)))
+        return fail(PETRA_ERR_ALIAS, "backward inputs or outputs overlap each other");
+      if (i == j ? partial_overlap(in[i], out[j], n) : any_overlap(in[i], out[j], n))
+        return fail(PETRA_ERR_ALIAS,
+                    "backward buffers overlap (only x1==y1, x2==y2, dx1==dy1, dx2==dy2 allowed)");
+    }
+  return PETRA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* petra_status_str(petra_status s) {
+  switch (s) {
+    case PETRA_OK: return "PETRA_OK";
+    case PETRA_ERR_INVALID_ARG: return "PETRA_ERR_INVALID_ARG";
+    case PETRA_ERR_SHAPE: return "PETRA_ERR_SHAPE";
+    case PETRA_ERR_DTYPE: return "PETRA_ERR_DTYPE";
+    case PETRA_ERR_ALIGN: return "PETRA_ERR_ALIGN";
+    case PETRA_ERR_WORKSPACE: return "PETRA_ERR_WORKSPACE";
+    case PETRA_ERR_STATE: return "PETRA_ERR_STATE";
+    case PETRA_ERR_HIP: return "PETRA_ERR_HIP";
+    case PETRA_ERR_ALIAS: return "PETRA_ERR_ALIAS";
+  }
+  return "PETRA_ERR_UNKNOWN";
+}
+
+const char* petra_last_error(void) { return g_last_error.c_str(); }
+
+petra_status petra_stage_create(const petra_stage_desc* d, petra_stage** out) {
+  g_last_error.clear();
+  if (d == nullptr || out == nullptr) return fail(PETRA_ERR_INVALID_ARG, "null argument");
+  *out = nullptr;
+  if (d->dtype != PETRA_FP32 && d->dtype != PETRA_BF16)
+    return fail(PETRA_ERR_DTYPE, "dtype must be PETRA_FP32 or PETRA_BF16");
+  if (d->kind != PETRA_BLOCK_BASIC && d->kind != PETRA_BLOCK_BOTTLENECK)
+    return fail(PETRA_ERR_INVALID_ARG, "unknown block kind");
+  if (d->n < 1 || d->h < 1 || d->w < 1 || d->num_blocks < 1)
+    return fail(PETRA_ERR_SHAPE, "n, h, w and num_blocks must be positive");
+  if (!pow2_multiple_of_8(d->c_half))
+    return fail(PETRA_ERR_SHAPE, "c_half must be 8 times a power of two, at most 512");
+  if (d->kind == PETRA_BLOCK_BOTTLENECK && !pow2_multiple_of_8(d->c_mid))
+    return fail(PETRA_ERR_SHAPE, "c_mid must be 8 times a power of two, at most 512");
+  const long m = static_cast<long>(d->n) * d->h * d->w;
+  const long cm = d->kind == PETRA_BLOCK_BOTTLENECK && d->c_mid > d->c_half ? d->c_mid : d->c_half;
+  if (m * cm >= (1L << 31) || m >= (1L << 30))
+    return fail(PETRA_ERR_SHAPE, "activation too large (N*H*W*C must stay below 2^31)");
+  if (!(d->bn_eps > 0.f) || d->bn_momentum < 0.f || d->bn_momentum > 1.f)
+    return fail(PETRA_ERR_INVALID_ARG, "bn_eps must be > 0 and bn_momentum in [0, 1]");
+  const int convs = d->num_blocks * 2 * (d->kind == PETRA_BLOCK_BASIC ? 2 : 3);
+  if (convs > petra::MAX_WEIGHT_SEGS)
+    return fail(PETRA_ERR_SHAPE, "too many blocks for one stage handle");
+  petra_stage* h = new (std::nothrow) petra_stage;
+  if (h == nullptr) return fail(PETRA_ERR_INVALID_ARG, "host allocation failed");
+  h->impl = new (std::nothrow) petra::Stage(*d);
+  if (h->impl == nullptr) {
+    delete h;
+    return fail(PETRA_ERR_INVALID_ARG, "host allocation failed");
+  }
+  *out = h;
+  return ok();
+}
+
+petra_status petra_stage_destroy(petra_stage* st) {
+  if (st == nullptr) return PETRA_OK;
+  delete st->impl;
+  delete st;
+  return PETRA_OK;
+}
+
+petra_status petra_stage_query(const petra_stage* st, int64_t* n_params, int32_t* n_tensors,
+                               int64_t* n_bn_channels, size_t* workspace_bytes) {
+  if (st == nullptr || st->impl == nullptr) return fail(PETRA_ERR_INVALID_ARG, "null stage handle");
+  const petra::Stage& s = *st->impl;
+  if (n_params) *n_params = s.n_params;
+  if (n_tensors) *n_tensors = static_cast<int32_t>(s.infos.size());
+  if (n_bn_channels) *n_bn_channels = s.n_bnch;
+  if (workspace_bytes) *workspace_bytes = s.ws_need;
+  return ok();
+}
+
+petra_status petra_stage_param_info(const petra_stage* st, int32_t index, petra_param_info* out) {
+  if (st == nullptr || st->impl == nullptr || out == nullptr)
+    return fail(PETRA_ERR_INVALID_ARG, "null argument");
+  const petra::Stage& s = *st->impl;
+  if (index < 0 || index >= static_cast<int32_t>(s.infos.size()))
+    return fail(PETRA_ERR_INVALID_ARG, "tensor index out of range");
+  *out = s.infos[index];
+  return ok();
+}
+
+petra_status petra_stage_bind(petra_stage* st, float* params, float* grad_accum, float* momentum,
+                              float* run_mean, float* run_var, void* workspace,
+                              size_t workspace_bytes) {
+  if (st == nullptr || st->impl == nullptr) return fail(PETRA_ERR_INVALID_ARG, "null stage handle");
+  if (!params || !grad_accum || !momentum || !run_mean || !run_var)
+    return fail(PETRA_ERR_INVALID_ARG, "null buffer");
+  if (workspace == nullptr || workspace_bytes < st->impl->ws_need)
+    return fail(PETRA_ERR_WORKSPACE, "workspace missing or smaller than petra_stage_query()");
+  const void* ptrs[6] = {params, grad_accum, momentum, run_mean, run_var, workspace};
+  for (const void* p : ptrs)
+    if (!aligned16(p)) return fail(PETRA_ERR_ALIGN, "buffers must be 16-byte aligned");
+  if (reinterpret_cast<uintptr_t>(workspace) & 255u)
+    return fail(PETRA_ERR_ALIGN, "workspace must be 256-byte aligned");
+  st->impl->bind(params, grad_accum, momentum, run_mean, run_var, workspace);
+  return ok();
+}
+
+petra_status petra_stage_set_optimizer(petra_stage* st, const petra_sgd* opt) {
+  if (st == nullptr || st->impl == nullptr || opt == nullptr)
+    return fail(PETRA_ERR_INVALID_ARG, "null argument");
+  if (!(opt->lr >= 0.f) || !(opt->momentum >= 0.f) || opt->momentum >= 1.f ||
+      !(opt->weight_decay >= 0.f) || opt->accum_k < 1)
+    return fail(PETRA_ERR_INVALID_ARG, "need lr >= 0, 0 <= momentum < 1, weight_decay >= 0, accum_k >= 1");
+  st->impl->opt = *opt;
+  return ok();
+}
+
+petra_status petra_stage_sync_weights(petra_stage* st, void* stream) {
+  petra_status r = check_ready(st);
+  if (r) return r;
+  (void)hipGetLastError();
+  st->impl->sync_weights(static_cast<hipStream_t>(stream));
+  return check_hip("petra_stage_sync_weights");
+}
+
+petra_status petra_stage_forward(petra_stage* st, const void* x1, const void* x2, void* y1,
+                                 void* y2, void* stream) {
+  petra_status r = check_ready(st);
+  if (r) return r;
+  if ((r = check_fwd(*st->impl, x1, x2, y1, y2))) return r;
+  if ((r = check_hip("before petra_stage_forward"))) return r;
+  st->impl->forward(x1, x2, y1, y2, static_cast<hipStream_t>(stream));
+  return check_hip("petra_stage_forward");
+}
+
+petra_status petra_stage_reconstruct_backward(petra_stage* st, const void* y1, const void* y2,
+                                              const void* dy1, const void* dy2, void* x1,
+                                              void* x2, void* dx1, void* dx2, void* stream) {
+  petra_status r = check_ready(st);
+  if (r) return r;
+  if ((r = check_bwd(*st->impl, y1, y2, dy1, dy2, x1, x2, dx1, dx2))) return r;
+  if ((r = check_hip("before petra_stage_reconstruct_backward"))) return r;
+  st->impl->backward(y1, y2, dy1, dy2, x1, x2, dx1, dx2, static_cast<hipStream_t>(stream));
+  return check_hip("petra_stage_reconstruct_backward");
+}
+
+petra_status petra_stage_update(petra_stage* st, void* stream, int32_t* updated) {
+  petra_status r = check_ready(st);
+  if (r) return r;
+  if ((r = check_hip("before petra_stage_update"))) return r;
+  const bool did = st->impl->update(static_cast<hipStream_t>(stream));
+  if (updated) *updated = did ? 1 : 0;
+  return check_hip("petra_stage_update");
+}
+
+petra_status petra_stage_step(petra_stage* st, const void* x1, const void* x2, void* y1, void* y2,
+                              const void* yb1, const void* yb2, const void* dyb1,
+                              const void* dyb2, void* xb1, void* xb2, void* dxb1, void* dxb2,
+                              void* stream, int32_t* updated) {
+  petra_status r = check_ready(st);
+  if (r) return r;
+  petra::Stage& s = *st->impl;
+  if ((r = check_fwd(s, x1, x2, y1, y2))) return r;
+  if ((r = check_bwd(s, yb1, yb2, dyb1, dyb2, xb1, xb2, dxb1, dxb2))) return r;
+  const size_t n = static_cast<size_t>(s.M) * s.desc.c_half * s.esz;
+  const void* f[4] = {x1, x2, y1, y2};
+  const void* b[8] = {yb1, yb2, dyb1, dyb2, xb1, xb2, dxb1, dxb2};
+  for (const void* p : f)
+    for (const void* q : b)
+      if (any_overlap(p, q, n))
+        return fail(PETRA_ERR_ALIAS, "forward and backward buffers of a step overlap");
+  if ((r = check_hip("before petra_stage_step"))) return r;
+  const hipError_t e = s.ensure_streams();
+  if (e != hipSuccess) return fail(PETRA_ERR_HIP, std::string("stream setup: ") + hipGetErrorString(e));
+  hipStream_t main = static_cast<hipStream_t>(stream);
+  // fork: both passes start after prior work on `stream`
+  if (hipEventRecord(s.ev_fork, main) != hipSuccess ||
+      hipStreamWaitEvent(s.s_fwd, s.ev_fork, 0) != hipSuccess ||
+      hipStreamWaitEvent(s.s_bwd, s.ev_fork, 0) != hipSuccess)
+    return check_hip("petra_stage_step fork");
+  s.forward(x1, x2, y1, y2, s.s_fwd);
+  s.backward(yb1, yb2, dyb1, dyb2, xb1, xb2, dxb1, dxb2, s.s_bwd);
+  // join: the update (and later work on `stream`) follow both passes (Eq. 5)
+  if (hipEventRecord(s.ev_fwd, s.s_fwd) != hipSuccess ||
+      hipEventRecord(s.ev_bwd, s.s_bwd) != hipSuccess ||
+      hipStreamWaitEvent(main, s.ev_fwd, 0) != hipSuccess ||
+      hipStreamWaitEvent(main, s.ev_bwd, 0) != hipSuccess)
+    return check_hip("petra_stage_step join");
+  const bool did = s.update(main);
+  if (updated) *updated = did ? 1 : 0;
+  return check_hip("petra_stage_step");
+}
+
+}  // extern "C"

@@ -1,0 +1,111 @@
+// Host-side program of one reversible stage: layer tables, workspace plan and
+// the kernel sequences of the forward, the reconstruct+VJP backward and the
+// update (internal to the library; the C ABI wraps it).
+#pragma once
+
+#include <string>
+#include <vector>
+
+#include "../../include/petra.h"
+#include "kernels.h"
+
+namespace petra {
+
+struct ConvLayer {
+  int cin, cout, r, s, pad;
+  int64_t w_off;   // offset of the KRSC weight in the flat buffers and the forward copy
+  int64_t dg_off;  // offset in the transposed/flipped copy
+  int bn;          // BN layer that follows
+};
+
+struct BnLayer {
+  int c;
+  int64_t g_off, b_off;  // gamma / beta offsets in the flat buffers
+  int64_t run_off;       // offset into the running-statistics arrays
+};
+
+struct ResidualFn {
+  int nconv;
+  int conv[3];
+};
+
+struct Block {
+  ResidualFn f, g;
+};
+
+// Device scratch of one pass (forward or backward), carved from the workspace.
+struct Scratch {
+  void* h[3] = {nullptr, nullptr, nullptr};  // pre-BN conv outputs of the current function
+  void* d0 = nullptr;                        // BN input gradient dh (backward)
+  void* d1 = nullptr;                        // masked gradient dz (backward)
+  float* part = nullptr;                     // per-tile statistic partials [tiles][2][c]
+  float* bnp = nullptr;                      // per layer: scale, shift, mean, rstd, ca, cb, cc
+  float* wpart = nullptr;                    // weight-gradient split partials
+  float* vec(int layer, int which, int cmax) const { return bnp + (layer * 8 + which) * cmax; }
+};
+
+enum { V_SCALE = 0, V_SHIFT, V_MEAN, V_RSTD, V_CA, V_CB, V_CC };
+
+class Stage {
+ public:
+  explicit Stage(const petra_stage_desc& d);
+  ~Stage();
+
+  petra_stage_desc desc;
+  int dt;
+  size_t esz;
+  long M;
+  int cmax;
+  std::vector<ConvLayer> convs;
+  std::vector<BnLayer> bns;
+  std::vector<Block> blocks;
+  std::vector<petra_param_info> infos;
+  int64_t n_params = 0, n_conv = 0, n_bnch = 0;
+  WeightSegTable segs{};
+
+  // Workspace plan (byte offsets).
+  size_t ws_need = 0;
+  size_t off_wfwd = 0, off_wdg = 0;
+  struct ScratchPlan {
+    size_t h[3], d0, d1, part, bnp, wpart;
+  } plan_f{}, plan_b{};
+  int64_t wpart_floats = 0;
+
+  // Bound buffers.
+  float* theta = nullptr;
+  float* grad = nullptr;
+  float* mom = nullptr;
+  float* rmean = nullptr;
+  float* rvar = nullptr;
+  char* ws = nullptr;
+  void* wfwd = nullptr;
+  void* wdg = nullptr;
+  Scratch sf, sb;
+
+  petra_sgd opt{0.1f, 0.9f, 0.0f, 1, 1};
+  int64_t bwd_count = 0, last_update = 0;
+
+  hipStream_t s_fwd = nullptr, s_bwd = nullptr;
+  hipEvent_t ev_fork = nullptr, ev_fwd = nullptr, ev_bwd = nullptr;
+
+  bool bound() const { return theta != nullptr; }
+  void bind(float* th, float* gr, float* mo, float* rm, float* rv, void* w);
+  void sync_weights(hipStream_t st);
+  void forward(const void* x1, const void* x2, void* y1, void* y2, hipStream_t st);
+  void backward(const void* y1, const void* y2, const void* dy1, const void* dy2, void* x1,
+                void* x2, void* dx1, void* dx2, hipStream_t st);
+  bool update(hipStream_t st);
+  hipError_t ensure_streams();
+
+ private:
+  void fn_recompute(const ResidualFn& fn, const void* u, Scratch& s, bool running,
+                    hipStream_t st);
+  void fn_forward(const ResidualFn& fn, const void* u, const void* r, void* y, Scratch& s,
+                  hipStream_t st);
+  void fn_backward(const ResidualFn& fn, const void* u, const void* v, const void* d,
+                   const void* rg, void* xrec, void* dout, Scratch& s, hipStream_t st);
+  ConvArgs conv_args(const ConvLayer& cv) const;
+  void wgrad_splits(const ConvLayer& cv, int* splits, int* rows_per_split) const;
+};
+
+}  // namespace petra

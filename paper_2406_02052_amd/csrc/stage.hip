@@ -1,0 +1,338 @@
+// Kernel sequences of one reversible stage (host side).
+//
+// Forward of a residual function Phi = conv-BN[-ReLU-conv-BN...] on input u,
+// coupled as y = r + Phi(u) (Sec. 3.2):
+//   conv_l (BN_{l-1}+ReLU applied in the prologue; sum/sum^2 partials in the
+//   epilogue) -> finalize BN_l -> ... -> combine_fwd y = r + BN_L(h_L).
+// Backward of the same coupling given its output-side stream v, the upstream
+// gradient d of the coupling output and the residual gradient rg (Eq. 4-5):
+//   recompute convs (running statistics move here only, Sec. 4.1)
+//   -> combine_bwd: x = v - BN_L(h_L), with sum d and sum d*xhat partials
+//   -> per layer from the top: dh = BN backward (elementwise), weight gradient
+//      (split rows, fixed-order reduce into the accumulator, scaled 1/k),
+//      input gradient conv whose epilogue applies the ReLU mask of the layer
+//      below and emits that layer's BN-backward partials, or, for the first
+//      layer, adds the residual gradient: dout = rg + d Phi/du^T d.
+#include <algorithm>
+#include <cstring>
+
+#include "stage.h"
+
+namespace petra {
+
+namespace {
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+}  // namespace
+
+Stage::Stage(const petra_stage_desc& d) : desc(d) {
+  dt = d.dtype == PETRA_BF16 ? DT_BF16 : DT_FP32;
+  esz = dt == DT_BF16 ? 2 : 4;
+  M = static_cast<long>(d.n) * d.h * d.w;
+  const int c = d.c_half, cm = d.c_mid;
+
+  // Canonical order: block, function F then G, conv; each conv followed by its BN.
+  struct Shape { int cout, r, s, cin; };
+  std::vector<Shape> fn_shapes;
+  if (d.kind == PETRA_BLOCK_BASIC)
+    fn_shapes = {{c, 3, 3, c}, {c, 3, 3, c}};
+  else
+    fn_shapes = {{cm, 1, 1, c}, {cm, 3, 3, cm}, {c, 1, 1, cm}};
+  cmax = 0;
+  for (auto& s : fn_shapes) cmax = std::max(cmax, std::max(s.cout, s.cin));
+
+  // Flat layout: all conv weights first (weight-decayed range), then per BN gamma, beta.
+  int64_t woff = 0;
+  for (int b = 0; b < d.num_blocks; ++b)
+    for (int f = 0; f < 2; ++f)
+      for (auto& s : fn_shapes) woff += static_cast<int64_t>(s.cout) * s.r * s.s * s.cin;
+  n_conv = woff;
+  int64_t w_cur = 0, bn_cur = n_conv, run_cur = 0;
+  blocks.resize(d.num_blocks);
+  for (int b = 0; b < d.num_blocks; ++b) {
+    for (int f = 0; f < 2; ++f) {
+      ResidualFn fn{};
+      fn.nconv = static_cast<int>(fn_shapes.size());
+      for (size_t l = 0; l < fn_shapes.size(); ++l) {
+        const Shape& s = fn_shapes[l];
+        ConvLayer cv{};
+        cv.cin = s.cin; cv.cout = s.cout; cv.r = s.r; cv.s = s.s; cv.pad = (s.r - 1) / 2;
+        cv.w_off = w_cur;
+        cv.dg_off = w_cur;  // the transposed copy uses the same offsets in its own buffer
+        const int64_t numel = static_cast<int64_t>(s.cout) * s.r * s.s * s.cin;
+        w_cur += numel;
+        BnLayer bnl{};
+        bnl.c = s.cout;
+        bnl.g_off = bn_cur;
+        bnl.b_off = bn_cur + s.cout;
+        bnl.run_off = run_cur;
+        bn_cur += 2 * s.cout;
+        run_cur += s.cout;
+        cv.bn = static_cast<int>(bns.size());
+        bns.push_back(bnl);
+        fn.conv[l] = static_cast<int>(convs.size());
+        convs.push_back(cv);
+
+        petra_param_info wi{};
+        wi.offset = cv.w_off; wi.numel = numel; wi.role = PETRA_ROLE_CONV_WEIGHT; wi.ndim = 4;
+        wi.shape[0] = s.cout; wi.shape[1] = s.r; wi.shape[2] = s.s; wi.shape[3] = s.cin;
+        wi.weight_decay = 1; wi.bn_index = cv.bn;
+        infos.push_back(wi);
+        petra_param_info gi{};
+        gi.offset = bnl.g_off; gi.numel = s.cout; gi.role = PETRA_ROLE_BN_GAMMA; gi.ndim = 1;
+        gi.shape[0] = s.cout; gi.weight_decay = 0; gi.bn_index = cv.bn;
+        infos.push_back(gi);
+        petra_param_info bi = gi;
+        bi.offset = bnl.b_off; bi.role = PETRA_ROLE_BN_BETA;
+        infos.push_back(bi);
+      }
+      if (f == 0) blocks[b].f = fn; else blocks[b].g = fn;
+    }
+  }
+  n_params = bn_cur;
+  n_bnch = run_cur;
+  segs.nseg = static_cast<int>(convs.size());
+  for (size_t i = 0; i < convs.size() && i < static_cast<size_t>(MAX_WEIGHT_SEGS); ++i) {
+    const ConvLayer& cv = convs[i];
+    segs.seg[i] = WeightSeg{cv.w_off, cv.dg_off, cv.cout, cv.r, cv.s, cv.cin};
+  }
+
+  // Workspace plan.
+  const int tiles_conv = static_cast<int>((M + CONV_BM - 1) / CONV_BM);
+  int tiles_max = tiles_conv;
+  for (auto& s : fn_shapes) tiles_max = std::max(tiles_max, ew_tiles(M, s.cout));
+  int64_t wmax = 0;
+  for (auto& cv : convs) {
+    int sp, rps;
+    wgrad_splits(cv, &sp, &rps);
+    wmax = std::max<int64_t>(wmax, static_cast<int64_t>(sp) * cv.cout * cv.r * cv.s * cv.cin);
+  }
+  wpart_floats = wmax;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align_up(off + bytes, 256);
+    return o;
+  };
+  off_wfwd = take(static_cast<size_t>(n_conv) * esz);
+  off_wdg = take(static_cast<size_t>(n_conv) * esz);
+  for (ScratchPlan* p : {&plan_f, &plan_b}) {
+    for (size_t l = 0; l < 3; ++l)
+      p->h[l] = l < fn_shapes.size() ? take(static_cast<size_t>(M) * fn_shapes[l].cout * esz) : 0;
+    const bool bwd = p == &plan_b;
+    p->d0 = bwd ? take(static_cast<size_t>(M) * cmax * esz) : 0;
+    p->d1 = bwd ? take(static_cast<size_t>(M) * cmax * esz) : 0;
+    p->part = take(static_cast<size_t>(tiles_max) * 2 * cmax * sizeof(float));
+    p->bnp = take(static_cast<size_t>(3) * 8 * cmax * sizeof(float));
+    p->wpart = bwd ? take(static_cast<size_t>(wpart_floats) * sizeof(float)) : 0;
+  }
+  ws_need = off;
+}
+
+Stage::~Stage() {
+  if (ev_fork) (void)hipEventDestroy(ev_fork);
+  if (ev_fwd) (void)hipEventDestroy(ev_fwd);
+  if (ev_bwd) (void)hipEventDestroy(ev_bwd);
+  if (s_fwd) (void)hipStreamDestroy(s_fwd);
+  if (s_bwd) (void)hipStreamDestroy(s_bwd);
+}
+
+void Stage::bind(float* th, float* gr, float* mo, float* rm, float* rv, void* w) {
+  theta = th; grad = gr; mom = mo; rmean = rm; rvar = rv;
+  ws = static_cast<char*>(w);
+  wfwd = ws + off_wfwd;
+  wdg = ws + off_wdg;
+  for (int pass = 0; pass < 2; ++pass) {
+    const ScratchPlan& p = pass == 0 ? plan_f : plan_b;
+    Scratch& s = pass == 0 ? sf : sb;
+    const int nl = blocks.empty() ? 0 : blocks[0].f.nconv;
+    for (int l = 0; l < 3; ++l) s.h[l] = l < nl ? ws + p.h[l] : nullptr;
+    s.d0 = pass == 1 ? ws + p.d0 : nullptr;
+    s.d1 = pass == 1 ? ws + p.d1 : nullptr;
+    s.part = reinterpret_cast<float*>(ws + p.part);
+    s.bnp = reinterpret_cast<float*>(ws + p.bnp);
+    s.wpart = pass == 1 ? reinterpret_cast<float*>(ws + p.wpart) : nullptr;
+  }
+}
+
+hipError_t Stage::ensure_streams() {
+  if (s_fwd) return hipSuccess;
+  hipError_t e;
+  if ((e = hipStreamCreateWithFlags(&s_fwd, hipStreamNonBlocking)) != hipSuccess) return e;
+  if ((e = hipStreamCreateWithFlags(&s_bwd, hipStreamNonBlocking)) != hipSuccess) return e;
+  if ((e = hipEventCreateWithFlags(&ev_fork, hipEventDisableTiming)) != hipSuccess) return e;
+  if ((e = hipEventCreateWithFlags(&ev_fwd, hipEventDisableTiming)) != hipSuccess) return e;
+  return hipEventCreateWithFlags(&ev_bwd, hipEventDisableTiming);
+}
+
+void Stage::sync_weights(hipStream_t st) { refresh_weights(dt, theta, segs, n_conv, wfwd, wdg, st); }
+
+ConvArgs Stage::conv_args(const ConvLayer& cv) const {
+  ConvArgs a{};
+  a.n = desc.n; a.h = desc.h; a.w = desc.w;
+  a.p = desc.h; a.q = desc.w;
+  a.r = cv.r; a.s = cv.s; a.stride = 1; a.pad = cv.pad;
+  a.m = static_cast<int>(M);
+  return a;
+}
+
+void Stage::wgrad_splits(const ConvLayer& cv, int* splits, int* rows_per_split) const {
+  const int ktot = cv.r * cv.s * cv.cin;
+  const int bo = cv.cout <= 32 ? 32 : 64;
+  const int tiles = ((ktot + 63) / 64) * ((cv.cout + bo - 1) / bo);
+  int sp = std::max(1, 1024 / std::max(1, tiles));
+  long rps = (M + sp - 1) / sp;
+  rps = std::max<long>(rps, 256);
+  rps = (rps + 31) / 32 * 32;
+  sp = static_cast<int>((M + rps - 1) / rps);
+  *splits = sp;
+  *rows_per_split = static_cast<int>(rps);
+}
+
+void Stage::fn_recompute(const ResidualFn& fn, const void* u, Scratch& s, bool running,
+                         hipStream_t st) {
+  const int tiles = static_cast<int>((M + CONV_BM - 1) / CONV_BM);
+  for (int l = 0; l < fn.nconv; ++l) {
+    const ConvLayer& cv = convs[fn.conv[l]];
+    const BnLayer& bn = bns[cv.bn];
+    ConvArgs a = conv_args(cv);
+    a.src = l == 0 ? u : s.h[l - 1];
+    a.c_in = cv.cin;
+    a.c_split = cv.cin;
+    if (l > 0) {
+      a.pro_scale = s.vec(l - 1, V_SCALE, cmax);
+      a.pro_shift = s.vec(l - 1, V_SHIFT, cmax);
+    }
+    a.wt = static_cast<char*>(wfwd) + cv.w_off * esz;
+    a.out = s.h[l];
+    a.c_out = cv.cout;
+    a.k_tot = cv.r * cv.s * cv.cin;
+    a.partials = s.part;
+    conv_gemm(dt, a, EP_STATS, st);
+    bn_stats_finalize(s.part, tiles, cv.cout, M, theta + bn.g_off, theta + bn.b_off, desc.bn_eps,
+                      s.vec(l, V_SCALE, cmax), s.vec(l, V_SHIFT, cmax), s.vec(l, V_MEAN, cmax),
+                      s.vec(l, V_RSTD, cmax), running ? rmean + bn.run_off : nullptr,
+                      running ? rvar + bn.run_off : nullptr, desc.bn_momentum, st);
+  }
+}
+
+void Stage::fn_forward(const ResidualFn& fn, const void* u, const void* r, void* y, Scratch& s,
+                       hipStream_t st) {
+  fn_recompute(fn, u, s, false, st);
+  const int L = fn.nconv - 1;
+  combine_fwd(dt, r, s.h[L], s.vec(L, V_SCALE, cmax), s.vec(L, V_SHIFT, cmax), y, M,
+              convs[fn.conv[L]].cout, st);
+}
+
+void Stage::fn_backward(const ResidualFn& fn, const void* u, const void* v, const void* d,
+                        const void* rg, void* xrec, void* dout, Scratch& s, hipStream_t st) {
+  const float inv_k = 1.0f / static_cast<float>(std::max(1, opt.accum_k));
+  const int tiles_conv = static_cast<int>((M + CONV_BM - 1) / CONV_BM);
+  fn_recompute(fn, u, s, true, st);
+  const int L = fn.nconv - 1;
+  {
+    const ConvLayer& cv = convs[fn.conv[L]];
+    const BnLayer& bn = bns[cv.bn];
+    combine_bwd(dt, v, s.h[L], d, s.vec(L, V_SCALE, cmax), s.vec(L, V_SHIFT, cmax),
+                s.vec(L, V_MEAN, cmax), s.vec(L, V_RSTD, cmax), xrec, s.part, M, cv.cout, st);
+    bn_bwd_finalize(s.part, ew_tiles(M, cv.cout), cv.cout, M, theta + bn.g_off,
+                    s.vec(L, V_MEAN, cmax), s.vec(L, V_RSTD, cmax), inv_k, grad + bn.g_off,
+                    grad + bn.b_off, s.vec(L, V_CA, cmax), s.vec(L, V_CB, cmax),
+                    s.vec(L, V_CC, cmax), st);
+  }
+  const void* dsrc = d;
+  for (int l = L; l >= 0; --l) {
+    const ConvLayer& cv = convs[fn.conv[l]];
+    // dh_l = BN_l backward applied to the gradient of its output
+    bn_bwd_apply(dt, dsrc, s.h[l], s.vec(l, V_CA, cmax), s.vec(l, V_CB, cmax),
+                 s.vec(l, V_CC, cmax), s.vec(l, V_MEAN, cmax), s.d0, M, cv.cout, st);
+    // weight gradient of conv_l
+    WgradArgs w{};
+    w.dh = s.d0;
+    w.src = l == 0 ? u : s.h[l - 1];
+    w.c_split = cv.cin;
+    if (l > 0) {
+      w.pro_scale = s.vec(l - 1, V_SCALE, cmax);
+      w.pro_shift = s.vec(l - 1, V_SHIFT, cmax);
+    }
+    w.partials = s.wpart;
+    w.n = desc.n; w.h = desc.h; w.w = desc.w; w.c_in = cv.cin; w.p = desc.h; w.q = desc.w;
+    w.c_out = cv.cout; w.r = cv.r; w.s = cv.s; w.stride = 1; w.pad = cv.pad;
+    w.k_tot = cv.r * cv.s * cv.cin;
+    w.m = static_cast<int>(M);
+    wgrad_splits(cv, &w.splits, &w.rows_per_split);
+    conv_wgrad(dt, w, st);
+    wgrad_reduce(s.wpart, w.splits, static_cast<long>(cv.cout) * w.k_tot, inv_k, grad + cv.w_off,
+                 st);
+    // input gradient: conv of dh with the transposed, flipped weights
+    ConvArgs a = conv_args(cv);
+    a.src = s.d0;
+    a.c_in = cv.cout;
+    a.c_split = cv.cout;
+    a.wt = static_cast<char*>(wdg) + cv.dg_off * esz;
+    a.c_out = cv.cin;
+    a.k_tot = cv.r * cv.s * cv.cout;
+    if (l > 0) {
+      const ConvLayer& lo = convs[fn.conv[l - 1]];
+      const BnLayer& bl = bns[lo.bn];
+      a.out = s.d1;
+      a.ep_h = s.h[l - 1];
+      a.ep_scale = s.vec(l - 1, V_SCALE, cmax);
+      a.ep_shift = s.vec(l - 1, V_SHIFT, cmax);
+      a.ep_mean = s.vec(l - 1, V_MEAN, cmax);
+      a.ep_rstd = s.vec(l - 1, V_RSTD, cmax);
+      a.partials = s.part;
+      conv_gemm(dt, a, EP_MASK, st);
+      bn_bwd_finalize(s.part, tiles_conv, lo.cout, M, theta + bl.g_off, s.vec(l - 1, V_MEAN, cmax),
+                      s.vec(l - 1, V_RSTD, cmax), inv_k, grad + bl.g_off, grad + bl.b_off,
+                      s.vec(l - 1, V_CA, cmax), s.vec(l - 1, V_CB, cmax),
+                      s.vec(l - 1, V_CC, cmax), st);
+      dsrc = s.d1;
+    } else {
+      a.out = dout;
+      a.resid = rg;
+      conv_gemm(dt, a, EP_RESID, st);
+    }
+  }
+}
+
+void Stage::forward(const void* x1, const void* x2, void* y1, void* y2, hipStream_t st) {
+  const void* a1 = x1;
+  const void* a2 = x2;
+  for (const Block& b : blocks) {
+    fn_forward(b.f, a2, a1, y1, sf, st);   // y1 = x1 + F(x2)
+    fn_forward(b.g, y1, a2, y2, sf, st);   // y2 = x2 + G(y1)
+    a1 = y1;
+    a2 = y2;
+  }
+}
+
+void Stage::backward(const void* y1, const void* y2, const void* dy1, const void* dy2, void* x1,
+                     void* x2, void* dx1, void* dx2, hipStream_t st) {
+  const void* c1 = y1;
+  const void* c2 = y2;
+  const void* g1 = dy1;
+  const void* g2 = dy2;
+  for (int b = static_cast<int>(blocks.size()) - 1; b >= 0; --b) {
+    const Block& blk = blocks[b];
+    // x2 = y2 - G(y1); z1 = g1 + dG/dy1^T g2  (written to dx1)
+    fn_backward(blk.g, c1, c2, g2, g1, x2, dx1, sb, st);
+    // x1 = y1 - F(x2); dx2 = g2 + dF/dx2^T z1
+    fn_backward(blk.f, x2, c1, dx1, g2, x1, dx2, sb, st);
+    c1 = x1; c2 = x2; g1 = dx1; g2 = dx2;
+  }
+  ++bwd_count;
+}
+
+bool Stage::update(hipStream_t st) {
+  const int k = std::max(1, opt.accum_k);
+  if (bwd_count == 0 || bwd_count == last_update || bwd_count % k != 0) return false;
+  sgd_update(theta, grad, mom, n_params, n_conv, opt.lr, opt.momentum, opt.weight_decay,
+             opt.nesterov, st);
+  sync_weights(st);
+  last_update = bwd_count;
+  return true;
+}
+
+}  // namespace petra

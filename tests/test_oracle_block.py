@@ -158,3 +158,34 @@ def test_running_stats_only_in_backward_and_match_torch():
             slot = (base + 3 * l) // 3
             np.testing.assert_allclose(st.run_mean[slot], run[l][0].numpy(), rtol=1e-10, atol=1e-14)
             np.testing.assert_allclose(st.run_var[slot], run[l][1].numpy(), rtol=1e-10)
+
+
+def test_storage_hook_points_and_fixed_points():
+    # The storage map is applied where tensors are materialised: per function
+    # L conv outputs + (L-1) ReLU activations, plus the coupling output.
+    wl = tiny("basic", 2, n=2, h=4, w=4, c=4)
+    calls = []
+
+    def store(a):
+        calls.append(a.shape)
+        return synth.round_bf16(a)
+    params = [p.astype(np.float64) for p in synth.stage_params(wl, "random")]
+    st = StageState(params, [n for n, _ in wl.param_shapes()], 2, store=store)
+    x1, x2, dy1, dy2 = (synth.round_bf16(a.astype(np.float32)).astype(np.float64)
+                        for a in rand_io(wl, 2))
+    y1, y2 = st.forward(x1, x2)
+    assert len(calls) == wl.blocks * 2 * (2 + 1 + 1)
+    for t in (y1, y2):
+        assert np.array_equal(synth.round_bf16(t.astype(np.float32)), t)
+    calls.clear()
+    rx1, rx2, dx1, dx2, _ = st.backward(y1, y2, dy1, dy2)
+    # per function: recompute (2 h + 1 act) + reconstruction + output gradient
+    # + dh of both layers + dz of the inner layer
+    assert len(calls) == wl.blocks * 2 * (3 + 1 + 1 + 2 + 1)
+    for t in (rx1, rx2, dx1, dx2):
+        assert np.array_equal(synth.round_bf16(t.astype(np.float32)), t)
+    # the bf16-stored result stays near the fp64 one
+    ref = make_state(wl)
+    ry1, ry2 = ref.forward(x1, x2)
+    assert np.linalg.norm(y1 - ry1) <= 1e-2 * np.linalg.norm(ry1)
+    assert np.linalg.norm(rx1 - x1) <= 5e-2 * np.linalg.norm(x1)
