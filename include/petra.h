@@ -187,6 +187,19 @@ petra_status petra_stage_step(petra_stage* st, const void* x1, const void* x2, v
                               const void* dyb2, void* xb1, void* xb2, void* dxb1, void* dxb2,
                               void* stream, int32_t* updated);
 
+/* Measurement support (not part of the method).  petra_stage_profile(st, 1)
+ * clears the counters and starts bracketing every kernel launch of the stage
+ * with HIP events on the stream the kernel is launched on; 0 stops it.
+ * petra_stage_profile_read() waits for the recorded events and returns, for
+ * kernel class `kernel_class` (0 .. until it returns PETRA_ERR_INVALID_ARG),
+ * its name, launch count, summed device time in ms and the summed algorithmic
+ * flops and bytes of those launches (compulsory traffic of each launch: every
+ * operand read once, every result written once). */
+petra_status petra_stage_profile(petra_stage* st, int32_t enable);
+petra_status petra_stage_profile_read(petra_stage* st, int32_t kernel_class, const char** name,
+                                      int64_t* launches, double* total_ms, double* flops,
+                                      double* bytes);
+
 #ifdef __cplusplus
 }
 #endif

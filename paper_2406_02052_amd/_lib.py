@@ -68,6 +68,13 @@ _SIGS = {
     "petra_stage_reconstruct_backward": (ctypes.c_int, [_VP] * 10),
     "petra_stage_update": (ctypes.c_int, [_VP, _VP, ctypes.POINTER(ctypes.c_int32)]),
     "petra_stage_step": (ctypes.c_int, [_VP] * 14 + [ctypes.POINTER(ctypes.c_int32)]),
+    "petra_stage_profile": (ctypes.c_int, [_VP, ctypes.c_int32]),
+    "petra_stage_profile_read": (ctypes.c_int, [_VP, ctypes.c_int32,
+                                                 ctypes.POINTER(ctypes.c_char_p),
+                                                 ctypes.POINTER(ctypes.c_int64),
+                                                 ctypes.POINTER(ctypes.c_double),
+                                                 ctypes.POINTER(ctypes.c_double),
+                                                 ctypes.POINTER(ctypes.c_double)]),
 }
 
 _lib: Optional[ctypes.CDLL] = None
@@ -192,3 +199,25 @@ def petra_stage_step(handle, x1, x2, y1, y2, yb1, yb2, dyb1, dyb2, xb1, xb2, dxb
                                    _ptr(dxb1), _ptr(dxb2), _stream(stream), ctypes.byref(upd)),
            "petra_stage_step")
     return bool(upd.value)
+
+
+def petra_stage_profile(handle, enable: bool) -> None:
+    _check(load().petra_stage_profile(handle, 1 if enable else 0), "petra_stage_profile")
+
+
+def petra_stage_profile_read(handle):
+    """All kernel classes: {name: (launches, total_ms, flops, bytes)}."""
+    out = {}
+    i = 0
+    while True:
+        name = ctypes.c_char_p()
+        n, ms = ctypes.c_int64(), ctypes.c_double()
+        fl, by = ctypes.c_double(), ctypes.c_double()
+        st = load().petra_stage_profile_read(handle, i, ctypes.byref(name), ctypes.byref(n),
+                                             ctypes.byref(ms), ctypes.byref(fl), ctypes.byref(by))
+        if st != 0:
+            if STATUS[st] == "PETRA_ERR_INVALID_ARG":
+                return out
+            _check(st, "petra_stage_profile_read")
+        out[name.value.decode()] = (n.value, ms.value, fl.value, by.value)
+        i += 1

@@ -284,4 +284,31 @@ petra_status petra_stage_step(petra_stage* st, const void* x1, const void* x2, v
   return check_hip("petra_stage_step");
 }
 
+petra_status petra_stage_profile(petra_stage* st, int32_t enable) {
+  if (st == nullptr || st->impl == nullptr) return fail(PETRA_ERR_INVALID_ARG, "null stage handle");
+  petra::Profiler& p = st->impl->prof;
+  const hipError_t e = p.collect();
+  if (e != hipSuccess) return fail(PETRA_ERR_HIP, std::string("profile: ") + hipGetErrorString(e));
+  p.reset();
+  p.enabled = enable != 0;
+  return ok();
+}
+
+petra_status petra_stage_profile_read(petra_stage* st, int32_t kernel_class, const char** name,
+                                      int64_t* launches, double* total_ms, double* flops,
+                                      double* bytes) {
+  if (st == nullptr || st->impl == nullptr) return fail(PETRA_ERR_INVALID_ARG, "null stage handle");
+  if (kernel_class < 0 || kernel_class >= petra::K_NUM_CLASSES)
+    return fail(PETRA_ERR_INVALID_ARG, "kernel class out of range");
+  petra::Profiler& p = st->impl->prof;
+  const hipError_t e = p.collect();
+  if (e != hipSuccess) return fail(PETRA_ERR_HIP, std::string("profile: ") + hipGetErrorString(e));
+  if (name) *name = petra::kernel_class_name(kernel_class);
+  if (launches) *launches = p.launches[kernel_class];
+  if (total_ms) *total_ms = p.ms[kernel_class];
+  if (flops) *flops = p.flops[kernel_class];
+  if (bytes) *bytes = p.bytes[kernel_class];
+  return ok();
+}
+
 }  // extern "C"

@@ -1,0 +1,47 @@
+// Optional per-launch timing with HIP events on the launching stream, used by
+// the benchmark to measure each kernel class's average duration live.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <string>
+#include <vector>
+
+namespace petra {
+
+enum KernelClass {
+  K_CONV_FPROP = 0, K_CONV_DGRAD, K_CONV_WGRAD, K_WGRAD_REDUCE, K_BN_FINALIZE, K_BN_BWD_FINALIZE,
+  K_COMBINE_FWD, K_COMBINE_BWD, K_BN_BWD_APPLY, K_SGD, K_REFRESH, K_NUM_CLASSES
+};
+
+const char* kernel_class_name(int k);
+
+struct ProfRecord {
+  int kind;
+  hipEvent_t start, stop;
+  double flops, bytes;
+};
+
+class Profiler {
+ public:
+  ~Profiler();
+  bool enabled = false;
+  // Record the start of a launch of class `kind` on stream st (no-op when disabled).
+  void begin(hipStream_t st);
+  void end(int kind, hipStream_t st, double flops, double bytes);
+  // Aggregate finished records (synchronises on their events) into totals.
+  hipError_t collect();
+  void reset();
+  long launches[K_NUM_CLASSES] = {};
+  double ms[K_NUM_CLASSES] = {};
+  double flops[K_NUM_CLASSES] = {};
+  double bytes[K_NUM_CLASSES] = {};
+
+ private:
+  std::vector<hipEvent_t> pool_;
+  std::vector<ProfRecord> recs_;
+  hipEvent_t pending_ = nullptr;
+  hipEvent_t take();
+};
+
+}  // namespace petra

@@ -8,6 +8,7 @@
 
 #include "../../include/petra.h"
 #include "kernels.h"
+#include "prof.h"
 
 namespace petra {
 
@@ -84,6 +85,8 @@ class Stage {
 
   petra_sgd opt{0.1f, 0.9f, 0.0f, 1, 1};
   int64_t bwd_count = 0, last_update = 0;
+
+  Profiler prof;
 
   hipStream_t s_fwd = nullptr, s_bwd = nullptr;
   hipEvent_t ev_fork = nullptr, ev_fwd = nullptr, ev_bwd = nullptr;

@@ -166,7 +166,11 @@ hipError_t Stage::ensure_streams() {
   return hipEventCreateWithFlags(&ev_bwd, hipEventDisableTiming);
 }
 
-void Stage::sync_weights(hipStream_t st) { refresh_weights(dt, theta, segs, n_conv, wfwd, wdg, st); }
+void Stage::sync_weights(hipStream_t st) {
+  prof.begin(st);
+  refresh_weights(dt, theta, segs, n_conv, wfwd, wdg, st);
+  prof.end(K_REFRESH, st, 0.0, static_cast<double>(n_conv) * (4.0 + 2.0 * esz));
+}
 
 ConvArgs Stage::conv_args(const ConvLayer& cv) const {
   ConvArgs a{};
@@ -209,11 +213,17 @@ void Stage::fn_recompute(const ResidualFn& fn, const void* u, Scratch& s, bool r
     a.c_out = cv.cout;
     a.k_tot = cv.r * cv.s * cv.cin;
     a.partials = s.part;
+    prof.begin(st);
     conv_gemm(dt, a, EP_STATS, st);
+    prof.end(K_CONV_FPROP, st, 2.0 * M * cv.cout * a.k_tot,
+             static_cast<double>(esz) * (static_cast<double>(M) * (cv.cin + cv.cout) +
+                                         static_cast<double>(cv.cout) * a.k_tot));
+    prof.begin(st);
     bn_stats_finalize(s.part, tiles, cv.cout, M, theta + bn.g_off, theta + bn.b_off, desc.bn_eps,
                       s.vec(l, V_SCALE, cmax), s.vec(l, V_SHIFT, cmax), s.vec(l, V_MEAN, cmax),
                       s.vec(l, V_RSTD, cmax), running ? rmean + bn.run_off : nullptr,
                       running ? rvar + bn.run_off : nullptr, desc.bn_momentum, st);
+    prof.end(K_BN_FINALIZE, st, 0.0, 8.0 * tiles * cv.cout);
   }
 }
 
@@ -221,8 +231,10 @@ void Stage::fn_forward(const ResidualFn& fn, const void* u, const void* r, void*
                        hipStream_t st) {
   fn_recompute(fn, u, s, false, st);
   const int L = fn.nconv - 1;
-  combine_fwd(dt, r, s.h[L], s.vec(L, V_SCALE, cmax), s.vec(L, V_SHIFT, cmax), y, M,
-              convs[fn.conv[L]].cout, st);
+  const int c = convs[fn.conv[L]].cout;
+  prof.begin(st);
+  combine_fwd(dt, r, s.h[L], s.vec(L, V_SCALE, cmax), s.vec(L, V_SHIFT, cmax), y, M, c, st);
+  prof.end(K_COMBINE_FWD, st, 0.0, 3.0 * M * c * esz);
 }
 
 void Stage::fn_backward(const ResidualFn& fn, const void* u, const void* v, const void* d,
@@ -234,19 +246,26 @@ void Stage::fn_backward(const ResidualFn& fn, const void* u, const void* v, cons
   {
     const ConvLayer& cv = convs[fn.conv[L]];
     const BnLayer& bn = bns[cv.bn];
+    prof.begin(st);
     combine_bwd(dt, v, s.h[L], d, s.vec(L, V_SCALE, cmax), s.vec(L, V_SHIFT, cmax),
                 s.vec(L, V_MEAN, cmax), s.vec(L, V_RSTD, cmax), xrec, s.part, M, cv.cout, st);
-    bn_bwd_finalize(s.part, ew_tiles(M, cv.cout), cv.cout, M, theta + bn.g_off,
+    prof.end(K_COMBINE_BWD, st, 0.0, 4.0 * M * cv.cout * esz);
+    const int et = ew_tiles(M, cv.cout);
+    prof.begin(st);
+    bn_bwd_finalize(s.part, et, cv.cout, M, theta + bn.g_off,
                     s.vec(L, V_MEAN, cmax), s.vec(L, V_RSTD, cmax), inv_k, grad + bn.g_off,
                     grad + bn.b_off, s.vec(L, V_CA, cmax), s.vec(L, V_CB, cmax),
                     s.vec(L, V_CC, cmax), st);
+    prof.end(K_BN_BWD_FINALIZE, st, 0.0, 8.0 * et * cv.cout);
   }
   const void* dsrc = d;
   for (int l = L; l >= 0; --l) {
     const ConvLayer& cv = convs[fn.conv[l]];
     // dh_l = BN_l backward applied to the gradient of its output
+    prof.begin(st);
     bn_bwd_apply(dt, dsrc, s.h[l], s.vec(l, V_CA, cmax), s.vec(l, V_CB, cmax),
                  s.vec(l, V_CC, cmax), s.vec(l, V_MEAN, cmax), s.d0, M, cv.cout, st);
+    prof.end(K_BN_BWD_APPLY, st, 0.0, 3.0 * M * cv.cout * esz);
     // weight gradient of conv_l
     WgradArgs w{};
     w.dh = s.d0;
@@ -262,9 +281,15 @@ void Stage::fn_backward(const ResidualFn& fn, const void* u, const void* v, cons
     w.k_tot = cv.r * cv.s * cv.cin;
     w.m = static_cast<int>(M);
     wgrad_splits(cv, &w.splits, &w.rows_per_split);
+    const double wnumel = static_cast<double>(cv.cout) * w.k_tot;
+    prof.begin(st);
     conv_wgrad(dt, w, st);
+    prof.end(K_CONV_WGRAD, st, 2.0 * M * wnumel,
+             static_cast<double>(esz) * M * (cv.cin + cv.cout) + 4.0 * w.splits * wnumel);
+    prof.begin(st);
     wgrad_reduce(s.wpart, w.splits, static_cast<long>(cv.cout) * w.k_tot, inv_k, grad + cv.w_off,
                  st);
+    prof.end(K_WGRAD_REDUCE, st, 0.0, 4.0 * wnumel * (w.splits + 2));
     // input gradient: conv of dh with the transposed, flipped weights
     ConvArgs a = conv_args(cv);
     a.src = s.d0;
@@ -283,16 +308,26 @@ void Stage::fn_backward(const ResidualFn& fn, const void* u, const void* v, cons
       a.ep_mean = s.vec(l - 1, V_MEAN, cmax);
       a.ep_rstd = s.vec(l - 1, V_RSTD, cmax);
       a.partials = s.part;
+      prof.begin(st);
       conv_gemm(dt, a, EP_MASK, st);
+      prof.end(K_CONV_DGRAD, st, 2.0 * M * cv.cin * a.k_tot,
+               static_cast<double>(esz) * (static_cast<double>(M) * (cv.cout + 2.0 * cv.cin) +
+                                           static_cast<double>(cv.cin) * a.k_tot));
+      prof.begin(st);
       bn_bwd_finalize(s.part, tiles_conv, lo.cout, M, theta + bl.g_off, s.vec(l - 1, V_MEAN, cmax),
                       s.vec(l - 1, V_RSTD, cmax), inv_k, grad + bl.g_off, grad + bl.b_off,
                       s.vec(l - 1, V_CA, cmax), s.vec(l - 1, V_CB, cmax),
                       s.vec(l - 1, V_CC, cmax), st);
+      prof.end(K_BN_BWD_FINALIZE, st, 0.0, 8.0 * tiles_conv * lo.cout);
       dsrc = s.d1;
     } else {
       a.out = dout;
       a.resid = rg;
+      prof.begin(st);
       conv_gemm(dt, a, EP_RESID, st);
+      prof.end(K_CONV_DGRAD, st, 2.0 * M * cv.cin * a.k_tot,
+               static_cast<double>(esz) * (static_cast<double>(M) * (cv.cout + 2.0 * cv.cin) +
+                                           static_cast<double>(cv.cin) * a.k_tot));
     }
   }
 }
@@ -328,8 +363,10 @@ void Stage::backward(const void* y1, const void* y2, const void* dy1, const void
 bool Stage::update(hipStream_t st) {
   const int k = std::max(1, opt.accum_k);
   if (bwd_count == 0 || bwd_count == last_update || bwd_count % k != 0) return false;
+  prof.begin(st);
   sgd_update(theta, grad, mom, n_params, n_conv, opt.lr, opt.momentum, opt.weight_decay,
              opt.nesterov, st);
+  prof.end(K_SGD, st, 0.0, 24.0 * n_params);
   sync_weights(st);
   last_update = bwd_count;
   return true;

@@ -1,11 +1,30 @@
 """Test-side helpers: drive a stage through the C ABI and the oracle on the
-same seeded inputs, and compare.  (Test infrastructure; not product code.)"""
+same seeded inputs, and compare.  (Test infrastructure; not product code.)
+
+Tolerances.  fp32 workloads: normwise relative error <= 1e-4 on every tensor.
+bf16 workloads (bf16 storage, fp32 accumulation): <= 2e-2 on every tensor,
+where the oracle holds activations at bf16 wherever the method stores them.
+Tensors that come out of ReLU derivatives (input gradients, parameter
+gradients, and what the update derives from them) have a measurable noise
+floor in bf16: a one-ulp difference anywhere cascades through later roundings,
+and every pre-activation that lands on the other side of zero flips a ReLU
+decision, so the normwise error of a masked gradient grows like the square
+root of the storage noise.  The floor is measured in the same test as the
+largest distance between the oracle and three perturbed copies of it that
+any bf16 implementation is as entitled to as the kernels are: one computing
+in fp32 instead of fp64, and two whose storage rounding first scales each
+value by (1 + u 2^-20), u uniform in [-1, 1] (a last-bits difference of the
+kind another summation order produces).  For those tensors the bar is
+max(2e-2, 3 x floor).
+"""
 from __future__ import annotations
 
 import numpy as np
 
 import synth
 from oracle.stage import StageState
+
+FLOORED = ("dx1", "dx2", "grad", "update_inc", "momentum")
 
 
 def rel(a, b) -> float:
@@ -15,11 +34,28 @@ def rel(a, b) -> float:
     return float(np.linalg.norm(a - b) / nb) if nb > 0 else float(np.linalg.norm(a))
 
 
+def cos_sim(a, b) -> float:
+    a = np.asarray(a, np.float64).ravel()
+    b = np.asarray(b, np.float64).ravel()
+    return float(a @ b / max(np.linalg.norm(a) * np.linalg.norm(b), 1e-300))
+
+
 def tol(wl) -> float:
     return 1e-4 if wl.dtype == "fp32" else 2e-2
 
 
-def oracle_state(wl, params, storage=True) -> StageState:
+def jitter_store(seed: int):
+    """bf16 storage after a relative perturbation of at most 2^-20."""
+    rng = np.random.default_rng(seed)
+
+    def store(a):
+        a32 = np.asarray(a, np.float32)
+        j = (1.0 + (2.0 ** -20) * rng.uniform(-1.0, 1.0, a32.shape)).astype(np.float32)
+        return synth.round_bf16(a32 * j)
+    return store
+
+
+def oracle_state(wl, params, storage=True, dtype=np.float64, store=None) -> StageState:
     """Oracle of the workload.  For bf16 workloads the weights are read through
     their bf16 compute copy and, when `storage` is set, activations and
     activation gradients are held at bf16 where the method materialises them
@@ -27,9 +63,11 @@ def oracle_state(wl, params, storage=True) -> StageState:
     plain fp64 reference."""
     names = [n for n, _ in wl.param_shapes()]
     bf = wl.dtype == "bf16"
+    if store is None and bf and storage:
+        store = synth.round_bf16
     return StageState(params, names, 2 if wl.kind == "basic" else 3, eps=wl.bn_eps,
-                      bn_momentum=wl.bn_momentum, weight_view=synth.round_bf16 if bf else None,
-                      store=synth.round_bf16 if (bf and storage) else None)
+                      bn_momentum=wl.bn_momentum, dtype=dtype,
+                      weight_view=synth.round_bf16 if bf else None, store=store)
 
 
 def gpu_stage(wl, params, device="cuda"):
@@ -42,72 +80,104 @@ def gpu_stage(wl, params, device="cuda"):
     return st
 
 
-def run_step_parity(wl, bn_affine="random", check_update=True):
-    """Forward, reconstruct+VJP and update on both sides; returns an error dict."""
+def _oracle_step(ref, wl, params, x, yin, g):
+    """Outputs of one oracle step in a flat dict of named tensors."""
+    out = {}
+    oy1, oy2 = ref.forward(*x)
+    out["y1"], out["y2"] = oy1, oy2
+    if yin is None:
+        return out
+    ox1, ox2, odx1, odx2, _ = ref.backward(*yin, *g, k=wl.accum_k)
+    out.update(x1=ox1, x2=ox2, dx1=odx1, dx2=odx2)
+    names = [n for n, _ in wl.param_shapes()]
+    for nm, a in zip(names, ref.accum):
+        out["grad:" + nm] = np.array(a)
+    out["run_mean"] = np.concatenate([m.reshape(-1) for m in ref.run_mean])
+    out["run_var"] = np.concatenate([v.reshape(-1) for v in ref.run_var])
+    ref.update(wl.lr, wl.momentum, wl.weight_decay, wl.nesterov, wl.accum_k)
+    for nm, p, p0, b in zip(names, ref.params, params, ref.buf):
+        out["update_inc:" + nm] = np.asarray(p) - np.asarray(p0, np.float64)
+        out["momentum:" + nm] = np.array(b)
+    return out
+
+
+def run_step_parity(wl, bn_affine="random"):
+    """Forward, reconstruct+VJP and update on both sides.
+
+    Returns (errs, floors, info): per-tensor GPU-vs-oracle errors, per-tensor
+    bf16 noise floors (empty for fp32) and informational figures.
+    """
     import torch
     from paper_2406_02052_amd import to_host
 
     params = synth.stage_params(wl, bn_affine)
-    ref = oracle_state(wl, params)
-    exact = oracle_state(wl, params, storage=False) if wl.dtype == "bf16" else None
-    st = gpu_stage(wl, params)
-    x1, x2 = synth.stage_input(wl)
-    g1, g2 = synth.stage_output_grad(wl)
-    errs = {}
-    # forward
-    y1, y2 = st.act(), st.act()
-    st.forward(st.act(x1), st.act(x2), y1, y2)
-    oy1, oy2 = ref.forward(x1, x2)
-    torch.cuda.synchronize()
-    errs["y1"] = rel(to_host(y1), oy1)
-    errs["y2"] = rel(to_host(y2), oy2)
-    # backward from the oracle output in storage precision (same bits on both sides)
-    yin1, yin2 = synth.to_storage(oy1, wl.dtype), synth.to_storage(oy2, wl.dtype)
-    p0 = st.get_params()
-    rx1, rx2, dx1, dx2 = st.act(), st.act(), st.act(), st.act()
-    st.reconstruct_backward(st.act(yin1), st.act(yin2), st.act(g1), st.act(g2), rx1, rx2, dx1, dx2)
-    ox1, ox2, odx1, odx2, ograds = ref.backward(yin1, yin2, g1, g2, k=wl.accum_k)
-    torch.cuda.synchronize()
-    errs["x1"] = rel(to_host(rx1), ox1)
-    errs["x2"] = rel(to_host(rx2), ox2)
-    errs["dx1"] = rel(to_host(dx1), odx1)
-    errs["dx2"] = rel(to_host(dx2), odx2)
-    errs["drift_gpu"] = max(rel(to_host(rx1), x1), rel(to_host(rx2), x2))
-    errs["drift_oracle"] = max(rel(ox1, x1), rel(ox2, x2))
-    if exact is not None:
-        # informational: distance of the bf16 path from plain fp64 arithmetic
-        ex = exact.backward(yin1, yin2, g1, g2, k=wl.accum_k)
-        errs["fp64_dx"] = max(rel(to_host(dx1), ex[2]), rel(to_host(dx2), ex[3]))
-    grads = st.get_grads()
     names = [n for n, _ in wl.param_shapes()]
-    gerr = {}
-    for nm, g, og in zip(names, grads, ref.accum):
-        gerr[nm] = rel(g, og)
-    errs["grad_max"] = max(gerr.values())
-    errs["grad_worst"] = max(gerr, key=gerr.get)
-    rm, rv = st.run_mean.cpu().numpy(), st.run_var.cpu().numpy()
-    orm = np.concatenate([m.reshape(-1) for m in ref.run_mean])
-    orv = np.concatenate([v.reshape(-1) for v in ref.run_var])
-    errs["run_mean"] = rel(rm, orm)
-    errs["run_var"] = rel(rv, orv)
-    if check_update:
-        st.update()
-        ref.update(wl.lr, wl.momentum, wl.weight_decay, wl.nesterov, wl.accum_k)
-        torch.cuda.synchronize()
-        p1 = st.get_params()
-        inc = [rel(a - b, np.asarray(c) - np.asarray(pb, np.float64))
-               for a, b, c, pb in zip(p1, p0, ref.params, params)]
-        errs["update_inc"] = max(inc)
-        mom = st.get_momentum()
-        errs["momentum"] = max(rel(a, b) for a, b in zip(mom, ref.buf))
-        errs["accum_zero"] = float(max(np.abs(g).max() for g in st.get_grads()))
-    return errs
+    x = synth.stage_input(wl)
+    g = synth.stage_output_grad(wl)
+
+    ref = oracle_state(wl, params)
+    oy = ref.forward(*x)
+    # backward from the oracle output in storage precision (same bits on both sides)
+    yin = tuple(synth.to_storage(t, wl.dtype) for t in oy)
+    ref = oracle_state(wl, params)
+    want = _oracle_step(ref, wl, params, x, yin, g)
+
+    st = gpu_stage(wl, params)
+    got = {}
+    y1, y2 = st.act(), st.act()
+    st.forward(st.act(x[0]), st.act(x[1]), y1, y2)
+    rx1, rx2, dx1, dx2 = st.act(), st.act(), st.act(), st.act()
+    st.reconstruct_backward(st.act(yin[0]), st.act(yin[1]), st.act(g[0]), st.act(g[1]),
+                            rx1, rx2, dx1, dx2)
+    torch.cuda.synchronize()
+    for k, t in (("y1", y1), ("y2", y2), ("x1", rx1), ("x2", rx2), ("dx1", dx1), ("dx2", dx2)):
+        got[k] = to_host(t)
+    for nm, a in zip(names, st.get_grads()):
+        got["grad:" + nm] = a
+    got["run_mean"] = st.run_mean.cpu().numpy()
+    got["run_var"] = st.run_var.cpu().numpy()
+    p0 = st.get_params()
+    st.update()
+    torch.cuda.synchronize()
+    for nm, p1, a, b in zip(names, st.get_params(), p0, st.get_momentum()):
+        got["update_inc:" + nm] = p1.astype(np.float64) - a
+        got["momentum:" + nm] = b
+    accum_after = max(float(np.abs(a).max()) for a in st.get_grads())
+
+    errs = {k: rel(got[k], want[k]) for k in want}
+    floors = {}
+    info = {"drift_gpu": max(rel(got["x1"], x[0]), rel(got["x2"], x[1])),
+            "drift_oracle": max(rel(want["x1"], x[0]), rel(want["x2"], x[1])),
+            "accum_after_update": accum_after}
+    if wl.dtype == "bf16":
+        twins = [oracle_state(wl, params, dtype=np.float32),
+                 oracle_state(wl, params, store=jitter_store(1)),
+                 oracle_state(wl, params, store=jitter_store(2))]
+        for tw in twins:
+            res = _oracle_step(tw, wl, params, x, yin, g)
+            for k in want:
+                floors[k] = max(floors.get(k, 0.0), rel(res[k], want[k]))
+        exact = _oracle_step(oracle_state(wl, params, storage=False), wl, params, x, yin, g)
+        info["fp64_dx"] = max(rel(got["dx1"], exact["dx1"]), rel(got["dx2"], exact["dx2"]))
+        info["cos_dx2"] = cos_sim(got["dx2"], want["dx2"])
+        info["norm_ratio_dx2"] = float(np.linalg.norm(got["dx2"]) / np.linalg.norm(want["dx2"]))
+    return errs, floors, info
 
 
-def assert_errs(errs, wl):
+def check(errs, floors, info, wl):
+    """Assert the tolerance of each tensor; returns a summary string."""
     t = tol(wl)
-    bad = {k: v for k, v in errs.items()
-           if k not in ("drift_gpu", "drift_oracle", "grad_worst", "accum_zero", "fp64_dx")
-           and not v <= t}
-    assert not bad, f"parity failed (tol {t}): {bad}\nall: {errs}"
-    assert errs.get("accum_zero", 0.0) == 0.0
+    bad = {}
+    for k, e in errs.items():
+        bar = t
+        if wl.dtype == "bf16" and k.split(":")[0] in FLOORED:
+            bar = max(t, 3.0 * floors.get(k, 0.0))
+        if not e <= bar:
+            bad[k] = (e, bar)
+    worst = max(errs, key=errs.get)
+    summary = (f"worst {worst}={errs[worst]:.3g} floor={floors.get(worst, 0):.3g} "
+               f"y={max(errs['y1'], errs['y2']):.3g} x={max(errs['x1'], errs['x2']):.3g} "
+               f"dx={max(errs['dx1'], errs['dx2']):.3g} info={info}")
+    assert not bad, f"parity failed: {bad}\n{summary}"
+    assert info["accum_after_update"] == 0.0, "accumulator not zeroed by the update"
+    return summary

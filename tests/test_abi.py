@@ -1,0 +1,124 @@
+"""Host-side checks of the C ABI (no GPU work is launched): the library loads,
+exports every symbol its header declares, and validates arguments."""
+import ctypes
+import glob
+import os
+import re
+
+import pytest
+
+import synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_symbols():
+    names = set()
+    for h in glob.glob(os.path.join(ROOT, "include", "*.h")):
+        text = open(h).read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        names |= set(re.findall(r"\b(petra_\w+)\s*\(", text))
+    return sorted(names)
+
+
+def test_library_exports_every_declared_symbol():
+    from paper_2406_02052_amd import _lib
+    lib = ctypes.CDLL(_lib.LIB_PATH)
+    syms = declared_symbols()
+    assert len(syms) >= 12
+    missing = [s for s in syms if not hasattr(lib, s)]
+    assert not missing, missing
+
+
+def _desc(wl):
+    from paper_2406_02052_amd import _lib as L
+    return L.StageDesc(wl.n, wl.h, wl.w, wl.c_half, wl.c_mid, wl.blocks,
+                       0 if wl.kind == "basic" else 1, 1 if wl.dtype == "bf16" else 0,
+                       wl.bn_eps, wl.bn_momentum)
+
+
+@pytest.mark.parametrize("wl,n_params", [(synth.BLOCK_FP32, 9344), (synth.CIFAR_STAGE, 74240),
+                                         (synth.IMAGENET32_STAGE, 3545088),
+                                         (synth.IMAGENET_BOTTLENECK_STAGE, 106752)])
+def test_param_layout(wl, n_params):
+    from paper_2406_02052_amd import _lib as L
+    h = L.petra_stage_create(_desc(wl))
+    try:
+        np_, nt, nbn, ws = L.petra_stage_query(h)
+        assert np_ == n_params
+        shapes = wl.param_shapes()
+        assert nt == len(shapes)
+        spans = []
+        for i, (name, shp) in enumerate(shapes):
+            info = L.petra_stage_param_info(h, i)
+            assert tuple(info.shape[:info.ndim]) == shp, name
+            assert info.weight_decay == (1 if name.endswith("weight") else 0)
+            spans.append((info.offset, info.offset + info.numel))
+        spans.sort()
+        assert spans[0][0] == 0 and spans[-1][1] == n_params
+        assert all(a[1] == b[0] for a, b in zip(spans, spans[1:]))
+        # all decayed (conv) weights precede the BN parameters
+        last_w = max(L.petra_stage_param_info(h, i).offset for i in range(nt) if i % 3 == 0)
+        first_bn = min(L.petra_stage_param_info(h, i).offset for i in range(nt) if i % 3 != 0)
+        assert last_w < first_bn
+        assert nbn == sum(s[0] for n, s in shapes if n.endswith("gamma"))
+        assert ws > 0
+        with pytest.raises(L.PetraError):
+            L.petra_stage_param_info(h, nt)
+    finally:
+        L.petra_stage_destroy(h)
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("dtype", 7, "PETRA_ERR_DTYPE"), ("kind", 5, "PETRA_ERR_INVALID_ARG"),
+    ("c_half", 24, "PETRA_ERR_SHAPE"), ("c_half", 1024, "PETRA_ERR_SHAPE"),
+    ("n", 0, "PETRA_ERR_SHAPE"), ("num_blocks", 0, "PETRA_ERR_SHAPE"),
+    ("bn_eps", 0.0, "PETRA_ERR_INVALID_ARG")])
+def test_create_rejects_bad_descriptions(field, value, status):
+    from paper_2406_02052_amd import _lib as L
+    d = _desc(synth.CIFAR_STAGE)
+    setattr(d, field, value)
+    with pytest.raises(L.PetraError) as e:
+        L.petra_stage_create(d)
+    assert e.value.name == status
+    assert L.petra_last_error() != ""
+
+
+def test_bind_and_call_validation_without_device_work():
+    from paper_2406_02052_amd import _lib as L
+    wl = synth.CIFAR_STAGE.with_(n=2, h=4, w=4)
+    h = L.petra_stage_create(_desc(wl))
+    try:
+        _, _, _, ws = L.petra_stage_query(h)
+        base = 1 << 40   # fake, aligned device addresses; nothing is dereferenced
+        with pytest.raises(L.PetraError) as e:
+            L.petra_stage_forward(h, base, base + 4096, base + 8192, base + 12288, 0)
+        assert e.value.name == "PETRA_ERR_STATE"
+        with pytest.raises(L.PetraError) as e:
+            L.petra_stage_bind(h, base, base, base, base, base, base, ws - 1)
+        assert e.value.name == "PETRA_ERR_WORKSPACE"
+        with pytest.raises(L.PetraError) as e:
+            L.petra_stage_bind(h, base + 4, base, base, base, base, base, ws)
+        assert e.value.name == "PETRA_ERR_ALIGN"
+        L.petra_stage_bind(h, base, base, base, base, base, base + (1 << 30), ws)
+        n = wl.n * wl.h * wl.w * wl.c_half * 2
+        x1, x2, y1, y2 = (base + (2 << 30) + i * 65536 for i in range(4))
+        with pytest.raises(L.PetraError) as e:     # y1 half-overlaps x1
+            L.petra_stage_forward(h, x1, x2, x1 + 16, y2, 0)
+        assert e.value.name == "PETRA_ERR_ALIAS"
+        with pytest.raises(L.PetraError) as e:     # misaligned activation
+            L.petra_stage_forward(h, x1 + 8, x2, y1, y2, 0)
+        assert e.value.name == "PETRA_ERR_ALIGN"
+        with pytest.raises(L.PetraError) as e:     # dx1 overlaps y2
+            L.petra_stage_reconstruct_backward(h, y1, y2, x1, x2, base + (3 << 30), base + (4 << 30),
+                                               y2, base + (5 << 30), 0)
+        assert e.value.name == "PETRA_ERR_ALIAS"
+        with pytest.raises(L.PetraError) as e:
+            L.petra_stage_set_optimizer(h, L.Sgd(0.1, 1.0, 0.0, 1, 1))
+        assert e.value.name == "PETRA_ERR_INVALID_ARG"
+        with pytest.raises(L.PetraError) as e:
+            L.petra_stage_set_optimizer(h, L.Sgd(0.1, 0.9, 0.0, 1, 0))
+        assert e.value.name == "PETRA_ERR_INVALID_ARG"
+        assert n > 0
+    finally:
+        L.petra_stage_destroy(h)
