@@ -11,22 +11,33 @@ namespace petra {
 
 namespace {
 
-constexpr int FIN_TX = 32, FIN_TY = 16;
+constexpr int FIN_TX = 32, FIN_TY = 32;
 
 // Fixed-order reduction of partials[tile][which][c] over tiles, in fp64.
+// 32 channels x 32 row groups per block; each thread keeps four independent
+// accumulator pairs so that several loads are in flight.
 __device__ void reduce_partials(const float* partials, int tiles, int c, int ch, double& s1,
                                 double& s2) {
-  __shared__ double red[2][FIN_TY][FIN_TX];
+  __shared__ double red[2][FIN_TY][FIN_TX + 1];
   const int tx = threadIdx.x, ty = threadIdx.y;
-  double a = 0.0, b = 0.0;
+  double a[4] = {0.0, 0.0, 0.0, 0.0}, b[4] = {0.0, 0.0, 0.0, 0.0};
   if (ch < c) {
-    for (int t = ty; t < tiles; t += FIN_TY) {
-      a += partials[(static_cast<long>(t) * 2 + 0) * c + ch];
-      b += partials[(static_cast<long>(t) * 2 + 1) * c + ch];
+    int t = ty;
+    for (; t + 3 * FIN_TY < tiles; t += 4 * FIN_TY) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const long row = static_cast<long>(t + u * FIN_TY) * 2;
+        a[u] += partials[row * c + ch];
+        b[u] += partials[(row + 1) * c + ch];
+      }
+    }
+    for (; t < tiles; t += FIN_TY) {
+      a[0] += partials[(static_cast<long>(t) * 2) * c + ch];
+      b[0] += partials[(static_cast<long>(t) * 2 + 1) * c + ch];
     }
   }
-  red[0][ty][tx] = a;
-  red[1][ty][tx] = b;
+  red[0][ty][tx] = (a[0] + a[1]) + (a[2] + a[3]);
+  red[1][ty][tx] = (b[0] + b[1]) + (b[2] + b[3]);
   __syncthreads();
   s1 = s2 = 0.0;
   if (ty == 0) {

@@ -198,6 +198,514 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
   }
 }
 
+// Staged variant for bf16 with C_in a multiple of 32 (every stage conv of the
+// bf16 workloads).  Per 32-wide reduction step (one filter tap, 32 input
+// channels) all 256 threads gather the A tile (im2col rows, prologue applied)
+// and the B tile into registers one step ahead, park them in a double-buffered
+// LDS stage, and the 4 waves feed MFMA from LDS.  The epilogue goes through LDS
+// one 16-row slice per wave at a time so that every lane stores 16 contiguous
+// bytes of one output row.
+template <int BM, int BN, int WAVES_M, int EP, bool PRO>
+__global__ __launch_bounds__(256) void conv_staged_kernel(ConvArgs a) {
+  using T = bf16_t;
+  constexpr int WAVES_N = 4 / WAVES_M;
+  constexpr int TM = BM / WAVES_M, TN = BN / WAVES_N;
+  constexpr int FM = TM / 16, FN = TN / 16;
+  constexpr int PITCH = 40;                  // bf16 per LDS row: 32 k + 8 pad (80 B)
+  constexpr int A_CHUNKS = BM * 4 / 256;     // 16-byte A chunks per thread and step
+  constexpr int B_CHUNKS = (BN * 4 + 255) / 256;  // 16-byte B chunks per thread and step
+  constexpr int EPITCH = TN + 4;             // fp32 per LDS row of the epilogue slice
+  static_assert(BM * 4 % 256 == 0, "tile");
+  constexpr int STAGE_ELEMS = (BM + BN) * PITCH;
+  constexpr int EPI_FLOATS = 4 * 16 * EPITCH;
+  constexpr int LDS_BYTES = (2 * STAGE_ELEMS * 2 > EPI_FLOATS * 4) ? 2 * STAGE_ELEMS * 2 : EPI_FLOATS * 4;
+  __shared__ __attribute__((aligned(16))) unsigned char lds[LDS_BYTES];
+  __shared__ float pro_tab[2][512];
+  __shared__ float red[WAVES_M][2][BN];
+
+  T* stage_base = reinterpret_cast<T*>(lds);
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wm = wave % WAVES_M, wn = wave / WAVES_M;
+  const int lr = lane & 15, lg = lane >> 4;
+  const int m0 = blockIdx.x * BM;
+  const int n0 = blockIdx.y * BN;
+  const int pq = a.p * a.q;
+  const int csteps = a.c_in / 32;
+  const int steps = a.r * a.s * csteps;
+
+  if constexpr (PRO) {
+    for (int i = tid; i < a.c_in; i += 256) {
+      pro_tab[0][i] = a.pro_scale[i];
+      pro_tab[1][i] = a.pro_shift[i];
+    }
+  }
+
+  // Fixed per-thread load roles.
+  int a_row[A_CHUNKS], a_sub[A_CHUNKS], a_ih0[A_CHUNKS], a_iw0[A_CHUNKS];
+  long a_pix0[A_CHUNKS];
+  bool a_ok[A_CHUNKS];
+#pragma unroll
+  for (int i = 0; i < A_CHUNKS; ++i) {
+    const int q = tid + 256 * i;
+    a_row[i] = q >> 2;
+    a_sub[i] = q & 3;
+    const int m = m0 + a_row[i];
+    a_ok[i] = m < a.m;
+    const int mm = a_ok[i] ? m : 0;
+    const int n = mm / pq;
+    const int rem = mm - n * pq;
+    const int pp = rem / a.q;
+    const int qq = rem - pp * a.q;
+    a_ih0[i] = pp * a.stride - a.pad;
+    a_iw0[i] = qq * a.stride - a.pad;
+    a_pix0[i] = static_cast<long>(n) * a.h * a.w;
+  }
+  int b_col[B_CHUNKS], b_sub[B_CHUNKS];
+  bool b_in[B_CHUNKS], b_ok[B_CHUNKS];
+#pragma unroll
+  for (int i = 0; i < B_CHUNKS; ++i) {
+    const int q = tid + 256 * i;
+    b_col[i] = q >> 2;
+    b_sub[i] = q & 3;
+    b_in[i] = q < BN * 4;
+    b_ok[i] = b_in[i] && (n0 + b_col[i]) < a.c_out;
+  }
+  const T* wt = static_cast<const T*>(a.wt);
+  const T* src = static_cast<const T*>(a.src);
+  if constexpr (PRO) __syncthreads();
+
+  Raw8<T> ra[A_CHUNKS], rb[B_CHUNKS];
+  auto load_step = [&](int step) {
+    const int tap = step / csteps;
+    const int c0 = (step - tap * csteps) * 32;
+    const int fr = tap / a.s, fs = tap - fr * a.s;
+#pragma unroll
+    for (int i = 0; i < A_CHUNKS; ++i) {
+      const int ih = a_ih0[i] + fr, iw = a_iw0[i] + fs;
+      const int c = c0 + a_sub[i] * 8;
+      if (a_ok[i] && ih >= 0 && ih < a.h && iw >= 0 && iw < a.w) {
+        ra[i].load(src + (a_pix0[i] + static_cast<long>(ih) * a.w + iw) * a.c_in + c);
+        if constexpr (PRO) {
+          float v[8];
+          ra[i].to_f32(v);
+#pragma unroll
+          for (int j = 0; j < 8; ++j) v[j] = fmaxf(fmaf(pro_tab[0][c + j], v[j], pro_tab[1][c + j]), 0.f);
+          ra[i].from_f32(v);
+        }
+      } else {
+        ra[i].zero();
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < B_CHUNKS; ++i) {
+      if (b_ok[i])
+        rb[i].load(wt + static_cast<long>(n0 + b_col[i]) * a.k_tot + tap * a.c_in + c0 + b_sub[i] * 8);
+      else
+        rb[i].zero();
+    }
+  };
+  auto park = [&](int buf) {
+    T* sA = stage_base + buf * STAGE_ELEMS;
+    T* sB = sA + BM * PITCH;
+#pragma unroll
+    for (int i = 0; i < A_CHUNKS; ++i)
+      *reinterpret_cast<uint4*>(sA + a_row[i] * PITCH + a_sub[i] * 8) =
+          make_uint4(ra[i].w[0], ra[i].w[1], ra[i].w[2], ra[i].w[3]);
+#pragma unroll
+    for (int i = 0; i < B_CHUNKS; ++i)
+      if (b_in[i])
+        *reinterpret_cast<uint4*>(sB + b_col[i] * PITCH + b_sub[i] * 8) =
+            make_uint4(rb[i].w[0], rb[i].w[1], rb[i].w[2], rb[i].w[3]);
+  };
+
+  f32x4_t acc[FM][FN];
+#pragma unroll
+  for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  load_step(0);
+  park(0);
+  __syncthreads();
+  for (int step = 0; step < steps; ++step) {
+    const int buf = step & 1;
+    if (step + 1 < steps) load_step(step + 1);
+    const T* sA = stage_base + buf * STAGE_ELEMS;
+    const T* sB = sA + BM * PITCH;
+    Frag<T> af[FM], bfr[FN];
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm) af[fm].load(sA + (wm * TM + fm * 16 + lr) * PITCH + lg * 8);
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn) bfr[fn].load(sB + (wn * TN + fn * 16 + lr) * PITCH + lg * 8);
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+      for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma(af[fm], bfr[fn], acc[fm][fn]);
+    if (step + 1 < steps) park(buf ^ 1);
+    __syncthreads();
+  }
+
+  // Epilogue: per 16-row slice, stage fp32 results of each wave in LDS, then
+  // each lane handles 8 consecutive columns of one row.
+  float* ep = reinterpret_cast<float*>(lds) + wave * 16 * EPITCH;
+  constexpr int CG = TN / 8;                  // column groups per slice row
+  constexpr int TASKS = 16 * CG;              // (row, group) tasks per slice
+  const int my_cg = lane % CG;
+  const int col = n0 + wn * TN + my_cg * 8;
+  const bool cvalid = col < a.c_out;
+  float s1[8], s2[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) s1[j] = s2[j] = 0.f;
+  float es[8], esh[8], emu[8], ers[8];
+  if constexpr (EP == EP_MASK) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      es[j] = cvalid ? a.ep_scale[col + j] : 0.f;
+      esh[j] = cvalid ? a.ep_shift[col + j] : 0.f;
+      emu[j] = cvalid ? a.ep_mean[col + j] : 0.f;
+      ers[j] = cvalid ? a.ep_rstd[col + j] : 0.f;
+    }
+  }
+  T* out = static_cast<T*>(a.out);
+#pragma unroll
+  for (int fm = 0; fm < FM; ++fm) {
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) ep[(lg * 4 + j) * EPITCH + fn * 16 + lr] = acc[fm][fn][j];
+    __syncthreads();
+    for (int t = lane; t < TASKS; t += 64) {
+      const int rr = t / CG;
+      const int row = m0 + wm * TM + fm * 16 + rr;
+      if (!(cvalid && row < a.m)) continue;
+      float v[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[j] = ep[rr * EPITCH + my_cg * 8 + j];
+      const long idx = static_cast<long>(row) * a.c_out + col;
+      Raw8<T> o;
+      if constexpr (EP == EP_STATS) {
+        o.from_f32(v);
+        o.to_f32(v);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          s1[j] += v[j];
+          s2[j] += v[j] * v[j];
+        }
+      } else if constexpr (EP == EP_MASK) {
+        Raw8<T> hr;
+        hr.load(static_cast<const T*>(a.ep_h) + idx);
+        float hl[8];
+        hr.to_f32(hl);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = fmaf(es[j], hl[j], esh[j]) > 0.f ? v[j] : 0.f;
+        o.from_f32(v);
+        o.to_f32(v);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          s1[j] += v[j];
+          s2[j] += v[j] * ((hl[j] - emu[j]) * ers[j]);
+        }
+      } else {
+        Raw8<T> rr8;
+        rr8.load(static_cast<const T*>(a.resid) + idx);
+        float rv[8];
+        rr8.to_f32(rv);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] += rv[j];
+        o.from_f32(v);
+      }
+      *reinterpret_cast<uint4*>(out + idx) = make_uint4(o.w[0], o.w[1], o.w[2], o.w[3]);
+    }
+    __syncthreads();
+  }
+  if constexpr (EP == EP_STATS || EP == EP_MASK) {
+    // lanes with the same column group: lane % CG equal -> xor over the higher lane bits
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      for (int off = CG; off < 64; off <<= 1) {
+        s1[j] += __shfl_xor(s1[j], off, 64);
+        s2[j] += __shfl_xor(s2[j], off, 64);
+      }
+    }
+    if (lane < CG) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        red[wm][0][wn * TN + lane * 8 + j] = s1[j];
+        red[wm][1][wn * TN + lane * 8 + j] = s2[j];
+      }
+    }
+    __syncthreads();
+    for (int i = tid; i < 2 * BN; i += 256) {
+      const int which = i / BN, cl = i - which * BN;
+      const int c = n0 + cl;
+      if (c >= a.c_out) continue;
+      float t = 0.f;
+#pragma unroll
+      for (int w = 0; w < WAVES_M; ++w) t += red[w][which][cl];
+      a.partials[(static_cast<long>(blockIdx.x) * 2 + which) * a.c_out + c] = t;
+    }
+  }
+}
+
+// Halo-tile variant for 3x3 / stride 1 / pad 1 bf16 convolutions with C_in a
+// multiple of 32.  A workgroup owns a TH x TW patch of output pixels of one
+// image; per 32-channel chunk it loads the (TH+2) x (TW+2) input patch once into
+// LDS (BN-apply + ReLU prologue applied there, once per element, zero padding
+// kept zero) and runs the 9 taps from LDS by shifting the pixel index, while the
+// 32-channel weight slab of each (chunk, tap) step streams through a double
+// buffer.  The next chunk's patch and the next slab are fetched into registers
+// one step ahead.  HB = number of patch buffers (1 when there is one chunk).
+template <int TH, int TW, int BN, int WAVES_M, int HB, int EP, bool PRO>
+__global__ __launch_bounds__(256) void conv_halo_kernel(ConvArgs a) {
+  using T = bf16_t;
+  constexpr int BM = TH * TW;
+  constexpr int WAVES_N = 4 / WAVES_M;
+  constexpr int TM = BM / WAVES_M, TN = BN / WAVES_N;
+  constexpr int FM = TM / 16, FN = TN / 16;
+  static_assert(TM % 16 == 0 && TN % 16 == 0, "tile");
+  constexpr int HTH = TH + 2, HTW = TW + 2, HPIX = HTH * HTW;
+  constexpr int HP = 40;                              // bf16 per patch pixel (32 + pad)
+  constexpr int H_CHUNKS = (HPIX * 4 + 255) / 256;    // 16-byte patch chunks per thread
+  constexpr int B_CHUNKS = (BN * 4 + 255) / 256;
+  constexpr int BPITCH = 40;
+  constexpr int PATCH = HPIX * HP;
+  constexpr int SLAB = BN * BPITCH;
+  constexpr int EPITCH = TN + 4;
+  constexpr int MAIN_BYTES = (HB * PATCH + 2 * SLAB) * 2;
+  constexpr int EPI_BYTES = 4 * 16 * EPITCH * 4;
+  constexpr int LDS_BYTES = MAIN_BYTES > EPI_BYTES ? MAIN_BYTES : EPI_BYTES;
+  __shared__ __attribute__((aligned(16))) unsigned char lds[LDS_BYTES];
+  __shared__ float pro_tab[2][512];
+  __shared__ float red[WAVES_M][2][BN];
+
+  T* patch_base = reinterpret_cast<T*>(lds);
+  T* slab_base = patch_base + HB * PATCH;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wm = wave % WAVES_M, wn = wave / WAVES_M;
+  const int lr = lane & 15, lg = lane >> 4;
+  const int tiles_x = (a.w + TW - 1) / TW, tiles_y = (a.h + TH - 1) / TH;
+  const int tx = blockIdx.x % tiles_x;
+  const int ty = (blockIdx.x / tiles_x) % tiles_y;
+  const int img = blockIdx.x / (tiles_x * tiles_y);
+  const int p0 = ty * TH, q0 = tx * TW;
+  const int n0 = blockIdx.y * BN;
+  const int chunks = a.c_in / 32;
+  const int steps = chunks * 9;
+  const T* src = static_cast<const T*>(a.src);
+  const T* wt = static_cast<const T*>(a.wt);
+  const long img_base = static_cast<long>(img) * a.h * a.w;
+
+  if constexpr (PRO) {
+    for (int i = tid; i < a.c_in; i += 256) {
+      pro_tab[0][i] = a.pro_scale[i];
+      pro_tab[1][i] = a.pro_shift[i];
+    }
+    __syncthreads();
+  }
+
+  Raw8<T> rh[H_CHUNKS], rb[B_CHUNKS];
+  auto load_patch = [&](int chunk) {
+    const int c0 = chunk * 32;
+#pragma unroll
+    for (int i = 0; i < H_CHUNKS; ++i) {
+      const int q = tid + 256 * i;
+      const int hp = q >> 2, sub = q & 3;
+      const int hy = hp / HTW, hx = hp - hy * HTW;
+      const int ih = p0 - 1 + hy, iw = q0 - 1 + hx;
+      if (hp < HPIX && ih >= 0 && ih < a.h && iw >= 0 && iw < a.w) {
+        const int c = c0 + sub * 8;
+        rh[i].load(src + (img_base + static_cast<long>(ih) * a.w + iw) * a.c_in + c);
+        if constexpr (PRO) {
+          float v[8];
+          rh[i].to_f32(v);
+#pragma unroll
+          for (int j = 0; j < 8; ++j) v[j] = fmaxf(fmaf(pro_tab[0][c + j], v[j], pro_tab[1][c + j]), 0.f);
+          rh[i].from_f32(v);
+        }
+      } else {
+        rh[i].zero();
+      }
+    }
+  };
+  auto park_patch = [&](int buf) {
+    T* dst = patch_base + buf * PATCH;
+#pragma unroll
+    for (int i = 0; i < H_CHUNKS; ++i) {
+      const int q = tid + 256 * i;
+      const int hp = q >> 2, sub = q & 3;
+      if (hp < HPIX)
+        *reinterpret_cast<uint4*>(dst + hp * HP + sub * 8) = make_uint4(rh[i].w[0], rh[i].w[1], rh[i].w[2], rh[i].w[3]);
+    }
+  };
+  auto load_slab = [&](int step) {
+    const int chunk = step / 9, tap = step - chunk * 9;
+#pragma unroll
+    for (int i = 0; i < B_CHUNKS; ++i) {
+      const int q = tid + 256 * i;
+      const int col = q >> 2, sub = q & 3;
+      if (q < BN * 4 && n0 + col < a.c_out)
+        rb[i].load(wt + static_cast<long>(n0 + col) * a.k_tot + tap * a.c_in + chunk * 32 + sub * 8);
+      else
+        rb[i].zero();
+    }
+  };
+  auto park_slab = [&](int buf) {
+    T* dst = slab_base + buf * SLAB;
+#pragma unroll
+    for (int i = 0; i < B_CHUNKS; ++i) {
+      const int q = tid + 256 * i;
+      if (q < BN * 4)
+        *reinterpret_cast<uint4*>(dst + (q >> 2) * BPITCH + (q & 3) * 8) = make_uint4(rb[i].w[0], rb[i].w[1], rb[i].w[2], rb[i].w[3]);
+    }
+  };
+
+  // Patch-pixel offset of each MFMA row this lane feeds (tap (0,0)).
+  int rowpix[FM];
+#pragma unroll
+  for (int fm = 0; fm < FM; ++fm) {
+    const int i = wm * TM + fm * 16 + lr;
+    const int ph = i / TW, pw = i - ph * TW;
+    rowpix[fm] = ph * HTW + pw;
+  }
+
+  f32x4_t acc[FM][FN];
+#pragma unroll
+  for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  load_patch(0);
+  load_slab(0);
+  park_patch(0);
+  park_slab(0);
+  __syncthreads();
+  for (int step = 0; step < steps; ++step) {
+    const int chunk = step / 9, tap = step - chunk * 9;
+    const bool next_patch = HB > 1 && tap == 0 && chunk + 1 < chunks;
+    if (step + 1 < steps) load_slab(step + 1);
+    if (next_patch) load_patch(chunk + 1);
+    const T* pt = patch_base + (HB > 1 ? (chunk & 1) : 0) * PATCH;
+    const T* sb = slab_base + (step & 1) * SLAB;
+    const int fr = tap / 3, fs = tap - fr * 3;
+    const int toff = fr * HTW + fs;
+    Frag<T> af[FM], bfr[FN];
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm) af[fm].load(pt + (rowpix[fm] + toff) * HP + lg * 8);
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn) bfr[fn].load(sb + (wn * TN + fn * 16 + lr) * BPITCH + lg * 8);
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+      for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma(af[fm], bfr[fn], acc[fm][fn]);
+    if (step + 1 < steps) park_slab((step + 1) & 1);
+    if (next_patch) park_patch((chunk + 1) & 1);
+    __syncthreads();
+  }
+
+  // Epilogue (as in the staged kernel, pixels mapped back to NHWC rows).
+  float* ep = reinterpret_cast<float*>(lds) + wave * 16 * EPITCH;
+  constexpr int CG = TN / 8;
+  constexpr int TASKS = 16 * CG;
+  const int my_cg = lane % CG;
+  const int col = n0 + wn * TN + my_cg * 8;
+  const bool cvalid = col < a.c_out;
+  float s1[8], s2[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) s1[j] = s2[j] = 0.f;
+  float es[8], esh[8], emu[8], ers[8];
+  if constexpr (EP == EP_MASK) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      es[j] = cvalid ? a.ep_scale[col + j] : 0.f;
+      esh[j] = cvalid ? a.ep_shift[col + j] : 0.f;
+      emu[j] = cvalid ? a.ep_mean[col + j] : 0.f;
+      ers[j] = cvalid ? a.ep_rstd[col + j] : 0.f;
+    }
+  }
+  T* out = static_cast<T*>(a.out);
+#pragma unroll
+  for (int fm = 0; fm < FM; ++fm) {
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) ep[(lg * 4 + j) * EPITCH + fn * 16 + lr] = acc[fm][fn][j];
+    __syncthreads();
+    for (int t = lane; t < TASKS; t += 64) {
+      const int rr = t / CG;
+      const int i = wm * TM + fm * 16 + rr;
+      const int ph = i / TW, pw = i - ph * TW;
+      const int pp = p0 + ph, qq = q0 + pw;
+      if (!(cvalid && pp < a.h && qq < a.w)) continue;
+      float v[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[j] = ep[rr * EPITCH + my_cg * 8 + j];
+      const long idx = (img_base + static_cast<long>(pp) * a.w + qq) * a.c_out + col;
+      Raw8<T> o;
+      if constexpr (EP == EP_STATS) {
+        o.from_f32(v);
+        o.to_f32(v);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          s1[j] += v[j];
+          s2[j] += v[j] * v[j];
+        }
+      } else if constexpr (EP == EP_MASK) {
+        Raw8<T> hr;
+        hr.load(static_cast<const T*>(a.ep_h) + idx);
+        float hl[8];
+        hr.to_f32(hl);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = fmaf(es[j], hl[j], esh[j]) > 0.f ? v[j] : 0.f;
+        o.from_f32(v);
+        o.to_f32(v);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          s1[j] += v[j];
+          s2[j] += v[j] * ((hl[j] - emu[j]) * ers[j]);
+        }
+      } else {
+        Raw8<T> rr8;
+        rr8.load(static_cast<const T*>(a.resid) + idx);
+        float rv[8];
+        rr8.to_f32(rv);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] += rv[j];
+        o.from_f32(v);
+      }
+      *reinterpret_cast<uint4*>(out + idx) = make_uint4(o.w[0], o.w[1], o.w[2], o.w[3]);
+    }
+    __syncthreads();
+  }
+  if constexpr (EP == EP_STATS || EP == EP_MASK) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      for (int off = CG; off < 64; off <<= 1) {
+        s1[j] += __shfl_xor(s1[j], off, 64);
+        s2[j] += __shfl_xor(s2[j], off, 64);
+      }
+    }
+    if (lane < CG) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        red[wm][0][wn * TN + lane * 8 + j] = s1[j];
+        red[wm][1][wn * TN + lane * 8 + j] = s2[j];
+      }
+    }
+    __syncthreads();
+    for (int i = tid; i < 2 * BN; i += 256) {
+      const int which = i / BN, cl = i - which * BN;
+      const int c = n0 + cl;
+      if (c >= a.c_out) continue;
+      float t = 0.f;
+#pragma unroll
+      for (int w = 0; w < WAVES_M; ++w) t += red[w][which][cl];
+      a.partials[(static_cast<long>(blockIdx.x) * 2 + which) * a.c_out + c] = t;
+    }
+  }
+}
+
 // Weight gradient partials over one chunk of rows:
 //   part[split][o][k] = sum_{m in chunk} dh[m][o] * A[m][k]
 // BO x BK output tile, 4 waves in a 2 x 2 grid; rows advance 32 at a time.
@@ -295,15 +803,322 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a) {
       }
 }
 
-// grad[o*K + k] += inv_k * sum_split part[split][o][k]   (fixed split order)
+// bf16 weight gradient, 64 rows per step: register prefetch one step ahead,
+// double-buffered LDS, and each thread transposes a pair of rows into 32-bit
+// LDS words (two consecutive m of one channel), so both operands become
+// m-contiguous rows that feed MFMA directly.
+template <int BO, int BK, bool PRO>
+__global__ __launch_bounds__(256) void wgrad_staged_kernel(WgradArgs a) {
+  using T = bf16_t;
+  constexpr int RS = 64;                    // rows (m) per step
+  constexpr int PITCH = RS + 8;             // bf16 per LDS row (144 B)
+  constexpr int FO = BO / 32, FK = BK / 32;
+  constexpr int A_TASKS = 32 * (BO / 8);    // (row pair, 8-channel group) tasks of dh
+  constexpr int B_TASKS = 32 * (BK / 8);    // (row pair, 8-column group) tasks of the input
+  static_assert(A_TASKS <= 256 && B_TASKS <= 256, "tile");
+  constexpr int BUF = (BO + BK) * PITCH;
+  __shared__ __attribute__((aligned(16))) T lds[2 * BUF];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wo = wave & 1, wk = wave >> 1;
+  const int lr = lane & 15, lg = lane >> 4;
+  const int k0 = blockIdx.x * BK, o0 = blockIdx.y * BO;
+  const int m_begin = blockIdx.z * a.rows_per_split;
+  const int m_end = min(a.m, m_begin + a.rows_per_split);
+  const int steps = (m_end - m_begin + RS - 1) / RS;
+  const int pq = a.p * a.q;
+  const T* dh = static_cast<const T*>(a.dh);
+
+  const bool a_on = tid < A_TASKS;
+  const int a_pair = tid / (BO / 8), a_og = tid % (BO / 8);
+  const int a_o = o0 + a_og * 8;
+  const bool a_ook = a_on && a_o < a.c_out;
+  const bool b_on = tid < B_TASKS;
+  const int b_pair = tid / (BK / 8), b_kg = tid % (BK / 8);
+  const int kb = k0 + b_kg * 8;
+  const bool kb_ok = b_on && kb < a.k_tot;
+  const int kbb = kb_ok ? kb : 0;
+  const int tap = kbb / a.c_in;
+  const int cb = kbb - tap * a.c_in;
+  const int fr = tap / a.s, fs = tap - fr * a.s;
+
+  ConvArgs ca;
+  ca.src = a.src; ca.src2 = a.src2; ca.c_split = a.c_split;
+  ca.pro_scale = a.pro_scale; ca.pro_shift = a.pro_shift;
+  ca.h = a.h; ca.w = a.w; ca.c_in = a.c_in; ca.stride = a.stride; ca.pad = a.pad;
+
+  Raw8<T> ra[2], rb[2];
+  auto load_step = [&](int step) {
+    const int mb = m_begin + step * RS;
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      const int m = mb + 2 * a_pair + e;
+      if (a_ook && m < m_end) ra[e].load(dh + static_cast<long>(m) * a.c_out + a_o);
+      else ra[e].zero();
+      const int mm = mb + 2 * b_pair + e;
+      RowPos rp;
+      rp.valid = b_on && mm < m_end;
+      const int m2 = rp.valid ? mm : 0;
+      rp.n = m2 / pq;
+      const int rem = m2 - rp.n * pq;
+      rp.p = rem / a.q;
+      rp.q = rem - rp.p * a.q;
+      gather_a<T, PRO>(ca, rp, kb_ok, fr, fs, cb, rb[e]);
+    }
+  };
+  auto pair_word = [](const Raw8<T>& lo, const Raw8<T>& hi, int j) -> uint32_t {
+    const uint32_t a0 = lo.w[j >> 1], b0 = hi.w[j >> 1];
+    return (j & 1) ? ((a0 >> 16) | (b0 & 0xffff0000u)) : ((a0 & 0xffffu) | (b0 << 16));
+  };
+  auto park = [&](int buf) {
+    T* sA = lds + buf * BUF;
+    T* sB = sA + BO * PITCH;
+    if (a_on) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        *reinterpret_cast<uint32_t*>(sA + (a_og * 8 + j) * PITCH + 2 * a_pair) = pair_word(ra[0], ra[1], j);
+    }
+    if (b_on) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        *reinterpret_cast<uint32_t*>(sB + (b_kg * 8 + j) * PITCH + 2 * b_pair) = pair_word(rb[0], rb[1], j);
+    }
+  };
+
+  f32x4_t acc[FO][FK];
+#pragma unroll
+  for (int i = 0; i < FO; ++i)
+#pragma unroll
+    for (int j = 0; j < FK; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  if (steps > 0) {
+    load_step(0);
+    park(0);
+  }
+  __syncthreads();
+  for (int step = 0; step < steps; ++step) {
+    const int buf = step & 1;
+    if (step + 1 < steps) load_step(step + 1);
+    const T* sA = lds + buf * BUF;
+    const T* sB = sA + BO * PITCH;
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      Frag<T> fa[FO], fb[FK];
+#pragma unroll
+      for (int i = 0; i < FO; ++i) fa[i].load(sA + (wo * (BO / 2) + i * 16 + lr) * PITCH + kk * 32 + lg * 8);
+#pragma unroll
+      for (int j = 0; j < FK; ++j) fb[j].load(sB + (wk * (BK / 2) + j * 16 + lr) * PITCH + kk * 32 + lg * 8);
+#pragma unroll
+      for (int i = 0; i < FO; ++i)
+#pragma unroll
+        for (int j = 0; j < FK; ++j) acc[i][j] = mfma(fa[i], fb[j], acc[i][j]);
+    }
+    if (step + 1 < steps) park(buf ^ 1);
+    __syncthreads();
+  }
+
+  float* part = a.partials + static_cast<long>(blockIdx.z) * a.c_out * a.k_tot;
+#pragma unroll
+  for (int i = 0; i < FO; ++i)
+#pragma unroll
+    for (int j = 0; j < FK; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int o = o0 + wo * (BO / 2) + i * 16 + lg * 4 + e;
+        const int k = k0 + wk * (BK / 2) + j * 16 + lr;
+        if (o < a.c_out && k < a.k_tot) part[static_cast<long>(o) * a.k_tot + k] = acc[i][j][e];
+      }
+}
+
+// Halo-tile weight gradient for 3x3 / stride 1 / pad 1 bf16 convolutions with
+// C_in a multiple of 32:
+//   part[split][o][(tap, c)] = sum over the split's pixels of dh[pix][o] * x[pix + tap][c]
+// A workgroup owns one output-channel tile (BO), one 32-channel input chunk
+// and a strided set of TH x TW pixel tiles.  Per pixel tile it stores dh
+// transposed ([o][pixel]) and the (TH+2)-row input patch transposed three
+// times, pre-shifted by 0, 1 and 2 columns ([c][row][col + s]), so that the
+// MFMA operands of every tap are 16-byte aligned LDS rows.  The BN-apply +
+// ReLU prologue runs once per patch element.  The next tile is fetched into
+// registers while the current one is multiplied; the 9 taps accumulate in
+// registers across all tiles of the split.
+template <int TH, int TW, int BO, bool PRO>
+__global__ __launch_bounds__(256) void wgrad_halo_kernel(WgradArgs a) {
+  using T = bf16_t;
+  constexpr int NPIX = TH * TW;
+  static_assert(NPIX % 32 == 0 && TW % 8 == 0, "tile");
+  constexpr int HTH = TH + 2, HTW = TW + 2, HPIX = HTH * HTW;
+  constexpr int HROW = HTH * TW + 8;        // bf16 per channel row of one shifted copy
+  constexpr int DROW = NPIX + 8;            // bf16 per output-channel row of dh^T
+  constexpr int OT = BO / 16;               // output-channel MFMA tiles
+  constexpr int WPO = 4 / OT;               // waves per output-channel tile
+  constexpr int NP = 18 / WPO;              // (tap, 16-channel half) pairs per wave
+  static_assert(OT * WPO == 4 && NP * WPO == 18, "waves");
+  constexpr int H_CHUNKS = (HPIX * 4 + 255) / 256;
+  constexpr int D_CHUNKS = (NPIX * (BO / 8) + 255) / 256;
+  __shared__ __attribute__((aligned(16))) T sh[3 * 32 * HROW];
+  __shared__ __attribute__((aligned(16))) T sd[BO * DROW];
+  __shared__ float pro_tab[2][32];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int lr = lane & 15, lg = lane >> 4;
+  const int ot = wave % OT, part = wave / OT;
+  const int o0 = blockIdx.y * BO;
+  const int chunk = blockIdx.z;
+  const int c0 = chunk * 32;
+  const int tiles_x = (a.w + TW - 1) / TW, tiles_y = (a.h + TH - 1) / TH;
+  const int ntiles = tiles_x * tiles_y * a.n;
+  const T* src = static_cast<const T*>(a.src);
+  const T* dh = static_cast<const T*>(a.dh);
+
+  if constexpr (PRO) {
+    if (tid < 32) {
+      pro_tab[0][tid] = a.pro_scale[c0 + tid];
+      pro_tab[1][tid] = a.pro_shift[c0 + tid];
+    }
+    __syncthreads();
+  }
+
+  Raw8<T> rh[H_CHUNKS], rd[D_CHUNKS];
+  auto tile_origin = [&](int t, int& img, int& p0, int& q0) {
+    const int tx = t % tiles_x;
+    const int ty = (t / tiles_x) % tiles_y;
+    img = t / (tiles_x * tiles_y);
+    p0 = ty * TH;
+    q0 = tx * TW;
+  };
+  auto load_tile = [&](int t) {
+    int img, p0, q0;
+    tile_origin(t, img, p0, q0);
+    const long base = static_cast<long>(img) * a.h * a.w;
+#pragma unroll
+    for (int i = 0; i < H_CHUNKS; ++i) {
+      const int q = tid + 256 * i;
+      const int hp = q >> 2, sub = q & 3;
+      const int hy = hp / HTW, hx = hp - hy * HTW;
+      const int ih = p0 - 1 + hy, iw = q0 - 1 + hx;
+      if (hp < HPIX && ih >= 0 && ih < a.h && iw >= 0 && iw < a.w) {
+        rh[i].load(src + (base + static_cast<long>(ih) * a.w + iw) * a.c_in + c0 + sub * 8);
+        if constexpr (PRO) {
+          float v[8];
+          rh[i].to_f32(v);
+#pragma unroll
+          for (int j = 0; j < 8; ++j)
+            v[j] = fmaxf(fmaf(pro_tab[0][sub * 8 + j], v[j], pro_tab[1][sub * 8 + j]), 0.f);
+          rh[i].from_f32(v);
+        }
+      } else {
+        rh[i].zero();
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < D_CHUNKS; ++i) {
+      const int q = tid + 256 * i;
+      const int pix = q / (BO / 8), og = q % (BO / 8);
+      const int ph = pix / TW, pw = pix - ph * TW;
+      const int pp = p0 + ph, qq = q0 + pw;
+      if (pix < NPIX && pp < a.h && qq < a.w && o0 + og * 8 < a.c_out)
+        rd[i].load(dh + (base + static_cast<long>(pp) * a.w + qq) * a.c_out + o0 + og * 8);
+      else
+        rd[i].zero();
+    }
+  };
+  auto park_tile = [&]() {
+#pragma unroll
+    for (int i = 0; i < H_CHUNKS; ++i) {
+      const int q = tid + 256 * i;
+      const int hp = q >> 2, sub = q & 3;
+      if (hp >= HPIX) continue;
+      const int hy = hp / HTW, hx = hp - hy * HTW;
+#pragma unroll
+      for (int sft = 0; sft < 3; ++sft) {
+        const int col = hx - sft;
+        if (col < 0 || col >= TW) continue;
+        T* dst = sh + sft * 32 * HROW + hy * TW + col;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) rh[i].put(j, dst + (sub * 8 + j) * HROW);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < D_CHUNKS; ++i) {
+      const int q = tid + 256 * i;
+      const int pix = q / (BO / 8), og = q % (BO / 8);
+      if (pix >= NPIX) continue;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) rd[i].put(j, sd + (og * 8 + j) * DROW + pix);
+    }
+  };
+
+  f32x4_t acc[NP];
+#pragma unroll
+  for (int i = 0; i < NP; ++i) acc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  int t = blockIdx.x;
+  if (t < ntiles) load_tile(t);
+  for (; t < ntiles; t += gridDim.x) {
+    __syncthreads();            // previous tile's operands fully consumed
+    park_tile();
+    __syncthreads();
+    if (t + static_cast<int>(gridDim.x) < ntiles) load_tile(t + gridDim.x);
+#pragma unroll
+    for (int g = 0; g < NPIX / 32; ++g) {
+      const int pix = g * 32 + lg * 8;
+      const int ph = pix / TW, pw = pix - ph * TW;
+      Frag<T> fa;
+      fa.load(sd + (ot * 16 + lr) * DROW + pix);
+#pragma unroll
+      for (int pi = 0; pi < NP; ++pi) {
+        const int pr = part + pi * WPO;          // 0..17
+        const int tap = pr >> 1, half = pr & 1;
+        const int fr = tap / 3, fs = tap - fr * 3;
+        Frag<T> fb;
+        fb.load(sh + fs * 32 * HROW + (half * 16 + lr) * HROW + (ph + fr) * TW + pw);
+        acc[pi] = mfma(fa, fb, acc[pi]);
+      }
+    }
+  }
+
+  float* outp = a.partials + static_cast<long>(blockIdx.x) * a.c_out * a.k_tot;
+#pragma unroll
+  for (int pi = 0; pi < NP; ++pi) {
+    const int pr = part + pi * WPO;
+    const int tap = pr >> 1, half = pr & 1;
+    const int k = tap * a.c_in + c0 + half * 16 + lr;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int o = o0 + ot * 16 + lg * 4 + e;
+      if (o < a.c_out) outp[static_cast<long>(o) * a.k_tot + k] = acc[pi][e];
+    }
+  }
+}
+
+// grad[o*K + k] += inv_k * sum_split part[split][o][k]   (fixed order)
+// A block owns 32 consecutive elements; its 8 thread rows take interleaved
+// split ranges, and the 8 row sums are combined in a fixed order.
 __global__ __launch_bounds__(256) void wgrad_reduce_kernel(const float* __restrict__ part, int splits,
                                                            long numel, float inv_k,
                                                            float* __restrict__ grad) {
-  const long i = static_cast<long>(blockIdx.x) * 256 + threadIdx.x;
-  if (i >= numel) return;
-  float s = 0.f;
-  for (int t = 0; t < splits; ++t) s += part[static_cast<long>(t) * numel + i];
-  grad[i] += inv_k * s;
+  __shared__ float red[8][33];
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  const long i = static_cast<long>(blockIdx.x) * 32 + tx;
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};
+  if (i < numel) {
+    int t = ty;
+    for (; t + 24 < splits; t += 32) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) acc[u] += part[static_cast<long>(t + 8 * u) * numel + i];
+    }
+    for (; t < splits; t += 8) acc[0] += part[static_cast<long>(t) * numel + i];
+  }
+  red[ty][tx] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+  __syncthreads();
+  if (ty == 0 && i < numel) {
+    float s = 0.f;
+#pragma unroll
+    for (int r = 0; r < 8; ++r) s += red[r][tx];
+    grad[i] += inv_k * s;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -331,6 +1146,79 @@ void launch_gemm_tiles(const ConvArgs& a, hipStream_t st) {
     launch_gemm<T, 128, 2, EP, PRO>(a, st);
 }
 
+template <int BM, int BN, int WM, int EP, bool PRO>
+void launch_staged(const ConvArgs& a, hipStream_t st) {
+  dim3 grid((a.m + BM - 1) / BM, (a.c_out + BN - 1) / BN);
+  hipLaunchKernelGGL((conv_staged_kernel<BM, BN, WM, EP, PRO>), grid, dim3(256), 0, st, a);
+}
+
+template <int EP, bool PRO>
+void launch_staged_tiles(const ConvArgs& a, hipStream_t st) {
+  if (a.c_out <= 32)
+    launch_staged<256, 32, 4, EP, PRO>(a, st);
+  else if (a.c_out <= 64)
+    launch_staged<128, 64, 2, EP, PRO>(a, st);
+  else
+    launch_staged<128, 128, 2, EP, PRO>(a, st);
+}
+
+// Halo-tile geometry for a 3x3 stride-1 bf16 conv, or tw = 0 when it does not apply.
+struct HaloShape { int th, tw, bn, wm, hb; };
+
+HaloShape halo_shape(int dtype, const ConvArgs& a) {
+  HaloShape z{0, 0, 0, 0, 0};
+  if (!(dtype == DT_BF16 && a.src2 == nullptr && a.r == 3 && a.s == 3 && a.stride == 1 &&
+        a.pad == 1 && a.c_in % 32 == 0 && a.c_in <= 512 && a.c_out % 8 == 0 && a.p == a.h &&
+        a.q == a.w))
+    return z;
+  const int hb = a.c_in > 32 ? 2 : 1;
+  if (a.w == 32 && a.c_out <= 32) return HaloShape{8, 32, 32, 4, hb};
+  if (a.w == 16 && a.c_out <= 64) return HaloShape{8, 16, 64, 2, hb};
+  if (a.w == 16) return HaloShape{8, 16, 128, 2, hb};
+  if (a.w == 56 && a.c_out <= 32 && a.c_in == 32) return HaloShape{4, 56, 32, 2, 1};
+  return z;
+}
+
+template <int TH, int TW, int BN, int WM, int HB>
+void launch_halo(const ConvArgs& a, int ep, hipStream_t st) {
+  const int tiles = ((a.w + TW - 1) / TW) * ((a.h + TH - 1) / TH) * a.n;
+  dim3 grid(tiles, (a.c_out + BN - 1) / BN);
+  const bool pro = a.pro_scale != nullptr;
+  if (ep == EP_STATS) {
+    if (pro)
+      hipLaunchKernelGGL((conv_halo_kernel<TH, TW, BN, WM, HB, EP_STATS, true>), grid, dim3(256), 0, st, a);
+    else
+      hipLaunchKernelGGL((conv_halo_kernel<TH, TW, BN, WM, HB, EP_STATS, false>), grid, dim3(256), 0, st, a);
+  } else if (ep == EP_MASK) {
+    hipLaunchKernelGGL((conv_halo_kernel<TH, TW, BN, WM, HB, EP_MASK, false>), grid, dim3(256), 0, st, a);
+  } else {
+    hipLaunchKernelGGL((conv_halo_kernel<TH, TW, BN, WM, HB, EP_RESID, false>), grid, dim3(256), 0, st, a);
+  }
+}
+
+bool launch_halo_any(int dtype, const ConvArgs& a, int ep, hipStream_t st) {
+  const HaloShape h = halo_shape(dtype, a);
+  if (h.tw == 0) return false;
+  if (h.tw == 32) {
+    if (h.hb == 1) launch_halo<8, 32, 32, 4, 1>(a, ep, st);
+    else launch_halo<8, 32, 32, 4, 2>(a, ep, st);
+  } else if (h.tw == 16 && h.bn == 64) {
+    if (h.hb == 1) launch_halo<8, 16, 64, 2, 1>(a, ep, st);
+    else launch_halo<8, 16, 64, 2, 2>(a, ep, st);
+  } else if (h.tw == 16) {
+    if (h.hb == 1) launch_halo<8, 16, 128, 2, 1>(a, ep, st);
+    else launch_halo<8, 16, 128, 2, 2>(a, ep, st);
+  } else {
+    launch_halo<4, 56, 32, 2, 1>(a, ep, st);
+  }
+  return true;
+}
+
+bool use_staged(int dtype, const ConvArgs& a) {
+  return dtype == DT_BF16 && a.src2 == nullptr && a.c_in % 32 == 0 && a.c_out % 8 == 0 &&
+         a.c_in <= 512 && a.c_out >= 16;
+}
+
 template <typename T>
 void conv_gemm_t(const ConvArgs& a, int ep, hipStream_t st) {
   const bool pro = a.pro_scale != nullptr;
@@ -353,8 +1241,57 @@ void launch_wgrad_bk(const WgradArgs& a, hipStream_t st) {
     hipLaunchKernelGGL((wgrad_kernel<T, BO, BK, false>), grid, dim3(256), 0, st, a);
 }
 
+}  // namespace
+
+// 0: no halo kernel; 1: 4x32 tiles, 32 output channels per group; 2: 8x16 tiles, 64.
+int wgrad_halo_shape(int dtype, const WgradArgs& a) {
+  if (!(dtype == DT_BF16 && a.src2 == nullptr && a.r == 3 && a.s == 3 && a.stride == 1 &&
+        a.pad == 1 && a.c_in % 32 == 0 && a.c_out % 8 == 0 && a.p == a.h && a.q == a.w))
+    return 0;
+  if (a.w == 32 && a.c_out <= 32) return 1;
+  if (a.w == 16 && a.c_out % 64 == 0) return 2;
+  return 0;
+}
+
+int wgrad_halo_tiles(int dtype, const WgradArgs& a) {
+  const int shape = wgrad_halo_shape(dtype, a);
+  if (shape == 1) return ((a.w + 31) / 32) * ((a.h + 3) / 4) * a.n;
+  if (shape == 2) return ((a.w + 15) / 16) * ((a.h + 7) / 8) * a.n;
+  return 0;
+}
+
+namespace {
+
+template <int BO, int BK>
+void launch_wgrad_staged(const WgradArgs& a, hipStream_t st) {
+  dim3 grid((a.k_tot + BK - 1) / BK, (a.c_out + BO - 1) / BO, a.splits);
+  if (a.pro_scale != nullptr)
+    hipLaunchKernelGGL((wgrad_staged_kernel<BO, BK, true>), grid, dim3(256), 0, st, a);
+  else
+    hipLaunchKernelGGL((wgrad_staged_kernel<BO, BK, false>), grid, dim3(256), 0, st, a);
+}
+
+template <int TH, int TW, int BO>
+void launch_wgrad_halo(const WgradArgs& a, hipStream_t st) {
+  dim3 grid(a.splits, (a.c_out + BO - 1) / BO, a.c_in / 32);
+  if (a.pro_scale != nullptr)
+    hipLaunchKernelGGL((wgrad_halo_kernel<TH, TW, BO, true>), grid, dim3(256), 0, st, a);
+  else
+    hipLaunchKernelGGL((wgrad_halo_kernel<TH, TW, BO, false>), grid, dim3(256), 0, st, a);
+}
+
 template <typename T>
 void wgrad_t(const WgradArgs& a, hipStream_t st) {
+  if constexpr (sizeof(T) == 2) {
+    const int shape = wgrad_halo_shape(DT_BF16, a);
+    if (shape == 1) { launch_wgrad_halo<4, 32, 32>(a, st); return; }
+    if (shape == 2) { launch_wgrad_halo<8, 16, 64>(a, st); return; }
+    if (a.c_out <= 32)
+      launch_wgrad_staged<32, 64>(a, st);
+    else
+      launch_wgrad_staged<64, 64>(a, st);
+    return;
+  }
   if (a.c_out <= 32)
     launch_wgrad_bk<T, 32, 64>(a, st);
   else
@@ -363,7 +1300,28 @@ void wgrad_t(const WgradArgs& a, hipStream_t st) {
 
 }  // namespace
 
+int conv_row_tiles(int dtype, const ConvArgs& a) {
+  const HaloShape hs = halo_shape(dtype, a);
+  if (hs.tw != 0) return ((a.w + hs.tw - 1) / hs.tw) * ((a.h + hs.th - 1) / hs.th) * a.n;
+  int bm = CONV_BM;
+  if (use_staged(dtype, a)) bm = a.c_out <= 32 ? 256 : 128;
+  return (a.m + bm - 1) / bm;
+}
+
 void conv_gemm(int dtype, const ConvArgs& a, int ep, hipStream_t st) {
+  if (launch_halo_any(dtype, a, ep, st)) return;
+  if (use_staged(dtype, a)) {
+    const bool pro = a.pro_scale != nullptr;
+    if (ep == EP_STATS) {
+      if (pro) launch_staged_tiles<EP_STATS, true>(a, st);
+      else launch_staged_tiles<EP_STATS, false>(a, st);
+    } else if (ep == EP_MASK) {
+      launch_staged_tiles<EP_MASK, false>(a, st);
+    } else {
+      launch_staged_tiles<EP_RESID, false>(a, st);
+    }
+    return;
+  }
   if (dtype == DT_BF16)
     conv_gemm_t<bf16_t>(a, ep, st);
   else
@@ -379,7 +1337,7 @@ void conv_wgrad(int dtype, const WgradArgs& a, hipStream_t st) {
 
 void wgrad_reduce(const float* part, int splits, long numel, float inv_k, float* grad,
                   hipStream_t st) {
-  const long blocks = (numel + 255) / 256;
+  const long blocks = (numel + 31) / 32;
   hipLaunchKernelGGL(wgrad_reduce_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, st,
                      part, splits, numel, inv_k, grad);
 }

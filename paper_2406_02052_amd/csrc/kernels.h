@@ -44,7 +44,13 @@ struct WgradArgs {
 constexpr int CONV_BM = 128;  // rows per conv output tile (= partial-sum tile)
 
 void conv_gemm(int dtype, const ConvArgs& a, int ep, hipStream_t st);
+// Number of partial-sum rows (output row tiles) conv_gemm writes for these arguments.
+int conv_row_tiles(int dtype, const ConvArgs& a);
 void conv_wgrad(int dtype, const WgradArgs& a, hipStream_t st);
+// Halo-tile weight-gradient kernel selection (0 = not applicable) and the
+// number of pixel tiles it splits over.
+int wgrad_halo_shape(int dtype, const WgradArgs& a);
+int wgrad_halo_tiles(int dtype, const WgradArgs& a);
 void wgrad_reduce(const float* part, int splits, long numel, float inv_k, float* grad,
                   hipStream_t st);
 

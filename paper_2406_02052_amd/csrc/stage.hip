@@ -99,9 +99,16 @@ Stage::Stage(const petra_stage_desc& d) : desc(d) {
   }
 
   // Workspace plan.
-  const int tiles_conv = static_cast<int>((M + CONV_BM - 1) / CONV_BM);
-  int tiles_max = tiles_conv;
+  int tiles_max = 1;
   for (auto& s : fn_shapes) tiles_max = std::max(tiles_max, ew_tiles(M, s.cout));
+  for (const ConvLayer& cv : convs) {
+    ConvArgs f = conv_args(cv);
+    f.c_in = cv.cin; f.c_out = cv.cout; f.k_tot = cv.r * cv.s * cv.cin;
+    tiles_max = std::max(tiles_max, conv_row_tiles(dt, f));
+    ConvArgs g = conv_args(cv);
+    g.c_in = cv.cout; g.c_out = cv.cin; g.k_tot = cv.r * cv.s * cv.cout;
+    tiles_max = std::max(tiles_max, conv_row_tiles(dt, g));
+  }
   int64_t wmax = 0;
   for (auto& cv : convs) {
     int sp, rps;
@@ -182,12 +189,27 @@ ConvArgs Stage::conv_args(const ConvLayer& cv) const {
 }
 
 void Stage::wgrad_splits(const ConvLayer& cv, int* splits, int* rows_per_split) const {
+  WgradArgs w{};
+  w.n = desc.n; w.h = desc.h; w.w = desc.w; w.p = desc.h; w.q = desc.w;
+  w.c_in = cv.cin; w.c_out = cv.cout; w.r = cv.r; w.s = cv.s; w.stride = 1; w.pad = cv.pad;
+  w.k_tot = cv.r * cv.s * cv.cin; w.m = static_cast<int>(M);
+  const int hshape = wgrad_halo_shape(dt, w);
+  if (hshape != 0) {
+    // pixel tiles strided over `splits` workgroups per (output tile, channel chunk)
+    const int ntiles = wgrad_halo_tiles(dt, w);
+    const int bo = hshape == 1 ? 32 : 64;
+    const int per_split = ((cv.cout + bo - 1) / bo) * (cv.cin / 32);
+    *splits = std::max(1, std::min(ntiles, 512 / std::max(1, per_split)));
+    *rows_per_split = 0;
+    return;
+  }
+  // About two workgroups per CU in total, each over at least 512 rows.
   const int ktot = cv.r * cv.s * cv.cin;
   const int bo = cv.cout <= 32 ? 32 : 64;
   const int tiles = ((ktot + 63) / 64) * ((cv.cout + bo - 1) / bo);
-  int sp = std::max(1, 1024 / std::max(1, tiles));
+  int sp = std::max(1, 512 / std::max(1, tiles));
   long rps = (M + sp - 1) / sp;
-  rps = std::max<long>(rps, 256);
+  rps = std::max<long>(rps, 512);
   rps = (rps + 31) / 32 * 32;
   sp = static_cast<int>((M + rps - 1) / rps);
   *splits = sp;
@@ -196,7 +218,6 @@ void Stage::wgrad_splits(const ConvLayer& cv, int* splits, int* rows_per_split) 
 
 void Stage::fn_recompute(const ResidualFn& fn, const void* u, Scratch& s, bool running,
                          hipStream_t st) {
-  const int tiles = static_cast<int>((M + CONV_BM - 1) / CONV_BM);
   for (int l = 0; l < fn.nconv; ++l) {
     const ConvLayer& cv = convs[fn.conv[l]];
     const BnLayer& bn = bns[cv.bn];
@@ -213,6 +234,7 @@ void Stage::fn_recompute(const ResidualFn& fn, const void* u, Scratch& s, bool r
     a.c_out = cv.cout;
     a.k_tot = cv.r * cv.s * cv.cin;
     a.partials = s.part;
+    const int tiles = conv_row_tiles(dt, a);
     prof.begin(st);
     conv_gemm(dt, a, EP_STATS, st);
     prof.end(K_CONV_FPROP, st, 2.0 * M * cv.cout * a.k_tot,
@@ -240,7 +262,6 @@ void Stage::fn_forward(const ResidualFn& fn, const void* u, const void* r, void*
 void Stage::fn_backward(const ResidualFn& fn, const void* u, const void* v, const void* d,
                         const void* rg, void* xrec, void* dout, Scratch& s, hipStream_t st) {
   const float inv_k = 1.0f / static_cast<float>(std::max(1, opt.accum_k));
-  const int tiles_conv = static_cast<int>((M + CONV_BM - 1) / CONV_BM);
   fn_recompute(fn, u, s, true, st);
   const int L = fn.nconv - 1;
   {
@@ -308,6 +329,7 @@ void Stage::fn_backward(const ResidualFn& fn, const void* u, const void* v, cons
       a.ep_mean = s.vec(l - 1, V_MEAN, cmax);
       a.ep_rstd = s.vec(l - 1, V_RSTD, cmax);
       a.partials = s.part;
+      const int tiles_conv = conv_row_tiles(dt, a);
       prof.begin(st);
       conv_gemm(dt, a, EP_MASK, st);
       prof.end(K_CONV_DGRAD, st, 2.0 * M * cv.cin * a.k_tot,

@@ -25,6 +25,11 @@ SMALL = {
     "bf16_c128_3x6x6": synth.IMAGENET32_STAGE.with_(n=3, h=6, w=6, blocks=2),
     "bf16_bottleneck_2x12x12": synth.IMAGENET_BOTTLENECK_STAGE.with_(n=2, h=12, w=12, blocks=2),
     "bf16_c256_2x4x4": synth.IMAGENET32_STAGE.with_(n=2, h=4, w=4, c_half=256, blocks=1),
+    # halo-tile conv shapes (image widths 32 / 16 / 56), with ragged row tiles
+    "bf16_halo_c32_2x5x32": synth.CIFAR_STAGE.with_(n=2, h=5, w=32),
+    "bf16_halo_c64_2x9x16": synth.CIFAR_STAGE.with_(n=2, h=9, w=16, c_half=64, blocks=1),
+    "bf16_halo_c128_1x9x16": synth.IMAGENET32_STAGE.with_(n=1, h=9, w=16, blocks=2),
+    "bf16_halo_bottleneck_1x5x56": synth.IMAGENET_BOTTLENECK_STAGE.with_(n=1, h=5, w=56, blocks=1),
 }
 
 
