@@ -75,8 +75,8 @@ typedef enum {
  * BN runs in training mode with batch statistics over N*H*W (eps bn_eps);
  * running statistics use momentum bn_momentum and move only during the
  * backward recompute (Sec. 4.1, "Model adaptations").
- * Limits: c_half and c_mid multiples of 16 (bf16) or 8 (fp32), at most 512;
- * N*H*W < 2^31 / c_half. */
+ * Limits: c_half and c_mid are 8 times a power of two, at most 512;
+ * N*H*W*max(c_half, c_mid) < 2^31. */
 typedef struct {
   int32_t n, h, w;
   int32_t c_half;
@@ -146,6 +146,13 @@ petra_status petra_stage_bind(petra_stage* st, float* params, float* grad_accum,
  * scale of petra_stage_reconstruct_backward(). */
 petra_status petra_stage_set_optimizer(petra_stage* st, const petra_sgd* opt);
 
+/* Graph replay (default on): each distinct call (kind of call and the device
+ * pointers passed) is captured once into a HIP graph and replayed on a private
+ * stream ordered with events after prior work on the caller's stream and
+ * before later work on it; set_optimizer() drops the cached graphs.
+ * enable = 0 launches every kernel directly on the caller's stream. */
+petra_status petra_stage_set_graphs(petra_stage* st, int32_t enable);
+
 /* Refresh the storage-type compute copies of the conv weights from the fp32
  * master (needed once after the caller writes params directly). */
 petra_status petra_stage_sync_weights(petra_stage* st, void* stream);
@@ -170,10 +177,11 @@ petra_status petra_stage_reconstruct_backward(petra_stage* st, const void* y1, c
                                               const void* dy1, const void* dy2, void* x1,
                                               void* x2, void* dx1, void* dx2, void* stream);
 
-/* Parameter update (Eq. 5, last line; Alg. 1): counts one backward step and,
- * when the count is a multiple of accum_k, applies the optimizer to params
- * from grad_accum, zeroes grad_accum and refreshes the compute copies.
- * *updated (nullable) receives 1 if the update ran. */
+/* Parameter update (Eq. 5, last line; Alg. 1): when the number of backward
+ * calls so far is a multiple of accum_k (and no update has run since the last
+ * backward), applies the optimizer to params from grad_accum, zeroes
+ * grad_accum and refreshes the compute copies.  *updated (nullable) receives
+ * 1 if the update ran. */
 petra_status petra_stage_update(petra_stage* st, void* stream, int32_t* updated);
 
 /* One PETRA stage step (Eq. 5): the forward of one micro-batch (x -> y) and

@@ -64,6 +64,7 @@ _SIGS = {
     "petra_stage_bind": (ctypes.c_int, [_VP, _VP, _VP, _VP, _VP, _VP, _VP, ctypes.c_size_t]),
     "petra_stage_set_optimizer": (ctypes.c_int, [_VP, ctypes.POINTER(Sgd)]),
     "petra_stage_sync_weights": (ctypes.c_int, [_VP, _VP]),
+    "petra_stage_set_graphs": (ctypes.c_int, [_VP, ctypes.c_int32]),
     "petra_stage_forward": (ctypes.c_int, [_VP, _VP, _VP, _VP, _VP, _VP]),
     "petra_stage_reconstruct_backward": (ctypes.c_int, [_VP] * 10),
     "petra_stage_update": (ctypes.c_int, [_VP, _VP, ctypes.POINTER(ctypes.c_int32)]),
@@ -166,6 +167,10 @@ def petra_stage_bind(handle, params, grad_accum, momentum, run_mean, run_var, wo
 
 def petra_stage_set_optimizer(handle: int, opt: Sgd) -> None:
     _check(load().petra_stage_set_optimizer(handle, ctypes.byref(opt)), "petra_stage_set_optimizer")
+
+
+def petra_stage_set_graphs(handle: int, enable: bool) -> None:
+    _check(load().petra_stage_set_graphs(handle, 1 if enable else 0), "petra_stage_set_graphs")
 
 
 def petra_stage_sync_weights(handle: int, stream=None) -> None:

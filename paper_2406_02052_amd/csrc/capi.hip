@@ -2,6 +2,7 @@
 // and dispatch to the stage program.  Nothing here allocates device memory.
 #include <cstdint>
 #include <cstdio>
+#include <functional>
 #include <new>
 #include <string>
 
@@ -97,6 +98,23 @@ petra_status check_bwd(const petra::Stage& s, const void* y1, const void* y2, co
     }
   return PETRA_OK;
 }
+
+enum CallKind : uintptr_t { CALL_FWD = 1, CALL_BWD, CALL_UPD, CALL_STEP, CALL_SYNC };
+
+// Enqueue `work` on `stream`, through the stage's graph cache unless graphs are
+// off or per-launch profiling is active.
+petra_status launch(petra::Stage& s, const petra::GraphCache::Key& key, hipStream_t stream,
+                    const char* where, const std::function<void(hipStream_t)>& work) {
+  if (s.use_graphs && !s.prof.enabled) {
+    const hipError_t e = s.graphs.run(key, stream, work);
+    if (e != hipSuccess) return fail(PETRA_ERR_HIP, std::string(where) + ": " + hipGetErrorString(e));
+    return check_hip(where);
+  }
+  work(stream);
+  return check_hip(where);
+}
+
+uintptr_t P(const void* p) { return reinterpret_cast<uintptr_t>(p); }
 
 }  // namespace
 
@@ -205,15 +223,24 @@ petra_status petra_stage_set_optimizer(petra_stage* st, const petra_sgd* opt) {
       !(opt->weight_decay >= 0.f) || opt->accum_k < 1)
     return fail(PETRA_ERR_INVALID_ARG, "need lr >= 0, 0 <= momentum < 1, weight_decay >= 0, accum_k >= 1");
   st->impl->opt = *opt;
+  st->impl->graphs.clear();  // cached graphs carry the old settings in their arguments
+  return ok();
+}
+
+petra_status petra_stage_set_graphs(petra_stage* st, int32_t enable) {
+  if (st == nullptr || st->impl == nullptr) return fail(PETRA_ERR_INVALID_ARG, "null stage handle");
+  st->impl->use_graphs = enable != 0;
+  st->impl->graphs.clear();
   return ok();
 }
 
 petra_status petra_stage_sync_weights(petra_stage* st, void* stream) {
   petra_status r = check_ready(st);
   if (r) return r;
-  (void)hipGetLastError();
-  st->impl->sync_weights(static_cast<hipStream_t>(stream));
-  return check_hip("petra_stage_sync_weights");
+  if ((r = check_hip("before petra_stage_sync_weights"))) return r;
+  petra::Stage& s = *st->impl;
+  return launch(s, {CALL_SYNC}, static_cast<hipStream_t>(stream), "petra_stage_sync_weights",
+                [&](hipStream_t q) { s.sync_weights(q); });
 }
 
 petra_status petra_stage_forward(petra_stage* st, const void* x1, const void* x2, void* y1,
@@ -222,8 +249,9 @@ petra_status petra_stage_forward(petra_stage* st, const void* x1, const void* x2
   if (r) return r;
   if ((r = check_fwd(*st->impl, x1, x2, y1, y2))) return r;
   if ((r = check_hip("before petra_stage_forward"))) return r;
-  st->impl->forward(x1, x2, y1, y2, static_cast<hipStream_t>(stream));
-  return check_hip("petra_stage_forward");
+  petra::Stage& s = *st->impl;
+  return launch(s, {CALL_FWD, P(x1), P(x2), P(y1), P(y2)}, static_cast<hipStream_t>(stream),
+                "petra_stage_forward", [&](hipStream_t q) { s.forward(x1, x2, y1, y2, q); });
 }
 
 petra_status petra_stage_reconstruct_backward(petra_stage* st, const void* y1, const void* y2,
@@ -233,17 +261,28 @@ petra_status petra_stage_reconstruct_backward(petra_stage* st, const void* y1, c
   if (r) return r;
   if ((r = check_bwd(*st->impl, y1, y2, dy1, dy2, x1, x2, dx1, dx2))) return r;
   if ((r = check_hip("before petra_stage_reconstruct_backward"))) return r;
-  st->impl->backward(y1, y2, dy1, dy2, x1, x2, dx1, dx2, static_cast<hipStream_t>(stream));
-  return check_hip("petra_stage_reconstruct_backward");
+  petra::Stage& s = *st->impl;
+  const hipError_t se = s.ensure_streams();
+  if (se != hipSuccess) return fail(PETRA_ERR_HIP, std::string("stream setup: ") + hipGetErrorString(se));
+  r = launch(s, {CALL_BWD, P(y1), P(y2), P(dy1), P(dy2), P(x1), P(x2), P(dx1), P(dx2)},
+             static_cast<hipStream_t>(stream), "petra_stage_reconstruct_backward",
+             [&](hipStream_t q) { s.backward(y1, y2, dy1, dy2, x1, x2, dx1, dx2, q); });
+  if (r == PETRA_OK) s.count_backward();
+  return r;
 }
 
 petra_status petra_stage_update(petra_stage* st, void* stream, int32_t* updated) {
   petra_status r = check_ready(st);
   if (r) return r;
   if ((r = check_hip("before petra_stage_update"))) return r;
-  const bool did = st->impl->update(static_cast<hipStream_t>(stream));
-  if (updated) *updated = did ? 1 : 0;
-  return check_hip("petra_stage_update");
+  petra::Stage& s = *st->impl;
+  const bool due = s.update_due();
+  if (updated) *updated = due ? 1 : 0;
+  if (!due) return ok();
+  r = launch(s, {CALL_UPD}, static_cast<hipStream_t>(stream), "petra_stage_update",
+             [&](hipStream_t q) { s.update_kernels(q); });
+  if (r == PETRA_OK) s.mark_updated();
+  return r;
 }
 
 petra_status petra_stage_step(petra_stage* st, const void* x1, const void* x2, void* y1, void* y2,
@@ -265,23 +304,28 @@ petra_status petra_stage_step(petra_stage* st, const void* x1, const void* x2, v
   if ((r = check_hip("before petra_stage_step"))) return r;
   const hipError_t e = s.ensure_streams();
   if (e != hipSuccess) return fail(PETRA_ERR_HIP, std::string("stream setup: ") + hipGetErrorString(e));
-  hipStream_t main = static_cast<hipStream_t>(stream);
-  // fork: both passes start after prior work on `stream`
-  if (hipEventRecord(s.ev_fork, main) != hipSuccess ||
-      hipStreamWaitEvent(s.s_fwd, s.ev_fork, 0) != hipSuccess ||
-      hipStreamWaitEvent(s.s_bwd, s.ev_fork, 0) != hipSuccess)
-    return check_hip("petra_stage_step fork");
-  s.forward(x1, x2, y1, y2, s.s_fwd);
-  s.backward(yb1, yb2, dyb1, dyb2, xb1, xb2, dxb1, dxb2, s.s_bwd);
-  // join: the update (and later work on `stream`) follow both passes (Eq. 5)
-  if (hipEventRecord(s.ev_fwd, s.s_fwd) != hipSuccess ||
-      hipEventRecord(s.ev_bwd, s.s_bwd) != hipSuccess ||
-      hipStreamWaitEvent(main, s.ev_fwd, 0) != hipSuccess ||
-      hipStreamWaitEvent(main, s.ev_bwd, 0) != hipSuccess)
-    return check_hip("petra_stage_step join");
-  const bool did = s.update(main);
-  if (updated) *updated = did ? 1 : 0;
-  return check_hip("petra_stage_step");
+  // The update follows this step's backward (Eq. 5); whether it fires is decided
+  // on the host from the backward count before the work is enqueued.
+  s.count_backward();
+  const bool due = s.update_due();
+  auto work = [&](hipStream_t main) {
+    // fork: the forward runs on its own stream after prior work on `main`;
+    // the backward (and its weight-gradient branch) runs on `main` itself
+    (void)hipEventRecord(s.ev_fork, main);
+    (void)hipStreamWaitEvent(s.s_fwd, s.ev_fork, 0);
+    s.forward(x1, x2, y1, y2, s.s_fwd);
+    s.backward(yb1, yb2, dyb1, dyb2, xb1, xb2, dxb1, dxb2, main);
+    // join: the update (and later work on `main`) follow both passes
+    (void)hipEventRecord(s.ev_fwd, s.s_fwd);
+    (void)hipStreamWaitEvent(main, s.ev_fwd, 0);
+    if (due) s.update_kernels(main);
+  };
+  r = launch(s, {CALL_STEP, P(x1), P(x2), P(y1), P(y2), P(yb1), P(yb2), P(dyb1), P(dyb2), P(xb1),
+                 P(xb2), P(dxb1), P(dxb2), due ? 1u : 0u},
+             static_cast<hipStream_t>(stream), "petra_stage_step", work);
+  if (r == PETRA_OK && due) s.mark_updated();
+  if (updated) *updated = (r == PETRA_OK && due) ? 1 : 0;
+  return r;
 }
 
 petra_status petra_stage_profile(petra_stage* st, int32_t enable) {

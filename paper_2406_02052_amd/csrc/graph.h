@@ -1,0 +1,36 @@
+// Cache of instantiated HIP graphs, one per distinct call signature (kind of
+// call plus the device pointers it was given).  A cached call replays its
+// graph on a private stream that is fenced with events to the caller's
+// stream, so launch cost on the host is one graph launch per call.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <functional>
+#include <list>
+#include <map>
+#include <vector>
+
+namespace petra {
+
+class GraphCache {
+ public:
+  using Key = std::vector<uintptr_t>;
+  ~GraphCache();
+  // Run `enqueue` (which launches work on the stream it is given, possibly
+  // forking to other streams through events) as a graph keyed by `key`.
+  hipError_t run(const Key& key, hipStream_t caller, const std::function<void(hipStream_t)>& enqueue);
+  void clear();
+  size_t size() const { return execs_.size(); }
+  static constexpr size_t kMaxGraphs = 64;
+
+ private:
+  hipError_t ensure();
+  hipStream_t cap_ = nullptr;
+  hipEvent_t in_ = nullptr, out_ = nullptr;
+  std::map<Key, hipGraphExec_t> execs_;
+  std::list<Key> order_;
+};
+
+}  // namespace petra

@@ -8,6 +8,7 @@
 
 #include "../../include/petra.h"
 #include "kernels.h"
+#include "graph.h"
 #include "prof.h"
 
 namespace petra {
@@ -37,7 +38,7 @@ struct Block {
 // Device scratch of one pass (forward or backward), carved from the workspace.
 struct Scratch {
   void* h[3] = {nullptr, nullptr, nullptr};  // pre-BN conv outputs of the current function
-  void* d0 = nullptr;                        // BN input gradient dh (backward)
+  void* d0[2] = {nullptr, nullptr};          // BN input gradient dh (backward, per layer parity)
   void* d1 = nullptr;                        // masked gradient dz (backward)
   float* part = nullptr;                     // per-tile statistic partials [tiles][2][c]
   float* bnp = nullptr;                      // per layer: scale, shift, mean, rstd, ca, cb, cc
@@ -68,7 +69,7 @@ class Stage {
   size_t ws_need = 0;
   size_t off_wfwd = 0, off_wdg = 0;
   struct ScratchPlan {
-    size_t h[3], d0, d1, part, bnp, wpart;
+    size_t h[3], d0[2], d1, part, bnp, wpart;
   } plan_f{}, plan_b{};
   int64_t wpart_floats = 0;
 
@@ -89,16 +90,27 @@ class Stage {
   Profiler prof;
 
   hipStream_t s_fwd = nullptr, s_bwd = nullptr;
+  hipStream_t s_wg = nullptr;                 // weight-gradient branch of the backward
   hipEvent_t ev_fork = nullptr, ev_fwd = nullptr, ev_bwd = nullptr;
+  hipEvent_t ev_dh = nullptr, ev_wg = nullptr;
+  hipEvent_t ev_wpar[2] = {nullptr, nullptr};  // weight-gradient branch done with dh[parity]
 
   bool bound() const { return theta != nullptr; }
   void bind(float* th, float* gr, float* mo, float* rm, float* rv, void* w);
   void sync_weights(hipStream_t st);
+  // Kernel sequences (enqueue only; no host-side bookkeeping).
   void forward(const void* x1, const void* x2, void* y1, void* y2, hipStream_t st);
   void backward(const void* y1, const void* y2, const void* dy1, const void* dy2, void* x1,
                 void* x2, void* dx1, void* dx2, hipStream_t st);
-  bool update(hipStream_t st);
+  void update_kernels(hipStream_t st);
+  // Host-side accumulation bookkeeping: count one backward; does the update fire now?
+  void count_backward() { ++bwd_count; }
+  bool update_due() const;
+  void mark_updated() { last_update = bwd_count; }
   hipError_t ensure_streams();
+
+  GraphCache graphs;
+  bool use_graphs = true;
 
  private:
   void fn_recompute(const ResidualFn& fn, const void* u, Scratch& s, bool running,

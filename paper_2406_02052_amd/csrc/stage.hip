@@ -128,7 +128,8 @@ Stage::Stage(const petra_stage_desc& d) : desc(d) {
     for (size_t l = 0; l < 3; ++l)
       p->h[l] = l < fn_shapes.size() ? take(static_cast<size_t>(M) * fn_shapes[l].cout * esz) : 0;
     const bool bwd = p == &plan_b;
-    p->d0 = bwd ? take(static_cast<size_t>(M) * cmax * esz) : 0;
+    p->d0[0] = bwd ? take(static_cast<size_t>(M) * cmax * esz) : 0;
+    p->d0[1] = bwd ? take(static_cast<size_t>(M) * cmax * esz) : 0;
     p->d1 = bwd ? take(static_cast<size_t>(M) * cmax * esz) : 0;
     p->part = take(static_cast<size_t>(tiles_max) * 2 * cmax * sizeof(float));
     p->bnp = take(static_cast<size_t>(3) * 8 * cmax * sizeof(float));
@@ -138,9 +139,16 @@ Stage::Stage(const petra_stage_desc& d) : desc(d) {
 }
 
 Stage::~Stage() {
+  // graph executables reference the streams and events below: release them first
+  graphs.clear();
   if (ev_fork) (void)hipEventDestroy(ev_fork);
   if (ev_fwd) (void)hipEventDestroy(ev_fwd);
   if (ev_bwd) (void)hipEventDestroy(ev_bwd);
+  if (ev_dh) (void)hipEventDestroy(ev_dh);
+  if (ev_wg) (void)hipEventDestroy(ev_wg);
+  for (hipEvent_t e : ev_wpar)
+    if (e) (void)hipEventDestroy(e);
+  if (s_wg) (void)hipStreamDestroy(s_wg);
   if (s_fwd) (void)hipStreamDestroy(s_fwd);
   if (s_bwd) (void)hipStreamDestroy(s_bwd);
 }
@@ -155,7 +163,8 @@ void Stage::bind(float* th, float* gr, float* mo, float* rm, float* rv, void* w)
     Scratch& s = pass == 0 ? sf : sb;
     const int nl = blocks.empty() ? 0 : blocks[0].f.nconv;
     for (int l = 0; l < 3; ++l) s.h[l] = l < nl ? ws + p.h[l] : nullptr;
-    s.d0 = pass == 1 ? ws + p.d0 : nullptr;
+    s.d0[0] = pass == 1 ? ws + p.d0[0] : nullptr;
+    s.d0[1] = pass == 1 ? ws + p.d0[1] : nullptr;
     s.d1 = pass == 1 ? ws + p.d1 : nullptr;
     s.part = reinterpret_cast<float*>(ws + p.part);
     s.bnp = reinterpret_cast<float*>(ws + p.bnp);
@@ -170,6 +179,11 @@ hipError_t Stage::ensure_streams() {
   if ((e = hipStreamCreateWithFlags(&s_bwd, hipStreamNonBlocking)) != hipSuccess) return e;
   if ((e = hipEventCreateWithFlags(&ev_fork, hipEventDisableTiming)) != hipSuccess) return e;
   if ((e = hipEventCreateWithFlags(&ev_fwd, hipEventDisableTiming)) != hipSuccess) return e;
+  if ((e = hipStreamCreateWithFlags(&s_wg, hipStreamNonBlocking)) != hipSuccess) return e;
+  if ((e = hipEventCreateWithFlags(&ev_dh, hipEventDisableTiming)) != hipSuccess) return e;
+  if ((e = hipEventCreateWithFlags(&ev_wg, hipEventDisableTiming)) != hipSuccess) return e;
+  for (hipEvent_t& ev : ev_wpar)
+    if ((e = hipEventCreateWithFlags(&ev, hipEventDisableTiming)) != hipSuccess) return e;
   return hipEventCreateWithFlags(&ev_bwd, hipEventDisableTiming);
 }
 
@@ -280,16 +294,28 @@ void Stage::fn_backward(const ResidualFn& fn, const void* u, const void* v, cons
     prof.end(K_BN_BWD_FINALIZE, st, 0.0, 8.0 * et * cv.cout);
   }
   const void* dsrc = d;
+  // The weight-gradient branch (wgrad + split reduce) of each layer runs on its
+  // own stream, concurrently with the input-gradient chain; dh alternates
+  // between two buffers so the next layer's dh does not wait for it.
+  const bool branch = s_wg != nullptr && !prof.enabled;
+  hipStream_t wst = branch ? s_wg : st;
   for (int l = L; l >= 0; --l) {
     const ConvLayer& cv = convs[fn.conv[l]];
+    void* d0 = s.d0[l & 1];
+    // dh[l & 1] was last read by the weight gradient of layer l + 2
+    if (branch && l + 2 <= L) (void)hipStreamWaitEvent(st, ev_wpar[l & 1], 0);
     // dh_l = BN_l backward applied to the gradient of its output
     prof.begin(st);
     bn_bwd_apply(dt, dsrc, s.h[l], s.vec(l, V_CA, cmax), s.vec(l, V_CB, cmax),
-                 s.vec(l, V_CC, cmax), s.vec(l, V_MEAN, cmax), s.d0, M, cv.cout, st);
+                 s.vec(l, V_CC, cmax), s.vec(l, V_MEAN, cmax), d0, M, cv.cout, st);
     prof.end(K_BN_BWD_APPLY, st, 0.0, 3.0 * M * cv.cout * esz);
+    if (branch) {
+      (void)hipEventRecord(ev_dh, st);
+      (void)hipStreamWaitEvent(wst, ev_dh, 0);
+    }
     // weight gradient of conv_l
     WgradArgs w{};
-    w.dh = s.d0;
+    w.dh = d0;
     w.src = l == 0 ? u : s.h[l - 1];
     w.c_split = cv.cin;
     if (l > 0) {
@@ -303,17 +329,18 @@ void Stage::fn_backward(const ResidualFn& fn, const void* u, const void* v, cons
     w.m = static_cast<int>(M);
     wgrad_splits(cv, &w.splits, &w.rows_per_split);
     const double wnumel = static_cast<double>(cv.cout) * w.k_tot;
-    prof.begin(st);
-    conv_wgrad(dt, w, st);
-    prof.end(K_CONV_WGRAD, st, 2.0 * M * wnumel,
+    prof.begin(wst);
+    conv_wgrad(dt, w, wst);
+    prof.end(K_CONV_WGRAD, wst, 2.0 * M * wnumel,
              static_cast<double>(esz) * M * (cv.cin + cv.cout) + 4.0 * w.splits * wnumel);
-    prof.begin(st);
+    prof.begin(wst);
     wgrad_reduce(s.wpart, w.splits, static_cast<long>(cv.cout) * w.k_tot, inv_k, grad + cv.w_off,
-                 st);
-    prof.end(K_WGRAD_REDUCE, st, 0.0, 4.0 * wnumel * (w.splits + 2));
+                 wst);
+    prof.end(K_WGRAD_REDUCE, wst, 0.0, 4.0 * wnumel * (w.splits + 2));
+    if (branch) (void)hipEventRecord(ev_wpar[l & 1], wst);
     // input gradient: conv of dh with the transposed, flipped weights
     ConvArgs a = conv_args(cv);
-    a.src = s.d0;
+    a.src = d0;
     a.c_in = cv.cout;
     a.c_split = cv.cout;
     a.wt = static_cast<char*>(wdg) + cv.dg_off * esz;
@@ -352,6 +379,10 @@ void Stage::fn_backward(const ResidualFn& fn, const void* u, const void* v, cons
                                            static_cast<double>(cv.cin) * a.k_tot));
     }
   }
+  if (branch) {  // later work overwrites the scratch the branch reads
+    (void)hipEventRecord(ev_wg, wst);
+    (void)hipStreamWaitEvent(st, ev_wg, 0);
+  }
 }
 
 void Stage::forward(const void* x1, const void* x2, void* y1, void* y2, hipStream_t st) {
@@ -379,19 +410,19 @@ void Stage::backward(const void* y1, const void* y2, const void* dy1, const void
     fn_backward(blk.f, x2, c1, dx1, g2, x1, dx2, sb, st);
     c1 = x1; c2 = x2; g1 = dx1; g2 = dx2;
   }
-  ++bwd_count;
 }
 
-bool Stage::update(hipStream_t st) {
+bool Stage::update_due() const {
   const int k = std::max(1, opt.accum_k);
-  if (bwd_count == 0 || bwd_count == last_update || bwd_count % k != 0) return false;
+  return !(bwd_count == 0 || bwd_count == last_update || bwd_count % k != 0);
+}
+
+void Stage::update_kernels(hipStream_t st) {
   prof.begin(st);
   sgd_update(theta, grad, mom, n_params, n_conv, opt.lr, opt.momentum, opt.weight_decay,
              opt.nesterov, st);
   prof.end(K_SGD, st, 0.0, 24.0 * n_params);
   sync_weights(st);
-  last_update = bwd_count;
-  return true;
 }
 
 }  // namespace petra

@@ -123,3 +123,35 @@ def test_accumulation_k_updates_every_kth_backward():
         fired.append(st.update())
     torch.cuda.synchronize()
     assert fired == [False, False, True, False, False, True]
+
+
+def test_graph_replay_matches_eager_every_replay():
+    """The cached-graph path must give the eager path's bits on every replay,
+    with unrelated eager work and synchronisations between the replays."""
+    import torch
+    from paper_2406_02052_amd import to_host
+
+    wl = synth.CIFAR_STAGE.with_(n=4, h=8, w=32)
+    params = synth.stage_params(wl, "random")
+    stages = []
+    for graphs in (False, True):
+        st = gpu_stage(wl, params)
+        st.set_graphs(graphs)
+        stages.append((st, _io(st, wl, 11), _io(st, wl, 12)))
+    scratch = torch.zeros(1 << 20, device="cuda")
+    for rep in range(3):
+        outs = []
+        for st, (xa1, xa2, _, _), (yb1, yb2, db1, db2) in stages:
+            ya1, ya2, xb1, xb2, dxb1, dxb2 = (st.act() for _ in range(6))
+            if rep == 2:
+                st.forward(xa1, xa2, ya1, ya2)
+                st.reconstruct_backward(yb1, yb2, db1, db2, xb1, xb2, dxb1, dxb2)
+                st.update()
+            else:
+                st.step(xa1, xa2, ya1, ya2, yb1, yb2, db1, db2, xb1, xb2, dxb1, dxb2)
+            scratch.add_(1.0)           # unrelated eager work between replays
+            torch.cuda.synchronize()
+            outs.append([to_host(t) for t in (ya1, ya2, xb1, xb2, dxb1, dxb2)] +
+                        [st.params.cpu().numpy(), st.mom.cpu().numpy(), st.run_var.cpu().numpy()])
+        for a, b in zip(*outs):
+            assert np.array_equal(a, b), f"replay {rep} differs from eager"
