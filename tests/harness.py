@@ -9,7 +9,10 @@ gradients, and what the update derives from them) have a measurable noise
 floor in bf16: a one-ulp difference anywhere cascades through later roundings,
 and every pre-activation that lands on the other side of zero flips a ReLU
 decision, so the normwise error of a masked gradient grows like the square
-root of the storage noise.  The floor is measured in the same test as the
+root of the storage noise.  The reconstructed inputs share that floor: each
+block subtracts a freshly recomputed residual function of the previous
+block's reconstruction, so storage noise is amplified block after block (the
+reconstruction drift against the true input is reported).  The floor is measured in the same test as the
 largest distance between the oracle and three perturbed copies of it that
 any bf16 implementation is as entitled to as the kernels are: one computing
 in fp32 instead of fp64, and two whose storage rounding first scales each
@@ -24,7 +27,7 @@ import numpy as np
 import synth
 from oracle.stage import StageState
 
-FLOORED = ("dx1", "dx2", "grad", "update_inc", "momentum")
+FLOORED = ("x1", "x2", "dx1", "dx2", "grad", "update_inc", "momentum")
 
 
 def rel(a, b) -> float:
