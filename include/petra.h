@@ -195,6 +195,73 @@ petra_status petra_stage_step(petra_stage* st, const void* x1, const void* x2, v
                               const void* dyb2, void* xb1, void* xb2, void* dxb1, void* dxb2,
                               void* stream, int32_t* updated);
 
+/* ------------------------------------------------------------------------
+ * Multi-stage schedule on one GPU (Alg. 1, Eq. 5; delays of App. B).
+ *
+ * The network is split into num_stages stages.  Stage 0 opens with a 3x3 conv
+ * (pad 1) + BN + ReLU on the images; stage j > 0 opens with a non-reversible
+ * 1x1 stride-2 conv + BN on the previous stage's output (both streams taken as
+ * one tensor, x1 first); each stage then runs blocks_per_stage reversible basic
+ * blocks at width widths[j] (two streams of widths[j]/2 channels); the last
+ * stage ends with global average pooling, a linear layer with bias and softmax
+ * cross-entropy averaged over the micro-batch (Sec. 4.1, "Model adaptations").
+ *
+ * petra_net_tick() runs one time step of every stage: stage j (0-based) runs
+ * the forward of micro-batch t - j and the backward of micro-batch
+ * t - (2 num_stages - 2 - j), both with its current parameters, and then its
+ * update, so the delay between a stage's forward and backward of the same
+ * micro-batch is 2(num_stages - 1 - j).  Front layers keep their input in a
+ * ring of micro-batches and recompute it on the backward (Sec. 3.2,
+ * "Non-reversible stages"); the reversible blocks rebuild their input from
+ * their output.  All stages of a tick run concurrently on library streams; the
+ * tick is ordered after prior work on `stream` and later work on `stream`
+ * follows it.
+ *
+ * Limits: h and w divisible by 2^(num_stages-1); widths[j]/2 is 8 times a
+ * power of two, at most 512; c_img <= 8; classes <= 64; num_stages <= 8.
+ * ------------------------------------------------------------------------ */
+#define PETRA_MAX_STAGES 8
+
+typedef struct {
+  int32_t n, h, w, c_img;              /* micro-batch of images [n][h][w][c_img] */
+  int32_t num_stages;
+  int32_t widths[PETRA_MAX_STAGES];    /* full width of each stage (both streams) */
+  int32_t blocks_per_stage;
+  int32_t classes;
+  int32_t dtype;                       /* petra_dtype */
+  float bn_eps;
+  float bn_momentum;
+} petra_net_desc;
+
+typedef struct petra_net petra_net;
+
+petra_status petra_net_create(const petra_net_desc* desc, petra_net** out);
+petra_status petra_net_destroy(petra_net* net);
+/* Sizes as for a stage.  Parameter tensors in canonical order: per stage j,
+ * the front conv weight (KRSC, [w_j][3][3][c_img] or [w_j][1][1][w_{j-1}]), its
+ * BN gamma and beta, the reversible blocks' tensors in the stage order, and
+ * for the last stage the linear weight [classes][w_last] and bias [classes]. */
+petra_status petra_net_query(const petra_net* net, int64_t* n_params, int32_t* n_tensors,
+                             int64_t* n_bn_channels, size_t* workspace_bytes);
+petra_status petra_net_param_info(const petra_net* net, int32_t index, petra_param_info* out);
+/* Caller-owned buffers as for petra_stage_bind (workspace 256-byte aligned). */
+petra_status petra_net_bind(petra_net* net, float* params, float* grad_accum, float* momentum,
+                            float* run_mean, float* run_var, void* workspace,
+                            size_t workspace_bytes);
+petra_status petra_net_set_optimizer(petra_net* net, const petra_sgd* opt);
+petra_status petra_net_sync_weights(petra_net* net, void* stream);
+/* One tick.  images: the next micro-batch [n][h][w][c_img] in the storage type
+ * and labels: its [n] int32 class ids (device pointers), or both NULL once the
+ * input has ended (then only the micro-batches in flight advance; feeding
+ * cannot resume).  loss (nullable, device fp32): receives the mean loss of the
+ * micro-batch that reached the head in this tick; *loss_written (nullable)
+ * tells whether one did. */
+petra_status petra_net_tick(petra_net* net, const void* images, const int32_t* labels,
+                            float* loss, void* stream, int32_t* loss_written);
+/* Ticks run so far, micro-batches fed, and micro-batches still in flight. */
+petra_status petra_net_state(const petra_net* net, int64_t* ticks, int64_t* fed,
+                             int64_t* in_flight);
+
 /* Measurement support (not part of the method).  petra_stage_profile(st, 1)
  * clears the counters and starts bracketing every kernel launch of the stage
  * with HIP events on the stream the kernel is launched on; 0 stops it.

@@ -11,6 +11,13 @@ downsampling + blocks, the last stage also owns the head; the stem has a ReLU
 after its BN, the downsampling has none; the downsampling convolves the two
 streams as one tensor (x1 first) and its output is split into halves again.
 
+The linear head reads the fp32 master weights (it is not a convolution and
+has no lower-precision compute copy); `weight_view` applies to conv weights.
+`store` (identity by default) holds activations and activation gradients at a
+storage precision where the method materialises them, as in revblock: the
+front conv output, its BN(+ReLU) output, the block tensors, and the front
+layer's gradients.
+
 Schedule (0-based stage index j, J stages, one hop per tick): at tick t stage j
 runs the forward of micro-batch t - j and the backward of micro-batch
 t - (2J - 2 - j), so the delay between a stage's forward and backward of the
@@ -33,20 +40,25 @@ import numpy as np
 from . import bn, conv, revblock, sgd
 
 
-def nonrev_forward(x, w, g, b, eps, stride, relu):
-    h = conv.forward(x, w, stride=stride, pad=(w.shape[1] - 1) // 2)
+def _identity(a):
+    return a
+
+
+def nonrev_forward(x, w, g, b, eps, stride, relu, store=_identity):
+    h = store(conv.forward(x, w, stride=stride, pad=(w.shape[1] - 1) // 2))
     o, cache = bn.forward(h, g, b, eps)
-    a = np.maximum(o, 0.0) if relu else o
+    a = store(np.maximum(o, 0.0) if relu else o)
     return a, (x, h, o, cache)
 
 
-def nonrev_vjp(d, w, g, graph, stride, relu):
+def nonrev_vjp(d, w, g, graph, stride, relu, store=_identity):
     x, _, o, cache = graph
     if relu:
         d = d * (o > 0.0)
     dh, dg, db = bn.backward(d, cache, g)
+    dh = store(dh)
     pad = (w.shape[1] - 1) // 2
-    return conv.dgrad(dh, w, x.shape, stride=stride, pad=pad), (
+    return store(conv.dgrad(dh, w, x.shape, stride=stride, pad=pad)), (
         conv.wgrad(x, dh, w.shape, stride=stride, pad=pad), dg, db)
 
 
@@ -78,12 +90,16 @@ class NetStage:
     """One stage: a non-reversible front layer, reversible blocks, optional head."""
 
     def __init__(self, params, names, first: bool, last: bool, blocks: int, eps: float,
-                 bn_momentum: float, dtype, weight_view):
+                 bn_momentum: float, dtype, weight_view, store=None):
         self.params = [np.array(p, dtype=dtype) for p in params]
         self.names = list(names)
         self.first, self.last, self.blocks = first, last, blocks
         self.eps, self.bn_momentum, self.dtype = eps, bn_momentum, dtype
         self.weight_view = weight_view
+        if store is None:
+            self.store = _identity
+        else:
+            self.store = lambda a: np.asarray(store(np.asarray(a, np.float32)), dtype=dtype)
         self.accum = [np.zeros_like(p) for p in self.params]
         self.buf = [np.zeros_like(p) for p in self.params]
         nbn = 1 + blocks * 4
@@ -107,14 +123,15 @@ class NetStage:
         x = x1 if self.first else np.concatenate([x1, x2], axis=-1)
         stride = 1 if self.first else 2
         a, graph = nonrev_forward(x, self._w(0), self.params[1], self.params[2], self.eps,
-                                  stride, relu=self.first)
+                                  stride, relu=self.first, store=self.store)
         c = a.shape[-1] // 2
         return a[..., :c], a[..., c:], graph
 
     def forward(self, x1, x2):
         y1, y2, _ = self._front(x1, x2)
         for b in range(self.blocks):
-            y1, y2 = revblock.block_forward(y1, y2, self._layers(b, 0), self._layers(b, 1), self.eps)
+            y1, y2 = revblock.block_forward(y1, y2, self._layers(b, 0), self._layers(b, 1), self.eps,
+                                            self.store)
         return y1, y2
 
     def backward(self, y1, y2, g1, g2, x1, x2, k):
@@ -123,7 +140,7 @@ class NetStage:
         grads: List[Optional[np.ndarray]] = [None] * len(self.params)
         for b in reversed(range(self.blocks)):
             r = revblock.block_reconstruct_vjp(y1, y2, g1, g2, self._layers(b, 0),
-                                               self._layers(b, 1), self.eps)
+                                               self._layers(b, 1), self.eps, self.store)
             for f, key in ((0, "dF"), (1, "dG")):
                 base = 3 + (2 * b + f) * 6
                 stats = r["stats_F" if f == 0 else "stats_G"]
@@ -138,7 +155,8 @@ class NetStage:
         _, _, graph = self._front(x1, x2)
         stride = 1 if self.first else 2
         dx, (dw, dg, db) = nonrev_vjp(np.concatenate([g1, g2], axis=-1), self._w(0),
-                                      self.params[1], graph, stride, relu=self.first)
+                                      self.params[1], graph, stride, relu=self.first,
+                                      store=self.store)
         grads[0:3] = [dw, dg, db]
         h = graph[1]
         self.run_mean[0], self.run_var[0] = bn.running_update(
@@ -175,12 +193,12 @@ class PetraNet:
     """Tick-level simulation of the PETRA schedule over J stages."""
 
     def __init__(self, params, names, stages: int, blocks_per_stage: int, eps=1e-5,
-                 bn_momentum=0.1, dtype=np.float64, weight_view=None):
+                 bn_momentum=0.1, dtype=np.float64, weight_view=None, store=None):
         self.J = stages
         self.stages = []
         for j, (ps, ns) in enumerate(split_params(names, params, stages)):
             self.stages.append(NetStage(ps, ns, j == 0, j == stages - 1, blocks_per_stage,
-                                        eps, bn_momentum, dtype, weight_view))
+                                        eps, bn_momentum, dtype, weight_view, store))
         self.dtype = dtype
         self.fwd_msg: List[Optional[tuple]] = [None] * stages
         self.bwd_msg: List[Optional[tuple]] = [None] * stages
@@ -220,9 +238,9 @@ class PetraNet:
                     y1, y2 = last_out
                     lab = labels(mb)
                     loss, hc = head_loss(np.concatenate([y1, y2], -1), st.params[-2], st.params[-1], lab)
-                    dx, dwfc, dbfc = head_vjp(st._w(len(st.params) - 2), lab, hc)
+                    dx, dwfc, dbfc = head_vjp(st.params[-2], lab, hc)
                     c = y1.shape[-1]
-                    g1, g2 = dx[..., :c], dx[..., c:]
+                    g1, g2 = st.store(dx[..., :c]), st.store(dx[..., c:])
                 else:
                     y1, y2, g1, g2 = self.bwd_msg[j + 1]
                 if j == 0:

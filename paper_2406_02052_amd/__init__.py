@@ -10,4 +10,4 @@ from ._lib import *  # noqa: F401,F403  (the petra_* wrappers, same names as the
 
 _lib.load()
 
-from .stage import Stage, to_host  # noqa: E402,F401
+from .stage import Net, Stage, to_host  # noqa: E402,F401

@@ -50,6 +50,17 @@ class ParamInfo(ctypes.Structure):
                 ("weight_decay", ctypes.c_int32), ("bn_index", ctypes.c_int32)]
 
 
+MAX_STAGES = 8
+
+
+class NetDesc(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int32), ("h", ctypes.c_int32), ("w", ctypes.c_int32),
+                ("c_img", ctypes.c_int32), ("num_stages", ctypes.c_int32),
+                ("widths", ctypes.c_int32 * MAX_STAGES), ("blocks_per_stage", ctypes.c_int32),
+                ("classes", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("bn_eps", ctypes.c_float), ("bn_momentum", ctypes.c_float)]
+
+
 _VP = ctypes.c_void_p
 _SIGS = {
     "petra_status_str": (ctypes.c_char_p, [ctypes.c_int]),
@@ -69,6 +80,20 @@ _SIGS = {
     "petra_stage_reconstruct_backward": (ctypes.c_int, [_VP] * 10),
     "petra_stage_update": (ctypes.c_int, [_VP, _VP, ctypes.POINTER(ctypes.c_int32)]),
     "petra_stage_step": (ctypes.c_int, [_VP] * 14 + [ctypes.POINTER(ctypes.c_int32)]),
+    "petra_net_create": (ctypes.c_int, [ctypes.POINTER(NetDesc), ctypes.POINTER(_VP)]),
+    "petra_net_destroy": (ctypes.c_int, [_VP]),
+    "petra_net_query": (ctypes.c_int, [_VP, ctypes.POINTER(ctypes.c_int64),
+                                        ctypes.POINTER(ctypes.c_int32),
+                                        ctypes.POINTER(ctypes.c_int64),
+                                        ctypes.POINTER(ctypes.c_size_t)]),
+    "petra_net_param_info": (ctypes.c_int, [_VP, ctypes.c_int32, ctypes.POINTER(ParamInfo)]),
+    "petra_net_bind": (ctypes.c_int, [_VP, _VP, _VP, _VP, _VP, _VP, _VP, ctypes.c_size_t]),
+    "petra_net_set_optimizer": (ctypes.c_int, [_VP, ctypes.POINTER(Sgd)]),
+    "petra_net_sync_weights": (ctypes.c_int, [_VP, _VP]),
+    "petra_net_tick": (ctypes.c_int, [_VP, _VP, _VP, _VP, _VP, ctypes.POINTER(ctypes.c_int32)]),
+    "petra_net_state": (ctypes.c_int, [_VP, ctypes.POINTER(ctypes.c_int64),
+                                        ctypes.POINTER(ctypes.c_int64),
+                                        ctypes.POINTER(ctypes.c_int64)]),
     "petra_stage_profile": (ctypes.c_int, [_VP, ctypes.c_int32]),
     "petra_stage_profile_read": (ctypes.c_int, [_VP, ctypes.c_int32,
                                                  ctypes.POINTER(ctypes.c_char_p),
@@ -226,3 +251,58 @@ def petra_stage_profile_read(handle):
             _check(st, "petra_stage_profile_read")
         out[name.value.decode()] = (n.value, ms.value, fl.value, by.value)
         i += 1
+
+
+# ---- multi-stage schedule ----------------------------------------------------
+
+def petra_net_create(desc: NetDesc) -> int:
+    h = _VP()
+    _check(load().petra_net_create(ctypes.byref(desc), ctypes.byref(h)), "petra_net_create")
+    return h.value
+
+
+def petra_net_destroy(handle: int) -> None:
+    _check(load().petra_net_destroy(handle), "petra_net_destroy")
+
+
+def petra_net_query(handle: int):
+    n_params, n_tensors = ctypes.c_int64(), ctypes.c_int32()
+    n_bn, ws = ctypes.c_int64(), ctypes.c_size_t()
+    _check(load().petra_net_query(handle, ctypes.byref(n_params), ctypes.byref(n_tensors),
+                                  ctypes.byref(n_bn), ctypes.byref(ws)), "petra_net_query")
+    return n_params.value, n_tensors.value, n_bn.value, ws.value
+
+
+def petra_net_param_info(handle: int, index: int) -> ParamInfo:
+    info = ParamInfo()
+    _check(load().petra_net_param_info(handle, index, ctypes.byref(info)), "petra_net_param_info")
+    return info
+
+
+def petra_net_bind(handle, params, grad_accum, momentum, run_mean, run_var, workspace,
+                   workspace_bytes: int) -> None:
+    _check(load().petra_net_bind(handle, _ptr(params), _ptr(grad_accum), _ptr(momentum),
+                                 _ptr(run_mean), _ptr(run_var), _ptr(workspace),
+                                 workspace_bytes), "petra_net_bind")
+
+
+def petra_net_set_optimizer(handle: int, opt: Sgd) -> None:
+    _check(load().petra_net_set_optimizer(handle, ctypes.byref(opt)), "petra_net_set_optimizer")
+
+
+def petra_net_sync_weights(handle: int, stream=None) -> None:
+    _check(load().petra_net_sync_weights(handle, _stream(stream)), "petra_net_sync_weights")
+
+
+def petra_net_tick(handle, images, labels, loss=None, stream=None) -> bool:
+    wrote = ctypes.c_int32()
+    _check(load().petra_net_tick(handle, _ptr(images), _ptr(labels), _ptr(loss), _stream(stream),
+                                 ctypes.byref(wrote)), "petra_net_tick")
+    return bool(wrote.value)
+
+
+def petra_net_state(handle):
+    t, fed, fl = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+    _check(load().petra_net_state(handle, ctypes.byref(t), ctypes.byref(fed), ctypes.byref(fl)),
+           "petra_net_state")
+    return t.value, fed.value, fl.value

@@ -13,7 +13,7 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libpetra.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = ["conv.hip", "bn.hip", "sgd.hip", "prof.hip", "graph.hip", "stage.hip", "capi.hip"]
+SOURCES = ["conv.hip", "bn.hip", "sgd.hip", "prof.hip", "graph.hip", "stage.hip", "netkern.hip", "net.hip", "capi.hip"]
 FLAGS = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950", "-Wall",
          # keep hipcc from forming packed fp32 instructions
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

@@ -48,18 +48,65 @@ __device__ void reduce_partials(const float* partials, int tiles, int c, int ch,
   }
 }
 
+// Chan's pairwise combination of (count, mean, centred sum of squares).
+__device__ __forceinline__ void chan_combine(double& n, double& mean, double& m2, double nb,
+                                             double mb, double qb) {
+  if (nb <= 0.0) return;
+  const double nn = n + nb;
+  const double d = mb - mean;
+  mean += d * (nb / nn);
+  m2 += qb + d * d * (n * nb / nn);
+  n = nn;
+}
+
+// partials[tile][3][c] = (rows, sum, centred sum of squares) -> fp64 totals,
+// combined in a fixed order (thread row ty takes tiles ty, ty + 32, ...).
+__device__ void reduce_stats(const float* partials, int tiles, int c, int ch, double& n,
+                             double& mean, double& m2) {
+  __shared__ double red[3][FIN_TY][FIN_TX + 1];
+  const int tx = threadIdx.x, ty = threadIdx.y;
+  double na = 0.0, ma = 0.0, qa = 0.0;
+  if (ch < c) {
+    int t = ty;
+    for (; t + 3 * FIN_TY < tiles; t += 4 * FIN_TY) {
+      float v[4][3];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int q = 0; q < 3; ++q)
+          v[u][q] = partials[(static_cast<long>(t + u * FIN_TY) * 3 + q) * c + ch];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (v[u][0] > 0.f) chan_combine(na, ma, qa, v[u][0], static_cast<double>(v[u][1]) / v[u][0], v[u][2]);
+    }
+    for (; t < tiles; t += FIN_TY) {
+      const float nb = partials[(static_cast<long>(t) * 3 + 0) * c + ch];
+      if (nb > 0.f)
+        chan_combine(na, ma, qa, nb,
+                     static_cast<double>(partials[(static_cast<long>(t) * 3 + 1) * c + ch]) / nb,
+                     partials[(static_cast<long>(t) * 3 + 2) * c + ch]);
+    }
+  }
+  red[0][ty][tx] = na;
+  red[1][ty][tx] = ma;
+  red[2][ty][tx] = qa;
+  __syncthreads();
+  n = mean = m2 = 0.0;
+  if (ty == 0)
+    for (int i = 0; i < FIN_TY; ++i) chan_combine(n, mean, m2, red[0][i][tx], red[1][i][tx], red[2][i][tx]);
+}
+
 __global__ void bn_stats_finalize_kernel(const float* partials, int tiles, int c, long m,
                                          const float* gamma, const float* beta, float eps,
                                          float* scale, float* shift, float* mean_out,
                                          float* rstd_out, float* run_mean, float* run_var,
                                          float momentum) {
   const int ch = blockIdx.x * FIN_TX + threadIdx.x;
-  double s1, s2;
-  reduce_partials(partials, tiles, c, ch, s1, s2);
+  double n, mean, m2;
+  reduce_stats(partials, tiles, c, ch, n, mean, m2);
   if (threadIdx.y != 0 || ch >= c) return;
-  const double mean = s1 / static_cast<double>(m);
-  double var = s2 / static_cast<double>(m) - mean * mean;
-  if (var < 0.0) var = 0.0;
+  (void)m;
+  const double var = n > 0.0 ? m2 / n : 0.0;   // biased batch variance
   const double rstd = 1.0 / sqrt(var + static_cast<double>(eps));
   const double sc = static_cast<double>(gamma[ch]) * rstd;
   scale[ch] = static_cast<float>(sc);
@@ -68,7 +115,7 @@ __global__ void bn_stats_finalize_kernel(const float* partials, int tiles, int c
   rstd_out[ch] = static_cast<float>(rstd);
   if (run_mean != nullptr) {
     const double mom = momentum;
-    const double unbiased = m > 1 ? var * static_cast<double>(m) / static_cast<double>(m - 1) : var;
+    const double unbiased = n > 1.0 ? var * n / (n - 1.0) : var;
     run_mean[ch] = static_cast<float>((1.0 - mom) * run_mean[ch] + mom * mean);
     run_var[ch] = static_cast<float>((1.0 - mom) * run_var[ch] + mom * unbiased);
   }

@@ -6,10 +6,15 @@
 #include <new>
 #include <string>
 
+#include "net.h"
 #include "stage.h"
 
 struct petra_stage {
   petra::Stage* impl;
+};
+
+struct petra_net {
+  petra::Net* impl;
 };
 
 namespace {
@@ -326,6 +331,151 @@ petra_status petra_stage_step(petra_stage* st, const void* x1, const void* x2, v
   if (r == PETRA_OK && due) s.mark_updated();
   if (updated) *updated = (r == PETRA_OK && due) ? 1 : 0;
   return r;
+}
+
+// ---------------------------------------------------------------------------
+// multi-stage schedule
+// ---------------------------------------------------------------------------
+
+petra_status petra_net_create(const petra_net_desc* d, petra_net** out) {
+  g_last_error.clear();
+  if (d == nullptr || out == nullptr) return fail(PETRA_ERR_INVALID_ARG, "null argument");
+  *out = nullptr;
+  if (d->dtype != PETRA_FP32 && d->dtype != PETRA_BF16)
+    return fail(PETRA_ERR_DTYPE, "dtype must be PETRA_FP32 or PETRA_BF16");
+  if (d->num_stages < 1 || d->num_stages > PETRA_MAX_STAGES)
+    return fail(PETRA_ERR_SHAPE, "num_stages must be in [1, PETRA_MAX_STAGES]");
+  if (d->n < 1 || d->h < 1 || d->w < 1 || d->blocks_per_stage < 1)
+    return fail(PETRA_ERR_SHAPE, "n, h, w and blocks_per_stage must be positive");
+  if (d->c_img < 1 || d->c_img > 8) return fail(PETRA_ERR_SHAPE, "c_img must be in [1, 8]");
+  if (d->classes < 1 || d->classes > 64) return fail(PETRA_ERR_SHAPE, "classes must be in [1, 64]");
+  const int div = 1 << (d->num_stages - 1);
+  if (d->h % div != 0 || d->w % div != 0)
+    return fail(PETRA_ERR_SHAPE, "h and w must be divisible by 2^(num_stages-1)");
+  for (int j = 0; j < d->num_stages; ++j) {
+    if (d->widths[j] % 2 != 0 || !pow2_multiple_of_8(d->widths[j] / 2))
+      return fail(PETRA_ERR_SHAPE, "widths[j]/2 must be 8 times a power of two, at most 512");
+    const long m = static_cast<long>(d->n) * (d->h >> j) * (d->w >> j);
+    if (m * d->widths[j] >= (1L << 31)) return fail(PETRA_ERR_SHAPE, "activation too large");
+  }
+  if (!(d->bn_eps > 0.f) || d->bn_momentum < 0.f || d->bn_momentum > 1.f)
+    return fail(PETRA_ERR_INVALID_ARG, "bn_eps must be > 0 and bn_momentum in [0, 1]");
+  if (d->blocks_per_stage * 4 > petra::MAX_WEIGHT_SEGS)
+    return fail(PETRA_ERR_SHAPE, "too many blocks per stage");
+  petra_net* h = new (std::nothrow) petra_net;
+  if (h == nullptr) return fail(PETRA_ERR_INVALID_ARG, "host allocation failed");
+  h->impl = new (std::nothrow) petra::Net(*d);
+  if (h->impl == nullptr) {
+    delete h;
+    return fail(PETRA_ERR_INVALID_ARG, "host allocation failed");
+  }
+  *out = h;
+  return ok();
+}
+
+petra_status petra_net_destroy(petra_net* net) {
+  if (net == nullptr) return PETRA_OK;
+  delete net->impl;
+  delete net;
+  return PETRA_OK;
+}
+
+petra_status petra_net_query(const petra_net* net, int64_t* n_params, int32_t* n_tensors,
+                             int64_t* n_bn_channels, size_t* workspace_bytes) {
+  if (net == nullptr || net->impl == nullptr) return fail(PETRA_ERR_INVALID_ARG, "null net handle");
+  const petra::Net& s = *net->impl;
+  if (n_params) *n_params = s.n_params;
+  if (n_tensors) *n_tensors = static_cast<int32_t>(s.infos.size());
+  if (n_bn_channels) *n_bn_channels = s.n_bnch;
+  if (workspace_bytes) *workspace_bytes = s.ws_need;
+  return ok();
+}
+
+petra_status petra_net_param_info(const petra_net* net, int32_t index, petra_param_info* out) {
+  if (net == nullptr || net->impl == nullptr || out == nullptr)
+    return fail(PETRA_ERR_INVALID_ARG, "null argument");
+  const petra::Net& s = *net->impl;
+  if (index < 0 || index >= static_cast<int32_t>(s.infos.size()))
+    return fail(PETRA_ERR_INVALID_ARG, "tensor index out of range");
+  *out = s.infos[index];
+  return ok();
+}
+
+petra_status petra_net_bind(petra_net* net, float* params, float* grad_accum, float* momentum,
+                            float* run_mean, float* run_var, void* workspace,
+                            size_t workspace_bytes) {
+  if (net == nullptr || net->impl == nullptr) return fail(PETRA_ERR_INVALID_ARG, "null net handle");
+  if (!params || !grad_accum || !momentum || !run_mean || !run_var)
+    return fail(PETRA_ERR_INVALID_ARG, "null buffer");
+  if (workspace == nullptr || workspace_bytes < net->impl->ws_need)
+    return fail(PETRA_ERR_WORKSPACE, "workspace missing or smaller than petra_net_query()");
+  const void* ptrs[5] = {params, grad_accum, momentum, run_mean, run_var};
+  for (const void* p : ptrs)
+    if (!aligned16(p)) return fail(PETRA_ERR_ALIGN, "buffers must be 16-byte aligned");
+  if (reinterpret_cast<uintptr_t>(workspace) & 255u)
+    return fail(PETRA_ERR_ALIGN, "workspace must be 256-byte aligned");
+  net->impl->bind(params, grad_accum, momentum, run_mean, run_var, workspace);
+  return ok();
+}
+
+petra_status petra_net_set_optimizer(petra_net* net, const petra_sgd* opt) {
+  if (net == nullptr || net->impl == nullptr || opt == nullptr)
+    return fail(PETRA_ERR_INVALID_ARG, "null argument");
+  if (!(opt->lr >= 0.f) || !(opt->momentum >= 0.f) || opt->momentum >= 1.f ||
+      !(opt->weight_decay >= 0.f) || opt->accum_k < 1)
+    return fail(PETRA_ERR_INVALID_ARG, "need lr >= 0, 0 <= momentum < 1, weight_decay >= 0, accum_k >= 1");
+  net->impl->opt = *opt;
+  for (petra::NetStage& s : net->impl->st) {
+    s.blocks->opt = *opt;
+    s.blocks->graphs.clear();
+  }
+  return ok();
+}
+
+petra_status petra_net_sync_weights(petra_net* net, void* stream) {
+  if (net == nullptr || net->impl == nullptr) return fail(PETRA_ERR_INVALID_ARG, "null net handle");
+  if (!net->impl->bound()) return fail(PETRA_ERR_STATE, "net buffers not bound");
+  petra_status r;
+  if ((r = check_hip("before petra_net_sync_weights"))) return r;
+  net->impl->sync_weights(static_cast<hipStream_t>(stream));
+  return check_hip("petra_net_sync_weights");
+}
+
+petra_status petra_net_tick(petra_net* net, const void* images, const int32_t* labels,
+                            float* loss, void* stream, int32_t* loss_written) {
+  if (net == nullptr || net->impl == nullptr) return fail(PETRA_ERR_INVALID_ARG, "null net handle");
+  petra::Net& s = *net->impl;
+  if (!s.bound()) return fail(PETRA_ERR_STATE, "net buffers not bound");
+  if ((images == nullptr) != (labels == nullptr))
+    return fail(PETRA_ERR_INVALID_ARG, "images and labels must both be given or both be NULL");
+  if (images != nullptr && !s.feeding)
+    return fail(PETRA_ERR_STATE, "feeding cannot resume after a tick without input");
+  if (images != nullptr && (!aligned16(images) || !aligned16(labels)))
+    return fail(PETRA_ERR_ALIGN, "images and labels must be 16-byte aligned");
+  if (images != nullptr && s.fed != s.t)
+    return fail(PETRA_ERR_STATE, "micro-batch m must enter at tick m");
+  petra_status r;
+  if ((r = check_hip("before petra_net_tick"))) return r;
+  const hipError_t e = s.ensure_streams();
+  if (e != hipSuccess) return fail(PETRA_ERR_HIP, std::string("stream setup: ") + hipGetErrorString(e));
+  if (images == nullptr) s.feeding = false;
+  const bool wrote = s.tick(images, labels, loss, static_cast<hipStream_t>(stream));
+  if (loss_written) *loss_written = wrote ? 1 : 0;
+  return check_hip("petra_net_tick");
+}
+
+petra_status petra_net_state(const petra_net* net, int64_t* ticks, int64_t* fed,
+                             int64_t* in_flight) {
+  if (net == nullptr || net->impl == nullptr) return fail(PETRA_ERR_INVALID_ARG, "null net handle");
+  const petra::Net& s = *net->impl;
+  if (ticks) *ticks = s.t;
+  if (fed) *fed = s.fed;
+  // micro-batch m finishes its last backward (stage 0) at tick m + 2J - 2
+  int64_t done = s.t - (2 * static_cast<int64_t>(s.J) - 2);
+  if (done < 0) done = 0;
+  if (done > s.fed) done = s.fed;
+  if (in_flight) *in_flight = s.fed - done;
+  return ok();
 }
 
 petra_status petra_stage_profile(petra_stage* st, int32_t enable) {

@@ -60,6 +60,86 @@ __device__ __forceinline__ void gather_a(const ConvArgs& a, const RowPos& rp, bo
   }
 }
 
+// BN statistics of one output tile, mean-centred: per column the number of
+// valid rows, their sum and the sum of squared deviations from the tile mean
+// (of the values as stored in T), written to partials[tile][3][c_out].  Works
+// on the MFMA accumulator layout: lane (lr, lg) of tile (fm, fn) holds column
+// wn*TN + fn*16 + lr, rows fm*16 + lg*4 + j; valid(fm, j) says whether that row
+// is a real output row.
+template <typename T, int FM, int FN, int WAVES_M, int TN, int BN, typename Valid>
+__device__ void tile_stats(const f32x4_t (&acc)[FM][FN], Valid valid, int wm, int wn, int lane,
+                           int n0, int c_out, float* partials, int tile) {
+  __shared__ float red[WAVES_M][3][BN];
+  const int lr = lane & 15, lg = lane >> 4;
+  const T* tag = nullptr;
+  float sum[FN], cnt = 0.f;
+#pragma unroll
+  for (int fn = 0; fn < FN; ++fn) sum[fn] = 0.f;
+#pragma unroll
+  for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (!valid(fm, j)) continue;
+      cnt += 1.f;
+#pragma unroll
+      for (int fn = 0; fn < FN; ++fn) sum[fn] += quant(acc[fm][fn][j], tag);
+    }
+  cnt = sum_lane_groups(cnt);
+#pragma unroll
+  for (int fn = 0; fn < FN; ++fn) {
+    sum[fn] = sum_lane_groups(sum[fn]);
+    if (lg == 0) {
+      red[wm][0][wn * TN + fn * 16 + lr] = sum[fn];
+      red[wm][1][wn * TN + fn * 16 + lr] = cnt;
+    }
+  }
+  __syncthreads();
+  float mean[FN], m2[FN];
+#pragma unroll
+  for (int fn = 0; fn < FN; ++fn) {
+    const int cl = wn * TN + fn * 16 + lr;
+    float S = 0.f, N = 0.f;
+#pragma unroll
+    for (int w = 0; w < WAVES_M; ++w) {
+      S += red[w][0][cl];
+      N += red[w][1][cl];
+    }
+    mean[fn] = N > 0.f ? S / N : 0.f;
+    m2[fn] = 0.f;
+  }
+#pragma unroll
+  for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (!valid(fm, j)) continue;
+#pragma unroll
+      for (int fn = 0; fn < FN; ++fn) {
+        const float d = quant(acc[fm][fn][j], tag) - mean[fn];
+        m2[fn] += d * d;
+      }
+    }
+#pragma unroll
+  for (int fn = 0; fn < FN; ++fn) {
+    m2[fn] = sum_lane_groups(m2[fn]);
+    if (lg == 0) red[wm][2][wn * TN + fn * 16 + lr] = m2[fn];
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < BN; i += blockDim.x) {
+    const int col = n0 + i;
+    if (col >= c_out) continue;
+    float S = 0.f, N = 0.f, Q = 0.f;
+#pragma unroll
+    for (int w = 0; w < WAVES_M; ++w) {
+      S += red[w][0][i];
+      N += red[w][1][i];
+      Q += red[w][2][i];
+    }
+    partials[(static_cast<long>(tile) * 3 + 0) * c_out + col] = N;
+    partials[(static_cast<long>(tile) * 3 + 1) * c_out + col] = S;
+    partials[(static_cast<long>(tile) * 3 + 2) * c_out + col] = Q;
+  }
+}
+
 }  // namespace
 
 // One workgroup = 4 waves computing a BM x BN output tile; the waves form a
@@ -155,11 +235,7 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
         const long idx = static_cast<long>(row) * a.c_out + col;
         const float v = acc[fm][fn][j];
         if constexpr (EP == EP_STATS) {
-          // statistics of the stored tensor, so BN normalises exactly what it reads back
-          const float vs = quant(v, out);
-          store1(out + idx, vs);
-          s1[fn] += vs;
-          s2[fn] += vs * vs;
+          store1(out + idx, v);
         } else if constexpr (EP == EP_MASK) {
           const float hl = load1(static_cast<const T*>(a.ep_h) + idx);
           const float o = fmaf(e_scale, hl, e_shift);
@@ -168,13 +244,19 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
           s1[fn] += dz;
           s2[fn] += dz * ((hl - e_mean) * e_rstd);
         } else {
-          const float rv = load1(static_cast<const T*>(a.resid) + idx);
+          const float rv = a.resid != nullptr ? load1(static_cast<const T*>(a.resid) + idx) : 0.f;
           store1(out + idx, rv + v);
         }
       }
     }
   }
-  if constexpr (EP == EP_STATS || EP == EP_MASK) {
+  if constexpr (EP == EP_STATS) {
+    // statistics of the stored tensor, so BN normalises exactly what it reads back
+    tile_stats<T, FM, FN, WAVES_M, TN, BN>(
+        acc, [&](int fm, int j) { return row_base + fm * 16 + lg * 4 + j < a.m; }, wm, wn, lane,
+        blockIdx.y * BN, a.c_out, a.partials, blockIdx.x);
+  }
+  if constexpr (EP == EP_MASK) {
     __shared__ float red[WAVES_M][2][BN];
 #pragma unroll
     for (int fn = 0; fn < FN; ++fn) {
@@ -346,6 +428,11 @@ __global__ __launch_bounds__(256) void conv_staged_kernel(ConvArgs a) {
     __syncthreads();
   }
 
+  if constexpr (EP == EP_STATS) {
+    tile_stats<T, FM, FN, WAVES_M, TN, BN>(
+        acc, [&](int fm, int j) { return m0 + wm * TM + fm * 16 + lg * 4 + j < a.m; }, wm, wn,
+        lane, n0, a.c_out, a.partials, blockIdx.x);
+  }
   // Epilogue: per 16-row slice, stage fp32 results of each wave in LDS, then
   // each lane handles 8 consecutive columns of one row.
   float* ep = reinterpret_cast<float*>(lds) + wave * 16 * EPITCH;
@@ -386,12 +473,6 @@ __global__ __launch_bounds__(256) void conv_staged_kernel(ConvArgs a) {
       Raw8<T> o;
       if constexpr (EP == EP_STATS) {
         o.from_f32(v);
-        o.to_f32(v);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          s1[j] += v[j];
-          s2[j] += v[j] * v[j];
-        }
       } else if constexpr (EP == EP_MASK) {
         Raw8<T> hr;
         hr.load(static_cast<const T*>(a.ep_h) + idx);
@@ -407,19 +488,21 @@ __global__ __launch_bounds__(256) void conv_staged_kernel(ConvArgs a) {
           s2[j] += v[j] * ((hl[j] - emu[j]) * ers[j]);
         }
       } else {
-        Raw8<T> rr8;
-        rr8.load(static_cast<const T*>(a.resid) + idx);
-        float rv[8];
-        rr8.to_f32(rv);
+        if (a.resid != nullptr) {  // without a residual the epilogue is a plain store
+          Raw8<T> rr8;
+          rr8.load(static_cast<const T*>(a.resid) + idx);
+          float rv[8];
+          rr8.to_f32(rv);
 #pragma unroll
-        for (int j = 0; j < 8; ++j) v[j] += rv[j];
+          for (int j = 0; j < 8; ++j) v[j] += rv[j];
+        }
         o.from_f32(v);
       }
       *reinterpret_cast<uint4*>(out + idx) = make_uint4(o.w[0], o.w[1], o.w[2], o.w[3]);
     }
     __syncthreads();
   }
-  if constexpr (EP == EP_STATS || EP == EP_MASK) {
+  if constexpr (EP == EP_MASK) {
     // lanes with the same column group: lane % CG equal -> xor over the higher lane bits
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
@@ -604,6 +687,16 @@ __global__ __launch_bounds__(256) void conv_halo_kernel(ConvArgs a) {
     __syncthreads();
   }
 
+  if constexpr (EP == EP_STATS) {
+    tile_stats<T, FM, FN, WAVES_M, TN, BN>(
+        acc,
+        [&](int fm, int j) {
+          const int i = wm * TM + fm * 16 + lg * 4 + j;
+          const int ph = i / TW;
+          return p0 + ph < a.h && q0 + (i - ph * TW) < a.w;
+        },
+        wm, wn, lane, n0, a.c_out, a.partials, blockIdx.x);
+  }
   // Epilogue (as in the staged kernel, pixels mapped back to NHWC rows).
   float* ep = reinterpret_cast<float*>(lds) + wave * 16 * EPITCH;
   constexpr int CG = TN / 8;
@@ -645,12 +738,6 @@ __global__ __launch_bounds__(256) void conv_halo_kernel(ConvArgs a) {
       Raw8<T> o;
       if constexpr (EP == EP_STATS) {
         o.from_f32(v);
-        o.to_f32(v);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          s1[j] += v[j];
-          s2[j] += v[j] * v[j];
-        }
       } else if constexpr (EP == EP_MASK) {
         Raw8<T> hr;
         hr.load(static_cast<const T*>(a.ep_h) + idx);
@@ -666,19 +753,21 @@ __global__ __launch_bounds__(256) void conv_halo_kernel(ConvArgs a) {
           s2[j] += v[j] * ((hl[j] - emu[j]) * ers[j]);
         }
       } else {
-        Raw8<T> rr8;
-        rr8.load(static_cast<const T*>(a.resid) + idx);
-        float rv[8];
-        rr8.to_f32(rv);
+        if (a.resid != nullptr) {  // without a residual the epilogue is a plain store
+          Raw8<T> rr8;
+          rr8.load(static_cast<const T*>(a.resid) + idx);
+          float rv[8];
+          rr8.to_f32(rv);
 #pragma unroll
-        for (int j = 0; j < 8; ++j) v[j] += rv[j];
+          for (int j = 0; j < 8; ++j) v[j] += rv[j];
+        }
         o.from_f32(v);
       }
       *reinterpret_cast<uint4*>(out + idx) = make_uint4(o.w[0], o.w[1], o.w[2], o.w[3]);
     }
     __syncthreads();
   }
-  if constexpr (EP == EP_STATS || EP == EP_MASK) {
+  if constexpr (EP == EP_MASK) {
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       for (int off = CG; off < 64; off <<= 1) {

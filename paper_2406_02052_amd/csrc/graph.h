@@ -20,15 +20,18 @@ class GraphCache {
   ~GraphCache();
   // Run `enqueue` (which launches work on the stream it is given, possibly
   // forking to other streams through events) as a graph keyed by `key`.
-  hipError_t run(const Key& key, hipStream_t caller, const std::function<void(hipStream_t)>& enqueue);
+  // `lane` (0 or 1) selects one of two private replay streams, so that two
+  // independent calls of one owner can replay concurrently.
+  hipError_t run(const Key& key, hipStream_t caller, const std::function<void(hipStream_t)>& enqueue,
+                 int lane = 0);
   void clear();
   size_t size() const { return execs_.size(); }
   static constexpr size_t kMaxGraphs = 64;
 
  private:
   hipError_t ensure();
-  hipStream_t cap_ = nullptr;
-  hipEvent_t in_ = nullptr, out_ = nullptr;
+  hipStream_t cap_[2] = {nullptr, nullptr};
+  hipEvent_t in_[2] = {nullptr, nullptr}, out_[2] = {nullptr, nullptr};
   std::map<Key, hipGraphExec_t> execs_;
   std::list<Key> order_;
 };

@@ -18,13 +18,14 @@ struct ConvArgs {
   const float* pro_shift;
   const void* wt;          // [c_out][k_tot], k = (r, s, c)
   void* out;               // [m][c_out]
-  const void* resid;       // EP_RESID: out = resid + conv (may alias out)
+  const void* resid;       // EP_RESID: out = resid + conv (may alias out); null: out = conv
   const void* ep_h;        // EP_MASK: pre-BN tensor of the layer below, [m][c_out]
   const float* ep_scale;   // EP_MASK: BN scale/shift/mean/rstd of that layer
   const float* ep_shift;
   const float* ep_mean;
   const float* ep_rstd;
-  float* partials;         // EP_STATS / EP_MASK: [tiles_m][2][c_out]
+  float* partials;         // EP_STATS: [tiles][3][c_out] (rows, sum, centred sum of squares);
+                           // EP_MASK: [tiles][2][c_out] (sum dz, sum dz*xhat)
   int n, h, w, c_in, p, q, c_out, r, s, stride, pad, k_tot, m;
 };
 
@@ -54,7 +55,8 @@ int wgrad_halo_tiles(int dtype, const WgradArgs& a);
 void wgrad_reduce(const float* part, int splits, long numel, float inv_k, float* grad,
                   hipStream_t st);
 
-// BN statistics: partials [tiles][2][c] of (sum h, sum h^2) over m rows.
+// BN statistics: partials [tiles][3][c] of (rows, sum h, sum (h - tile mean)^2)
+// combined across tiles with Chan's pairwise formula in fp64 (m rows in all).
 // Writes scale = gamma*rstd, shift = beta - mean*scale, mean, rstd; when
 // run_mean != nullptr also moves the running statistics (unbiased variance).
 void bn_stats_finalize(const float* partials, int tiles, int c, long m, const float* gamma,
@@ -86,9 +88,10 @@ void bn_bwd_apply(int dtype, const void* d, const void* h, const float* ca, cons
 // Conv weight tensors inside the flat parameter buffer, for the refresh of
 // the storage-type compute copies.
 struct WeightSeg {
-  int64_t off;     // element offset of [c_out][r][s][c_in] in the flat buffer (== in fwd copy)
+  int64_t off;     // element offset of the master [c_out][r][s][c_in] in the flat buffer
+  int64_t fwd_off; // element offset of the forward copy [c_out][r][s][c_in_pad] (pads zeroed)
   int64_t dg_off;  // element offset of the transposed/flipped copy [c_in][r][s][c_out]
-  int c_out, r, s, c_in;
+  int c_out, r, s, c_in, c_in_pad;
 };
 
 constexpr int MAX_WEIGHT_SEGS = 96;
@@ -102,8 +105,47 @@ struct WeightSegTable {
 void sgd_update(float* theta, float* accum, float* mom, int64_t n, int64_t n_decay, float lr,
                 float momentum, float wd, int nesterov, hipStream_t st);
 // Write the forward and transposed compute copies of the conv weights listed
-// in the table (segments sorted by offset, covering [0, n_conv)).
-void refresh_weights(int dtype, const float* theta, const WeightSegTable& segs, int64_t n_conv,
+// in the table; max_numel bounds the padded size of the largest segment.
+void refresh_weights(int dtype, const float* theta, const WeightSegTable& segs, int64_t max_numel,
                      void* fwd_copy, void* dg_copy, hipStream_t st);
+
+// ---- multi-stage network helpers ------------------------------------------
+// dst[m][0..8) = src[m][0..c_img) zero-padded to 8 channels (c_img <= 8).
+void pad_channels8(int dtype, const void* src, int c_img, void* dst, long m, hipStream_t st);
+void copy_i32(const int32_t* src, int32_t* dst, int n, hipStream_t st);
+// out1/out2 [m][c/2] = (relu)(scale*h + shift) of h [m][c], split into halves.
+void bn_apply_split(int dtype, const void* h, const float* scale, const float* shift, int relu,
+                    void* out1, void* out2, long m, int c, hipStream_t st);
+// BN backward over an input gradient given as halves d1/d2 [m][c/2] of h [m][c]
+// (optionally through the ReLU that followed the BN): partial sums of
+// (dz, dz*xhat) per tile, then dh = ca*dz + cb*(h - mean) + cc.
+int split_tiles(long m, int c);
+void split_bwd_partials(int dtype, const void* d1, const void* d2, const void* h,
+                        const float* scale, const float* shift, const float* mean,
+                        const float* rstd, int relu, float* partials, long m, int c,
+                        hipStream_t st);
+void split_bwd_apply(int dtype, const void* d1, const void* d2, const void* h,
+                     const float* scale, const float* shift, const float* ca, const float* cb,
+                     const float* cc, const float* mean, int relu, void* dh, long m, int c,
+                     hipStream_t st);
+// dst1/dst2 [n][h][w][c/2]: rows of src [n*(h/2)*(w/2)][c] at even pixels, zero elsewhere.
+void scatter_stride2_split(int dtype, const void* src, void* dst1, void* dst2, int n, int h,
+                           int w, int c, hipStream_t st);
+// Head: global average pool of [x1|x2] ([n][hw][c/2] each), linear layer
+// (fp32 weight [k][c], bias [k]), softmax cross-entropy against labels.
+// Writes pooled [n][c], dlogits [n][k] (already divided by n), per-image loss
+// [n] and the input gradient halves g1/g2.
+void head_forward_backward(int dtype, const void* x1, const void* x2, int n, int hw, int c,
+                           const float* wfc, const float* bfc, int k, const int32_t* labels,
+                           float* pooled, float* dlogits, float* loss_n, void* g1, void* g2,
+                           hipStream_t st);
+// grad_w += inv_k * dlogits^T pooled; grad_b += inv_k * sum dlogits; loss = mean(loss_n).
+void head_param_grads(const float* pooled, const float* dlogits, const float* loss_n, int n,
+                      int c, int k, float inv_k, float* grad_w, float* grad_b, float* loss,
+                      hipStream_t st);
+// Split-K reduce for weights stored with padded input channels:
+// grad[o][tap][c] += inv_k * sum_split part[split][o][tap][c_pad] for c < c_real.
+void wgrad_reduce_pad(const float* part, int splits, int c_out, int taps, int c_pad, int c_real,
+                      float inv_k, float* grad, hipStream_t st);
 
 }  // namespace petra

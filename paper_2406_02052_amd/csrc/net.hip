@@ -1,0 +1,441 @@
+// Kernel sequences and buffers of the one-GPU multi-stage schedule.
+//
+// Buffers per stage j (all in the caller's workspace):
+//  * input ring: the front layer's input of the last 2(J - j) + 1 micro-batches
+//    (stage 0: the images, padded to 8 channels; the labels ride along in a
+//    ring of J).  It serves the front layer's recompute on the backward and,
+//    for stage j - 1, as the reconstructed output it receives from stage j.
+//    Stage j - 1's forward writes its output straight into slot m of it.
+//  * gradient messages to stage j - 1, double-buffered by tick parity.
+//  * front-layer scratch for the forward and for the backward, the block
+//    program's own workspace, and the head's buffers in the last stage.
+#include <algorithm>
+
+#include "net.h"
+
+namespace petra {
+
+namespace {
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+}  // namespace
+
+Net::Net(const petra_net_desc& d) : desc(d) {
+  dt = d.dtype == PETRA_BF16 ? DT_BF16 : DT_FP32;
+  esz = dt == DT_BF16 ? 2 : 4;
+  J = d.num_stages;
+  st.resize(J);
+  const int k = d.classes;
+  int64_t off = 0, run = 0;
+  for (int j = 0; j < J; ++j) {
+    NetStage& s = st[j];
+    s.j = j;
+    s.first = j == 0;
+    s.last = j == J - 1;
+    s.C = d.widths[j];
+    s.H = d.h >> j;
+    s.W = d.w >> j;
+    if (s.first) {
+      s.Hin = d.h; s.Win = d.w; s.Cin = 8; s.cin_real = d.c_img; s.R = 3; s.stride = 1; s.pad = 1;
+    } else {
+      s.Hin = st[j - 1].H; s.Win = st[j - 1].W; s.Cin = st[j - 1].C; s.cin_real = s.Cin;
+      s.R = 1; s.stride = 2; s.pad = 0;
+    }
+    s.M = static_cast<long>(d.n) * s.H * s.W;
+    s.Min = static_cast<long>(d.n) * s.Hin * s.Win;
+    petra_stage_desc sd{};
+    sd.n = d.n; sd.h = s.H; sd.w = s.W; sd.c_half = s.C / 2; sd.c_mid = 0;
+    sd.num_blocks = d.blocks_per_stage; sd.kind = PETRA_BLOCK_BASIC; sd.dtype = d.dtype;
+    sd.bn_eps = d.bn_eps; sd.bn_momentum = d.bn_momentum;
+    s.blocks.reset(new Stage(sd));
+    // flat layout: [front w][fc w] (decayed) [blocks] [front gamma][front beta][fc b]
+    s.off_front_w = off;
+    s.n_front_w = static_cast<int64_t>(s.C) * s.R * s.R * s.cin_real;
+    off += s.n_front_w;
+    s.off_fc_w = off;
+    s.n_fc_w = s.last ? static_cast<int64_t>(k) * s.C : 0;
+    off += s.n_fc_w;
+    s.off_decay = s.off_front_w;
+    s.n_decay = s.n_front_w + s.n_fc_w;
+    s.off_blocks = off;
+    off += s.blocks->n_params;
+    s.off_front_g = off;
+    s.off_front_b = off + s.C;
+    off += 2 * s.C;
+    s.off_fc_b = off;
+    off += s.last ? k : 0;
+    s.off_plain = s.off_front_g;
+    s.n_plain = off - s.off_front_g;
+    s.run_front = run;
+    run += s.C;
+    s.run_blocks = run;
+    run += s.blocks->n_bnch;
+
+    // canonical parameter order
+    petra_param_info wi{};
+    wi.offset = s.off_front_w; wi.numel = s.n_front_w; wi.role = PETRA_ROLE_CONV_WEIGHT; wi.ndim = 4;
+    wi.shape[0] = s.C; wi.shape[1] = s.R; wi.shape[2] = s.R; wi.shape[3] = s.cin_real;
+    wi.weight_decay = 1; wi.bn_index = -1;
+    infos.push_back(wi);
+    petra_param_info gi{};
+    gi.offset = s.off_front_g; gi.numel = s.C; gi.role = PETRA_ROLE_BN_GAMMA; gi.ndim = 1;
+    gi.shape[0] = s.C; gi.weight_decay = 0; gi.bn_index = -1;
+    infos.push_back(gi);
+    petra_param_info bi = gi;
+    bi.offset = s.off_front_b; bi.role = PETRA_ROLE_BN_BETA;
+    infos.push_back(bi);
+    for (petra_param_info p : s.blocks->infos) {
+      p.offset += s.off_blocks;
+      p.bn_index = -1;
+      infos.push_back(p);
+    }
+    if (s.last) {
+      petra_param_info fw{};
+      fw.offset = s.off_fc_w; fw.numel = s.n_fc_w; fw.role = PETRA_ROLE_FC_WEIGHT; fw.ndim = 2;
+      fw.shape[0] = k; fw.shape[1] = s.C; fw.weight_decay = 1; fw.bn_index = -1;
+      infos.push_back(fw);
+      petra_param_info fb{};
+      fb.offset = s.off_fc_b; fb.numel = k; fb.role = PETRA_ROLE_FC_BIAS; fb.ndim = 1;
+      fb.shape[0] = k; fb.weight_decay = 0; fb.bn_index = -1;
+      infos.push_back(fb);
+    }
+  }
+  n_params = off;
+  n_bnch = run;
+
+  // front weight copies
+  int64_t fw_off = 0, dg_off = 0;
+  front_segs.nseg = J;
+  for (int j = 0; j < J; ++j) {
+    NetStage& s = st[j];
+    front_segs.seg[j] = WeightSeg{s.off_front_w, fw_off, dg_off, s.C, s.R, s.R, s.cin_real, s.Cin};
+    const int64_t padded = static_cast<int64_t>(s.C) * s.R * s.R * s.Cin;
+    front_max_numel = std::max(front_max_numel, padded);
+    fw_off += padded;
+    dg_off += s.n_front_w;
+  }
+
+  // workspace plan
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    const size_t r = o;
+    o = align_up(o + bytes, 256);
+    return r;
+  };
+  o_front_wfwd = take(static_cast<size_t>(fw_off) * esz);
+  o_front_wdg = take(static_cast<size_t>(dg_off) * esz);
+  for (int j = 0; j < J; ++j) {
+    NetStage& s = st[j];
+    const size_t act = static_cast<size_t>(s.M) * s.C * esz;   // full-width block activation
+    const size_t half = act / 2;
+    s.o_blocks_ws = take(s.blocks->ws_need);
+    s.ring_depth = s.first ? 2 * J - 1 : 2 * (J - j) + 1;
+    s.ring_slot_bytes = align_up(static_cast<size_t>(s.Min) * s.Cin * esz, 256);
+    s.o_ring = take(s.ring_slot_bytes * s.ring_depth);
+    // conv args of the front layer, for tile counts and weight-gradient splits
+    ConvArgs f{};
+    f.n = d.n; f.h = s.Hin; f.w = s.Win; f.c_in = s.Cin; f.p = s.H; f.q = s.W; f.c_out = s.C;
+    f.r = s.R; f.s = s.R; f.stride = s.stride; f.pad = s.pad; f.k_tot = s.R * s.R * s.Cin;
+    f.m = static_cast<int>(s.M);
+    f.c_split = s.first ? s.Cin : s.Cin / 2;
+    f.src2 = s.first ? nullptr : reinterpret_cast<const void*>(16);  // marks the two-tensor input
+    const int tiles = std::max(std::max(conv_row_tiles(dt, f), split_tiles(s.M, s.C)), 1);
+    const size_t part = static_cast<size_t>(tiles) * 3 * s.C * sizeof(float);
+    const size_t bnp = static_cast<size_t>(8) * s.C * sizeof(float);
+    s.o_fh = take(act);
+    s.o_fx1 = take(half);
+    s.o_fx2 = take(half);
+    s.o_fpart = take(part);
+    s.o_fbnp = take(bnp);
+    s.o_bh = take(act);
+    s.o_bpart = take(part);
+    s.o_bbnp = take(bnp);
+    s.o_dh = take(act);
+    // weight-gradient splits of the front conv (rows strided over ~2 workgroups per CU)
+    {
+      const int ktot = s.R * s.R * s.Cin;
+      const int bo = s.C <= 32 ? 32 : 64;
+      const int wt = ((ktot + 63) / 64) * ((s.C + bo - 1) / bo);
+      int sp = std::max(1, 512 / std::max(1, wt));
+      long rps = (s.M + sp - 1) / sp;
+      rps = std::max<long>(rps, 512);
+      rps = (rps + 31) / 32 * 32;
+      s.wsplits = static_cast<int>((s.M + rps - 1) / rps);
+      s.wrows = static_cast<int>(rps);
+      s.o_wpart = take(static_cast<size_t>(s.wsplits) * s.C * ktot * sizeof(float));
+    }
+    s.o_dtmp = s.first ? 0 : take(static_cast<size_t>(s.M) * s.Cin * esz);
+    s.o_xr1 = take(half);
+    s.o_xr2 = take(half);
+    s.o_dx1 = take(half);
+    s.o_dx2 = take(half);
+    if (!s.first) {
+      const size_t in_half = static_cast<size_t>(s.Min) * (s.Cin / 2) * esz;
+      for (int p = 0; p < 2; ++p)
+        for (int h = 0; h < 2; ++h) s.o_msg[p][h] = take(in_half);
+    }
+    if (s.last) {
+      s.o_y1 = take(half);
+      s.o_y2 = take(half);
+      s.o_g1 = take(half);
+      s.o_g2 = take(half);
+      s.o_pooled = take(static_cast<size_t>(d.n) * s.C * sizeof(float));
+      s.o_dlogits = take(static_cast<size_t>(d.n) * k * sizeof(float));
+      s.o_lossn = take(static_cast<size_t>(d.n) * sizeof(float));
+    }
+    if (s.first) s.o_labels = take(static_cast<size_t>(J) * d.n * sizeof(int32_t));
+  }
+  ws_need = o;
+}
+
+Net::~Net() {
+  for (NetStage& s : st) {
+    s.blocks.reset();  // its graphs reference its own streams only
+    if (s.ev_f) (void)hipEventDestroy(s.ev_f);
+    if (s.ev_b) (void)hipEventDestroy(s.ev_b);
+    if (s.sf) (void)hipStreamDestroy(s.sf);
+    if (s.sb) (void)hipStreamDestroy(s.sb);
+  }
+  if (ev_tick) (void)hipEventDestroy(ev_tick);
+}
+
+void Net::bind(float* th, float* gr, float* mo, float* rm, float* rv, void* w) {
+  theta = th; grad = gr; mom = mo; rmean = rm; rvar = rv;
+  ws = static_cast<char*>(w);
+  for (NetStage& s : st) {
+    s.blocks->bind(th + s.off_blocks, gr + s.off_blocks, mo + s.off_blocks, rm + s.run_blocks,
+                   rv + s.run_blocks, ws + s.o_blocks_ws);
+    s.blocks->opt = opt;
+  }
+}
+
+hipError_t Net::ensure_streams() {
+  hipError_t e;
+  if (!ev_tick && (e = hipEventCreateWithFlags(&ev_tick, hipEventDisableTiming)) != hipSuccess) return e;
+  for (NetStage& s : st) {
+    if (s.sf) continue;
+    if ((e = hipStreamCreateWithFlags(&s.sf, hipStreamNonBlocking)) != hipSuccess) return e;
+    if ((e = hipStreamCreateWithFlags(&s.sb, hipStreamNonBlocking)) != hipSuccess) return e;
+    if ((e = hipEventCreateWithFlags(&s.ev_f, hipEventDisableTiming)) != hipSuccess) return e;
+    if ((e = hipEventCreateWithFlags(&s.ev_b, hipEventDisableTiming)) != hipSuccess) return e;
+    if ((e = s.blocks->ensure_streams()) != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+void Net::sync_weights(hipStream_t q) {
+  refresh_weights(dt, theta, front_segs, front_max_numel, ws + o_front_wfwd, ws + o_front_wdg, q);
+  for (NetStage& s : st) s.blocks->sync_weights(q);
+}
+
+void* Net::ring_slot(const NetStage& s, int64_t m, int half) const {
+  char* slot = ws + s.o_ring + static_cast<size_t>(m % s.ring_depth) * s.ring_slot_bytes;
+  if (half == 0) return slot;
+  return slot + static_cast<size_t>(s.Min) * (s.Cin / 2) * esz;
+}
+
+// Front conv + BN (+ ReLU on the images) into the two half-tensors the blocks read.
+void Net::front_forward(NetStage& s, const void* in1, const void* in2, hipStream_t q) {
+  ConvArgs a{};
+  a.src = in1;
+  a.src2 = in2;
+  a.c_split = in2 ? s.Cin / 2 : s.Cin;
+  a.wt = ws + o_front_wfwd + front_segs.seg[s.j].fwd_off * esz;
+  a.out = ws + s.o_fh;
+  a.partials = at<float>(s.o_fpart);
+  a.n = desc.n; a.h = s.Hin; a.w = s.Win; a.c_in = s.Cin; a.p = s.H; a.q = s.W; a.c_out = s.C;
+  a.r = s.R; a.s = s.R; a.stride = s.stride; a.pad = s.pad; a.k_tot = s.R * s.R * s.Cin;
+  a.m = static_cast<int>(s.M);
+  conv_gemm(dt, a, EP_STATS, q);
+  float* v = at<float>(s.o_fbnp);
+  bn_stats_finalize(at<float>(s.o_fpart), conv_row_tiles(dt, a), s.C, s.M, theta + s.off_front_g,
+                    theta + s.off_front_b, desc.bn_eps, v, v + s.C, v + 2 * s.C, v + 3 * s.C,
+                    nullptr, nullptr, desc.bn_momentum, q);
+  bn_apply_split(dt, ws + s.o_fh, v, v + s.C, s.first ? 1 : 0, ws + s.o_fx1, ws + s.o_fx2, s.M,
+                 s.C, q);
+}
+
+// Recompute the front layer from its buffered input and take its VJP given the
+// gradient (d1, d2) of its output; writes the gradient message for stage j - 1.
+void Net::front_backward(NetStage& s, const void* in1, const void* in2, const void* d1,
+                         const void* d2, int parity, hipStream_t q) {
+  const float inv_k = 1.0f / static_cast<float>(std::max(1, opt.accum_k));
+  ConvArgs a{};
+  a.src = in1;
+  a.src2 = in2;
+  a.c_split = in2 ? s.Cin / 2 : s.Cin;
+  a.wt = ws + o_front_wfwd + front_segs.seg[s.j].fwd_off * esz;
+  a.out = ws + s.o_bh;
+  a.partials = at<float>(s.o_bpart);
+  a.n = desc.n; a.h = s.Hin; a.w = s.Win; a.c_in = s.Cin; a.p = s.H; a.q = s.W; a.c_out = s.C;
+  a.r = s.R; a.s = s.R; a.stride = s.stride; a.pad = s.pad; a.k_tot = s.R * s.R * s.Cin;
+  a.m = static_cast<int>(s.M);
+  conv_gemm(dt, a, EP_STATS, q);
+  float* v = at<float>(s.o_bbnp);
+  float* scale = v;
+  float* shift = v + s.C;
+  float* mean = v + 2 * s.C;
+  float* rstd = v + 3 * s.C;
+  float* ca = v + 4 * s.C;
+  float* cb = v + 5 * s.C;
+  float* cc = v + 6 * s.C;
+  bn_stats_finalize(at<float>(s.o_bpart), conv_row_tiles(dt, a), s.C, s.M, theta + s.off_front_g,
+                    theta + s.off_front_b, desc.bn_eps, scale, shift, mean, rstd,
+                    rmean + s.run_front, rvar + s.run_front, desc.bn_momentum, q);
+  const int relu = s.first ? 1 : 0;
+  split_bwd_partials(dt, d1, d2, ws + s.o_bh, scale, shift, mean, rstd, relu,
+                     at<float>(s.o_bpart), s.M, s.C, q);
+  bn_bwd_finalize(at<float>(s.o_bpart), split_tiles(s.M, s.C), s.C, s.M, theta + s.off_front_g,
+                  mean, rstd, inv_k, grad + s.off_front_g, grad + s.off_front_b, ca, cb, cc, q);
+  split_bwd_apply(dt, d1, d2, ws + s.o_bh, scale, shift, ca, cb, cc, mean, relu, ws + s.o_dh,
+                  s.M, s.C, q);
+  // weight gradient
+  WgradArgs w{};
+  w.dh = ws + s.o_dh;
+  w.src = in1;
+  w.src2 = in2;
+  w.c_split = a.c_split;
+  w.partials = at<float>(s.o_wpart);
+  w.n = desc.n; w.h = s.Hin; w.w = s.Win; w.c_in = s.Cin; w.p = s.H; w.q = s.W; w.c_out = s.C;
+  w.r = s.R; w.s = s.R; w.stride = s.stride; w.pad = s.pad; w.k_tot = a.k_tot;
+  w.m = static_cast<int>(s.M);
+  w.splits = s.wsplits;
+  w.rows_per_split = s.wrows;
+  conv_wgrad(dt, w, q);
+  if (s.Cin != s.cin_real)
+    wgrad_reduce_pad(w.partials, w.splits, s.C, s.R * s.R, s.Cin, s.cin_real, inv_k,
+                     grad + s.off_front_w, q);
+  else
+    wgrad_reduce(w.partials, w.splits, static_cast<long>(s.C) * a.k_tot, inv_k,
+                 grad + s.off_front_w, q);
+  if (s.first) return;  // the images need no gradient
+  // input gradient of the 1x1 stride-2 conv: dh @ W on the output grid, then
+  // scattered to the even pixels of the input grid (zero elsewhere)
+  ConvArgs g{};
+  g.src = ws + s.o_dh;
+  g.c_split = s.C;
+  g.wt = ws + o_front_wdg + front_segs.seg[s.j].dg_off * esz;
+  g.out = ws + s.o_dtmp;
+  g.n = desc.n; g.h = s.H; g.w = s.W; g.c_in = s.C; g.p = s.H; g.q = s.W; g.c_out = s.Cin;
+  g.r = 1; g.s = 1; g.stride = 1; g.pad = 0; g.k_tot = s.C; g.m = static_cast<int>(s.M);
+  conv_gemm(dt, g, EP_RESID, q);
+  scatter_stride2_split(dt, ws + s.o_dtmp, ws + s.o_msg[parity][0], ws + s.o_msg[parity][1],
+                        desc.n, s.Hin, s.Win, s.Cin, q);
+}
+
+void Net::stage_update(NetStage& s, hipStream_t q) {
+  sgd_update(theta + s.off_decay, grad + s.off_decay, mom + s.off_decay, s.n_decay, s.n_decay,
+             opt.lr, opt.momentum, opt.weight_decay, opt.nesterov, q);
+  s.blocks->update_kernels(q);
+  sgd_update(theta + s.off_plain, grad + s.off_plain, mom + s.off_plain, s.n_plain, 0, opt.lr,
+             opt.momentum, opt.weight_decay, opt.nesterov, q);
+  WeightSegTable one{};
+  one.nseg = 1;
+  one.seg[0] = front_segs.seg[s.j];
+  refresh_weights(dt, theta, one, static_cast<int64_t>(s.C) * s.R * s.R * s.Cin, ws + o_front_wfwd,
+                  ws + o_front_wdg, q);
+}
+
+bool Net::tick(const void* images, const int32_t* labels, float* loss, hipStream_t caller) {
+  const int64_t J2 = 2 * static_cast<int64_t>(J) - 2;
+  if (images != nullptr) ++fed;   // micro-batch number t enters at this tick
+  (void)hipEventRecord(ev_tick, caller);
+  bool wrote_loss = false;
+  for (NetStage& s : st) {
+    (void)hipStreamWaitEvent(s.sf, ev_tick, 0);
+    (void)hipStreamWaitEvent(s.sb, ev_tick, 0);
+  }
+  for (NetStage& s : st) {
+    Stage& blk = *s.blocks;
+    const int64_t mf = t - s.j;
+    const int64_t mb = t - (J2 - s.j);
+    const bool do_f = mf >= 0 && mf < fed;
+    const bool do_b = mb >= 0 && mb < fed;
+    void* y1 = nullptr;
+    void* y2 = nullptr;
+    if (do_f) {
+      hipStream_t q = s.sf;
+      const void* in1;
+      const void* in2 = nullptr;
+      if (s.first) {
+        pad_channels8(dt, images, desc.c_img, ring_slot(s, mf, 0), s.Min, q);
+        copy_i32(labels, at<int32_t>(st[0].o_labels) + (mf % J) * desc.n, desc.n, q);
+        in1 = ring_slot(s, mf, 0);
+      } else {
+        in1 = ring_slot(s, mf, 0);
+        in2 = ring_slot(s, mf, 1);
+      }
+      front_forward(s, in1, in2, q);
+      if (s.last) {
+        y1 = ws + s.o_y1;
+        y2 = ws + s.o_y2;
+      } else {
+        y1 = ring_slot(st[s.j + 1], mf, 0);
+        y2 = ring_slot(st[s.j + 1], mf, 1);
+      }
+      void* fx1 = ws + s.o_fx1;
+      void* fx2 = ws + s.o_fx2;
+      (void)blk.graphs.run({1, reinterpret_cast<uintptr_t>(fx1), reinterpret_cast<uintptr_t>(y1)}, q,
+                           [&](hipStream_t c) { blk.forward(fx1, fx2, y1, y2, c); }, 0);
+      if (s.last) {
+        const int32_t* lab = at<int32_t>(st[0].o_labels) + (mf % J) * desc.n;
+        head_forward_backward(dt, y1, y2, desc.n, s.H * s.W, s.C, theta + s.off_fc_w,
+                              theta + s.off_fc_b, desc.classes, lab, at<float>(s.o_pooled),
+                              at<float>(s.o_dlogits), at<float>(s.o_lossn), ws + s.o_g1,
+                              ws + s.o_g2, q);
+        const float inv_k = 1.0f / static_cast<float>(std::max(1, opt.accum_k));
+        head_param_grads(at<float>(s.o_pooled), at<float>(s.o_dlogits), at<float>(s.o_lossn),
+                         desc.n, s.C, desc.classes, inv_k, grad + s.off_fc_w, grad + s.off_fc_b,
+                         loss, q);
+        wrote_loss = loss != nullptr;
+      }
+    }
+    if (do_b) {
+      // the last stage continues on the stream of its own forward (same micro-batch)
+      hipStream_t q = s.last ? s.sf : s.sb;
+      const void *by1, *by2, *bg1, *bg2;
+      if (s.last) {
+        by1 = ws + s.o_y1; by2 = ws + s.o_y2; bg1 = ws + s.o_g1; bg2 = ws + s.o_g2;
+      } else {
+        const NetStage& nx = st[s.j + 1];
+        const int par = static_cast<int>((t - 1) & 1);
+        by1 = ring_slot(nx, mb, 0); by2 = ring_slot(nx, mb, 1);
+        bg1 = ws + nx.o_msg[par][0]; bg2 = ws + nx.o_msg[par][1];
+      }
+      void* xr1 = ws + s.o_xr1;
+      void* xr2 = ws + s.o_xr2;
+      void* dx1 = ws + s.o_dx1;
+      void* dx2 = ws + s.o_dx2;
+      (void)blk.graphs.run({2, reinterpret_cast<uintptr_t>(by1), reinterpret_cast<uintptr_t>(bg1)}, q,
+                           [&](hipStream_t c) { blk.backward(by1, by2, bg1, bg2, xr1, xr2, dx1, dx2, c); },
+                           1);
+      blk.count_backward();
+      const void* in1 = ring_slot(s, mb, 0);
+      const void* in2 = s.first ? nullptr : ring_slot(s, mb, 1);
+      front_backward(s, in1, in2, dx1, dx2, static_cast<int>(t & 1), q);
+      if (blk.update_due()) {
+        // the update follows this stage's forward and backward of the tick (Eq. 5)
+        if (q != s.sb) {
+          (void)hipEventRecord(s.ev_f, q);
+          (void)hipStreamWaitEvent(s.sb, s.ev_f, 0);
+        } else if (do_f) {
+          (void)hipEventRecord(s.ev_f, s.sf);
+          (void)hipStreamWaitEvent(s.sb, s.ev_f, 0);
+        }
+        stage_update(s, s.sb);
+        blk.mark_updated();
+      }
+    }
+  }
+  for (NetStage& s : st) {
+    (void)hipEventRecord(s.ev_f, s.sf);
+    (void)hipEventRecord(s.ev_b, s.sb);
+    (void)hipStreamWaitEvent(caller, s.ev_f, 0);
+    (void)hipStreamWaitEvent(caller, s.ev_b, 0);
+  }
+  ++t;
+  return wrote_loss;
+}
+
+}  // namespace petra

@@ -26,30 +26,28 @@ __global__ __launch_bounds__(256) void sgd_kernel(float* __restrict__ theta, flo
   }
 }
 
+// blockIdx.y = segment; threads stride over its padded forward layout.
 template <typename T>
 __global__ __launch_bounds__(256) void refresh_kernel(const float* __restrict__ theta, WeightSegTable segs,
-                                                      int64_t n_conv, T* __restrict__ fwd,
-                                                      T* __restrict__ dg) {
-  for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < n_conv;
+                                                      T* __restrict__ fwd, T* __restrict__ dg) {
+  const WeightSeg& sg = segs.seg[blockIdx.y];
+  const int64_t n = static_cast<int64_t>(sg.c_out) * sg.r * sg.s * sg.c_in_pad;
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < n;
        i += static_cast<int64_t>(gridDim.x) * 256) {
-    int lo = 0, hi = segs.nseg - 1;
-    while (lo < hi) {  // last segment with off <= i
-      const int mid = (lo + hi + 1) >> 1;
-      if (segs.seg[mid].off <= i) lo = mid; else hi = mid - 1;
-    }
-    const WeightSeg& sg = segs.seg[lo];
-    const int64_t local = i - sg.off;
-    const int ci = static_cast<int>(local % sg.c_in);
-    const int64_t t1 = local / sg.c_in;
+    const int ci = static_cast<int>(i % sg.c_in_pad);
+    const int64_t t1 = i / sg.c_in_pad;
     const int s = static_cast<int>(t1 % sg.s);
     const int64_t t2 = t1 / sg.s;
     const int r = static_cast<int>(t2 % sg.r);
     const int o = static_cast<int>(t2 / sg.r);
-    const float v = theta[i];
-    store1(fwd + i, v);
-    const int64_t j = sg.dg_off +
-                      ((static_cast<int64_t>(ci) * sg.r + (sg.r - 1 - r)) * sg.s + (sg.s - 1 - s)) * sg.c_out + o;
-    store1(dg + j, v);
+    float v = 0.f;
+    if (ci < sg.c_in) {
+      v = theta[sg.off + ((static_cast<int64_t>(o) * sg.r + r) * sg.s + s) * sg.c_in + ci];
+      const int64_t j = sg.dg_off +
+                        ((static_cast<int64_t>(ci) * sg.r + (sg.r - 1 - r)) * sg.s + (sg.s - 1 - s)) * sg.c_out + o;
+      store1(dg + j, v);
+    }
+    store1(fwd + sg.fwd_off + i, v);
   }
 }
 
@@ -68,14 +66,16 @@ void sgd_update(float* theta, float* accum, float* mom, int64_t n, int64_t n_dec
                      lr, momentum, wd, nesterov);
 }
 
-void refresh_weights(int dtype, const float* theta, const WeightSegTable& segs, int64_t n_conv,
+void refresh_weights(int dtype, const float* theta, const WeightSegTable& segs, int64_t max_numel,
                      void* fwd_copy, void* dg_copy, hipStream_t st) {
+  if (segs.nseg <= 0) return;
+  dim3 grid(grid_for(max_numel), segs.nseg);
   if (dtype == DT_BF16)
-    hipLaunchKernelGGL(refresh_kernel<bf16_t>, dim3(grid_for(n_conv)), dim3(256), 0, st, theta, segs,
-                       n_conv, static_cast<bf16_t*>(fwd_copy), static_cast<bf16_t*>(dg_copy));
+    hipLaunchKernelGGL(refresh_kernel<bf16_t>, grid, dim3(256), 0, st, theta, segs,
+                       static_cast<bf16_t*>(fwd_copy), static_cast<bf16_t*>(dg_copy));
   else
-    hipLaunchKernelGGL(refresh_kernel<float>, dim3(grid_for(n_conv)), dim3(256), 0, st, theta, segs,
-                       n_conv, static_cast<float*>(fwd_copy), static_cast<float*>(dg_copy));
+    hipLaunchKernelGGL(refresh_kernel<float>, grid, dim3(256), 0, st, theta, segs,
+                       static_cast<float*>(fwd_copy), static_cast<float*>(dg_copy));
 }
 
 }  // namespace petra

@@ -62,7 +62,7 @@ class Stage {
   std::vector<BnLayer> bns;
   std::vector<Block> blocks;
   std::vector<petra_param_info> infos;
-  int64_t n_params = 0, n_conv = 0, n_bnch = 0;
+  int64_t n_params = 0, n_conv = 0, n_bnch = 0, max_wnumel = 0;
   WeightSegTable segs{};
 
   // Workspace plan (byte offsets).

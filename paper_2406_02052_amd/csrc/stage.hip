@@ -95,7 +95,8 @@ Stage::Stage(const petra_stage_desc& d) : desc(d) {
   segs.nseg = static_cast<int>(convs.size());
   for (size_t i = 0; i < convs.size() && i < static_cast<size_t>(MAX_WEIGHT_SEGS); ++i) {
     const ConvLayer& cv = convs[i];
-    segs.seg[i] = WeightSeg{cv.w_off, cv.dg_off, cv.cout, cv.r, cv.s, cv.cin};
+    segs.seg[i] = WeightSeg{cv.w_off, cv.w_off, cv.dg_off, cv.cout, cv.r, cv.s, cv.cin, cv.cin};
+    max_wnumel = std::max<int64_t>(max_wnumel, static_cast<int64_t>(cv.cout) * cv.r * cv.s * cv.cin);
   }
 
   // Workspace plan.
@@ -131,7 +132,7 @@ Stage::Stage(const petra_stage_desc& d) : desc(d) {
     p->d0[0] = bwd ? take(static_cast<size_t>(M) * cmax * esz) : 0;
     p->d0[1] = bwd ? take(static_cast<size_t>(M) * cmax * esz) : 0;
     p->d1 = bwd ? take(static_cast<size_t>(M) * cmax * esz) : 0;
-    p->part = take(static_cast<size_t>(tiles_max) * 2 * cmax * sizeof(float));
+    p->part = take(static_cast<size_t>(tiles_max) * 3 * cmax * sizeof(float));
     p->bnp = take(static_cast<size_t>(3) * 8 * cmax * sizeof(float));
     p->wpart = bwd ? take(static_cast<size_t>(wpart_floats) * sizeof(float)) : 0;
   }
@@ -189,7 +190,7 @@ hipError_t Stage::ensure_streams() {
 
 void Stage::sync_weights(hipStream_t st) {
   prof.begin(st);
-  refresh_weights(dt, theta, segs, n_conv, wfwd, wdg, st);
+  refresh_weights(dt, theta, segs, max_wnumel, wfwd, wdg, st);
   prof.end(K_REFRESH, st, 0.0, static_cast<double>(n_conv) * (4.0 + 2.0 * esz));
 }
 

@@ -109,3 +109,85 @@ class Stage:
 
 def to_host(t) -> np.ndarray:
     return t.detach().float().cpu().numpy()
+
+
+class Net:
+    """Owner of a multi-stage schedule's device buffers (marshalling only)."""
+
+    def __init__(self, n: int, h: int, w: int, c_img: int, widths, blocks_per_stage: int,
+                 classes: int, dtype: str = "bf16", bn_eps: float = 1e-5,
+                 bn_momentum: float = 0.1, device: str = "cuda"):
+        import torch
+        self.torch = torch
+        self.device = device
+        self.dtype = dtype
+        self.tdtype = torch.bfloat16 if dtype == "bf16" else torch.float32
+        self.img_shape = (n, h, w, c_img)
+        ws = (ctypes_int_array(widths))
+        desc = L.NetDesc(n, h, w, c_img, len(widths), ws, blocks_per_stage, classes,
+                         L.PETRA_BF16 if dtype == "bf16" else L.PETRA_FP32, bn_eps, bn_momentum)
+        self.handle = L.petra_net_create(desc)
+        self.n_params, self.n_tensors, self.n_bn, self.ws_bytes = L.petra_net_query(self.handle)
+        self.infos = [L.petra_net_param_info(self.handle, i) for i in range(self.n_tensors)]
+        f32 = dict(dtype=torch.float32, device=device)
+        self.params = torch.zeros(self.n_params, **f32)
+        self.grad = torch.zeros(self.n_params, **f32)
+        self.mom = torch.zeros(self.n_params, **f32)
+        self.run_mean = torch.zeros(self.n_bn, **f32)
+        self.run_var = torch.ones(self.n_bn, **f32)
+        self.workspace = torch.empty(self.ws_bytes + 256, dtype=torch.uint8, device=device)
+        ws_ptr = (self.workspace.data_ptr() + 255) // 256 * 256
+        L.petra_net_bind(self.handle, self.params, self.grad, self.mom, self.run_mean,
+                         self.run_var, ws_ptr, self.ws_bytes)
+        self.loss = torch.zeros(1, **f32)
+
+    def __del__(self):
+        h = getattr(self, "handle", None)
+        if h:
+            try:
+                L.petra_net_destroy(h)
+            except Exception:
+                pass
+            self.handle = None
+
+    def set_params(self, tensors, stream=None) -> None:
+        flat = np.zeros(self.n_params, np.float32)
+        for info, t in zip(self.infos, tensors, strict=True):
+            t = np.asarray(t, np.float32)
+            assert t.shape == tuple(info.shape[:info.ndim]), (t.shape, tuple(info.shape[:info.ndim]))
+            flat[info.offset:info.offset + info.numel] = t.reshape(-1)
+        self.params.copy_(self.torch.from_numpy(flat))
+        L.petra_net_sync_weights(self.handle, stream)
+
+    def _unflatten(self, buf):
+        host = buf.detach().cpu().numpy()
+        return [host[i.offset:i.offset + i.numel].reshape(tuple(i.shape[:i.ndim])).copy()
+                for i in self.infos]
+
+    def get_params(self):
+        return self._unflatten(self.params)
+
+    def set_optimizer(self, lr=0.1, momentum=0.9, weight_decay=0.0, nesterov=True, accum_k=1):
+        L.petra_net_set_optimizer(self.handle, L.Sgd(lr, momentum, weight_decay,
+                                                    1 if nesterov else 0, accum_k))
+
+    def images(self, a):
+        t = self.torch.from_numpy(np.ascontiguousarray(a, np.float32))
+        return t.to(device=self.device).to(self.tdtype).contiguous()
+
+    def labels(self, a):
+        return self.torch.from_numpy(np.ascontiguousarray(a, np.int32)).to(self.device)
+
+    def tick(self, images=None, labels=None, stream=None) -> bool:
+        return L.petra_net_tick(self.handle, images, labels, self.loss, stream)
+
+    def state(self):
+        return L.petra_net_state(self.handle)
+
+
+def ctypes_int_array(vals):
+    import ctypes
+    arr = (ctypes.c_int32 * L.MAX_STAGES)()
+    for i, v in enumerate(vals):
+        arr[i] = int(v)
+    return arr

@@ -15,6 +15,9 @@ SMALL = {
     "fp32_3tiles_5x9x7_c32": synth.BLOCK_FP32.with_(n=5, h=9, w=7, c_half=32, blocks=1),
     "fp32_bottleneck_2x6x6": synth.BLOCK_FP32.with_(n=2, h=6, w=6, c_half=32, c_mid=16,
                                                      kind="bottleneck", blocks=1),
+    # BN over two rows: the variance must not come from E[h^2] - E[h]^2
+    "fp32_two_rows_2x1x1": synth.BLOCK_FP32.with_(n=2, h=1, w=1, blocks=2),
+    "fp32_three_rows_3x1x1_c64": synth.BLOCK_FP32.with_(n=3, h=1, w=1, c_half=64, blocks=1),
     # fp32 twins of the bf16 stage shapes (same kernels' structure, 1e-4)
     "fp32_c32_4x9x9": synth.CIFAR_STAGE.with_(n=4, h=9, w=9, dtype="fp32"),
     "fp32_c128_3x6x6": synth.IMAGENET32_STAGE.with_(n=3, h=6, w=6, blocks=2, dtype="fp32"),
