@@ -36,7 +36,7 @@ def parse():
     p.add_argument("--steps", type=int, default=100)
     p.add_argument("--warmup", type=int, default=20)
     p.add_argument("--workload", default=synth.CIFAR_STAGE.name,
-                   choices=sorted(synth.STAGE_WORKLOADS))
+                   choices=sorted(synth.STAGE_WORKLOADS) + [synth.REVNET18_SCHEDULE.name])
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-profile", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=12.0,
@@ -129,12 +129,54 @@ def cpu_baseline(wl, target_s):
                       f"on {n} of the {wl.n} images ({t:.1f} s); BN statistics over the sample"}
 
 
+def bench_schedule(args):
+    """Steady-state ticks of the J-stage schedule (every stage busy every tick)."""
+    import torch
+    from paper_2406_02052_amd import Net
+
+    wl = synth.REVNET18_SCHEDULE
+    net = Net(wl.n, wl.h, wl.w, wl.c_img, wl.widths, wl.blocks_per_stage, wl.classes, wl.dtype,
+              device="cuda:0")
+    net.set_params(synth.net_params(wl))
+    net.set_optimizer(wl.lr, wl.momentum, wl.weight_decay, wl.nesterov, wl.accum_k)
+    D = 8  # a synthetic dataset of 8 micro-batches, fed in turn
+    imgs = [net.images(x) for x in synth.net_images(wl, D)]
+    labs = [net.labels(l) for l in synth.net_labels(wl, D)]
+    J = len(wl.widths)
+    warm = max(args.warmup, 2 * J - 1)   # fill the pipeline first
+    for t in range(warm):
+        net.tick(imgs[t % D], labs[t % D])
+    print(f"[bench] {wl.name}: {warm} warm-up ticks done, timing {args.steps}", file=sys.stderr,
+          flush=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for t in range(warm, warm + args.steps):
+        net.tick(imgs[t % D], labs[t % D])
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t0
+    loss = float(net.loss.item())
+    out = {"metric": "images/sec per stage step (fwd+reconstruct+VJP+update)",
+           "value": wl.n * args.steps / el, "unit": "images/s", "n_gpus": 1,
+           "steps": args.steps, "warmup": warm, "ms_per_step": el / args.steps * 1e3,
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": wl.dtype,
+           "data": "synthetic (seeded; CIFAR-shaped images, uniform labels over 10 classes)",
+           "config": {"workload": wl.name, "batch": wl.n, "hw": [wl.h, wl.w],
+                      "widths": list(wl.widths), "blocks_per_stage": wl.blocks_per_stage,
+                      "stages": J, "step": "one tick: every stage's forward and backward "
+                      "(delays 2(J-j)) and updates"},
+           "last_loss": loss, "outputs_finite": bool(np.isfinite(loss))}
+    print(json.dumps(out))
+
+
 def main():
     args = parse()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
                           "n_gpus": args.gpus}))
         sys.exit(2)
+    if args.workload == synth.REVNET18_SCHEDULE.name:
+        bench_schedule(args)
+        return
     import torch
     from paper_2406_02052_amd import Stage, petra_stage_profile, petra_stage_profile_read
 
