@@ -146,12 +146,20 @@ petra_status petra_stage_bind(petra_stage* st, float* params, float* grad_accum,
  * scale of petra_stage_reconstruct_backward(). */
 petra_status petra_stage_set_optimizer(petra_stage* st, const petra_sgd* opt);
 
-/* Graph replay (default on): each distinct call (kind of call and the device
+/* Graph replay (default off): each distinct call (kind of call and the device
  * pointers passed) is captured once into a HIP graph and replayed on a private
  * stream ordered with events after prior work on the caller's stream and
  * before later work on it; set_optimizer() drops the cached graphs.
- * enable = 0 launches every kernel directly on the caller's stream. */
+ * enable = 0 launches every kernel directly (on the caller's stream and the
+ * stage's side streams). */
 petra_status petra_stage_set_graphs(petra_stage* st, int32_t enable);
+
+/* Streams used by one backward call (default 3): 1 = every kernel on one
+ * stream; 2 = the weight gradients on a second stream; 3 = in addition the
+ * recompute of the next residual function on a third stream, overlapped with
+ * the input-gradient chain of the current one.  Results are identical in every
+ * mode.  PETRA_ERR_INVALID_ARG outside [1, 3]. */
+petra_status petra_stage_set_streams(petra_stage* st, int32_t n);
 
 /* Refresh the storage-type compute copies of the conv weights from the fp32
  * master (needed once after the caller writes params directly). */

@@ -76,6 +76,7 @@ _SIGS = {
     "petra_stage_set_optimizer": (ctypes.c_int, [_VP, ctypes.POINTER(Sgd)]),
     "petra_stage_sync_weights": (ctypes.c_int, [_VP, _VP]),
     "petra_stage_set_graphs": (ctypes.c_int, [_VP, ctypes.c_int32]),
+    "petra_stage_set_streams": (ctypes.c_int, [_VP, ctypes.c_int32]),
     "petra_stage_forward": (ctypes.c_int, [_VP, _VP, _VP, _VP, _VP, _VP]),
     "petra_stage_reconstruct_backward": (ctypes.c_int, [_VP] * 10),
     "petra_stage_update": (ctypes.c_int, [_VP, _VP, ctypes.POINTER(ctypes.c_int32)]),
@@ -196,6 +197,10 @@ def petra_stage_set_optimizer(handle: int, opt: Sgd) -> None:
 
 def petra_stage_set_graphs(handle: int, enable: bool) -> None:
     _check(load().petra_stage_set_graphs(handle, 1 if enable else 0), "petra_stage_set_graphs")
+
+
+def petra_stage_set_streams(handle: int, n: int) -> None:
+    _check(load().petra_stage_set_streams(handle, int(n)), "petra_stage_set_streams")
 
 
 def petra_stage_sync_weights(handle: int, stream=None) -> None:

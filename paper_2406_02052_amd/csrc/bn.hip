@@ -11,100 +11,105 @@ namespace petra {
 
 namespace {
 
-constexpr int FIN_TX = 32, FIN_TY = 32;
-
-// Fixed-order reduction of partials[tile][which][c] over tiles, in fp64.
-// 32 channels x 32 row groups per block; each thread keeps four independent
-// accumulator pairs so that several loads are in flight.
-__device__ void reduce_partials(const float* partials, int tiles, int c, int ch, double& s1,
-                                double& s2) {
-  __shared__ double red[2][FIN_TY][FIN_TX + 1];
-  const int tx = threadIdx.x, ty = threadIdx.y;
-  double a[4] = {0.0, 0.0, 0.0, 0.0}, b[4] = {0.0, 0.0, 0.0, 0.0};
-  if (ch < c) {
-    int t = ty;
-    for (; t + 3 * FIN_TY < tiles; t += 4 * FIN_TY) {
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const long row = static_cast<long>(t + u * FIN_TY) * 2;
-        a[u] += partials[row * c + ch];
-        b[u] += partials[(row + 1) * c + ch];
-      }
-    }
-    for (; t < tiles; t += FIN_TY) {
-      a[0] += partials[(static_cast<long>(t) * 2) * c + ch];
-      b[0] += partials[(static_cast<long>(t) * 2 + 1) * c + ch];
-    }
-  }
-  red[0][ty][tx] = (a[0] + a[1]) + (a[2] + a[3]);
-  red[1][ty][tx] = (b[0] + b[1]) + (b[2] + b[3]);
-  __syncthreads();
-  s1 = s2 = 0.0;
-  if (ty == 0) {
-    for (int i = 0; i < FIN_TY; ++i) {
-      s1 += red[0][i][tx];
-      s2 += red[1][i][tx];
-    }
-  }
-}
+// Finalize kernels: one 256-thread block per channel.  Thread t takes tiles
+// t, t + 256, ... (loads of up to FIN_U tiles in flight), then the block's
+// values are combined in a fixed tree: xor-shuffle levels inside each wave,
+// then the four wave results in order.  Deterministic run to run.
+constexpr int FIN_THREADS = 256;
+constexpr int FIN_U = 4;
 
 // Chan's pairwise combination of (count, mean, centred sum of squares).
 __device__ __forceinline__ void chan_combine(double& n, double& mean, double& m2, double nb,
                                              double mb, double qb) {
   if (nb <= 0.0) return;
   const double nn = n + nb;
+  const double r = nb / nn;
   const double d = mb - mean;
-  mean += d * (nb / nn);
-  m2 += qb + d * d * (n * nb / nn);
+  mean += d * r;
+  m2 += qb + d * d * n * r;
   n = nn;
 }
 
-// partials[tile][3][c] = (rows, sum, centred sum of squares) -> fp64 totals,
-// combined in a fixed order (thread row ty takes tiles ty, ty + 32, ...).
-__device__ void reduce_stats(const float* partials, int tiles, int c, int ch, double& n,
-                             double& mean, double& m2) {
-  __shared__ double red[3][FIN_TY][FIN_TX + 1];
-  const int tx = threadIdx.x, ty = threadIdx.y;
-  double na = 0.0, ma = 0.0, qa = 0.0;
-  if (ch < c) {
-    int t = ty;
-    for (; t + 3 * FIN_TY < tiles; t += 4 * FIN_TY) {
-      float v[4][3];
+// Sum of (a, b) over partials[tile][2][c] for channel ch.
+__device__ void reduce_partials(const float* partials, int tiles, int c, int ch, double& s1,
+                                double& s2) {
+  __shared__ double red[2][FIN_THREADS / 64];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  double a = 0.0, b = 0.0;
+  for (int base = tid; base < tiles; base += FIN_THREADS * FIN_U) {
+    float va[FIN_U], vb[FIN_U];
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
-#pragma unroll
-        for (int q = 0; q < 3; ++q)
-          v[u][q] = partials[(static_cast<long>(t + u * FIN_TY) * 3 + q) * c + ch];
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
-        if (v[u][0] > 0.f) chan_combine(na, ma, qa, v[u][0], static_cast<double>(v[u][1]) / v[u][0], v[u][2]);
+    for (int u = 0; u < FIN_U; ++u) {
+      const int t = base + u * FIN_THREADS;
+      const bool ok = t < tiles;
+      va[u] = ok ? partials[(static_cast<long>(t) * 2) * c + ch] : 0.f;
+      vb[u] = ok ? partials[(static_cast<long>(t) * 2 + 1) * c + ch] : 0.f;
     }
-    for (; t < tiles; t += FIN_TY) {
-      const float nb = partials[(static_cast<long>(t) * 3 + 0) * c + ch];
-      if (nb > 0.f)
-        chan_combine(na, ma, qa, nb,
-                     static_cast<double>(partials[(static_cast<long>(t) * 3 + 1) * c + ch]) / nb,
-                     partials[(static_cast<long>(t) * 3 + 2) * c + ch]);
+#pragma unroll
+    for (int u = 0; u < FIN_U; ++u) {
+      a += va[u];
+      b += vb[u];
     }
   }
-  red[0][ty][tx] = na;
-  red[1][ty][tx] = ma;
-  red[2][ty][tx] = qa;
+  for (int off = 1; off < 64; off <<= 1) {
+    a += __shfl_xor(a, off, 64);
+    b += __shfl_xor(b, off, 64);
+  }
+  if (lane == 0) {
+    red[0][wave] = a;
+    red[1][wave] = b;
+  }
   __syncthreads();
-  n = mean = m2 = 0.0;
-  if (ty == 0)
-    for (int i = 0; i < FIN_TY; ++i) chan_combine(n, mean, m2, red[0][i][tx], red[1][i][tx], red[2][i][tx]);
+  s1 = (red[0][0] + red[0][1]) + (red[0][2] + red[0][3]);
+  s2 = (red[1][0] + red[1][1]) + (red[1][2] + red[1][3]);
 }
 
-__global__ void bn_stats_finalize_kernel(const float* partials, int tiles, int c, long m,
-                                         const float* gamma, const float* beta, float eps,
-                                         float* scale, float* shift, float* mean_out,
-                                         float* rstd_out, float* run_mean, float* run_var,
-                                         float momentum) {
-  const int ch = blockIdx.x * FIN_TX + threadIdx.x;
+// partials[tile][3][c] = (rows, sum, centred sum of squares) -> fp64 totals for ch.
+__device__ void reduce_stats(const float* partials, int tiles, int c, int ch, double& n,
+                             double& mean, double& m2) {
+  __shared__ double red[3][FIN_THREADS / 64];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  double na = 0.0, ma = 0.0, qa = 0.0;
+  for (int base = tid; base < tiles; base += FIN_THREADS * FIN_U) {
+    float vn[FIN_U], vs[FIN_U], vq[FIN_U];
+#pragma unroll
+    for (int u = 0; u < FIN_U; ++u) {
+      const int t = base + u * FIN_THREADS;
+      const bool ok = t < tiles;
+      const long row = static_cast<long>(t) * 3;
+      vn[u] = ok ? partials[row * c + ch] : 0.f;
+      vs[u] = ok ? partials[(row + 1) * c + ch] : 0.f;
+      vq[u] = ok ? partials[(row + 2) * c + ch] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < FIN_U; ++u)
+      if (vn[u] > 0.f) chan_combine(na, ma, qa, vn[u], static_cast<double>(vs[u]) / vn[u], vq[u]);
+  }
+  for (int off = 1; off < 64; off <<= 1) {
+    const double nb = __shfl_xor(na, off, 64), mb = __shfl_xor(ma, off, 64),
+                 qb = __shfl_xor(qa, off, 64);
+    chan_combine(na, ma, qa, nb, mb, qb);
+  }
+  if (lane == 0) {
+    red[0][wave] = na;
+    red[1][wave] = ma;
+    red[2][wave] = qa;
+  }
+  __syncthreads();
+  n = red[0][0];
+  mean = red[1][0];
+  m2 = red[2][0];
+  for (int w = 1; w < FIN_THREADS / 64; ++w) chan_combine(n, mean, m2, red[0][w], red[1][w], red[2][w]);
+}
+
+__global__ __launch_bounds__(FIN_THREADS) void bn_stats_finalize_kernel(
+    const float* partials, int tiles, int c, long m, const float* gamma, const float* beta,
+    float eps, float* scale, float* shift, float* mean_out, float* rstd_out, float* run_mean,
+    float* run_var, float momentum) {
+  const int ch = blockIdx.x;
   double n, mean, m2;
   reduce_stats(partials, tiles, c, ch, n, mean, m2);
-  if (threadIdx.y != 0 || ch >= c) return;
+  if (threadIdx.x != 0) return;
   (void)m;
   const double var = n > 0.0 ? m2 / n : 0.0;   // biased batch variance
   const double rstd = 1.0 / sqrt(var + static_cast<double>(eps));
@@ -121,14 +126,13 @@ __global__ void bn_stats_finalize_kernel(const float* partials, int tiles, int c
   }
 }
 
-__global__ void bn_bwd_finalize_kernel(const float* partials, int tiles, int c, long m,
-                                       const float* gamma, const float* mean, const float* rstd,
-                                       float inv_k, float* dgamma, float* dbeta, float* ca,
-                                       float* cb, float* cc) {
-  const int ch = blockIdx.x * FIN_TX + threadIdx.x;
+__global__ __launch_bounds__(FIN_THREADS) void bn_bwd_finalize_kernel(
+    const float* partials, int tiles, int c, long m, const float* gamma, const float* mean,
+    const float* rstd, float inv_k, float* dgamma, float* dbeta, float* ca, float* cb, float* cc) {
+  const int ch = blockIdx.x;
   double sd, sdx;
   reduce_partials(partials, tiles, c, ch, sd, sdx);
-  if (threadIdx.y != 0 || ch >= c) return;
+  if (threadIdx.x != 0) return;
   (void)mean;
   dbeta[ch] += inv_k * static_cast<float>(sd);
   dgamma[ch] += inv_k * static_cast<float>(sdx);
@@ -152,6 +156,23 @@ __global__ __launch_bounds__(256) void combine_fwd_kernel(const T* r, const T* h
 #pragma unroll
     for (int j = 0; j < 8; ++j) o[j] = rv[j] + fmaf(scale[ch + j], hv[j], shift[ch + j]);
     Vec8<T>::store(y + i * 8, o);
+  }
+}
+
+// x = v - (scale*h + shift): the reconstruction of a coupling input.
+template <typename T>
+__global__ __launch_bounds__(256) void combine_rec_kernel(const T* v, const T* h,
+                                                          const float* scale, const float* shift,
+                                                          T* x, long total8, int c8) {
+  for (long i = static_cast<long>(blockIdx.x) * 256 + threadIdx.x; i < total8;
+       i += static_cast<long>(gridDim.x) * 256) {
+    const int ch = static_cast<int>(i % c8) * 8;
+    float vv[8], hv[8], o[8];
+    Vec8<T>::load(v + i * 8, vv);
+    Vec8<T>::load(h + i * 8, hv);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) o[j] = vv[j] - fmaf(scale[ch + j], hv[j], shift[ch + j]);
+    Vec8<T>::store(x + i * 8, o);
   }
 }
 
@@ -257,16 +278,14 @@ void bn_stats_finalize(const float* partials, int tiles, int c, long m, const fl
                        const float* beta, float eps, float* scale, float* shift, float* mean,
                        float* rstd, float* run_mean, float* run_var, float momentum,
                        hipStream_t st) {
-  dim3 grid((c + FIN_TX - 1) / FIN_TX), block(FIN_TX, FIN_TY);
-  hipLaunchKernelGGL(bn_stats_finalize_kernel, grid, block, 0, st, partials, tiles, c, m, gamma,
+  hipLaunchKernelGGL(bn_stats_finalize_kernel, dim3(c), dim3(FIN_THREADS), 0, st, partials, tiles, c, m, gamma,
                      beta, eps, scale, shift, mean, rstd, run_mean, run_var, momentum);
 }
 
 void bn_bwd_finalize(const float* partials, int tiles, int c, long m, const float* gamma,
                      const float* mean, const float* rstd, float inv_k, float* dgamma,
                      float* dbeta, float* ca, float* cb, float* cc, hipStream_t st) {
-  dim3 grid((c + FIN_TX - 1) / FIN_TX), block(FIN_TX, FIN_TY);
-  hipLaunchKernelGGL(bn_bwd_finalize_kernel, grid, block, 0, st, partials, tiles, c, m, gamma,
+  hipLaunchKernelGGL(bn_bwd_finalize_kernel, dim3(c), dim3(FIN_THREADS), 0, st, partials, tiles, c, m, gamma,
                      mean, rstd, inv_k, dgamma, dbeta, ca, cb, cc);
 }
 
@@ -281,6 +300,19 @@ void combine_fwd(int dtype, const void* r, const void* h, const float* scale, co
     hipLaunchKernelGGL(combine_fwd_kernel<float>, dim3(ew_grid(total8)), dim3(256), 0, st,
                        static_cast<const float*>(r), static_cast<const float*>(h), scale, shift,
                        static_cast<float*>(y), total8, c / 8);
+}
+
+void combine_rec(int dtype, const void* v, const void* h, const float* scale, const float* shift,
+                 void* x, long m, int c, hipStream_t st) {
+  const long total8 = m * c / 8;
+  if (dtype == DT_BF16)
+    hipLaunchKernelGGL(combine_rec_kernel<bf16_t>, dim3(ew_grid(total8)), dim3(256), 0, st,
+                       static_cast<const bf16_t*>(v), static_cast<const bf16_t*>(h), scale, shift,
+                       static_cast<bf16_t*>(x), total8, c / 8);
+  else
+    hipLaunchKernelGGL(combine_rec_kernel<float>, dim3(ew_grid(total8)), dim3(256), 0, st,
+                       static_cast<const float*>(v), static_cast<const float*>(h), scale, shift,
+                       static_cast<float*>(x), total8, c / 8);
 }
 
 void bn_bwd_apply(int dtype, const void* d, const void* h, const float* ca, const float* cb,

@@ -104,19 +104,27 @@ petra_status check_bwd(const petra::Stage& s, const void* y1, const void* y2, co
   return PETRA_OK;
 }
 
-enum CallKind : uintptr_t { CALL_FWD = 1, CALL_BWD, CALL_UPD, CALL_STEP, CALL_SYNC };
+enum CallKind : uintptr_t { CALL_FWD = 1, CALL_BWD, CALL_UPD, CALL_SYNC };
 
 // Enqueue `work` on `stream`, through the stage's graph cache unless graphs are
 // off or per-launch profiling is active.
+petra_status launch_status(petra::Stage& s, const char* where) {
+  if (s.launch_error) {
+    s.launch_error = false;
+    return fail(PETRA_ERR_STATE, std::string(where) + ": internal error: unsupported kernel variant");
+  }
+  return check_hip(where);
+}
+
 petra_status launch(petra::Stage& s, const petra::GraphCache::Key& key, hipStream_t stream,
                     const char* where, const std::function<void(hipStream_t)>& work) {
   if (s.use_graphs && !s.prof.enabled) {
     const hipError_t e = s.graphs.run(key, stream, work);
     if (e != hipSuccess) return fail(PETRA_ERR_HIP, std::string(where) + ": " + hipGetErrorString(e));
-    return check_hip(where);
+    return launch_status(s, where);
   }
   work(stream);
-  return check_hip(where);
+  return launch_status(s, where);
 }
 
 uintptr_t P(const void* p) { return reinterpret_cast<uintptr_t>(p); }
@@ -239,6 +247,14 @@ petra_status petra_stage_set_graphs(petra_stage* st, int32_t enable) {
   return ok();
 }
 
+petra_status petra_stage_set_streams(petra_stage* st, int32_t n) {
+  if (st == nullptr || st->impl == nullptr) return fail(PETRA_ERR_INVALID_ARG, "null stage handle");
+  if (n < 1 || n > 3) return fail(PETRA_ERR_INVALID_ARG, "streams must be 1, 2 or 3");
+  st->impl->bwd_streams = n;
+  st->impl->graphs.clear();
+  return ok();
+}
+
 petra_status petra_stage_sync_weights(petra_stage* st, void* stream) {
   petra_status r = check_ready(st);
   if (r) return r;
@@ -313,21 +329,36 @@ petra_status petra_stage_step(petra_stage* st, const void* x1, const void* x2, v
   // on the host from the backward count before the work is enqueued.
   s.count_backward();
   const bool due = s.update_due();
-  auto work = [&](hipStream_t main) {
-    // fork: the forward runs on its own stream after prior work on `main`;
-    // the backward (and its weight-gradient branch) runs on `main` itself
-    (void)hipEventRecord(s.ev_fork, main);
-    (void)hipStreamWaitEvent(s.s_fwd, s.ev_fork, 0);
+  hipStream_t main = static_cast<hipStream_t>(stream);
+  // fork: the forward runs on its own stream after prior work on `main`, the
+  // backward on `main` itself; join: the update (and later work on `main`)
+  // follow both passes.  With graphs on, each pass replays the graph of its
+  // standalone call (two replay lanes), so the step shares them.
+  (void)hipEventRecord(s.ev_fork, main);
+  (void)hipStreamWaitEvent(s.s_fwd, s.ev_fork, 0);
+  if (s.use_graphs && !s.prof.enabled) {
+    hipError_t ge = s.graphs.run({CALL_FWD, P(x1), P(x2), P(y1), P(y2)}, s.s_fwd,
+                                 [&](hipStream_t c) { s.forward(x1, x2, y1, y2, c); }, 1);
+    if (ge == hipSuccess)
+      ge = s.graphs.run({CALL_BWD, P(yb1), P(yb2), P(dyb1), P(dyb2), P(xb1), P(xb2), P(dxb1), P(dxb2)},
+                        main, [&](hipStream_t c) {
+                          s.backward(yb1, yb2, dyb1, dyb2, xb1, xb2, dxb1, dxb2, c);
+                        }, 0);
+    (void)hipEventRecord(s.ev_fwd, s.s_fwd);
+    (void)hipStreamWaitEvent(main, s.ev_fwd, 0);
+    if (ge == hipSuccess && due)
+      ge = s.graphs.run({CALL_UPD}, main, [&](hipStream_t c) { s.update_kernels(c); }, 0);
+    r = ge != hipSuccess
+            ? fail(PETRA_ERR_HIP, std::string("petra_stage_step: ") + hipGetErrorString(ge))
+            : launch_status(s, "petra_stage_step");
+  } else {
     s.forward(x1, x2, y1, y2, s.s_fwd);
     s.backward(yb1, yb2, dyb1, dyb2, xb1, xb2, dxb1, dxb2, main);
-    // join: the update (and later work on `main`) follow both passes
     (void)hipEventRecord(s.ev_fwd, s.s_fwd);
     (void)hipStreamWaitEvent(main, s.ev_fwd, 0);
     if (due) s.update_kernels(main);
-  };
-  r = launch(s, {CALL_STEP, P(x1), P(x2), P(y1), P(y2), P(yb1), P(yb2), P(dyb1), P(dyb2), P(xb1),
-                 P(xb2), P(dxb1), P(dxb2), due ? 1u : 0u},
-             static_cast<hipStream_t>(stream), "petra_stage_step", work);
+    r = launch_status(s, "petra_stage_step");
+  }
   if (r == PETRA_OK && due) s.mark_updated();
   if (updated) *updated = (r == PETRA_OK && due) ? 1 : 0;
   return r;
@@ -461,6 +492,8 @@ petra_status petra_net_tick(petra_net* net, const void* images, const int32_t* l
   if (images == nullptr) s.feeding = false;
   const bool wrote = s.tick(images, labels, loss, static_cast<hipStream_t>(stream));
   if (loss_written) *loss_written = wrote ? 1 : 0;
+  for (petra::NetStage& ns : s.st)
+    if ((r = launch_status(*ns.blocks, "petra_net_tick"))) return r;
   return check_hip("petra_net_tick");
 }
 

@@ -39,8 +39,30 @@ __device__ __forceinline__ const T* src_pixel(const ConvArgs& a, int n, int ih, 
   return static_cast<const T*>(a.src) + pix * a.c_split + c;
 }
 
+// Prologue on 8 consecutive input channels c..c+7 of a loaded chunk r (hr: the
+// same chunk of pro_h for PRO_BWD).  Tables t0..t3: scale, shift for PRO_RELU;
+// ca, cb, cc, mean for PRO_BWD (LDS or global).  The result is rounded to T, as
+// the materialised tensor would be.
+template <typename T, int PRO>
+__device__ __forceinline__ void pro8(Raw8<T>& r, const Raw8<T>& hr, const float* t0,
+                                     const float* t1, const float* t2, const float* t3, int c) {
+  if constexpr (PRO == PRO_NONE) return;
+  float v[8];
+  r.to_f32(v);
+  if constexpr (PRO == PRO_RELU) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = fmaxf(fmaf(t0[c + j], v[j], t1[c + j]), 0.f);
+  } else {
+    float h[8];
+    hr.to_f32(h);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = fmaf(t0[c + j], v[j], fmaf(t1[c + j], h[j] - t3[c + j], t2[c + j]));
+  }
+  r.from_f32(v);
+}
+
 // Gather 8 consecutive input channels of one im2col element group.
-template <typename T, bool PRO>
+template <typename T, int PRO>
 __device__ __forceinline__ void gather_a(const ConvArgs& a, const RowPos& rp, bool kvalid, int fr,
                                          int fs, int c, Raw8<T>& f) {
   const int ih = rp.p * a.stride + fr - a.pad;
@@ -51,12 +73,38 @@ __device__ __forceinline__ void gather_a(const ConvArgs& a, const RowPos& rp, bo
   }
   const T* ptr = src_pixel<T>(a, rp.n, ih, iw, c);
   f.load(ptr);
-  if constexpr (PRO) {
-    float v[8];
-    f.to_f32(v);
+  if constexpr (PRO == PRO_RELU) {
+    pro8<T, PRO>(f, f, a.pro_scale, a.pro_shift, nullptr, nullptr, c);
+  } else if constexpr (PRO == PRO_BWD) {
+    Raw8<T> hr;
+    hr.load(static_cast<const T*>(a.pro_h) + (ptr - static_cast<const T*>(a.src)));
+    pro8<T, PRO>(f, hr, a.pro_ca, a.pro_cb, a.pro_cc, a.pro_mean, c);
+  }
+}
+
+// Output-side operand of the weight gradient: with dh_h set, 8 channels o..o+7
+// of the BN input gradient are formed from the loaded chunk (coefficients in
+// registers: ca, cb, cc, mean), rounded to T as the materialised tensor would be.
+template <typename T>
+__device__ __forceinline__ void dh_bwd8(Raw8<T>& r, const T* hptr, const float (&k)[4][8]) {
+  Raw8<T> hr;
+  hr.load(hptr);
+  float v[8], h[8];
+  r.to_f32(v);
+  hr.to_f32(h);
 #pragma unroll
-    for (int j = 0; j < 8; ++j) v[j] = fmaxf(fmaf(a.pro_scale[c + j], v[j], a.pro_shift[c + j]), 0.f);
-    f.from_f32(v);
+  for (int j = 0; j < 8; ++j) v[j] = fmaf(k[0][j], v[j], fmaf(k[1][j], h[j] - k[3][j], k[2][j]));
+  r.from_f32(v);
+}
+
+__device__ __forceinline__ void dh_coeffs(const WgradArgs& a, int o, float (&k)[4][8]) {
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const bool ok = a.dh_h != nullptr && o + j < a.c_out;
+    k[0][j] = ok ? a.dh_ca[o + j] : 0.f;
+    k[1][j] = ok ? a.dh_cb[o + j] : 0.f;
+    k[2][j] = ok ? a.dh_cc[o + j] : 0.f;
+    k[3][j] = ok ? a.dh_mean[o + j] : 0.f;
   }
 }
 
@@ -72,18 +120,28 @@ __device__ void tile_stats(const f32x4_t (&acc)[FM][FN], Valid valid, int wm, in
   __shared__ float red[WAVES_M][3][BN];
   const int lr = lane & 15, lg = lane >> 4;
   const T* tag = nullptr;
-  float sum[FN], cnt = 0.f;
-#pragma unroll
-  for (int fn = 0; fn < FN; ++fn) sum[fn] = 0.f;
+  // Branch-free: invalid rows contribute zero (their weight vm is 0).
+  float vm[FM][4], q[FM][FN][4];
+  float cnt = 0.f;
 #pragma unroll
   for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      if (!valid(fm, j)) continue;
-      cnt += 1.f;
+      vm[fm][j] = valid(fm, j) ? 1.f : 0.f;
+      cnt += vm[fm][j];
 #pragma unroll
-      for (int fn = 0; fn < FN; ++fn) sum[fn] += quant(acc[fm][fn][j], tag);
+      for (int fn = 0; fn < FN; ++fn) q[fm][fn][j] = vm[fm][j] * quant(acc[fm][fn][j], tag);
     }
+  float sum[FN];
+#pragma unroll
+  for (int fn = 0; fn < FN; ++fn) {
+    float t = 0.f;
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) t += q[fm][fn][j];
+    sum[fn] = t;
+  }
   cnt = sum_lane_groups(cnt);
 #pragma unroll
   for (int fn = 0; fn < FN; ++fn) {
@@ -94,7 +152,7 @@ __device__ void tile_stats(const f32x4_t (&acc)[FM][FN], Valid valid, int wm, in
     }
   }
   __syncthreads();
-  float mean[FN], m2[FN];
+  float m2[FN];
 #pragma unroll
   for (int fn = 0; fn < FN; ++fn) {
     const int cl = wn * TN + fn * 16 + lr;
@@ -104,23 +162,16 @@ __device__ void tile_stats(const f32x4_t (&acc)[FM][FN], Valid valid, int wm, in
       S += red[w][0][cl];
       N += red[w][1][cl];
     }
-    mean[fn] = N > 0.f ? S / N : 0.f;
-    m2[fn] = 0.f;
-  }
+    const float mean = N > 0.f ? S / N : 0.f;
+    float t = 0.f;
 #pragma unroll
-  for (int fm = 0; fm < FM; ++fm)
+    for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      if (!valid(fm, j)) continue;
-#pragma unroll
-      for (int fn = 0; fn < FN; ++fn) {
-        const float d = quant(acc[fm][fn][j], tag) - mean[fn];
-        m2[fn] += d * d;
+      for (int j = 0; j < 4; ++j) {
+        const float d = q[fm][fn][j] - mean;
+        t += vm[fm][j] * (d * d);
       }
-    }
-#pragma unroll
-  for (int fn = 0; fn < FN; ++fn) {
-    m2[fn] = sum_lane_groups(m2[fn]);
+    m2[fn] = sum_lane_groups(t);
     if (lg == 0) red[wm][2][wn * TN + fn * 16 + lr] = m2[fn];
   }
   __syncthreads();
@@ -142,9 +193,14 @@ __device__ void tile_stats(const f32x4_t (&acc)[FM][FN], Valid valid, int wm, in
 
 }  // namespace
 
+// Epilogue slice in LDS: column-major, 16 rows + 4 pad per column, so every
+// lane writes its four accumulator rows with one aligned 16-byte store
+// (conflict-free across the 16 lanes of a store pass).
+constexpr int EP_RP = 20;
+
 // One workgroup = 4 waves computing a BM x BN output tile; the waves form a
 // WAVES_M x (4 / WAVES_M) grid, each owning FM x FN 16x16 MFMA tiles.
-template <typename T, int BM, int BN, int WAVES_M, int EP, bool PRO>
+template <typename T, int BM, int BN, int WAVES_M, int EP, int PRO>
 __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
   constexpr int WAVES_N = 4 / WAVES_M;
   constexpr int TM = BM / WAVES_M, TN = BN / WAVES_N;
@@ -222,6 +278,10 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
       if (cvalid) {
         e_scale = a.ep_scale[col];
         e_shift = a.ep_shift[col];
+      }
+    }
+    if constexpr (EP == EP_MASK || EP == EP_RESID_STATS) {
+      if (cvalid) {
         e_mean = a.ep_mean[col];
         e_rstd = a.ep_rstd[col];
       }
@@ -246,6 +306,12 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
         } else {
           const float rv = a.resid != nullptr ? load1(static_cast<const T*>(a.resid) + idx) : 0.f;
           store1(out + idx, rv + v);
+          if constexpr (EP == EP_RESID_STATS) {
+            const float g = quant(rv + v, out);
+            const float hl = load1(static_cast<const T*>(a.ep_h) + idx);
+            s1[fn] += g;
+            s2[fn] += g * ((hl - e_mean) * e_rstd);
+          }
         }
       }
     }
@@ -256,7 +322,7 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
         acc, [&](int fm, int j) { return row_base + fm * 16 + lg * 4 + j < a.m; }, wm, wn, lane,
         blockIdx.y * BN, a.c_out, a.partials, blockIdx.x);
   }
-  if constexpr (EP == EP_MASK) {
+  if constexpr (EP == EP_MASK || EP == EP_RESID_STATS) {
     __shared__ float red[WAVES_M][2][BN];
 #pragma unroll
     for (int fn = 0; fn < FN; ++fn) {
@@ -287,7 +353,7 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
 // LDS stage, and the 4 waves feed MFMA from LDS.  The epilogue goes through LDS
 // one 16-row slice per wave at a time so that every lane stores 16 contiguous
 // bytes of one output row.
-template <int BM, int BN, int WAVES_M, int EP, bool PRO>
+template <int BM, int BN, int WAVES_M, int EP, int PRO>
 __global__ __launch_bounds__(256) void conv_staged_kernel(ConvArgs a) {
   using T = bf16_t;
   constexpr int WAVES_N = 4 / WAVES_M;
@@ -296,13 +362,12 @@ __global__ __launch_bounds__(256) void conv_staged_kernel(ConvArgs a) {
   constexpr int PITCH = 40;                  // bf16 per LDS row: 32 k + 8 pad (80 B)
   constexpr int A_CHUNKS = BM * 4 / 256;     // 16-byte A chunks per thread and step
   constexpr int B_CHUNKS = (BN * 4 + 255) / 256;  // 16-byte B chunks per thread and step
-  constexpr int EPITCH = TN + 4;             // fp32 per LDS row of the epilogue slice
   static_assert(BM * 4 % 256 == 0, "tile");
   constexpr int STAGE_ELEMS = (BM + BN) * PITCH;
-  constexpr int EPI_FLOATS = 4 * 16 * EPITCH;
+  constexpr int EPI_FLOATS = 4 * TN * EP_RP;
   constexpr int LDS_BYTES = (2 * STAGE_ELEMS * 2 > EPI_FLOATS * 4) ? 2 * STAGE_ELEMS * 2 : EPI_FLOATS * 4;
   __shared__ __attribute__((aligned(16))) unsigned char lds[LDS_BYTES];
-  __shared__ float pro_tab[2][512];
+  __shared__ float pro_tab[PRO == PRO_BWD ? 4 : 2][512];
   __shared__ float red[WAVES_M][2][BN];
 
   T* stage_base = reinterpret_cast<T*>(lds);
@@ -316,10 +381,17 @@ __global__ __launch_bounds__(256) void conv_staged_kernel(ConvArgs a) {
   const int csteps = a.c_in / 32;
   const int steps = a.r * a.s * csteps;
 
-  if constexpr (PRO) {
+  if constexpr (PRO == PRO_RELU) {
     for (int i = tid; i < a.c_in; i += 256) {
       pro_tab[0][i] = a.pro_scale[i];
       pro_tab[1][i] = a.pro_shift[i];
+    }
+  } else if constexpr (PRO == PRO_BWD) {
+    for (int i = tid; i < a.c_in; i += 256) {
+      pro_tab[0][i] = a.pro_ca[i];
+      pro_tab[1][i] = a.pro_cb[i];
+      pro_tab[2][i] = a.pro_cc[i];
+      pro_tab[3][i] = a.pro_mean[i];
     }
   }
 
@@ -355,7 +427,8 @@ __global__ __launch_bounds__(256) void conv_staged_kernel(ConvArgs a) {
   }
   const T* wt = static_cast<const T*>(a.wt);
   const T* src = static_cast<const T*>(a.src);
-  if constexpr (PRO) __syncthreads();
+  const T* proh = static_cast<const T*>(a.pro_h);
+  if constexpr (PRO != PRO_NONE) __syncthreads();
 
   Raw8<T> ra[A_CHUNKS], rb[B_CHUNKS];
   auto load_step = [&](int step) {
@@ -367,14 +440,12 @@ __global__ __launch_bounds__(256) void conv_staged_kernel(ConvArgs a) {
       const int ih = a_ih0[i] + fr, iw = a_iw0[i] + fs;
       const int c = c0 + a_sub[i] * 8;
       if (a_ok[i] && ih >= 0 && ih < a.h && iw >= 0 && iw < a.w) {
-        ra[i].load(src + (a_pix0[i] + static_cast<long>(ih) * a.w + iw) * a.c_in + c);
-        if constexpr (PRO) {
-          float v[8];
-          ra[i].to_f32(v);
-#pragma unroll
-          for (int j = 0; j < 8; ++j) v[j] = fmaxf(fmaf(pro_tab[0][c + j], v[j], pro_tab[1][c + j]), 0.f);
-          ra[i].from_f32(v);
-        }
+        const long off = (a_pix0[i] + static_cast<long>(ih) * a.w + iw) * a.c_in + c;
+        ra[i].load(src + off);
+        Raw8<T> hr;
+        if constexpr (PRO == PRO_BWD) hr.load(proh + off);
+        pro8<T, PRO>(ra[i], hr, pro_tab[0], pro_tab[1], pro_tab[PRO == PRO_BWD ? 2 : 0],
+                     pro_tab[PRO == PRO_BWD ? 3 : 0], c);
       } else {
         ra[i].zero();
       }
@@ -433,9 +504,10 @@ __global__ __launch_bounds__(256) void conv_staged_kernel(ConvArgs a) {
         acc, [&](int fm, int j) { return m0 + wm * TM + fm * 16 + lg * 4 + j < a.m; }, wm, wn,
         lane, n0, a.c_out, a.partials, blockIdx.x);
   }
-  // Epilogue: per 16-row slice, stage fp32 results of each wave in LDS, then
-  // each lane handles 8 consecutive columns of one row.
-  float* ep = reinterpret_cast<float*>(lds) + wave * 16 * EPITCH;
+  // Epilogue: per 16-row slice, stage fp32 results of each wave in LDS
+  // (column-major, one 16-byte store per fragment), then each lane handles 8
+  // consecutive columns of one row.
+  float* ep = reinterpret_cast<float*>(lds) + wave * TN * EP_RP;
   constexpr int CG = TN / 8;                  // column groups per slice row
   constexpr int TASKS = 16 * CG;              // (row, group) tasks per slice
   const int my_cg = lane % CG;
@@ -445,11 +517,11 @@ __global__ __launch_bounds__(256) void conv_staged_kernel(ConvArgs a) {
 #pragma unroll
   for (int j = 0; j < 8; ++j) s1[j] = s2[j] = 0.f;
   float es[8], esh[8], emu[8], ers[8];
-  if constexpr (EP == EP_MASK) {
+  if constexpr (EP == EP_MASK || EP == EP_RESID_STATS) {
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      es[j] = cvalid ? a.ep_scale[col + j] : 0.f;
-      esh[j] = cvalid ? a.ep_shift[col + j] : 0.f;
+      es[j] = cvalid && EP == EP_MASK ? a.ep_scale[col + j] : 0.f;
+      esh[j] = cvalid && EP == EP_MASK ? a.ep_shift[col + j] : 0.f;
       emu[j] = cvalid ? a.ep_mean[col + j] : 0.f;
       ers[j] = cvalid ? a.ep_rstd[col + j] : 0.f;
     }
@@ -459,8 +531,7 @@ __global__ __launch_bounds__(256) void conv_staged_kernel(ConvArgs a) {
   for (int fm = 0; fm < FM; ++fm) {
 #pragma unroll
     for (int fn = 0; fn < FN; ++fn)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) ep[(lg * 4 + j) * EPITCH + fn * 16 + lr] = acc[fm][fn][j];
+      *reinterpret_cast<f32x4_t*>(ep + (fn * 16 + lr) * EP_RP + lg * 4) = acc[fm][fn];
     __syncthreads();
     for (int t = lane; t < TASKS; t += 64) {
       const int rr = t / CG;
@@ -468,7 +539,7 @@ __global__ __launch_bounds__(256) void conv_staged_kernel(ConvArgs a) {
       if (!(cvalid && row < a.m)) continue;
       float v[8];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) v[j] = ep[rr * EPITCH + my_cg * 8 + j];
+      for (int j = 0; j < 8; ++j) v[j] = ep[(my_cg * 8 + j) * EP_RP + rr];
       const long idx = static_cast<long>(row) * a.c_out + col;
       Raw8<T> o;
       if constexpr (EP == EP_STATS) {
@@ -497,12 +568,24 @@ __global__ __launch_bounds__(256) void conv_staged_kernel(ConvArgs a) {
           for (int j = 0; j < 8; ++j) v[j] += rv[j];
         }
         o.from_f32(v);
+        if constexpr (EP == EP_RESID_STATS) {  // BN-backward partials of the stored values
+          Raw8<T> hr;
+          hr.load(static_cast<const T*>(a.ep_h) + idx);
+          float hl[8];
+          hr.to_f32(hl);
+          o.to_f32(v);
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            s1[j] += v[j];
+            s2[j] += v[j] * ((hl[j] - emu[j]) * ers[j]);
+          }
+        }
       }
       *reinterpret_cast<uint4*>(out + idx) = make_uint4(o.w[0], o.w[1], o.w[2], o.w[3]);
     }
     __syncthreads();
   }
-  if constexpr (EP == EP_MASK) {
+  if constexpr (EP == EP_MASK || EP == EP_RESID_STATS) {
     // lanes with the same column group: lane % CG equal -> xor over the higher lane bits
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
@@ -539,7 +622,9 @@ __global__ __launch_bounds__(256) void conv_staged_kernel(ConvArgs a) {
 // 32-channel weight slab of each (chunk, tap) step streams through a double
 // buffer.  The next chunk's patch and the next slab are fetched into registers
 // one step ahead.  HB = number of patch buffers (1 when there is one chunk).
-template <int TH, int TW, int BN, int WAVES_M, int HB, int EP, bool PRO>
+// FB (C_in == 32, a single chunk): all nine slabs are staged with the patch up
+// front, so the nine taps run from LDS behind a single barrier.
+template <int TH, int TW, int BN, int WAVES_M, int HB, int EP, int PRO, bool FB>
 __global__ __launch_bounds__(256) void conv_halo_kernel(ConvArgs a) {
   using T = bf16_t;
   constexpr int BM = TH * TW;
@@ -549,17 +634,18 @@ __global__ __launch_bounds__(256) void conv_halo_kernel(ConvArgs a) {
   static_assert(TM % 16 == 0 && TN % 16 == 0, "tile");
   constexpr int HTH = TH + 2, HTW = TW + 2, HPIX = HTH * HTW;
   constexpr int HP = 40;                              // bf16 per patch pixel (32 + pad)
+  static_assert(!FB || HB == 1, "a single chunk has one patch buffer");
+  constexpr int NSLAB = FB ? 9 : 2;
   constexpr int H_CHUNKS = (HPIX * 4 + 255) / 256;    // 16-byte patch chunks per thread
-  constexpr int B_CHUNKS = (BN * 4 + 255) / 256;
+  constexpr int B_CHUNKS = ((FB ? 9 : 1) * BN * 4 + 255) / 256;
   constexpr int BPITCH = 40;
   constexpr int PATCH = HPIX * HP;
   constexpr int SLAB = BN * BPITCH;
-  constexpr int EPITCH = TN + 4;
-  constexpr int MAIN_BYTES = (HB * PATCH + 2 * SLAB) * 2;
-  constexpr int EPI_BYTES = 4 * 16 * EPITCH * 4;
+  constexpr int MAIN_BYTES = (HB * PATCH + NSLAB * SLAB) * 2;
+  constexpr int EPI_BYTES = 4 * TN * EP_RP * 4;
   constexpr int LDS_BYTES = MAIN_BYTES > EPI_BYTES ? MAIN_BYTES : EPI_BYTES;
   __shared__ __attribute__((aligned(16))) unsigned char lds[LDS_BYTES];
-  __shared__ float pro_tab[2][512];
+  __shared__ float pro_tab[PRO == PRO_BWD ? 4 : 2][512];
   __shared__ float red[WAVES_M][2][BN];
 
   T* patch_base = reinterpret_cast<T*>(lds);
@@ -580,17 +666,13 @@ __global__ __launch_bounds__(256) void conv_halo_kernel(ConvArgs a) {
   const T* wt = static_cast<const T*>(a.wt);
   const long img_base = static_cast<long>(img) * a.h * a.w;
 
-  if constexpr (PRO) {
-    for (int i = tid; i < a.c_in; i += 256) {
-      pro_tab[0][i] = a.pro_scale[i];
-      pro_tab[1][i] = a.pro_shift[i];
-    }
-    __syncthreads();
-  }
-
+  const T* proh = static_cast<const T*>(a.pro_h);
   Raw8<T> rh[H_CHUNKS], rb[B_CHUNKS];
+  Raw8<T> rhh[PRO == PRO_BWD ? H_CHUNKS : 1];   // pro_h at the patch positions
+  uint32_t hvalid = 0;   // bit i: patch chunk i lies inside the image
   auto load_patch = [&](int chunk) {
     const int c0 = chunk * 32;
+    hvalid = 0;
 #pragma unroll
     for (int i = 0; i < H_CHUNKS; ++i) {
       const int q = tid + 256 * i;
@@ -598,17 +680,24 @@ __global__ __launch_bounds__(256) void conv_halo_kernel(ConvArgs a) {
       const int hy = hp / HTW, hx = hp - hy * HTW;
       const int ih = p0 - 1 + hy, iw = q0 - 1 + hx;
       if (hp < HPIX && ih >= 0 && ih < a.h && iw >= 0 && iw < a.w) {
-        const int c = c0 + sub * 8;
-        rh[i].load(src + (img_base + static_cast<long>(ih) * a.w + iw) * a.c_in + c);
-        if constexpr (PRO) {
-          float v[8];
-          rh[i].to_f32(v);
-#pragma unroll
-          for (int j = 0; j < 8; ++j) v[j] = fmaxf(fmaf(pro_tab[0][c + j], v[j], pro_tab[1][c + j]), 0.f);
-          rh[i].from_f32(v);
-        }
+        const long off = (img_base + static_cast<long>(ih) * a.w + iw) * a.c_in + c0 + sub * 8;
+        rh[i].load(src + off);
+        if constexpr (PRO == PRO_BWD) rhh[i].load(proh + off);
+        hvalid |= 1u << i;
       } else {
         rh[i].zero();
+      }
+    }
+  };
+  // Prologue on the loaded patch (padding stays zero).
+  auto pro_patch = [&](int chunk) {
+    if constexpr (PRO != PRO_NONE) {
+#pragma unroll
+      for (int i = 0; i < H_CHUNKS; ++i) {
+        if (!(hvalid & (1u << i))) continue;
+        const int c = chunk * 32 + ((tid + 256 * i) & 3) * 8;
+        pro8<T, PRO>(rh[i], rhh[PRO == PRO_BWD ? i : 0], pro_tab[0], pro_tab[1],
+                     pro_tab[PRO == PRO_BWD ? 2 : 0], pro_tab[PRO == PRO_BWD ? 3 : 0], c);
       }
     }
   };
@@ -622,25 +711,30 @@ __global__ __launch_bounds__(256) void conv_halo_kernel(ConvArgs a) {
         *reinterpret_cast<uint4*>(dst + hp * HP + sub * 8) = make_uint4(rh[i].w[0], rh[i].w[1], rh[i].w[2], rh[i].w[3]);
     }
   };
+  // One (chunk, tap) slab, or with FB all nine taps of chunk 0 (slab t = tap t).
   auto load_slab = [&](int step) {
-    const int chunk = step / 9, tap = step - chunk * 9;
+    const int chunk = step / 9, tap0 = step - chunk * 9;
 #pragma unroll
     for (int i = 0; i < B_CHUNKS; ++i) {
       const int q = tid + 256 * i;
-      const int col = q >> 2, sub = q & 3;
-      if (q < BN * 4 && n0 + col < a.c_out)
+      const int tap = FB ? q / (BN * 4) : tap0;
+      const int rem = FB ? q - (q / (BN * 4)) * (BN * 4) : q;
+      const int col = rem >> 2, sub = rem & 3;
+      if (q < (FB ? 9 : 1) * BN * 4 && n0 + col < a.c_out)
         rb[i].load(wt + static_cast<long>(n0 + col) * a.k_tot + tap * a.c_in + chunk * 32 + sub * 8);
       else
         rb[i].zero();
     }
   };
   auto park_slab = [&](int buf) {
-    T* dst = slab_base + buf * SLAB;
 #pragma unroll
     for (int i = 0; i < B_CHUNKS; ++i) {
       const int q = tid + 256 * i;
-      if (q < BN * 4)
-        *reinterpret_cast<uint4*>(dst + (q >> 2) * BPITCH + (q & 3) * 8) = make_uint4(rb[i].w[0], rb[i].w[1], rb[i].w[2], rb[i].w[3]);
+      if (q >= (FB ? 9 : 1) * BN * 4) continue;
+      const int tap = FB ? q / (BN * 4) : 0;
+      const int rem = q - tap * (BN * 4);
+      T* dst = slab_base + (FB ? tap : buf) * SLAB;
+      *reinterpret_cast<uint4*>(dst + (rem >> 2) * BPITCH + (rem & 3) * 8) = make_uint4(rb[i].w[0], rb[i].w[1], rb[i].w[2], rb[i].w[3]);
     }
   };
 
@@ -659,12 +753,47 @@ __global__ __launch_bounds__(256) void conv_halo_kernel(ConvArgs a) {
 #pragma unroll
     for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
+  // Operand loads go out first; the prologue table is fetched while they fly.
   load_patch(0);
   load_slab(0);
+  if constexpr (PRO == PRO_RELU) {
+    for (int i = tid; i < a.c_in; i += 256) {
+      pro_tab[0][i] = a.pro_scale[i];
+      pro_tab[1][i] = a.pro_shift[i];
+    }
+    __syncthreads();
+  } else if constexpr (PRO == PRO_BWD) {
+    for (int i = tid; i < a.c_in; i += 256) {
+      pro_tab[0][i] = a.pro_ca[i];
+      pro_tab[1][i] = a.pro_cb[i];
+      pro_tab[2][i] = a.pro_cc[i];
+      pro_tab[3][i] = a.pro_mean[i];
+    }
+    __syncthreads();
+  }
+  pro_patch(0);
   park_patch(0);
   park_slab(0);
   __syncthreads();
-  for (int step = 0; step < steps; ++step) {
+  if constexpr (FB) {
+#pragma unroll
+    for (int tap = 0; tap < 9; ++tap) {
+      const int fr = tap / 3, fs = tap - fr * 3;
+      const int toff = fr * HTW + fs;
+      const T* sb = slab_base + tap * SLAB;
+      Frag<T> af[FM], bfr[FN];
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm) af[fm].load(patch_base + (rowpix[fm] + toff) * HP + lg * 8);
+#pragma unroll
+      for (int fn = 0; fn < FN; ++fn) bfr[fn].load(sb + (wn * TN + fn * 16 + lr) * BPITCH + lg * 8);
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+        for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma(af[fm], bfr[fn], acc[fm][fn]);
+    }
+    __syncthreads();   // the epilogue reuses the operand LDS
+  }
+  for (int step = 0; step < (FB ? 0 : steps); ++step) {
     const int chunk = step / 9, tap = step - chunk * 9;
     const bool next_patch = HB > 1 && tap == 0 && chunk + 1 < chunks;
     if (step + 1 < steps) load_slab(step + 1);
@@ -683,7 +812,10 @@ __global__ __launch_bounds__(256) void conv_halo_kernel(ConvArgs a) {
 #pragma unroll
       for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma(af[fm], bfr[fn], acc[fm][fn]);
     if (step + 1 < steps) park_slab((step + 1) & 1);
-    if (next_patch) park_patch((chunk + 1) & 1);
+    if (next_patch) {
+      pro_patch(chunk + 1);
+      park_patch((chunk + 1) & 1);
+    }
     __syncthreads();
   }
 
@@ -698,7 +830,7 @@ __global__ __launch_bounds__(256) void conv_halo_kernel(ConvArgs a) {
         wm, wn, lane, n0, a.c_out, a.partials, blockIdx.x);
   }
   // Epilogue (as in the staged kernel, pixels mapped back to NHWC rows).
-  float* ep = reinterpret_cast<float*>(lds) + wave * 16 * EPITCH;
+  float* ep = reinterpret_cast<float*>(lds) + wave * TN * EP_RP;
   constexpr int CG = TN / 8;
   constexpr int TASKS = 16 * CG;
   const int my_cg = lane % CG;
@@ -708,11 +840,11 @@ __global__ __launch_bounds__(256) void conv_halo_kernel(ConvArgs a) {
 #pragma unroll
   for (int j = 0; j < 8; ++j) s1[j] = s2[j] = 0.f;
   float es[8], esh[8], emu[8], ers[8];
-  if constexpr (EP == EP_MASK) {
+  if constexpr (EP == EP_MASK || EP == EP_RESID_STATS) {
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      es[j] = cvalid ? a.ep_scale[col + j] : 0.f;
-      esh[j] = cvalid ? a.ep_shift[col + j] : 0.f;
+      es[j] = cvalid && EP == EP_MASK ? a.ep_scale[col + j] : 0.f;
+      esh[j] = cvalid && EP == EP_MASK ? a.ep_shift[col + j] : 0.f;
       emu[j] = cvalid ? a.ep_mean[col + j] : 0.f;
       ers[j] = cvalid ? a.ep_rstd[col + j] : 0.f;
     }
@@ -722,8 +854,7 @@ __global__ __launch_bounds__(256) void conv_halo_kernel(ConvArgs a) {
   for (int fm = 0; fm < FM; ++fm) {
 #pragma unroll
     for (int fn = 0; fn < FN; ++fn)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) ep[(lg * 4 + j) * EPITCH + fn * 16 + lr] = acc[fm][fn][j];
+      *reinterpret_cast<f32x4_t*>(ep + (fn * 16 + lr) * EP_RP + lg * 4) = acc[fm][fn];
     __syncthreads();
     for (int t = lane; t < TASKS; t += 64) {
       const int rr = t / CG;
@@ -733,7 +864,7 @@ __global__ __launch_bounds__(256) void conv_halo_kernel(ConvArgs a) {
       if (!(cvalid && pp < a.h && qq < a.w)) continue;
       float v[8];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) v[j] = ep[rr * EPITCH + my_cg * 8 + j];
+      for (int j = 0; j < 8; ++j) v[j] = ep[(my_cg * 8 + j) * EP_RP + rr];
       const long idx = (img_base + static_cast<long>(pp) * a.w + qq) * a.c_out + col;
       Raw8<T> o;
       if constexpr (EP == EP_STATS) {
@@ -762,12 +893,24 @@ __global__ __launch_bounds__(256) void conv_halo_kernel(ConvArgs a) {
           for (int j = 0; j < 8; ++j) v[j] += rv[j];
         }
         o.from_f32(v);
+        if constexpr (EP == EP_RESID_STATS) {  // BN-backward partials of the stored values
+          Raw8<T> hr;
+          hr.load(static_cast<const T*>(a.ep_h) + idx);
+          float hl[8];
+          hr.to_f32(hl);
+          o.to_f32(v);
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            s1[j] += v[j];
+            s2[j] += v[j] * ((hl[j] - emu[j]) * ers[j]);
+          }
+        }
       }
       *reinterpret_cast<uint4*>(out + idx) = make_uint4(o.w[0], o.w[1], o.w[2], o.w[3]);
     }
     __syncthreads();
   }
-  if constexpr (EP == EP_MASK) {
+  if constexpr (EP == EP_MASK || EP == EP_RESID_STATS) {
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       for (int off = CG; off < 64; off <<= 1) {
@@ -833,20 +976,25 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a) {
 #pragma unroll
     for (int j = 0; j < FK; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  ConvArgs ca;  // reuse the gather helper
+  ConvArgs ca{};  // reuse the gather helper
   ca.src = a.src; ca.src2 = a.src2; ca.c_split = a.c_split;
   ca.pro_scale = a.pro_scale; ca.pro_shift = a.pro_shift;
   ca.h = a.h; ca.w = a.w; ca.c_in = a.c_in; ca.stride = a.stride; ca.pad = a.pad;
+  const bool dhb = a.dh_h != nullptr;
+  float dk[4][8];
+  dh_coeffs(a, o0 + a_og * 8, dk);
 
   for (int mb = m_begin; mb < m_end; mb += 32) {
     if (a_active) {
       const int m = mb + a_row;
       const int o = o0 + a_og * 8;
       Raw8<T> r;
-      if (m < m_end && o < a.c_out)
+      if (m < m_end && o < a.c_out) {
         r.load(dh + static_cast<long>(m) * a.c_out + o);
-      else
+        if (dhb) dh_bwd8(r, static_cast<const T*>(a.dh_h) + static_cast<long>(m) * a.c_out + o, dk);
+      } else {
         r.zero();
+      }
 #pragma unroll
       for (int j = 0; j < 8; ++j) r.put(j, &sA[(a_og * 8 + j) * PITCH + a_row]);
     }
@@ -860,7 +1008,7 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a) {
       rp.p = rem / a.q;
       rp.q = rem - rp.p * a.q;
       Raw8<T> r;
-      gather_a<T, PRO>(ca, rp, kb_valid, fr, fs, cb, r);
+      gather_a<T, PRO ? PRO_RELU : PRO_NONE>(ca, rp, kb_valid, fr, fs, cb, r);
 #pragma unroll
       for (int j = 0; j < 8; ++j) r.put(j, &sB[(b_kg * 8 + j) * PITCH + b_row]);
     }
@@ -932,10 +1080,13 @@ __global__ __launch_bounds__(256) void wgrad_staged_kernel(WgradArgs a) {
   const int cb = kbb - tap * a.c_in;
   const int fr = tap / a.s, fs = tap - fr * a.s;
 
-  ConvArgs ca;
+  ConvArgs ca{};
   ca.src = a.src; ca.src2 = a.src2; ca.c_split = a.c_split;
   ca.pro_scale = a.pro_scale; ca.pro_shift = a.pro_shift;
   ca.h = a.h; ca.w = a.w; ca.c_in = a.c_in; ca.stride = a.stride; ca.pad = a.pad;
+  const bool dhb = a.dh_h != nullptr;
+  float dk[4][8];
+  dh_coeffs(a, a_o, dk);
 
   Raw8<T> ra[2], rb[2];
   auto load_step = [&](int step) {
@@ -943,8 +1094,12 @@ __global__ __launch_bounds__(256) void wgrad_staged_kernel(WgradArgs a) {
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
       const int m = mb + 2 * a_pair + e;
-      if (a_ook && m < m_end) ra[e].load(dh + static_cast<long>(m) * a.c_out + a_o);
-      else ra[e].zero();
+      if (a_ook && m < m_end) {
+        ra[e].load(dh + static_cast<long>(m) * a.c_out + a_o);
+        if (dhb) dh_bwd8(ra[e], static_cast<const T*>(a.dh_h) + static_cast<long>(m) * a.c_out + a_o, dk);
+      } else {
+        ra[e].zero();
+      }
       const int mm = mb + 2 * b_pair + e;
       RowPos rp;
       rp.valid = b_on && mm < m_end;
@@ -953,7 +1108,7 @@ __global__ __launch_bounds__(256) void wgrad_staged_kernel(WgradArgs a) {
       const int rem = m2 - rp.n * pq;
       rp.p = rem / a.q;
       rp.q = rem - rp.p * a.q;
-      gather_a<T, PRO>(ca, rp, kb_ok, fr, fs, cb, rb[e]);
+      gather_a<T, PRO ? PRO_RELU : PRO_NONE>(ca, rp, kb_ok, fr, fs, cb, rb[e]);
     }
   };
   auto pair_word = [](const Raw8<T>& lo, const Raw8<T>& hi, int j) -> uint32_t {
@@ -1035,7 +1190,7 @@ template <int TH, int TW, int BO, bool PRO>
 __global__ __launch_bounds__(256) void wgrad_halo_kernel(WgradArgs a) {
   using T = bf16_t;
   constexpr int NPIX = TH * TW;
-  static_assert(NPIX % 32 == 0 && TW % 8 == 0, "tile");
+  static_assert(NPIX % 32 == 0 && TW % 8 == 0 && 256 % (BO / 8) == 0, "tile");
   constexpr int HTH = TH + 2, HTW = TW + 2, HPIX = HTH * HTW;
   constexpr int HROW = HTH * TW + 8;        // bf16 per channel row of one shifted copy
   constexpr int DROW = NPIX + 8;            // bf16 per output-channel row of dh^T
@@ -1069,6 +1224,9 @@ __global__ __launch_bounds__(256) void wgrad_halo_kernel(WgradArgs a) {
     __syncthreads();
   }
 
+  const bool dhb = a.dh_h != nullptr;
+  float dk[4][8];
+  dh_coeffs(a, o0 + (tid % (BO / 8)) * 8, dk);   // this thread's output-channel group is fixed
   Raw8<T> rh[H_CHUNKS], rd[D_CHUNKS];
   auto tile_origin = [&](int t, int& img, int& p0, int& q0) {
     const int tx = t % tiles_x;
@@ -1107,10 +1265,13 @@ __global__ __launch_bounds__(256) void wgrad_halo_kernel(WgradArgs a) {
       const int pix = q / (BO / 8), og = q % (BO / 8);
       const int ph = pix / TW, pw = pix - ph * TW;
       const int pp = p0 + ph, qq = q0 + pw;
-      if (pix < NPIX && pp < a.h && qq < a.w && o0 + og * 8 < a.c_out)
-        rd[i].load(dh + (base + static_cast<long>(pp) * a.w + qq) * a.c_out + o0 + og * 8);
-      else
+      if (pix < NPIX && pp < a.h && qq < a.w && o0 + og * 8 < a.c_out) {
+        const long off = (base + static_cast<long>(pp) * a.w + qq) * a.c_out + o0 + og * 8;
+        rd[i].load(dh + off);
+        if (dhb) dh_bwd8(rd[i], static_cast<const T*>(a.dh_h) + off, dk);
+      } else {
         rd[i].zero();
+      }
     }
   };
   auto park_tile = [&]() {
@@ -1216,39 +1377,72 @@ __global__ __launch_bounds__(256) void wgrad_reduce_kernel(const float* __restri
 
 namespace {
 
-template <typename T, int BN, int WM, int EP, bool PRO>
-void launch_gemm(const ConvArgs& a, hipStream_t st) {
+// Supported (epilogue, prologue) pairs: statistics with no prologue or BN-apply
+// + ReLU (forward convs); every gradient epilogue with no prologue or the BN
+// backward prologue (input-gradient convs).  f receives both as constants.
+template <int E, int P> struct EpPro {
+  static constexpr int ep = E, pro = P;
+};
+
+template <typename F>
+bool dispatch_ep_pro(int ep, int pro, F&& f) {
+  if (ep == EP_STATS) {
+    if (pro == PRO_NONE) { f(EpPro<EP_STATS, PRO_NONE>{}); return true; }
+    if (pro == PRO_RELU) { f(EpPro<EP_STATS, PRO_RELU>{}); return true; }
+    return false;
+  }
+  if (pro == PRO_RELU) return false;
+  const bool bwd = pro == PRO_BWD;
+  if (ep == EP_MASK) {
+    if (bwd) f(EpPro<EP_MASK, PRO_BWD>{}); else f(EpPro<EP_MASK, PRO_NONE>{});
+    return true;
+  }
+  if (ep == EP_RESID) {
+    if (bwd) f(EpPro<EP_RESID, PRO_BWD>{}); else f(EpPro<EP_RESID, PRO_NONE>{});
+    return true;
+  }
+  if (ep == EP_RESID_STATS) {
+    if (bwd) f(EpPro<EP_RESID_STATS, PRO_BWD>{}); else f(EpPro<EP_RESID_STATS, PRO_NONE>{});
+    return true;
+  }
+  return false;
+}
+
+int pro_mode(const ConvArgs& a) {
+  return a.pro_h != nullptr ? PRO_BWD : (a.pro_scale != nullptr ? PRO_RELU : PRO_NONE);
+}
+
+template <typename T, int BN, int WM>
+bool launch_gemm(const ConvArgs& a, int ep, hipStream_t st) {
   constexpr int BM = 128;
   dim3 grid((a.m + BM - 1) / BM, (a.c_out + BN - 1) / BN);
-  hipLaunchKernelGGL((conv_gemm_kernel<T, BM, BN, WM, EP, PRO>), grid, dim3(256), 0, st, a);
+  return dispatch_ep_pro(ep, pro_mode(a), [&](auto k) {
+    hipLaunchKernelGGL((conv_gemm_kernel<T, BM, BN, WM, decltype(k)::ep, decltype(k)::pro>), grid,
+                       dim3(256), 0, st, a);
+  });
 }
 
-template <typename T, int EP, bool PRO>
-void launch_gemm_tiles(const ConvArgs& a, hipStream_t st) {
-  if (a.c_out <= 16)
-    launch_gemm<T, 16, 4, EP, PRO>(a, st);
-  else if (a.c_out <= 32)
-    launch_gemm<T, 32, 4, EP, PRO>(a, st);
-  else if (a.c_out <= 64)
-    launch_gemm<T, 64, 2, EP, PRO>(a, st);
-  else
-    launch_gemm<T, 128, 2, EP, PRO>(a, st);
+template <typename T>
+bool conv_gemm_t(const ConvArgs& a, int ep, hipStream_t st) {
+  if (a.c_out <= 16) return launch_gemm<T, 16, 4>(a, ep, st);
+  if (a.c_out <= 32) return launch_gemm<T, 32, 4>(a, ep, st);
+  if (a.c_out <= 64) return launch_gemm<T, 64, 2>(a, ep, st);
+  return launch_gemm<T, 128, 2>(a, ep, st);
 }
 
-template <int BM, int BN, int WM, int EP, bool PRO>
-void launch_staged(const ConvArgs& a, hipStream_t st) {
+template <int BM, int BN, int WM>
+bool launch_staged(const ConvArgs& a, int ep, hipStream_t st) {
   dim3 grid((a.m + BM - 1) / BM, (a.c_out + BN - 1) / BN);
-  hipLaunchKernelGGL((conv_staged_kernel<BM, BN, WM, EP, PRO>), grid, dim3(256), 0, st, a);
+  return dispatch_ep_pro(ep, pro_mode(a), [&](auto k) {
+    hipLaunchKernelGGL((conv_staged_kernel<BM, BN, WM, decltype(k)::ep, decltype(k)::pro>), grid,
+                       dim3(256), 0, st, a);
+  });
 }
 
-template <int EP, bool PRO>
-void launch_staged_tiles(const ConvArgs& a, hipStream_t st) {
-  if (a.c_out <= 32)
-    launch_staged<256, 32, 4, EP, PRO>(a, st);
-  else if (a.c_out <= 64)
-    launch_staged<128, 64, 2, EP, PRO>(a, st);
-  else
-    launch_staged<128, 128, 2, EP, PRO>(a, st);
+bool launch_staged_tiles(const ConvArgs& a, int ep, hipStream_t st) {
+  if (a.c_out <= 32) return launch_staged<256, 32, 4>(a, ep, st);
+  if (a.c_out <= 64) return launch_staged<128, 64, 2>(a, ep, st);
+  return launch_staged<128, 128, 2>(a, ep, st);
 }
 
 // Halo-tile geometry for a 3x3 stride-1 bf16 conv, or tw = 0 when it does not apply.
@@ -1268,57 +1462,39 @@ HaloShape halo_shape(int dtype, const ConvArgs& a) {
   return z;
 }
 
-template <int TH, int TW, int BN, int WM, int HB>
-void launch_halo(const ConvArgs& a, int ep, hipStream_t st) {
+template <int TH, int TW, int BN, int WM, int HB, bool FB>
+bool launch_halo(const ConvArgs& a, int ep, hipStream_t st) {
   const int tiles = ((a.w + TW - 1) / TW) * ((a.h + TH - 1) / TH) * a.n;
   dim3 grid(tiles, (a.c_out + BN - 1) / BN);
-  const bool pro = a.pro_scale != nullptr;
-  if (ep == EP_STATS) {
-    if (pro)
-      hipLaunchKernelGGL((conv_halo_kernel<TH, TW, BN, WM, HB, EP_STATS, true>), grid, dim3(256), 0, st, a);
-    else
-      hipLaunchKernelGGL((conv_halo_kernel<TH, TW, BN, WM, HB, EP_STATS, false>), grid, dim3(256), 0, st, a);
-  } else if (ep == EP_MASK) {
-    hipLaunchKernelGGL((conv_halo_kernel<TH, TW, BN, WM, HB, EP_MASK, false>), grid, dim3(256), 0, st, a);
-  } else {
-    hipLaunchKernelGGL((conv_halo_kernel<TH, TW, BN, WM, HB, EP_RESID, false>), grid, dim3(256), 0, st, a);
-  }
+  return dispatch_ep_pro(ep, pro_mode(a), [&](auto k) {
+    hipLaunchKernelGGL((conv_halo_kernel<TH, TW, BN, WM, HB, decltype(k)::ep, decltype(k)::pro, FB>),
+                       grid, dim3(256), 0, st, a);
+  });
 }
 
-bool launch_halo_any(int dtype, const ConvArgs& a, int ep, hipStream_t st) {
+// Returns -1 when no halo kernel applies, else whether the launch was made.
+int launch_halo_any(int dtype, const ConvArgs& a, int ep, hipStream_t st) {
   const HaloShape h = halo_shape(dtype, a);
-  if (h.tw == 0) return false;
-  if (h.tw == 32) {
-    if (h.hb == 1) launch_halo<8, 32, 32, 4, 1>(a, ep, st);
-    else launch_halo<8, 32, 32, 4, 2>(a, ep, st);
-  } else if (h.tw == 16 && h.bn == 64) {
-    if (h.hb == 1) launch_halo<8, 16, 64, 2, 1>(a, ep, st);
-    else launch_halo<8, 16, 64, 2, 2>(a, ep, st);
-  } else if (h.tw == 16) {
-    if (h.hb == 1) launch_halo<8, 16, 128, 2, 1>(a, ep, st);
-    else launch_halo<8, 16, 128, 2, 2>(a, ep, st);
-  } else {
-    launch_halo<4, 56, 32, 2, 1>(a, ep, st);
-  }
-  return true;
+  if (h.tw == 0) return -1;
+  bool ok;
+  // a single 32-channel chunk (HB == 1) stages all nine weight slabs at once
+  if (h.tw == 32)
+    ok = h.hb == 1 ? launch_halo<8, 32, 32, 4, 1, true>(a, ep, st)
+                   : launch_halo<8, 32, 32, 4, 2, false>(a, ep, st);
+  else if (h.tw == 16 && h.bn == 64)
+    ok = h.hb == 1 ? launch_halo<8, 16, 64, 2, 1, true>(a, ep, st)
+                   : launch_halo<8, 16, 64, 2, 2, false>(a, ep, st);
+  else if (h.tw == 16)
+    ok = h.hb == 1 ? launch_halo<8, 16, 128, 2, 1, false>(a, ep, st)
+                   : launch_halo<8, 16, 128, 2, 2, false>(a, ep, st);
+  else
+    ok = launch_halo<4, 56, 32, 2, 1, true>(a, ep, st);
+  return ok ? 1 : 0;
 }
 
 bool use_staged(int dtype, const ConvArgs& a) {
   return dtype == DT_BF16 && a.src2 == nullptr && a.c_in % 32 == 0 && a.c_out % 8 == 0 &&
          a.c_in <= 512 && a.c_out >= 16;
-}
-
-template <typename T>
-void conv_gemm_t(const ConvArgs& a, int ep, hipStream_t st) {
-  const bool pro = a.pro_scale != nullptr;
-  if (ep == EP_STATS) {
-    if (pro) launch_gemm_tiles<T, EP_STATS, true>(a, st);
-    else launch_gemm_tiles<T, EP_STATS, false>(a, st);
-  } else if (ep == EP_MASK) {
-    launch_gemm_tiles<T, EP_MASK, false>(a, st);
-  } else {
-    launch_gemm_tiles<T, EP_RESID, false>(a, st);
-  }
 }
 
 template <typename T, int BO, int BK>
@@ -1397,24 +1573,12 @@ int conv_row_tiles(int dtype, const ConvArgs& a) {
   return (a.m + bm - 1) / bm;
 }
 
-void conv_gemm(int dtype, const ConvArgs& a, int ep, hipStream_t st) {
-  if (launch_halo_any(dtype, a, ep, st)) return;
-  if (use_staged(dtype, a)) {
-    const bool pro = a.pro_scale != nullptr;
-    if (ep == EP_STATS) {
-      if (pro) launch_staged_tiles<EP_STATS, true>(a, st);
-      else launch_staged_tiles<EP_STATS, false>(a, st);
-    } else if (ep == EP_MASK) {
-      launch_staged_tiles<EP_MASK, false>(a, st);
-    } else {
-      launch_staged_tiles<EP_RESID, false>(a, st);
-    }
-    return;
-  }
-  if (dtype == DT_BF16)
-    conv_gemm_t<bf16_t>(a, ep, st);
-  else
-    conv_gemm_t<float>(a, ep, st);
+bool conv_gemm(int dtype, const ConvArgs& a, int ep, hipStream_t st) {
+  const int h = launch_halo_any(dtype, a, ep, st);
+  if (h >= 0) return h == 1;
+  if (use_staged(dtype, a)) return launch_staged_tiles(a, ep, st);
+  if (dtype == DT_BF16) return conv_gemm_t<bf16_t>(a, ep, st);
+  return conv_gemm_t<float>(a, ep, st);
 }
 
 void conv_wgrad(int dtype, const WgradArgs& a, hipStream_t st) {

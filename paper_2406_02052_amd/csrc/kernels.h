@@ -7,7 +7,13 @@
 namespace petra {
 
 enum { DT_FP32 = 0, DT_BF16 = 1 };
-enum { EP_STATS = 0, EP_MASK = 1, EP_RESID = 2 };
+// Epilogues: BN statistics of the output; ReLU mask of the layer below plus its
+// BN-backward partials; residual add; residual add plus the BN-backward
+// partials of the stored result against a BN layer given by ep_h/ep_mean/ep_rstd.
+enum { EP_STATS = 0, EP_MASK = 1, EP_RESID = 2, EP_RESID_STATS = 3 };
+// Prologues applied to the gathered input: none; BN-apply + ReLU
+// (pro_scale/pro_shift); BN backward (pro_h, pro_ca/cb/cc/mean).
+enum { PRO_NONE = 0, PRO_RELU = 1, PRO_BWD = 2 };
 
 // Implicit-GEMM convolution (forward, or input gradient with transposed weights).
 struct ConvArgs {
@@ -16,16 +22,23 @@ struct ConvArgs {
   int c_split;             // channels held by src (== c_in without src2)
   const float* pro_scale;  // optional prologue: input -> max(scale*x + shift, 0) per input channel
   const float* pro_shift;
+  // optional prologue (with pro_h set): input d -> ca*d + cb*(h - mean) + cc per input
+  // channel, h read from pro_h at the same position (BN input gradient formed on the fly)
+  const void* pro_h;
+  const float* pro_ca;
+  const float* pro_cb;
+  const float* pro_cc;
+  const float* pro_mean;
   const void* wt;          // [c_out][k_tot], k = (r, s, c)
   void* out;               // [m][c_out]
   const void* resid;       // EP_RESID: out = resid + conv (may alias out); null: out = conv
-  const void* ep_h;        // EP_MASK: pre-BN tensor of the layer below, [m][c_out]
-  const float* ep_scale;   // EP_MASK: BN scale/shift/mean/rstd of that layer
+  const void* ep_h;        // EP_MASK / EP_RESID_STATS: pre-BN tensor of that BN layer, [m][c_out]
+  const float* ep_scale;   // EP_MASK: BN scale/shift of the layer below
   const float* ep_shift;
-  const float* ep_mean;
+  const float* ep_mean;    // EP_MASK / EP_RESID_STATS: BN mean/rstd of that layer
   const float* ep_rstd;
   float* partials;         // EP_STATS: [tiles][3][c_out] (rows, sum, centred sum of squares);
-                           // EP_MASK: [tiles][2][c_out] (sum dz, sum dz*xhat)
+                           // EP_MASK / EP_RESID_STATS: [tiles][2][c_out] (sum g, sum g*xhat)
   int n, h, w, c_in, p, q, c_out, r, s, stride, pad, k_tot, m;
 };
 
@@ -37,6 +50,13 @@ struct WgradArgs {
   int c_split;
   const float* pro_scale;
   const float* pro_shift;
+  // optional (with dh_h set): the output-side operand is ca*dh + cb*(h - mean) + cc per
+  // output channel, h read from dh_h [m][c_out]
+  const void* dh_h;
+  const float* dh_ca;
+  const float* dh_cb;
+  const float* dh_cc;
+  const float* dh_mean;
   float* partials;         // [splits][c_out][k_tot]
   int n, h, w, c_in, p, q, c_out, r, s, stride, pad, k_tot, m;
   int rows_per_split, splits;
@@ -44,7 +64,10 @@ struct WgradArgs {
 
 constexpr int CONV_BM = 128;  // rows per conv output tile (= partial-sum tile)
 
-void conv_gemm(int dtype, const ConvArgs& a, int ep, hipStream_t st);
+// Launches the conv; false (nothing launched) for an unsupported epilogue /
+// prologue pair (EP_STATS takes PRO_NONE or PRO_RELU, the others PRO_NONE or
+// PRO_BWD).
+bool conv_gemm(int dtype, const ConvArgs& a, int ep, hipStream_t st);
 // Number of partial-sum rows (output row tiles) conv_gemm writes for these arguments.
 int conv_row_tiles(int dtype, const ConvArgs& a);
 void conv_wgrad(int dtype, const WgradArgs& a, hipStream_t st);
@@ -77,6 +100,9 @@ int ew_tiles(long m, int c);
 // y = r + scale*h + shift  (forward coupling add)
 void combine_fwd(int dtype, const void* r, const void* h, const float* scale, const float* shift,
                  void* y, long m, int c, hipStream_t st);
+// x = v - (scale*h + shift)  (reconstruction only).
+void combine_rec(int dtype, const void* v, const void* h, const float* scale, const float* shift,
+                 void* x, long m, int c, hipStream_t st);
 // x = v - (scale*h + shift)  (reconstruction), with partials of (sum d, sum d*xhat).
 void combine_bwd(int dtype, const void* v, const void* h, const void* d, const float* scale,
                  const float* shift, const float* mean, const float* rstd, void* x,

@@ -376,8 +376,11 @@ bool Net::tick(const void* images, const int32_t* labels, float* loss, hipStream
       }
       void* fx1 = ws + s.o_fx1;
       void* fx2 = ws + s.o_fx2;
-      (void)blk.graphs.run({1, reinterpret_cast<uintptr_t>(fx1), reinterpret_cast<uintptr_t>(y1)}, q,
-                           [&](hipStream_t c) { blk.forward(fx1, fx2, y1, y2, c); }, 0);
+      if (blk.use_graphs)
+        (void)blk.graphs.run({1, reinterpret_cast<uintptr_t>(fx1), reinterpret_cast<uintptr_t>(y1)}, q,
+                             [&](hipStream_t c) { blk.forward(fx1, fx2, y1, y2, c); }, 0);
+      else
+        blk.forward(fx1, fx2, y1, y2, q);
       if (s.last) {
         const int32_t* lab = at<int32_t>(st[0].o_labels) + (mf % J) * desc.n;
         head_forward_backward(dt, y1, y2, desc.n, s.H * s.W, s.C, theta + s.off_fc_w,
@@ -407,9 +410,12 @@ bool Net::tick(const void* images, const int32_t* labels, float* loss, hipStream
       void* xr2 = ws + s.o_xr2;
       void* dx1 = ws + s.o_dx1;
       void* dx2 = ws + s.o_dx2;
-      (void)blk.graphs.run({2, reinterpret_cast<uintptr_t>(by1), reinterpret_cast<uintptr_t>(bg1)}, q,
-                           [&](hipStream_t c) { blk.backward(by1, by2, bg1, bg2, xr1, xr2, dx1, dx2, c); },
-                           1);
+      if (blk.use_graphs)
+        (void)blk.graphs.run({2, reinterpret_cast<uintptr_t>(by1), reinterpret_cast<uintptr_t>(bg1)}, q,
+                             [&](hipStream_t c) { blk.backward(by1, by2, bg1, bg2, xr1, xr2, dx1, dx2, c); },
+                             1);
+      else
+        blk.backward(by1, by2, bg1, bg2, xr1, xr2, dx1, dx2, q);
       blk.count_backward();
       const void* in1 = ring_slot(s, mb, 0);
       const void* in2 = s.first ? nullptr : ring_slot(s, mb, 1);

@@ -35,14 +35,18 @@ struct Block {
   ResidualFn f, g;
 };
 
-// Device scratch of one pass (forward or backward), carved from the workspace.
+// Device scratch of one residual function's pass, carved from the workspace.
+// The forward uses one set; the backward alternates two sets between
+// consecutive residual functions, so the recompute of the next function can run
+// while the gradient chain of the current one still reads its own set.
 struct Scratch {
-  void* h[3] = {nullptr, nullptr, nullptr};  // pre-BN conv outputs of the current function
-  void* d0[2] = {nullptr, nullptr};          // BN input gradient dh (backward, per layer parity)
-  void* d1 = nullptr;                        // masked gradient dz (backward)
-  float* part = nullptr;                     // per-tile statistic partials [tiles][2][c]
+  void* h[3] = {nullptr, nullptr, nullptr};  // pre-BN conv outputs of the function
+  void* d1[2] = {nullptr, nullptr};          // masked gradients dz of inner layers (backward)
+  float* part = nullptr;                     // BN statistic partials of the recompute [tiles][3][c]
+  float* gpart = nullptr;                    // BN-backward partials of the last BN [tiles][2][c]
+  float* bpart = nullptr;                    // BN-backward partials of an inner BN [tiles][2][c]
   float* bnp = nullptr;                      // per layer: scale, shift, mean, rstd, ca, cb, cc
-  float* wpart = nullptr;                    // weight-gradient split partials
+  int gtiles = 0;                            // tile count of gpart (host side, set at enqueue)
   float* vec(int layer, int which, int cmax) const { return bnp + (layer * 8 + which) * cmax; }
 };
 
@@ -69,8 +73,9 @@ class Stage {
   size_t ws_need = 0;
   size_t off_wfwd = 0, off_wdg = 0;
   struct ScratchPlan {
-    size_t h[3], d0[2], d1, part, bnp, wpart;
-  } plan_f{}, plan_b{};
+    size_t h[3], d1[2], part, gpart, bpart, bnp;
+  } plan_f{}, plan_b[2]{};
+  size_t off_wpart = 0;
   int64_t wpart_floats = 0;
 
   // Bound buffers.
@@ -82,18 +87,24 @@ class Stage {
   char* ws = nullptr;
   void* wfwd = nullptr;
   void* wdg = nullptr;
-  Scratch sf, sb;
+  Scratch sf, sb[2];
+  float* wpart = nullptr;  // weight-gradient split partials (weight-gradient stream only)
 
   petra_sgd opt{0.1f, 0.9f, 0.0f, 1, 1};
   int64_t bwd_count = 0, last_update = 0;
 
   Profiler prof;
+  bool launch_error = false;  // a conv variant was requested that no kernel implements
 
   hipStream_t s_fwd = nullptr, s_bwd = nullptr;
-  hipStream_t s_wg = nullptr;                 // weight-gradient branch of the backward
+  // Backward streams: the recompute of residual functions runs ahead on s_rec,
+  // the weight gradients on s_wg, the input-gradient chain on the caller's stream.
+  hipStream_t s_rec = nullptr, s_wg = nullptr;
   hipEvent_t ev_fork = nullptr, ev_fwd = nullptr, ev_bwd = nullptr;
-  hipEvent_t ev_dh = nullptr, ev_wg = nullptr;
-  hipEvent_t ev_wpar[2] = {nullptr, nullptr};  // weight-gradient branch done with dh[parity]
+  hipEvent_t ev_start = nullptr, ev_d = nullptr, ev_rec_end = nullptr;
+  hipEvent_t ev_rec[2] = {nullptr, nullptr};     // recompute of set p done (h, BN statistics)
+  hipEvent_t ev_gdone[2] = {nullptr, nullptr};   // input-gradient chain done with set p
+  hipEvent_t ev_wgdone[2] = {nullptr, nullptr};  // weight gradients done with set p
 
   bool bound() const { return theta != nullptr; }
   void bind(float* th, float* gr, float* mo, float* rm, float* rv, void* w);
@@ -110,15 +121,28 @@ class Stage {
   hipError_t ensure_streams();
 
   GraphCache graphs;
-  bool use_graphs = true;
+  bool use_graphs = false;
+  int bwd_streams = 3;  // 1: one stream; 2: + weight gradients; 3: + recompute ahead
 
  private:
+  // One residual function of the backward, in the order the backward visits them.
+  struct BwdFn {
+    const ResidualFn* fn;
+    const void* u;     // function input (recomputed from)
+    const void* v;     // output-side stream: the reconstruction is v - Phi(u)
+    const void* d;     // gradient of the coupling output
+    const void* rg;    // residual gradient added to the input gradient
+    void* xrec;        // reconstructed stream
+    void* dout;        // input gradient: rg + dPhi/du^T d
+  };
   void fn_recompute(const ResidualFn& fn, const void* u, Scratch& s, bool running,
                     hipStream_t st);
   void fn_forward(const ResidualFn& fn, const void* u, const void* r, void* y, Scratch& s,
                   hipStream_t st);
-  void fn_backward(const ResidualFn& fn, const void* u, const void* v, const void* d,
-                   const void* rg, void* xrec, void* dout, Scratch& s, hipStream_t st);
+  void fn_grad(const BwdFn& f, Scratch& s, const BwdFn* next, Scratch* sn, hipStream_t st,
+               hipStream_t wst, hipStream_t rs, bool wait_prev_wg, int parity, int part,
+               const void** dsrc_io);
+  bool conv(const ConvArgs& a, int ep, hipStream_t st);
   ConvArgs conv_args(const ConvLayer& cv) const;
   void wgrad_splits(const ConvLayer& cv, int* splits, int* rows_per_split) const;
 };

@@ -2,17 +2,24 @@
 //
 // Forward of a residual function Phi = conv-BN[-ReLU-conv-BN...] on input u,
 // coupled as y = r + Phi(u) (Sec. 3.2):
-//   conv_l (BN_{l-1}+ReLU applied in the prologue; sum/sum^2 partials in the
-//   epilogue) -> finalize BN_l -> ... -> combine_fwd y = r + BN_L(h_L).
-// Backward of the same coupling given its output-side stream v, the upstream
-// gradient d of the coupling output and the residual gradient rg (Eq. 4-5):
-//   recompute convs (running statistics move here only, Sec. 4.1)
-//   -> combine_bwd: x = v - BN_L(h_L), with sum d and sum d*xhat partials
-//   -> per layer from the top: dh = BN backward (elementwise), weight gradient
-//      (split rows, fixed-order reduce into the accumulator, scaled 1/k),
-//      input gradient conv whose epilogue applies the ReLU mask of the layer
-//      below and emits that layer's BN-backward partials, or, for the first
-//      layer, adds the residual gradient: dout = rg + d Phi/du^T d.
+//   conv_l (BN_{l-1}+ReLU applied in the prologue; BN partials in the epilogue)
+//   -> finalize BN_l -> ... -> combine_fwd y = r + BN_L(h_L).
+// Backward of the couplings in reverse order (Eq. 4-5).  For each residual
+// function, given its output-side stream v, the gradient d of the coupling
+// output and the residual gradient rg:
+//   recompute:  the convs again (running statistics move here only, Sec. 4.1),
+//               then the reconstruction x = v - BN_L(h_L);
+//   gradient:   BN_L backward coefficients from partials of (d, h_L), then per
+//               layer from the top an input-gradient conv whose prologue forms
+//               dh_l = BN_l backward of its input on the fly and whose epilogue
+//               applies the ReLU mask of the layer below and emits that layer's
+//               BN-backward partials, or, for the first layer, adds rg
+//               (dout = rg + dPhi/du^T d) and emits the BN_L-backward partials of
+//               the next function visited; the weight gradient of each conv runs
+//               on a side stream from the same on-the-fly dh (split rows,
+//               fixed-order reduce into the accumulator, scaled 1/k).
+// The recompute of the next function runs on its own stream while the gradient
+// chain of the current one proceeds; two scratch sets alternate between them.
 #include <algorithm>
 #include <cstring>
 
@@ -125,17 +132,18 @@ Stage::Stage(const petra_stage_desc& d) : desc(d) {
   };
   off_wfwd = take(static_cast<size_t>(n_conv) * esz);
   off_wdg = take(static_cast<size_t>(n_conv) * esz);
-  for (ScratchPlan* p : {&plan_f, &plan_b}) {
+  for (ScratchPlan* p : {&plan_f, &plan_b[0], &plan_b[1]}) {
     for (size_t l = 0; l < 3; ++l)
       p->h[l] = l < fn_shapes.size() ? take(static_cast<size_t>(M) * fn_shapes[l].cout * esz) : 0;
-    const bool bwd = p == &plan_b;
-    p->d0[0] = bwd ? take(static_cast<size_t>(M) * cmax * esz) : 0;
-    p->d0[1] = bwd ? take(static_cast<size_t>(M) * cmax * esz) : 0;
-    p->d1 = bwd ? take(static_cast<size_t>(M) * cmax * esz) : 0;
+    const bool bwd = p != &plan_f;
+    p->d1[0] = bwd ? take(static_cast<size_t>(M) * cmax * esz) : 0;
+    p->d1[1] = bwd && fn_shapes.size() > 2 ? take(static_cast<size_t>(M) * cmax * esz) : 0;
     p->part = take(static_cast<size_t>(tiles_max) * 3 * cmax * sizeof(float));
+    p->gpart = bwd ? take(static_cast<size_t>(tiles_max) * 2 * cmax * sizeof(float)) : 0;
+    p->bpart = bwd ? take(static_cast<size_t>(tiles_max) * 2 * cmax * sizeof(float)) : 0;
     p->bnp = take(static_cast<size_t>(3) * 8 * cmax * sizeof(float));
-    p->wpart = bwd ? take(static_cast<size_t>(wpart_floats) * sizeof(float)) : 0;
   }
+  off_wpart = take(static_cast<size_t>(wpart_floats) * sizeof(float));
   ws_need = off;
 }
 
@@ -145,11 +153,11 @@ Stage::~Stage() {
   if (ev_fork) (void)hipEventDestroy(ev_fork);
   if (ev_fwd) (void)hipEventDestroy(ev_fwd);
   if (ev_bwd) (void)hipEventDestroy(ev_bwd);
-  if (ev_dh) (void)hipEventDestroy(ev_dh);
-  if (ev_wg) (void)hipEventDestroy(ev_wg);
-  for (hipEvent_t e : ev_wpar)
+  for (hipEvent_t e : {ev_start, ev_d, ev_rec_end, ev_rec[0], ev_rec[1], ev_gdone[0],
+                       ev_gdone[1], ev_wgdone[0], ev_wgdone[1]})
     if (e) (void)hipEventDestroy(e);
   if (s_wg) (void)hipStreamDestroy(s_wg);
+  if (s_rec) (void)hipStreamDestroy(s_rec);
   if (s_fwd) (void)hipStreamDestroy(s_fwd);
   if (s_bwd) (void)hipStreamDestroy(s_bwd);
 }
@@ -159,18 +167,20 @@ void Stage::bind(float* th, float* gr, float* mo, float* rm, float* rv, void* w)
   ws = static_cast<char*>(w);
   wfwd = ws + off_wfwd;
   wdg = ws + off_wdg;
-  for (int pass = 0; pass < 2; ++pass) {
-    const ScratchPlan& p = pass == 0 ? plan_f : plan_b;
-    Scratch& s = pass == 0 ? sf : sb;
-    const int nl = blocks.empty() ? 0 : blocks[0].f.nconv;
+  const int nl = blocks.empty() ? 0 : blocks[0].f.nconv;
+  for (int pass = 0; pass < 3; ++pass) {
+    const ScratchPlan& p = pass == 0 ? plan_f : plan_b[pass - 1];
+    Scratch& s = pass == 0 ? sf : sb[pass - 1];
+    const bool bwd = pass > 0;
     for (int l = 0; l < 3; ++l) s.h[l] = l < nl ? ws + p.h[l] : nullptr;
-    s.d0[0] = pass == 1 ? ws + p.d0[0] : nullptr;
-    s.d0[1] = pass == 1 ? ws + p.d0[1] : nullptr;
-    s.d1 = pass == 1 ? ws + p.d1 : nullptr;
+    s.d1[0] = bwd ? ws + p.d1[0] : nullptr;
+    s.d1[1] = bwd && nl > 2 ? ws + p.d1[1] : nullptr;
     s.part = reinterpret_cast<float*>(ws + p.part);
+    s.gpart = bwd ? reinterpret_cast<float*>(ws + p.gpart) : nullptr;
+    s.bpart = bwd ? reinterpret_cast<float*>(ws + p.bpart) : nullptr;
     s.bnp = reinterpret_cast<float*>(ws + p.bnp);
-    s.wpart = pass == 1 ? reinterpret_cast<float*>(ws + p.wpart) : nullptr;
   }
+  wpart = reinterpret_cast<float*>(ws + off_wpart);
 }
 
 hipError_t Stage::ensure_streams() {
@@ -181,10 +191,10 @@ hipError_t Stage::ensure_streams() {
   if ((e = hipEventCreateWithFlags(&ev_fork, hipEventDisableTiming)) != hipSuccess) return e;
   if ((e = hipEventCreateWithFlags(&ev_fwd, hipEventDisableTiming)) != hipSuccess) return e;
   if ((e = hipStreamCreateWithFlags(&s_wg, hipStreamNonBlocking)) != hipSuccess) return e;
-  if ((e = hipEventCreateWithFlags(&ev_dh, hipEventDisableTiming)) != hipSuccess) return e;
-  if ((e = hipEventCreateWithFlags(&ev_wg, hipEventDisableTiming)) != hipSuccess) return e;
-  for (hipEvent_t& ev : ev_wpar)
-    if ((e = hipEventCreateWithFlags(&ev, hipEventDisableTiming)) != hipSuccess) return e;
+  if ((e = hipStreamCreateWithFlags(&s_rec, hipStreamNonBlocking)) != hipSuccess) return e;
+  for (hipEvent_t* ev : {&ev_start, &ev_d, &ev_rec_end, &ev_rec[0], &ev_rec[1], &ev_gdone[0],
+                         &ev_gdone[1], &ev_wgdone[0], &ev_wgdone[1]})
+    if ((e = hipEventCreateWithFlags(ev, hipEventDisableTiming)) != hipSuccess) return e;
   return hipEventCreateWithFlags(&ev_bwd, hipEventDisableTiming);
 }
 
@@ -251,7 +261,7 @@ void Stage::fn_recompute(const ResidualFn& fn, const void* u, Scratch& s, bool r
     a.partials = s.part;
     const int tiles = conv_row_tiles(dt, a);
     prof.begin(st);
-    conv_gemm(dt, a, EP_STATS, st);
+    conv(a, EP_STATS, st);
     prof.end(K_CONV_FPROP, st, 2.0 * M * cv.cout * a.k_tot,
              static_cast<double>(esz) * (static_cast<double>(M) * (cv.cin + cv.cout) +
                                          static_cast<double>(cv.cout) * a.k_tot));
@@ -274,56 +284,120 @@ void Stage::fn_forward(const ResidualFn& fn, const void* u, const void* r, void*
   prof.end(K_COMBINE_FWD, st, 0.0, 3.0 * M * c * esz);
 }
 
-void Stage::fn_backward(const ResidualFn& fn, const void* u, const void* v, const void* d,
-                        const void* rg, void* xrec, void* dout, Scratch& s, hipStream_t st) {
+bool Stage::conv(const ConvArgs& a, int ep, hipStream_t st) {
+  const bool ok = conv_gemm(dt, a, ep, st);
+  if (!ok) launch_error = true;
+  return ok;
+}
+
+// Gradient chain of one residual function (enqueue only), in two parts so the
+// recompute of the next function can be enqueued between them: part 0 is the
+// BN_L-backward coefficients and the layers L..1, part 1 the first layer.  s
+// holds the function's recomputed h and BN statistics and, in gpart, the
+// BN_L-backward partials of its output gradient d.  next/sn: the function
+// visited next (recompute enqueued before part 1), whose BN_L-backward partials
+// the first-layer conv emits.  Each layer's input-gradient conv is enqueued
+// before its weight gradient, which runs on the side stream.
+void Stage::fn_grad(const BwdFn& f, Scratch& s, const BwdFn* next, Scratch* sn, hipStream_t st,
+                    hipStream_t wst, hipStream_t rs, bool wait_prev_wg, int parity, int part,
+                    const void** dsrc_io) {
+  const ResidualFn& fn = *f.fn;
+  const bool wb = wst != st;  // weight gradients on their own stream
+  const bool rb = rs != st;   // recompute on its own stream
   const float inv_k = 1.0f / static_cast<float>(std::max(1, opt.accum_k));
-  fn_recompute(fn, u, s, true, st);
   const int L = fn.nconv - 1;
-  {
+  if (part == 0) {
     const ConvLayer& cv = convs[fn.conv[L]];
     const BnLayer& bn = bns[cv.bn];
     prof.begin(st);
-    combine_bwd(dt, v, s.h[L], d, s.vec(L, V_SCALE, cmax), s.vec(L, V_SHIFT, cmax),
-                s.vec(L, V_MEAN, cmax), s.vec(L, V_RSTD, cmax), xrec, s.part, M, cv.cout, st);
-    prof.end(K_COMBINE_BWD, st, 0.0, 4.0 * M * cv.cout * esz);
-    const int et = ew_tiles(M, cv.cout);
-    prof.begin(st);
-    bn_bwd_finalize(s.part, et, cv.cout, M, theta + bn.g_off,
-                    s.vec(L, V_MEAN, cmax), s.vec(L, V_RSTD, cmax), inv_k, grad + bn.g_off,
-                    grad + bn.b_off, s.vec(L, V_CA, cmax), s.vec(L, V_CB, cmax),
-                    s.vec(L, V_CC, cmax), st);
-    prof.end(K_BN_BWD_FINALIZE, st, 0.0, 8.0 * et * cv.cout);
+    bn_bwd_finalize(s.gpart, s.gtiles, cv.cout, M, theta + bn.g_off, s.vec(L, V_MEAN, cmax),
+                    s.vec(L, V_RSTD, cmax), inv_k, grad + bn.g_off, grad + bn.b_off,
+                    s.vec(L, V_CA, cmax), s.vec(L, V_CB, cmax), s.vec(L, V_CC, cmax), st);
+    prof.end(K_BN_BWD_FINALIZE, st, 0.0, 8.0 * s.gtiles * cv.cout);
+    *dsrc_io = f.d;
   }
-  const void* dsrc = d;
-  // The weight-gradient branch (wgrad + split reduce) of each layer runs on its
-  // own stream, concurrently with the input-gradient chain; dh alternates
-  // between two buffers so the next layer's dh does not wait for it.
-  const bool branch = s_wg != nullptr && !prof.enabled;
-  hipStream_t wst = branch ? s_wg : st;
-  for (int l = L; l >= 0; --l) {
+  const int l_hi = part == 0 ? L : 0, l_lo = part == 0 ? 1 : 0;
+  for (int l = l_hi; l >= l_lo; --l) {
     const ConvLayer& cv = convs[fn.conv[l]];
-    void* d0 = s.d0[l & 1];
-    // dh[l & 1] was last read by the weight gradient of layer l + 2
-    if (branch && l + 2 <= L) (void)hipStreamWaitEvent(st, ev_wpar[l & 1], 0);
-    // dh_l = BN_l backward applied to the gradient of its output
-    prof.begin(st);
-    bn_bwd_apply(dt, dsrc, s.h[l], s.vec(l, V_CA, cmax), s.vec(l, V_CB, cmax),
-                 s.vec(l, V_CC, cmax), s.vec(l, V_MEAN, cmax), d0, M, cv.cout, st);
-    prof.end(K_BN_BWD_APPLY, st, 0.0, 3.0 * M * cv.cout * esz);
-    if (branch) {
-      (void)hipEventRecord(ev_dh, st);
-      (void)hipStreamWaitEvent(wst, ev_dh, 0);
+    const void* dsrc = *dsrc_io;
+    // Both consumers form dh_l = BN_l backward of dsrc on the fly from (dsrc, h_l).
+    if (wb) (void)hipEventRecord(ev_d, st);
+    // input gradient: conv of dh_l with the transposed, flipped weights
+    ConvArgs a = conv_args(cv);
+    a.src = dsrc;
+    a.c_in = cv.cout;
+    a.c_split = cv.cout;
+    a.pro_h = s.h[l];
+    a.pro_ca = s.vec(l, V_CA, cmax);
+    a.pro_cb = s.vec(l, V_CB, cmax);
+    a.pro_cc = s.vec(l, V_CC, cmax);
+    a.pro_mean = s.vec(l, V_MEAN, cmax);
+    a.wt = static_cast<char*>(wdg) + cv.dg_off * esz;
+    a.c_out = cv.cin;
+    a.k_tot = cv.r * cv.s * cv.cout;
+    const double dbytes = static_cast<double>(esz) *
+                          (static_cast<double>(M) * (2.0 * cv.cout + 2.0 * cv.cin) +
+                           static_cast<double>(cv.cin) * a.k_tot);
+    if (l > 0) {
+      const ConvLayer& lo = convs[fn.conv[l - 1]];
+      const BnLayer& bl = bns[lo.bn];
+      a.out = s.d1[(L - l) & 1];
+      a.ep_h = s.h[l - 1];
+      a.ep_scale = s.vec(l - 1, V_SCALE, cmax);
+      a.ep_shift = s.vec(l - 1, V_SHIFT, cmax);
+      a.ep_mean = s.vec(l - 1, V_MEAN, cmax);
+      a.ep_rstd = s.vec(l - 1, V_RSTD, cmax);
+      a.partials = s.bpart;
+      const int tiles_conv = conv_row_tiles(dt, a);
+      prof.begin(st);
+      conv(a, EP_MASK, st);
+      prof.end(K_CONV_DGRAD, st, 2.0 * M * cv.cin * a.k_tot, dbytes);
+      prof.begin(st);
+      bn_bwd_finalize(s.bpart, tiles_conv, lo.cout, M, theta + bl.g_off, s.vec(l - 1, V_MEAN, cmax),
+                      s.vec(l - 1, V_RSTD, cmax), inv_k, grad + bl.g_off, grad + bl.b_off,
+                      s.vec(l - 1, V_CA, cmax), s.vec(l - 1, V_CB, cmax),
+                      s.vec(l - 1, V_CC, cmax), st);
+      prof.end(K_BN_BWD_FINALIZE, st, 0.0, 8.0 * tiles_conv * lo.cout);
+      *dsrc_io = s.d1[(L - l) & 1];
+    } else {
+      a.out = f.dout;
+      a.resid = f.rg;
+      // dout may alias the previous function's output gradient, which that
+      // function's weight gradients read
+      if (wb && wait_prev_wg) (void)hipStreamWaitEvent(st, ev_wgdone[parity ^ 1], 0);
+      if (next != nullptr) {
+        if (rb) (void)hipStreamWaitEvent(st, ev_rec[parity ^ 1], 0);
+        const int NL = next->fn->nconv - 1;
+        a.ep_h = sn->h[NL];
+        a.ep_mean = sn->vec(NL, V_MEAN, cmax);
+        a.ep_rstd = sn->vec(NL, V_RSTD, cmax);
+        a.partials = sn->gpart;
+        sn->gtiles = conv_row_tiles(dt, a);
+        prof.begin(st);
+        conv(a, EP_RESID_STATS, st);
+        prof.end(K_CONV_DGRAD, st, 2.0 * M * cv.cin * a.k_tot, dbytes + 2.0 * esz * M * cv.cin);
+      } else {
+        prof.begin(st);
+        conv(a, EP_RESID, st);
+        prof.end(K_CONV_DGRAD, st, 2.0 * M * cv.cin * a.k_tot, dbytes);
+      }
     }
-    // weight gradient of conv_l
+    // weight gradient of conv_l (side stream), from the same dsrc and h_l
+    if (wb) (void)hipStreamWaitEvent(wst, ev_d, 0);
     WgradArgs w{};
-    w.dh = d0;
-    w.src = l == 0 ? u : s.h[l - 1];
+    w.dh = dsrc;
+    w.dh_h = s.h[l];
+    w.dh_ca = s.vec(l, V_CA, cmax);
+    w.dh_cb = s.vec(l, V_CB, cmax);
+    w.dh_cc = s.vec(l, V_CC, cmax);
+    w.dh_mean = s.vec(l, V_MEAN, cmax);
+    w.src = l == 0 ? f.u : s.h[l - 1];
     w.c_split = cv.cin;
     if (l > 0) {
       w.pro_scale = s.vec(l - 1, V_SCALE, cmax);
       w.pro_shift = s.vec(l - 1, V_SHIFT, cmax);
     }
-    w.partials = s.wpart;
+    w.partials = wpart;
     w.n = desc.n; w.h = desc.h; w.w = desc.w; w.c_in = cv.cin; w.p = desc.h; w.q = desc.w;
     w.c_out = cv.cout; w.r = cv.r; w.s = cv.s; w.stride = 1; w.pad = cv.pad;
     w.k_tot = cv.r * cv.s * cv.cin;
@@ -333,56 +407,15 @@ void Stage::fn_backward(const ResidualFn& fn, const void* u, const void* v, cons
     prof.begin(wst);
     conv_wgrad(dt, w, wst);
     prof.end(K_CONV_WGRAD, wst, 2.0 * M * wnumel,
-             static_cast<double>(esz) * M * (cv.cin + cv.cout) + 4.0 * w.splits * wnumel);
+             static_cast<double>(esz) * M * (cv.cin + 2.0 * cv.cout) + 4.0 * w.splits * wnumel);
     prof.begin(wst);
-    wgrad_reduce(s.wpart, w.splits, static_cast<long>(cv.cout) * w.k_tot, inv_k, grad + cv.w_off,
+    wgrad_reduce(wpart, w.splits, static_cast<long>(cv.cout) * w.k_tot, inv_k, grad + cv.w_off,
                  wst);
     prof.end(K_WGRAD_REDUCE, wst, 0.0, 4.0 * wnumel * (w.splits + 2));
-    if (branch) (void)hipEventRecord(ev_wpar[l & 1], wst);
-    // input gradient: conv of dh with the transposed, flipped weights
-    ConvArgs a = conv_args(cv);
-    a.src = d0;
-    a.c_in = cv.cout;
-    a.c_split = cv.cout;
-    a.wt = static_cast<char*>(wdg) + cv.dg_off * esz;
-    a.c_out = cv.cin;
-    a.k_tot = cv.r * cv.s * cv.cout;
-    if (l > 0) {
-      const ConvLayer& lo = convs[fn.conv[l - 1]];
-      const BnLayer& bl = bns[lo.bn];
-      a.out = s.d1;
-      a.ep_h = s.h[l - 1];
-      a.ep_scale = s.vec(l - 1, V_SCALE, cmax);
-      a.ep_shift = s.vec(l - 1, V_SHIFT, cmax);
-      a.ep_mean = s.vec(l - 1, V_MEAN, cmax);
-      a.ep_rstd = s.vec(l - 1, V_RSTD, cmax);
-      a.partials = s.part;
-      const int tiles_conv = conv_row_tiles(dt, a);
-      prof.begin(st);
-      conv_gemm(dt, a, EP_MASK, st);
-      prof.end(K_CONV_DGRAD, st, 2.0 * M * cv.cin * a.k_tot,
-               static_cast<double>(esz) * (static_cast<double>(M) * (cv.cout + 2.0 * cv.cin) +
-                                           static_cast<double>(cv.cin) * a.k_tot));
-      prof.begin(st);
-      bn_bwd_finalize(s.part, tiles_conv, lo.cout, M, theta + bl.g_off, s.vec(l - 1, V_MEAN, cmax),
-                      s.vec(l - 1, V_RSTD, cmax), inv_k, grad + bl.g_off, grad + bl.b_off,
-                      s.vec(l - 1, V_CA, cmax), s.vec(l - 1, V_CB, cmax),
-                      s.vec(l - 1, V_CC, cmax), st);
-      prof.end(K_BN_BWD_FINALIZE, st, 0.0, 8.0 * tiles_conv * lo.cout);
-      dsrc = s.d1;
-    } else {
-      a.out = dout;
-      a.resid = rg;
-      prof.begin(st);
-      conv_gemm(dt, a, EP_RESID, st);
-      prof.end(K_CONV_DGRAD, st, 2.0 * M * cv.cin * a.k_tot,
-               static_cast<double>(esz) * (static_cast<double>(M) * (cv.cout + 2.0 * cv.cin) +
-                                           static_cast<double>(cv.cin) * a.k_tot));
-    }
   }
-  if (branch) {  // later work overwrites the scratch the branch reads
-    (void)hipEventRecord(ev_wg, wst);
-    (void)hipStreamWaitEvent(st, ev_wg, 0);
+  if (part == 1) {
+    if (rb) (void)hipEventRecord(ev_gdone[parity], st);
+    if (wb || rs != wst) (void)hipEventRecord(ev_wgdone[parity], wst);
   }
 }
 
@@ -399,6 +432,8 @@ void Stage::forward(const void* x1, const void* x2, void* y1, void* y2, hipStrea
 
 void Stage::backward(const void* y1, const void* y2, const void* dy1, const void* dy2, void* x1,
                      void* x2, void* dx1, void* dx2, hipStream_t st) {
+  // Residual functions in the order the backward visits them.
+  std::vector<BwdFn> fl;
   const void* c1 = y1;
   const void* c2 = y2;
   const void* g1 = dy1;
@@ -406,11 +441,71 @@ void Stage::backward(const void* y1, const void* y2, const void* dy1, const void
   for (int b = static_cast<int>(blocks.size()) - 1; b >= 0; --b) {
     const Block& blk = blocks[b];
     // x2 = y2 - G(y1); z1 = g1 + dG/dy1^T g2  (written to dx1)
-    fn_backward(blk.g, c1, c2, g2, g1, x2, dx1, sb, st);
+    fl.push_back(BwdFn{&blk.g, c1, c2, g2, g1, x2, dx1});
     // x1 = y1 - F(x2); dx2 = g2 + dF/dx2^T z1
-    fn_backward(blk.f, x2, c1, dx1, g2, x1, dx2, sb, st);
+    fl.push_back(BwdFn{&blk.f, x2, c1, dx1, g2, x1, dx2});
     c1 = x1; c2 = x2; g1 = dx1; g2 = dx2;
   }
+  const int nf = static_cast<int>(fl.size());
+  // streams: the weight gradients (2+) and the recompute of the next function
+  // (3) on side streams; one stream when profiling per launch
+  const bool par = s_rec != nullptr && s_wg != nullptr && !prof.enabled;
+  hipStream_t rs = par && bwd_streams >= 3 ? s_rec : st;
+  hipStream_t wst = par && bwd_streams >= 2 ? s_wg : st;
+  const bool rb = rs != st, wb = wst != st;
+  if (rb || wb) (void)hipEventRecord(ev_start, st);
+  if (rb) (void)hipStreamWaitEvent(rs, ev_start, 0);
+  if (wb) (void)hipStreamWaitEvent(wst, ev_start, 0);
+  auto last_c = [&](const BwdFn& f) { return convs[f.fn->conv[f.fn->nconv - 1]].cout; };
+  // First function: recompute, reconstruction and the BN_L-backward partials of
+  // the given output gradient.
+  {
+    fn_recompute(*fl[0].fn, fl[0].u, sb[0], true, rs);
+    const int L = fl[0].fn->nconv - 1;
+    const int c = last_c(fl[0]);
+    prof.begin(rs);
+    combine_bwd(dt, fl[0].v, sb[0].h[L], fl[0].d, sb[0].vec(L, V_SCALE, cmax),
+                sb[0].vec(L, V_SHIFT, cmax), sb[0].vec(L, V_MEAN, cmax),
+                sb[0].vec(L, V_RSTD, cmax), fl[0].xrec, sb[0].gpart, M, c, rs);
+    prof.end(K_COMBINE_BWD, rs, 0.0, 4.0 * M * c * esz);
+    sb[0].gtiles = ew_tiles(M, c);
+    if (rb) (void)hipEventRecord(ev_rec[0], rs);
+  }
+  for (int f = 0; f < nf; ++f) {
+    const int p = f & 1;
+    const bool has_next = f + 1 < nf;
+    const BwdFn* nx = has_next ? &fl[f + 1] : nullptr;
+    Scratch* sn = has_next ? &sb[p ^ 1] : nullptr;
+    const void* dsrc = nullptr;
+    if (rb) (void)hipStreamWaitEvent(st, ev_rec[p], 0);
+    fn_grad(fl[f], sb[p], nx, sn, st, wst, rs, f >= 1, p, 0, &dsrc);
+    if (has_next) {
+      // recompute of the next function (its input is this function's
+      // reconstruction); its scratch set was last used by function f - 1
+      if (rb && f >= 1) (void)hipStreamWaitEvent(rs, ev_gdone[p ^ 1], 0);
+      fn_recompute(*fl[f + 1].fn, fl[f + 1].u, sb[p ^ 1], true, rs);
+      if (rb) (void)hipEventRecord(ev_rec[p ^ 1], rs);
+    }
+    fn_grad(fl[f], sb[p], nx, sn, st, wst, rs, f >= 1, p, 1, &dsrc);
+    if (has_next) {
+      // reconstruction of the next function; it may overwrite this function's
+      // input, which this function's weight gradients read
+      if (rs != wst) (void)hipStreamWaitEvent(rs, ev_wgdone[p], 0);
+      const BwdFn& nx = fl[f + 1];
+      const int L = nx.fn->nconv - 1;
+      const int c = last_c(nx);
+      prof.begin(rs);
+      combine_rec(dt, nx.v, sb[p ^ 1].h[L], sb[p ^ 1].vec(L, V_SCALE, cmax),
+                  sb[p ^ 1].vec(L, V_SHIFT, cmax), nx.xrec, M, c, rs);
+      prof.end(K_COMBINE_BWD, rs, 0.0, 3.0 * M * c * esz);
+    }
+  }
+  // join the side streams
+  if (rb) {
+    (void)hipEventRecord(ev_rec_end, rs);
+    (void)hipStreamWaitEvent(st, ev_rec_end, 0);
+  }
+  if (wb) (void)hipStreamWaitEvent(st, ev_wgdone[(nf - 1) & 1], 0);
 }
 
 bool Stage::update_due() const {

@@ -81,6 +81,9 @@ class Stage:
     def set_graphs(self, enable: bool) -> None:
         L.petra_stage_set_graphs(self.handle, enable)
 
+    def set_streams(self, n: int) -> None:
+        L.petra_stage_set_streams(self.handle, n)
+
     def set_optimizer(self, lr=0.1, momentum=0.9, weight_decay=0.0, nesterov=True, accum_k=1):
         L.petra_stage_set_optimizer(self.handle, L.Sgd(lr, momentum, weight_decay,
                                                       1 if nesterov else 0, accum_k))

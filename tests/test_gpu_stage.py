@@ -158,3 +158,34 @@ def test_graph_replay_matches_eager_every_replay():
                         [st.params.cpu().numpy(), st.mom.cpu().numpy(), st.run_var.cpu().numpy()])
         for a, b in zip(*outs):
             assert np.array_equal(a, b), f"replay {rep} differs from eager"
+
+
+@pytest.mark.parametrize("wl_name,shape", [
+    ("cifar", dict(n=4, h=8, w=32)),
+    ("bottleneck", dict(n=1, h=5, w=56, blocks=2)),
+])
+def test_backward_stream_modes_bitwise(wl_name, shape):
+    """One, two or three streams per backward (and graph replay of the
+    three-stream program) must give identical bits: the cross-stream ordering
+    covers every read-after-write and in-place hazard."""
+    import torch
+    from paper_2406_02052_amd import to_host
+
+    base = synth.CIFAR_STAGE if wl_name == "cifar" else synth.IMAGENET_BOTTLENECK_STAGE
+    wl = base.with_(**shape)
+    params = synth.stage_params(wl, "random")
+    res = []
+    for streams, graphs in ((1, False), (2, False), (3, False), (3, True)):
+        st = gpu_stage(wl, params)
+        st.set_streams(streams)
+        st.set_graphs(graphs)
+        a1, a2, g1, g2 = _io(st, wl, 21)
+        for _ in range(2):   # in place: y -> x and dy -> dx in the same buffers
+            st.reconstruct_backward(a1, a2, g1, g2, a1, a2, g1, g2)
+            st.update()
+        torch.cuda.synchronize()
+        res.append([to_host(t) for t in (a1, a2, g1, g2)] +
+                   [st.params.cpu().numpy(), st.run_mean.cpu().numpy(), st.run_var.cpu().numpy()])
+    for mode in res[1:]:
+        for a, b in zip(res[0], mode):
+            assert np.array_equal(a, b)
