@@ -17,12 +17,19 @@ __device__ __forceinline__ float bf16_to_f32(uint16_t b) {
   return __uint_as_float(static_cast<uint32_t>(b) << 16);
 }
 
-// fp32 -> bf16, round to nearest even (inputs here are finite; NaN is kept quiet).
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+// Two fp32 -> packed bf16 (lo in bits 0-15), round to nearest even.  gfx950
+// converts a pair in one instruction (v_cvt_pk_bf16_f32); it agrees bit for bit
+// with integer round-to-nearest-even on every non-NaN input and keeps NaN NaN.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{lo, hi}, bf16x2_t));
+}
+
+// fp32 -> bf16, round to nearest even.
 __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return static_cast<uint16_t>(u >> 16);
+  return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f));
 }
 
 // Eight consecutive elements of a tensor, widened to fp32.
@@ -41,9 +48,7 @@ template <> struct Vec8<bf16_t> {
   static __device__ __forceinline__ void store(bf16_t* p, const float* o) {
     uint32_t w[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      w[i] = static_cast<uint32_t>(f32_to_bf16(o[2 * i])) |
-             (static_cast<uint32_t>(f32_to_bf16(o[2 * i + 1])) << 16);
+    for (int i = 0; i < 4; ++i) w[i] = pack_bf16x2(o[2 * i], o[2 * i + 1]);
     *reinterpret_cast<uint4*>(p) = make_uint4(w[0], w[1], w[2], w[3]);
   }
 };
@@ -89,9 +94,7 @@ template <> struct Raw8<bf16_t> {
   }
   __device__ __forceinline__ void from_f32(const float* o) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      w[i] = static_cast<uint32_t>(f32_to_bf16(o[2 * i])) |
-             (static_cast<uint32_t>(f32_to_bf16(o[2 * i + 1])) << 16);
+    for (int i = 0; i < 4; ++i) w[i] = pack_bf16x2(o[2 * i], o[2 * i + 1]);
   }
   // Store element j into a 16-bit LDS/global slot.
   __device__ __forceinline__ void put(int j, bf16_t* dst) const {
@@ -157,6 +160,30 @@ __device__ __forceinline__ float sum_lane_groups(float v) {
   v += __shfl_xor(v, 16, 64);
   v += __shfl_xor(v, 32, 64);
   return v;
+}
+
+// Buffer resources (raw, stride 0) over [p, p + bytes): a load at a byte offset
+// past the end returns zeros and a store there is dropped, which gives
+// branch-free zero padding and masked stores.  Offsets are 32-bit.
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
+constexpr uint32_t BUF_OOB = 0x80000000u;   // an offset past every buffer used here
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, long bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), 0, static_cast<int>(bytes),
+                                           0x00020000);
+}
+__device__ __forceinline__ u32x4_t buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, static_cast<int>(off), 0, 0);
+}
+__device__ __forceinline__ u32x2_t buf_load8(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b64(r, static_cast<int>(off), 0, 0);
+}
+__device__ __forceinline__ void buf_store8(u32x2_t v, __amdgpu_buffer_rsrc_t r, uint32_t off) {
+  __builtin_amdgcn_raw_buffer_store_b64(v, r, static_cast<int>(off), 0, 0);
+}
+__device__ __forceinline__ void buf_store16(u32x4_t v, __amdgpu_buffer_rsrc_t r, uint32_t off) {
+  __builtin_amdgcn_raw_buffer_store_b128(v, r, static_cast<int>(off), 0, 0);
 }
 
 }  // namespace petra

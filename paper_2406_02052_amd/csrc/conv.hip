@@ -938,6 +938,342 @@ __global__ __launch_bounds__(256) void conv_halo_kernel(ConvArgs a) {
   }
 }
 
+// Persistent 3x3 / stride 1 / pad 1 conv for 32 -> 32 bf16 channels (the
+// HBM-bound shapes: C/2 = 32 at 32x32 and 56x56).  A workgroup takes tiles
+// g, g + G, g + 2G, ... of TH x TW output pixels; while the MFMAs of one tile
+// run, the input patch of the next one is already in flight into registers, so
+// loads, multiplies and stores of successive tiles overlap.  The 9 x 2 weight
+// fragments stay in registers for the whole launch.  The MFMA is issued as
+// D[cout][pixel] = W x patch^T, so each lane ends up with 4 consecutive output
+// channels of one pixel and stores them directly (8 bytes).  Statistics are
+// combined across the workgroup's tiles in registers (Chan's formula for the
+// BN moments, plain fixed-order sums for the gradient partials) and written
+// once per workgroup: partial row = blockIdx.x.
+template <int TH, int TW, int EP, int PRO>
+__global__ __launch_bounds__(256, 2) void conv32_kernel(ConvArgs a, int ntiles) {
+  using T = bf16_t;
+  constexpr int NR = TH * TW;                          // output pixels per tile
+  constexpr int FM = (NR + 63) / 64;                   // 16-pixel fragments per wave
+  constexpr int HTH = TH + 2, HTW = TW + 2, HPIX = HTH * HTW;
+  constexpr int HP = 40;                               // bf16 per patch pixel (32 + 8 pad)
+  constexpr int PATCH = HPIX * HP;
+  constexpr int H_CHUNKS = (HPIX * 4 + 255) / 256;
+  constexpr bool BWD = PRO == PRO_BWD;
+  __shared__ __attribute__((aligned(16))) T lds[2 * PATCH];
+  __shared__ float pro_tab[4][32];
+  __shared__ float red[4][3][32];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int lr = lane & 15, lg = lane >> 4;
+  const int G = gridDim.x;
+  // XCD-aware numbering: workgroups that share an L2 take neighbouring tiles
+  const int g = (G % 8 == 0) ? (blockIdx.x % 8) * (G / 8) + blockIdx.x / 8 : blockIdx.x;
+  const int tiles_x = (a.w + TW - 1) / TW, tiles_y = (a.h + TH - 1) / TH;
+  // Activations go through buffer resources: out-of-range offsets read zero
+  // (halo padding) or drop the store (rows past the image), with no branches.
+  const long in_bytes = static_cast<long>(a.n) * a.h * a.w * 64;
+  const long out_bytes = static_cast<long>(a.m) * 64;
+  const __amdgpu_buffer_rsrc_t r_src = make_rsrc(a.src, in_bytes);
+  const __amdgpu_buffer_rsrc_t r_proh = make_rsrc(BWD ? a.pro_h : a.src, in_bytes);
+  const __amdgpu_buffer_rsrc_t r_out = make_rsrc(a.out, out_bytes);
+  const __amdgpu_buffer_rsrc_t r_eph = make_rsrc(a.ep_h != nullptr ? a.ep_h : a.out, out_bytes);
+  const __amdgpu_buffer_rsrc_t r_res = make_rsrc(a.resid != nullptr ? a.resid : a.out,
+                                                 a.resid != nullptr ? out_bytes : 0);
+
+  if (tid < 32) {
+    if constexpr (PRO == PRO_RELU) {
+      pro_tab[0][tid] = a.pro_scale[tid];
+      pro_tab[1][tid] = a.pro_shift[tid];
+    } else if constexpr (BWD) {
+      pro_tab[0][tid] = a.pro_ca[tid];
+      pro_tab[1][tid] = a.pro_cb[tid];
+      pro_tab[2][tid] = a.pro_cc[tid];
+      pro_tab[3][tid] = a.pro_mean[tid];
+    }
+  }
+
+  auto origin = [&](int t, int& img, int& p0, int& q0) {
+    const int tx = t % tiles_x;
+    const int ty = (t / tiles_x) % tiles_y;
+    img = t / (tiles_x * tiles_y);
+    p0 = ty * TH;
+    q0 = tx * TW;
+  };
+  u32x4_t rh[H_CHUNKS];
+  u32x4_t rhh[BWD ? H_CHUNKS : 1];
+  uint32_t hvalid = 0;
+  // Per-thread patch chunks are fixed: patch row/column and the element offset
+  // relative to the tile origin.
+  int ch_y[H_CHUNKS], ch_x[H_CHUNKS], ch_rel[H_CHUNKS];
+#pragma unroll
+  for (int i = 0; i < H_CHUNKS; ++i) {
+    const int q = tid + 256 * i;
+    const int hp = q >> 2, sub = q & 3;
+    const int hy = hp / HTW, hx = hp - hy * HTW;
+    ch_y[i] = hp < HPIX ? hy - 1 : -(1 << 20);   // rows past the patch never load
+    ch_x[i] = hx - 1;
+    ch_rel[i] = ((hy - 1) * a.w + (hx - 1)) * 32 + sub * 8;
+  }
+  auto load_patch = [&](int t) {
+    int img, p0, q0;
+    origin(t, img, p0, q0);
+    const int tbase = ((img * a.h + p0) * a.w + q0) * 32;
+    hvalid = 0;
+#pragma unroll
+    for (int i = 0; i < H_CHUNKS; ++i) {
+      const int ih = p0 + ch_y[i], iw = q0 + ch_x[i];
+      const bool ok = static_cast<unsigned>(ih) < static_cast<unsigned>(a.h) &&
+                      static_cast<unsigned>(iw) < static_cast<unsigned>(a.w);
+      const uint32_t off = ok ? static_cast<uint32_t>(tbase + ch_rel[i]) * 2u : BUF_OOB;
+      rh[i] = buf_load16(r_src, off);
+      if constexpr (BWD) rhh[i] = buf_load16(r_proh, off);
+      hvalid |= ok ? 1u << i : 0u;
+    }
+  };
+  auto park_patch = [&](int buf) {
+    T* dst = lds + buf * PATCH;
+#pragma unroll
+    for (int i = 0; i < H_CHUNKS; ++i) {
+      const int q = tid + 256 * i;
+      const int hp = q >> 2, sub = q & 3;
+      if (hp >= HPIX) continue;
+      u32x4_t v = rh[i];
+      if constexpr (PRO != PRO_NONE) {
+        Raw8<T> r, hr;
+        r.w[0] = v.x; r.w[1] = v.y; r.w[2] = v.z; r.w[3] = v.w;
+        if constexpr (BWD) {
+          hr.w[0] = rhh[i].x; hr.w[1] = rhh[i].y; hr.w[2] = rhh[i].z; hr.w[3] = rhh[i].w;
+        }
+        pro8<T, PRO>(r, hr, pro_tab[0], pro_tab[1], pro_tab[BWD ? 2 : 0], pro_tab[BWD ? 3 : 0],
+                     sub * 8);
+        const bool ok = (hvalid >> i) & 1u;   // padding stays zero
+        v = u32x4_t{ok ? r.w[0] : 0u, ok ? r.w[1] : 0u, ok ? r.w[2] : 0u, ok ? r.w[3] : 0u};
+      }
+      *reinterpret_cast<u32x4_t*>(dst + hp * HP + sub * 8) = v;
+    }
+  };
+
+  // Weight fragments: lane (lr, lg) holds output channel fn*16 + lr, inputs lg*8..+7 of tap.
+  Frag<T> wf[9][2];
+  {
+    const T* wt = static_cast<const T*>(a.wt);
+#pragma unroll
+    for (int tap = 0; tap < 9; ++tap)
+#pragma unroll
+      for (int fn = 0; fn < 2; ++fn) wf[tap][fn].load(wt + (fn * 16 + lr) * a.k_tot + tap * 32 + lg * 8);
+  }
+  // Loads are unconditional (a workgroup past the last tile, and the prefetch
+  // after its last tile, re-read tile ntiles - 1) so that the number of loads in
+  // flight is the same on every path and the waits stay tight.
+  int t = g;
+  load_patch(min(t, ntiles - 1));
+  if constexpr (PRO != PRO_NONE) __syncthreads();   // prologue table
+  // Patch offset of each fragment's pixel lr (tap (0,0)); rows past NR are padding.
+  int rowpix[FM], rowi[FM];
+#pragma unroll
+  for (int fm = 0; fm < FM; ++fm) {
+    const int i = (wave * FM + fm) * 16 + lr;
+    rowi[fm] = i;
+    const int ii = i < NR ? i : 0;
+    const int ph = ii / TW, pw = ii - ph * TW;
+    rowpix[fm] = ph * HTW + pw;
+  }
+  // This lane's 8 output channels: fn*16 + lg*4 + e.
+  float es[2][4], esh[2][4], emu[2][4], ers[2][4];
+  if constexpr (EP == EP_MASK || EP == EP_RESID_STATS) {
+#pragma unroll
+    for (int fn = 0; fn < 2; ++fn)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int c = fn * 16 + lg * 4 + e;
+        es[fn][e] = EP == EP_MASK ? a.ep_scale[c] : 0.f;
+        esh[fn][e] = EP == EP_MASK ? a.ep_shift[c] : 0.f;
+        emu[fn][e] = a.ep_mean[c];
+        ers[fn][e] = a.ep_rstd[c];
+      }
+  }
+  // Running per-lane statistics.  EP_STATS: count and sums of (v - K), (v - K)^2
+  // with K a per-channel shift taken from the first tile (keeps the moments
+  // free of cancellation); gradient epilogues: sums of g and g*xhat.
+  float st_n = 0.f, st_a[2][4], st_b[2][4], st_k[2][4];
+  bool have_k = false;
+#pragma unroll
+  for (int fn = 0; fn < 2; ++fn)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) st_a[fn][e] = st_b[fn][e] = st_k[fn][e] = 0.f;
+
+  int buf = 0;
+  for (; t < ntiles; t += G) {
+    park_patch(buf);
+    __syncthreads();
+    int img, p0, q0;
+    origin(t, img, p0, q0);
+    load_patch(min(t + G, ntiles - 1));
+    f32x4_t acc[FM][2];
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm) acc[fm][0] = acc[fm][1] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    const T* pt = lds + buf * PATCH;
+#pragma unroll
+    for (int tap = 0; tap < 9; ++tap) {
+      const int toff = (tap / 3) * HTW + (tap % 3);
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm) {
+        Frag<T> pb;
+        pb.load(pt + (rowpix[fm] + toff) * HP + lg * 8);
+        acc[fm][0] = mfma(wf[tap][0], pb, acc[fm][0]);
+        acc[fm][1] = mfma(wf[tap][1], pb, acc[fm][1]);
+      }
+    }
+    // Epilogue: lane holds channels fn*16 + lg*4 + e of pixel rowi[fm].
+    bool vm[FM];
+    uint32_t pix[FM];
+    float nv = 0.f;
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm) {
+      const int i = rowi[fm];
+      const int ii = i < NR ? i : 0;
+      const int ph = ii / TW, pw = ii - ph * TW;
+      vm[fm] = i < NR && p0 + ph < a.h && q0 + pw < a.w;
+      pix[fm] = vm[fm] ? static_cast<uint32_t>(((img * a.h + p0 + ph) * a.w + q0 + pw) * 64) : BUF_OOB;
+      nv += vm[fm] ? 1.f : 0.f;
+    }
+    float q[FM][2][4];
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm) {
+#pragma unroll
+      for (int fn = 0; fn < 2; ++fn) {
+        float v[4] = {acc[fm][fn][0], acc[fm][fn][1], acc[fm][fn][2], acc[fm][fn][3]};
+        // byte offset of channels fn*16 + lg*4 .. +3 (past the end for padding rows)
+        const uint32_t boff = vm[fm] ? pix[fm] + (fn * 16 + lg * 4) * 2 : BUF_OOB;
+        float hl[4] = {0.f, 0.f, 0.f, 0.f}, rv[4] = {0.f, 0.f, 0.f, 0.f};
+        if constexpr (EP == EP_MASK || EP == EP_RESID_STATS || EP == EP_RESID) {
+          if constexpr (EP != EP_RESID) {
+            const u32x2_t hw = buf_load8(r_eph, boff);
+            hl[0] = __uint_as_float(hw.x << 16); hl[1] = __uint_as_float(hw.x & 0xffff0000u);
+            hl[2] = __uint_as_float(hw.y << 16); hl[3] = __uint_as_float(hw.y & 0xffff0000u);
+          }
+          if constexpr (EP != EP_MASK) {
+            // a null residual has a zero-sized resource: reads give zero
+            const u32x2_t rw = buf_load8(r_res, boff);
+            rv[0] = __uint_as_float(rw.x << 16); rv[1] = __uint_as_float(rw.x & 0xffff0000u);
+            rv[2] = __uint_as_float(rw.y << 16); rv[3] = __uint_as_float(rw.y & 0xffff0000u);
+          }
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            if constexpr (EP == EP_MASK)
+              v[e] = fmaf(es[fn][e], hl[e], esh[fn][e]) > 0.f ? v[e] : 0.f;
+            else
+              v[e] += rv[e];
+          }
+        }
+        // one conversion per pair; statistics use the stored values
+        const uint32_t w0 = pack_bf16x2(v[0], v[1]), w1 = pack_bf16x2(v[2], v[3]);
+        buf_store8(u32x2_t{w0, w1}, r_out, boff);
+        v[0] = __uint_as_float(w0 << 16); v[1] = __uint_as_float(w0 & 0xffff0000u);
+        v[2] = __uint_as_float(w1 << 16); v[3] = __uint_as_float(w1 & 0xffff0000u);
+        if constexpr (EP == EP_MASK || EP == EP_RESID_STATS) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float g = vm[fm] ? v[e] : 0.f;
+            st_a[fn][e] += g;
+            st_b[fn][e] += g * ((hl[e] - emu[fn][e]) * ers[fn][e]);
+          }
+        } else if constexpr (EP == EP_STATS) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) q[fm][fn][e] = vm[fm] ? v[e] : 0.f;
+        }
+      }
+    }
+    if constexpr (EP == EP_STATS) {
+      if (!have_k) {
+        // shift: the stored value of the wave's first pixel of this tile, per channel
+#pragma unroll
+        for (int fn = 0; fn < 2; ++fn)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) st_k[fn][e] = __shfl(q[0][fn][e], lane & 48, 64);
+        have_k = true;
+      }
+      st_n += nv;
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+        for (int fn = 0; fn < 2; ++fn)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float d = vm[fm] ? q[fm][fn][e] - st_k[fn][e] : 0.f;
+            st_a[fn][e] += d;
+            st_b[fn][e] = fmaf(d, d, st_b[fn][e]);
+          }
+    }
+    buf ^= 1;
+  }
+
+  // Workgroup partials: lane sums over the 16 pixels lanes, then the four waves in order.
+  if constexpr (EP != EP_RESID) {
+    float n16 = st_n;
+    n16 += __shfl_xor(n16, 1, 64); n16 += __shfl_xor(n16, 2, 64);
+    n16 += __shfl_xor(n16, 4, 64); n16 += __shfl_xor(n16, 8, 64);
+#pragma unroll
+    for (int fn = 0; fn < 2; ++fn)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        float x = st_a[fn][e], y = st_b[fn][e];
+        x += __shfl_xor(x, 1, 64); x += __shfl_xor(x, 2, 64);
+        x += __shfl_xor(x, 4, 64); x += __shfl_xor(x, 8, 64);
+        y += __shfl_xor(y, 1, 64); y += __shfl_xor(y, 2, 64);
+        y += __shfl_xor(y, 4, 64); y += __shfl_xor(y, 8, 64);
+        if constexpr (EP == EP_STATS) {
+          // (count, mean, centred M2) of this wave from the shifted sums
+          const float mean_d = n16 > 0.f ? x / n16 : 0.f;
+          st_a[fn][e] = st_k[fn][e] + mean_d;
+          st_b[fn][e] = n16 > 0.f ? fmaxf(y - x * mean_d, 0.f) : 0.f;
+        } else {
+          st_a[fn][e] = x;
+          st_b[fn][e] = y;
+        }
+      }
+    if (lr == 0) {
+#pragma unroll
+      for (int fn = 0; fn < 2; ++fn)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int c = fn * 16 + lg * 4 + e;
+          red[wave][0][c] = n16;
+          red[wave][1][c] = st_a[fn][e];
+          red[wave][2][c] = st_b[fn][e];
+        }
+    }
+    __syncthreads();
+    if (tid < 32) {
+      const int c = tid;
+      float* pr = a.partials;
+      const long row = static_cast<long>(blockIdx.x);
+      if constexpr (EP == EP_STATS) {
+        float n = 0.f, mean = 0.f, m2 = 0.f;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          const float nb = red[w][0][c];
+          if (nb > 0.f) {
+            const float nn = n + nb, rb = nb / nn, d = red[w][1][c] - mean;
+            mean += d * rb;
+            m2 += red[w][2][c] + d * d * n * rb;
+            n = nn;
+          }
+        }
+        pr[(row * 3 + 0) * 32 + c] = n;
+        pr[(row * 3 + 1) * 32 + c] = n * mean;
+        pr[(row * 3 + 2) * 32 + c] = m2;
+      } else {
+        const float s1 = (red[0][1][c] + red[1][1][c]) + (red[2][1][c] + red[3][1][c]);
+        const float s2 = (red[0][2][c] + red[1][2][c]) + (red[2][2][c] + red[3][2][c]);
+        pr[(row * 2 + 0) * 32 + c] = s1;
+        pr[(row * 2 + 1) * 32 + c] = s2;
+      }
+    }
+  }
+}
+
 // Weight gradient partials over one chunk of rows:
 //   part[split][o][k] = sum_{m in chunk} dh[m][o] * A[m][k]
 // BO x BK output tile, 4 waves in a 2 x 2 grid; rows advance 32 at a time.
@@ -1472,8 +1808,37 @@ bool launch_halo(const ConvArgs& a, int ep, hipStream_t st) {
   });
 }
 
+// Persistent 32 -> 32 kernel: tile geometry and grid (th == 0: not used).  It
+// wins where the image is wide enough for several tiles per workgroup (56 wide);
+// at 32 x 32 the one-shot halo kernel is faster.
+struct C32Shape { int th, tw, tiles, grid; };
+
+C32Shape conv32_shape(int dtype, const ConvArgs& a) {
+  C32Shape z{0, 0, 0, 0};
+  if (!(dtype == DT_BF16 && a.src2 == nullptr && a.r == 3 && a.s == 3 && a.stride == 1 &&
+        a.pad == 1 && a.c_in == 32 && a.c_out == 32 && a.p == a.h && a.q == a.w &&
+        a.k_tot == 288 && a.w == 56))
+    return z;
+  // byte offsets of the buffer loads/stores are 32-bit
+  if (static_cast<long>(a.n) * a.h * a.w * 64 >= static_cast<long>(BUF_OOB)) return z;
+  C32Shape c{4, 56, 0, 0};
+  c.tiles = ((a.w + c.tw - 1) / c.tw) * ((a.h + c.th - 1) / c.th) * a.n;
+  const int per = (c.tiles + 511) / 512;
+  c.grid = ((c.tiles + per - 1) / per + 7) / 8 * 8;
+  return c;
+}
+
+bool launch_conv32(const C32Shape& c, const ConvArgs& a, int ep, hipStream_t st) {
+  return dispatch_ep_pro(ep, pro_mode(a), [&](auto k) {
+    hipLaunchKernelGGL((conv32_kernel<4, 56, decltype(k)::ep, decltype(k)::pro>), dim3(c.grid),
+                       dim3(256), 0, st, a, c.tiles);
+  });
+}
+
 // Returns -1 when no halo kernel applies, else whether the launch was made.
 int launch_halo_any(int dtype, const ConvArgs& a, int ep, hipStream_t st) {
+  const C32Shape c32 = conv32_shape(dtype, a);
+  if (c32.th != 0) return launch_conv32(c32, a, ep, st) ? 1 : 0;
   const HaloShape h = halo_shape(dtype, a);
   if (h.tw == 0) return -1;
   bool ok;
@@ -1566,6 +1931,8 @@ void wgrad_t(const WgradArgs& a, hipStream_t st) {
 }  // namespace
 
 int conv_row_tiles(int dtype, const ConvArgs& a) {
+  const C32Shape c32 = conv32_shape(dtype, a);
+  if (c32.th != 0) return c32.grid;
   const HaloShape hs = halo_shape(dtype, a);
   if (hs.tw != 0) return ((a.w + hs.tw - 1) / hs.tw) * ((a.h + hs.th - 1) / hs.th) * a.n;
   int bm = CONV_BM;
