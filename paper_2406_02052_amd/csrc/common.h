@@ -85,6 +85,10 @@ template <> struct Raw8<bf16_t> {
     uint4 v = *reinterpret_cast<const uint4*>(p);
     w[0] = v.x; w[1] = v.y; w[2] = v.z; w[3] = v.w;
   }
+  template <typename V>
+  __device__ __forceinline__ void set(const V& v) {
+    w[0] = v[0]; w[1] = v[1]; w[2] = v[2]; w[3] = v[3];
+  }
   __device__ __forceinline__ void to_f32(float* o) const {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {

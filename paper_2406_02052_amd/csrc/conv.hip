@@ -425,37 +425,53 @@ __global__ __launch_bounds__(256) void conv_staged_kernel(ConvArgs a) {
     b_in[i] = q < BN * 4;
     b_ok[i] = b_in[i] && (n0 + b_col[i]) < a.c_out;
   }
-  const T* wt = static_cast<const T*>(a.wt);
-  const T* src = static_cast<const T*>(a.src);
-  const T* proh = static_cast<const T*>(a.pro_h);
+  // Buffer resources: rows outside the image and columns past c_out load zeros
+  // without branches, so the next step's loads stay in flight.
+  const long in_bytes = static_cast<long>(a.n) * a.h * a.w * a.c_in * 2;
+  const __amdgpu_buffer_rsrc_t r_src = make_rsrc(a.src, in_bytes);
+  const __amdgpu_buffer_rsrc_t r_proh = make_rsrc(PRO == PRO_BWD ? a.pro_h : a.src, in_bytes);
+  const __amdgpu_buffer_rsrc_t r_wt = make_rsrc(a.wt, static_cast<long>(a.c_out) * a.k_tot * 2);
   if constexpr (PRO != PRO_NONE) __syncthreads();
 
   Raw8<T> ra[A_CHUNKS], rb[B_CHUNKS];
+  Raw8<T> rah[PRO == PRO_BWD ? A_CHUNKS : 1];
+  uint32_t avalid = 0;
+  int step_c0 = 0;
   auto load_step = [&](int step) {
     const int tap = step / csteps;
     const int c0 = (step - tap * csteps) * 32;
     const int fr = tap / a.s, fs = tap - fr * a.s;
+    step_c0 = c0;
+    avalid = 0;
 #pragma unroll
     for (int i = 0; i < A_CHUNKS; ++i) {
       const int ih = a_ih0[i] + fr, iw = a_iw0[i] + fs;
       const int c = c0 + a_sub[i] * 8;
-      if (a_ok[i] && ih >= 0 && ih < a.h && iw >= 0 && iw < a.w) {
-        const long off = (a_pix0[i] + static_cast<long>(ih) * a.w + iw) * a.c_in + c;
-        ra[i].load(src + off);
-        Raw8<T> hr;
-        if constexpr (PRO == PRO_BWD) hr.load(proh + off);
-        pro8<T, PRO>(ra[i], hr, pro_tab[0], pro_tab[1], pro_tab[PRO == PRO_BWD ? 2 : 0],
-                     pro_tab[PRO == PRO_BWD ? 3 : 0], c);
-      } else {
-        ra[i].zero();
-      }
+      const bool ok = a_ok[i] && ih >= 0 && ih < a.h && iw >= 0 && iw < a.w;
+      const uint32_t off =
+          ok ? static_cast<uint32_t>(((a_pix0[i] + static_cast<long>(ih) * a.w + iw) * a.c_in + c) * 2) : BUF_OOB;
+      ra[i].set(buf_load16(r_src, off));
+      if constexpr (PRO == PRO_BWD) rah[i].set(buf_load16(r_proh, off));
+      avalid |= ok ? 1u << i : 0u;
     }
 #pragma unroll
     for (int i = 0; i < B_CHUNKS; ++i) {
-      if (b_ok[i])
-        rb[i].load(wt + static_cast<long>(n0 + b_col[i]) * a.k_tot + tap * a.c_in + c0 + b_sub[i] * 8);
-      else
-        rb[i].zero();
+      const uint32_t off =
+          b_ok[i] ? static_cast<uint32_t>(((n0 + b_col[i]) * a.k_tot + tap * a.c_in + c0 + b_sub[i] * 8) * 2)
+                  : BUF_OOB;
+      rb[i].set(buf_load16(r_wt, off));
+    }
+  };
+  // prologue of the loaded A chunks (padding stays zero)
+  auto pro_step = [&]() {
+    if constexpr (PRO != PRO_NONE) {
+#pragma unroll
+      for (int i = 0; i < A_CHUNKS; ++i) {
+        pro8<T, PRO>(ra[i], rah[PRO == PRO_BWD ? i : 0], pro_tab[0], pro_tab[1],
+                     pro_tab[PRO == PRO_BWD ? 2 : 0], pro_tab[PRO == PRO_BWD ? 3 : 0],
+                     step_c0 + a_sub[i] * 8);
+        if (!((avalid >> i) & 1u)) ra[i].zero();
+      }
     }
   };
   auto park = [&](int buf) {
@@ -479,6 +495,7 @@ __global__ __launch_bounds__(256) void conv_staged_kernel(ConvArgs a) {
     for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
   load_step(0);
+  pro_step();
   park(0);
   __syncthreads();
   for (int step = 0; step < steps; ++step) {
@@ -495,7 +512,10 @@ __global__ __launch_bounds__(256) void conv_staged_kernel(ConvArgs a) {
     for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
       for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma(af[fm], bfr[fn], acc[fm][fn]);
-    if (step + 1 < steps) park(buf ^ 1);
+    if (step + 1 < steps) {
+      pro_step();
+      park(buf ^ 1);
+    }
     __syncthreads();
   }
 
@@ -662,11 +682,16 @@ __global__ __launch_bounds__(256) void conv_halo_kernel(ConvArgs a) {
   const int n0 = blockIdx.y * BN;
   const int chunks = a.c_in / 32;
   const int steps = chunks * 9;
-  const T* src = static_cast<const T*>(a.src);
-  const T* wt = static_cast<const T*>(a.wt);
   const long img_base = static_cast<long>(img) * a.h * a.w;
 
-  const T* proh = static_cast<const T*>(a.pro_h);
+  // Operands come through buffer resources: padding and columns past c_out
+  // load as zeros without branches, so the next chunk's loads stay in flight
+  // while the current one is multiplied.
+  const __amdgpu_buffer_rsrc_t r_src =
+      make_rsrc(a.src, static_cast<long>(a.n) * a.h * a.w * a.c_in * 2);
+  const __amdgpu_buffer_rsrc_t r_proh =
+      make_rsrc(PRO == PRO_BWD ? a.pro_h : a.src, static_cast<long>(a.n) * a.h * a.w * a.c_in * 2);
+  const __amdgpu_buffer_rsrc_t r_wt = make_rsrc(a.wt, static_cast<long>(a.c_out) * a.k_tot * 2);
   Raw8<T> rh[H_CHUNKS], rb[B_CHUNKS];
   Raw8<T> rhh[PRO == PRO_BWD ? H_CHUNKS : 1];   // pro_h at the patch positions
   uint32_t hvalid = 0;   // bit i: patch chunk i lies inside the image
@@ -679,25 +704,24 @@ __global__ __launch_bounds__(256) void conv_halo_kernel(ConvArgs a) {
       const int hp = q >> 2, sub = q & 3;
       const int hy = hp / HTW, hx = hp - hy * HTW;
       const int ih = p0 - 1 + hy, iw = q0 - 1 + hx;
-      if (hp < HPIX && ih >= 0 && ih < a.h && iw >= 0 && iw < a.w) {
-        const long off = (img_base + static_cast<long>(ih) * a.w + iw) * a.c_in + c0 + sub * 8;
-        rh[i].load(src + off);
-        if constexpr (PRO == PRO_BWD) rhh[i].load(proh + off);
-        hvalid |= 1u << i;
-      } else {
-        rh[i].zero();
-      }
+      const bool ok = hp < HPIX && ih >= 0 && ih < a.h && iw >= 0 && iw < a.w;
+      const uint32_t off =
+          ok ? static_cast<uint32_t>(((img_base + static_cast<long>(ih) * a.w + iw) * a.c_in + c0 + sub * 8) * 2)
+             : BUF_OOB;
+      rh[i].set(buf_load16(r_src, off));
+      if constexpr (PRO == PRO_BWD) rhh[i].set(buf_load16(r_proh, off));
+      hvalid |= ok ? 1u << i : 0u;
     }
   };
-  // Prologue on the loaded patch (padding stays zero).
+  // Prologue on the loaded patch; padding stays zero.
   auto pro_patch = [&](int chunk) {
     if constexpr (PRO != PRO_NONE) {
 #pragma unroll
       for (int i = 0; i < H_CHUNKS; ++i) {
-        if (!(hvalid & (1u << i))) continue;
         const int c = chunk * 32 + ((tid + 256 * i) & 3) * 8;
         pro8<T, PRO>(rh[i], rhh[PRO == PRO_BWD ? i : 0], pro_tab[0], pro_tab[1],
                      pro_tab[PRO == PRO_BWD ? 2 : 0], pro_tab[PRO == PRO_BWD ? 3 : 0], c);
+        if (!((hvalid >> i) & 1u)) rh[i].zero();
       }
     }
   };
@@ -720,10 +744,10 @@ __global__ __launch_bounds__(256) void conv_halo_kernel(ConvArgs a) {
       const int tap = FB ? q / (BN * 4) : tap0;
       const int rem = FB ? q - (q / (BN * 4)) * (BN * 4) : q;
       const int col = rem >> 2, sub = rem & 3;
-      if (q < (FB ? 9 : 1) * BN * 4 && n0 + col < a.c_out)
-        rb[i].load(wt + static_cast<long>(n0 + col) * a.k_tot + tap * a.c_in + chunk * 32 + sub * 8);
-      else
-        rb[i].zero();
+      const bool ok = q < (FB ? 9 : 1) * BN * 4 && n0 + col < a.c_out;
+      const uint32_t off =
+          ok ? static_cast<uint32_t>(((n0 + col) * a.k_tot + tap * a.c_in + chunk * 32 + sub * 8) * 2) : BUF_OOB;
+      rb[i].set(buf_load16(r_wt, off));
     }
   };
   auto park_slab = [&](int buf) {
@@ -793,30 +817,37 @@ __global__ __launch_bounds__(256) void conv_halo_kernel(ConvArgs a) {
     }
     __syncthreads();   // the epilogue reuses the operand LDS
   }
-  for (int step = 0; step < (FB ? 0 : steps); ++step) {
-    const int chunk = step / 9, tap = step - chunk * 9;
-    const bool next_patch = HB > 1 && tap == 0 && chunk + 1 < chunks;
-    if (step + 1 < steps) load_slab(step + 1);
-    if (next_patch) load_patch(chunk + 1);
+  // Chunks x nine unrolled taps.  Every prefetch is unconditional (past the
+  // end it re-reads the last chunk / slab into the buffer not being read), so
+  // the number of loads in flight is fixed and the waits stay tight: the next
+  // chunk's patch is in flight for all nine taps, each next slab for one tap.
+  for (int chunk = 0; chunk < (FB ? 0 : chunks); ++chunk) {
+    if constexpr (HB > 1) load_patch(min(chunk + 1, chunks - 1));
     const T* pt = patch_base + (HB > 1 ? (chunk & 1) : 0) * PATCH;
-    const T* sb = slab_base + (step & 1) * SLAB;
-    const int fr = tap / 3, fs = tap - fr * 3;
-    const int toff = fr * HTW + fs;
-    Frag<T> af[FM], bfr[FN];
 #pragma unroll
-    for (int fm = 0; fm < FM; ++fm) af[fm].load(pt + (rowpix[fm] + toff) * HP + lg * 8);
+    for (int tap = 0; tap < 9; ++tap) {
+      const int step = chunk * 9 + tap;
+      load_slab(min(step + 1, steps - 1));
+      const T* sb = slab_base + (step & 1) * SLAB;
+      const int toff = (tap / 3) * HTW + (tap % 3);
+      Frag<T> af[FM], bfr[FN];
 #pragma unroll
-    for (int fn = 0; fn < FN; ++fn) bfr[fn].load(sb + (wn * TN + fn * 16 + lr) * BPITCH + lg * 8);
+      for (int fm = 0; fm < FM; ++fm) af[fm].load(pt + (rowpix[fm] + toff) * HP + lg * 8);
 #pragma unroll
-    for (int fm = 0; fm < FM; ++fm)
+      for (int fn = 0; fn < FN; ++fn) bfr[fn].load(sb + (wn * TN + fn * 16 + lr) * BPITCH + lg * 8);
 #pragma unroll
-      for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma(af[fm], bfr[fn], acc[fm][fn]);
-    if (step + 1 < steps) park_slab((step + 1) & 1);
-    if (next_patch) {
-      pro_patch(chunk + 1);
-      park_patch((chunk + 1) & 1);
+      for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+        for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma(af[fm], bfr[fn], acc[fm][fn]);
+      park_slab((step + 1) & 1);
+      if constexpr (HB > 1) {
+        if (tap == 8) {
+          pro_patch(min(chunk + 1, chunks - 1));
+          park_patch((chunk + 1) & 1);
+        }
+      }
+      __syncthreads();
     }
-    __syncthreads();
   }
 
   if constexpr (EP == EP_STATS) {
@@ -934,6 +965,601 @@ __global__ __launch_bounds__(256) void conv_halo_kernel(ConvArgs a) {
 #pragma unroll
       for (int w = 0; w < WAVES_M; ++w) t += red[w][which][cl];
       a.partials[(static_cast<long>(blockIdx.x) * 2 + which) * a.c_out + c] = t;
+    }
+  }
+}
+
+// Full-patch variant for the MFMA-bound 3x3 convs with several 32-channel input
+// chunks (C_in = 32 * CH).  The workgroup loads the whole (TH+2) x (TW+2)
+// input patch of all chunks into LDS once (chunk c + 1 in flight while chunk c
+// gets its prologue and is parked), then runs the CH x 9 (chunk, tap) steps
+// with no barrier: patch fragments come from LDS and weight fragments straight
+// from L2 into a ring of registers issued three steps ahead, so the MFMAs never
+// wait on a load issued in the same step.
+template <int TH, int TW, int BN, int WAVES_M, int CH, int EP, int PRO>
+__global__ __launch_bounds__(256, 2) void conv_fp_kernel(ConvArgs a) {
+  using T = bf16_t;
+  constexpr int BM = TH * TW;
+  constexpr int WAVES_N = 4 / WAVES_M;
+  constexpr int TM = BM / WAVES_M, TN = BN / WAVES_N;
+  constexpr int FM = TM / 16, FN = TN / 16;
+  static_assert(TM % 16 == 0 && TN % 16 == 0, "tile");
+  constexpr int HTH = TH + 2, HTW = TW + 2, HPIX = HTH * HTW;
+  constexpr int HP = 40;                              // bf16 per patch pixel and chunk (32 + pad)
+  constexpr int PLANE = HPIX * HP;                    // one chunk of the patch
+  constexpr int P_CHUNKS = (HPIX * 4 + 255) / 256;    // 16-byte loads per thread and chunk
+  constexpr int STEPS = CH * 9;
+  constexpr int D = 3;                                // weight prefetch depth (steps)
+  constexpr int MAIN_BYTES = CH * PLANE * 2;
+  constexpr int EPI_BYTES = 4 * TN * EP_RP * 4;
+  constexpr int LDS_BYTES = MAIN_BYTES > EPI_BYTES ? MAIN_BYTES : EPI_BYTES;
+  constexpr bool BWD = PRO == PRO_BWD;
+  __shared__ __attribute__((aligned(16))) unsigned char lds[LDS_BYTES];
+  __shared__ float pro_tab[BWD ? 4 : 2][PRO == PRO_NONE ? 1 : CH * 32];
+  __shared__ float red[WAVES_M][2][BN];
+
+  T* patch = reinterpret_cast<T*>(lds);
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wm = wave % WAVES_M, wn = wave / WAVES_M;
+  const int lr = lane & 15, lg = lane >> 4;
+  const int tiles_x = (a.w + TW - 1) / TW, tiles_y = (a.h + TH - 1) / TH;
+  const int tx = blockIdx.x % tiles_x;
+  const int ty = (blockIdx.x / tiles_x) % tiles_y;
+  const int img = blockIdx.x / (tiles_x * tiles_y);
+  const int p0 = ty * TH, q0 = tx * TW;
+  const int n0 = blockIdx.y * BN;
+  const long img_base = static_cast<long>(img) * a.h * a.w;
+  const long in_bytes = static_cast<long>(a.n) * a.h * a.w * a.c_in * 2;
+  const __amdgpu_buffer_rsrc_t r_src = make_rsrc(a.src, in_bytes);
+  const __amdgpu_buffer_rsrc_t r_proh = make_rsrc(BWD ? a.pro_h : a.src, in_bytes);
+  const __amdgpu_buffer_rsrc_t r_wt = make_rsrc(a.wt, static_cast<long>(a.c_out) * a.k_tot * 2);
+
+  // Weight fragments of step s: lane (lr, lg) of fragment fn holds output
+  // channel n0 + wn*TN + fn*16 + lr, k = tap*C_in + chunk*32 + lg*8 .. +7.
+  uint32_t wrow[FN];
+#pragma unroll
+  for (int fn = 0; fn < FN; ++fn) {
+    const int col = n0 + wn * TN + fn * 16 + lr;
+    wrow[fn] = col < a.c_out ? static_cast<uint32_t>(col * a.k_tot + lg * 8) * 2u : BUF_OOB;
+  }
+  Frag<T> wb[D][FN];
+  auto load_w = [&](int s, int slot) {
+    const int chunk = s / 9, tap = s - chunk * 9;
+    const uint32_t koff = static_cast<uint32_t>(tap * a.c_in + chunk * 32) * 2u;
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn) {
+      const uint32_t off = wrow[fn] == BUF_OOB ? BUF_OOB : wrow[fn] + koff;
+      wb[slot][fn].v = __builtin_bit_cast(bf16x8_t, buf_load16(r_wt, off));
+    }
+  };
+#pragma unroll
+  for (int d = 0; d < D; ++d) load_w(d, d);
+
+  if constexpr (PRO == PRO_RELU) {
+    for (int i = tid; i < a.c_in; i += 256) {
+      pro_tab[0][i] = a.pro_scale[i];
+      pro_tab[1][i] = a.pro_shift[i];
+    }
+  } else if constexpr (BWD) {
+    for (int i = tid; i < a.c_in; i += 256) {
+      pro_tab[0][i] = a.pro_ca[i];
+      pro_tab[1][i] = a.pro_cb[i];
+      pro_tab[2][i] = a.pro_cc[i];
+      pro_tab[3][i] = a.pro_mean[i];
+    }
+  }
+
+  // Patch fill, one chunk at a time with the next chunk's loads in flight.
+  int p_off[P_CHUNKS];
+  uint32_t pvalid = 0;
+#pragma unroll
+  for (int i = 0; i < P_CHUNKS; ++i) {
+    const int q = tid + 256 * i;
+    const int hp = q >> 2, sub = q & 3;
+    const int hy = hp / HTW, hx = hp - hy * HTW;
+    const int ih = p0 - 1 + hy, iw = q0 - 1 + hx;
+    const bool ok = hp < HPIX && ih >= 0 && ih < a.h && iw >= 0 && iw < a.w;
+    p_off[i] = ok ? static_cast<int>(((img_base + static_cast<long>(ih) * a.w + iw) * a.c_in + sub * 8) * 2) : -1;
+    pvalid |= ok ? 1u << i : 0u;
+  }
+  Raw8<T> ph[2][P_CHUNKS], phh[2][BWD ? P_CHUNKS : 1];
+  auto load_chunk = [&](int c, int slot) {
+#pragma unroll
+    for (int i = 0; i < P_CHUNKS; ++i) {
+      const uint32_t off = p_off[i] >= 0 ? static_cast<uint32_t>(p_off[i] + c * 64) : BUF_OOB;
+      ph[slot][i].set(buf_load16(r_src, off));
+      if constexpr (BWD) phh[slot][i].set(buf_load16(r_proh, off));
+    }
+  };
+  auto park_chunk = [&](int c, int slot) {
+    T* dst = patch + c * PLANE;
+#pragma unroll
+    for (int i = 0; i < P_CHUNKS; ++i) {
+      const int q = tid + 256 * i;
+      const int hp = q >> 2, sub = q & 3;
+      if (hp >= HPIX) continue;
+      Raw8<T> r = ph[slot][i];
+      if constexpr (PRO != PRO_NONE) {
+        pro8<T, PRO>(r, phh[slot][BWD ? i : 0], pro_tab[0], pro_tab[1], pro_tab[BWD ? 2 : 0],
+                     pro_tab[BWD ? 3 : 0], c * 32 + sub * 8);
+        if (!((pvalid >> i) & 1u)) r.zero();
+      }
+      *reinterpret_cast<uint4*>(dst + hp * HP + sub * 8) = make_uint4(r.w[0], r.w[1], r.w[2], r.w[3]);
+    }
+  };
+  load_chunk(0, 0);
+  if constexpr (PRO != PRO_NONE) __syncthreads();   // prologue table
+#pragma unroll
+  for (int c = 0; c < CH; ++c) {
+    if (c + 1 < CH) load_chunk(c + 1, (c + 1) & 1);
+    park_chunk(c, c & 1);
+  }
+  __syncthreads();
+
+  int rowpix[FM];
+#pragma unroll
+  for (int fm = 0; fm < FM; ++fm) {
+    const int i = wm * TM + fm * 16 + lr;
+    const int ph_ = i / TW, pw = i - ph_ * TW;
+    rowpix[fm] = ph_ * HTW + pw;
+  }
+  f32x4_t acc[FM][FN];
+#pragma unroll
+  for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  // Patch fragments of step s (double-buffered one step ahead).
+  Frag<T> af[2][FM];
+  auto load_a = [&](int s, int buf) {
+    const int chunk = s / 9, tap = s - chunk * 9;
+    const T* pt = patch + chunk * PLANE + ((tap / 3) * HTW + (tap % 3)) * HP + lg * 8;
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm) af[buf][fm].load(pt + rowpix[fm] * HP);
+  };
+  load_a(0, 0);
+#pragma unroll
+  for (int s = 0; s < STEPS; ++s) {
+    const int slot = s % D;
+    Frag<T> cur[FN];
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn) cur[fn] = wb[slot][fn];
+    // refill this slot D steps ahead (past the end: reload the last step) and
+    // fetch the next step's patch fragments; the scheduling barriers keep the
+    // compiler from sinking these loads down to their uses
+    load_w(s + D < STEPS ? s + D : STEPS - 1, slot);
+    if (s + 1 < STEPS) load_a(s + 1, (s + 1) & 1);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+      for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma(af[s & 1][fm], cur[fn], acc[fm][fn]);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  __syncthreads();   // the epilogue reuses the patch LDS
+
+  if constexpr (EP == EP_STATS) {
+    tile_stats<T, FM, FN, WAVES_M, TN, BN>(
+        acc,
+        [&](int fm, int j) {
+          const int i = wm * TM + fm * 16 + lg * 4 + j;
+          const int ph = i / TW;
+          return p0 + ph < a.h && q0 + (i - ph * TW) < a.w;
+        },
+        wm, wn, lane, n0, a.c_out, a.partials, blockIdx.x);
+  }
+  // Epilogue (as in the staged kernel, pixels mapped back to NHWC rows).
+  float* ep = reinterpret_cast<float*>(lds) + wave * TN * EP_RP;
+  constexpr int CG = TN / 8;
+  constexpr int TASKS = 16 * CG;
+  const int my_cg = lane % CG;
+  const int col = n0 + wn * TN + my_cg * 8;
+  const bool cvalid = col < a.c_out;
+  float s1[8], s2[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) s1[j] = s2[j] = 0.f;
+  float es[8], esh[8], emu[8], ers[8];
+  if constexpr (EP == EP_MASK || EP == EP_RESID_STATS) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      es[j] = cvalid && EP == EP_MASK ? a.ep_scale[col + j] : 0.f;
+      esh[j] = cvalid && EP == EP_MASK ? a.ep_shift[col + j] : 0.f;
+      emu[j] = cvalid ? a.ep_mean[col + j] : 0.f;
+      ers[j] = cvalid ? a.ep_rstd[col + j] : 0.f;
+    }
+  }
+  T* out = static_cast<T*>(a.out);
+#pragma unroll
+  for (int fm = 0; fm < FM; ++fm) {
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn)
+      *reinterpret_cast<f32x4_t*>(ep + (fn * 16 + lr) * EP_RP + lg * 4) = acc[fm][fn];
+    __syncthreads();
+    for (int t = lane; t < TASKS; t += 64) {
+      const int rr = t / CG;
+      const int i = wm * TM + fm * 16 + rr;
+      const int ph = i / TW, pw = i - ph * TW;
+      const int pp = p0 + ph, qq = q0 + pw;
+      if (!(cvalid && pp < a.h && qq < a.w)) continue;
+      float v[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[j] = ep[(my_cg * 8 + j) * EP_RP + rr];
+      const long idx = (img_base + static_cast<long>(pp) * a.w + qq) * a.c_out + col;
+      Raw8<T> o;
+      if constexpr (EP == EP_STATS) {
+        o.from_f32(v);
+      } else if constexpr (EP == EP_MASK) {
+        Raw8<T> hr;
+        hr.load(static_cast<const T*>(a.ep_h) + idx);
+        float hl[8];
+        hr.to_f32(hl);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = fmaf(es[j], hl[j], esh[j]) > 0.f ? v[j] : 0.f;
+        o.from_f32(v);
+        o.to_f32(v);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          s1[j] += v[j];
+          s2[j] += v[j] * ((hl[j] - emu[j]) * ers[j]);
+        }
+      } else {
+        if (a.resid != nullptr) {  // without a residual the epilogue is a plain store
+          Raw8<T> rr8;
+          rr8.load(static_cast<const T*>(a.resid) + idx);
+          float rv[8];
+          rr8.to_f32(rv);
+#pragma unroll
+          for (int j = 0; j < 8; ++j) v[j] += rv[j];
+        }
+        o.from_f32(v);
+        if constexpr (EP == EP_RESID_STATS) {  // BN-backward partials of the stored values
+          Raw8<T> hr;
+          hr.load(static_cast<const T*>(a.ep_h) + idx);
+          float hl[8];
+          hr.to_f32(hl);
+          o.to_f32(v);
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            s1[j] += v[j];
+            s2[j] += v[j] * ((hl[j] - emu[j]) * ers[j]);
+          }
+        }
+      }
+      *reinterpret_cast<uint4*>(out + idx) = make_uint4(o.w[0], o.w[1], o.w[2], o.w[3]);
+    }
+    __syncthreads();
+  }
+  if constexpr (EP == EP_MASK || EP == EP_RESID_STATS) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      for (int off = CG; off < 64; off <<= 1) {
+        s1[j] += __shfl_xor(s1[j], off, 64);
+        s2[j] += __shfl_xor(s2[j], off, 64);
+      }
+    }
+    if (lane < CG) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        red[wm][0][wn * TN + lane * 8 + j] = s1[j];
+        red[wm][1][wn * TN + lane * 8 + j] = s2[j];
+      }
+    }
+    __syncthreads();
+    for (int i = tid; i < 2 * BN; i += 256) {
+      const int which = i / BN, cl = i - which * BN;
+      const int c = n0 + cl;
+      if (c >= a.c_out) continue;
+      float t = 0.f;
+#pragma unroll
+      for (int w = 0; w < WAVES_M; ++w) t += red[w][which][cl];
+      a.partials[(static_cast<long>(blockIdx.x) * 2 + which) * a.c_out + c] = t;
+    }
+  }
+}
+
+// Whole-image 3x3 / stride 1 / pad 1 conv for the MFMA-bound shapes: one
+// 512-thread workgroup per TH x TW image, C_in = 32 * CH, C_out = 128.
+//  * The (TH+2) x (TW+2) input patch of every input chunk is loaded into LDS
+//    once (prologue applied there, chunk c + 1 in flight while chunk c parks).
+//  * The reduction runs in k order (k = tap * C_in + c), so two consecutive
+//    32-wide steps are one contiguous 128-byte run of every weight row: the
+//    workgroup stages weight slabs of two steps through a double-buffered LDS
+//    slab with full-line loads issued one slab ahead, one barrier per slab.
+//  * The MFMA is issued as D[cout][pixel] = W x patch^T: each lane ends with 4
+//    consecutive output channels of one pixel, stored directly (8 bytes), and
+//    the BN statistics are shifted sums in registers reduced once at the end.
+// Partial row of the statistics = blockIdx.x (the image).
+template <int TH, int TW, int CH, int EP, int PRO>
+__global__ __launch_bounds__(512, 1) void conv_img_kernel(ConvArgs a) {
+  using T = bf16_t;
+  constexpr int NT = 512;
+  constexpr int WAVES_M = 4, WAVES_N = 2;
+  constexpr int BN = 128, BM = TH * TW;
+  constexpr int TM = BM / WAVES_M, TN = BN / WAVES_N;
+  constexpr int FM = TM / 16, FN = TN / 16;
+  static_assert(TM % 16 == 0 && BM % 64 == 0, "tile");
+  constexpr int HTH = TH + 2, HTW = TW + 2, HPIX = HTH * HTW;
+  constexpr int HP = 40;                             // bf16 per patch pixel and chunk (32 + pad)
+  constexpr int PLANE = HPIX * HP;
+  constexpr int P_CHUNKS = (HPIX * 4 + NT - 1) / NT;
+  constexpr int STEPS = CH * 9;                      // 32-wide k steps
+  static_assert(STEPS % 2 == 0, "two steps per slab");
+  constexpr int SLABS = STEPS / 2;
+  constexpr int SP = 72;                             // bf16 per weight row of a slab (64 + pad)
+  constexpr int SLAB = BN * SP;
+  constexpr int S_CHUNKS = BN * 8 / NT;              // 16-byte weight loads per thread and slab
+  constexpr bool BWD = PRO == PRO_BWD;
+  constexpr bool STATS = EP == EP_STATS;
+  __shared__ __attribute__((aligned(16))) T lds[CH * PLANE + 2 * SLAB];
+  __shared__ float pro_tab[BWD ? 4 : 2][PRO == PRO_NONE ? 1 : CH * 32];
+  __shared__ float red[WAVES_M][3][BN];
+
+  T* patch = lds;
+  T* slabs = lds + CH * PLANE;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wm = wave % WAVES_M, wn = wave / WAVES_M;
+  const int lr = lane & 15, lg = lane >> 4;
+  const int img = blockIdx.x;
+  const long img_base = static_cast<long>(img) * a.h * a.w;
+  const long in_bytes = static_cast<long>(a.n) * a.h * a.w * a.c_in * 2;
+  const long out_bytes = static_cast<long>(a.m) * BN * 2;
+  const __amdgpu_buffer_rsrc_t r_src = make_rsrc(a.src, in_bytes);
+  const __amdgpu_buffer_rsrc_t r_proh = make_rsrc(BWD ? a.pro_h : a.src, in_bytes);
+  const __amdgpu_buffer_rsrc_t r_wt = make_rsrc(a.wt, static_cast<long>(BN) * a.k_tot * 2);
+  const __amdgpu_buffer_rsrc_t r_out = make_rsrc(a.out, out_bytes);
+  const __amdgpu_buffer_rsrc_t r_eph = make_rsrc(a.ep_h != nullptr ? a.ep_h : a.out, out_bytes);
+  const __amdgpu_buffer_rsrc_t r_res = make_rsrc(a.resid != nullptr ? a.resid : a.out,
+                                                 a.resid != nullptr ? out_bytes : 0);
+
+  // Weight slab j holds k = 64 j .. 64 j + 63 of every output channel; thread
+  // q loads 16 bytes of row q / 8, so 8 neighbouring threads read one row's
+  // 128 bytes.
+  Raw8<T> rs[S_CHUNKS];
+  auto load_slab = [&](int j) {
+#pragma unroll
+    for (int i = 0; i < S_CHUNKS; ++i) {
+      const int q = tid + NT * i;
+      const int row = q >> 3, sub = q & 7;
+      rs[i].set(buf_load16(r_wt, static_cast<uint32_t>((row * a.k_tot + j * 64 + sub * 8) * 2)));
+    }
+  };
+  auto park_slab = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < S_CHUNKS; ++i) {
+      const int q = tid + NT * i;
+      const int row = q >> 3, sub = q & 7;
+      *reinterpret_cast<uint4*>(slabs + buf * SLAB + row * SP + sub * 8) =
+          make_uint4(rs[i].w[0], rs[i].w[1], rs[i].w[2], rs[i].w[3]);
+    }
+  };
+  load_slab(0);
+
+  if constexpr (PRO == PRO_RELU) {
+    for (int i = tid; i < a.c_in; i += NT) {
+      pro_tab[0][i] = a.pro_scale[i];
+      pro_tab[1][i] = a.pro_shift[i];
+    }
+  } else if constexpr (BWD) {
+    for (int i = tid; i < a.c_in; i += NT) {
+      pro_tab[0][i] = a.pro_ca[i];
+      pro_tab[1][i] = a.pro_cb[i];
+      pro_tab[2][i] = a.pro_cc[i];
+      pro_tab[3][i] = a.pro_mean[i];
+    }
+  }
+
+  // Patch fill, one chunk at a time with the next chunk's loads in flight.
+  int p_off[P_CHUNKS];
+  uint32_t pvalid = 0;
+#pragma unroll
+  for (int i = 0; i < P_CHUNKS; ++i) {
+    const int q = tid + NT * i;
+    const int hp = q >> 2, sub = q & 3;
+    const int hy = hp / HTW, hx = hp - hy * HTW;
+    const int ih = hy - 1, iw = hx - 1;
+    const bool ok = hp < HPIX && ih >= 0 && ih < a.h && iw >= 0 && iw < a.w;
+    p_off[i] = ok ? static_cast<int>(((img_base + static_cast<long>(ih) * a.w + iw) * a.c_in + sub * 8) * 2) : -1;
+    pvalid |= ok ? 1u << i : 0u;
+  }
+  Raw8<T> ph[2][P_CHUNKS], phh[2][BWD ? P_CHUNKS : 1];
+  auto load_chunk = [&](int c, int slot) {
+#pragma unroll
+    for (int i = 0; i < P_CHUNKS; ++i) {
+      const uint32_t off = p_off[i] >= 0 ? static_cast<uint32_t>(p_off[i] + c * 64) : BUF_OOB;
+      ph[slot][i].set(buf_load16(r_src, off));
+      if constexpr (BWD) phh[slot][i].set(buf_load16(r_proh, off));
+    }
+  };
+  auto park_chunk = [&](int c, int slot) {
+    T* dst = patch + c * PLANE;
+#pragma unroll
+    for (int i = 0; i < P_CHUNKS; ++i) {
+      const int q = tid + NT * i;
+      const int hp = q >> 2, sub = q & 3;
+      if (hp >= HPIX) continue;
+      Raw8<T> r = ph[slot][i];
+      if constexpr (PRO != PRO_NONE) {
+        pro8<T, PRO>(r, phh[slot][BWD ? i : 0], pro_tab[0], pro_tab[1], pro_tab[BWD ? 2 : 0],
+                     pro_tab[BWD ? 3 : 0], c * 32 + sub * 8);
+        if (!((pvalid >> i) & 1u)) r.zero();
+      }
+      *reinterpret_cast<uint4*>(dst + hp * HP + sub * 8) = make_uint4(r.w[0], r.w[1], r.w[2], r.w[3]);
+    }
+  };
+  load_chunk(0, 0);
+  if constexpr (PRO != PRO_NONE) __syncthreads();   // prologue table
+#pragma unroll
+  for (int c = 0; c < CH; ++c) {
+    if (c + 1 < CH) load_chunk(c + 1, (c + 1) & 1);
+    park_chunk(c, c & 1);
+  }
+  park_slab(0);
+  __syncthreads();
+
+  int rowpix[FM];
+#pragma unroll
+  for (int fm = 0; fm < FM; ++fm) {
+    const int i = wm * TM + fm * 16 + lr;
+    const int ph_ = i / TW, pw = i - ph_ * TW;
+    rowpix[fm] = ph_ * HTW + pw;
+  }
+  f32x4_t acc[FM][FN];
+#pragma unroll
+  for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  for (int j = 0; j < SLABS; ++j) {
+    const int buf = j & 1;
+    load_slab(min(j + 1, SLABS - 1));   // past the end: reload the last slab (not parked)
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int s = 2 * j + u;              // k = 32 s .. 32 s + 31
+      const int tap = s / CH, chunk = s - tap * CH;
+      const T* pt = patch + chunk * PLANE + ((tap / 3) * HTW + (tap % 3)) * HP + lg * 8;
+      const T* sb = slabs + buf * SLAB + (wn * TN + lr) * SP + u * 32 + lg * 8;
+      Frag<T> wf[FN], pf[FM];
+#pragma unroll
+      for (int fn = 0; fn < FN; ++fn) wf[fn].load(sb + fn * 16 * SP);
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm) pf[fm].load(pt + rowpix[fm] * HP);
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+        for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma(wf[fn], pf[fm], acc[fm][fn]);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    if (j + 1 < SLABS) park_slab(buf ^ 1);
+    __syncthreads();
+  }
+
+  // Epilogue: lane (lr, lg) holds channels wn*TN + fn*16 + lg*4 + e of pixel
+  // wm*TM + fm*16 + lr.
+  float es[FN][4], esh[FN][4], emu[FN][4], ers[FN][4];
+  if constexpr (EP == EP_MASK || EP == EP_RESID_STATS) {
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int c = wn * TN + fn * 16 + lg * 4 + e;
+        es[fn][e] = EP == EP_MASK ? a.ep_scale[c] : 0.f;
+        esh[fn][e] = EP == EP_MASK ? a.ep_shift[c] : 0.f;
+        emu[fn][e] = a.ep_mean[c];
+        ers[fn][e] = a.ep_rstd[c];
+      }
+  }
+  float sa[FN][4], sb2[FN][4], kk[FN][4];
+#pragma unroll
+  for (int fn = 0; fn < FN; ++fn)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) sa[fn][e] = sb2[fn][e] = kk[fn][e] = 0.f;
+  float nv = 0.f;
+#pragma unroll
+  for (int fm = 0; fm < FM; ++fm) {
+    const int i = wm * TM + fm * 16 + lr;
+    const int ph_ = i / TW, pw = i - ph_ * TW;
+    const bool vm = ph_ < a.h && pw < a.w;
+    nv += vm ? 1.f : 0.f;
+    const uint32_t pixoff = vm ? static_cast<uint32_t>(((img_base + static_cast<long>(ph_) * a.w + pw) * BN) * 2) : BUF_OOB;
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn) {
+      const uint32_t boff = vm ? pixoff + (wn * TN + fn * 16 + lg * 4) * 2 : BUF_OOB;
+      float v[4] = {acc[fm][fn][0], acc[fm][fn][1], acc[fm][fn][2], acc[fm][fn][3]};
+      float hl[4] = {0.f, 0.f, 0.f, 0.f};
+      if constexpr (EP == EP_MASK || EP == EP_RESID_STATS) {
+        const u32x2_t hw = buf_load8(r_eph, boff);
+        hl[0] = __uint_as_float(hw.x << 16); hl[1] = __uint_as_float(hw.x & 0xffff0000u);
+        hl[2] = __uint_as_float(hw.y << 16); hl[3] = __uint_as_float(hw.y & 0xffff0000u);
+      }
+      if constexpr (EP == EP_RESID || EP == EP_RESID_STATS) {
+        const u32x2_t rw = buf_load8(r_res, boff);   // a null residual reads zeros
+        v[0] += __uint_as_float(rw.x << 16); v[1] += __uint_as_float(rw.x & 0xffff0000u);
+        v[2] += __uint_as_float(rw.y << 16); v[3] += __uint_as_float(rw.y & 0xffff0000u);
+      }
+      if constexpr (EP == EP_MASK) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = fmaf(es[fn][e], hl[e], esh[fn][e]) > 0.f ? v[e] : 0.f;
+      }
+      const uint32_t w0 = pack_bf16x2(v[0], v[1]), w1 = pack_bf16x2(v[2], v[3]);
+      buf_store8(u32x2_t{w0, w1}, r_out, boff);
+      // statistics of the stored values
+      v[0] = __uint_as_float(w0 << 16); v[1] = __uint_as_float(w0 & 0xffff0000u);
+      v[2] = __uint_as_float(w1 << 16); v[3] = __uint_as_float(w1 & 0xffff0000u);
+      if constexpr (STATS) {
+        if (fm == 0) {
+          // shift per channel: the value at this wave's first pixel
+#pragma unroll
+          for (int e = 0; e < 4; ++e) kk[fn][e] = __shfl(v[e], lane & 48, 64);
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float d = vm ? v[e] - kk[fn][e] : 0.f;
+          sa[fn][e] += d;
+          sb2[fn][e] = fmaf(d, d, sb2[fn][e]);
+        }
+      } else if constexpr (EP != EP_RESID) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float g = vm ? v[e] : 0.f;
+          sa[fn][e] += g;
+          sb2[fn][e] += g * ((hl[e] - emu[fn][e]) * ers[fn][e]);
+        }
+      }
+    }
+  }
+  if constexpr (EP != EP_RESID) {
+    float n16 = nv;
+    n16 += __shfl_xor(n16, 1, 64); n16 += __shfl_xor(n16, 2, 64);
+    n16 += __shfl_xor(n16, 4, 64); n16 += __shfl_xor(n16, 8, 64);
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        float x = sa[fn][e], y = sb2[fn][e];
+        x += __shfl_xor(x, 1, 64); x += __shfl_xor(x, 2, 64);
+        x += __shfl_xor(x, 4, 64); x += __shfl_xor(x, 8, 64);
+        y += __shfl_xor(y, 1, 64); y += __shfl_xor(y, 2, 64);
+        y += __shfl_xor(y, 4, 64); y += __shfl_xor(y, 8, 64);
+        if (lr == 0) {
+          const int c = wn * TN + fn * 16 + lg * 4 + e;
+          if constexpr (STATS) {
+            const float md = n16 > 0.f ? x / n16 : 0.f;
+            red[wm][0][c] = n16;
+            red[wm][1][c] = kk[fn][e] + md;                          // mean
+            red[wm][2][c] = n16 > 0.f ? fmaxf(y - x * md, 0.f) : 0.f;  // centred M2
+          } else {
+            red[wm][1][c] = x;
+            red[wm][2][c] = y;
+          }
+        }
+      }
+    __syncthreads();
+    if (tid < BN) {
+      const int c = tid;
+      float* pr = a.partials;
+      const long row = static_cast<long>(blockIdx.x);
+      if constexpr (STATS) {
+        float n = 0.f, mean = 0.f, m2 = 0.f;
+#pragma unroll
+        for (int w = 0; w < WAVES_M; ++w) {
+          const float nb = red[w][0][c];
+          if (nb > 0.f) {
+            const float nn = n + nb, rb = nb / nn, d = red[w][1][c] - mean;
+            mean += d * rb;
+            m2 += red[w][2][c] + d * d * n * rb;
+            n = nn;
+          }
+        }
+        pr[(row * 3 + 0) * BN + c] = n;
+        pr[(row * 3 + 1) * BN + c] = n * mean;
+        pr[(row * 3 + 2) * BN + c] = m2;
+      } else {
+        pr[(row * 2 + 0) * BN + c] = (red[0][1][c] + red[1][1][c]) + (red[2][1][c] + red[3][1][c]);
+        pr[(row * 2 + 1) * BN + c] = (red[0][2][c] + red[1][2][c]) + (red[2][2][c] + red[3][2][c]);
+      }
     }
   }
 }
@@ -1380,7 +2006,7 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a) {
 // double-buffered LDS, and each thread transposes a pair of rows into 32-bit
 // LDS words (two consecutive m of one channel), so both operands become
 // m-contiguous rows that feed MFMA directly.
-template <int BO, int BK, bool PRO>
+template <int BO, int BK, bool PRO, bool CAT>
 __global__ __launch_bounds__(256) void wgrad_staged_kernel(WgradArgs a) {
   using T = bf16_t;
   constexpr int RS = 64;                    // rows (m) per step
@@ -1424,27 +2050,87 @@ __global__ __launch_bounds__(256) void wgrad_staged_kernel(WgradArgs a) {
   float dk[4][8];
   dh_coeffs(a, a_o, dk);
 
-  Raw8<T> ra[2], rb[2];
+  Raw8<T> ra[2], rb[2], rah[2];
+  uint32_t aval = 0, bval = 0;
+  // Without a concatenated second input, operands come through buffer
+  // resources: rows past the split, padding and channels past the end load
+  // zeros without branches, so the next step's loads stay in flight.  The
+  // BN-backward (dh) and BN-apply + ReLU prologues run when the step is parked.
+  const long in_bytes = static_cast<long>(a.n) * a.h * a.w * a.c_split * 2;
+  const long out_bytes = static_cast<long>(a.m) * a.c_out * 2;
+  const __amdgpu_buffer_rsrc_t r_src = make_rsrc(a.src, in_bytes);
+  const __amdgpu_buffer_rsrc_t r_dh = make_rsrc(a.dh, out_bytes);
+  const __amdgpu_buffer_rsrc_t r_dhh = make_rsrc(dhb ? a.dh_h : a.dh, out_bytes);
   auto load_step = [&](int step) {
     const int mb = m_begin + step * RS;
+    aval = bval = 0;
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
       const int m = mb + 2 * a_pair + e;
-      if (a_ook && m < m_end) {
-        ra[e].load(dh + static_cast<long>(m) * a.c_out + a_o);
-        if (dhb) dh_bwd8(ra[e], static_cast<const T*>(a.dh_h) + static_cast<long>(m) * a.c_out + a_o, dk);
-      } else {
-        ra[e].zero();
-      }
       const int mm = mb + 2 * b_pair + e;
-      RowPos rp;
-      rp.valid = b_on && mm < m_end;
-      const int m2 = rp.valid ? mm : 0;
-      rp.n = m2 / pq;
-      const int rem = m2 - rp.n * pq;
-      rp.p = rem / a.q;
-      rp.q = rem - rp.p * a.q;
-      gather_a<T, PRO ? PRO_RELU : PRO_NONE>(ca, rp, kb_ok, fr, fs, cb, rb[e]);
+      if constexpr (!CAT) {
+        const bool oka = a_ook && m < m_end;
+        const uint32_t offa = oka ? static_cast<uint32_t>((static_cast<long>(m) * a.c_out + a_o) * 2) : BUF_OOB;
+        ra[e].set(buf_load16(r_dh, offa));
+        rah[e].set(buf_load16(r_dhh, offa));
+        aval |= oka ? 1u << e : 0u;
+        const bool vb = b_on && mm < m_end;
+        const int m2 = vb ? mm : 0;
+        const int n = m2 / pq;
+        const int rem = m2 - n * pq;
+        const int pp = rem / a.q, qq = rem - pp * a.q;
+        const int ih = pp * a.stride + fr - a.pad, iw = qq * a.stride + fs - a.pad;
+        const bool okb = vb && kb_ok && ih >= 0 && ih < a.h && iw >= 0 && iw < a.w;
+        const uint32_t offb =
+            okb ? static_cast<uint32_t>((((static_cast<long>(n) * a.h + ih) * a.w + iw) * a.c_split + cb) * 2) : BUF_OOB;
+        rb[e].set(buf_load16(r_src, offb));
+        bval |= okb ? 1u << e : 0u;
+      } else {
+        if (a_ook && m < m_end) {
+          ra[e].load(dh + static_cast<long>(m) * a.c_out + a_o);
+          if (dhb) dh_bwd8(ra[e], static_cast<const T*>(a.dh_h) + static_cast<long>(m) * a.c_out + a_o, dk);
+        } else {
+          ra[e].zero();
+        }
+        RowPos rp;
+        rp.valid = b_on && mm < m_end;
+        const int m2 = rp.valid ? mm : 0;
+        rp.n = m2 / pq;
+        const int rem = m2 - rp.n * pq;
+        rp.p = rem / a.q;
+        rp.q = rem - rp.p * a.q;
+        gather_a<T, PRO ? PRO_RELU : PRO_NONE>(ca, rp, kb_ok, fr, fs, cb, rb[e]);
+      }
+    }
+  };
+  float bsc[8], bsh[8];   // BN-apply of this thread's 8 input channels (fixed)
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    bsc[j] = PRO && !CAT && kb_ok ? a.pro_scale[cb + j] : 0.f;
+    bsh[j] = PRO && !CAT && kb_ok ? a.pro_shift[cb + j] : 0.f;
+  }
+  auto pro_step = [&]() {
+    if constexpr (!CAT) {
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        if (dhb) {
+          float v[8], h[8];
+          ra[e].to_f32(v);
+          rah[e].to_f32(h);
+#pragma unroll
+          for (int j = 0; j < 8; ++j) v[j] = fmaf(dk[0][j], v[j], fmaf(dk[1][j], h[j] - dk[3][j], dk[2][j]));
+          ra[e].from_f32(v);
+          if (!((aval >> e) & 1u)) ra[e].zero();
+        }
+        if constexpr (PRO) {
+          float v[8];
+          rb[e].to_f32(v);
+#pragma unroll
+          for (int j = 0; j < 8; ++j) v[j] = fmaxf(fmaf(bsc[j], v[j], bsh[j]), 0.f);
+          rb[e].from_f32(v);
+          if (!((bval >> e) & 1u)) rb[e].zero();
+        }
+      }
     }
   };
   auto pair_word = [](const Raw8<T>& lo, const Raw8<T>& hi, int j) -> uint32_t {
@@ -1474,6 +2160,7 @@ __global__ __launch_bounds__(256) void wgrad_staged_kernel(WgradArgs a) {
 
   if (steps > 0) {
     load_step(0);
+    pro_step();
     park(0);
   }
   __syncthreads();
@@ -1494,7 +2181,10 @@ __global__ __launch_bounds__(256) void wgrad_staged_kernel(WgradArgs a) {
 #pragma unroll
         for (int j = 0; j < FK; ++j) acc[i][j] = mfma(fa[i], fb[j], acc[i][j]);
     }
-    if (step + 1 < steps) park(buf ^ 1);
+    if (step + 1 < steps) {
+      pro_step();
+      park(buf ^ 1);
+    }
     __syncthreads();
   }
 
@@ -1549,8 +2239,6 @@ __global__ __launch_bounds__(256) void wgrad_halo_kernel(WgradArgs a) {
   const int c0 = chunk * 32;
   const int tiles_x = (a.w + TW - 1) / TW, tiles_y = (a.h + TH - 1) / TH;
   const int ntiles = tiles_x * tiles_y * a.n;
-  const T* src = static_cast<const T*>(a.src);
-  const T* dh = static_cast<const T*>(a.dh);
 
   if constexpr (PRO) {
     if (tid < 32) {
@@ -1563,7 +2251,15 @@ __global__ __launch_bounds__(256) void wgrad_halo_kernel(WgradArgs a) {
   const bool dhb = a.dh_h != nullptr;
   float dk[4][8];
   dh_coeffs(a, o0 + (tid % (BO / 8)) * 8, dk);   // this thread's output-channel group is fixed
-  Raw8<T> rh[H_CHUNKS], rd[D_CHUNKS];
+  // Buffer resources: padding and rows past the image load zeros without
+  // branches, so the next tile's loads stay in flight during the MFMAs.
+  const long in_bytes = static_cast<long>(a.n) * a.h * a.w * a.c_in * 2;
+  const long out_bytes = static_cast<long>(a.m) * a.c_out * 2;
+  const __amdgpu_buffer_rsrc_t r_src = make_rsrc(a.src, in_bytes);
+  const __amdgpu_buffer_rsrc_t r_dh = make_rsrc(a.dh, out_bytes);
+  const __amdgpu_buffer_rsrc_t r_dhh = make_rsrc(dhb ? a.dh_h : a.dh, out_bytes);
+  Raw8<T> rh[H_CHUNKS], rd[D_CHUNKS], rdh[D_CHUNKS];
+  uint32_t hval = 0, dval = 0;
   auto tile_origin = [&](int t, int& img, int& p0, int& q0) {
     const int tx = t % tiles_x;
     const int ty = (t / tiles_x) % tiles_y;
@@ -1575,25 +2271,19 @@ __global__ __launch_bounds__(256) void wgrad_halo_kernel(WgradArgs a) {
     int img, p0, q0;
     tile_origin(t, img, p0, q0);
     const long base = static_cast<long>(img) * a.h * a.w;
+    hval = dval = 0;
 #pragma unroll
     for (int i = 0; i < H_CHUNKS; ++i) {
       const int q = tid + 256 * i;
       const int hp = q >> 2, sub = q & 3;
       const int hy = hp / HTW, hx = hp - hy * HTW;
       const int ih = p0 - 1 + hy, iw = q0 - 1 + hx;
-      if (hp < HPIX && ih >= 0 && ih < a.h && iw >= 0 && iw < a.w) {
-        rh[i].load(src + (base + static_cast<long>(ih) * a.w + iw) * a.c_in + c0 + sub * 8);
-        if constexpr (PRO) {
-          float v[8];
-          rh[i].to_f32(v);
-#pragma unroll
-          for (int j = 0; j < 8; ++j)
-            v[j] = fmaxf(fmaf(pro_tab[0][sub * 8 + j], v[j], pro_tab[1][sub * 8 + j]), 0.f);
-          rh[i].from_f32(v);
-        }
-      } else {
-        rh[i].zero();
-      }
+      const bool ok = hp < HPIX && ih >= 0 && ih < a.h && iw >= 0 && iw < a.w;
+      const uint32_t off =
+          ok ? static_cast<uint32_t>(((base + static_cast<long>(ih) * a.w + iw) * a.c_in + c0 + sub * 8) * 2)
+             : BUF_OOB;
+      rh[i].set(buf_load16(r_src, off));
+      hval |= ok ? 1u << i : 0u;
     }
 #pragma unroll
     for (int i = 0; i < D_CHUNKS; ++i) {
@@ -1601,21 +2291,32 @@ __global__ __launch_bounds__(256) void wgrad_halo_kernel(WgradArgs a) {
       const int pix = q / (BO / 8), og = q % (BO / 8);
       const int ph = pix / TW, pw = pix - ph * TW;
       const int pp = p0 + ph, qq = q0 + pw;
-      if (pix < NPIX && pp < a.h && qq < a.w && o0 + og * 8 < a.c_out) {
-        const long off = (base + static_cast<long>(pp) * a.w + qq) * a.c_out + o0 + og * 8;
-        rd[i].load(dh + off);
-        if (dhb) dh_bwd8(rd[i], static_cast<const T*>(a.dh_h) + off, dk);
-      } else {
-        rd[i].zero();
-      }
+      const bool ok = pix < NPIX && pp < a.h && qq < a.w && o0 + og * 8 < a.c_out;
+      const uint32_t off =
+          ok ? static_cast<uint32_t>(((base + static_cast<long>(pp) * a.w + qq) * a.c_out + o0 + og * 8) * 2)
+             : BUF_OOB;
+      rd[i].set(buf_load16(r_dh, off));
+      rdh[i].set(buf_load16(r_dhh, off));
+      dval |= ok ? 1u << i : 0u;
     }
   };
+  // Prologues on the landed registers (padding stays zero), then the
+  // transposed LDS layout.
   auto park_tile = [&]() {
 #pragma unroll
     for (int i = 0; i < H_CHUNKS; ++i) {
       const int q = tid + 256 * i;
       const int hp = q >> 2, sub = q & 3;
       if (hp >= HPIX) continue;
+      if constexpr (PRO) {
+        float v[8];
+        rh[i].to_f32(v);
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          v[j] = fmaxf(fmaf(pro_tab[0][sub * 8 + j], v[j], pro_tab[1][sub * 8 + j]), 0.f);
+        rh[i].from_f32(v);
+        if (!((hval >> i) & 1u)) rh[i].zero();
+      }
       const int hy = hp / HTW, hx = hp - hy * HTW;
 #pragma unroll
       for (int sft = 0; sft < 3; ++sft) {
@@ -1631,6 +2332,17 @@ __global__ __launch_bounds__(256) void wgrad_halo_kernel(WgradArgs a) {
       const int q = tid + 256 * i;
       const int pix = q / (BO / 8), og = q % (BO / 8);
       if (pix >= NPIX) continue;
+      if (dhb) {
+        Raw8<T> r = rd[i];
+        float v[8], h[8];
+        r.to_f32(v);
+        rdh[i].to_f32(h);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = fmaf(dk[0][j], v[j], fmaf(dk[1][j], h[j] - dk[3][j], dk[2][j]));
+        r.from_f32(v);
+        if (!((dval >> i) & 1u)) r.zero();
+        rd[i] = r;
+      }
 #pragma unroll
       for (int j = 0; j < 8; ++j) rd[i].put(j, sd + (og * 8 + j) * DROW + pix);
     }
@@ -1640,13 +2352,15 @@ __global__ __launch_bounds__(256) void wgrad_halo_kernel(WgradArgs a) {
 #pragma unroll
   for (int i = 0; i < NP; ++i) acc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
+  // Loads are unconditional (the prefetch after the last tile re-reads tile
+  // ntiles - 1) so the number of loads in flight is the same on every path.
   int t = blockIdx.x;
-  if (t < ntiles) load_tile(t);
+  load_tile(min(t, ntiles - 1));
   for (; t < ntiles; t += gridDim.x) {
     __syncthreads();            // previous tile's operands fully consumed
     park_tile();
     __syncthreads();
-    if (t + static_cast<int>(gridDim.x) < ntiles) load_tile(t + gridDim.x);
+    load_tile(min(t + static_cast<int>(gridDim.x), ntiles - 1));
 #pragma unroll
     for (int g = 0; g < NPIX / 32; ++g) {
       const int pix = g * 32 + lg * 8;
@@ -1808,6 +2522,32 @@ bool launch_halo(const ConvArgs& a, int ep, hipStream_t st) {
   });
 }
 
+template <int TH, int TW, int CH>
+bool launch_img(const ConvArgs& a, int ep, hipStream_t st) {
+  return dispatch_ep_pro(ep, pro_mode(a), [&](auto k) {
+    hipLaunchKernelGGL((conv_img_kernel<TH, TW, CH, decltype(k)::ep, decltype(k)::pro>),
+                       dim3(a.n), dim3(512), 0, st, a);
+  });
+}
+
+// Whole-image kernel: 16 x 16 images, C_in 128, C_out 128.
+bool use_img(int dtype, const ConvArgs& a) {
+  return dtype == DT_BF16 && a.src2 == nullptr && a.r == 3 && a.s == 3 && a.stride == 1 &&
+         a.pad == 1 && a.h == 16 && a.w == 16 && a.p == 16 && a.q == 16 && a.c_in == 128 &&
+         a.c_out == 128 && a.k_tot == 1152 &&
+         static_cast<long>(a.n) * a.h * a.w * 256 < static_cast<long>(BUF_OOB);
+}
+
+template <int TH, int TW, int BN, int WM, int CH>
+bool launch_fp(const ConvArgs& a, int ep, hipStream_t st) {
+  const int tiles = ((a.w + TW - 1) / TW) * ((a.h + TH - 1) / TH) * a.n;
+  dim3 grid(tiles, (a.c_out + BN - 1) / BN);
+  return dispatch_ep_pro(ep, pro_mode(a), [&](auto k) {
+    hipLaunchKernelGGL((conv_fp_kernel<TH, TW, BN, WM, CH, decltype(k)::ep, decltype(k)::pro>),
+                       grid, dim3(256), 0, st, a);
+  });
+}
+
 // Persistent 32 -> 32 kernel: tile geometry and grid (th == 0: not used).  It
 // wins where the image is wide enough for several tiles per workgroup (56 wide);
 // at 32 x 32 the one-shot halo kernel is faster.
@@ -1837,6 +2577,7 @@ bool launch_conv32(const C32Shape& c, const ConvArgs& a, int ep, hipStream_t st)
 
 // Returns -1 when no halo kernel applies, else whether the launch was made.
 int launch_halo_any(int dtype, const ConvArgs& a, int ep, hipStream_t st) {
+  if (use_img(dtype, a)) return launch_img<16, 16, 4>(a, ep, st) ? 1 : 0;
   const C32Shape c32 = conv32_shape(dtype, a);
   if (c32.th != 0) return launch_conv32(c32, a, ep, st) ? 1 : 0;
   const HaloShape h = halo_shape(dtype, a);
@@ -1848,10 +2589,14 @@ int launch_halo_any(int dtype, const ConvArgs& a, int ep, hipStream_t st) {
                    : launch_halo<8, 32, 32, 4, 2, false>(a, ep, st);
   else if (h.tw == 16 && h.bn == 64)
     ok = h.hb == 1 ? launch_halo<8, 16, 64, 2, 1, true>(a, ep, st)
-                   : launch_halo<8, 16, 64, 2, 2, false>(a, ep, st);
+         : a.c_in == 64 ? launch_fp<8, 16, 64, 2, 2>(a, ep, st)
+         : a.c_in == 128 ? launch_fp<8, 16, 64, 2, 4>(a, ep, st)
+                         : launch_halo<8, 16, 64, 2, 2, false>(a, ep, st);
   else if (h.tw == 16)
     ok = h.hb == 1 ? launch_halo<8, 16, 128, 2, 1, false>(a, ep, st)
-                   : launch_halo<8, 16, 128, 2, 2, false>(a, ep, st);
+         : a.c_in == 64 ? launch_fp<8, 16, 128, 2, 2>(a, ep, st)
+         : a.c_in == 128 ? launch_fp<8, 16, 128, 2, 4>(a, ep, st)
+                         : launch_halo<8, 16, 128, 2, 2, false>(a, ep, st);
   else
     ok = launch_halo<4, 56, 32, 2, 1, true>(a, ep, st);
   return ok ? 1 : 0;
@@ -1895,10 +2640,18 @@ namespace {
 template <int BO, int BK>
 void launch_wgrad_staged(const WgradArgs& a, hipStream_t st) {
   dim3 grid((a.k_tot + BK - 1) / BK, (a.c_out + BO - 1) / BO, a.splits);
-  if (a.pro_scale != nullptr)
-    hipLaunchKernelGGL((wgrad_staged_kernel<BO, BK, true>), grid, dim3(256), 0, st, a);
-  else
-    hipLaunchKernelGGL((wgrad_staged_kernel<BO, BK, false>), grid, dim3(256), 0, st, a);
+  const bool pro = a.pro_scale != nullptr, cat = a.src2 != nullptr;
+  if (cat) {
+    if (pro)
+      hipLaunchKernelGGL((wgrad_staged_kernel<BO, BK, true, true>), grid, dim3(256), 0, st, a);
+    else
+      hipLaunchKernelGGL((wgrad_staged_kernel<BO, BK, false, true>), grid, dim3(256), 0, st, a);
+  } else {
+    if (pro)
+      hipLaunchKernelGGL((wgrad_staged_kernel<BO, BK, true, false>), grid, dim3(256), 0, st, a);
+    else
+      hipLaunchKernelGGL((wgrad_staged_kernel<BO, BK, false, false>), grid, dim3(256), 0, st, a);
+  }
 }
 
 template <int TH, int TW, int BO>
@@ -1931,6 +2684,7 @@ void wgrad_t(const WgradArgs& a, hipStream_t st) {
 }  // namespace
 
 int conv_row_tiles(int dtype, const ConvArgs& a) {
+  if (use_img(dtype, a)) return a.n;
   const C32Shape c32 = conv32_shape(dtype, a);
   if (c32.th != 0) return c32.grid;
   const HaloShape hs = halo_shape(dtype, a);
