@@ -19,6 +19,8 @@
 // of its operands are staged through LDS transposed to k-contiguous rows, and
 // the reduction is split over row chunks whose fp32 partial sums are reduced
 // in a fixed order by wgrad_reduce (deterministic, no float atomics).
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -2393,6 +2395,205 @@ __global__ __launch_bounds__(256) void wgrad_halo_kernel(WgradArgs a) {
   }
 }
 
+// Weight gradient on transposing LDS reads (gfx950 ds_read_b64_tr_b16):
+//   part[split][o][tap*C_in + c] = sum over the split's pixels of dh[px][o] * x[px + tap][c]
+// Both MFMA operands need pixels along the reduction, but the tensors are
+// channel-contiguous.  The tiles stay in LDS exactly as loaded ([pixel][channel]);
+// each operand fragment is two transposing reads: in a group of 16 lanes, lane
+// 4r + q supplies the address of 4 channels (q-th quarter of a 16-channel run)
+// of pixel r, and lane j receives channel j of the 4 pixels.  A workgroup owns
+// BO output x BC input channels and all R*R taps, and sums a strided set of
+// TH x TW pixel tiles; the next tile is in flight while the current one is
+// multiplied (double-buffered LDS, one barrier per tile).  Waves split the
+// output: WO x WC channel blocks of OF x CF fragments, and WT groups of taps.
+template <int R, int TH, int TW, int WO, int OF, int WC, int CF, int WT, bool PRO, bool DH>
+__global__ __launch_bounds__(64 * WO * WC * WT) void wgrad_tr_kernel(WgradArgs a) {
+  using T = bf16_t;
+  typedef short v4i16 __attribute__((ext_vector_type(4)));
+  typedef short v8i16 __attribute__((ext_vector_type(8)));
+  constexpr int NT = 64 * WO * WC * WT;
+  constexpr int TAPS = R * R, TPW = TAPS / WT;
+  static_assert(TPW * WT == TAPS, "taps per wave");
+  constexpr int BO = WO * OF * 16, BC = WC * CF * 16;
+  constexpr int NPIX = TH * TW;
+  static_assert(NPIX % 32 == 0, "pixel tile");
+  constexpr int KSTEPS = NPIX / 32;
+  constexpr int PAD = R / 2;
+  constexpr int HTH = TH + 2 * PAD, HTW = TW + 2 * PAD, HPIX = HTH * HTW;
+  constexpr int PO = BO + 16, PC = BC + 16;          // LDS row pitches (bf16)
+  constexpr int DG = BO / 8, XG = BC / 8;            // 16-byte groups per row
+  static_assert(NT % DG == 0 && NT % XG == 0, "fixed channel group per thread");
+  constexpr int D_PT = (NPIX * DG + NT - 1) / NT;
+  constexpr int X_PT = (HPIX * XG + NT - 1) / NT;
+  __shared__ __attribute__((aligned(16))) T sd[2][NPIX * PO];
+  __shared__ __attribute__((aligned(16))) T sx[2][HPIX * PC];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wo = wave % WO, wc = (wave / WO) % WC, wt = wave / (WO * WC);
+  const int li = lane & 15, kg = lane >> 4;
+  const int o0 = blockIdx.y * BO, c0 = blockIdx.z * BC;
+  // 1x1: no halo; tiles are runs of NPIX consecutive pixels of the flat [m] index
+  constexpr bool FLAT = R == 1;
+  const int tiles_x = (a.w + TW - 1) / TW, tiles_y = (a.h + TH - 1) / TH;
+  const int ntiles = FLAT ? (a.m + NPIX - 1) / NPIX : tiles_x * tiles_y * a.n;
+  const int splits = gridDim.x;
+
+  const long in_bytes = static_cast<long>(a.n) * a.h * a.w * a.c_in * 2;
+  const long out_bytes = static_cast<long>(a.m) * a.c_out * 2;
+  const __amdgpu_buffer_rsrc_t r_x = make_rsrc(a.src, in_bytes);
+  const __amdgpu_buffer_rsrc_t r_d = make_rsrc(a.dh, out_bytes);
+  const __amdgpu_buffer_rsrc_t r_h = make_rsrc(DH ? a.dh_h : a.dh, out_bytes);
+
+  // Fixed channel groups of this thread and their prologue coefficients.
+  const int og = tid % DG, cg = tid % XG;
+  float dk[4][8], xs[8], xsh[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int o = o0 + og * 8 + j, c = c0 + cg * 8 + j;
+    dk[0][j] = DH ? a.dh_ca[o] : 0.f;
+    dk[1][j] = DH ? a.dh_cb[o] : 0.f;
+    dk[2][j] = DH ? a.dh_cc[o] : 0.f;
+    dk[3][j] = DH ? a.dh_mean[o] : 0.f;
+    xs[j] = PRO ? a.pro_scale[c] : 0.f;
+    xsh[j] = PRO ? a.pro_shift[c] : 0.f;
+  }
+
+  Raw8<T> rd[D_PT], rdh[DH ? D_PT : 1], rx[X_PT];
+  uint32_t dval = 0, xval = 0;
+  auto load_tile = [&](int t) {
+    const int tx = t % tiles_x, ty = (t / tiles_x) % tiles_y, img = t / (tiles_x * tiles_y);
+    const int p0 = ty * TH, q0 = tx * TW;
+    dval = xval = 0;
+#pragma unroll
+    for (int i = 0; i < D_PT; ++i) {
+      const int px = (tid + NT * i) / DG;
+      const int pp = p0 + px / TW, qq = q0 + px % TW;
+      const long m = FLAT ? static_cast<long>(t) * NPIX + px : (static_cast<long>(img) * a.h + pp) * a.w + qq;
+      const bool ok = px < NPIX && (FLAT ? m < a.m : pp < a.h && qq < a.w);
+      const uint32_t off = ok ? static_cast<uint32_t>((m * a.c_out + o0 + og * 8) * 2) : BUF_OOB;
+      rd[i].set(buf_load16(r_d, off));
+      if constexpr (DH) rdh[i].set(buf_load16(r_h, off));
+      dval |= ok ? 1u << i : 0u;
+    }
+#pragma unroll
+    for (int i = 0; i < X_PT; ++i) {
+      const int hp = (tid + NT * i) / XG;
+      const int ih = p0 - PAD + hp / HTW, iw = q0 - PAD + hp % HTW;
+      const long m = FLAT ? static_cast<long>(t) * NPIX + hp : (static_cast<long>(img) * a.h + ih) * a.w + iw;
+      const bool ok = hp < HPIX && (FLAT ? m < a.m : ih >= 0 && ih < a.h && iw >= 0 && iw < a.w);
+      const uint32_t off = ok ? static_cast<uint32_t>((m * a.c_in + c0 + cg * 8) * 2) : BUF_OOB;
+      rx[i].set(buf_load16(r_x, off));
+      xval |= ok ? 1u << i : 0u;
+    }
+  };
+  auto park_tile = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < D_PT; ++i) {
+      const int px = (tid + NT * i) / DG;
+      if (px >= NPIX) continue;
+      Raw8<T> r = rd[i];
+      if constexpr (DH) {
+        float v[8], h[8];
+        r.to_f32(v);
+        rdh[i].to_f32(h);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = fmaf(dk[0][j], v[j], fmaf(dk[1][j], h[j] - dk[3][j], dk[2][j]));
+        r.from_f32(v);
+        if (!((dval >> i) & 1u)) r.zero();
+      }
+      *reinterpret_cast<uint4*>(&sd[buf][px * PO + og * 8]) = make_uint4(r.w[0], r.w[1], r.w[2], r.w[3]);
+    }
+#pragma unroll
+    for (int i = 0; i < X_PT; ++i) {
+      const int hp = (tid + NT * i) / XG;
+      if (hp >= HPIX) continue;
+      Raw8<T> r = rx[i];
+      if constexpr (PRO) {
+        float v[8];
+        r.to_f32(v);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = fmaxf(fmaf(xs[j], v[j], xsh[j]), 0.f);
+        r.from_f32(v);
+        if (!((xval >> i) & 1u)) r.zero();   // padding stays zero
+      }
+      *reinterpret_cast<uint4*>(&sx[buf][hp * PC + cg * 8]) = make_uint4(r.w[0], r.w[1], r.w[2], r.w[3]);
+    }
+  };
+  // two transposing reads give one bf16 MFMA operand: 8 pixels x one channel
+  auto tr_frag = [](const T* p0, const T* p1) {
+    const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) v4i16*)(p0));
+    const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) v4i16*)(p1));
+    Frag<T> f;
+    f.v = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+    return f;
+  };
+
+  f32x4_t acc[OF][CF][TPW];
+#pragma unroll
+  for (int of = 0; of < OF; ++of)
+#pragma unroll
+    for (int cf = 0; cf < CF; ++cf)
+#pragma unroll
+      for (int u = 0; u < TPW; ++u) acc[of][cf][u] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  // Loads are unconditional (re-reading the last tile past the end) so the
+  // number of loads in flight does not depend on the path.
+  int t = blockIdx.x;
+  load_tile(min(t, ntiles - 1));
+  int buf = 0;
+  for (; t < ntiles; t += splits) {
+    park_tile(buf);
+    __syncthreads();
+    load_tile(min(t + splits, ntiles - 1));
+#pragma unroll
+    for (int ks = 0; ks < KSTEPS; ++ks) {
+      // this lane's two pixels (rows of the transposing reads)
+      const int pa = ks * 32 + kg * 8 + (li >> 2), pb = pa + 4;
+      const int qo = (li & 3) * 4;
+      Frag<T> fa[OF];
+#pragma unroll
+      for (int of = 0; of < OF; ++of) {
+        const int ob = (wo * OF + of) * 16 + qo;
+        fa[of] = tr_frag(&sd[buf][pa * PO + ob], &sd[buf][pb * PO + ob]);
+      }
+      const int ra = (pa / TW) * HTW + pa % TW, rb = (pb / TW) * HTW + pb % TW;
+#pragma unroll
+      for (int u = 0; u < TPW; ++u) {
+        const int tap = wt * TPW + u;
+        const int toff = (tap / R) * HTW + tap % R;
+#pragma unroll
+        for (int cf = 0; cf < CF; ++cf) {
+          const int cb = (wc * CF + cf) * 16 + qo;
+          const Frag<T> fb = tr_frag(&sx[buf][(ra + toff) * PC + cb], &sx[buf][(rb + toff) * PC + cb]);
+#pragma unroll
+          for (int of = 0; of < OF; ++of) acc[of][cf][u] = mfma(fa[of], fb, acc[of][cf][u]);
+        }
+      }
+    }
+    buf ^= 1;
+  }
+
+  // lane (li, kg) holds D[o = 4 kg + e][c = li] of each fragment
+  float* outp = a.partials + static_cast<long>(blockIdx.x) * a.c_out * a.k_tot;
+#pragma unroll
+  for (int of = 0; of < OF; ++of)
+#pragma unroll
+    for (int cf = 0; cf < CF; ++cf)
+#pragma unroll
+      for (int u = 0; u < TPW; ++u) {
+        const int tap = wt * TPW + u;
+        const int k = tap * a.c_in + c0 + (wc * CF + cf) * 16 + li;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int o = o0 + (wo * OF + of) * 16 + kg * 4 + e;
+          outp[static_cast<long>(o) * a.k_tot + k] = acc[of][cf][u][e];
+        }
+      }
+}
+
 // grad[o*K + k] += inv_k * sum_split part[split][o][k]   (fixed order)
 // A block owns 32 consecutive elements; its 8 thread rows take interleaved
 // split ranges, and the 8 row sums are combined in a fixed order.
@@ -2618,6 +2819,63 @@ void launch_wgrad_bk(const WgradArgs& a, hipStream_t st) {
 
 }  // namespace
 
+// Transposed-read weight gradient: configuration for these arguments (0: not
+// applicable) and the split count it uses.
+int wgrad_tr_plan(int dtype, const WgradArgs& a, int* splits) {
+  if (!(dtype == DT_BF16 && a.src2 == nullptr && a.stride == 1 && a.r == a.s &&
+        (a.r == 3 || a.r == 1) && a.pad == a.r / 2 && a.p == a.h && a.q == a.w &&
+        a.dh_h != nullptr))
+    return 0;
+  if (static_cast<long>(a.n) * a.h * a.w * a.c_in * 2 >= static_cast<long>(BUF_OOB) ||
+      static_cast<long>(a.m) * a.c_out * 2 >= static_cast<long>(BUF_OOB))
+    return 0;
+  int cfg = 0, th = 0, tw = 0, bo = 0, bc = 0;
+  if (a.r == 3 && a.c_in == 32 && a.c_out == 32 && (a.w == 32 || a.w == 56)) {
+    cfg = a.w == 32 ? 1 : 2; th = 4; tw = a.w; bo = 32; bc = 32;
+  } else if (a.r == 3 && a.c_in % 64 == 0 && a.c_out % 64 == 0 && a.w == 16) {
+    cfg = 3; th = 8; tw = 16; bo = 64; bc = 64;
+  } else if (a.r == 3 && a.c_in % 64 == 0 && a.c_out % 64 == 0 && a.w == 8) {
+    cfg = 4; th = 8; tw = 8; bo = 64; bc = 64;
+  } else if (a.r == 1 && a.c_in == 128 && a.c_out == 32) {
+    cfg = 5; th = 1; tw = 128; bo = 32; bc = 128;
+  } else if (a.r == 1 && a.c_in == 32 && a.c_out == 128) {
+    cfg = 6; th = 1; tw = 128; bo = 128; bc = 32;
+  } else {
+    return 0;
+  }
+  const int ntiles = a.r == 1 ? (a.m + th * tw - 1) / (th * tw)
+                              : ((a.w + tw - 1) / tw) * ((a.h + th - 1) / th) * a.n;
+  const int per = (a.c_out / bo) * (a.c_in / bc);
+  if (splits) *splits = std::max(1, std::min(ntiles, 256 / per));
+  return cfg;
+}
+
+namespace {
+template <int R, int TH, int TW, int WO, int OF, int WC, int CF, int WT>
+void launch_wgrad_tr(const WgradArgs& a, hipStream_t st) {
+  constexpr int BO = WO * OF * 16, BC = WC * CF * 16;
+  dim3 grid(a.splits, a.c_out / BO, a.c_in / BC);
+  dim3 block(64 * WO * WC * WT);
+  if (a.pro_scale != nullptr)
+    hipLaunchKernelGGL((wgrad_tr_kernel<R, TH, TW, WO, OF, WC, CF, WT, true, true>), grid, block, 0, st, a);
+  else
+    hipLaunchKernelGGL((wgrad_tr_kernel<R, TH, TW, WO, OF, WC, CF, WT, false, true>), grid, block, 0, st, a);
+}
+}  // namespace
+
+bool conv_wgrad_tr(int dtype, const WgradArgs& a, hipStream_t st) {
+  int sp = 0;
+  switch (wgrad_tr_plan(dtype, a, &sp)) {
+    case 1: launch_wgrad_tr<3, 4, 32, 1, 2, 1, 2, 3>(a, st); return true;
+    case 2: launch_wgrad_tr<3, 4, 56, 1, 2, 1, 2, 3>(a, st); return true;
+    case 3: launch_wgrad_tr<3, 8, 16, 1, 4, 4, 1, 1>(a, st); return true;
+    case 4: launch_wgrad_tr<3, 8, 8, 1, 4, 4, 1, 1>(a, st); return true;
+    case 5: launch_wgrad_tr<1, 1, 128, 1, 2, 4, 2, 1>(a, st); return true;
+    case 6: launch_wgrad_tr<1, 1, 128, 4, 2, 1, 2, 1>(a, st); return true;
+    default: return false;
+  }
+}
+
 // 0: no halo kernel; 1: 4x32 tiles, 32 output channels per group; 2: 8x16 tiles, 64.
 int wgrad_halo_shape(int dtype, const WgradArgs& a) {
   if (!(dtype == DT_BF16 && a.src2 == nullptr && a.r == 3 && a.s == 3 && a.stride == 1 &&
@@ -2703,6 +2961,7 @@ bool conv_gemm(int dtype, const ConvArgs& a, int ep, hipStream_t st) {
 }
 
 void conv_wgrad(int dtype, const WgradArgs& a, hipStream_t st) {
+  if (conv_wgrad_tr(dtype, a, st)) return;
   if (dtype == DT_BF16)
     wgrad_t<bf16_t>(a, st);
   else

@@ -71,6 +71,10 @@ bool conv_gemm(int dtype, const ConvArgs& a, int ep, hipStream_t st);
 // Number of partial-sum rows (output row tiles) conv_gemm writes for these arguments.
 int conv_row_tiles(int dtype, const ConvArgs& a);
 void conv_wgrad(int dtype, const WgradArgs& a, hipStream_t st);
+// Transposed-read weight-gradient kernel: configuration (0 = not applicable)
+// and its split count (partial rows) for these arguments; conv_wgrad uses it
+// whenever it applies, with a.splits set to that count.
+int wgrad_tr_plan(int dtype, const WgradArgs& a, int* splits);
 // Halo-tile weight-gradient kernel selection (0 = not applicable) and the
 // number of pixel tiles it splits over.
 int wgrad_halo_shape(int dtype, const WgradArgs& a);

@@ -218,6 +218,13 @@ void Stage::wgrad_splits(const ConvLayer& cv, int* splits, int* rows_per_split) 
   w.n = desc.n; w.h = desc.h; w.w = desc.w; w.p = desc.h; w.q = desc.w;
   w.c_in = cv.cin; w.c_out = cv.cout; w.r = cv.r; w.s = cv.s; w.stride = 1; w.pad = cv.pad;
   w.k_tot = cv.r * cv.s * cv.cin; w.m = static_cast<int>(M);
+  w.dh_h = w.src;   // the stage always forms dh on the fly from a pre-BN tensor
+  int tr_splits = 0;
+  if (wgrad_tr_plan(dt, w, &tr_splits) != 0) {
+    *splits = tr_splits;
+    *rows_per_split = 0;
+    return;
+  }
   const int hshape = wgrad_halo_shape(dt, w);
   if (hshape != 0) {
     // pixel tiles strided over `splits` workgroups per (output tile, channel chunk)
