@@ -41,7 +41,57 @@ def parse():
     p.add_argument("--no-profile", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="target duration of the CPU-oracle sample")
+    p.add_argument("--copy-calibration", action="store_true",
+                   help="only run a plain device copy of 256 MiB ten times (reference kernel "
+                        "for scaling the FETCH_SIZE / WRITE_SIZE counters)")
     return p.parse_args()
+
+
+def copy_calibration():
+    """A plain elementwise pass of known size (256 MiB read, 256 MiB written, one
+    vectorized kernel per call): its FETCH_SIZE / WRITE_SIZE readings per dispatch
+    calibrate the counters against bytes actually moved."""
+    import torch
+    n = 64 << 20
+    src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(10):
+        torch.neg(src, out=dst)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes_read": 4 * n, "bytes_written": 4 * n,
+                      "dispatches": 10}))
+
+
+def kernel_source_sha():
+    """Hash of the HIP sources, to tell whether stored counter readings still
+    describe the kernels that run."""
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2406_02052_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        if f.endswith((".hip", ".h")):
+            with open(os.path.join(csrc, f), "rb") as fh:
+                h.update(f.encode() + fh.read())
+    return h.hexdigest()[:16]
+
+
+def stored_traffic(workload, kernel):
+    """HBM bytes per launch of `kernel` from the committed counter summary
+    (FETCH_SIZE and WRITE_SIZE, each scaled by the copy calibration), or None
+    when no reading exists or the kernel sources changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", "traffic_counters.md")
+    if not os.path.exists(path):
+        return None
+    sha = kernel_source_sha()
+    with open(path) as fh:
+        for line in fh:
+            cells = [c.strip().strip("`") for c in line.strip().strip("|").split("|")]
+            if len(cells) >= 5 and cells[0] == workload and cells[1] == kernel and cells[2] == sha:
+                try:
+                    return float(cells[-1])
+                except ValueError:
+                    return None
+    return None
 
 
 def gpu_inputs(st, wl):
@@ -170,6 +220,9 @@ def bench_schedule(args):
 
 def main():
     args = parse()
+    if args.copy_calibration:
+        copy_calibration()
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
                           "n_gpus": args.gpus}))
@@ -213,6 +266,8 @@ def main():
         petra_stage_profile(st.handle, False)
         rl = roofline(prof, wl.dtype)
         rl["launches_per_step"] = prof[rl["kernel"]][0] / args.steps
+        rl["traffic"] = stored_traffic(wl.name, rl["kernel"])
+        rl["kernel_source_sha"] = kernel_source_sha()
         out["roofline"] = rl
         out["kernels"] = {k: {"launches_per_step": v[0] / args.steps,
                               "avg_us": v[1] * 1e3 / v[0],

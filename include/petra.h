@@ -154,11 +154,13 @@ petra_status petra_stage_set_optimizer(petra_stage* st, const petra_sgd* opt);
  * stage's side streams). */
 petra_status petra_stage_set_graphs(petra_stage* st, int32_t enable);
 
-/* Streams used by one backward call (default 3): 1 = every kernel on one
- * stream; 2 = the weight gradients on a second stream; 3 = in addition the
- * recompute of the next residual function on a third stream, overlapped with
- * the input-gradient chain of the current one.  Results are identical in every
- * mode.  PETRA_ERR_INVALID_ARG outside [1, 3]. */
+/* Streams used by one backward call: 1 = every kernel on one stream; 2 = the
+ * weight gradients on a second stream; 3 = in addition the recompute of the
+ * next residual function on a third stream, overlapped with the input-gradient
+ * chain of the current one.  Default: 1 for PETRA_BLOCK_BASIC stages (the
+ * cross-stream event calls cost more host time than the overlap saves), 3 for
+ * PETRA_BLOCK_BOTTLENECK stages.  Results are identical in every mode.
+ * PETRA_ERR_INVALID_ARG outside [1, 3]. */
 petra_status petra_stage_set_streams(petra_stage* st, int32_t n);
 
 /* Refresh the storage-type compute copies of the conv weights from the fp32

@@ -6,6 +6,7 @@
 // fixed order in fp64, so results are run-to-run deterministic.
 #include "common.h"
 #include "kernels.h"
+#include "prof.h"
 
 namespace petra {
 
@@ -278,14 +279,14 @@ void bn_stats_finalize(const float* partials, int tiles, int c, long m, const fl
                        const float* beta, float eps, float* scale, float* shift, float* mean,
                        float* rstd, float* run_mean, float* run_var, float momentum,
                        hipStream_t st) {
-  hipLaunchKernelGGL(bn_stats_finalize_kernel, dim3(c), dim3(FIN_THREADS), 0, st, partials, tiles, c, m, gamma,
+  PETRA_LAUNCH(bn_stats_finalize_kernel, dim3(c), dim3(FIN_THREADS), 0, st, partials, tiles, c, m, gamma,
                      beta, eps, scale, shift, mean, rstd, run_mean, run_var, momentum);
 }
 
 void bn_bwd_finalize(const float* partials, int tiles, int c, long m, const float* gamma,
                      const float* mean, const float* rstd, float inv_k, float* dgamma,
                      float* dbeta, float* ca, float* cb, float* cc, hipStream_t st) {
-  hipLaunchKernelGGL(bn_bwd_finalize_kernel, dim3(c), dim3(FIN_THREADS), 0, st, partials, tiles, c, m, gamma,
+  PETRA_LAUNCH(bn_bwd_finalize_kernel, dim3(c), dim3(FIN_THREADS), 0, st, partials, tiles, c, m, gamma,
                      mean, rstd, inv_k, dgamma, dbeta, ca, cb, cc);
 }
 
@@ -293,11 +294,11 @@ void combine_fwd(int dtype, const void* r, const void* h, const float* scale, co
                  void* y, long m, int c, hipStream_t st) {
   const long total8 = m * c / 8;
   if (dtype == DT_BF16)
-    hipLaunchKernelGGL(combine_fwd_kernel<bf16_t>, dim3(ew_grid(total8)), dim3(256), 0, st,
+    PETRA_LAUNCH(combine_fwd_kernel<bf16_t>, dim3(ew_grid(total8)), dim3(256), 0, st,
                        static_cast<const bf16_t*>(r), static_cast<const bf16_t*>(h), scale, shift,
                        static_cast<bf16_t*>(y), total8, c / 8);
   else
-    hipLaunchKernelGGL(combine_fwd_kernel<float>, dim3(ew_grid(total8)), dim3(256), 0, st,
+    PETRA_LAUNCH(combine_fwd_kernel<float>, dim3(ew_grid(total8)), dim3(256), 0, st,
                        static_cast<const float*>(r), static_cast<const float*>(h), scale, shift,
                        static_cast<float*>(y), total8, c / 8);
 }
@@ -306,11 +307,11 @@ void combine_rec(int dtype, const void* v, const void* h, const float* scale, co
                  void* x, long m, int c, hipStream_t st) {
   const long total8 = m * c / 8;
   if (dtype == DT_BF16)
-    hipLaunchKernelGGL(combine_rec_kernel<bf16_t>, dim3(ew_grid(total8)), dim3(256), 0, st,
+    PETRA_LAUNCH(combine_rec_kernel<bf16_t>, dim3(ew_grid(total8)), dim3(256), 0, st,
                        static_cast<const bf16_t*>(v), static_cast<const bf16_t*>(h), scale, shift,
                        static_cast<bf16_t*>(x), total8, c / 8);
   else
-    hipLaunchKernelGGL(combine_rec_kernel<float>, dim3(ew_grid(total8)), dim3(256), 0, st,
+    PETRA_LAUNCH(combine_rec_kernel<float>, dim3(ew_grid(total8)), dim3(256), 0, st,
                        static_cast<const float*>(v), static_cast<const float*>(h), scale, shift,
                        static_cast<float*>(x), total8, c / 8);
 }
@@ -319,11 +320,11 @@ void bn_bwd_apply(int dtype, const void* d, const void* h, const float* ca, cons
                   const float* cc, const float* mean, void* out, long m, int c, hipStream_t st) {
   const long total8 = m * c / 8;
   if (dtype == DT_BF16)
-    hipLaunchKernelGGL(bn_bwd_apply_kernel<bf16_t>, dim3(ew_grid(total8)), dim3(256), 0, st,
+    PETRA_LAUNCH(bn_bwd_apply_kernel<bf16_t>, dim3(ew_grid(total8)), dim3(256), 0, st,
                        static_cast<const bf16_t*>(d), static_cast<const bf16_t*>(h), ca, cb, cc,
                        mean, static_cast<bf16_t*>(out), total8, c / 8);
   else
-    hipLaunchKernelGGL(bn_bwd_apply_kernel<float>, dim3(ew_grid(total8)), dim3(256), 0, st,
+    PETRA_LAUNCH(bn_bwd_apply_kernel<float>, dim3(ew_grid(total8)), dim3(256), 0, st,
                        static_cast<const float*>(d), static_cast<const float*>(h), ca, cb, cc,
                        mean, static_cast<float*>(out), total8, c / 8);
 }
@@ -334,12 +335,12 @@ void combine_bwd(int dtype, const void* v, const void* h, const void* d, const f
   const int rpt = ew_rows_per_tile(m, c);
   const int tiles = static_cast<int>((m + rpt - 1) / rpt);
   if (dtype == DT_BF16)
-    hipLaunchKernelGGL(combine_bwd_kernel<bf16_t>, dim3(tiles), dim3(256), 0, st,
+    PETRA_LAUNCH(combine_bwd_kernel<bf16_t>, dim3(tiles), dim3(256), 0, st,
                        static_cast<const bf16_t*>(v), static_cast<const bf16_t*>(h),
                        static_cast<const bf16_t*>(d), scale, shift, mean, rstd,
                        static_cast<bf16_t*>(x), partials, m, c, rpt);
   else
-    hipLaunchKernelGGL(combine_bwd_kernel<float>, dim3(tiles), dim3(256), 0, st,
+    PETRA_LAUNCH(combine_bwd_kernel<float>, dim3(tiles), dim3(256), 0, st,
                        static_cast<const float*>(v), static_cast<const float*>(h),
                        static_cast<const float*>(d), scale, shift, mean, rstd,
                        static_cast<float*>(x), partials, m, c, rpt);

@@ -23,6 +23,7 @@
 
 #include "common.h"
 #include "kernels.h"
+#include "prof.h"
 
 namespace petra {
 
@@ -2576,7 +2577,11 @@ __global__ __launch_bounds__(64 * WO * WC * WT) void wgrad_tr_kernel(WgradArgs a
     buf ^= 1;
   }
 
-  // lane (li, kg) holds D[o = 4 kg + e][c = li] of each fragment
+  // Partials in fragment order: every (wave, fragment) owns 256 consecutive
+  // floats, lane l at 4 l .. 4 l + 3, so each wave writes whole cache lines;
+  // wgrad_tr_reduce maps them back to [o][k].
+  constexpr int NW = WO * WC * WT;
+  const long wg_base = (static_cast<long>(blockIdx.y) * gridDim.z + blockIdx.z) * NW + wave;
   float* outp = a.partials + static_cast<long>(blockIdx.x) * a.c_out * a.k_tot;
 #pragma unroll
   for (int of = 0; of < OF; ++of)
@@ -2584,14 +2589,62 @@ __global__ __launch_bounds__(64 * WO * WC * WT) void wgrad_tr_kernel(WgradArgs a
     for (int cf = 0; cf < CF; ++cf)
 #pragma unroll
       for (int u = 0; u < TPW; ++u) {
-        const int tap = wt * TPW + u;
-        const int k = tap * a.c_in + c0 + (wc * CF + cf) * 16 + li;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int o = o0 + (wo * OF + of) * 16 + kg * 4 + e;
-          outp[static_cast<long>(o) * a.k_tot + k] = acc[of][cf][u][e];
-        }
+        const long blk = ((wg_base * OF + of) * CF + cf) * TPW + u;
+        *reinterpret_cast<f32x4_t*>(outp + blk * 256 + lane * 4) = acc[of][cf][u];
       }
+}
+
+// Fixed-order sum over the splits of the fragment-ordered partials of
+// wgrad_tr_kernel, scaled by inv_k and added to grad[o][k].  One thread per
+// lane-quad (4 consecutive partial floats = 4 output channels of one k).
+struct TrMap {
+  int wo, of, wc, cf, wt, tpw, bo, bc, nz, c_in, k_tot;
+};
+
+__global__ __launch_bounds__(256) void wgrad_tr_reduce_kernel(const float* __restrict__ part,
+                                                              int splits, long numel, TrMap mp,
+                                                              float inv_k, float* __restrict__ grad) {
+  // 16 quads per block; the 16 thread rows take splits r, r + 16, ... and the
+  // row sums are combined in a fixed order.
+  __shared__ f32x4_t red[16][17];
+  const int tq = threadIdx.x & 15, tr = threadIdx.x >> 4;
+  const long q = static_cast<long>(blockIdx.x) * 16 + tq;   // quad index
+  const bool live = q * 4 < numel;
+  f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+  if (live) {
+    int sp = tr;
+    for (; sp + 48 < splits; sp += 64) {
+      f32x4_t v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) v[u] = *reinterpret_cast<const f32x4_t*>(part + (sp + 16 * u) * numel + q * 4);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) acc += v[u];
+    }
+    for (; sp < splits; sp += 16) acc += *reinterpret_cast<const f32x4_t*>(part + sp * numel + q * 4);
+  }
+  red[tr][tq] = acc;
+  __syncthreads();
+  if (tr != 0 || !live) return;
+#pragma unroll
+  for (int r = 1; r < 16; ++r) acc += red[r][tq];
+  // decode (block, lane) -> (o, k)
+  const int lane = static_cast<int>(q & 63);
+  long blk = q >> 6;
+  const int u = static_cast<int>(blk % mp.tpw); blk /= mp.tpw;
+  const int cf = static_cast<int>(blk % mp.cf); blk /= mp.cf;
+  const int of = static_cast<int>(blk % mp.of); blk /= mp.of;
+  const int nw = mp.wo * mp.wc * mp.wt;
+  const int wave = static_cast<int>(blk % nw); blk /= nw;
+  const int bz = static_cast<int>(blk % mp.nz), by = static_cast<int>(blk / mp.nz);
+  const int wo = wave % mp.wo, wc = (wave / mp.wo) % mp.wc, wt = wave / (mp.wo * mp.wc);
+  const int li = lane & 15, kg = lane >> 4;
+  const int tap = wt * mp.tpw + u;
+  const int k = tap * mp.c_in + bz * mp.bc + (wc * mp.cf + cf) * 16 + li;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int o = by * mp.bo + (wo * mp.of + of) * 16 + kg * 4 + e;
+    grad[static_cast<long>(o) * mp.k_tot + k] += inv_k * acc[e];
+  }
 }
 
 // grad[o*K + k] += inv_k * sum_split part[split][o][k]   (fixed order)
@@ -2668,7 +2721,7 @@ bool launch_gemm(const ConvArgs& a, int ep, hipStream_t st) {
   constexpr int BM = 128;
   dim3 grid((a.m + BM - 1) / BM, (a.c_out + BN - 1) / BN);
   return dispatch_ep_pro(ep, pro_mode(a), [&](auto k) {
-    hipLaunchKernelGGL((conv_gemm_kernel<T, BM, BN, WM, decltype(k)::ep, decltype(k)::pro>), grid,
+    PETRA_LAUNCH((conv_gemm_kernel<T, BM, BN, WM, decltype(k)::ep, decltype(k)::pro>), grid,
                        dim3(256), 0, st, a);
   });
 }
@@ -2685,7 +2738,7 @@ template <int BM, int BN, int WM>
 bool launch_staged(const ConvArgs& a, int ep, hipStream_t st) {
   dim3 grid((a.m + BM - 1) / BM, (a.c_out + BN - 1) / BN);
   return dispatch_ep_pro(ep, pro_mode(a), [&](auto k) {
-    hipLaunchKernelGGL((conv_staged_kernel<BM, BN, WM, decltype(k)::ep, decltype(k)::pro>), grid,
+    PETRA_LAUNCH((conv_staged_kernel<BM, BN, WM, decltype(k)::ep, decltype(k)::pro>), grid,
                        dim3(256), 0, st, a);
   });
 }
@@ -2718,7 +2771,7 @@ bool launch_halo(const ConvArgs& a, int ep, hipStream_t st) {
   const int tiles = ((a.w + TW - 1) / TW) * ((a.h + TH - 1) / TH) * a.n;
   dim3 grid(tiles, (a.c_out + BN - 1) / BN);
   return dispatch_ep_pro(ep, pro_mode(a), [&](auto k) {
-    hipLaunchKernelGGL((conv_halo_kernel<TH, TW, BN, WM, HB, decltype(k)::ep, decltype(k)::pro, FB>),
+    PETRA_LAUNCH((conv_halo_kernel<TH, TW, BN, WM, HB, decltype(k)::ep, decltype(k)::pro, FB>),
                        grid, dim3(256), 0, st, a);
   });
 }
@@ -2726,7 +2779,7 @@ bool launch_halo(const ConvArgs& a, int ep, hipStream_t st) {
 template <int TH, int TW, int CH>
 bool launch_img(const ConvArgs& a, int ep, hipStream_t st) {
   return dispatch_ep_pro(ep, pro_mode(a), [&](auto k) {
-    hipLaunchKernelGGL((conv_img_kernel<TH, TW, CH, decltype(k)::ep, decltype(k)::pro>),
+    PETRA_LAUNCH((conv_img_kernel<TH, TW, CH, decltype(k)::ep, decltype(k)::pro>),
                        dim3(a.n), dim3(512), 0, st, a);
   });
 }
@@ -2744,7 +2797,7 @@ bool launch_fp(const ConvArgs& a, int ep, hipStream_t st) {
   const int tiles = ((a.w + TW - 1) / TW) * ((a.h + TH - 1) / TH) * a.n;
   dim3 grid(tiles, (a.c_out + BN - 1) / BN);
   return dispatch_ep_pro(ep, pro_mode(a), [&](auto k) {
-    hipLaunchKernelGGL((conv_fp_kernel<TH, TW, BN, WM, CH, decltype(k)::ep, decltype(k)::pro>),
+    PETRA_LAUNCH((conv_fp_kernel<TH, TW, BN, WM, CH, decltype(k)::ep, decltype(k)::pro>),
                        grid, dim3(256), 0, st, a);
   });
 }
@@ -2771,7 +2824,7 @@ C32Shape conv32_shape(int dtype, const ConvArgs& a) {
 
 bool launch_conv32(const C32Shape& c, const ConvArgs& a, int ep, hipStream_t st) {
   return dispatch_ep_pro(ep, pro_mode(a), [&](auto k) {
-    hipLaunchKernelGGL((conv32_kernel<4, 56, decltype(k)::ep, decltype(k)::pro>), dim3(c.grid),
+    PETRA_LAUNCH((conv32_kernel<4, 56, decltype(k)::ep, decltype(k)::pro>), dim3(c.grid),
                        dim3(256), 0, st, a, c.tiles);
   });
 }
@@ -2812,9 +2865,9 @@ template <typename T, int BO, int BK>
 void launch_wgrad_bk(const WgradArgs& a, hipStream_t st) {
   dim3 grid((a.k_tot + BK - 1) / BK, (a.c_out + BO - 1) / BO, a.splits);
   if (a.pro_scale != nullptr)
-    hipLaunchKernelGGL((wgrad_kernel<T, BO, BK, true>), grid, dim3(256), 0, st, a);
+    PETRA_LAUNCH((wgrad_kernel<T, BO, BK, true>), grid, dim3(256), 0, st, a);
   else
-    hipLaunchKernelGGL((wgrad_kernel<T, BO, BK, false>), grid, dim3(256), 0, st, a);
+    PETRA_LAUNCH((wgrad_kernel<T, BO, BK, false>), grid, dim3(256), 0, st, a);
 }
 
 }  // namespace
@@ -2852,16 +2905,41 @@ int wgrad_tr_plan(int dtype, const WgradArgs& a, int* splits) {
 
 namespace {
 template <int R, int TH, int TW, int WO, int OF, int WC, int CF, int WT>
+TrMap tr_map(const WgradArgs& a) {
+  constexpr int BO = WO * OF * 16, BC = WC * CF * 16;
+  return TrMap{WO, OF, WC, CF, WT, R * R / WT, BO, BC, a.c_in / BC, a.c_in, a.k_tot};
+}
+
+template <int R, int TH, int TW, int WO, int OF, int WC, int CF, int WT>
 void launch_wgrad_tr(const WgradArgs& a, hipStream_t st) {
   constexpr int BO = WO * OF * 16, BC = WC * CF * 16;
   dim3 grid(a.splits, a.c_out / BO, a.c_in / BC);
   dim3 block(64 * WO * WC * WT);
   if (a.pro_scale != nullptr)
-    hipLaunchKernelGGL((wgrad_tr_kernel<R, TH, TW, WO, OF, WC, CF, WT, true, true>), grid, block, 0, st, a);
+    PETRA_LAUNCH((wgrad_tr_kernel<R, TH, TW, WO, OF, WC, CF, WT, true, true>), grid, block, 0, st, a);
   else
-    hipLaunchKernelGGL((wgrad_tr_kernel<R, TH, TW, WO, OF, WC, CF, WT, false, true>), grid, block, 0, st, a);
+    PETRA_LAUNCH((wgrad_tr_kernel<R, TH, TW, WO, OF, WC, CF, WT, false, true>), grid, block, 0, st, a);
 }
 }  // namespace
+
+bool wgrad_tr_reduce(int dtype, const WgradArgs& a, float inv_k, float* grad, hipStream_t st) {
+  int sp = 0;
+  TrMap mp{};
+  switch (wgrad_tr_plan(dtype, a, &sp)) {
+    case 1: mp = tr_map<3, 4, 32, 1, 2, 1, 2, 3>(a); break;
+    case 2: mp = tr_map<3, 4, 56, 1, 2, 1, 2, 3>(a); break;
+    case 3: mp = tr_map<3, 8, 16, 1, 4, 4, 1, 1>(a); break;
+    case 4: mp = tr_map<3, 8, 8, 1, 4, 4, 1, 1>(a); break;
+    case 5: mp = tr_map<1, 1, 128, 1, 2, 4, 2, 1>(a); break;
+    case 6: mp = tr_map<1, 1, 128, 4, 2, 1, 2, 1>(a); break;
+    default: return false;
+  }
+  const long numel = static_cast<long>(a.c_out) * a.k_tot;
+  const long quads = numel / 4;
+  PETRA_LAUNCH(wgrad_tr_reduce_kernel, dim3(static_cast<unsigned>((quads + 15) / 16)), dim3(256), 0,
+               st, a.partials, a.splits, numel, mp, inv_k, grad);
+  return true;
+}
 
 bool conv_wgrad_tr(int dtype, const WgradArgs& a, hipStream_t st) {
   int sp = 0;
@@ -2901,14 +2979,14 @@ void launch_wgrad_staged(const WgradArgs& a, hipStream_t st) {
   const bool pro = a.pro_scale != nullptr, cat = a.src2 != nullptr;
   if (cat) {
     if (pro)
-      hipLaunchKernelGGL((wgrad_staged_kernel<BO, BK, true, true>), grid, dim3(256), 0, st, a);
+      PETRA_LAUNCH((wgrad_staged_kernel<BO, BK, true, true>), grid, dim3(256), 0, st, a);
     else
-      hipLaunchKernelGGL((wgrad_staged_kernel<BO, BK, false, true>), grid, dim3(256), 0, st, a);
+      PETRA_LAUNCH((wgrad_staged_kernel<BO, BK, false, true>), grid, dim3(256), 0, st, a);
   } else {
     if (pro)
-      hipLaunchKernelGGL((wgrad_staged_kernel<BO, BK, true, false>), grid, dim3(256), 0, st, a);
+      PETRA_LAUNCH((wgrad_staged_kernel<BO, BK, true, false>), grid, dim3(256), 0, st, a);
     else
-      hipLaunchKernelGGL((wgrad_staged_kernel<BO, BK, false, false>), grid, dim3(256), 0, st, a);
+      PETRA_LAUNCH((wgrad_staged_kernel<BO, BK, false, false>), grid, dim3(256), 0, st, a);
   }
 }
 
@@ -2916,9 +2994,9 @@ template <int TH, int TW, int BO>
 void launch_wgrad_halo(const WgradArgs& a, hipStream_t st) {
   dim3 grid(a.splits, (a.c_out + BO - 1) / BO, a.c_in / 32);
   if (a.pro_scale != nullptr)
-    hipLaunchKernelGGL((wgrad_halo_kernel<TH, TW, BO, true>), grid, dim3(256), 0, st, a);
+    PETRA_LAUNCH((wgrad_halo_kernel<TH, TW, BO, true>), grid, dim3(256), 0, st, a);
   else
-    hipLaunchKernelGGL((wgrad_halo_kernel<TH, TW, BO, false>), grid, dim3(256), 0, st, a);
+    PETRA_LAUNCH((wgrad_halo_kernel<TH, TW, BO, false>), grid, dim3(256), 0, st, a);
 }
 
 template <typename T>
@@ -2971,7 +3049,7 @@ void conv_wgrad(int dtype, const WgradArgs& a, hipStream_t st) {
 void wgrad_reduce(const float* part, int splits, long numel, float inv_k, float* grad,
                   hipStream_t st) {
   const long blocks = (numel + 31) / 32;
-  hipLaunchKernelGGL(wgrad_reduce_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, st,
+  PETRA_LAUNCH(wgrad_reduce_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, st,
                      part, splits, numel, inv_k, grad);
 }
 

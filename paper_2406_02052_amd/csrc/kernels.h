@@ -81,6 +81,10 @@ int wgrad_halo_shape(int dtype, const WgradArgs& a);
 int wgrad_halo_tiles(int dtype, const WgradArgs& a);
 void wgrad_reduce(const float* part, int splits, long numel, float inv_k, float* grad,
                   hipStream_t st);
+// Split reduce of the transposed-read kernel's fragment-ordered partials
+// (a.partials, a.splits) into grad[o][k] += inv_k * sum; false when that
+// kernel does not apply to these arguments (use wgrad_reduce then).
+bool wgrad_tr_reduce(int dtype, const WgradArgs& a, float inv_k, float* grad, hipStream_t st);
 
 // BN statistics: partials [tiles][3][c] of (rows, sum h, sum (h - tile mean)^2)
 // combined across tiles with Chan's pairwise formula in fp64 (m rows in all).

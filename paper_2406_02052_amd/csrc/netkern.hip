@@ -3,6 +3,7 @@
 // the softmax cross-entropy head and the padded-channel split-K reduce.
 #include "common.h"
 #include "kernels.h"
+#include "prof.h"
 
 namespace petra {
 
@@ -268,26 +269,26 @@ __global__ __launch_bounds__(256) void wgrad_reduce_pad_kernel(const float* part
 
 void pad_channels8(int dtype, const void* src, int c_img, void* dst, long m, hipStream_t st) {
   if (dtype == DT_BF16)
-    hipLaunchKernelGGL(pad8_kernel<bf16_t>, dim3(grid_of(m * 8)), dim3(256), 0, st,
+    PETRA_LAUNCH(pad8_kernel<bf16_t>, dim3(grid_of(m * 8)), dim3(256), 0, st,
                        static_cast<const bf16_t*>(src), c_img, static_cast<bf16_t*>(dst), m);
   else
-    hipLaunchKernelGGL(pad8_kernel<float>, dim3(grid_of(m * 8)), dim3(256), 0, st,
+    PETRA_LAUNCH(pad8_kernel<float>, dim3(grid_of(m * 8)), dim3(256), 0, st,
                        static_cast<const float*>(src), c_img, static_cast<float*>(dst), m);
 }
 
 void copy_i32(const int32_t* src, int32_t* dst, int n, hipStream_t st) {
-  hipLaunchKernelGGL(copy_i32_kernel, dim3((n + 255) / 256), dim3(256), 0, st, src, dst, n);
+  PETRA_LAUNCH(copy_i32_kernel, dim3((n + 255) / 256), dim3(256), 0, st, src, dst, n);
 }
 
 void bn_apply_split(int dtype, const void* h, const float* scale, const float* shift, int relu,
                     void* out1, void* out2, long m, int c, hipStream_t st) {
   const unsigned g = grid_of(m * (c / 8));
   if (dtype == DT_BF16)
-    hipLaunchKernelGGL(bn_apply_split_kernel<bf16_t>, dim3(g), dim3(256), 0, st,
+    PETRA_LAUNCH(bn_apply_split_kernel<bf16_t>, dim3(g), dim3(256), 0, st,
                        static_cast<const bf16_t*>(h), scale, shift, relu,
                        static_cast<bf16_t*>(out1), static_cast<bf16_t*>(out2), m, c);
   else
-    hipLaunchKernelGGL(bn_apply_split_kernel<float>, dim3(g), dim3(256), 0, st,
+    PETRA_LAUNCH(bn_apply_split_kernel<float>, dim3(g), dim3(256), 0, st,
                        static_cast<const float*>(h), scale, shift, relu,
                        static_cast<float*>(out1), static_cast<float*>(out2), m, c);
 }
@@ -304,12 +305,12 @@ void split_bwd_partials(int dtype, const void* d1, const void* d2, const void* h
   const int rpt = split_rows_per_tile(m, c);
   const int tiles = static_cast<int>((m + rpt - 1) / rpt);
   if (dtype == DT_BF16)
-    hipLaunchKernelGGL(split_bwd_partials_kernel<bf16_t>, dim3(tiles), dim3(256), 0, st,
+    PETRA_LAUNCH(split_bwd_partials_kernel<bf16_t>, dim3(tiles), dim3(256), 0, st,
                        static_cast<const bf16_t*>(d1), static_cast<const bf16_t*>(d2),
                        static_cast<const bf16_t*>(h), scale, shift, mean, rstd, relu, partials, m,
                        c, rpt);
   else
-    hipLaunchKernelGGL(split_bwd_partials_kernel<float>, dim3(tiles), dim3(256), 0, st,
+    PETRA_LAUNCH(split_bwd_partials_kernel<float>, dim3(tiles), dim3(256), 0, st,
                        static_cast<const float*>(d1), static_cast<const float*>(d2),
                        static_cast<const float*>(h), scale, shift, mean, rstd, relu, partials, m,
                        c, rpt);
@@ -321,12 +322,12 @@ void split_bwd_apply(int dtype, const void* d1, const void* d2, const void* h,
                      hipStream_t st) {
   const unsigned g = grid_of(m * (c / 8));
   if (dtype == DT_BF16)
-    hipLaunchKernelGGL(split_bwd_apply_kernel<bf16_t>, dim3(g), dim3(256), 0, st,
+    PETRA_LAUNCH(split_bwd_apply_kernel<bf16_t>, dim3(g), dim3(256), 0, st,
                        static_cast<const bf16_t*>(d1), static_cast<const bf16_t*>(d2),
                        static_cast<const bf16_t*>(h), scale, shift, ca, cb, cc, mean, relu,
                        static_cast<bf16_t*>(dh), m, c);
   else
-    hipLaunchKernelGGL(split_bwd_apply_kernel<float>, dim3(g), dim3(256), 0, st,
+    PETRA_LAUNCH(split_bwd_apply_kernel<float>, dim3(g), dim3(256), 0, st,
                        static_cast<const float*>(d1), static_cast<const float*>(d2),
                        static_cast<const float*>(h), scale, shift, ca, cb, cc, mean, relu,
                        static_cast<float*>(dh), m, c);
@@ -336,11 +337,11 @@ void scatter_stride2_split(int dtype, const void* src, void* dst1, void* dst2, i
                            int w, int c, hipStream_t st) {
   const unsigned g = grid_of(static_cast<long>(n) * h * w * (c / 8));
   if (dtype == DT_BF16)
-    hipLaunchKernelGGL(scatter2_kernel<bf16_t>, dim3(g), dim3(256), 0, st,
+    PETRA_LAUNCH(scatter2_kernel<bf16_t>, dim3(g), dim3(256), 0, st,
                        static_cast<const bf16_t*>(src), static_cast<bf16_t*>(dst1),
                        static_cast<bf16_t*>(dst2), n, h, w, c);
   else
-    hipLaunchKernelGGL(scatter2_kernel<float>, dim3(g), dim3(256), 0, st,
+    PETRA_LAUNCH(scatter2_kernel<float>, dim3(g), dim3(256), 0, st,
                        static_cast<const float*>(src), static_cast<float*>(dst1),
                        static_cast<float*>(dst2), n, h, w, c);
 }
@@ -350,12 +351,12 @@ void head_forward_backward(int dtype, const void* x1, const void* x2, int n, int
                            float* pooled, float* dlogits, float* loss_n, void* g1, void* g2,
                            hipStream_t st) {
   if (dtype == DT_BF16)
-    hipLaunchKernelGGL(head_kernel<bf16_t>, dim3(n), dim3(256), 0, st,
+    PETRA_LAUNCH(head_kernel<bf16_t>, dim3(n), dim3(256), 0, st,
                        static_cast<const bf16_t*>(x1), static_cast<const bf16_t*>(x2), hw, c, wfc,
                        bfc, k, labels, n, pooled, dlogits, loss_n, static_cast<bf16_t*>(g1),
                        static_cast<bf16_t*>(g2));
   else
-    hipLaunchKernelGGL(head_kernel<float>, dim3(n), dim3(256), 0, st,
+    PETRA_LAUNCH(head_kernel<float>, dim3(n), dim3(256), 0, st,
                        static_cast<const float*>(x1), static_cast<const float*>(x2), hw, c, wfc,
                        bfc, k, labels, n, pooled, dlogits, loss_n, static_cast<float*>(g1),
                        static_cast<float*>(g2));
@@ -365,14 +366,14 @@ void head_param_grads(const float* pooled, const float* dlogits, const float* lo
                       int c, int k, float inv_k, float* grad_w, float* grad_b, float* loss,
                       hipStream_t st) {
   const long total = static_cast<long>(k) * c;
-  hipLaunchKernelGGL(head_grads_kernel, dim3(grid_of(total)), dim3(256), 0, st, pooled, dlogits,
+  PETRA_LAUNCH(head_grads_kernel, dim3(grid_of(total)), dim3(256), 0, st, pooled, dlogits,
                      loss_n, n, c, k, inv_k, grad_w, grad_b, loss);
 }
 
 void wgrad_reduce_pad(const float* part, int splits, int c_out, int taps, int c_pad, int c_real,
                       float inv_k, float* grad, hipStream_t st) {
   const long numel = static_cast<long>(c_out) * taps * c_real;
-  hipLaunchKernelGGL(wgrad_reduce_pad_kernel, dim3(grid_of(numel)), dim3(256), 0, st, part, splits,
+  PETRA_LAUNCH(wgrad_reduce_pad_kernel, dim3(grid_of(numel)), dim3(256), 0, st, part, splits,
                      c_out, taps, c_pad, c_real, inv_k, grad);
 }
 

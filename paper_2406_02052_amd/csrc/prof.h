@@ -2,6 +2,7 @@
 // the benchmark to measure each kernel class's average duration live.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <string>
@@ -16,6 +17,20 @@ enum KernelClass {
 
 const char* kernel_class_name(int k);
 
+// Start/stop events that the next kernel launch attaches to its dispatch
+// (set by Profiler::begin, cleared by Profiler::end; null when not profiling).
+struct LaunchEvents {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+extern thread_local LaunchEvents g_launch_events;
+
+// Every kernel launch of the library goes through this macro: with profiling
+// on, the runtime timestamps the dispatch itself (kernel start to end), so the
+// per-launch durations are kernel durations, not event-packet intervals.
+#define PETRA_LAUNCH(kernel, grid, block, shmem, stream, ...)                                 \
+  hipExtLaunchKernelGGL(kernel, grid, block, shmem, stream, ::petra::g_launch_events.start, \
+                        ::petra::g_launch_events.stop, 0, __VA_ARGS__)
+
 struct ProfRecord {
   int kind;
   hipEvent_t start, stop;
@@ -26,7 +41,8 @@ class Profiler {
  public:
   ~Profiler();
   bool enabled = false;
-  // Record the start of a launch of class `kind` on stream st (no-op when disabled).
+  // Bracket exactly one kernel launch of class `kind` (no-op when disabled): the
+  // launch in between carries the start/stop events on its dispatch.
   void begin(hipStream_t st);
   void end(int kind, hipStream_t st, double flops, double bytes);
   // Aggregate finished records (synchronises on their events) into totals.
@@ -40,7 +56,7 @@ class Profiler {
  private:
   std::vector<hipEvent_t> pool_;
   std::vector<ProfRecord> recs_;
-  hipEvent_t pending_ = nullptr;
+  hipEvent_t pending_ = nullptr, pending_stop_ = nullptr;
   hipEvent_t take();
 };
 

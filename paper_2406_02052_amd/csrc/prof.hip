@@ -2,6 +2,8 @@
 
 namespace petra {
 
+thread_local LaunchEvents g_launch_events;
+
 const char* kernel_class_name(int k) {
   static const char* names[K_NUM_CLASSES] = {
       "conv_fprop", "conv_dgrad", "conv_wgrad", "wgrad_reduce", "bn_finalize",
@@ -30,18 +32,24 @@ hipEvent_t Profiler::take() {
 }
 
 void Profiler::begin(hipStream_t st) {
+  (void)st;
   if (!enabled) return;
   pending_ = take();
-  if (pending_) (void)hipEventRecord(pending_, st);
+  pending_stop_ = take();
+  if (pending_ == nullptr || pending_stop_ == nullptr) {
+    pending_ = pending_stop_ = nullptr;
+    return;
+  }
+  g_launch_events.start = pending_;
+  g_launch_events.stop = pending_stop_;
 }
 
 void Profiler::end(int kind, hipStream_t st, double fl, double by) {
+  (void)st;
+  g_launch_events = LaunchEvents{};
   if (!enabled || pending_ == nullptr) return;
-  hipEvent_t stop = take();
-  if (stop == nullptr) return;
-  (void)hipEventRecord(stop, st);
-  recs_.push_back(ProfRecord{kind, pending_, stop, fl, by});
-  pending_ = nullptr;
+  recs_.push_back(ProfRecord{kind, pending_, pending_stop_, fl, by});
+  pending_ = pending_stop_ = nullptr;
 }
 
 hipError_t Profiler::collect() {

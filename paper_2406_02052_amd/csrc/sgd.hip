@@ -7,6 +7,7 @@
 // the KRSC copy and the transposed, R/S-flipped copy used for input gradients.
 #include "common.h"
 #include "kernels.h"
+#include "prof.h"
 
 namespace petra {
 
@@ -62,7 +63,7 @@ unsigned grid_for(int64_t n) {
 
 void sgd_update(float* theta, float* accum, float* mom, int64_t n, int64_t n_decay, float lr,
                 float momentum, float wd, int nesterov, hipStream_t st) {
-  hipLaunchKernelGGL(sgd_kernel, dim3(grid_for(n)), dim3(256), 0, st, theta, accum, mom, n, n_decay,
+  PETRA_LAUNCH(sgd_kernel, dim3(grid_for(n)), dim3(256), 0, st, theta, accum, mom, n, n_decay,
                      lr, momentum, wd, nesterov);
 }
 
@@ -71,10 +72,10 @@ void refresh_weights(int dtype, const float* theta, const WeightSegTable& segs, 
   if (segs.nseg <= 0) return;
   dim3 grid(grid_for(max_numel), segs.nseg);
   if (dtype == DT_BF16)
-    hipLaunchKernelGGL(refresh_kernel<bf16_t>, grid, dim3(256), 0, st, theta, segs,
+    PETRA_LAUNCH(refresh_kernel<bf16_t>, grid, dim3(256), 0, st, theta, segs,
                        static_cast<bf16_t*>(fwd_copy), static_cast<bf16_t*>(dg_copy));
   else
-    hipLaunchKernelGGL(refresh_kernel<float>, grid, dim3(256), 0, st, theta, segs,
+    PETRA_LAUNCH(refresh_kernel<float>, grid, dim3(256), 0, st, theta, segs,
                        static_cast<float*>(fwd_copy), static_cast<float*>(dg_copy));
 }
 

@@ -122,7 +122,11 @@ class Stage {
 
   GraphCache graphs;
   bool use_graphs = false;
-  int bwd_streams = 3;  // 1: one stream; 2: + weight gradients; 3: + recompute ahead
+  // 1: one stream; 2: + weight gradients; 3: + recompute ahead.  Set in the
+  // constructor: one stream for basic blocks (each cross-stream event costs more
+  // host time than the overlap gains there), three for bottleneck blocks (their
+  // HBM-bound 1x1 convs overlap well).
+  int bwd_streams = 1;
 
  private:
   // One residual function of the backward, in the order the backward visits them.

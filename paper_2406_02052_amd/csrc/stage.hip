@@ -35,6 +35,7 @@ size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 Stage::Stage(const petra_stage_desc& d) : desc(d) {
   dt = d.dtype == PETRA_BF16 ? DT_BF16 : DT_FP32;
+  bwd_streams = d.kind == PETRA_BLOCK_BOTTLENECK ? 3 : 1;
   esz = dt == DT_BF16 ? 2 : 4;
   M = static_cast<long>(d.n) * d.h * d.w;
   const int c = d.c_half, cm = d.c_mid;
@@ -416,8 +417,9 @@ void Stage::fn_grad(const BwdFn& f, Scratch& s, const BwdFn* next, Scratch* sn, 
     prof.end(K_CONV_WGRAD, wst, 2.0 * M * wnumel,
              static_cast<double>(esz) * M * (cv.cin + 2.0 * cv.cout) + 4.0 * w.splits * wnumel);
     prof.begin(wst);
-    wgrad_reduce(wpart, w.splits, static_cast<long>(cv.cout) * w.k_tot, inv_k, grad + cv.w_off,
-                 wst);
+    if (!wgrad_tr_reduce(dt, w, inv_k, grad + cv.w_off, wst))
+      wgrad_reduce(wpart, w.splits, static_cast<long>(cv.cout) * w.k_tot, inv_k, grad + cv.w_off,
+                   wst);
     prof.end(K_WGRAD_REDUCE, wst, 0.0, 4.0 * wnumel * (w.splits + 2));
   }
   if (part == 1) {
