@@ -159,6 +159,21 @@ __device__ __forceinline__ f32x4_t mfma(const Frag<float>& a, const Frag<float>&
   return c;
 }
 
+// Sum over the 16 lanes of a DPP row (lanes 16 r .. 16 r + 15), returned in
+// every lane of the row: pairs and quads by quad permutes, then the row's
+// half-mirror and mirror.  Four VALU ops with DPP modifiers, no LDS traffic.
+__device__ __forceinline__ float sum16(float v) {
+  int x = __builtin_bit_cast(int, v);
+  v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, x, 0xB1, 0xF, 0xF, false));  // [1,0,3,2]
+  x = __builtin_bit_cast(int, v);
+  v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, x, 0x4E, 0xF, 0xF, false));  // [2,3,0,1]
+  x = __builtin_bit_cast(int, v);
+  v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, x, 0x141, 0xF, 0xF, false)); // half mirror
+  x = __builtin_bit_cast(int, v);
+  v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, x, 0x140, 0xF, 0xF, false)); // mirror
+  return v;
+}
+
 // Sum over the 4 lane groups (lanes l, l^16, l^32, l^48) of a wave64.
 __device__ __forceinline__ float sum_lane_groups(float v) {
   v += __shfl_xor(v, 16, 64);

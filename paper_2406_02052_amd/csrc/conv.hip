@@ -1514,18 +1514,12 @@ __global__ __launch_bounds__(512, 1) void conv_img_kernel(ConvArgs a) {
     }
   }
   if constexpr (EP != EP_RESID) {
-    float n16 = nv;
-    n16 += __shfl_xor(n16, 1, 64); n16 += __shfl_xor(n16, 2, 64);
-    n16 += __shfl_xor(n16, 4, 64); n16 += __shfl_xor(n16, 8, 64);
+    const float n16 = sum16(nv);
 #pragma unroll
     for (int fn = 0; fn < FN; ++fn)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        float x = sa[fn][e], y = sb2[fn][e];
-        x += __shfl_xor(x, 1, 64); x += __shfl_xor(x, 2, 64);
-        x += __shfl_xor(x, 4, 64); x += __shfl_xor(x, 8, 64);
-        y += __shfl_xor(y, 1, 64); y += __shfl_xor(y, 2, 64);
-        y += __shfl_xor(y, 4, 64); y += __shfl_xor(y, 8, 64);
+        const float x = sum16(sa[fn][e]), y = sum16(sb2[fn][e]);
         if (lr == 0) {
           const int c = wn * TN + fn * 16 + lg * 4 + e;
           if constexpr (STATS) {
@@ -1840,18 +1834,12 @@ __global__ __launch_bounds__(256, 2) void conv32_kernel(ConvArgs a, int ntiles) 
 
   // Workgroup partials: lane sums over the 16 pixels lanes, then the four waves in order.
   if constexpr (EP != EP_RESID) {
-    float n16 = st_n;
-    n16 += __shfl_xor(n16, 1, 64); n16 += __shfl_xor(n16, 2, 64);
-    n16 += __shfl_xor(n16, 4, 64); n16 += __shfl_xor(n16, 8, 64);
+    const float n16 = sum16(st_n);
 #pragma unroll
     for (int fn = 0; fn < 2; ++fn)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        float x = st_a[fn][e], y = st_b[fn][e];
-        x += __shfl_xor(x, 1, 64); x += __shfl_xor(x, 2, 64);
-        x += __shfl_xor(x, 4, 64); x += __shfl_xor(x, 8, 64);
-        y += __shfl_xor(y, 1, 64); y += __shfl_xor(y, 2, 64);
-        y += __shfl_xor(y, 4, 64); y += __shfl_xor(y, 8, 64);
+        const float x = sum16(st_a[fn][e]), y = sum16(st_b[fn][e]);
         if constexpr (EP == EP_STATS) {
           // (count, mean, centred M2) of this wave from the shifted sums
           const float mean_d = n16 > 0.f ? x / n16 : 0.f;
