@@ -637,6 +637,162 @@ __global__ __launch_bounds__(256) void conv_staged_kernel(ConvArgs a) {
   }
 }
 
+// Epilogue for accumulators issued as D[cout][pixel] (the MFMA's A operand is
+// the weight fragment): lane (lr, lg) of fragment (fm, fn) holds output channels
+// n0 + wn*TN + fn*16 + lg*4 + e of tile pixel wm*TM + fm*16 + lr, pixel i of the
+// TH x TW tile at (p0 + i / TW, q0 + i % TW) of image img.  Each lane stores its
+// 4 channels directly (8 bytes, buffer store: pixels past the image are
+// dropped); BN statistics are shifted sums per lane, summed over the 16 pixel
+// lanes with DPP and over the WAVES_M waves in LDS, written as partial row
+// blockIdx.x.  Epilogues as in conv_gemm_kernel.
+template <int TW, int FM, int FN, int WAVES_M, int TM, int TN, int BN, int EP>
+__device__ __forceinline__ void epilogue_cp(const f32x4_t (&acc)[FM][FN], const ConvArgs& a,
+                                            int img, int p0, int q0, int n0, int wm, int wn,
+                                            int lane, int tid, int nthreads,
+                                            float (*red)[3][BN]) {
+  const int lr = lane & 15, lg = lane >> 4;
+  const long out_bytes = static_cast<long>(a.m) * a.c_out * 2;
+  const __amdgpu_buffer_rsrc_t r_out = make_rsrc(a.out, out_bytes);
+  const __amdgpu_buffer_rsrc_t r_eph = make_rsrc(a.ep_h != nullptr ? a.ep_h : a.out, out_bytes);
+  const __amdgpu_buffer_rsrc_t r_res = make_rsrc(a.resid != nullptr ? a.resid : a.out,
+                                                 a.resid != nullptr ? out_bytes : 0);
+  constexpr bool STATS = EP == EP_STATS;
+  constexpr bool GRAD = EP == EP_MASK || EP == EP_RESID_STATS;
+  float es[FN][4], esh[FN][4], emu[FN][4], ers[FN][4];
+  bool cok[FN];
+#pragma unroll
+  for (int fn = 0; fn < FN; ++fn) {
+    const int c0 = n0 + wn * TN + fn * 16 + lg * 4;
+    cok[fn] = c0 < a.c_out;   // c_out is a multiple of 8 and of 4
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      es[fn][e] = esh[fn][e] = emu[fn][e] = ers[fn][e] = 0.f;
+      if constexpr (GRAD) {
+        if (cok[fn]) {
+          es[fn][e] = EP == EP_MASK ? a.ep_scale[c0 + e] : 0.f;
+          esh[fn][e] = EP == EP_MASK ? a.ep_shift[c0 + e] : 0.f;
+          emu[fn][e] = a.ep_mean[c0 + e];
+          ers[fn][e] = a.ep_rstd[c0 + e];
+        }
+      }
+    }
+  }
+  float sa[FN][4], sb[FN][4], kk[FN][4];
+#pragma unroll
+  for (int fn = 0; fn < FN; ++fn)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) sa[fn][e] = sb[fn][e] = kk[fn][e] = 0.f;
+  float nv = 0.f;
+#pragma unroll
+  for (int fm = 0; fm < FM; ++fm) {
+    const int i = wm * TM + fm * 16 + lr;
+    const int ph = i / TW, pw = i - ph * TW;
+    const bool vm = p0 + ph < a.h && q0 + pw < a.w;
+    nv += vm ? 1.f : 0.f;
+    const long pix = (static_cast<long>(img) * a.h + p0 + ph) * a.w + q0 + pw;
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn) {
+      const bool ok = vm && cok[fn];
+      const uint32_t boff =
+          ok ? static_cast<uint32_t>((pix * a.c_out + n0 + wn * TN + fn * 16 + lg * 4) * 2) : BUF_OOB;
+      float v[4] = {acc[fm][fn][0], acc[fm][fn][1], acc[fm][fn][2], acc[fm][fn][3]};
+      float hl[4] = {0.f, 0.f, 0.f, 0.f};
+      if constexpr (GRAD) {
+        const u32x2_t hw = buf_load8(r_eph, boff);
+        hl[0] = __uint_as_float(hw.x << 16); hl[1] = __uint_as_float(hw.x & 0xffff0000u);
+        hl[2] = __uint_as_float(hw.y << 16); hl[3] = __uint_as_float(hw.y & 0xffff0000u);
+      }
+      if constexpr (EP == EP_RESID || EP == EP_RESID_STATS) {
+        const u32x2_t rw = buf_load8(r_res, boff);   // a null residual reads zeros
+        v[0] += __uint_as_float(rw.x << 16); v[1] += __uint_as_float(rw.x & 0xffff0000u);
+        v[2] += __uint_as_float(rw.y << 16); v[3] += __uint_as_float(rw.y & 0xffff0000u);
+      }
+      if constexpr (EP == EP_MASK) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = fmaf(es[fn][e], hl[e], esh[fn][e]) > 0.f ? v[e] : 0.f;
+      }
+      const uint32_t w0 = pack_bf16x2(v[0], v[1]), w1 = pack_bf16x2(v[2], v[3]);
+      buf_store8(u32x2_t{w0, w1}, r_out, boff);
+      // statistics of the stored values
+      v[0] = __uint_as_float(w0 << 16); v[1] = __uint_as_float(w0 & 0xffff0000u);
+      v[2] = __uint_as_float(w1 << 16); v[3] = __uint_as_float(w1 & 0xffff0000u);
+      if constexpr (STATS) {
+        if (fm == 0) {
+          // shift per channel: the stored value of this wave's first pixel
+#pragma unroll
+          for (int e = 0; e < 4; ++e) kk[fn][e] = __shfl(v[e], lane & 48, 64);
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float d = vm ? v[e] - kk[fn][e] : 0.f;
+          sa[fn][e] += d;
+          sb[fn][e] = fmaf(d, d, sb[fn][e]);
+        }
+      } else if constexpr (GRAD) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float g = vm ? v[e] : 0.f;
+          sa[fn][e] += g;
+          sb[fn][e] += g * ((hl[e] - emu[fn][e]) * ers[fn][e]);
+        }
+      }
+    }
+  }
+  if constexpr (STATS || GRAD) {
+    const float n16 = sum16(nv);
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float x = sum16(sa[fn][e]), y = sum16(sb[fn][e]);
+        if (lr == 0) {
+          const int c = wn * TN + fn * 16 + lg * 4 + e;
+          if constexpr (STATS) {
+            const float md = n16 > 0.f ? x / n16 : 0.f;
+            red[wm][0][c] = n16;
+            red[wm][1][c] = kk[fn][e] + md;                            // mean
+            red[wm][2][c] = n16 > 0.f ? fmaxf(y - x * md, 0.f) : 0.f;  // centred M2
+          } else {
+            red[wm][1][c] = x;
+            red[wm][2][c] = y;
+          }
+        }
+      }
+    __syncthreads();
+    for (int c = tid; c < BN; c += nthreads) {
+      const int col = n0 + c;
+      if (col >= a.c_out) continue;
+      float* pr = a.partials;
+      const long row = static_cast<long>(blockIdx.x);
+      if constexpr (STATS) {
+        float n = 0.f, mean = 0.f, m2 = 0.f;
+#pragma unroll
+        for (int w = 0; w < WAVES_M; ++w) {
+          const float nb = red[w][0][c];
+          if (nb > 0.f) {
+            const float nn = n + nb, rb = nb / nn, d = red[w][1][c] - mean;
+            mean += d * rb;
+            m2 += red[w][2][c] + d * d * n * rb;
+            n = nn;
+          }
+        }
+        pr[(row * 3 + 0) * a.c_out + col] = n;
+        pr[(row * 3 + 1) * a.c_out + col] = n * mean;
+        pr[(row * 3 + 2) * a.c_out + col] = m2;
+      } else {
+        float t1 = 0.f, t2 = 0.f;
+#pragma unroll
+        for (int w = 0; w < WAVES_M; ++w) {
+          t1 += red[w][1][c];
+          t2 += red[w][2][c];
+        }
+        pr[(row * 2 + 0) * a.c_out + col] = t1;
+        pr[(row * 2 + 1) * a.c_out + col] = t2;
+      }
+    }
+  }
+}
+
 // Halo-tile variant for 3x3 / stride 1 / pad 1 bf16 convolutions with C_in a
 // multiple of 32.  A workgroup owns a TH x TW patch of output pixels of one
 // image; per 32-channel chunk it loads the (TH+2) x (TW+2) input patch once into
@@ -665,11 +821,10 @@ __global__ __launch_bounds__(256) void conv_halo_kernel(ConvArgs a) {
   constexpr int PATCH = HPIX * HP;
   constexpr int SLAB = BN * BPITCH;
   constexpr int MAIN_BYTES = (HB * PATCH + NSLAB * SLAB) * 2;
-  constexpr int EPI_BYTES = 4 * TN * EP_RP * 4;
-  constexpr int LDS_BYTES = MAIN_BYTES > EPI_BYTES ? MAIN_BYTES : EPI_BYTES;
+  constexpr int LDS_BYTES = MAIN_BYTES;
   __shared__ __attribute__((aligned(16))) unsigned char lds[LDS_BYTES];
   __shared__ float pro_tab[PRO == PRO_BWD ? 4 : 2][512];
-  __shared__ float red[WAVES_M][2][BN];
+  __shared__ float red3[WAVES_M][3][BN];
 
   T* patch_base = reinterpret_cast<T*>(lds);
   T* slab_base = patch_base + HB * PATCH;
@@ -816,9 +971,8 @@ __global__ __launch_bounds__(256) void conv_halo_kernel(ConvArgs a) {
 #pragma unroll
       for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
-        for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma(af[fm], bfr[fn], acc[fm][fn]);
+        for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma(bfr[fn], af[fm], acc[fm][fn]);
     }
-    __syncthreads();   // the epilogue reuses the operand LDS
   }
   // Chunks x nine unrolled taps.  Every prefetch is unconditional (past the
   // end it re-reads the last chunk / slab into the buffer not being read), so
@@ -841,7 +995,7 @@ __global__ __launch_bounds__(256) void conv_halo_kernel(ConvArgs a) {
 #pragma unroll
       for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
-        for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma(af[fm], bfr[fn], acc[fm][fn]);
+        for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma(bfr[fn], af[fm], acc[fm][fn]);
       park_slab((step + 1) & 1);
       if constexpr (HB > 1) {
         if (tap == 8) {
@@ -853,132 +1007,11 @@ __global__ __launch_bounds__(256) void conv_halo_kernel(ConvArgs a) {
     }
   }
 
-  if constexpr (EP == EP_STATS) {
-    tile_stats<T, FM, FN, WAVES_M, TN, BN>(
-        acc,
-        [&](int fm, int j) {
-          const int i = wm * TM + fm * 16 + lg * 4 + j;
-          const int ph = i / TW;
-          return p0 + ph < a.h && q0 + (i - ph * TW) < a.w;
-        },
-        wm, wn, lane, n0, a.c_out, a.partials, blockIdx.x);
-  }
-  // Epilogue (as in the staged kernel, pixels mapped back to NHWC rows).
-  float* ep = reinterpret_cast<float*>(lds) + wave * TN * EP_RP;
-  constexpr int CG = TN / 8;
-  constexpr int TASKS = 16 * CG;
-  const int my_cg = lane % CG;
-  const int col = n0 + wn * TN + my_cg * 8;
-  const bool cvalid = col < a.c_out;
-  float s1[8], s2[8];
-#pragma unroll
-  for (int j = 0; j < 8; ++j) s1[j] = s2[j] = 0.f;
-  float es[8], esh[8], emu[8], ers[8];
-  if constexpr (EP == EP_MASK || EP == EP_RESID_STATS) {
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      es[j] = cvalid && EP == EP_MASK ? a.ep_scale[col + j] : 0.f;
-      esh[j] = cvalid && EP == EP_MASK ? a.ep_shift[col + j] : 0.f;
-      emu[j] = cvalid ? a.ep_mean[col + j] : 0.f;
-      ers[j] = cvalid ? a.ep_rstd[col + j] : 0.f;
-    }
-  }
-  T* out = static_cast<T*>(a.out);
-#pragma unroll
-  for (int fm = 0; fm < FM; ++fm) {
-#pragma unroll
-    for (int fn = 0; fn < FN; ++fn)
-      *reinterpret_cast<f32x4_t*>(ep + (fn * 16 + lr) * EP_RP + lg * 4) = acc[fm][fn];
-    __syncthreads();
-    for (int t = lane; t < TASKS; t += 64) {
-      const int rr = t / CG;
-      const int i = wm * TM + fm * 16 + rr;
-      const int ph = i / TW, pw = i - ph * TW;
-      const int pp = p0 + ph, qq = q0 + pw;
-      if (!(cvalid && pp < a.h && qq < a.w)) continue;
-      float v[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) v[j] = ep[(my_cg * 8 + j) * EP_RP + rr];
-      const long idx = (img_base + static_cast<long>(pp) * a.w + qq) * a.c_out + col;
-      Raw8<T> o;
-      if constexpr (EP == EP_STATS) {
-        o.from_f32(v);
-      } else if constexpr (EP == EP_MASK) {
-        Raw8<T> hr;
-        hr.load(static_cast<const T*>(a.ep_h) + idx);
-        float hl[8];
-        hr.to_f32(hl);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) v[j] = fmaf(es[j], hl[j], esh[j]) > 0.f ? v[j] : 0.f;
-        o.from_f32(v);
-        o.to_f32(v);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          s1[j] += v[j];
-          s2[j] += v[j] * ((hl[j] - emu[j]) * ers[j]);
-        }
-      } else {
-        if (a.resid != nullptr) {  // without a residual the epilogue is a plain store
-          Raw8<T> rr8;
-          rr8.load(static_cast<const T*>(a.resid) + idx);
-          float rv[8];
-          rr8.to_f32(rv);
-#pragma unroll
-          for (int j = 0; j < 8; ++j) v[j] += rv[j];
-        }
-        o.from_f32(v);
-        if constexpr (EP == EP_RESID_STATS) {  // BN-backward partials of the stored values
-          Raw8<T> hr;
-          hr.load(static_cast<const T*>(a.ep_h) + idx);
-          float hl[8];
-          hr.to_f32(hl);
-          o.to_f32(v);
-#pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            s1[j] += v[j];
-            s2[j] += v[j] * ((hl[j] - emu[j]) * ers[j]);
-          }
-        }
-      }
-      *reinterpret_cast<uint4*>(out + idx) = make_uint4(o.w[0], o.w[1], o.w[2], o.w[3]);
-    }
-    __syncthreads();
-  }
-  if constexpr (EP == EP_MASK || EP == EP_RESID_STATS) {
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      for (int off = CG; off < 64; off <<= 1) {
-        s1[j] += __shfl_xor(s1[j], off, 64);
-        s2[j] += __shfl_xor(s2[j], off, 64);
-      }
-    }
-    if (lane < CG) {
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        red[wm][0][wn * TN + lane * 8 + j] = s1[j];
-        red[wm][1][wn * TN + lane * 8 + j] = s2[j];
-      }
-    }
-    __syncthreads();
-    for (int i = tid; i < 2 * BN; i += 256) {
-      const int which = i / BN, cl = i - which * BN;
-      const int c = n0 + cl;
-      if (c >= a.c_out) continue;
-      float t = 0.f;
-#pragma unroll
-      for (int w = 0; w < WAVES_M; ++w) t += red[w][which][cl];
-      a.partials[(static_cast<long>(blockIdx.x) * 2 + which) * a.c_out + c] = t;
-    }
-  }
+  // acc holds D[cout][pixel] (weights are the MFMA's A operand)
+  epilogue_cp<TW, FM, FN, WAVES_M, TM, TN, BN, EP>(acc, a, img, p0, q0, n0, wm, wn, lane, tid, 256,
+                                                   red3);
 }
 
-// Full-patch variant for the MFMA-bound 3x3 convs with several 32-channel input
-// chunks (C_in = 32 * CH).  The workgroup loads the whole (TH+2) x (TW+2)
-// input patch of all chunks into LDS once (chunk c + 1 in flight while chunk c
-// gets its prologue and is parked), then runs the CH x 9 (chunk, tap) steps
-// with no barrier: patch fragments come from LDS and weight fragments straight
-// from L2 into a ring of registers issued three steps ahead, so the MFMAs never
-// wait on a load issued in the same step.
 template <int TH, int TW, int BN, int WAVES_M, int CH, int EP, int PRO>
 __global__ __launch_bounds__(256, 2) void conv_fp_kernel(ConvArgs a) {
   using T = bf16_t;
@@ -994,12 +1027,11 @@ __global__ __launch_bounds__(256, 2) void conv_fp_kernel(ConvArgs a) {
   constexpr int STEPS = CH * 9;
   constexpr int D = 3;                                // weight prefetch depth (steps)
   constexpr int MAIN_BYTES = CH * PLANE * 2;
-  constexpr int EPI_BYTES = 4 * TN * EP_RP * 4;
-  constexpr int LDS_BYTES = MAIN_BYTES > EPI_BYTES ? MAIN_BYTES : EPI_BYTES;
+  constexpr int LDS_BYTES = MAIN_BYTES;
   constexpr bool BWD = PRO == PRO_BWD;
   __shared__ __attribute__((aligned(16))) unsigned char lds[LDS_BYTES];
   __shared__ float pro_tab[BWD ? 4 : 2][PRO == PRO_NONE ? 1 : CH * 32];
-  __shared__ float red[WAVES_M][2][BN];
+  __shared__ float red3[WAVES_M][3][BN];
 
   T* patch = reinterpret_cast<T*>(lds);
   const int tid = threadIdx.x;
@@ -1137,128 +1169,13 @@ __global__ __launch_bounds__(256, 2) void conv_fp_kernel(ConvArgs a) {
 #pragma unroll
     for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
-      for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma(af[s & 1][fm], cur[fn], acc[fm][fn]);
+      for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma(cur[fn], af[s & 1][fm], acc[fm][fn]);
     __builtin_amdgcn_sched_barrier(0);
   }
-  __syncthreads();   // the epilogue reuses the patch LDS
 
-  if constexpr (EP == EP_STATS) {
-    tile_stats<T, FM, FN, WAVES_M, TN, BN>(
-        acc,
-        [&](int fm, int j) {
-          const int i = wm * TM + fm * 16 + lg * 4 + j;
-          const int ph = i / TW;
-          return p0 + ph < a.h && q0 + (i - ph * TW) < a.w;
-        },
-        wm, wn, lane, n0, a.c_out, a.partials, blockIdx.x);
-  }
-  // Epilogue (as in the staged kernel, pixels mapped back to NHWC rows).
-  float* ep = reinterpret_cast<float*>(lds) + wave * TN * EP_RP;
-  constexpr int CG = TN / 8;
-  constexpr int TASKS = 16 * CG;
-  const int my_cg = lane % CG;
-  const int col = n0 + wn * TN + my_cg * 8;
-  const bool cvalid = col < a.c_out;
-  float s1[8], s2[8];
-#pragma unroll
-  for (int j = 0; j < 8; ++j) s1[j] = s2[j] = 0.f;
-  float es[8], esh[8], emu[8], ers[8];
-  if constexpr (EP == EP_MASK || EP == EP_RESID_STATS) {
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      es[j] = cvalid && EP == EP_MASK ? a.ep_scale[col + j] : 0.f;
-      esh[j] = cvalid && EP == EP_MASK ? a.ep_shift[col + j] : 0.f;
-      emu[j] = cvalid ? a.ep_mean[col + j] : 0.f;
-      ers[j] = cvalid ? a.ep_rstd[col + j] : 0.f;
-    }
-  }
-  T* out = static_cast<T*>(a.out);
-#pragma unroll
-  for (int fm = 0; fm < FM; ++fm) {
-#pragma unroll
-    for (int fn = 0; fn < FN; ++fn)
-      *reinterpret_cast<f32x4_t*>(ep + (fn * 16 + lr) * EP_RP + lg * 4) = acc[fm][fn];
-    __syncthreads();
-    for (int t = lane; t < TASKS; t += 64) {
-      const int rr = t / CG;
-      const int i = wm * TM + fm * 16 + rr;
-      const int ph = i / TW, pw = i - ph * TW;
-      const int pp = p0 + ph, qq = q0 + pw;
-      if (!(cvalid && pp < a.h && qq < a.w)) continue;
-      float v[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) v[j] = ep[(my_cg * 8 + j) * EP_RP + rr];
-      const long idx = (img_base + static_cast<long>(pp) * a.w + qq) * a.c_out + col;
-      Raw8<T> o;
-      if constexpr (EP == EP_STATS) {
-        o.from_f32(v);
-      } else if constexpr (EP == EP_MASK) {
-        Raw8<T> hr;
-        hr.load(static_cast<const T*>(a.ep_h) + idx);
-        float hl[8];
-        hr.to_f32(hl);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) v[j] = fmaf(es[j], hl[j], esh[j]) > 0.f ? v[j] : 0.f;
-        o.from_f32(v);
-        o.to_f32(v);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          s1[j] += v[j];
-          s2[j] += v[j] * ((hl[j] - emu[j]) * ers[j]);
-        }
-      } else {
-        if (a.resid != nullptr) {  // without a residual the epilogue is a plain store
-          Raw8<T> rr8;
-          rr8.load(static_cast<const T*>(a.resid) + idx);
-          float rv[8];
-          rr8.to_f32(rv);
-#pragma unroll
-          for (int j = 0; j < 8; ++j) v[j] += rv[j];
-        }
-        o.from_f32(v);
-        if constexpr (EP == EP_RESID_STATS) {  // BN-backward partials of the stored values
-          Raw8<T> hr;
-          hr.load(static_cast<const T*>(a.ep_h) + idx);
-          float hl[8];
-          hr.to_f32(hl);
-          o.to_f32(v);
-#pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            s1[j] += v[j];
-            s2[j] += v[j] * ((hl[j] - emu[j]) * ers[j]);
-          }
-        }
-      }
-      *reinterpret_cast<uint4*>(out + idx) = make_uint4(o.w[0], o.w[1], o.w[2], o.w[3]);
-    }
-    __syncthreads();
-  }
-  if constexpr (EP == EP_MASK || EP == EP_RESID_STATS) {
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      for (int off = CG; off < 64; off <<= 1) {
-        s1[j] += __shfl_xor(s1[j], off, 64);
-        s2[j] += __shfl_xor(s2[j], off, 64);
-      }
-    }
-    if (lane < CG) {
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        red[wm][0][wn * TN + lane * 8 + j] = s1[j];
-        red[wm][1][wn * TN + lane * 8 + j] = s2[j];
-      }
-    }
-    __syncthreads();
-    for (int i = tid; i < 2 * BN; i += 256) {
-      const int which = i / BN, cl = i - which * BN;
-      const int c = n0 + cl;
-      if (c >= a.c_out) continue;
-      float t = 0.f;
-#pragma unroll
-      for (int w = 0; w < WAVES_M; ++w) t += red[w][which][cl];
-      a.partials[(static_cast<long>(blockIdx.x) * 2 + which) * a.c_out + c] = t;
-    }
-  }
+  // acc holds D[cout][pixel] (weights are the MFMA's A operand)
+  epilogue_cp<TW, FM, FN, WAVES_M, TM, TN, BN, EP>(acc, a, img, p0, q0, n0, wm, wn, lane, tid, 256,
+                                                   red3);
 }
 
 // Whole-image 3x3 / stride 1 / pad 1 conv for the MFMA-bound shapes: one
