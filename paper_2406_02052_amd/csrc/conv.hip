@@ -2312,18 +2312,19 @@ __global__ __launch_bounds__(256) void wgrad_halo_kernel(WgradArgs a) {
 // TH x TW pixel tiles; the next tile is in flight while the current one is
 // multiplied (double-buffered LDS, one barrier per tile).  Waves split the
 // output: WO x WC channel blocks of OF x CF fragments, and WT groups of taps.
-template <int R, int TH, int TW, int WO, int OF, int WC, int CF, int WT, bool PRO, bool DH>
-__global__ __launch_bounds__(64 * WO * WC * WT) void wgrad_tr_kernel(WgradArgs a) {
+template <int R, int TH, int TW, int WO, int OF, int WC, int CF, int WT, int WP, bool PRO, bool DH>
+__global__ __launch_bounds__(64 * WO * WC * WT * WP) void wgrad_tr_kernel(WgradArgs a) {
   using T = bf16_t;
   typedef short v4i16 __attribute__((ext_vector_type(4)));
   typedef short v8i16 __attribute__((ext_vector_type(8)));
-  constexpr int NT = 64 * WO * WC * WT;
+  constexpr int NW = WO * WC * WT;                    // waves of one pixel group
+  constexpr int NT = 64 * NW * WP;
   constexpr int TAPS = R * R, TPW = TAPS / WT;
   static_assert(TPW * WT == TAPS, "taps per wave");
   constexpr int BO = WO * OF * 16, BC = WC * CF * 16;
   constexpr int NPIX = TH * TW;
-  static_assert(NPIX % 32 == 0, "pixel tile");
-  constexpr int KSTEPS = NPIX / 32;
+  static_assert(NPIX % (32 * WP) == 0, "pixel tile");
+  constexpr int KSTEPS = NPIX / 32 / WP;             // k-steps per pixel group and tile
   constexpr int PAD = R / 2;
   constexpr int HTH = TH + 2 * PAD, HTW = TW + 2 * PAD, HPIX = HTH * HTW;
   constexpr int PO = BO + 16, PC = BC + 16;          // LDS row pitches (bf16)
@@ -2336,7 +2337,8 @@ __global__ __launch_bounds__(64 * WO * WC * WT) void wgrad_tr_kernel(WgradArgs a
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
-  const int wo = wave % WO, wc = (wave / WO) % WC, wt = wave / (WO * WC);
+  const int wo = wave % WO, wc = (wave / WO) % WC, wt = (wave / (WO * WC)) % WT;
+  const int wp = wave / NW;   // pixel group: k-steps wp, wp + WP, ... of each tile
   const int li = lane & 15, kg = lane >> 4;
   const int o0 = blockIdx.y * BO, c0 = blockIdx.z * BC;
   // 1x1: no halo; tiles are runs of NPIX consecutive pixels of the flat [m] index
@@ -2437,6 +2439,25 @@ __global__ __launch_bounds__(64 * WO * WC * WT) void wgrad_tr_kernel(WgradArgs a
     return f;
   };
 
+  // Per-lane LDS offsets of the transposing reads (independent of the tile):
+  // rows kg*8 + (li>>2) (+4) of k-step ks, quarter (li&3) of the 16-channel run.
+  int da[KSTEPS], xa[KSTEPS], xb[KSTEPS];
+#pragma unroll
+  for (int ks = 0; ks < KSTEPS; ++ks) {
+    const int pa = (ks * WP + wp) * 32 + kg * 8 + (li >> 2), pb = pa + 4;
+    const int qo = (li & 3) * 4;
+    da[ks] = pa * PO + wo * OF * 16 + qo;
+    xa[ks] = ((pa / TW) * HTW + pa % TW) * PC + wc * CF * 16 + qo;
+    xb[ks] = ((pb / TW) * HTW + pb % TW) * PC + wc * CF * 16 + qo;
+  }
+  // LDS offsets of this wave's taps (patch row/column shift), in elements
+  int u_off[TPW];
+#pragma unroll
+  for (int u = 0; u < TPW; ++u) {
+    const int tap = wt * TPW + u;
+    u_off[u] = ((tap / R) * HTW + tap % R) * PC;
+  }
+
   f32x4_t acc[OF][CF][TPW];
 #pragma unroll
   for (int of = 0; of < OF; ++of)
@@ -2454,26 +2475,20 @@ __global__ __launch_bounds__(64 * WO * WC * WT) void wgrad_tr_kernel(WgradArgs a
     park_tile(buf);
     __syncthreads();
     load_tile(min(t + splits, ntiles - 1));
+    const T* sdb = sd[buf];
+    const T* sxb = sx[buf];
 #pragma unroll
     for (int ks = 0; ks < KSTEPS; ++ks) {
-      // this lane's two pixels (rows of the transposing reads)
-      const int pa = ks * 32 + kg * 8 + (li >> 2), pb = pa + 4;
-      const int qo = (li & 3) * 4;
       Frag<T> fa[OF];
 #pragma unroll
-      for (int of = 0; of < OF; ++of) {
-        const int ob = (wo * OF + of) * 16 + qo;
-        fa[of] = tr_frag(&sd[buf][pa * PO + ob], &sd[buf][pb * PO + ob]);
-      }
-      const int ra = (pa / TW) * HTW + pa % TW, rb = (pb / TW) * HTW + pb % TW;
+      for (int of = 0; of < OF; ++of)
+        fa[of] = tr_frag(sdb + da[ks] + of * 16, sdb + da[ks] + 4 * PO + of * 16);
 #pragma unroll
       for (int u = 0; u < TPW; ++u) {
-        const int tap = wt * TPW + u;
-        const int toff = (tap / R) * HTW + tap % R;
+        const int toff = u_off[u];
 #pragma unroll
         for (int cf = 0; cf < CF; ++cf) {
-          const int cb = (wc * CF + cf) * 16 + qo;
-          const Frag<T> fb = tr_frag(&sx[buf][(ra + toff) * PC + cb], &sx[buf][(rb + toff) * PC + cb]);
+          const Frag<T> fb = tr_frag(sxb + xa[ks] + toff + cf * 16, sxb + xb[ks] + toff + cf * 16);
 #pragma unroll
           for (int of = 0; of < OF; ++of) acc[of][cf][u] = mfma(fa[of], fb, acc[of][cf][u]);
         }
@@ -2482,10 +2497,40 @@ __global__ __launch_bounds__(64 * WO * WC * WT) void wgrad_tr_kernel(WgradArgs a
     buf ^= 1;
   }
 
+  // Pixel groups 1.. add their sums into group 0 through LDS, one group per
+  // round (fixed order).
+  constexpr int NFRAG = OF * CF * TPW;
+  if constexpr (WP > 1) {
+    f32x4_t* xch = reinterpret_cast<f32x4_t*>(&sx[0][0]);   // tiles are no longer read
+    static_assert(NW * NFRAG * 64 * 16 <= static_cast<int>(sizeof(sx)), "exchange space");
+#pragma unroll
+    for (int g = 1; g < WP; ++g) {
+      __syncthreads();
+      if (wp == g) {
+#pragma unroll
+        for (int of = 0; of < OF; ++of)
+#pragma unroll
+          for (int cf = 0; cf < CF; ++cf)
+#pragma unroll
+            for (int u = 0; u < TPW; ++u)
+              xch[((wave % NW) * NFRAG + (of * CF + cf) * TPW + u) * 64 + lane] = acc[of][cf][u];
+      }
+      __syncthreads();
+      if (wp == 0) {
+#pragma unroll
+        for (int of = 0; of < OF; ++of)
+#pragma unroll
+          for (int cf = 0; cf < CF; ++cf)
+#pragma unroll
+            for (int u = 0; u < TPW; ++u)
+              acc[of][cf][u] += xch[(wave * NFRAG + (of * CF + cf) * TPW + u) * 64 + lane];
+      }
+    }
+    if (wp > 0) return;
+  }
   // Partials in fragment order: every (wave, fragment) owns 256 consecutive
   // floats, lane l at 4 l .. 4 l + 3, so each wave writes whole cache lines;
   // wgrad_tr_reduce maps them back to [o][k].
-  constexpr int NW = WO * WC * WT;
   const long wg_base = (static_cast<long>(blockIdx.y) * gridDim.z + blockIdx.z) * NW + wave;
   float* outp = a.partials + static_cast<long>(blockIdx.x) * a.c_out * a.k_tot;
 #pragma unroll
@@ -2809,21 +2854,22 @@ int wgrad_tr_plan(int dtype, const WgradArgs& a, int* splits) {
 }
 
 namespace {
-template <int R, int TH, int TW, int WO, int OF, int WC, int CF, int WT>
+template <int R, int TH, int TW, int WO, int OF, int WC, int CF, int WT, int WP>
 TrMap tr_map(const WgradArgs& a) {
   constexpr int BO = WO * OF * 16, BC = WC * CF * 16;
+  (void)WP;
   return TrMap{WO, OF, WC, CF, WT, R * R / WT, BO, BC, a.c_in / BC, a.c_in, a.k_tot};
 }
 
-template <int R, int TH, int TW, int WO, int OF, int WC, int CF, int WT>
+template <int R, int TH, int TW, int WO, int OF, int WC, int CF, int WT, int WP>
 void launch_wgrad_tr(const WgradArgs& a, hipStream_t st) {
   constexpr int BO = WO * OF * 16, BC = WC * CF * 16;
   dim3 grid(a.splits, a.c_out / BO, a.c_in / BC);
-  dim3 block(64 * WO * WC * WT);
+  dim3 block(64 * WO * WC * WT * WP);
   if (a.pro_scale != nullptr)
-    PETRA_LAUNCH((wgrad_tr_kernel<R, TH, TW, WO, OF, WC, CF, WT, true, true>), grid, block, 0, st, a);
+    PETRA_LAUNCH((wgrad_tr_kernel<R, TH, TW, WO, OF, WC, CF, WT, WP, true, true>), grid, block, 0, st, a);
   else
-    PETRA_LAUNCH((wgrad_tr_kernel<R, TH, TW, WO, OF, WC, CF, WT, false, true>), grid, block, 0, st, a);
+    PETRA_LAUNCH((wgrad_tr_kernel<R, TH, TW, WO, OF, WC, CF, WT, WP, false, true>), grid, block, 0, st, a);
 }
 }  // namespace
 
@@ -2831,12 +2877,12 @@ bool wgrad_tr_reduce(int dtype, const WgradArgs& a, float inv_k, float* grad, hi
   int sp = 0;
   TrMap mp{};
   switch (wgrad_tr_plan(dtype, a, &sp)) {
-    case 1: mp = tr_map<3, 4, 32, 1, 2, 1, 2, 3>(a); break;
-    case 2: mp = tr_map<3, 4, 56, 1, 2, 1, 2, 3>(a); break;
-    case 3: mp = tr_map<3, 8, 16, 1, 4, 4, 1, 1>(a); break;
-    case 4: mp = tr_map<3, 8, 8, 1, 4, 4, 1, 1>(a); break;
-    case 5: mp = tr_map<1, 1, 128, 1, 2, 4, 2, 1>(a); break;
-    case 6: mp = tr_map<1, 1, 128, 4, 2, 1, 2, 1>(a); break;
+    case 1: mp = tr_map<3, 4, 32, 1, 2, 1, 2, 3, 4>(a); break;
+    case 2: mp = tr_map<3, 4, 56, 1, 2, 1, 2, 3, 1>(a); break;
+    case 3: mp = tr_map<3, 8, 16, 1, 4, 4, 1, 1, 1>(a); break;
+    case 4: mp = tr_map<3, 8, 8, 1, 4, 4, 1, 1, 1>(a); break;
+    case 5: mp = tr_map<1, 1, 128, 1, 2, 4, 2, 1, 1>(a); break;
+    case 6: mp = tr_map<1, 1, 128, 4, 2, 1, 2, 1, 1>(a); break;
     default: return false;
   }
   const long numel = static_cast<long>(a.c_out) * a.k_tot;
@@ -2849,12 +2895,12 @@ bool wgrad_tr_reduce(int dtype, const WgradArgs& a, float inv_k, float* grad, hi
 bool conv_wgrad_tr(int dtype, const WgradArgs& a, hipStream_t st) {
   int sp = 0;
   switch (wgrad_tr_plan(dtype, a, &sp)) {
-    case 1: launch_wgrad_tr<3, 4, 32, 1, 2, 1, 2, 3>(a, st); return true;
-    case 2: launch_wgrad_tr<3, 4, 56, 1, 2, 1, 2, 3>(a, st); return true;
-    case 3: launch_wgrad_tr<3, 8, 16, 1, 4, 4, 1, 1>(a, st); return true;
-    case 4: launch_wgrad_tr<3, 8, 8, 1, 4, 4, 1, 1>(a, st); return true;
-    case 5: launch_wgrad_tr<1, 1, 128, 1, 2, 4, 2, 1>(a, st); return true;
-    case 6: launch_wgrad_tr<1, 1, 128, 4, 2, 1, 2, 1>(a, st); return true;
+    case 1: launch_wgrad_tr<3, 4, 32, 1, 2, 1, 2, 3, 4>(a, st); return true;
+    case 2: launch_wgrad_tr<3, 4, 56, 1, 2, 1, 2, 3, 1>(a, st); return true;
+    case 3: launch_wgrad_tr<3, 8, 16, 1, 4, 4, 1, 1, 1>(a, st); return true;
+    case 4: launch_wgrad_tr<3, 8, 8, 1, 4, 4, 1, 1, 1>(a, st); return true;
+    case 5: launch_wgrad_tr<1, 1, 128, 1, 2, 4, 2, 1, 1>(a, st); return true;
+    case 6: launch_wgrad_tr<1, 1, 128, 4, 2, 1, 2, 1, 1>(a, st); return true;
     default: return false;
   }
 }
