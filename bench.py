@@ -205,6 +205,20 @@ def bench_schedule(args):
     torch.cuda.synchronize()
     el = time.perf_counter() - t0
     loss = float(net.loss.item())
+    # Reversible backpropagation on the same network and kernels (the baseline
+    # of the paper's iteration-time comparison, Table 5): drain the pipeline,
+    # then time as many sequential steps as ticks were timed.
+    for _ in range(2 * J - 2):
+        net.tick()
+    for t in range(max(2, args.warmup // 4)):
+        net.backprop_step(imgs[t % D], labs[t % D])
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for t in range(args.steps):
+        net.backprop_step(imgs[t % D], labs[t % D])
+    torch.cuda.synchronize()
+    el_bp = time.perf_counter() - t0
+    bp_loss = float(net.loss.item())
     out = {"metric": "images/sec per stage step (fwd+reconstruct+VJP+update)",
            "value": wl.n * args.steps / el, "unit": "images/s", "n_gpus": 1,
            "steps": args.steps, "warmup": warm, "ms_per_step": el / args.steps * 1e3,
@@ -214,7 +228,13 @@ def bench_schedule(args):
                       "widths": list(wl.widths), "blocks_per_stage": wl.blocks_per_stage,
                       "stages": J, "step": "one tick: every stage's forward and backward "
                       "(delays 2(J-j)) and updates"},
-           "last_loss": loss, "outputs_finite": bool(np.isfinite(loss))}
+           "last_loss": loss, "outputs_finite": bool(np.isfinite(loss) and np.isfinite(bp_loss)),
+           "reversible_backprop": {
+               "ms_per_step": el_bp / args.steps * 1e3, "value": wl.n * args.steps / el_bp,
+               "unit": "images/s",
+               "step": "one micro-batch: all stages' forwards, head, all stages' backwards "
+                       "(blocks rebuilt from outputs) and updates, one stream",
+               "iteration_time_ratio": (el_bp / args.steps) / (el / args.steps)}}
     print(json.dumps(out))
 
 

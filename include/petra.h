@@ -271,6 +271,21 @@ petra_status petra_net_tick(petra_net* net, const void* images, const int32_t* l
 /* Ticks run so far, micro-batches fed, and micro-batches still in flight. */
 petra_status petra_net_state(const petra_net* net, int64_t* ticks, int64_t* fed,
                              int64_t* in_flight);
+/* Reversible backpropagation baseline (Sec. 4.2 and Table 5, the comparison
+ * of iteration times): one micro-batch through the same network and kernels
+ * with exact gradients and no overlap.  The forward of every stage in order
+ * (front layers keep their output, reversible blocks keep nothing), the loss
+ * head, then the backward of every stage from the last to the first, the
+ * blocks rebuilding their inputs from their outputs; each stage applies its
+ * update (petra_net_set_optimizer; accum_k counts these steps) right after its
+ * backward, which the stages below do not read.  All work is ordered on
+ * `stream`.  images [n][h][w][c_img] (storage type) and labels [n] int32 are
+ * device pointers (16-byte aligned); loss (nullable, device fp32) receives the
+ * micro-batch's mean loss.  Does not advance the tick counters.
+ * PETRA_ERR_STATE while micro-batches of petra_net_tick are in flight (their
+ * buffers are shared). */
+petra_status petra_net_backprop_step(petra_net* net, const void* images, const int32_t* labels,
+                                     float* loss, void* stream);
 
 /* Measurement support (not part of the method).  petra_stage_profile(st, 1)
  * clears the counters and starts bracketing every kernel launch of the stage

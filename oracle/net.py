@@ -262,3 +262,35 @@ class PetraNet:
                 st.update(lr, mu, wd, nesterov, k)
         self.fwd_msg, self.bwd_msg = new_fwd, new_bwd
         return loss
+
+    def backprop_step(self, images: np.ndarray, labels: np.ndarray, lr: float, mu: float,
+                      wd: float, nesterov=True, k=1):
+        """Reversible backpropagation of one micro-batch, the baseline of the
+        iteration-time comparison (Sec. 4.2, Table 5): the forward of every
+        stage in order, the loss, then the backward of every stage from the last
+        to the first with the parameters the forward used (exact gradients),
+        each stage accumulating and updating after its own backward.  The
+        stages' front layers see their input as in the schedule (the previous
+        stage's output); the blocks rebuild their inputs from their outputs."""
+        ins = []
+        x1, x2 = np.asarray(images, self.dtype), None
+        for st in self.stages:
+            ins.append((x1, x2))
+            x1, x2 = st.forward(x1, x2)
+        last = self.stages[-1]
+        loss, hc = head_loss(np.concatenate([x1, x2], -1), last.params[-2], last.params[-1], labels)
+        dx, dwfc, dbfc = head_vjp(last.params[-2], labels, hc)
+        c = x1.shape[-1]
+        y1, y2, g1, g2 = x1, x2, last.store(dx[..., :c]), last.store(dx[..., c:])
+        for j in reversed(range(self.J)):
+            st = self.stages[j]
+            bx1, bx2 = ins[j]
+            dx, grads = st.backward(y1, y2, g1, g2, bx1, bx2, k)
+            if st.last:
+                grads[-2], grads[-1] = dwfc, dbfc
+            st.accumulate(grads, k)
+            st.update(lr, mu, wd, nesterov, k)
+            if j > 0:
+                c = bx1.shape[-1]
+                y1, y2, g1, g2 = bx1, bx2, dx[..., :c], dx[..., c:]
+        return loss

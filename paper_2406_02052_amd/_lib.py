@@ -95,6 +95,7 @@ _SIGS = {
     "petra_net_state": (ctypes.c_int, [_VP, ctypes.POINTER(ctypes.c_int64),
                                         ctypes.POINTER(ctypes.c_int64),
                                         ctypes.POINTER(ctypes.c_int64)]),
+    "petra_net_backprop_step": (ctypes.c_int, [_VP, _VP, _VP, _VP, _VP]),
     "petra_stage_profile": (ctypes.c_int, [_VP, ctypes.c_int32]),
     "petra_stage_profile_read": (ctypes.c_int, [_VP, ctypes.c_int32,
                                                  ctypes.POINTER(ctypes.c_char_p),
@@ -304,6 +305,11 @@ def petra_net_tick(handle, images, labels, loss=None, stream=None) -> bool:
     _check(load().petra_net_tick(handle, _ptr(images), _ptr(labels), _ptr(loss), _stream(stream),
                                  ctypes.byref(wrote)), "petra_net_tick")
     return bool(wrote.value)
+
+
+def petra_net_backprop_step(handle, images, labels, loss=None, stream=None) -> None:
+    _check(load().petra_net_backprop_step(handle, _ptr(images), _ptr(labels), _ptr(loss),
+                                          _stream(stream)), "petra_net_backprop_step")
 
 
 def petra_net_state(handle):

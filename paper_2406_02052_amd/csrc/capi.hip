@@ -497,18 +497,47 @@ petra_status petra_net_tick(petra_net* net, const void* images, const int32_t* l
   return check_hip("petra_net_tick");
 }
 
+namespace {
+
+int64_t net_in_flight(const petra::Net& s) {
+  // micro-batch m finishes its last backward (stage 0) at tick m + 2J - 2
+  int64_t done = s.t - (2 * static_cast<int64_t>(s.J) - 2);
+  if (done < 0) done = 0;
+  if (done > s.fed) done = s.fed;
+  return s.fed - done;
+}
+
+}  // namespace
+
 petra_status petra_net_state(const petra_net* net, int64_t* ticks, int64_t* fed,
                              int64_t* in_flight) {
   if (net == nullptr || net->impl == nullptr) return fail(PETRA_ERR_INVALID_ARG, "null net handle");
   const petra::Net& s = *net->impl;
   if (ticks) *ticks = s.t;
   if (fed) *fed = s.fed;
-  // micro-batch m finishes its last backward (stage 0) at tick m + 2J - 2
-  int64_t done = s.t - (2 * static_cast<int64_t>(s.J) - 2);
-  if (done < 0) done = 0;
-  if (done > s.fed) done = s.fed;
-  if (in_flight) *in_flight = s.fed - done;
+  if (in_flight) *in_flight = net_in_flight(s);
   return ok();
+}
+
+petra_status petra_net_backprop_step(petra_net* net, const void* images, const int32_t* labels,
+                                     float* loss, void* stream) {
+  if (net == nullptr || net->impl == nullptr) return fail(PETRA_ERR_INVALID_ARG, "null net handle");
+  petra::Net& s = *net->impl;
+  if (!s.bound()) return fail(PETRA_ERR_STATE, "net buffers not bound");
+  if (images == nullptr || labels == nullptr)
+    return fail(PETRA_ERR_INVALID_ARG, "images and labels are required");
+  if (!aligned16(images) || !aligned16(labels) || (loss != nullptr && !aligned16(loss)))
+    return fail(PETRA_ERR_ALIGN, "images, labels and loss must be 16-byte aligned");
+  if (net_in_flight(s) != 0)
+    return fail(PETRA_ERR_STATE, "micro-batches of the tick schedule are still in flight");
+  petra_status r;
+  if ((r = check_hip("before petra_net_backprop_step"))) return r;
+  const hipError_t e = s.ensure_streams();
+  if (e != hipSuccess) return fail(PETRA_ERR_HIP, std::string("stream setup: ") + hipGetErrorString(e));
+  s.backprop_step(images, labels, loss, static_cast<hipStream_t>(stream));
+  for (petra::NetStage& ns : s.st)
+    if ((r = launch_status(*ns.blocks, "petra_net_backprop_step"))) return r;
+  return check_hip("petra_net_backprop_step");
 }
 
 petra_status petra_stage_profile(petra_stage* st, int32_t enable) {

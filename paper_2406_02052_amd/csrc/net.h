@@ -83,13 +83,23 @@ class Net {
   void sync_weights(hipStream_t s);
   // One tick; returns whether a loss was written.
   bool tick(const void* images, const int32_t* labels, float* loss, hipStream_t caller);
+  // One micro-batch through plain reversible backpropagation on stream q: the
+  // forward of every stage in order, the head, then every stage's backward from
+  // the last to the first (each followed by its update when due).  Front
+  // layers keep their forward output instead of recomputing it.  Uses ring
+  // slot 0 and message parity 0: no micro-batch of the tick schedule may be in
+  // flight.
+  void backprop_step(const void* images, const int32_t* labels, float* loss, hipStream_t q);
 
  private:
   template <typename P> P* at(size_t off) const { return reinterpret_cast<P*>(ws + off); }
   void* ring_slot(const NetStage& s, int64_t m, int half) const;
-  void front_forward(NetStage& s, const void* in1, const void* in2, hipStream_t q);
+  void front_forward(NetStage& s, const void* in1, const void* in2, hipStream_t q,
+                     bool keep = false);
   void front_backward(NetStage& s, const void* in1, const void* in2, const void* d1,
-                      const void* d2, int parity, hipStream_t q);
+                      const void* d2, int parity, hipStream_t q, bool recompute = true);
+  void head(NetStage& s, const void* y1, const void* y2, const int32_t* labels, float* loss,
+            hipStream_t q);
   void stage_update(NetStage& s, hipStream_t q);
 };
 

@@ -236,30 +236,34 @@ void* Net::ring_slot(const NetStage& s, int64_t m, int half) const {
 }
 
 // Front conv + BN (+ ReLU on the images) into the two half-tensors the blocks read.
-void Net::front_forward(NetStage& s, const void* in1, const void* in2, hipStream_t q) {
+// keep: the conv output and its BN vectors go to the backward's buffers (and move
+// the running statistics) so that front_backward can skip the recompute.
+void Net::front_forward(NetStage& s, const void* in1, const void* in2, hipStream_t q, bool keep) {
   ConvArgs a{};
   a.src = in1;
   a.src2 = in2;
   a.c_split = in2 ? s.Cin / 2 : s.Cin;
   a.wt = ws + o_front_wfwd + front_segs.seg[s.j].fwd_off * esz;
-  a.out = ws + s.o_fh;
-  a.partials = at<float>(s.o_fpart);
+  a.out = ws + (keep ? s.o_bh : s.o_fh);
+  a.partials = at<float>(keep ? s.o_bpart : s.o_fpart);
   a.n = desc.n; a.h = s.Hin; a.w = s.Win; a.c_in = s.Cin; a.p = s.H; a.q = s.W; a.c_out = s.C;
   a.r = s.R; a.s = s.R; a.stride = s.stride; a.pad = s.pad; a.k_tot = s.R * s.R * s.Cin;
   a.m = static_cast<int>(s.M);
   conv_gemm(dt, a, EP_STATS, q);
-  float* v = at<float>(s.o_fbnp);
-  bn_stats_finalize(at<float>(s.o_fpart), conv_row_tiles(dt, a), s.C, s.M, theta + s.off_front_g,
-                    theta + s.off_front_b, desc.bn_eps, v, v + s.C, v + 2 * s.C, v + 3 * s.C,
-                    nullptr, nullptr, desc.bn_momentum, q);
-  bn_apply_split(dt, ws + s.o_fh, v, v + s.C, s.first ? 1 : 0, ws + s.o_fx1, ws + s.o_fx2, s.M,
-                 s.C, q);
+  float* v = at<float>(keep ? s.o_bbnp : s.o_fbnp);
+  bn_stats_finalize(static_cast<const float*>(a.partials), conv_row_tiles(dt, a), s.C, s.M,
+                    theta + s.off_front_g, theta + s.off_front_b, desc.bn_eps, v, v + s.C,
+                    v + 2 * s.C, v + 3 * s.C, keep ? rmean + s.run_front : nullptr,
+                    keep ? rvar + s.run_front : nullptr, desc.bn_momentum, q);
+  bn_apply_split(dt, a.out, v, v + s.C, s.first ? 1 : 0, ws + s.o_fx1, ws + s.o_fx2, s.M, s.C, q);
 }
 
-// Recompute the front layer from its buffered input and take its VJP given the
-// gradient (d1, d2) of its output; writes the gradient message for stage j - 1.
+// Recompute the front layer from its buffered input (unless recompute is false:
+// then front_forward(keep) left its output and BN vectors in place) and take its
+// VJP given the gradient (d1, d2) of its output; writes the gradient message for
+// stage j - 1.
 void Net::front_backward(NetStage& s, const void* in1, const void* in2, const void* d1,
-                         const void* d2, int parity, hipStream_t q) {
+                         const void* d2, int parity, hipStream_t q, bool recompute) {
   const float inv_k = 1.0f / static_cast<float>(std::max(1, opt.accum_k));
   ConvArgs a{};
   a.src = in1;
@@ -271,7 +275,6 @@ void Net::front_backward(NetStage& s, const void* in1, const void* in2, const vo
   a.n = desc.n; a.h = s.Hin; a.w = s.Win; a.c_in = s.Cin; a.p = s.H; a.q = s.W; a.c_out = s.C;
   a.r = s.R; a.s = s.R; a.stride = s.stride; a.pad = s.pad; a.k_tot = s.R * s.R * s.Cin;
   a.m = static_cast<int>(s.M);
-  conv_gemm(dt, a, EP_STATS, q);
   float* v = at<float>(s.o_bbnp);
   float* scale = v;
   float* shift = v + s.C;
@@ -280,9 +283,12 @@ void Net::front_backward(NetStage& s, const void* in1, const void* in2, const vo
   float* ca = v + 4 * s.C;
   float* cb = v + 5 * s.C;
   float* cc = v + 6 * s.C;
-  bn_stats_finalize(at<float>(s.o_bpart), conv_row_tiles(dt, a), s.C, s.M, theta + s.off_front_g,
-                    theta + s.off_front_b, desc.bn_eps, scale, shift, mean, rstd,
-                    rmean + s.run_front, rvar + s.run_front, desc.bn_momentum, q);
+  if (recompute) {
+    conv_gemm(dt, a, EP_STATS, q);
+    bn_stats_finalize(at<float>(s.o_bpart), conv_row_tiles(dt, a), s.C, s.M,
+                      theta + s.off_front_g, theta + s.off_front_b, desc.bn_eps, scale, shift,
+                      mean, rstd, rmean + s.run_front, rvar + s.run_front, desc.bn_momentum, q);
+  }
   const int relu = s.first ? 1 : 0;
   split_bwd_partials(dt, d1, d2, ws + s.o_bh, scale, shift, mean, rstd, relu,
                      at<float>(s.o_bpart), s.M, s.C, q);
@@ -337,6 +343,57 @@ void Net::stage_update(NetStage& s, hipStream_t q) {
                   ws + o_front_wdg, q);
 }
 
+// Loss head of the last stage on its block output (y1, y2): loss, the gradient
+// halves o_g1/o_g2 and the linear layer's accumulated gradients.
+void Net::head(NetStage& s, const void* y1, const void* y2, const int32_t* labels, float* loss,
+               hipStream_t q) {
+  head_forward_backward(dt, y1, y2, desc.n, s.H * s.W, s.C, theta + s.off_fc_w,
+                        theta + s.off_fc_b, desc.classes, labels, at<float>(s.o_pooled),
+                        at<float>(s.o_dlogits), at<float>(s.o_lossn), ws + s.o_g1, ws + s.o_g2,
+                        q);
+  const float inv_k = 1.0f / static_cast<float>(std::max(1, opt.accum_k));
+  head_param_grads(at<float>(s.o_pooled), at<float>(s.o_dlogits), at<float>(s.o_lossn), desc.n,
+                   s.C, desc.classes, inv_k, grad + s.off_fc_w, grad + s.off_fc_b, loss, q);
+}
+
+void Net::backprop_step(const void* images, const int32_t* labels, float* loss, hipStream_t q) {
+  NetStage& s0 = st[0];
+  pad_channels8(dt, images, desc.c_img, ring_slot(s0, 0, 0), s0.Min, q);
+  copy_i32(labels, at<int32_t>(s0.o_labels), desc.n, q);
+  for (NetStage& s : st) {
+    const void* in1 = ring_slot(s, 0, 0);
+    const void* in2 = s.first ? nullptr : ring_slot(s, 0, 1);
+    front_forward(s, in1, in2, q, /*keep=*/true);
+    void* y1 = s.last ? ws + s.o_y1 : ring_slot(st[s.j + 1], 0, 0);
+    void* y2 = s.last ? ws + s.o_y2 : ring_slot(st[s.j + 1], 0, 1);
+    s.blocks->forward(ws + s.o_fx1, ws + s.o_fx2, y1, y2, q);
+  }
+  NetStage& sl = st[J - 1];
+  head(sl, ws + sl.o_y1, ws + sl.o_y2, at<int32_t>(s0.o_labels), loss, q);
+  for (int j = J - 1; j >= 0; --j) {
+    NetStage& s = st[j];
+    Stage& blk = *s.blocks;
+    const void *by1, *by2, *bg1, *bg2;
+    if (s.last) {
+      by1 = ws + s.o_y1; by2 = ws + s.o_y2; bg1 = ws + s.o_g1; bg2 = ws + s.o_g2;
+    } else {
+      const NetStage& nx = st[j + 1];
+      by1 = ring_slot(nx, 0, 0); by2 = ring_slot(nx, 0, 1);
+      bg1 = ws + nx.o_msg[0][0]; bg2 = ws + nx.o_msg[0][1];
+    }
+    blk.backward(by1, by2, bg1, bg2, ws + s.o_xr1, ws + s.o_xr2, ws + s.o_dx1, ws + s.o_dx2, q);
+    blk.count_backward();
+    const void* in1 = ring_slot(s, 0, 0);
+    const void* in2 = s.first ? nullptr : ring_slot(s, 0, 1);
+    front_backward(s, in1, in2, ws + s.o_dx1, ws + s.o_dx2, 0, q, /*recompute=*/false);
+    if (blk.update_due()) {
+      // stage j's gradient is complete; stages below read only its message
+      stage_update(s, q);
+      blk.mark_updated();
+    }
+  }
+}
+
 bool Net::tick(const void* images, const int32_t* labels, float* loss, hipStream_t caller) {
   const int64_t J2 = 2 * static_cast<int64_t>(J) - 2;
   if (images != nullptr) ++fed;   // micro-batch number t enters at this tick
@@ -382,15 +439,7 @@ bool Net::tick(const void* images, const int32_t* labels, float* loss, hipStream
       else
         blk.forward(fx1, fx2, y1, y2, q);
       if (s.last) {
-        const int32_t* lab = at<int32_t>(st[0].o_labels) + (mf % J) * desc.n;
-        head_forward_backward(dt, y1, y2, desc.n, s.H * s.W, s.C, theta + s.off_fc_w,
-                              theta + s.off_fc_b, desc.classes, lab, at<float>(s.o_pooled),
-                              at<float>(s.o_dlogits), at<float>(s.o_lossn), ws + s.o_g1,
-                              ws + s.o_g2, q);
-        const float inv_k = 1.0f / static_cast<float>(std::max(1, opt.accum_k));
-        head_param_grads(at<float>(s.o_pooled), at<float>(s.o_dlogits), at<float>(s.o_lossn),
-                         desc.n, s.C, desc.classes, inv_k, grad + s.off_fc_w, grad + s.off_fc_b,
-                         loss, q);
+        head(s, y1, y2, at<int32_t>(st[0].o_labels) + (mf % J) * desc.n, loss, q);
         wrote_loss = loss != nullptr;
       }
     }

@@ -184,6 +184,11 @@ class Net:
     def tick(self, images=None, labels=None, stream=None) -> bool:
         return L.petra_net_tick(self.handle, images, labels, self.loss, stream)
 
+    def backprop_step(self, images, labels, stream=None) -> None:
+        """Reversible backpropagation of one micro-batch (no pipelining); the
+        loss lands in self.loss."""
+        L.petra_net_backprop_step(self.handle, images, labels, self.loss, stream)
+
     def state(self):
         return L.petra_net_state(self.handle)
 

@@ -122,3 +122,31 @@ def test_bind_and_call_validation_without_device_work():
         assert n > 0
     finally:
         L.petra_stage_destroy(h)
+
+
+def test_net_backprop_step_validation_without_device_work():
+    from paper_2406_02052_amd import _lib as L
+    from paper_2406_02052_amd.stage import ctypes_int_array
+    wl = synth.REVNET18_SCHEDULE.with_(n=2, h=8, w=8, widths=(16, 32), blocks_per_stage=1)
+    desc = L.NetDesc(wl.n, wl.h, wl.w, wl.c_img, len(wl.widths), ctypes_int_array(wl.widths),
+                     wl.blocks_per_stage, wl.classes, L.PETRA_FP32, wl.bn_eps, wl.bn_momentum)
+    h = L.petra_net_create(desc)
+    try:
+        _, _, _, ws = L.petra_net_query(h)
+        base = 1 << 40   # fake, aligned device addresses; nothing is dereferenced
+        img, lab = base + (2 << 30), base + (3 << 30)
+        with pytest.raises(L.PetraError) as e:
+            L.petra_net_backprop_step(h, img, lab, None, 0)
+        assert e.value.name == "PETRA_ERR_STATE"
+        L.petra_net_bind(h, base, base, base, base, base, base + (1 << 30), ws)
+        with pytest.raises(L.PetraError) as e:
+            L.petra_net_backprop_step(h, None, lab, None, 0)
+        assert e.value.name == "PETRA_ERR_INVALID_ARG"
+        with pytest.raises(L.PetraError) as e:
+            L.petra_net_backprop_step(h, img + 8, lab, None, 0)
+        assert e.value.name == "PETRA_ERR_ALIGN"
+        with pytest.raises(L.PetraError) as e:
+            L.petra_net_backprop_step(h, img, lab, base + (4 << 30) + 4, 0)
+        assert e.value.name == "PETRA_ERR_ALIGN"
+    finally:
+        L.petra_net_destroy(h)

@@ -145,3 +145,66 @@ def test_full_schedule_first_losses_and_finite_run():
     torch.cuda.synchronize()
     assert np.isfinite(net.params.cpu().numpy()).all()
     assert np.isfinite(net.loss.item())
+
+
+def run_backprop(wl, names, params, steps, store=None):
+    import torch
+    from paper_2406_02052_amd import Net
+
+    rng = np.random.default_rng(4)
+    imgs = [synth.to_storage(rng.standard_normal((wl.n, wl.h, wl.w, wl.c_img), dtype=np.float32),
+                             wl.dtype) for _ in range(steps)]
+    labs = [rng.integers(0, wl.classes, wl.n).astype(np.int32) for _ in range(steps)]
+    bf = wl.dtype == "bf16"
+    ref = PetraNet([p.astype(np.float64) for p in params], names, len(wl.widths),
+                   wl.blocks_per_stage, weight_view=synth.round_bf16 if bf else None,
+                   store=store if store is not None else (synth.round_bf16 if bf else None))
+    oloss = [ref.backprop_step(imgs[i], labs[i], wl.lr, wl.momentum, wl.weight_decay,
+                               wl.nesterov, wl.accum_k) for i in range(steps)]
+    net = Net(wl.n, wl.h, wl.w, wl.c_img, wl.widths, wl.blocks_per_stage, wl.classes, wl.dtype)
+    net.set_params(params)
+    net.set_optimizer(wl.lr, wl.momentum, wl.weight_decay, wl.nesterov, wl.accum_k)
+    gloss = []
+    for i in range(steps):
+        net.backprop_step(net.images(imgs[i]), net.labels(labs[i]))
+        torch.cuda.synchronize()
+        gloss.append(float(net.loss.item()))
+    return ref, oloss, net, gloss
+
+
+def test_tiny_net_fp32_backprop_matches_oracle():
+    """The reversible-backpropagation baseline (Table 5 comparison) against the
+    oracle's sequential step: losses and parameters after three SGD steps."""
+    wl = TINY.with_(dtype="fp32")
+    names, params = affine_params(wl)
+    ref, oloss, net, gloss = run_backprop(wl, names, params, 3)
+    print("losses", gloss, oloss, flush=True)
+    worst = compare(wl, names, params, ref, oloss, net, gloss, 1e-4, 1e-4)
+    print("worst parameter increment error", worst, flush=True)
+    orm = np.concatenate([np.concatenate([m.reshape(-1) for m in st.run_mean]) for st in ref.stages])
+    np.testing.assert_allclose(net.run_mean.cpu().numpy(), orm, rtol=1e-4, atol=1e-5)
+    assert net.state() == (0, 0, 0)
+
+
+def test_backprop_after_drained_ticks_and_rejected_in_flight():
+    import torch
+    from paper_2406_02052_amd import Net, PetraError
+
+    wl = TINY.with_(dtype="fp32")
+    names, params = affine_params(wl)
+    net = Net(wl.n, wl.h, wl.w, wl.c_img, wl.widths, wl.blocks_per_stage, wl.classes, wl.dtype)
+    net.set_params(params)
+    rng = np.random.default_rng(9)
+    x = net.images(rng.standard_normal((wl.n, wl.h, wl.w, wl.c_img), dtype=np.float32))
+    y = net.labels(rng.integers(0, wl.classes, wl.n).astype(np.int32))
+    net.tick(x, y)
+    with pytest.raises(PetraError) as e:
+        net.backprop_step(x, y)
+    assert e.value.name == "PETRA_ERR_STATE"
+    J = len(wl.widths)
+    for _ in range(2 * J - 2):
+        net.tick()
+    assert net.state()[2] == 0
+    net.backprop_step(x, y)
+    torch.cuda.synchronize()
+    assert np.isfinite(net.loss.item())

@@ -116,3 +116,48 @@ def test_single_stage_is_plain_sgd():
         opt.step()
     for nm, p, leaf in zip(names, net.stages[0].params, leaves):
         np.testing.assert_allclose(p, leaf.detach().numpy(), rtol=1e-9, atol=1e-12, err_msg=nm)
+
+
+def test_backprop_step_is_sgd_on_end_to_end_gradients():
+    # The sequential baseline of the iteration-time comparison (Table 5): with
+    # J = 4 stages and blocks rebuilt from their outputs it is plain SGD on the
+    # end-to-end gradient, step after step (autograd over the non-reversible
+    # network as the independent reference).
+    names, params, net = build(TINY)
+    imgs, labs = data(TINY, 2)
+    leaves = [torch.tensor(p, requires_grad=True) for p in params]
+    groups = [{"params": [l], "weight_decay": 5e-4 if nm.endswith("weight") else 0.0}
+              for nm, l in zip(names, leaves)]
+    opt = torch.optim.SGD(groups, lr=0.05, momentum=0.9, nesterov=True)
+    for t in range(3):
+        loss = net.backprop_step(imgs[t % 2], labs[t % 2], 0.05, 0.9, 5e-4)
+        opt.zero_grad()
+        lt = Fn.cross_entropy(revnet(imgs[t % 2], leaves, names, 4, 1),
+                              torch.tensor(labs[t % 2]).long())
+        assert abs(loss - lt.item()) < 1e-10
+        lt.backward()
+        opt.step()
+    got = {nm: p for st in net.stages for nm, p in zip(st.names, st.params)}
+    for nm, leaf in zip(names, leaves):
+        np.testing.assert_allclose(got[nm], leaf.detach().numpy(), rtol=1e-9, atol=1e-12,
+                                   err_msg=nm)
+
+
+def test_backprop_step_with_accumulation_updates_every_k():
+    # k = 2: the first step only accumulates; the second applies the mean of
+    # the two end-to-end gradients (Sec. 4.1, gradient accumulation).
+    names, params, net = build(TINY)
+    imgs, labs = data(TINY, 2)
+    net.backprop_step(imgs[0], labs[0], 0.05, 0.0, 0.0, k=2)
+    p1 = {nm: p.copy() for st in net.stages for nm, p in zip(st.names, st.params)}
+    for nm, p in zip(names, params):
+        np.testing.assert_array_equal(p1[nm], p)
+    net.backprop_step(imgs[1], labs[1], 0.05, 0.0, 0.0, k=2)
+    leaves = [torch.tensor(p, requires_grad=True) for p in params]
+    total = sum(Fn.cross_entropy(revnet(imgs[m], leaves, names, 4, 1), torch.tensor(labs[m]).long())
+                for m in range(2)) / 2
+    total.backward()
+    got = {nm: p for st in net.stages for nm, p in zip(st.names, st.params)}
+    for nm, p, leaf in zip(names, params, leaves):
+        want = p - 0.05 * leaf.grad.numpy()
+        np.testing.assert_allclose(got[nm], want, rtol=1e-9, atol=1e-12, err_msg=nm)
