@@ -30,9 +30,24 @@ that arrives from above; stage 0 re-reads its images from the dataset
 (Alg. 1; Sec. 4.2).  A reversible stage sends back its reconstructed input; a
 stage with a buffer sends back the buffered input (Alg. 1, reading of the
 backward send).
+
+Buffer variants (Table 4 and App. B): every stage may also keep, per
+micro-batch in flight, the parameters its forward used (parameter buffer,
+PipeDream-style weight stash) and its blocks' input (input buffer).  The
+backward then uses, with `use_inputs`, the stored block input instead of the
+reconstruction and, with `use_params`, the stashed parameters for the
+Jacobians (blocks and front layer).  With a parameter buffer but no input
+buffer the input is reconstructed with the latest parameters and the VJP taken
+at the reconstruction with the stashed ones (reading of the fourth line of
+Table 4: reconstruction with the latest parameters, the delayed ones for the
+Jacobian; "the input" is the stage's block input).  Both switches on give the
+standard delayed gradient of the method's analysis (App. B); both off is PETRA.
+The last stage runs its forward and backward in the same tick, so all four
+variants coincide there.
 """
 from __future__ import annotations
 
+import copy
 from typing import Callable, Dict, List, Optional, Sequence
 
 import numpy as np
@@ -107,55 +122,95 @@ class NetStage:
         self.run_var = [np.ones(self.params[3 * i + 1].shape, dtype) for i in range(nbn)]
         self.t = 0
         self.buffer: Dict[int, tuple] = {}
+        self.stash: Dict[int, list] = {}     # parameter buffer: micro-batch -> parameters
+        self.inbuf: Dict[int, tuple] = {}    # input buffer: micro-batch -> block input
 
-    def _w(self, i):
-        w = self.params[i]
+    def _w(self, i, P=None):
+        w = (self.params if P is None else P)[i]
         if self.weight_view is not None:
             w = np.asarray(self.weight_view(w.astype(np.float32)), dtype=self.dtype)
         return w
 
-    def _layers(self, b, f):
+    def _layers(self, b, f, P=None):
+        P = self.params if P is None else P
         base = 3 + (2 * b + f) * 6
-        return [(self._w(base + 3 * l), self.params[base + 3 * l + 1], self.params[base + 3 * l + 2])
+        return [(self._w(base + 3 * l, P), P[base + 3 * l + 1], P[base + 3 * l + 2])
                 for l in range(2)]
 
-    def _front(self, x1, x2):
+    def _front(self, x1, x2, P=None):
+        P = self.params if P is None else P
         x = x1 if self.first else np.concatenate([x1, x2], axis=-1)
         stride = 1 if self.first else 2
-        a, graph = nonrev_forward(x, self._w(0), self.params[1], self.params[2], self.eps,
+        a, graph = nonrev_forward(x, self._w(0, P), P[1], P[2], self.eps,
                                   stride, relu=self.first, store=self.store)
         c = a.shape[-1] // 2
         return a[..., :c], a[..., c:], graph
 
-    def forward(self, x1, x2):
+    def forward(self, x1, x2, m=None):
+        if m is not None:
+            self.stash[m] = [p.copy() for p in self.params]
         y1, y2, _ = self._front(x1, x2)
+        if m is not None:
+            self.inbuf[m] = (y1, y2)
         for b in range(self.blocks):
             y1, y2 = revblock.block_forward(y1, y2, self._layers(b, 0), self._layers(b, 1), self.eps,
                                             self.store)
         return y1, y2
 
-    def backward(self, y1, y2, g1, g2, x1, x2, k):
-        """Blocks: reconstruct + VJP from (y, g).  Front: recompute from the
-        buffered input (x1, x2) and VJP.  Returns the input gradient halves."""
+    def _running(self, slot, stats):
+        cache, m = stats
+        self.run_mean[slot], self.run_var[slot] = bn.running_update(
+            self.run_mean[slot], self.run_var[slot], cache, m, self.bn_momentum)
+
+    def backward(self, y1, y2, g1, g2, x1, x2, k, m=None, use_inputs=False, use_params=False):
+        """Blocks: reconstruct + VJP from (y, g) (PETRA), or one of the buffer
+        variants for micro-batch m (see the module notes).  Front: recompute
+        from the buffered input (x1, x2) and VJP.  Returns the input gradient
+        halves and the parameter gradients."""
+        stash = self.stash.pop(m, None) if m is not None else None
+        inbuf = self.inbuf.pop(m, None) if m is not None else None
+        P = stash if use_params else self.params
         grads: List[Optional[np.ndarray]] = [None] * len(self.params)
-        for b in reversed(range(self.blocks)):
-            r = revblock.block_reconstruct_vjp(y1, y2, g1, g2, self._layers(b, 0),
-                                               self._layers(b, 1), self.eps, self.store)
+
+        def take(b, r):
             for f, key in ((0, "dF"), (1, "dG")):
                 base = 3 + (2 * b + f) * 6
                 stats = r["stats_F" if f == 0 else "stats_G"]
                 for l, (dw, dg, db) in enumerate(r[key]):
                     grads[base + 3 * l: base + 3 * l + 3] = [dw, dg, db]
-                    slot = (base + 3 * l) // 3
-                    cache, m = stats[l]
-                    self.run_mean[slot], self.run_var[slot] = bn.running_update(
-                        self.run_mean[slot], self.run_var[slot], cache, m, self.bn_momentum)
-            y1, y2, g1, g2 = r["x1"], r["x2"], r["dx1"], r["dx2"]
+                    self._running((base + 3 * l) // 3, stats[l])
+
+        if not use_inputs and not use_params:
+            for b in reversed(range(self.blocks)):
+                r = revblock.block_reconstruct_vjp(y1, y2, g1, g2, self._layers(b, 0),
+                                                   self._layers(b, 1), self.eps, self.store)
+                take(b, r)
+                y1, y2, g1, g2 = r["x1"], r["x2"], r["dx1"], r["dx2"]
+            self.last_used = dict(u=(y1, y2), P=list(P))
+        else:
+            if use_inputs:
+                u1, u2 = inbuf
+            else:   # reconstruction with the latest parameters
+                u1, u2 = y1, y2
+                for b in reversed(range(self.blocks)):
+                    u1, u2 = revblock.block_inverse(u1, u2, self._layers(b, 0), self._layers(b, 1),
+                                                    self.eps, self.store)
+            self.last_used = dict(u=(u1, u2), P=list(P))
+            acts = []
+            for b in range(self.blocks):
+                acts.append((u1, u2))
+                u1, u2 = revblock.block_forward(u1, u2, self._layers(b, 0, P),
+                                                self._layers(b, 1, P), self.eps, self.store)
+            for b in reversed(range(self.blocks)):
+                r = revblock.block_vjp(acts[b][0], acts[b][1], g1, g2, self._layers(b, 0, P),
+                                       self._layers(b, 1, P), self.eps, self.store)
+                take(b, r)
+                g1, g2 = r["dx1"], r["dx2"]
         # non-reversible front: recompute from the buffered input
-        _, _, graph = self._front(x1, x2)
+        _, _, graph = self._front(x1, x2, P)
         stride = 1 if self.first else 2
-        dx, (dw, dg, db) = nonrev_vjp(np.concatenate([g1, g2], axis=-1), self._w(0),
-                                      self.params[1], graph, stride, relu=self.first,
+        dx, (dw, dg, db) = nonrev_vjp(np.concatenate([g1, g2], axis=-1), self._w(0, P),
+                                      P[1], graph, stride, relu=self.first,
                                       store=self.store)
         grads[0:3] = [dw, dg, db]
         h = graph[1]
@@ -193,8 +248,11 @@ class PetraNet:
     """Tick-level simulation of the PETRA schedule over J stages."""
 
     def __init__(self, params, names, stages: int, blocks_per_stage: int, eps=1e-5,
-                 bn_momentum=0.1, dtype=np.float64, weight_view=None, store=None):
+                 bn_momentum=0.1, dtype=np.float64, weight_view=None, store=None,
+                 use_inputs=False, use_params=False):
         self.J = stages
+        self.use_inputs, self.use_params = use_inputs, use_params
+        self.record: Optional[dict] = None   # (stage, micro-batch) -> parameter gradients
         self.stages = []
         for j, (ps, ns) in enumerate(split_params(names, params, stages)):
             self.stages.append(NetStage(ps, ns, j == 0, j == stages - 1, blocks_per_stage,
@@ -227,7 +285,7 @@ class PetraNet:
                 else:
                     x1, x2 = self.fwd_msg[j - 1]
                     st.buffer[m] = (x1, x2)
-                y1, y2 = st.forward(x1, x2)
+                y1, y2 = st.forward(x1, x2, m)
                 if st.last:
                     last_out = (y1, y2)
                 else:
@@ -247,9 +305,13 @@ class PetraNet:
                     bx1, bx2 = np.asarray(images(mb), self.dtype), None
                 else:
                     bx1, bx2 = st.buffer.pop(mb)
-                dx, grads = st.backward(y1, y2, g1, g2, bx1, bx2, k)
+                dx, grads = st.backward(y1, y2, g1, g2, bx1, bx2, k, mb, self.use_inputs,
+                                        self.use_params)
                 if st.last:
                     grads[-2], grads[-1] = dwfc, dbfc
+                if self.record is not None:
+                    self.record[(j, mb)] = dict(grads=grads, y=(y1, y2), g=(g1, g2),
+                                                x_in=(bx1, bx2), **st.last_used)
                 st.accumulate(grads, k)
                 did_bwd[j] = True
                 if j > 0:
@@ -262,6 +324,33 @@ class PetraNet:
                 st.update(lr, mu, wd, nesterov, k)
         self.fwd_msg, self.bwd_msg = new_fwd, new_bwd
         return loss
+
+    def probe_tick(self, t: int, images, labels, n_micro: int, use_inputs: bool,
+                   use_params: bool) -> Dict[str, np.ndarray]:
+        """The parameter gradients (unscaled, by name) that the backward passes
+        of tick t would produce in the given buffer variant, leaving this
+        schedule untouched (App. B: the gradients compared at a snapshot).
+        Stages without a backward at tick t give zeros."""
+        c = copy.deepcopy(self)
+        c.use_inputs, c.use_params = use_inputs, use_params
+        c.record = {}
+        c.tick(t, images, labels, n_micro, 0.0, 0.0, 0.0, True, 1 << 40)
+        out = {}
+        for j, st in enumerate(c.stages):
+            got = [r["grads"] for (jj, _), r in c.record.items() if jj == j]
+            for i, nm in enumerate(st.names):
+                out[nm] = got[0][i] if got else np.zeros_like(st.params[i])
+        return out
+
+    def probe_backprop(self, images: np.ndarray, labels: np.ndarray) -> Dict[str, np.ndarray]:
+        """End-to-end gradient (by name) of one micro-batch's loss at the
+        current parameters of every stage, leaving this schedule untouched."""
+        c = copy.deepcopy(self)
+        for st in c.stages:
+            st.accum = [np.zeros_like(p) for p in st.params]
+        K = 1 << 40
+        c.backprop_step(images, labels, 0.0, 0.0, 0.0, True, K)
+        return {nm: a * K for st in c.stages for nm, a in zip(st.names, st.accum)}
 
     def backprop_step(self, images: np.ndarray, labels: np.ndarray, lr: float, mu: float,
                       wd: float, nesterov=True, k=1):

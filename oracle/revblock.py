@@ -120,3 +120,18 @@ def block_reconstruct_vjp(y1, y2, g1, g2, f_layers, g_layers, eps, store=_identi
     w, dF = function_vjp(z1, f_layers, f_graph, store)
     return dict(x1=x1, x2=x2, dx1=z1, dx2=store(g2 + w), dF=dF, dG=dG,
                 stats_F=batch_stats(f_graph), stats_G=batch_stats(g_graph))
+
+
+def block_vjp(x1, x2, g1, g2, f_layers, g_layers, eps, store=_identity):
+    """Plain backpropagation through a block whose input (x1, x2) was kept: the
+    forward graph is built from the stored input (no reconstruction) and the
+    VJP runs through it.  Same result layout as block_reconstruct_vjp, with
+    x1, x2 the given inputs (the input-buffer variant of Table 4)."""
+    fout, f_graph = function_forward(x2, f_layers, eps, store)
+    y1 = store(x1 + fout)
+    _, g_graph = function_forward(y1, g_layers, eps, store)
+    u, dG = function_vjp(g2, g_layers, g_graph, store)
+    z1 = store(g1 + u)                # total gradient reaching y1
+    w, dF = function_vjp(z1, f_layers, f_graph, store)
+    return dict(x1=x1, x2=x2, dx1=z1, dx2=store(g2 + w), dF=dF, dG=dG,
+                stats_F=batch_stats(f_graph), stats_G=batch_stats(g_graph))

@@ -87,6 +87,9 @@ class Stage {
   char* ws = nullptr;
   void* wfwd = nullptr;
   void* wdg = nullptr;
+  const float* v_th = nullptr;   // active parameter view (see set_view)
+  const void* v_wf = nullptr;
+  const void* v_wd = nullptr;
   Scratch sf, sb[2];
   float* wpart = nullptr;  // weight-gradient split partials (weight-gradient stream only)
 
@@ -111,6 +114,17 @@ class Stage {
   void sync_weights(hipStream_t st);
   // Kernel sequences (enqueue only; no host-side bookkeeping).
   void forward(const void* x1, const void* x2, void* y1, void* y2, hipStream_t st);
+  // The forward on a given scratch set (the backward's sb[0] for a recompute that
+  // runs on the backward's stream while another forward may be in flight).
+  void forward_with(const void* x1, const void* x2, void* y1, void* y2, Scratch& s,
+                    hipStream_t st);
+  // Reconstruction only (x = inverse of the blocks at y), on scratch sb[0].
+  void reconstruct(const void* y1, const void* y2, void* x1, void* x2, hipStream_t st);
+  // Parameters the forward, backward and reconstruction read: the bound master
+  // (BN) parameters and compute copies unless a view of another version of the
+  // same layout is set (a stashed copy); the update always writes the bound ones.
+  void set_view(const float* th, const void* wf, const void* wd) { v_th = th; v_wf = wf; v_wd = wd; }
+  void reset_view() { v_th = theta; v_wf = wfwd; v_wd = wdg; }
   void backward(const void* y1, const void* y2, const void* dy1, const void* dy2, void* x1,
                 void* x2, void* dx1, void* dx2, hipStream_t st);
   void update_kernels(hipStream_t st);

@@ -168,6 +168,7 @@ void Stage::bind(float* th, float* gr, float* mo, float* rm, float* rv, void* w)
   ws = static_cast<char*>(w);
   wfwd = ws + off_wfwd;
   wdg = ws + off_wdg;
+  reset_view();
   const int nl = blocks.empty() ? 0 : blocks[0].f.nconv;
   for (int pass = 0; pass < 3; ++pass) {
     const ScratchPlan& p = pass == 0 ? plan_f : plan_b[pass - 1];
@@ -262,7 +263,7 @@ void Stage::fn_recompute(const ResidualFn& fn, const void* u, Scratch& s, bool r
       a.pro_scale = s.vec(l - 1, V_SCALE, cmax);
       a.pro_shift = s.vec(l - 1, V_SHIFT, cmax);
     }
-    a.wt = static_cast<char*>(wfwd) + cv.w_off * esz;
+    a.wt = static_cast<const char*>(v_wf) + cv.w_off * esz;
     a.out = s.h[l];
     a.c_out = cv.cout;
     a.k_tot = cv.r * cv.s * cv.cin;
@@ -274,7 +275,7 @@ void Stage::fn_recompute(const ResidualFn& fn, const void* u, Scratch& s, bool r
              static_cast<double>(esz) * (static_cast<double>(M) * (cv.cin + cv.cout) +
                                          static_cast<double>(cv.cout) * a.k_tot));
     prof.begin(st);
-    bn_stats_finalize(s.part, tiles, cv.cout, M, theta + bn.g_off, theta + bn.b_off, desc.bn_eps,
+    bn_stats_finalize(s.part, tiles, cv.cout, M, v_th + bn.g_off, v_th + bn.b_off, desc.bn_eps,
                       s.vec(l, V_SCALE, cmax), s.vec(l, V_SHIFT, cmax), s.vec(l, V_MEAN, cmax),
                       s.vec(l, V_RSTD, cmax), running ? rmean + bn.run_off : nullptr,
                       running ? rvar + bn.run_off : nullptr, desc.bn_momentum, st);
@@ -318,7 +319,7 @@ void Stage::fn_grad(const BwdFn& f, Scratch& s, const BwdFn* next, Scratch* sn, 
     const ConvLayer& cv = convs[fn.conv[L]];
     const BnLayer& bn = bns[cv.bn];
     prof.begin(st);
-    bn_bwd_finalize(s.gpart, s.gtiles, cv.cout, M, theta + bn.g_off, s.vec(L, V_MEAN, cmax),
+    bn_bwd_finalize(s.gpart, s.gtiles, cv.cout, M, v_th + bn.g_off, s.vec(L, V_MEAN, cmax),
                     s.vec(L, V_RSTD, cmax), inv_k, grad + bn.g_off, grad + bn.b_off,
                     s.vec(L, V_CA, cmax), s.vec(L, V_CB, cmax), s.vec(L, V_CC, cmax), st);
     prof.end(K_BN_BWD_FINALIZE, st, 0.0, 8.0 * s.gtiles * cv.cout);
@@ -340,7 +341,7 @@ void Stage::fn_grad(const BwdFn& f, Scratch& s, const BwdFn* next, Scratch* sn, 
     a.pro_cb = s.vec(l, V_CB, cmax);
     a.pro_cc = s.vec(l, V_CC, cmax);
     a.pro_mean = s.vec(l, V_MEAN, cmax);
-    a.wt = static_cast<char*>(wdg) + cv.dg_off * esz;
+    a.wt = static_cast<const char*>(v_wd) + cv.dg_off * esz;
     a.c_out = cv.cin;
     a.k_tot = cv.r * cv.s * cv.cout;
     const double dbytes = static_cast<double>(esz) *
@@ -361,7 +362,7 @@ void Stage::fn_grad(const BwdFn& f, Scratch& s, const BwdFn* next, Scratch* sn, 
       conv(a, EP_MASK, st);
       prof.end(K_CONV_DGRAD, st, 2.0 * M * cv.cin * a.k_tot, dbytes);
       prof.begin(st);
-      bn_bwd_finalize(s.bpart, tiles_conv, lo.cout, M, theta + bl.g_off, s.vec(l - 1, V_MEAN, cmax),
+      bn_bwd_finalize(s.bpart, tiles_conv, lo.cout, M, v_th + bl.g_off, s.vec(l - 1, V_MEAN, cmax),
                       s.vec(l - 1, V_RSTD, cmax), inv_k, grad + bl.g_off, grad + bl.b_off,
                       s.vec(l - 1, V_CA, cmax), s.vec(l - 1, V_CB, cmax),
                       s.vec(l - 1, V_CC, cmax), st);
@@ -429,13 +430,42 @@ void Stage::fn_grad(const BwdFn& f, Scratch& s, const BwdFn* next, Scratch* sn, 
 }
 
 void Stage::forward(const void* x1, const void* x2, void* y1, void* y2, hipStream_t st) {
+  forward_with(x1, x2, y1, y2, sf, st);
+}
+
+void Stage::forward_with(const void* x1, const void* x2, void* y1, void* y2, Scratch& s,
+                         hipStream_t st) {
   const void* a1 = x1;
   const void* a2 = x2;
   for (const Block& b : blocks) {
-    fn_forward(b.f, a2, a1, y1, sf, st);   // y1 = x1 + F(x2)
-    fn_forward(b.g, y1, a2, y2, sf, st);   // y2 = x2 + G(y1)
+    fn_forward(b.f, a2, a1, y1, s, st);   // y1 = x1 + F(x2)
+    fn_forward(b.g, y1, a2, y2, s, st);   // y2 = x2 + G(y1)
     a1 = y1;
     a2 = y2;
+  }
+}
+
+void Stage::reconstruct(const void* y1, const void* y2, void* x1, void* x2, hipStream_t st) {
+  Scratch& s = sb[0];
+  const void* c1 = y1;
+  const void* c2 = y2;
+  for (int b = static_cast<int>(blocks.size()) - 1; b >= 0; --b) {
+    const Block& blk = blocks[b];
+    // x2 = y2 - G(y1), then x1 = y1 - F(x2); in place across blocks
+    for (int f = 0; f < 2; ++f) {
+      const ResidualFn& fn = f == 0 ? blk.g : blk.f;
+      const void* u = f == 0 ? c1 : x2;
+      const void* v = f == 0 ? c2 : c1;
+      void* out = f == 0 ? x2 : x1;
+      fn_recompute(fn, u, s, false, st);
+      const int L = fn.nconv - 1;
+      const int c = convs[fn.conv[L]].cout;
+      prof.begin(st);
+      combine_rec(dt, v, s.h[L], s.vec(L, V_SCALE, cmax), s.vec(L, V_SHIFT, cmax), out, M, c, st);
+      prof.end(K_COMBINE_BWD, st, 0.0, 3.0 * M * c * esz);
+    }
+    c1 = x1;
+    c2 = x2;
   }
 }
 

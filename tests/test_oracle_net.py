@@ -1,4 +1,6 @@
 """Pins of the multi-stage schedule (Alg. 1, Eq. 5, App. B delays)."""
+import copy
+
 import numpy as np
 import pytest
 import torch
@@ -161,3 +163,148 @@ def test_backprop_step_with_accumulation_updates_every_k():
     for nm, p, leaf in zip(names, params, leaves):
         want = p - 0.05 * leaf.grad.numpy()
         np.testing.assert_allclose(got[nm], want, rtol=1e-9, atol=1e-12, err_msg=nm)
+
+
+def _stage_vjp_torch(names, j, blocks, P, x_in, u, g):
+    """VJP of stage j in torch autograd (fp64): front layer at its buffered input
+    x_in, blocks at the block input u, parameters P (by name), cotangent g on
+    the block output; returns the parameter gradients by name."""
+    from tests.torch_ref import front, nchw, stage_blocks
+    leaves = {nm: torch.tensor(P[nm], requires_grad=True) for nm in names}
+    xi = nchw(x_in[0]) if x_in[1] is None else torch.cat([nchw(x_in[0]), nchw(x_in[1])], 1)
+    u1 = nchw(u[0]).clone().requires_grad_(True)
+    u2 = nchw(u[1]).clone().requires_grad_(True)
+    y1, y2 = stage_blocks(u1, u2, leaves, j, blocks)
+    ((y1 * nchw(g[0])).sum() + (y2 * nchw(g[1])).sum()).backward()
+    du = torch.cat([u1.grad, u2.grad], 1)
+    (front(xi, leaves, j) * du).sum().backward()
+    return {nm: leaves[nm].grad.numpy() for nm in names}
+
+
+@pytest.mark.parametrize("use_inputs,use_params", [(False, False), (True, False), (False, True),
+                                                   (True, True)])
+def test_buffer_variants_take_the_vjp_at_their_definition(use_inputs, use_params):
+    # Table 4 variants: every recorded backward is the VJP of its stage at the
+    # block input and parameters its variant prescribes, with the received
+    # cotangent; the block input is the stored one (input buffer) or the
+    # inverse of the received output under the latest parameters; the
+    # parameters are the forward's (parameter buffer) or the latest.
+    names, params, net = build(TINY)
+    net.use_inputs, net.use_params = use_inputs, use_params
+    net.record = {}
+    imgs, labs = data(TINY, 3)
+    J = 4
+    latest, at_fwd = {}, {}
+    for t in range(3 + 2 * J):
+        for j, st in enumerate(net.stages):
+            for m, P in st.stash.items():
+                at_fwd.setdefault((j, m), dict(zip(st.names, P)))
+            latest[(j, t)] = dict(zip(st.names, [p.copy() for p in st.params]))
+        net.tick(t, lambda m: imgs[m], lambda m: labs[m], 3, 0.05, 0.9, 5e-4)
+    from oracle import revblock
+    stale = 0
+    for (j, m), r in net.record.items():
+        if j == J - 1:
+            continue    # forward and backward in one tick: nothing is delayed
+        st = net.stages[j]
+        t_b = m + 2 * J - 2 - j
+        want_P = at_fwd[(j, m)] if use_params else latest[(j, t_b)]
+        for nm, p in zip(st.names, r["P"]):
+            np.testing.assert_array_equal(p, want_P[nm])
+        stale += any(np.abs(latest[(j, t_b)][nm] - at_fwd[(j, m)][nm]).max() > 0
+                     for nm in st.names)
+        u1, u2 = r["u"]
+        if use_inputs:
+            # the forward's block input: front layer at the forward's parameters
+            from tests.torch_ref import front, nchw
+            Pf = {nm: torch.tensor(v) for nm, v in at_fwd[(j, m)].items()}
+            x = r["x_in"]
+            xi = nchw(x[0]) if x[1] is None else torch.cat([nchw(x[0]), nchw(x[1])], 1)
+            a = front(xi, Pf, j).permute(0, 2, 3, 1).numpy()
+            c = a.shape[-1] // 2
+            np.testing.assert_allclose(u1, a[..., :c], rtol=1e-10, atol=1e-12)
+            np.testing.assert_allclose(u2, a[..., c:], rtol=1e-10, atol=1e-12)
+        else:
+            # reconstruction under the latest parameters maps back onto the received output
+            v1, v2 = u1, u2
+            for b in range(TINY.blocks_per_stage):
+                v1, v2 = revblock.block_forward(v1, v2, st._layers(b, 0, r["P"] if not use_params
+                                                                  else [latest[(j, t_b)][nm] for nm in st.names]),
+                                                st._layers(b, 1, r["P"] if not use_params
+                                                           else [latest[(j, t_b)][nm] for nm in st.names]),
+                                                st.eps)
+            np.testing.assert_allclose(v1, r["y"][0], rtol=1e-9, atol=1e-10)
+            np.testing.assert_allclose(v2, r["y"][1], rtol=1e-9, atol=1e-10)
+        tg = _stage_vjp_torch(st.names, j, TINY.blocks_per_stage, dict(zip(st.names, r["P"])),
+                              r["x_in"], r["u"], r["g"])
+        for nm, gv in zip(st.names, r["grads"]):
+            err = np.linalg.norm(gv - tg[nm])
+            assert err <= 1e-9 * np.linalg.norm(tg[nm]) + 1e-12, (j, m, nm, err)
+    assert stale >= 3   # backwards whose stage was updated after their forward
+
+
+def test_both_buffers_give_exact_delayed_gradients():
+    # Input and parameter buffers together (PipeDream weight stashing): the
+    # gradient stage j accumulates for micro-batch m is the end-to-end gradient
+    # of m's loss through the network at the parameters each stage's forward
+    # of m used (App. B, the standard delayed gradient).
+    names, params, net = build(TINY)
+    net.use_inputs = net.use_params = True
+    net.record = {}
+    imgs, labs = data(TINY, 3)
+    J = 4
+    at_fwd = {}
+    for t in range(3 + 2 * J):
+        net.tick(t, lambda m: imgs[m], lambda m: labs[m], 3, 0.05, 0.9, 5e-4)
+        for j, st in enumerate(net.stages):
+            for m, P in st.stash.items():
+                at_fwd.setdefault((j, m), dict(zip(st.names, P)))
+    for m in range(3):
+        # the last stage stashes and consumes within one tick: its forward used the
+        # parameters it had before that tick's update, as the record shows
+        P = {}
+        for j, st in enumerate(net.stages):
+            P.update(at_fwd[(j, m)] if (j, m) in at_fwd else
+                     dict(zip(st.names, net.record[(j, m)]["P"])))
+        leaves = [torch.tensor(P[nm], requires_grad=True) for nm in names]
+        loss = Fn.cross_entropy(revnet(imgs[m], leaves, names, J, 1), torch.tensor(labs[m]).long())
+        loss.backward()
+        for j, st in enumerate(net.stages):
+            for nm, gv in zip(st.names, net.record[(j, m)]["grads"]):
+                ref = leaves[names.index(nm)].grad.numpy()
+                err = np.linalg.norm(gv - ref)
+                assert err <= 1e-9 * np.linalg.norm(ref) + 1e-12, (j, m, nm, err)
+
+
+def test_probes_leave_the_schedule_untouched_and_agree_at_the_last_stage():
+    names, params, net = build(TINY)
+    imgs, labs = data(TINY, 8)
+    J = 4
+    for t in range(2 * J):
+        net.tick(t, lambda m: imgs[m], lambda m: labs[m], 8, 0.05, 0.9, 5e-4)
+    before = copy.deepcopy(net)
+    t = 2 * J
+    probes = {mode: net.probe_tick(t, lambda m: imgs[m], lambda m: labs[m], 8, *mode)
+              for mode in [(False, False), (True, True)]}
+    m_last = t - (J - 1)
+    e2e = net.probe_backprop(imgs[m_last], labs[m_last])
+    for a, b in zip(before.stages, net.stages):
+        for p, q in zip(a.params, b.params):
+            np.testing.assert_array_equal(p, q)
+        assert a.stash.keys() == b.stash.keys() and a.inbuf.keys() == b.inbuf.keys()
+    last = net.stages[-1].names
+    for nm in last:
+        # no delay at the last stage: the PETRA and delayed gradients coincide
+        a, b = probes[(False, False)][nm], probes[(True, True)][nm]
+        assert np.linalg.norm(a - b) <= 1e-9 * np.linalg.norm(b) + 1e-12, nm
+    # the end-to-end probe is autograd's gradient at the current parameters
+    cur = {nm: p for st in net.stages for nm, p in zip(st.names, st.params)}
+    leaves = [torch.tensor(cur[nm], requires_grad=True) for nm in names]
+    Fn.cross_entropy(revnet(imgs[m_last], leaves, names, J, 1),
+                     torch.tensor(labs[m_last]).long()).backward()
+    for nm, leaf in zip(names, leaves):
+        ref = leaf.grad.numpy()
+        assert np.linalg.norm(e2e[nm] - ref) <= 1e-9 * np.linalg.norm(ref) + 1e-12, nm
+    # stage 0 has a delay of 2(J-1) ticks with updates in between: the variants differ
+    s0 = net.stages[0].names
+    assert max(np.abs(probes[(False, False)][nm] - probes[(True, True)][nm]).max() for nm in s0) > 0

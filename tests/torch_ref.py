@@ -37,28 +37,37 @@ def block(x1, x2, fl, gl, eps=1e-5):
     return y1, y2
 
 
+def front(x, P, j):
+    """Non-reversible layer that opens stage j (NCHW): the stem on the images or
+    the stride-2 downsampling."""
+    if j == 0:
+        w = P["s0.stem.weight"].permute(0, 3, 1, 2)
+        h = Fn.conv2d(x, w, padding=1)
+        return torch.relu(Fn.batch_norm(h, None, None, P["s0.stem_bn.gamma"],
+                                        P["s0.stem_bn.beta"], training=True, eps=1e-5))
+    w = P[f"s{j}.trans.weight"].permute(0, 3, 1, 2)
+    h = Fn.conv2d(x, w, stride=2)
+    return Fn.batch_norm(h, None, None, P[f"s{j}.trans_bn.gamma"], P[f"s{j}.trans_bn.beta"],
+                         training=True, eps=1e-5)
+
+
+def stage_blocks(x1, x2, P, j, blocks):
+    for b in range(blocks):
+        def lay(f):
+            return [(P[f"s{j}.b{b}.{f}.conv{l}.weight"].permute(0, 3, 1, 2),
+                     P[f"s{j}.b{b}.{f}.bn{l}.gamma"], P[f"s{j}.b{b}.{f}.bn{l}.beta"]) for l in range(2)]
+        x1, x2 = block(x1, x2, lay("F"), lay("G"))
+    return x1, x2
+
+
 def revnet(img_nhwc, params, names, stages, blocks):
     """Whole network in torch (NCHW inside), params as torch leaves in canonical order."""
     P = dict(zip(names, params))
     x = nchw(img_nhwc) if not isinstance(img_nhwc, torch.Tensor) else img_nhwc
     for j in range(stages):
-        if j == 0:
-            w = P[f"s0.stem.weight"].permute(0, 3, 1, 2)
-            h = Fn.conv2d(x, w, padding=1)
-            x = torch.relu(Fn.batch_norm(h, None, None, P["s0.stem_bn.gamma"], P["s0.stem_bn.beta"],
-                                         training=True, eps=1e-5))
-        else:
-            w = P[f"s{j}.trans.weight"].permute(0, 3, 1, 2)
-            h = Fn.conv2d(x, w, stride=2)
-            x = Fn.batch_norm(h, None, None, P[f"s{j}.trans_bn.gamma"], P[f"s{j}.trans_bn.beta"],
-                              training=True, eps=1e-5)
+        x = front(x, P, j)
         c = x.shape[1] // 2
-        x1, x2 = x[:, :c], x[:, c:]
-        for b in range(blocks):
-            def lay(f):
-                return [(P[f"s{j}.b{b}.{f}.conv{l}.weight"].permute(0, 3, 1, 2),
-                         P[f"s{j}.b{b}.{f}.bn{l}.gamma"], P[f"s{j}.b{b}.{f}.bn{l}.beta"]) for l in range(2)]
-            x1, x2 = block(x1, x2, lay("F"), lay("G"))
+        x1, x2 = stage_blocks(x[:, :c], x[:, c:], P, j, blocks)
         x = torch.cat([x1, x2], dim=1)
     pooled = x.mean(dim=(2, 3))
     J = stages - 1
