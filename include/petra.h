@@ -241,6 +241,12 @@ typedef struct {
   int32_t dtype;                       /* petra_dtype */
   float bn_eps;
   float bn_momentum;
+  /* Buffers kept per micro-batch in flight, for the backward variants of
+   * Table 4 (petra_net_set_backward) and the gradient probes: the blocks'
+   * input (input buffer) and the parameters of the forward (parameter
+   * buffer, a weight stash).  0 = PETRA's setting (neither). */
+  int32_t input_buffer;
+  int32_t param_buffer;
 } petra_net_desc;
 
 typedef struct petra_net petra_net;
@@ -271,6 +277,39 @@ petra_status petra_net_tick(petra_net* net, const void* images, const int32_t* l
 /* Ticks run so far, micro-batches fed, and micro-batches still in flight. */
 petra_status petra_net_state(const petra_net* net, int64_t* ticks, int64_t* fed,
                              int64_t* in_flight);
+/* Backward variants of the ticks (Table 4; App. B): which of the kept buffers
+ * the backward of a non-last stage uses.  RECONSTRUCT is PETRA: the blocks'
+ * input is rebuilt from their output with the current parameters and the VJP
+ * taken there.  INPUT_BUFFER takes the VJP at the stored block input with the
+ * current parameters; PARAM_BUFFER at the input reconstructed with the current
+ * parameters, with the parameters the forward used (blocks and front layer);
+ * DELAYED uses both buffers, the standard delayed gradient.  The last stage
+ * has no delay, so every variant is the PETRA backward there. */
+typedef enum {
+  PETRA_BWD_RECONSTRUCT = 0,
+  PETRA_BWD_INPUT_BUFFER = 1,
+  PETRA_BWD_PARAM_BUFFER = 2,
+  PETRA_BWD_DELAYED = 3
+} petra_bwd_mode;
+/* Sets the variant of the following ticks (default: the buffers kept).
+ * PETRA_ERR_STATE if it needs a buffer the description did not ask for. */
+petra_status petra_net_set_backward(petra_net* net, int32_t mode);
+/* Stage `stage`'s parameters are elements [*offset, *offset + *numel) of the
+ * flat buffers (front layer, blocks, and the head for the last stage). */
+petra_status petra_net_stage_params(const petra_net* net, int32_t stage, int64_t* offset,
+                                    int64_t* numel);
+/* Gradient probes for the gradient-quality diagnostics (App. B); neither
+ * changes parameters, accumulators, running statistics, counters or the
+ * micro-batches in flight.  grad_out: device fp32 [n_params], 16-byte aligned,
+ * zeroed and then filled with unscaled gradients (no 1/accum_k); ordered on
+ * `stream` after prior work.
+ * petra_net_probe_tick: the gradients the backward passes of the next tick
+ * would compute in variant `mode` (stages without a backward then stay zero).
+ * petra_net_probe_backprop: the end-to-end gradient of one micro-batch
+ * (images, labels as for petra_net_tick) at the current parameters. */
+petra_status petra_net_probe_tick(petra_net* net, int32_t mode, float* grad_out, void* stream);
+petra_status petra_net_probe_backprop(petra_net* net, const void* images, const int32_t* labels,
+                                      float* grad_out, void* stream);
 /* Reversible backpropagation baseline (Sec. 4.2 and Table 5, the comparison
  * of iteration times): one micro-batch through the same network and kernels
  * with exact gradients and no overlap.  The forward of every stage in order
@@ -282,8 +321,8 @@ petra_status petra_net_state(const petra_net* net, int64_t* ticks, int64_t* fed,
  * `stream`.  images [n][h][w][c_img] (storage type) and labels [n] int32 are
  * device pointers (16-byte aligned); loss (nullable, device fp32) receives the
  * micro-batch's mean loss.  Does not advance the tick counters.
- * PETRA_ERR_STATE while micro-batches of petra_net_tick are in flight (their
- * buffers are shared). */
+ * PETRA_ERR_STATE while micro-batches of petra_net_tick are in flight (the
+ * step would update parameters they have yet to use in their backward). */
 petra_status petra_net_backprop_step(petra_net* net, const void* images, const int32_t* labels,
                                      float* loss, void* stream);
 

@@ -58,8 +58,12 @@ class NetDesc(ctypes.Structure):
                 ("c_img", ctypes.c_int32), ("num_stages", ctypes.c_int32),
                 ("widths", ctypes.c_int32 * MAX_STAGES), ("blocks_per_stage", ctypes.c_int32),
                 ("classes", ctypes.c_int32), ("dtype", ctypes.c_int32),
-                ("bn_eps", ctypes.c_float), ("bn_momentum", ctypes.c_float)]
+                ("bn_eps", ctypes.c_float), ("bn_momentum", ctypes.c_float),
+                ("input_buffer", ctypes.c_int32), ("param_buffer", ctypes.c_int32)]
 
+
+# petra_bwd_mode
+BWD_RECONSTRUCT, BWD_INPUT_BUFFER, BWD_PARAM_BUFFER, BWD_DELAYED = 0, 1, 2, 3
 
 _VP = ctypes.c_void_p
 _SIGS = {
@@ -96,6 +100,11 @@ _SIGS = {
                                         ctypes.POINTER(ctypes.c_int64),
                                         ctypes.POINTER(ctypes.c_int64)]),
     "petra_net_backprop_step": (ctypes.c_int, [_VP, _VP, _VP, _VP, _VP]),
+    "petra_net_set_backward": (ctypes.c_int, [_VP, ctypes.c_int32]),
+    "petra_net_stage_params": (ctypes.c_int, [_VP, ctypes.c_int32, ctypes.POINTER(ctypes.c_int64),
+                                               ctypes.POINTER(ctypes.c_int64)]),
+    "petra_net_probe_tick": (ctypes.c_int, [_VP, ctypes.c_int32, _VP, _VP]),
+    "petra_net_probe_backprop": (ctypes.c_int, [_VP, _VP, _VP, _VP, _VP]),
     "petra_stage_profile": (ctypes.c_int, [_VP, ctypes.c_int32]),
     "petra_stage_profile_read": (ctypes.c_int, [_VP, ctypes.c_int32,
                                                  ctypes.POINTER(ctypes.c_char_p),
@@ -310,6 +319,27 @@ def petra_net_tick(handle, images, labels, loss=None, stream=None) -> bool:
 def petra_net_backprop_step(handle, images, labels, loss=None, stream=None) -> None:
     _check(load().petra_net_backprop_step(handle, _ptr(images), _ptr(labels), _ptr(loss),
                                           _stream(stream)), "petra_net_backprop_step")
+
+
+def petra_net_set_backward(handle, mode: int) -> None:
+    _check(load().petra_net_set_backward(handle, mode), "petra_net_set_backward")
+
+
+def petra_net_stage_params(handle, stage: int):
+    off, num = ctypes.c_int64(), ctypes.c_int64()
+    _check(load().petra_net_stage_params(handle, stage, ctypes.byref(off), ctypes.byref(num)),
+           "petra_net_stage_params")
+    return off.value, num.value
+
+
+def petra_net_probe_tick(handle, mode: int, grad_out, stream=None) -> None:
+    _check(load().petra_net_probe_tick(handle, mode, _ptr(grad_out), _stream(stream)),
+           "petra_net_probe_tick")
+
+
+def petra_net_probe_backprop(handle, images, labels, grad_out, stream=None) -> None:
+    _check(load().petra_net_probe_backprop(handle, _ptr(images), _ptr(labels), _ptr(grad_out),
+                                           _stream(stream)), "petra_net_probe_backprop")
 
 
 def petra_net_state(handle):

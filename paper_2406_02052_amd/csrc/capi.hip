@@ -393,6 +393,9 @@ petra_status petra_net_create(const petra_net_desc* d, petra_net** out) {
     return fail(PETRA_ERR_INVALID_ARG, "bn_eps must be > 0 and bn_momentum in [0, 1]");
   if (d->blocks_per_stage * 4 > petra::MAX_WEIGHT_SEGS)
     return fail(PETRA_ERR_SHAPE, "too many blocks per stage");
+  if ((d->input_buffer != 0 && d->input_buffer != 1) ||
+      (d->param_buffer != 0 && d->param_buffer != 1))
+    return fail(PETRA_ERR_INVALID_ARG, "input_buffer and param_buffer must be 0 or 1");
   petra_net* h = new (std::nothrow) petra_net;
   if (h == nullptr) return fail(PETRA_ERR_INVALID_ARG, "host allocation failed");
   h->impl = new (std::nothrow) petra::Net(*d);
@@ -517,6 +520,66 @@ petra_status petra_net_state(const petra_net* net, int64_t* ticks, int64_t* fed,
   if (fed) *fed = s.fed;
   if (in_flight) *in_flight = net_in_flight(s);
   return ok();
+}
+
+petra_status petra_net_set_backward(petra_net* net, int32_t mode) {
+  if (net == nullptr || net->impl == nullptr) return fail(PETRA_ERR_INVALID_ARG, "null net handle");
+  if (mode < 0 || mode > 3) return fail(PETRA_ERR_INVALID_ARG, "mode must be a petra_bwd_mode");
+  const petra_net_desc& d = net->impl->desc;
+  if (((mode & PETRA_BWD_INPUT_BUFFER) && !d.input_buffer) ||
+      ((mode & PETRA_BWD_PARAM_BUFFER) && !d.param_buffer))
+    return fail(PETRA_ERR_STATE, "the variant needs a buffer the net does not keep");
+  net->impl->bwd_mode = mode;
+  return ok();
+}
+
+petra_status petra_net_stage_params(const petra_net* net, int32_t stage, int64_t* offset,
+                                    int64_t* numel) {
+  if (net == nullptr || net->impl == nullptr) return fail(PETRA_ERR_INVALID_ARG, "null net handle");
+  const petra::Net& n = *net->impl;
+  if (stage < 0 || stage >= n.J) return fail(PETRA_ERR_INVALID_ARG, "stage out of range");
+  if (offset) *offset = n.st[stage].off_front_w;
+  if (numel) *numel = n.st[stage].n_span;
+  return ok();
+}
+
+petra_status petra_net_probe_tick(petra_net* net, int32_t mode, float* grad_out, void* stream) {
+  if (net == nullptr || net->impl == nullptr) return fail(PETRA_ERR_INVALID_ARG, "null net handle");
+  petra::Net& s = *net->impl;
+  if (!s.bound()) return fail(PETRA_ERR_STATE, "net buffers not bound");
+  if (mode < 0 || mode > 3) return fail(PETRA_ERR_INVALID_ARG, "mode must be a petra_bwd_mode");
+  if (((mode & PETRA_BWD_INPUT_BUFFER) && !s.desc.input_buffer) ||
+      ((mode & PETRA_BWD_PARAM_BUFFER) && !s.desc.param_buffer))
+    return fail(PETRA_ERR_STATE, "the variant needs a buffer the net does not keep");
+  if (grad_out == nullptr) return fail(PETRA_ERR_INVALID_ARG, "grad_out is required");
+  if (!aligned16(grad_out)) return fail(PETRA_ERR_ALIGN, "grad_out must be 16-byte aligned");
+  petra_status r;
+  if ((r = check_hip("before petra_net_probe_tick"))) return r;
+  const hipError_t e = s.ensure_streams();
+  if (e != hipSuccess) return fail(PETRA_ERR_HIP, std::string("stream setup: ") + hipGetErrorString(e));
+  s.probe_tick(mode, grad_out, static_cast<hipStream_t>(stream));
+  for (petra::NetStage& ns : s.st)
+    if ((r = launch_status(*ns.blocks, "petra_net_probe_tick"))) return r;
+  return check_hip("petra_net_probe_tick");
+}
+
+petra_status petra_net_probe_backprop(petra_net* net, const void* images, const int32_t* labels,
+                                      float* grad_out, void* stream) {
+  if (net == nullptr || net->impl == nullptr) return fail(PETRA_ERR_INVALID_ARG, "null net handle");
+  petra::Net& s = *net->impl;
+  if (!s.bound()) return fail(PETRA_ERR_STATE, "net buffers not bound");
+  if (images == nullptr || labels == nullptr || grad_out == nullptr)
+    return fail(PETRA_ERR_INVALID_ARG, "images, labels and grad_out are required");
+  if (!aligned16(images) || !aligned16(labels) || !aligned16(grad_out))
+    return fail(PETRA_ERR_ALIGN, "images, labels and grad_out must be 16-byte aligned");
+  petra_status r;
+  if ((r = check_hip("before petra_net_probe_backprop"))) return r;
+  const hipError_t e = s.ensure_streams();
+  if (e != hipSuccess) return fail(PETRA_ERR_HIP, std::string("stream setup: ") + hipGetErrorString(e));
+  s.probe_backprop(images, labels, grad_out, static_cast<hipStream_t>(stream));
+  for (petra::NetStage& ns : s.st)
+    if ((r = launch_status(*ns.blocks, "petra_net_probe_backprop"))) return r;
+  return check_hip("petra_net_probe_backprop");
 }
 
 petra_status petra_net_backprop_step(petra_net* net, const void* images, const int32_t* labels,

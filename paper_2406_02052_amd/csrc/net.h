@@ -32,6 +32,7 @@ struct NetStage {
   int64_t off_blocks = 0, off_front_g = 0, off_front_b = 0, off_fc_b = 0;
   int64_t off_decay = 0, n_decay = 0, off_plain = 0, n_plain = 0;
   int64_t run_front = 0, run_blocks = 0;
+  int64_t n_span = 0;               // the stage's parameters: [off_front_w, off_front_w + n_span)
   // workspace plan (byte offsets) and bound pointers
   int ring_depth = 0;
   size_t o_blocks_ws = 0, o_ring = 0, o_wfwd = 0, o_wdg = 0;
@@ -42,9 +43,25 @@ struct NetStage {
   size_t o_y1 = 0, o_y2 = 0, o_g1 = 0, o_g2 = 0;                          // last stage
   size_t o_pooled = 0, o_dlogits = 0, o_lossn = 0, o_labels = 0;
   size_t ring_slot_bytes = 0;
+  // buffer variants (Table 4): per micro-batch in flight, the blocks' input
+  // (input buffer) and the parameters of the forward (parameter buffer: fp32
+  // span, then the blocks' and the front's compute copies); rx/ry hold the
+  // reconstructed input and the recomputed output of the variant backward
+  int buf_depth = 0;
+  size_t o_ib = 0, ib_slot_bytes = 0;
+  size_t o_ps = 0, ps_slot_bytes = 0, ps_bwf = 0, ps_bwd = 0, ps_fwf = 0, ps_fwd = 0;
+  size_t o_rx1 = 0, o_rx2 = 0, o_ry1 = 0, o_ry2 = 0;
   int wsplits = 0, wrows = 0;
   hipStream_t sf = nullptr, sb = nullptr;
   hipEvent_t ev_f = nullptr, ev_b = nullptr;
+};
+
+// Parameters a front layer's backward reads: the live ones or a stashed copy.
+struct FrontView {
+  const void* wf;      // forward compute copy [C][R][R][Cin]
+  const void* wd;      // transposed compute copy
+  const float* gamma;
+  const float* beta;
 };
 
 class Net {
@@ -72,6 +89,11 @@ class Net {
   char* ws = nullptr;
   petra_sgd opt{0.1f, 0.9f, 0.0f, 1, 1};
 
+  // Backward variant of the ticks: bit 0 stored block inputs, bit 1 stashed
+  // parameters (each needs its buffer kept, desc.input_buffer/param_buffer).
+  int bwd_mode = 0;
+  size_t o_probe_run = 0;   // running-statistics sink of the probes [2][n_bnch]
+
   int64_t t = 0;       // ticks run
   int64_t fed = 0;     // micro-batches fed
   bool feeding = true;
@@ -90,14 +112,34 @@ class Net {
   // slot 0 and message parity 0: no micro-batch of the tick schedule may be in
   // flight.
   void backprop_step(const void* images, const int32_t* labels, float* loss, hipStream_t q);
+  // Gradient probes (App. B), no state change: the unscaled parameter
+  // gradients that the backward passes of the next tick would produce in
+  // variant `mode`, or the end-to-end gradient of one micro-batch at the
+  // current parameters; both into gout [n_params] (zeroed first).
+  void probe_tick(int mode, float* gout, hipStream_t q);
+  void probe_backprop(const void* images, const int32_t* labels, float* gout, hipStream_t q);
 
  private:
   template <typename P> P* at(size_t off) const { return reinterpret_cast<P*>(ws + off); }
+  // Slot m of the stage's input ring; m < 0: the extra slot of the backprop pass.
   void* ring_slot(const NetStage& s, int64_t m, int half) const;
+  void* ib_slot(const NetStage& s, int64_t m, int half) const;
+  char* ps_slot(const NetStage& s, int64_t m) const;
+  FrontView front_view(const NetStage& s) const;
+  FrontView stash_front_view(const NetStage& s, int64_t m) const;
+  void stash_params(NetStage& s, int64_t m, hipStream_t q);
   void front_forward(NetStage& s, const void* in1, const void* in2, hipStream_t q,
                      bool keep = false);
   void front_backward(NetStage& s, const void* in1, const void* in2, const void* d1,
-                      const void* d2, int parity, hipStream_t q, bool recompute = true);
+                      const void* d2, int parity, hipStream_t q, bool recompute = true,
+                      const FrontView* fv = nullptr);
+  // Blocks + front backward of micro-batch mb given the block output (by) and
+  // its gradient (bg), in variant `mode`; the message goes to parity `parity`.
+  void backward_stage(NetStage& s, int64_t mb, int mode, int parity, hipStream_t q,
+                      const void* by1, const void* by2, const void* bg1, const void* bg2);
+  void backprop_pass(const void* images, const int32_t* labels, float* loss, bool update,
+                     hipStream_t q);
+  struct Redirect;
   void head(NetStage& s, const void* y1, const void* y2, const int32_t* labels, float* loss,
             hipStream_t q);
   void stage_update(NetStage& s, hipStream_t q);

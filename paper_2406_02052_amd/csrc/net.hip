@@ -67,6 +67,7 @@ Net::Net(const petra_net_desc& d) : desc(d) {
     off += s.last ? k : 0;
     s.off_plain = s.off_front_g;
     s.n_plain = off - s.off_front_g;
+    s.n_span = off - s.off_front_w;
     s.run_front = run;
     run += s.C;
     s.run_blocks = run;
@@ -116,6 +117,7 @@ Net::Net(const petra_net_desc& d) : desc(d) {
     dg_off += s.n_front_w;
   }
 
+  bwd_mode = (d.input_buffer ? 1 : 0) | (d.param_buffer ? 2 : 0);
   // workspace plan
   size_t o = 0;
   auto take = [&](size_t bytes) {
@@ -132,7 +134,33 @@ Net::Net(const petra_net_desc& d) : desc(d) {
     s.o_blocks_ws = take(s.blocks->ws_need);
     s.ring_depth = s.first ? 2 * J - 1 : 2 * (J - j) + 1;
     s.ring_slot_bytes = align_up(static_cast<size_t>(s.Min) * s.Cin * esz, 256);
-    s.o_ring = take(s.ring_slot_bytes * s.ring_depth);
+    s.o_ring = take(s.ring_slot_bytes * (s.ring_depth + 1));   // + the backprop pass's slot
+    if (!s.last && (d.input_buffer || d.param_buffer)) {
+      // micro-batch m is kept from its forward (tick m + j) to its backward
+      // (tick m + 2J - 2 - j)
+      s.buf_depth = 2 * (J - 1 - j) + 1;
+      if (d.input_buffer) {
+        s.ib_slot_bytes = align_up(act, 256);
+        s.o_ib = take(s.ib_slot_bytes * s.buf_depth);
+      }
+      if (d.param_buffer) {
+        size_t q = align_up(static_cast<size_t>(s.n_span) * sizeof(float), 256);
+        s.ps_bwf = q;
+        q += align_up(static_cast<size_t>(s.blocks->n_conv) * esz, 256);
+        s.ps_bwd = q;
+        q += align_up(static_cast<size_t>(s.blocks->n_conv) * esz, 256);
+        s.ps_fwf = q;
+        q += align_up(static_cast<size_t>(s.C) * s.R * s.R * s.Cin * esz, 256);
+        s.ps_fwd = q;
+        q += align_up(static_cast<size_t>(s.n_front_w) * esz, 256);
+        s.ps_slot_bytes = q;
+        s.o_ps = take(s.ps_slot_bytes * s.buf_depth);
+      }
+      s.o_rx1 = take(half);
+      s.o_rx2 = take(half);
+      s.o_ry1 = take(half);
+      s.o_ry2 = take(half);
+    }
     // conv args of the front layer, for tile counts and weight-gradient splits
     ConvArgs f{};
     f.n = d.n; f.h = s.Hin; f.w = s.Win; f.c_in = s.Cin; f.p = s.H; f.q = s.W; f.c_out = s.C;
@@ -184,8 +212,9 @@ Net::Net(const petra_net_desc& d) : desc(d) {
       s.o_dlogits = take(static_cast<size_t>(d.n) * k * sizeof(float));
       s.o_lossn = take(static_cast<size_t>(d.n) * sizeof(float));
     }
-    if (s.first) s.o_labels = take(static_cast<size_t>(J) * d.n * sizeof(int32_t));
+    if (s.first) s.o_labels = take(static_cast<size_t>(J + 1) * d.n * sizeof(int32_t));
   }
+  o_probe_run = take(static_cast<size_t>(2 * n_bnch) * sizeof(float));
   ws_need = o;
 }
 
@@ -230,9 +259,49 @@ void Net::sync_weights(hipStream_t q) {
 }
 
 void* Net::ring_slot(const NetStage& s, int64_t m, int half) const {
-  char* slot = ws + s.o_ring + static_cast<size_t>(m % s.ring_depth) * s.ring_slot_bytes;
+  const int64_t idx = m < 0 ? s.ring_depth : m % s.ring_depth;
+  char* slot = ws + s.o_ring + static_cast<size_t>(idx) * s.ring_slot_bytes;
   if (half == 0) return slot;
   return slot + static_cast<size_t>(s.Min) * (s.Cin / 2) * esz;
+}
+
+void* Net::ib_slot(const NetStage& s, int64_t m, int half) const {
+  char* slot = ws + s.o_ib + static_cast<size_t>(m % s.buf_depth) * s.ib_slot_bytes;
+  return slot + (half ? static_cast<size_t>(s.M) * (s.C / 2) * esz : 0);
+}
+
+char* Net::ps_slot(const NetStage& s, int64_t m) const {
+  return ws + s.o_ps + static_cast<size_t>(m % s.buf_depth) * s.ps_slot_bytes;
+}
+
+FrontView Net::front_view(const NetStage& s) const {
+  const WeightSeg& g = front_segs.seg[s.j];
+  return FrontView{ws + o_front_wfwd + g.fwd_off * esz, ws + o_front_wdg + g.dg_off * esz,
+                   theta + s.off_front_g, theta + s.off_front_b};
+}
+
+FrontView Net::stash_front_view(const NetStage& s, int64_t m) const {
+  char* b = ps_slot(s, m);
+  const float* th = reinterpret_cast<const float*>(b);
+  return FrontView{b + s.ps_fwf, b + s.ps_fwd, th + (s.off_front_g - s.off_front_w),
+                   th + (s.off_front_b - s.off_front_w)};
+}
+
+// Parameter buffer: the version the forward of micro-batch m is about to read
+// (fp32 parameters and the compute copies), ahead of it on its stream.
+void Net::stash_params(NetStage& s, int64_t m, hipStream_t q) {
+  char* b = ps_slot(s, m);
+  const FrontView f = front_view(s);
+  const Stage& blk = *s.blocks;
+  const size_t cw = static_cast<size_t>(blk.n_conv) * esz;
+  (void)hipMemcpyAsync(b, theta + s.off_front_w, static_cast<size_t>(s.n_span) * sizeof(float),
+                       hipMemcpyDeviceToDevice, q);
+  (void)hipMemcpyAsync(b + s.ps_bwf, blk.wfwd, cw, hipMemcpyDeviceToDevice, q);
+  (void)hipMemcpyAsync(b + s.ps_bwd, blk.wdg, cw, hipMemcpyDeviceToDevice, q);
+  (void)hipMemcpyAsync(b + s.ps_fwf, f.wf, static_cast<size_t>(s.C) * s.R * s.R * s.Cin * esz,
+                       hipMemcpyDeviceToDevice, q);
+  (void)hipMemcpyAsync(b + s.ps_fwd, f.wd, static_cast<size_t>(s.n_front_w) * esz,
+                       hipMemcpyDeviceToDevice, q);
 }
 
 // Front conv + BN (+ ReLU on the images) into the two half-tensors the blocks read.
@@ -263,13 +332,15 @@ void Net::front_forward(NetStage& s, const void* in1, const void* in2, hipStream
 // VJP given the gradient (d1, d2) of its output; writes the gradient message for
 // stage j - 1.
 void Net::front_backward(NetStage& s, const void* in1, const void* in2, const void* d1,
-                         const void* d2, int parity, hipStream_t q, bool recompute) {
+                         const void* d2, int parity, hipStream_t q, bool recompute,
+                         const FrontView* fvp) {
   const float inv_k = 1.0f / static_cast<float>(std::max(1, opt.accum_k));
+  const FrontView fv = fvp ? *fvp : front_view(s);
   ConvArgs a{};
   a.src = in1;
   a.src2 = in2;
   a.c_split = in2 ? s.Cin / 2 : s.Cin;
-  a.wt = ws + o_front_wfwd + front_segs.seg[s.j].fwd_off * esz;
+  a.wt = fv.wf;
   a.out = ws + s.o_bh;
   a.partials = at<float>(s.o_bpart);
   a.n = desc.n; a.h = s.Hin; a.w = s.Win; a.c_in = s.Cin; a.p = s.H; a.q = s.W; a.c_out = s.C;
@@ -285,15 +356,15 @@ void Net::front_backward(NetStage& s, const void* in1, const void* in2, const vo
   float* cc = v + 6 * s.C;
   if (recompute) {
     conv_gemm(dt, a, EP_STATS, q);
-    bn_stats_finalize(at<float>(s.o_bpart), conv_row_tiles(dt, a), s.C, s.M,
-                      theta + s.off_front_g, theta + s.off_front_b, desc.bn_eps, scale, shift,
-                      mean, rstd, rmean + s.run_front, rvar + s.run_front, desc.bn_momentum, q);
+    bn_stats_finalize(at<float>(s.o_bpart), conv_row_tiles(dt, a), s.C, s.M, fv.gamma,
+                      fv.beta, desc.bn_eps, scale, shift, mean, rstd, rmean + s.run_front,
+                      rvar + s.run_front, desc.bn_momentum, q);
   }
   const int relu = s.first ? 1 : 0;
   split_bwd_partials(dt, d1, d2, ws + s.o_bh, scale, shift, mean, rstd, relu,
                      at<float>(s.o_bpart), s.M, s.C, q);
-  bn_bwd_finalize(at<float>(s.o_bpart), split_tiles(s.M, s.C), s.C, s.M, theta + s.off_front_g,
-                  mean, rstd, inv_k, grad + s.off_front_g, grad + s.off_front_b, ca, cb, cc, q);
+  bn_bwd_finalize(at<float>(s.o_bpart), split_tiles(s.M, s.C), s.C, s.M, fv.gamma, mean, rstd,
+                  inv_k, grad + s.off_front_g, grad + s.off_front_b, ca, cb, cc, q);
   split_bwd_apply(dt, d1, d2, ws + s.o_bh, scale, shift, ca, cb, cc, mean, relu, ws + s.o_dh,
                   s.M, s.C, q);
   // weight gradient
@@ -321,7 +392,7 @@ void Net::front_backward(NetStage& s, const void* in1, const void* in2, const vo
   ConvArgs g{};
   g.src = ws + s.o_dh;
   g.c_split = s.C;
-  g.wt = ws + o_front_wdg + front_segs.seg[s.j].dg_off * esz;
+  g.wt = fv.wd;
   g.out = ws + s.o_dtmp;
   g.n = desc.n; g.h = s.H; g.w = s.W; g.c_in = s.C; g.p = s.H; g.q = s.W; g.c_out = s.Cin;
   g.r = 1; g.s = 1; g.stride = 1; g.pad = 0; g.k_tot = s.C; g.m = static_cast<int>(s.M);
@@ -356,20 +427,107 @@ void Net::head(NetStage& s, const void* y1, const void* y2, const int32_t* label
                    s.C, desc.classes, inv_k, grad + s.off_fc_w, grad + s.off_fc_b, loss, q);
 }
 
-void Net::backprop_step(const void* images, const int32_t* labels, float* loss, hipStream_t q) {
+// Swaps the accumulator, the running statistics and the accumulation count
+// of the net and its stages for the duration of a probe's enqueue: gradients
+// land unscaled in gout, running-statistic moves in the probe sink.
+struct Net::Redirect {
+  Net& n;
+  float* g;
+  float* rm;
+  float* rv;
+  int k;
+  Redirect(Net& net, float* gout) : n(net), g(net.grad), rm(net.rmean), rv(net.rvar),
+                                    k(net.opt.accum_k) {
+    float* sink = net.at<float>(net.o_probe_run);
+    n.grad = gout;
+    n.rmean = sink;
+    n.rvar = sink + n.n_bnch;
+    n.opt.accum_k = 1;
+    for (NetStage& s : n.st) {
+      s.blocks->grad = gout + s.off_blocks;
+      s.blocks->rmean = sink + s.run_blocks;
+      s.blocks->rvar = sink + n.n_bnch + s.run_blocks;
+      s.blocks->opt.accum_k = 1;
+    }
+  }
+  ~Redirect() {
+    n.grad = g;
+    n.rmean = rm;
+    n.rvar = rv;
+    n.opt.accum_k = k;
+    for (NetStage& s : n.st) {
+      s.blocks->grad = g + s.off_blocks;
+      s.blocks->rmean = rm + s.run_blocks;
+      s.blocks->rvar = rv + s.run_blocks;
+      s.blocks->opt.accum_k = k;
+    }
+  }
+};
+
+void Net::backward_stage(NetStage& s, int64_t mb, int mode, int parity, hipStream_t q,
+                         const void* by1, const void* by2, const void* bg1, const void* bg2) {
+  Stage& blk = *s.blocks;
+  void* xr1 = ws + s.o_xr1;
+  void* xr2 = ws + s.o_xr2;
+  void* dx1 = ws + s.o_dx1;
+  void* dx2 = ws + s.o_dx2;
+  FrontView fv = front_view(s);
+  if (mode == 0) {
+    // PETRA: reconstruct the blocks' input from their output with the current
+    // parameters and take the VJP there
+    if (blk.use_graphs)
+      (void)blk.graphs.run({2, reinterpret_cast<uintptr_t>(by1), reinterpret_cast<uintptr_t>(bg1)}, q,
+                           [&](hipStream_t c) { blk.backward(by1, by2, bg1, bg2, xr1, xr2, dx1, dx2, c); },
+                           1);
+    else
+      blk.backward(by1, by2, bg1, bg2, xr1, xr2, dx1, dx2, q);
+  } else {
+    // Variants: the VJP at the stored input (bit 0) or at the input
+    // reconstructed with the current parameters, with the stashed parameters
+    // (bit 1) or the current ones.  The blocks' output at that point is
+    // recomputed, and the reversible backward runs from it.
+    const void* u1 = ib_slot(s, mb, 0);
+    const void* u2 = ib_slot(s, mb, 1);
+    if (!(mode & 1)) {
+      blk.reconstruct(by1, by2, ws + s.o_rx1, ws + s.o_rx2, q);
+      u1 = ws + s.o_rx1;
+      u2 = ws + s.o_rx2;
+    }
+    if (mode & 2) {
+      char* b = ps_slot(s, mb);
+      blk.set_view(reinterpret_cast<const float*>(b) + (s.off_blocks - s.off_front_w),
+                   b + s.ps_bwf, b + s.ps_bwd);
+      fv = stash_front_view(s, mb);
+    }
+    blk.forward_with(u1, u2, ws + s.o_ry1, ws + s.o_ry2, blk.sb[0], q);
+    blk.backward(ws + s.o_ry1, ws + s.o_ry2, bg1, bg2, xr1, xr2, dx1, dx2, q);
+    blk.reset_view();
+  }
+  const void* in1 = ring_slot(s, mb, 0);
+  const void* in2 = s.first ? nullptr : ring_slot(s, mb, 1);
+  front_backward(s, in1, in2, dx1, dx2, parity, q, true, &fv);
+}
+
+// The reversible-backpropagation pass over one micro-batch on stream q, on the
+// extra input-ring slot of every stage, the extra label slot and the message
+// parity the next tick does not read.
+void Net::backprop_pass(const void* images, const int32_t* labels, float* loss, bool update,
+                        hipStream_t q) {
+  const int par = static_cast<int>(t & 1);
   NetStage& s0 = st[0];
-  pad_channels8(dt, images, desc.c_img, ring_slot(s0, 0, 0), s0.Min, q);
-  copy_i32(labels, at<int32_t>(s0.o_labels), desc.n, q);
+  int32_t* lab = at<int32_t>(s0.o_labels) + static_cast<size_t>(J) * desc.n;
+  pad_channels8(dt, images, desc.c_img, ring_slot(s0, -1, 0), s0.Min, q);
+  copy_i32(labels, lab, desc.n, q);
   for (NetStage& s : st) {
-    const void* in1 = ring_slot(s, 0, 0);
-    const void* in2 = s.first ? nullptr : ring_slot(s, 0, 1);
+    const void* in1 = ring_slot(s, -1, 0);
+    const void* in2 = s.first ? nullptr : ring_slot(s, -1, 1);
     front_forward(s, in1, in2, q, /*keep=*/true);
-    void* y1 = s.last ? ws + s.o_y1 : ring_slot(st[s.j + 1], 0, 0);
-    void* y2 = s.last ? ws + s.o_y2 : ring_slot(st[s.j + 1], 0, 1);
+    void* y1 = s.last ? ws + s.o_y1 : ring_slot(st[s.j + 1], -1, 0);
+    void* y2 = s.last ? ws + s.o_y2 : ring_slot(st[s.j + 1], -1, 1);
     s.blocks->forward(ws + s.o_fx1, ws + s.o_fx2, y1, y2, q);
   }
   NetStage& sl = st[J - 1];
-  head(sl, ws + sl.o_y1, ws + sl.o_y2, at<int32_t>(s0.o_labels), loss, q);
+  head(sl, ws + sl.o_y1, ws + sl.o_y2, lab, loss, q);
   for (int j = J - 1; j >= 0; --j) {
     NetStage& s = st[j];
     Stage& blk = *s.blocks;
@@ -378,19 +536,58 @@ void Net::backprop_step(const void* images, const int32_t* labels, float* loss, 
       by1 = ws + s.o_y1; by2 = ws + s.o_y2; bg1 = ws + s.o_g1; bg2 = ws + s.o_g2;
     } else {
       const NetStage& nx = st[j + 1];
-      by1 = ring_slot(nx, 0, 0); by2 = ring_slot(nx, 0, 1);
-      bg1 = ws + nx.o_msg[0][0]; bg2 = ws + nx.o_msg[0][1];
+      by1 = ring_slot(nx, -1, 0); by2 = ring_slot(nx, -1, 1);
+      bg1 = ws + nx.o_msg[par][0]; bg2 = ws + nx.o_msg[par][1];
     }
     blk.backward(by1, by2, bg1, bg2, ws + s.o_xr1, ws + s.o_xr2, ws + s.o_dx1, ws + s.o_dx2, q);
+    const void* in1 = ring_slot(s, -1, 0);
+    const void* in2 = s.first ? nullptr : ring_slot(s, -1, 1);
+    front_backward(s, in1, in2, ws + s.o_dx1, ws + s.o_dx2, par, q, /*recompute=*/false);
+    if (!update) continue;
     blk.count_backward();
-    const void* in1 = ring_slot(s, 0, 0);
-    const void* in2 = s.first ? nullptr : ring_slot(s, 0, 1);
-    front_backward(s, in1, in2, ws + s.o_dx1, ws + s.o_dx2, 0, q, /*recompute=*/false);
     if (blk.update_due()) {
       // stage j's gradient is complete; stages below read only its message
       stage_update(s, q);
       blk.mark_updated();
     }
+  }
+}
+
+void Net::backprop_step(const void* images, const int32_t* labels, float* loss, hipStream_t q) {
+  backprop_pass(images, labels, loss, true, q);
+}
+
+void Net::probe_backprop(const void* images, const int32_t* labels, float* gout, hipStream_t q) {
+  Redirect r(*this, gout);
+  (void)hipMemsetAsync(gout, 0, static_cast<size_t>(n_params) * sizeof(float), q);
+  backprop_pass(images, labels, nullptr, false, q);
+}
+
+void Net::probe_tick(int mode, float* gout, hipStream_t q) {
+  Redirect r(*this, gout);
+  (void)hipMemsetAsync(gout, 0, static_cast<size_t>(n_params) * sizeof(float), q);
+  const int64_t J2 = 2 * static_cast<int64_t>(J) - 2;
+  const int par = static_cast<int>(t & 1);
+  for (NetStage& s : st) {
+    const int64_t mb = t - (J2 - s.j);
+    if (mb < 0 || mb >= fed) continue;
+    const void *by1, *by2, *bg1, *bg2;
+    if (s.last) {
+      // the last stage runs the forward of its micro-batch in the same tick
+      const void* in1 = ring_slot(s, mb, 0);
+      const void* in2 = s.first ? nullptr : ring_slot(s, mb, 1);
+      front_forward(s, in1, in2, q);
+      s.blocks->forward(ws + s.o_fx1, ws + s.o_fx2, ws + s.o_y1, ws + s.o_y2, q);
+      head(s, ws + s.o_y1, ws + s.o_y2, at<int32_t>(st[0].o_labels) + (mb % J) * desc.n, nullptr,
+           q);
+      by1 = ws + s.o_y1; by2 = ws + s.o_y2; bg1 = ws + s.o_g1; bg2 = ws + s.o_g2;
+    } else {
+      const NetStage& nx = st[s.j + 1];
+      const int pm = static_cast<int>((t - 1) & 1);
+      by1 = ring_slot(nx, mb, 0); by2 = ring_slot(nx, mb, 1);
+      bg1 = ws + nx.o_msg[pm][0]; bg2 = ws + nx.o_msg[pm][1];
+    }
+    backward_stage(s, mb, s.last ? 0 : mode, par, q, by1, by2, bg1, bg2);
   }
 }
 
@@ -423,7 +620,13 @@ bool Net::tick(const void* images, const int32_t* labels, float* loss, hipStream
         in1 = ring_slot(s, mf, 0);
         in2 = ring_slot(s, mf, 1);
       }
+      if (s.ps_slot_bytes) stash_params(s, mf, q);
       front_forward(s, in1, in2, q);
+      if (s.ib_slot_bytes) {
+        const size_t hb = static_cast<size_t>(s.M) * (s.C / 2) * esz;
+        (void)hipMemcpyAsync(ib_slot(s, mf, 0), ws + s.o_fx1, hb, hipMemcpyDeviceToDevice, q);
+        (void)hipMemcpyAsync(ib_slot(s, mf, 1), ws + s.o_fx2, hb, hipMemcpyDeviceToDevice, q);
+      }
       if (s.last) {
         y1 = ws + s.o_y1;
         y2 = ws + s.o_y2;
@@ -455,20 +658,9 @@ bool Net::tick(const void* images, const int32_t* labels, float* loss, hipStream
         by1 = ring_slot(nx, mb, 0); by2 = ring_slot(nx, mb, 1);
         bg1 = ws + nx.o_msg[par][0]; bg2 = ws + nx.o_msg[par][1];
       }
-      void* xr1 = ws + s.o_xr1;
-      void* xr2 = ws + s.o_xr2;
-      void* dx1 = ws + s.o_dx1;
-      void* dx2 = ws + s.o_dx2;
-      if (blk.use_graphs)
-        (void)blk.graphs.run({2, reinterpret_cast<uintptr_t>(by1), reinterpret_cast<uintptr_t>(bg1)}, q,
-                             [&](hipStream_t c) { blk.backward(by1, by2, bg1, bg2, xr1, xr2, dx1, dx2, c); },
-                             1);
-      else
-        blk.backward(by1, by2, bg1, bg2, xr1, xr2, dx1, dx2, q);
+      // the last stage has no delay: every variant is the PETRA backward there
+      backward_stage(s, mb, s.last ? 0 : bwd_mode, static_cast<int>(t & 1), q, by1, by2, bg1, bg2);
       blk.count_backward();
-      const void* in1 = ring_slot(s, mb, 0);
-      const void* in2 = s.first ? nullptr : ring_slot(s, mb, 1);
-      front_backward(s, in1, in2, dx1, dx2, static_cast<int>(t & 1), q);
       if (blk.update_due()) {
         // the update follows this stage's forward and backward of the tick (Eq. 5)
         if (q != s.sb) {

@@ -119,16 +119,19 @@ class Net:
 
     def __init__(self, n: int, h: int, w: int, c_img: int, widths, blocks_per_stage: int,
                  classes: int, dtype: str = "bf16", bn_eps: float = 1e-5,
-                 bn_momentum: float = 0.1, device: str = "cuda"):
+                 bn_momentum: float = 0.1, device: str = "cuda", input_buffer: bool = False,
+                 param_buffer: bool = False):
         import torch
         self.torch = torch
         self.device = device
         self.dtype = dtype
         self.tdtype = torch.bfloat16 if dtype == "bf16" else torch.float32
         self.img_shape = (n, h, w, c_img)
+        self.widths = tuple(widths)
         ws = (ctypes_int_array(widths))
         desc = L.NetDesc(n, h, w, c_img, len(widths), ws, blocks_per_stage, classes,
-                         L.PETRA_BF16 if dtype == "bf16" else L.PETRA_FP32, bn_eps, bn_momentum)
+                         L.PETRA_BF16 if dtype == "bf16" else L.PETRA_FP32, bn_eps, bn_momentum,
+                         int(input_buffer), int(param_buffer))
         self.handle = L.petra_net_create(desc)
         self.n_params, self.n_tensors, self.n_bn, self.ws_bytes = L.petra_net_query(self.handle)
         self.infos = [L.petra_net_param_info(self.handle, i) for i in range(self.n_tensors)]
@@ -191,6 +194,25 @@ class Net:
 
     def state(self):
         return L.petra_net_state(self.handle)
+
+    def set_backward(self, mode: int) -> None:
+        L.petra_net_set_backward(self.handle, mode)
+
+    def stage_spans(self):
+        return [L.petra_net_stage_params(self.handle, j) for j in range(len(self.widths))]
+
+    def probe_tick(self, mode: int, stream=None):
+        """Unscaled gradients the next tick's backward passes would produce in
+        variant `mode` (device fp32 [n_params]); nothing else changes."""
+        out = self.torch.empty(self.n_params, dtype=self.torch.float32, device=self.device)
+        L.petra_net_probe_tick(self.handle, mode, out, stream)
+        return out
+
+    def probe_backprop(self, images, labels, stream=None):
+        """End-to-end gradient of one micro-batch at the current parameters."""
+        out = self.torch.empty(self.n_params, dtype=self.torch.float32, device=self.device)
+        L.petra_net_probe_backprop(self.handle, images, labels, out, stream)
+        return out
 
 
 def ctypes_int_array(vals):

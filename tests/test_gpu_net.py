@@ -29,7 +29,7 @@ def affine_params(wl, seed=12):
     return names, params
 
 
-def run_both(wl, names, params, n_micro, ticks, store=None, gpu=True):
+def run_both(wl, names, params, n_micro, ticks, store=None, gpu=True, mode=0):
     import torch
     from paper_2406_02052_amd import Net
 
@@ -40,14 +40,16 @@ def run_both(wl, names, params, n_micro, ticks, store=None, gpu=True):
     bf = wl.dtype == "bf16"
     ref = PetraNet([p.astype(np.float64) for p in params], names, len(wl.widths),
                    wl.blocks_per_stage, weight_view=synth.round_bf16 if bf else None,
-                   store=store if store is not None else (synth.round_bf16 if bf else None))
+                   store=store if store is not None else (synth.round_bf16 if bf else None),
+                   use_inputs=bool(mode & 1), use_params=bool(mode & 2))
     oloss = []
     for t in range(ticks):
         oloss.append(ref.tick(t, lambda m: imgs[m], lambda m: labs[m], n_micro, wl.lr,
                               wl.momentum, wl.weight_decay, wl.nesterov, wl.accum_k))
     if not gpu:
         return ref, oloss, None, None
-    net = Net(wl.n, wl.h, wl.w, wl.c_img, wl.widths, wl.blocks_per_stage, wl.classes, wl.dtype)
+    net = Net(wl.n, wl.h, wl.w, wl.c_img, wl.widths, wl.blocks_per_stage, wl.classes, wl.dtype,
+              input_buffer=bool(mode & 1), param_buffer=bool(mode & 2))
     net.set_params(params)
     net.set_optimizer(wl.lr, wl.momentum, wl.weight_decay, wl.nesterov, wl.accum_k)
     gloss = []
@@ -208,3 +210,90 @@ def test_backprop_after_drained_ticks_and_rejected_in_flight():
     net.backprop_step(x, y)
     torch.cuda.synchronize()
     assert np.isfinite(net.loss.item())
+
+
+@pytest.mark.parametrize("mode", [1, 2, 3])
+def test_tiny_net_fp32_buffer_variants_match_oracle(mode):
+    """Table 4 variants (input buffer, parameter buffer, both) against the
+    oracle's schedule in the same variant: losses, parameters after every
+    update, running statistics."""
+    wl = TINY.with_(dtype="fp32")
+    names, params = affine_params(wl)
+    J = len(wl.widths)
+    n_micro, ticks = 4, 4 + 2 * J
+    ref, oloss, net, gloss = run_both(wl, names, params, n_micro, ticks, mode=mode)
+    print("mode", mode, "losses", gloss, oloss, flush=True)
+    worst = compare(wl, names, params, ref, oloss, net, gloss, 1e-4, 1e-4)
+    print("worst parameter increment error", worst, flush=True)
+    orm = np.concatenate([np.concatenate([m.reshape(-1) for m in st.run_mean]) for st in ref.stages])
+    np.testing.assert_allclose(net.run_mean.cpu().numpy(), orm, rtol=1e-4, atol=1e-5)
+
+
+def _grad_rel(names, got, want):
+    """Per-tensor relative error, floored at 1e-3 of the whole vector's norm."""
+    total = np.sqrt(sum(float(np.sum(want[nm] ** 2)) for nm in names))
+    return max(float(np.linalg.norm(got[nm] - want[nm]) / max(np.linalg.norm(want[nm]), 1e-3 * total))
+               for nm in names)
+
+
+def test_gradient_probes_match_oracle_and_leave_state_untouched():
+    """App. B probes mid-run (fp32): PETRA and delayed tick gradients and the
+    end-to-end gradient against the oracle's probes at the same state; the
+    schedule then continues exactly as if no probe had run."""
+    import torch
+    from paper_2406_02052_amd import Net
+
+    wl = TINY.with_(dtype="fp32")
+    names, params = affine_params(wl)
+    J = len(wl.widths)
+    rng = np.random.default_rng(6)
+    n_micro = 2 * J + 2
+    imgs = [rng.standard_normal((wl.n, wl.h, wl.w, wl.c_img), dtype=np.float32) for _ in range(n_micro)]
+    labs = [rng.integers(0, wl.classes, wl.n).astype(np.int32) for _ in range(n_micro)]
+    ref = PetraNet([p.astype(np.float64) for p in params], names, J, wl.blocks_per_stage)
+    net = Net(wl.n, wl.h, wl.w, wl.c_img, wl.widths, wl.blocks_per_stage, wl.classes, wl.dtype,
+              input_buffer=True, param_buffer=True)
+    net.set_params(params)
+    net.set_optimizer(wl.lr, wl.momentum, wl.weight_decay, wl.nesterov, wl.accum_k)
+    net.set_backward(0)
+    T = 2 * J
+    for t in range(T):
+        ref.tick(t, lambda m: imgs[m], lambda m: labs[m], n_micro, wl.lr, wl.momentum,
+                 wl.weight_decay, wl.nesterov, wl.accum_k)
+        net.tick(net.images(imgs[t]), net.labels(labs[t]))
+    torch.cuda.synchronize()
+    p_before = net.params.cpu().numpy().copy()
+    rm_before = net.run_mean.cpu().numpy().copy()
+    offs = [net.infos[i].offset for i in range(len(names))]
+    def by_name(vec):
+        v = vec.cpu().numpy()
+        return {nm: v[o:o + int(np.prod(p.shape))].reshape(p.shape)
+                for nm, o, p in zip(names, offs, params)}
+    m_last = T - (J - 1)
+    got = {0: by_name(net.probe_tick(0)), 3: by_name(net.probe_tick(3)),
+           "e2e": by_name(net.probe_backprop(net.images(imgs[m_last]), net.labels(labs[m_last])))}
+    torch.cuda.synchronize()
+    want = {0: ref.probe_tick(T, lambda m: imgs[m], lambda m: labs[m], n_micro, False, False),
+            3: ref.probe_tick(T, lambda m: imgs[m], lambda m: labs[m], n_micro, True, True),
+            "e2e": ref.probe_backprop(imgs[m_last], labs[m_last])}
+    for key in got:
+        e = _grad_rel(names, got[key], want[key])
+        print("probe", key, "max relative error", e, flush=True)
+        assert e <= 1e-4, (key, e)
+    np.testing.assert_array_equal(net.params.cpu().numpy(), p_before)
+    np.testing.assert_array_equal(net.run_mean.cpu().numpy(), rm_before)
+    # the schedule continues as the oracle's, which never probed
+    for t in range(T, T + 2):
+        ref.tick(t, lambda m: imgs[m], lambda m: labs[m], n_micro, wl.lr, wl.momentum,
+                 wl.weight_decay, wl.nesterov, wl.accum_k)
+        net.tick(net.images(imgs[t]), net.labels(labs[t]))
+    torch.cuda.synchronize()
+    want_p = {nm: p for st in ref.stages for nm, p in zip(st.names, st.params)}
+    got_p = dict(zip(names, net.get_params()))
+    p0 = dict(zip(names, params))
+    e = _grad_rel(names, {nm: np.asarray(got_p[nm], np.float64) - p0[nm] for nm in names},
+                  {nm: want_p[nm] - p0[nm] for nm in names})
+    assert e <= 1e-4, e
+    assert [net.stage_spans()[j][1] for j in range(J)] == [
+        sum(int(np.prod(p.shape)) for nm, p in zip(names, params) if nm.startswith(f"s{j}."))
+        for j in range(J)]
