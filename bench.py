@@ -41,6 +41,18 @@ def parse():
     p.add_argument("--no-profile", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="target duration of the CPU-oracle sample")
+    p.add_argument("--gradient-quality", action="store_true",
+                   help="train the schedule (PETRA backward, both buffers kept) and report "
+                        "per-stage cosine similarity / norm ratio of the PETRA, delayed and "
+                        "end-to-end gradients at snapshots (App. B)")
+    p.add_argument("--gq-ticks", type=int, default=240)
+    p.add_argument("--gq-every", type=int, default=20)
+    p.add_argument("--memory-report", action="store_true",
+                   help="per-stage device bytes of the schedule with the buffers on/off and "
+                        "the 18-stage RevNet-50 estimate (Tables 3 and 6); host only")
+    p.add_argument("--k-sweep", default=None,
+                   help="comma-separated accumulation factors: schedule throughput and loss "
+                        "per k with lr = 0.1 * batch * k / 256")
     p.add_argument("--copy-calibration", action="store_true",
                    help="only run a plain device copy of 256 MiB ten times (reference kernel "
                         "for scaling the FETCH_SIZE / WRITE_SIZE counters)")
@@ -238,6 +250,140 @@ def bench_schedule(args):
     print(json.dumps(out))
 
 
+def _cos(a, b):
+    na, nb = float(np.linalg.norm(a)), float(np.linalg.norm(b))
+    return float(np.dot(a.astype(np.float64), b.astype(np.float64)) / (na * nb)) if na and nb else 0.0
+
+
+def gradient_quality(args):
+    """App. B analog on synthetic data: the schedule trains with the PETRA
+    backward while keeping both buffers; every gq_every ticks the gradients the
+    next tick would produce as PETRA and as the standard delayed gradient, and
+    the end-to-end gradient of each stage's micro-batch at the current
+    parameters, are probed and compared per stage (cosine similarity, norm
+    ratio).  Host-side numpy on the probed vectors."""
+    import torch
+    from paper_2406_02052_amd import BWD_DELAYED, BWD_RECONSTRUCT, Net
+
+    wl = synth.REVNET18_SCHEDULE
+    net = Net(wl.n, wl.h, wl.w, wl.c_img, wl.widths, wl.blocks_per_stage, wl.classes, wl.dtype,
+              device="cuda:0", input_buffer=True, param_buffer=True)
+    net.set_params(synth.net_params(wl))
+    net.set_optimizer(wl.lr, wl.momentum, wl.weight_decay, wl.nesterov, 1)
+    net.set_backward(BWD_RECONSTRUCT)
+    D = 32
+    imgs = [net.images(x) for x in synth.net_images(wl, D)]
+    labs = [net.labels(l) for l in synth.net_labels(wl, D)]
+    J = len(wl.widths)
+    spans = net.stage_spans()
+    keys = ["cos_petra_delayed", "cos_petra_e2e", "cos_delayed_e2e", "norm_petra_delayed",
+            "norm_petra_e2e", "norm_delayed_e2e"]
+    snaps = []
+    for t in range(args.gq_ticks):
+        if t >= 2 * J and t % args.gq_every == 0:
+            gp = net.probe_tick(BWD_RECONSTRUCT).cpu().numpy()
+            gd = net.probe_tick(BWD_DELAYED).cpu().numpy()
+            rows = []
+            for j, (o, n) in enumerate(spans):
+                mb = t - (2 * J - 2 - j)
+                ge = net.probe_backprop(imgs[mb % D], labs[mb % D]).cpu().numpy()[o:o + n]
+                a, b = gp[o:o + n], gd[o:o + n]
+                na, nb, ne = (float(np.linalg.norm(v)) for v in (a, b, ge))
+                rows.append(dict(zip(keys, [_cos(a, b), _cos(a, ge), _cos(b, ge),
+                                            na / nb if nb else 0.0, na / ne if ne else 0.0,
+                                            nb / ne if ne else 0.0])))
+            torch.cuda.synchronize()
+            snaps.append({"tick": t, "loss": float(net.loss.item()), "stages": rows})
+            print(f"[gq] tick {t} loss {snaps[-1]['loss']:.4f} cos(petra,delayed) "
+                  + " ".join(f"{r['cos_petra_delayed']:.4f}" for r in rows), file=sys.stderr,
+                  flush=True)
+        net.tick(imgs[t % D], labs[t % D])
+    torch.cuda.synchronize()
+    mean = [{k: float(np.mean([s["stages"][j][k] for s in snaps])) for k in keys} for j in range(J)]
+    out = {"metric": "gradient approximation quality per stage (App. B)",
+           "config": {"workload": wl.name, "batch": wl.n, "widths": list(wl.widths),
+                      "blocks_per_stage": wl.blocks_per_stage, "stages": J, "lr": wl.lr,
+                      "accum_k": 1, "ticks": args.gq_ticks, "every": args.gq_every,
+                      "data": "32 synthetic micro-batches (N(0,1) images, uniform labels) in turn",
+                      "dtype": wl.dtype},
+           "delay_per_stage": [2 * (J - 1 - j) for j in range(J)],
+           "mean_over_snapshots": mean, "snapshots": snaps}
+    print(json.dumps(out))
+
+
+def memory_report():
+    """Tables 3 and 6 analogs: the library's plan per stage (bytes by purpose)
+    for the RevNet-18 schedule with the input/parameter buffers on and off, and
+    the host-side estimate for an 18-stage RevNet-50 on ImageNet at batch 64."""
+    from paper_2406_02052_amd import _lib as L
+    from paper_2406_02052_amd import memory as M
+    from paper_2406_02052_amd.stage import ctypes_int_array
+
+    wl = synth.REVNET18_SCHEDULE
+    lib = {}
+    for ib, pb in ((True, True), (True, False), (False, True), (False, False)):
+        desc = L.NetDesc(wl.n, wl.h, wl.w, wl.c_img, len(wl.widths), ctypes_int_array(wl.widths),
+                         wl.blocks_per_stage, wl.classes, L.PETRA_BF16, wl.bn_eps, wl.bn_momentum,
+                         int(ib), int(pb))
+        h = L.petra_net_create(desc)
+        rows = [L.petra_net_memory(h, j) for j in range(len(wl.widths))]
+        L.petra_net_destroy(h)
+        lib[f"input_buffer={int(ib)},param_buffer={int(pb)}"] = {
+            "per_stage": rows, "total": sum(r["total"] for r in rows)}
+    base = lib["input_buffer=1,param_buffer=1"]["total"]
+    for v in lib.values():
+        v["saving_pct"] = 100.0 * (1.0 - v["total"] / base)
+    est = M.revnet50_imagenet_18(64)
+    out = {"metric": "device bytes per stage by purpose (Tables 3 and 6)",
+           "schedule": {"workload": wl.name, "dtype": wl.dtype, "settings": lib},
+           "revnet50_imagenet_18_stages_batch64_estimate": {
+               "act_bytes": 4, "per_stage_petra": M.estimate(est, False, False),
+               "savings": M.savings_table(est)}}
+    print(json.dumps(out))
+
+
+def k_sweep(args):
+    """Accumulation sweep (Sec. 4.1, Fig. 3 mechanism): per k, the schedule's
+    tick time and the loss over a fixed number of micro-batches of synthetic
+    data, with the learning rate scaled linearly with the effective batch and
+    warmed up linearly over the first quarter of the ticks."""
+    import torch
+    from paper_2406_02052_amd import Net
+
+    wl = synth.REVNET18_SCHEDULE
+    D = 8
+    J = len(wl.widths)
+    res = []
+    for k in [int(v) for v in args.k_sweep.split(",")]:
+        net = Net(wl.n, wl.h, wl.w, wl.c_img, wl.widths, wl.blocks_per_stage, wl.classes,
+                  wl.dtype, device="cuda:0")
+        net.set_params(synth.net_params(wl))
+        lr = 0.1 * wl.n * k / 256
+        warm = max(1, args.steps // 4)   # linear warm-up of the scaled rate (large-batch recipe)
+        imgs = [net.images(x) for x in synth.net_images(wl, D)]
+        labs = [net.labels(l) for l in synth.net_labels(wl, D)]
+        losses = []
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for t in range(args.steps):
+            if t <= warm:
+                net.set_optimizer(lr * min(1.0, (t + 1) / warm), wl.momentum, wl.weight_decay,
+                                  wl.nesterov, k)
+            if net.tick(imgs[t % D], labs[t % D]) and (t % 8 == 0 or t == args.steps - 1):
+                losses.append(float(net.loss.item()))
+        torch.cuda.synchronize()
+        el = time.perf_counter() - t0
+        res.append({"k": k, "lr": lr, "warmup_ticks": warm, "ms_per_tick": el / args.steps * 1e3,
+                    "images_per_s": wl.n * args.steps / el, "loss_first": losses[0],
+                    "loss_last": losses[-1], "finite": bool(np.isfinite(losses[-1]))})
+        print(f"[k-sweep] k={k} {res[-1]['ms_per_tick']:.3f} ms/tick loss {losses[0]:.3f} -> "
+              f"{losses[-1]:.3f}", file=sys.stderr, flush=True)
+        del net
+    print(json.dumps({"metric": "accumulation sweep of the schedule", "workload": wl.name,
+                      "ticks": args.steps, "stages": J,
+                      "data": "8 synthetic micro-batches in turn", "results": res}))
+
+
 def main():
     args = parse()
     if args.copy_calibration:
@@ -247,6 +393,15 @@ def main():
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
                           "n_gpus": args.gpus}))
         sys.exit(2)
+    if args.memory_report:
+        memory_report()
+        return
+    if args.gradient_quality:
+        gradient_quality(args)
+        return
+    if args.k_sweep:
+        k_sweep(args)
+        return
     if args.workload == synth.REVNET18_SCHEDULE.name:
         bench_schedule(args)
         return

@@ -298,6 +298,21 @@ petra_status petra_net_set_backward(petra_net* net, int32_t mode);
  * flat buffers (front layer, blocks, and the head for the last stage). */
 petra_status petra_net_stage_params(const petra_net* net, int32_t stage, int64_t* offset,
                                     int64_t* numel);
+/* Device memory of stage `stage` by purpose, in bytes (Tables 3 and 6).  The
+ * first field counts the caller-owned fp32 buffers (parameters, accumulator,
+ * momentum, running statistics); the rest are the stage's parts of the
+ * workspace, which sum with the other stages' to petra_net_query()'s
+ * workspace_bytes. */
+typedef struct {
+  int64_t params;             /* fp32 parameters, accumulator, momentum, running stats */
+  int64_t weight_copies;      /* compute copies of the conv weights (forward, transposed) */
+  int64_t activation_buffer;  /* the front layer's input, one per micro-batch in flight */
+  int64_t input_buffer;       /* the blocks' input per micro-batch in flight (if kept) */
+  int64_t param_buffer;       /* stashed parameters per micro-batch in flight (if kept) */
+  int64_t scratch;            /* one micro-batch's working set, messages, the rest */
+  int64_t total;
+} petra_net_mem;
+petra_status petra_net_memory(const petra_net* net, int32_t stage, petra_net_mem* out);
 /* Gradient probes for the gradient-quality diagnostics (App. B); neither
  * changes parameters, accumulators, running statistics, counters or the
  * micro-batches in flight.  grad_out: device fp32 [n_params], 16-byte aligned,

@@ -62,6 +62,13 @@ class NetDesc(ctypes.Structure):
                 ("input_buffer", ctypes.c_int32), ("param_buffer", ctypes.c_int32)]
 
 
+class NetMem(ctypes.Structure):
+    _fields_ = [("params", ctypes.c_int64), ("weight_copies", ctypes.c_int64),
+                ("activation_buffer", ctypes.c_int64), ("input_buffer", ctypes.c_int64),
+                ("param_buffer", ctypes.c_int64), ("scratch", ctypes.c_int64),
+                ("total", ctypes.c_int64)]
+
+
 # petra_bwd_mode
 BWD_RECONSTRUCT, BWD_INPUT_BUFFER, BWD_PARAM_BUFFER, BWD_DELAYED = 0, 1, 2, 3
 
@@ -103,6 +110,7 @@ _SIGS = {
     "petra_net_set_backward": (ctypes.c_int, [_VP, ctypes.c_int32]),
     "petra_net_stage_params": (ctypes.c_int, [_VP, ctypes.c_int32, ctypes.POINTER(ctypes.c_int64),
                                                ctypes.POINTER(ctypes.c_int64)]),
+    "petra_net_memory": (ctypes.c_int, [_VP, ctypes.c_int32, ctypes.POINTER(NetMem)]),
     "petra_net_probe_tick": (ctypes.c_int, [_VP, ctypes.c_int32, _VP, _VP]),
     "petra_net_probe_backprop": (ctypes.c_int, [_VP, _VP, _VP, _VP, _VP]),
     "petra_stage_profile": (ctypes.c_int, [_VP, ctypes.c_int32]),
@@ -330,6 +338,12 @@ def petra_net_stage_params(handle, stage: int):
     _check(load().petra_net_stage_params(handle, stage, ctypes.byref(off), ctypes.byref(num)),
            "petra_net_stage_params")
     return off.value, num.value
+
+
+def petra_net_memory(handle, stage: int) -> dict:
+    m = NetMem()
+    _check(load().petra_net_memory(handle, stage, ctypes.byref(m)), "petra_net_memory")
+    return {name: getattr(m, name) for name, _ in NetMem._fields_}
 
 
 def petra_net_probe_tick(handle, mode: int, grad_out, stream=None) -> None:

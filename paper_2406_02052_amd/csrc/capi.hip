@@ -543,6 +543,23 @@ petra_status petra_net_stage_params(const petra_net* net, int32_t stage, int64_t
   return ok();
 }
 
+petra_status petra_net_memory(const petra_net* net, int32_t stage, petra_net_mem* out) {
+  if (net == nullptr || net->impl == nullptr || out == nullptr)
+    return fail(PETRA_ERR_INVALID_ARG, "null argument");
+  const petra::Net& n = *net->impl;
+  if (stage < 0 || stage >= n.J) return fail(PETRA_ERR_INVALID_ARG, "stage out of range");
+  const int64_t* m = n.st[stage].mem;
+  out->params = m[petra::MEM_PARAMS];
+  out->weight_copies = m[petra::MEM_WEIGHT_COPIES];
+  out->activation_buffer = m[petra::MEM_ACTIVATION_BUFFER];
+  out->input_buffer = m[petra::MEM_INPUT_BUFFER];
+  out->param_buffer = m[petra::MEM_PARAM_BUFFER];
+  out->scratch = m[petra::MEM_SCRATCH];
+  out->total = 0;
+  for (int c = 0; c < petra::MEM_COUNT; ++c) out->total += m[c];
+  return ok();
+}
+
 petra_status petra_net_probe_tick(petra_net* net, int32_t mode, float* grad_out, void* stream) {
   if (net == nullptr || net->impl == nullptr) return fail(PETRA_ERR_INVALID_ARG, "null net handle");
   petra::Net& s = *net->impl;

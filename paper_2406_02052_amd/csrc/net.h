@@ -18,6 +18,10 @@
 
 namespace petra {
 
+// Device bytes of a stage by purpose (memory accounting of Tables 3 and 6).
+enum { MEM_PARAMS = 0, MEM_WEIGHT_COPIES, MEM_ACTIVATION_BUFFER, MEM_INPUT_BUFFER,
+       MEM_PARAM_BUFFER, MEM_SCRATCH, MEM_COUNT };
+
 struct NetStage {
   int j = 0;
   bool first = false, last = false;
@@ -54,6 +58,7 @@ struct NetStage {
   int wsplits = 0, wrows = 0;
   hipStream_t sf = nullptr, sb = nullptr;
   hipEvent_t ev_f = nullptr, ev_b = nullptr;
+  int64_t mem[MEM_COUNT] = {0, 0, 0, 0, 0, 0};
 };
 
 // Parameters a front layer's backward reads: the live ones or a stashed copy.

@@ -119,10 +119,13 @@ Net::Net(const petra_net_desc& d) : desc(d) {
 
   bwd_mode = (d.input_buffer ? 1 : 0) | (d.param_buffer ? 2 : 0);
   // workspace plan
+  // (each allocation is also counted, by purpose, in the stage's mem[])
   size_t o = 0;
+  int64_t* cur = nullptr;
   auto take = [&](size_t bytes) {
     const size_t r = o;
     o = align_up(o + bytes, 256);
+    if (cur) *cur += static_cast<int64_t>(o - r);
     return r;
   };
   o_front_wfwd = take(static_cast<size_t>(fw_off) * esz);
@@ -131,17 +134,28 @@ Net::Net(const petra_net_desc& d) : desc(d) {
     NetStage& s = st[j];
     const size_t act = static_cast<size_t>(s.M) * s.C * esz;   // full-width block activation
     const size_t half = act / 2;
+    s.mem[MEM_WEIGHT_COPIES] += static_cast<int64_t>(
+        (static_cast<size_t>(s.C) * s.R * s.R * s.Cin + s.n_front_w) * esz +
+        2 * align_up(static_cast<size_t>(s.blocks->n_conv) * esz, 256));
+    s.mem[MEM_SCRATCH] -= static_cast<int64_t>(2 * align_up(static_cast<size_t>(s.blocks->n_conv) * esz, 256));
+    cur = &s.mem[MEM_SCRATCH];
     s.o_blocks_ws = take(s.blocks->ws_need);
     s.ring_depth = s.first ? 2 * J - 1 : 2 * (J - j) + 1;
     s.ring_slot_bytes = align_up(static_cast<size_t>(s.Min) * s.Cin * esz, 256);
+    cur = &s.mem[MEM_ACTIVATION_BUFFER];
     s.o_ring = take(s.ring_slot_bytes * (s.ring_depth + 1));   // + the backprop pass's slot
+    s.mem[MEM_ACTIVATION_BUFFER] -= static_cast<int64_t>(s.ring_slot_bytes);
+    s.mem[MEM_SCRATCH] += static_cast<int64_t>(s.ring_slot_bytes);
+    cur = &s.mem[MEM_SCRATCH];
     if (!s.last && (d.input_buffer || d.param_buffer)) {
       // micro-batch m is kept from its forward (tick m + j) to its backward
       // (tick m + 2J - 2 - j)
       s.buf_depth = 2 * (J - 1 - j) + 1;
       if (d.input_buffer) {
         s.ib_slot_bytes = align_up(act, 256);
+        cur = &s.mem[MEM_INPUT_BUFFER];
         s.o_ib = take(s.ib_slot_bytes * s.buf_depth);
+        cur = &s.mem[MEM_SCRATCH];
       }
       if (d.param_buffer) {
         size_t q = align_up(static_cast<size_t>(s.n_span) * sizeof(float), 256);
@@ -154,7 +168,9 @@ Net::Net(const petra_net_desc& d) : desc(d) {
         s.ps_fwd = q;
         q += align_up(static_cast<size_t>(s.n_front_w) * esz, 256);
         s.ps_slot_bytes = q;
+        cur = &s.mem[MEM_PARAM_BUFFER];
         s.o_ps = take(s.ps_slot_bytes * s.buf_depth);
+        cur = &s.mem[MEM_SCRATCH];
       }
       s.o_rx1 = take(half);
       s.o_rx2 = take(half);
@@ -213,9 +229,20 @@ Net::Net(const petra_net_desc& d) : desc(d) {
       s.o_lossn = take(static_cast<size_t>(d.n) * sizeof(float));
     }
     if (s.first) s.o_labels = take(static_cast<size_t>(J + 1) * d.n * sizeof(int32_t));
+    cur = nullptr;
   }
+  cur = &st[0].mem[MEM_SCRATCH];
   o_probe_run = take(static_cast<size_t>(2 * n_bnch) * sizeof(float));
   ws_need = o;
+  // caller-owned fp32 parameters, accumulator, momentum and running statistics;
+  // the front copies' alignment slack goes to stage 0
+  int64_t counted = 0;
+  for (NetStage& s : st) {
+    s.mem[MEM_PARAMS] = 3 * s.n_span * static_cast<int64_t>(sizeof(float)) +
+                        2 * (s.C + s.blocks->n_bnch) * static_cast<int64_t>(sizeof(float));
+    for (int c = MEM_WEIGHT_COPIES; c < MEM_COUNT; ++c) counted += s.mem[c];
+  }
+  st[0].mem[MEM_SCRATCH] += static_cast<int64_t>(ws_need) - counted;
 }
 
 Net::~Net() {

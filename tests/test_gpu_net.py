@@ -297,3 +297,15 @@ def test_gradient_probes_match_oracle_and_leave_state_untouched():
     assert [net.stage_spans()[j][1] for j in range(J)] == [
         sum(int(np.prod(p.shape)) for nm, p in zip(names, params) if nm.startswith(f"s{j}."))
         for j in range(J)]
+
+
+def test_tiny_net_fp32_accumulation_matches_oracle():
+    """Gradient accumulation k = 2 in the schedule (Sec. 4.1): each stage
+    updates after every second backward with the mean gradient."""
+    wl = TINY.with_(dtype="fp32", accum_k=2)
+    names, params = affine_params(wl)
+    J = len(wl.widths)
+    n_micro, ticks = 5, 5 + 2 * J
+    ref, oloss, net, gloss = run_both(wl, names, params, n_micro, ticks)
+    worst = compare(wl, names, params, ref, oloss, net, gloss, 1e-4, 1e-4)
+    print("worst parameter increment error", worst, flush=True)
