@@ -2312,8 +2312,10 @@ __global__ __launch_bounds__(256) void wgrad_halo_kernel(WgradArgs a) {
 // TH x TW pixel tiles; the next tile is in flight while the current one is
 // multiplied (double-buffered LDS, one barrier per tile).  Waves split the
 // output: WO x WC channel blocks of OF x CF fragments, and WT groups of taps.
-template <int R, int TH, int TW, int WO, int OF, int WC, int CF, int WT, int WP, bool PRO, bool DH>
-__global__ __launch_bounds__(64 * WO * WC * WT * WP) void wgrad_tr_kernel(WgradArgs a) {
+template <int R, int TH, int TW, int WO, int OF, int WC, int CF, int WT, int WP, bool DH>
+__device__ __forceinline__ void wgrad_tr_body(const WgradArgs& a, int bx, int by, int bz,
+                                              int splits, int nbz) {
+  const bool PRO = a.pro_scale != nullptr;   // BN-apply + ReLU prologue of the conv input
   using T = bf16_t;
   typedef short v4i16 __attribute__((ext_vector_type(4)));
   typedef short v8i16 __attribute__((ext_vector_type(8)));
@@ -2340,12 +2342,11 @@ __global__ __launch_bounds__(64 * WO * WC * WT * WP) void wgrad_tr_kernel(WgradA
   const int wo = wave % WO, wc = (wave / WO) % WC, wt = (wave / (WO * WC)) % WT;
   const int wp = wave / NW;   // pixel group: k-steps wp, wp + WP, ... of each tile
   const int li = lane & 15, kg = lane >> 4;
-  const int o0 = blockIdx.y * BO, c0 = blockIdx.z * BC;
+  const int o0 = by * BO, c0 = bz * BC;
   // 1x1: no halo; tiles are runs of NPIX consecutive pixels of the flat [m] index
   constexpr bool FLAT = R == 1;
   const int tiles_x = (a.w + TW - 1) / TW, tiles_y = (a.h + TH - 1) / TH;
   const int ntiles = FLAT ? (a.m + NPIX - 1) / NPIX : tiles_x * tiles_y * a.n;
-  const int splits = gridDim.x;
 
   const long in_bytes = static_cast<long>(a.n) * a.h * a.w * a.c_in * 2;
   const long out_bytes = static_cast<long>(a.m) * a.c_out * 2;
@@ -2417,7 +2418,7 @@ __global__ __launch_bounds__(64 * WO * WC * WT * WP) void wgrad_tr_kernel(WgradA
       const int hp = (tid + NT * i) / XG;
       if (hp >= HPIX) continue;
       Raw8<T> r = rx[i];
-      if constexpr (PRO) {
+      if (PRO) {
         float v[8];
         r.to_f32(v);
 #pragma unroll
@@ -2468,7 +2469,7 @@ __global__ __launch_bounds__(64 * WO * WC * WT * WP) void wgrad_tr_kernel(WgradA
 
   // Loads are unconditional (re-reading the last tile past the end) so the
   // number of loads in flight does not depend on the path.
-  int t = blockIdx.x;
+  int t = bx;
   load_tile(min(t, ntiles - 1));
   int buf = 0;
   for (; t < ntiles; t += splits) {
@@ -2531,8 +2532,8 @@ __global__ __launch_bounds__(64 * WO * WC * WT * WP) void wgrad_tr_kernel(WgradA
   // Partials in fragment order: every (wave, fragment) owns 256 consecutive
   // floats, lane l at 4 l .. 4 l + 3, so each wave writes whole cache lines;
   // wgrad_tr_reduce maps them back to [o][k].
-  const long wg_base = (static_cast<long>(blockIdx.y) * gridDim.z + blockIdx.z) * NW + wave;
-  float* outp = a.partials + static_cast<long>(blockIdx.x) * a.c_out * a.k_tot;
+  const long wg_base = (static_cast<long>(by) * nbz + bz) * NW + wave;
+  float* outp = a.partials + static_cast<long>(bx) * a.c_out * a.k_tot;
 #pragma unroll
   for (int of = 0; of < OF; ++of)
 #pragma unroll
@@ -2544,21 +2545,43 @@ __global__ __launch_bounds__(64 * WO * WC * WT * WP) void wgrad_tr_kernel(WgradA
       }
 }
 
+template <int R, int TH, int TW, int WO, int OF, int WC, int CF, int WT, int WP, bool DH>
+__global__ __launch_bounds__(64 * WO * WC * WT * WP) void wgrad_tr_kernel(WgradArgs a) {
+  wgrad_tr_body<R, TH, TW, WO, OF, WC, CF, WT, WP, DH>(a, blockIdx.x, blockIdx.y, blockIdx.z,
+                                                       gridDim.x, gridDim.z);
+}
+
+// Several layers' weight gradients (same configuration) in one launch: block b
+// belongs to the last entry whose first block is <= b; within an entry blocks
+// run over (split, output block, input block) as the single-layer grid does.
+template <int R, int TH, int TW, int WO, int OF, int WC, int CF, int WT, int WP, bool DH>
+__global__ __launch_bounds__(64 * WO * WC * WT * WP) void wgrad_tr_group_kernel(WgGroupTable tab) {
+  constexpr int BO = WO * OF * 16, BC = WC * CF * 16;
+  const long b = blockIdx.x;
+  int i = 0;
+  for (int e = 1; e < tab.n; ++e)
+    if (tab.block_begin[e] <= b) i = e;
+  const WgradArgs& a = tab.a[i];
+  const long local = b - tab.block_begin[i];
+  const int nby = a.c_out / BO, nbz = a.c_in / BC;
+  const int bx = static_cast<int>(local % a.splits);
+  const long r = local / a.splits;
+  wgrad_tr_body<R, TH, TW, WO, OF, WC, CF, WT, WP, DH>(a, bx, static_cast<int>(r % nby),
+                                                       static_cast<int>(r / nby), a.splits, nbz);
+}
+
 // Fixed-order sum over the splits of the fragment-ordered partials of
 // wgrad_tr_kernel, scaled by inv_k and added to grad[o][k].  One thread per
 // lane-quad (4 consecutive partial floats = 4 output channels of one k).
-struct TrMap {
-  int wo, of, wc, cf, wt, tpw, bo, bc, nz, c_in, k_tot;
-};
-
-__global__ __launch_bounds__(256) void wgrad_tr_reduce_kernel(const float* __restrict__ part,
-                                                              int splits, long numel, TrMap mp,
-                                                              float inv_k, float* __restrict__ grad) {
-  // 16 quads per block; the 16 thread rows take splits r, r + 16, ... and the
-  // row sums are combined in a fixed order.
+// Reduce of fragment-ordered partials: 16 quads per block; the 16 thread rows
+// take splits r, r + 16, ... and the row sums are combined in a fixed order.
+// blk is the block's index within its layer's partials.
+__device__ __forceinline__ void tr_reduce_block(const float* __restrict__ part, int splits,
+                                                long numel, const TrMap& mp, float inv_k,
+                                                float* __restrict__ grad, long blk_index) {
   __shared__ f32x4_t red[16][17];
   const int tq = threadIdx.x & 15, tr = threadIdx.x >> 4;
-  const long q = static_cast<long>(blockIdx.x) * 16 + tq;   // quad index
+  const long q = blk_index * 16 + tq;   // quad index
   const bool live = q * 4 < numel;
   f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
   if (live) {
@@ -2595,6 +2618,27 @@ __global__ __launch_bounds__(256) void wgrad_tr_reduce_kernel(const float* __res
     const int o = by * mp.bo + (wo * mp.of + of) * 16 + kg * 4 + e;
     grad[static_cast<long>(o) * mp.k_tot + k] += inv_k * acc[e];
   }
+}
+
+__global__ __launch_bounds__(256) void wgrad_tr_reduce_kernel(const float* __restrict__ part,
+                                                              int splits, long numel, TrMap mp,
+                                                              float inv_k, float* __restrict__ grad) {
+  tr_reduce_block(part, splits, numel, mp, inv_k, grad, blockIdx.x);
+}
+
+// Several layers' reduces in one launch: block b belongs to the last segment
+// whose first block is <= b (segments start on whole blocks).
+__global__ __launch_bounds__(256) void wgrad_tr_reduce_group_kernel(TrSegTable tab,
+                                                                    const float* __restrict__ base,
+                                                                    float inv_k,
+                                                                    float* __restrict__ grad_base) {
+  const long b = blockIdx.x;
+  int sidx = 0;
+  for (int i = 1; i < tab.n; ++i)
+    if (tab.seg[i].block_begin <= b) sidx = i;
+  const TrSeg& sg = tab.seg[sidx];
+  tr_reduce_block(base + sg.part_off, sg.splits, sg.numel, sg.mp, inv_k, grad_base + sg.w_off,
+                  b - sg.block_begin);
 }
 
 // grad[o*K + k] += inv_k * sum_split part[split][o][k]   (fixed order)
@@ -2866,12 +2910,71 @@ void launch_wgrad_tr(const WgradArgs& a, hipStream_t st) {
   constexpr int BO = WO * OF * 16, BC = WC * CF * 16;
   dim3 grid(a.splits, a.c_out / BO, a.c_in / BC);
   dim3 block(64 * WO * WC * WT * WP);
-  if (a.pro_scale != nullptr)
-    PETRA_LAUNCH((wgrad_tr_kernel<R, TH, TW, WO, OF, WC, CF, WT, WP, true, true>), grid, block, 0, st, a);
-  else
-    PETRA_LAUNCH((wgrad_tr_kernel<R, TH, TW, WO, OF, WC, CF, WT, WP, false, true>), grid, block, 0, st, a);
+  PETRA_LAUNCH((wgrad_tr_kernel<R, TH, TW, WO, OF, WC, CF, WT, WP, true>), grid, block, 0, st, a);
+}
+
+template <int R, int TH, int TW, int WO, int OF, int WC, int CF, int WT, int WP>
+void launch_wgrad_tr_group(const WgradArgs* args, int n, hipStream_t st) {
+  constexpr int BO = WO * OF * 16, BC = WC * CF * 16;
+  for (int i0 = 0; i0 < n; i0 += MAX_WG_GROUP) {
+    WgGroupTable tab{};
+    tab.n = std::min(MAX_WG_GROUP, n - i0);
+    long blocks = 0;
+    for (int i = 0; i < tab.n; ++i) {
+      tab.a[i] = args[i0 + i];
+      tab.block_begin[i] = blocks;
+      blocks += static_cast<long>(tab.a[i].splits) * (tab.a[i].c_out / BO) * (tab.a[i].c_in / BC);
+    }
+    PETRA_LAUNCH((wgrad_tr_group_kernel<R, TH, TW, WO, OF, WC, CF, WT, WP, true>),
+                 dim3(static_cast<unsigned>(blocks)), dim3(64 * WO * WC * WT * WP), 0, st, tab);
+  }
 }
 }  // namespace
+
+namespace {
+
+bool tr_map_of(int dtype, const WgradArgs& a, TrMap* out) {
+  int sp = 0;
+  TrMap& mp = *out;
+  switch (wgrad_tr_plan(dtype, a, &sp)) {
+    case 1: mp = tr_map<3, 4, 32, 1, 2, 1, 2, 3, 4>(a); return true;
+    case 2: mp = tr_map<3, 4, 56, 1, 2, 1, 2, 3, 1>(a); return true;
+    case 3: mp = tr_map<3, 8, 16, 1, 4, 4, 1, 1, 1>(a); return true;
+    case 4: mp = tr_map<3, 8, 8, 1, 4, 4, 1, 1, 1>(a); return true;
+    case 5: mp = tr_map<1, 1, 128, 1, 2, 4, 2, 1, 1>(a); return true;
+    case 6: mp = tr_map<1, 1, 128, 4, 2, 1, 2, 1, 1>(a); return true;
+    default: return false;
+  }
+}
+
+}  // namespace
+
+bool wgrad_tr_segment(int dtype, const WgradArgs& a, long part_off, long w_off, TrSeg* seg) {
+  TrSeg sg{};
+  if (!tr_map_of(dtype, a, &sg.mp)) return false;
+  sg.part_off = part_off;
+  sg.w_off = w_off;
+  sg.numel = static_cast<long>(a.c_out) * a.k_tot;
+  sg.splits = a.splits;
+  *seg = sg;
+  return true;
+}
+
+void wgrad_tr_reduce_group(const float* base, const TrSeg* segs, int nseg, float inv_k,
+                           float* grad_base, hipStream_t st) {
+  for (int i0 = 0; i0 < nseg; i0 += MAX_TR_SEGS) {
+    TrSegTable tab{};
+    tab.n = std::min(MAX_TR_SEGS, nseg - i0);
+    long blocks = 0;
+    for (int i = 0; i < tab.n; ++i) {
+      tab.seg[i] = segs[i0 + i];
+      tab.seg[i].block_begin = blocks;
+      blocks += (tab.seg[i].numel / 4 + 15) / 16;
+    }
+    PETRA_LAUNCH(wgrad_tr_reduce_group_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0,
+                 st, tab, base, inv_k, grad_base);
+  }
+}
 
 bool wgrad_tr_reduce(int dtype, const WgradArgs& a, float inv_k, float* grad, hipStream_t st) {
   int sp = 0;
@@ -2890,6 +2993,23 @@ bool wgrad_tr_reduce(int dtype, const WgradArgs& a, float inv_k, float* grad, hi
   PETRA_LAUNCH(wgrad_tr_reduce_kernel, dim3(static_cast<unsigned>((quads + 15) / 16)), dim3(256), 0,
                st, a.partials, a.splits, numel, mp, inv_k, grad);
   return true;
+}
+
+bool conv_wgrad_tr_group(int dtype, const WgradArgs* args, int n, hipStream_t st) {
+  if (n <= 0) return true;
+  int sp = 0;
+  const int plan = wgrad_tr_plan(dtype, args[0], &sp);
+  for (int i = 1; i < n; ++i)
+    if (wgrad_tr_plan(dtype, args[i], &sp) != plan) return false;
+  switch (plan) {
+    case 1: launch_wgrad_tr_group<3, 4, 32, 1, 2, 1, 2, 3, 4>(args, n, st); return true;
+    case 2: launch_wgrad_tr_group<3, 4, 56, 1, 2, 1, 2, 3, 1>(args, n, st); return true;
+    case 3: launch_wgrad_tr_group<3, 8, 16, 1, 4, 4, 1, 1, 1>(args, n, st); return true;
+    case 4: launch_wgrad_tr_group<3, 8, 8, 1, 4, 4, 1, 1, 1>(args, n, st); return true;
+    case 5: launch_wgrad_tr_group<1, 1, 128, 1, 2, 4, 2, 1, 1>(args, n, st); return true;
+    case 6: launch_wgrad_tr_group<1, 1, 128, 4, 2, 1, 2, 1, 1>(args, n, st); return true;
+    default: return false;
+  }
 }
 
 bool conv_wgrad_tr(int dtype, const WgradArgs& a, hipStream_t st) {

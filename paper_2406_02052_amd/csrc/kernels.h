@@ -75,6 +75,16 @@ void conv_wgrad(int dtype, const WgradArgs& a, hipStream_t st);
 // and its split count (partial rows) for these arguments; conv_wgrad uses it
 // whenever it applies, with a.splits set to that count.
 int wgrad_tr_plan(int dtype, const WgradArgs& a, int* splits);
+// Several layers' transposed-read weight gradients in one launch (each entry
+// as for conv_wgrad, partials to its own a.partials); false, with nothing
+// launched, unless that kernel applies to every entry with one configuration.
+constexpr int MAX_WG_GROUP = 16;
+struct WgGroupTable {
+  int n;
+  long block_begin[MAX_WG_GROUP];
+  WgradArgs a[MAX_WG_GROUP];
+};
+bool conv_wgrad_tr_group(int dtype, const WgradArgs* args, int n, hipStream_t st);
 // Halo-tile weight-gradient kernel selection (0 = not applicable) and the
 // number of pixel tiles it splits over.
 int wgrad_halo_shape(int dtype, const WgradArgs& a);
@@ -85,6 +95,26 @@ void wgrad_reduce(const float* part, int splits, long numel, float inv_k, float*
 // (a.partials, a.splits) into grad[o][k] += inv_k * sum; false when that
 // kernel does not apply to these arguments (use wgrad_reduce then).
 bool wgrad_tr_reduce(int dtype, const WgradArgs& a, float inv_k, float* grad, hipStream_t st);
+// Deferred form: one layer's reduce as a table entry (partials at base +
+// part_off, gradient at grad_base + w_off), false when the transposed-read
+// kernel does not apply; wgrad_tr_reduce_group then reduces many layers in one
+// launch (per element the same fixed order as wgrad_tr_reduce).
+struct TrMap {
+  int wo, of, wc, cf, wt, tpw, bo, bc, nz, c_in, k_tot;
+};
+struct TrSeg {
+  long part_off, w_off, numel, block_begin;
+  int splits;
+  TrMap mp;
+};
+constexpr int MAX_TR_SEGS = 32;
+struct TrSegTable {
+  int n;
+  TrSeg seg[MAX_TR_SEGS];
+};
+bool wgrad_tr_segment(int dtype, const WgradArgs& a, long part_off, long w_off, TrSeg* seg);
+void wgrad_tr_reduce_group(const float* base, const TrSeg* segs, int nseg, float inv_k,
+                           float* grad_base, hipStream_t st);
 
 // BN statistics: partials [tiles][3][c] of (rows, sum h, sum (h - tile mean)^2)
 // combined across tiles with Chan's pairwise formula in fp64 (m rows in all).

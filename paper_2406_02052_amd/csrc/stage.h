@@ -74,7 +74,15 @@ class Stage {
   size_t off_wfwd = 0, off_wdg = 0;
   struct ScratchPlan {
     size_t h[3], d1[2], part, gpart, bpart, bnp;
-  } plan_f{}, plan_b[2]{};
+  };
+  ScratchPlan plan_f{};
+  std::vector<ScratchPlan> plan_b;   // 2 sets, or one per residual function (defer_wgrad)
+  // Weight gradients of all residual functions but the first wait until the end
+  // of a single-stream backward and run as one launch; their inputs then stay
+  // alive: one scratch set per function, and the reconstructed inputs and input
+  // gradients of blocks 1.. in their own buffers (4 half-width tensors per block).
+  bool defer_wgrad = false;
+  size_t off_inter = 0;
   size_t off_wpart = 0;
   int64_t wpart_floats = 0;
 
@@ -90,8 +98,13 @@ class Stage {
   const float* v_th = nullptr;   // active parameter view (see set_view)
   const void* v_wf = nullptr;
   const void* v_wd = nullptr;
-  Scratch sf, sb[2];
-  float* wpart = nullptr;  // weight-gradient split partials (weight-gradient stream only)
+  Scratch sf;
+  std::vector<Scratch> sb;
+  float* wpart = nullptr;  // weight-gradient split partials, one region per conv layer
+  std::vector<int64_t> wpart_off;       // float offset of each conv layer's region
+  std::vector<TrSeg> pending_reduce;    // reduces deferred to the end of the backward
+  std::vector<WgradArgs> pending_wgrad; // weight gradients deferred to the end of the backward
+  bool defer_cur = false;               // the function being enqueued defers its weight gradients
 
   petra_sgd opt{0.1f, 0.9f, 0.0f, 1, 1};
   int64_t bwd_count = 0, last_update = 0;

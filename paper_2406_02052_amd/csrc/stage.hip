@@ -118,22 +118,43 @@ Stage::Stage(const petra_stage_desc& d) : desc(d) {
     g.c_in = cv.cout; g.c_out = cv.cin; g.k_tot = cv.r * cv.s * cv.cout;
     tiles_max = std::max(tiles_max, conv_row_tiles(dt, g));
   }
-  int64_t wmax = 0;
+  // each conv layer has its own weight-gradient partials, so their reduces can
+  // wait until the end of the backward and run as one launch
+  int64_t wtot = 0;
+  wpart_off.clear();
   for (auto& cv : convs) {
     int sp, rps;
     wgrad_splits(cv, &sp, &rps);
-    wmax = std::max<int64_t>(wmax, static_cast<int64_t>(sp) * cv.cout * cv.r * cv.s * cv.cin);
+    wpart_off.push_back(wtot);
+    wtot += (static_cast<int64_t>(sp) * cv.cout * cv.r * cv.s * cv.cin + 63) / 64 * 64;
   }
-  wpart_floats = wmax;
+  wpart_floats = wtot;
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t o = off;
     off = align_up(off + bytes, 256);
     return o;
   };
+  // deferred weight gradients: every layer on the transposed-read kernel
+  {
+    defer_wgrad = dt == DT_BF16 && blocks.size() >= 1;
+    for (const ConvLayer& cv : convs) {
+      WgradArgs w{};
+      w.n = desc.n; w.h = desc.h; w.w = desc.w; w.p = desc.h; w.q = desc.w;
+      w.c_in = cv.cin; w.c_out = cv.cout; w.r = cv.r; w.s = cv.s; w.stride = 1; w.pad = cv.pad;
+      w.k_tot = cv.r * cv.s * cv.cin; w.m = static_cast<int>(M);
+      w.dh_h = reinterpret_cast<const void*>(16);   // marks dh formed on the fly
+      int sp = 0;
+      if (wgrad_tr_plan(dt, w, &sp) == 0) defer_wgrad = false;
+    }
+  }
+  const int nfn = 2 * static_cast<int>(blocks.size());
+  plan_b.assign(defer_wgrad ? std::max(2, nfn) : 2, ScratchPlan{});
   off_wfwd = take(static_cast<size_t>(n_conv) * esz);
   off_wdg = take(static_cast<size_t>(n_conv) * esz);
-  for (ScratchPlan* p : {&plan_f, &plan_b[0], &plan_b[1]}) {
+  std::vector<ScratchPlan*> plans{&plan_f};
+  for (ScratchPlan& pb : plan_b) plans.push_back(&pb);
+  for (ScratchPlan* p : plans) {
     for (size_t l = 0; l < 3; ++l)
       p->h[l] = l < fn_shapes.size() ? take(static_cast<size_t>(M) * fn_shapes[l].cout * esz) : 0;
     const bool bwd = p != &plan_f;
@@ -145,6 +166,8 @@ Stage::Stage(const petra_stage_desc& d) : desc(d) {
     p->bnp = take(static_cast<size_t>(3) * 8 * cmax * sizeof(float));
   }
   off_wpart = take(static_cast<size_t>(wpart_floats) * sizeof(float));
+  if (defer_wgrad && blocks.size() > 1)
+    off_inter = take(static_cast<size_t>(blocks.size() - 1) * 4 * M * desc.c_half * esz);
   ws_need = off;
 }
 
@@ -170,7 +193,8 @@ void Stage::bind(float* th, float* gr, float* mo, float* rm, float* rv, void* w)
   wdg = ws + off_wdg;
   reset_view();
   const int nl = blocks.empty() ? 0 : blocks[0].f.nconv;
-  for (int pass = 0; pass < 3; ++pass) {
+  sb.assign(plan_b.size(), Scratch{});
+  for (int pass = 0; pass < 1 + static_cast<int>(plan_b.size()); ++pass) {
     const ScratchPlan& p = pass == 0 ? plan_f : plan_b[pass - 1];
     Scratch& s = pass == 0 ? sf : sb[pass - 1];
     const bool bwd = pass > 0;
@@ -220,7 +244,7 @@ void Stage::wgrad_splits(const ConvLayer& cv, int* splits, int* rows_per_split) 
   w.n = desc.n; w.h = desc.h; w.w = desc.w; w.p = desc.h; w.q = desc.w;
   w.c_in = cv.cin; w.c_out = cv.cout; w.r = cv.r; w.s = cv.s; w.stride = 1; w.pad = cv.pad;
   w.k_tot = cv.r * cv.s * cv.cin; w.m = static_cast<int>(M);
-  w.dh_h = w.src;   // the stage always forms dh on the fly from a pre-BN tensor
+  w.dh_h = reinterpret_cast<const void*>(16);   // dh is always formed on the fly (marker)
   int tr_splits = 0;
   if (wgrad_tr_plan(dt, w, &tr_splits) != 0) {
     *splits = tr_splits;
@@ -406,22 +430,34 @@ void Stage::fn_grad(const BwdFn& f, Scratch& s, const BwdFn* next, Scratch* sn, 
       w.pro_scale = s.vec(l - 1, V_SCALE, cmax);
       w.pro_shift = s.vec(l - 1, V_SHIFT, cmax);
     }
-    w.partials = wpart;
+    const int64_t poff = wpart_off[static_cast<size_t>(&cv - convs.data())];
+    w.partials = wpart + poff;
     w.n = desc.n; w.h = desc.h; w.w = desc.w; w.c_in = cv.cin; w.p = desc.h; w.q = desc.w;
     w.c_out = cv.cout; w.r = cv.r; w.s = cv.s; w.stride = 1; w.pad = cv.pad;
     w.k_tot = cv.r * cv.s * cv.cin;
     w.m = static_cast<int>(M);
     wgrad_splits(cv, &w.splits, &w.rows_per_split);
     const double wnumel = static_cast<double>(cv.cout) * w.k_tot;
+    TrSeg seg{};
+    if (defer_cur) {
+      // launched with the other deferred layers at the end of the backward
+      (void)wgrad_tr_segment(dt, w, static_cast<long>(poff), static_cast<long>(cv.w_off), &seg);
+      pending_wgrad.push_back(w);
+      pending_reduce.push_back(seg);
+      continue;
+    }
     prof.begin(wst);
     conv_wgrad(dt, w, wst);
     prof.end(K_CONV_WGRAD, wst, 2.0 * M * wnumel,
              static_cast<double>(esz) * M * (cv.cin + 2.0 * cv.cout) + 4.0 * w.splits * wnumel);
-    prof.begin(wst);
-    if (!wgrad_tr_reduce(dt, w, inv_k, grad + cv.w_off, wst))
-      wgrad_reduce(wpart, w.splits, static_cast<long>(cv.cout) * w.k_tot, inv_k, grad + cv.w_off,
-                   wst);
-    prof.end(K_WGRAD_REDUCE, wst, 0.0, 4.0 * wnumel * (w.splits + 2));
+    if (wgrad_tr_segment(dt, w, static_cast<long>(poff), static_cast<long>(cv.w_off), &seg)) {
+      pending_reduce.push_back(seg);   // reduced at the end of the backward
+    } else {
+      prof.begin(wst);
+      wgrad_reduce(w.partials, w.splits, static_cast<long>(cv.cout) * w.k_tot, inv_k,
+                   grad + cv.w_off, wst);
+      prof.end(K_WGRAD_REDUCE, wst, 0.0, 4.0 * wnumel * (w.splits + 2));
+    }
   }
   if (part == 1) {
     if (rb) (void)hipEventRecord(ev_gdone[parity], st);
@@ -472,26 +508,39 @@ void Stage::reconstruct(const void* y1, const void* y2, void* x1, void* x2, hipS
 void Stage::backward(const void* y1, const void* y2, const void* dy1, const void* dy2, void* x1,
                      void* x2, void* dx1, void* dx2, hipStream_t st) {
   // Residual functions in the order the backward visits them.
-  std::vector<BwdFn> fl;
-  const void* c1 = y1;
-  const void* c2 = y2;
-  const void* g1 = dy1;
-  const void* g2 = dy2;
-  for (int b = static_cast<int>(blocks.size()) - 1; b >= 0; --b) {
-    const Block& blk = blocks[b];
-    // x2 = y2 - G(y1); z1 = g1 + dG/dy1^T g2  (written to dx1)
-    fl.push_back(BwdFn{&blk.g, c1, c2, g2, g1, x2, dx1});
-    // x1 = y1 - F(x2); dx2 = g2 + dF/dx2^T z1
-    fl.push_back(BwdFn{&blk.f, x2, c1, dx1, g2, x1, dx2});
-    c1 = x1; c2 = x2; g1 = dx1; g2 = dx2;
-  }
-  const int nf = static_cast<int>(fl.size());
+  pending_reduce.clear();
+  pending_wgrad.clear();
   // streams: the weight gradients (2+) and the recompute of the next function
   // (3) on side streams; one stream when profiling per launch
   const bool par = s_rec != nullptr && s_wg != nullptr && !prof.enabled;
   hipStream_t rs = par && bwd_streams >= 3 ? s_rec : st;
   hipStream_t wst = par && bwd_streams >= 2 ? s_wg : st;
   const bool rb = rs != st, wb = wst != st;
+  // single stream: all weight gradients but the first function's wait for the end
+  const bool defer = defer_wgrad && !rb && !wb;
+  std::vector<BwdFn> fl;
+  const void* c1 = y1;
+  const void* c2 = y2;
+  const void* g1 = dy1;
+  const void* g2 = dy2;
+  const size_t half = static_cast<size_t>(M) * desc.c_half * esz;
+  for (int b = static_cast<int>(blocks.size()) - 1; b >= 0; --b) {
+    const Block& blk = blocks[b];
+    // blocks 1.. write to their own buffers when the weight gradients are deferred
+    char* ib = defer && b > 0 ? ws + off_inter + static_cast<size_t>(b - 1) * 4 * half : nullptr;
+    void* bx1 = ib ? ib : x1;
+    void* bx2 = ib ? ib + half : x2;
+    void* bdx1 = ib ? ib + 2 * half : dx1;
+    void* bdx2 = ib ? ib + 3 * half : dx2;
+    // x2 = y2 - G(y1); z1 = g1 + dG/dy1^T g2  (written to dx1)
+    fl.push_back(BwdFn{&blk.g, c1, c2, g2, g1, bx2, bdx1});
+    // x1 = y1 - F(x2); dx2 = g2 + dF/dx2^T z1
+    fl.push_back(BwdFn{&blk.f, bx2, c1, bdx1, g2, bx1, bdx2});
+    c1 = bx1; c2 = bx2; g1 = bdx1; g2 = bdx2;
+  }
+  const int nf = static_cast<int>(fl.size());
+  // scratch set of function f: its own when deferring, else alternating
+  auto S = [&](int f) -> Scratch& { return defer ? sb[f] : sb[f & 1]; };
   if (rb || wb) (void)hipEventRecord(ev_start, st);
   if (rb) (void)hipStreamWaitEvent(rs, ev_start, 0);
   if (wb) (void)hipStreamWaitEvent(wst, ev_start, 0);
@@ -499,33 +548,36 @@ void Stage::backward(const void* y1, const void* y2, const void* dy1, const void
   // First function: recompute, reconstruction and the BN_L-backward partials of
   // the given output gradient.
   {
-    fn_recompute(*fl[0].fn, fl[0].u, sb[0], true, rs);
+    Scratch& s0 = S(0);
+    fn_recompute(*fl[0].fn, fl[0].u, s0, true, rs);
     const int L = fl[0].fn->nconv - 1;
     const int c = last_c(fl[0]);
     prof.begin(rs);
-    combine_bwd(dt, fl[0].v, sb[0].h[L], fl[0].d, sb[0].vec(L, V_SCALE, cmax),
-                sb[0].vec(L, V_SHIFT, cmax), sb[0].vec(L, V_MEAN, cmax),
-                sb[0].vec(L, V_RSTD, cmax), fl[0].xrec, sb[0].gpart, M, c, rs);
+    combine_bwd(dt, fl[0].v, s0.h[L], fl[0].d, s0.vec(L, V_SCALE, cmax),
+                s0.vec(L, V_SHIFT, cmax), s0.vec(L, V_MEAN, cmax),
+                s0.vec(L, V_RSTD, cmax), fl[0].xrec, s0.gpart, M, c, rs);
     prof.end(K_COMBINE_BWD, rs, 0.0, 4.0 * M * c * esz);
-    sb[0].gtiles = ew_tiles(M, c);
+    s0.gtiles = ew_tiles(M, c);
     if (rb) (void)hipEventRecord(ev_rec[0], rs);
   }
   for (int f = 0; f < nf; ++f) {
     const int p = f & 1;
     const bool has_next = f + 1 < nf;
     const BwdFn* nx = has_next ? &fl[f + 1] : nullptr;
-    Scratch* sn = has_next ? &sb[p ^ 1] : nullptr;
+    Scratch& sc = S(f);
+    Scratch* sn = has_next ? &S(f + 1) : nullptr;
     const void* dsrc = nullptr;
+    defer_cur = defer && f >= 1;
     if (rb) (void)hipStreamWaitEvent(st, ev_rec[p], 0);
-    fn_grad(fl[f], sb[p], nx, sn, st, wst, rs, f >= 1, p, 0, &dsrc);
+    fn_grad(fl[f], sc, nx, sn, st, wst, rs, f >= 1, p, 0, &dsrc);
     if (has_next) {
       // recompute of the next function (its input is this function's
       // reconstruction); its scratch set was last used by function f - 1
       if (rb && f >= 1) (void)hipStreamWaitEvent(rs, ev_gdone[p ^ 1], 0);
-      fn_recompute(*fl[f + 1].fn, fl[f + 1].u, sb[p ^ 1], true, rs);
+      fn_recompute(*fl[f + 1].fn, fl[f + 1].u, *sn, true, rs);
       if (rb) (void)hipEventRecord(ev_rec[p ^ 1], rs);
     }
-    fn_grad(fl[f], sb[p], nx, sn, st, wst, rs, f >= 1, p, 1, &dsrc);
+    fn_grad(fl[f], sc, nx, sn, st, wst, rs, f >= 1, p, 1, &dsrc);
     if (has_next) {
       // reconstruction of the next function; it may overwrite this function's
       // input, which this function's weight gradients read
@@ -534,17 +586,64 @@ void Stage::backward(const void* y1, const void* y2, const void* dy1, const void
       const int L = nx.fn->nconv - 1;
       const int c = last_c(nx);
       prof.begin(rs);
-      combine_rec(dt, nx.v, sb[p ^ 1].h[L], sb[p ^ 1].vec(L, V_SCALE, cmax),
-                  sb[p ^ 1].vec(L, V_SHIFT, cmax), nx.xrec, M, c, rs);
+      combine_rec(dt, nx.v, sn->h[L], sn->vec(L, V_SCALE, cmax), sn->vec(L, V_SHIFT, cmax),
+                  nx.xrec, M, c, rs);
       prof.end(K_COMBINE_BWD, rs, 0.0, 3.0 * M * c * esz);
     }
   }
+  defer_cur = false;
   // join the side streams
   if (rb) {
     (void)hipEventRecord(ev_rec_end, rs);
     (void)hipStreamWaitEvent(st, ev_rec_end, 0);
   }
   if (wb) (void)hipStreamWaitEvent(st, ev_wgdone[(nf - 1) & 1], 0);
+  // the deferred weight gradients, in one launch (their inputs are still intact:
+  // each function kept its scratch set and its block's buffers)
+  if (!pending_wgrad.empty()) {
+    // one launch per kernel configuration (and per MAX_WG_GROUP layers)
+    std::vector<std::pair<int, WgradArgs>> byplan;
+    for (const WgradArgs& w : pending_wgrad) {
+      int sp = 0;
+      byplan.emplace_back(wgrad_tr_plan(dt, w, &sp), w);
+    }
+    std::stable_sort(byplan.begin(), byplan.end(),
+                     [](const auto& a, const auto& b) { return a.first < b.first; });
+    for (size_t i0 = 0; i0 < byplan.size();) {
+      size_t i1 = i0;
+      std::vector<WgradArgs> grp;
+      double fl = 0.0, by = 0.0;
+      while (i1 < byplan.size() && byplan[i1].first == byplan[i0].first &&
+             grp.size() < static_cast<size_t>(MAX_WG_GROUP)) {
+        const WgradArgs& w = byplan[i1].second;
+        const double wn = static_cast<double>(w.c_out) * w.k_tot;
+        fl += 2.0 * M * wn;
+        by += static_cast<double>(esz) * M * (w.c_in + 2.0 * w.c_out) + 4.0 * w.splits * wn;
+        grp.push_back(w);
+        ++i1;
+      }
+      prof.begin(st);
+      const bool ok = conv_wgrad_tr_group(dt, grp.data(), static_cast<int>(grp.size()), st);
+      prof.end(K_CONV_WGRAD, st, fl, by);
+      if (!ok) launch_error = true;
+      i0 = i1;
+    }
+    pending_wgrad.clear();
+  }
+  // the deferred weight-gradient reduces of every layer, in one launch
+  if (!pending_reduce.empty()) {
+    const float inv_k = 1.0f / static_cast<float>(std::max(1, opt.accum_k));
+    for (size_t i0 = 0; i0 < pending_reduce.size(); i0 += MAX_TR_SEGS) {
+      const int n = static_cast<int>(std::min<size_t>(MAX_TR_SEGS, pending_reduce.size() - i0));
+      double bytes = 0.0;
+      for (int i = 0; i < n; ++i)
+        bytes += 4.0 * pending_reduce[i0 + i].numel * (pending_reduce[i0 + i].splits + 2);
+      prof.begin(st);
+      wgrad_tr_reduce_group(wpart, pending_reduce.data() + i0, n, inv_k, grad, st);
+      prof.end(K_WGRAD_REDUCE, st, 0.0, bytes);
+    }
+    pending_reduce.clear();
+  }
 }
 
 bool Stage::update_due() const {
