@@ -2893,7 +2893,9 @@ int wgrad_tr_plan(int dtype, const WgradArgs& a, int* splits) {
   const int ntiles = a.r == 1 ? (a.m + th * tw - 1) / (th * tw)
                               : ((a.w + tw - 1) / tw) * ((a.h + th - 1) / th) * a.n;
   const int per = (a.c_out / bo) * (a.c_in / bc);
-  if (splits) *splits = std::max(1, std::min(ntiles, 256 / per));
+  // about half a workgroup per CU and layer: the backward launches the weight
+  // gradients of all but one layer together, so fewer, longer splits win
+  if (splits) *splits = std::max(1, std::min(ntiles, 128 / per));
   return cfg;
 }
 

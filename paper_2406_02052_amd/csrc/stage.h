@@ -77,10 +77,11 @@ class Stage {
   };
   ScratchPlan plan_f{};
   std::vector<ScratchPlan> plan_b;   // 2 sets, or one per residual function (defer_wgrad)
-  // Weight gradients of all residual functions but the first wait until the end
-  // of a single-stream backward and run as one launch; their inputs then stay
-  // alive: one scratch set per function, and the reconstructed inputs and input
-  // gradients of blocks 1.. in their own buffers (4 half-width tensors per block).
+  // Weight gradients wait until the end of a single-stream backward and run as
+  // one launch per kernel configuration (the first function's only when the
+  // call is not in place); their inputs then stay alive: one scratch set per
+  // function, and the reconstructed inputs and input gradients of blocks 1.. in
+  // their own buffers (4 half-width tensors per block).
   bool defer_wgrad = false;
   size_t off_inter = 0;
   size_t off_wpart = 0;

@@ -516,7 +516,8 @@ void Stage::backward(const void* y1, const void* y2, const void* dy1, const void
   hipStream_t rs = par && bwd_streams >= 3 ? s_rec : st;
   hipStream_t wst = par && bwd_streams >= 2 ? s_wg : st;
   const bool rb = rs != st, wb = wst != st;
-  // single stream: all weight gradients but the first function's wait for the end
+  // single stream: the weight gradients wait for the end (the first function's
+  // only when its inputs survive the backward)
   const bool defer = defer_wgrad && !rb && !wb;
   std::vector<BwdFn> fl;
   const void* c1 = y1;
@@ -567,7 +568,9 @@ void Stage::backward(const void* y1, const void* y2, const void* dy1, const void
     Scratch& sc = S(f);
     Scratch* sn = has_next ? &S(f + 1) : nullptr;
     const void* dsrc = nullptr;
-    defer_cur = defer && f >= 1;
+    // the first function's weight gradients read y1 and dy2, which the last
+    // function overwrites when the caller runs in place (x1 == y1, dx2 == dy2)
+    defer_cur = defer && (f >= 1 || (x1 != y1 && dx2 != dy2));
     if (rb) (void)hipStreamWaitEvent(st, ev_rec[p], 0);
     fn_grad(fl[f], sc, nx, sn, st, wst, rs, f >= 1, p, 0, &dsrc);
     if (has_next) {
