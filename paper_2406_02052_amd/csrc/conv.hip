@@ -1190,11 +1190,11 @@ __global__ __launch_bounds__(256, 2) void conv_fp_kernel(ConvArgs a) {
 //    consecutive output channels of one pixel, stored directly (8 bytes), and
 //    the BN statistics are shifted sums in registers reduced once at the end.
 // Partial row of the statistics = blockIdx.x (the image).
-template <int TH, int TW, int CH, int EP, int PRO>
-__global__ __launch_bounds__(512, 1) void conv_img_kernel(ConvArgs a) {
+template <int TH, int TW, int CH, int EP, int PRO, int NWM, int NWN>
+__global__ __launch_bounds__(64 * NWM * NWN, 1) void conv_img_kernel(ConvArgs a) {
   using T = bf16_t;
-  constexpr int NT = 512;
-  constexpr int WAVES_M = 4, WAVES_N = 2;
+  constexpr int NT = 64 * NWM * NWN;
+  constexpr int WAVES_M = NWM, WAVES_N = NWN;
   constexpr int BN = 128, BM = TH * TW;
   constexpr int TM = BM / WAVES_M, TN = BN / WAVES_N;
   constexpr int FM = TM / 16, FN = TN / 16;
@@ -1236,8 +1236,10 @@ __global__ __launch_bounds__(512, 1) void conv_img_kernel(ConvArgs a) {
   // Weight slab j holds k = 64 j .. 64 j + 63 of every output channel; thread
   // q loads 16 bytes of row q / 8, so 8 neighbouring threads read one row's
   // 128 bytes.
-  Raw8<T> rs[S_CHUNKS];
-  auto load_slab = [&](int j) {
+  // Two register sets: slab j + 1 is loaded one iteration before it is parked,
+  // so its L2 latency hides behind two slabs of MFMA work.
+  Raw8<T> rs0[S_CHUNKS], rs1[S_CHUNKS];
+  auto load_slab = [&](Raw8<T>* rs, int j) {
 #pragma unroll
     for (int i = 0; i < S_CHUNKS; ++i) {
       const int q = tid + NT * i;
@@ -1245,7 +1247,7 @@ __global__ __launch_bounds__(512, 1) void conv_img_kernel(ConvArgs a) {
       rs[i].set(buf_load16(r_wt, static_cast<uint32_t>((row * a.k_tot + j * 64 + sub * 8) * 2)));
     }
   };
-  auto park_slab = [&](int buf) {
+  auto park_slab = [&](const Raw8<T>* rs, int buf) {
 #pragma unroll
     for (int i = 0; i < S_CHUNKS; ++i) {
       const int q = tid + NT * i;
@@ -1254,7 +1256,8 @@ __global__ __launch_bounds__(512, 1) void conv_img_kernel(ConvArgs a) {
           make_uint4(rs[i].w[0], rs[i].w[1], rs[i].w[2], rs[i].w[3]);
     }
   };
-  load_slab(0);
+  load_slab(rs0, 0);
+  load_slab(rs1, SLABS > 1 ? 1 : 0);
 
   if constexpr (PRO == PRO_RELU) {
     for (int i = tid; i < a.c_in; i += NT) {
@@ -1315,7 +1318,7 @@ __global__ __launch_bounds__(512, 1) void conv_img_kernel(ConvArgs a) {
     if (c + 1 < CH) load_chunk(c + 1, (c + 1) & 1);
     park_chunk(c, c & 1);
   }
-  park_slab(0);
+  park_slab(rs0, 0);
   __syncthreads();
 
   int rowpix[FM];
@@ -1331,9 +1334,13 @@ __global__ __launch_bounds__(512, 1) void conv_img_kernel(ConvArgs a) {
 #pragma unroll
     for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  for (int j = 0; j < SLABS; ++j) {
+  // Iteration j: slab j + 2 into the set that held slab j, MFMAs on slab j from
+  // LDS, then slab j + 1 (loaded an iteration earlier) parked into the other
+  // LDS buffer.  Loads past the end re-read the last slab (never parked), so
+  // the number of loads in flight is the same every iteration.
+  auto slab_iter = [&](int j, Raw8<T>* rs_load, const Raw8<T>* rs_park) {
     const int buf = j & 1;
-    load_slab(min(j + 1, SLABS - 1));   // past the end: reload the last slab (not parked)
+    load_slab(rs_load, min(j + 2, SLABS - 1));
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
@@ -1352,8 +1359,12 @@ __global__ __launch_bounds__(512, 1) void conv_img_kernel(ConvArgs a) {
         for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma(wf[fn], pf[fm], acc[fm][fn]);
     }
     __builtin_amdgcn_sched_barrier(0);
-    if (j + 1 < SLABS) park_slab(buf ^ 1);
+    if (j + 1 < SLABS) park_slab(rs_park, buf ^ 1);
     __syncthreads();
+  };
+  for (int j = 0; j < SLABS; j += 2) {
+    slab_iter(j, rs0, rs1);
+    if (j + 1 < SLABS) slab_iter(j + 1, rs1, rs0);
   }
 
   // Epilogue: lane (lr, lg) holds channels wn*TN + fn*16 + lg*4 + e of pixel
@@ -1471,8 +1482,14 @@ __global__ __launch_bounds__(512, 1) void conv_img_kernel(ConvArgs a) {
         pr[(row * 3 + 1) * BN + c] = n * mean;
         pr[(row * 3 + 2) * BN + c] = m2;
       } else {
-        pr[(row * 2 + 0) * BN + c] = (red[0][1][c] + red[1][1][c]) + (red[2][1][c] + red[3][1][c]);
-        pr[(row * 2 + 1) * BN + c] = (red[0][2][c] + red[1][2][c]) + (red[2][2][c] + red[3][2][c]);
+        float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+        for (int w = 0; w < WAVES_M; ++w) {
+          s1 += red[w][1][c];
+          s2 += red[w][2][c];
+        }
+        pr[(row * 2 + 0) * BN + c] = s1;
+        pr[(row * 2 + 1) * BN + c] = s2;
       }
     }
   }
@@ -2770,11 +2787,15 @@ bool launch_halo(const ConvArgs& a, int ep, hipStream_t st) {
   });
 }
 
+// IMG_WM x IMG_WN waves per image, each 64 pixels x 64 channels (measured:
+// 2 x 2 waves of 128 x 64, with a third fewer LDS reads per MFMA but one wave
+// per SIMD, ran 17 % slower).
+constexpr int IMG_WM = 4, IMG_WN = 2;
 template <int TH, int TW, int CH>
 bool launch_img(const ConvArgs& a, int ep, hipStream_t st) {
   return dispatch_ep_pro(ep, pro_mode(a), [&](auto k) {
-    PETRA_LAUNCH((conv_img_kernel<TH, TW, CH, decltype(k)::ep, decltype(k)::pro>),
-                       dim3(a.n), dim3(512), 0, st, a);
+    PETRA_LAUNCH((conv_img_kernel<TH, TW, CH, decltype(k)::ep, decltype(k)::pro, IMG_WM, IMG_WN>),
+                 dim3(a.n), dim3(64 * IMG_WM * IMG_WN), 0, st, a);
   });
 }
 
