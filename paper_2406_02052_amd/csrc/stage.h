@@ -106,6 +106,8 @@ class Stage {
   std::vector<TrSeg> pending_reduce;    // reduces deferred to the end of the backward
   std::vector<WgradArgs> pending_wgrad; // weight gradients deferred to the end of the backward
   bool defer_cur = false;               // the function being enqueued defers its weight gradients
+  // launch the deferred weight gradients and reduces collected so far on q
+  void flush_deferred(hipStream_t q);
 
   petra_sgd opt{0.1f, 0.9f, 0.0f, 1, 1};
   int64_t bwd_count = 0, last_update = 0;
@@ -118,7 +120,7 @@ class Stage {
   // the weight gradients on s_wg, the input-gradient chain on the caller's stream.
   hipStream_t s_rec = nullptr, s_wg = nullptr;
   hipEvent_t ev_fork = nullptr, ev_fwd = nullptr, ev_bwd = nullptr;
-  hipEvent_t ev_start = nullptr, ev_d = nullptr, ev_rec_end = nullptr;
+  hipEvent_t ev_start = nullptr, ev_d = nullptr, ev_rec_end = nullptr, ev_side = nullptr;
   hipEvent_t ev_rec[2] = {nullptr, nullptr};     // recompute of set p done (h, BN statistics)
   hipEvent_t ev_gdone[2] = {nullptr, nullptr};   // input-gradient chain done with set p
   hipEvent_t ev_wgdone[2] = {nullptr, nullptr};  // weight gradients done with set p
@@ -139,8 +141,11 @@ class Stage {
   // same layout is set (a stashed copy); the update always writes the bound ones.
   void set_view(const float* th, const void* wf, const void* wd) { v_th = th; v_wf = wf; v_wd = wd; }
   void reset_view() { v_th = theta; v_wf = wfwd; v_wd = wdg; }
+  // side (optional, single-stream deferred mode only): a stream that is idle
+  // during the second half of the backward; the first half's weight gradients
+  // run there, after one event, and the caller joins it before the update.
   void backward(const void* y1, const void* y2, const void* dy1, const void* dy2, void* x1,
-                void* x2, void* dx1, void* dx2, hipStream_t st);
+                void* x2, void* dx1, void* dx2, hipStream_t st, hipStream_t side = nullptr);
   void update_kernels(hipStream_t st);
   // Host-side accumulation bookkeeping: count one backward; does the update fire now?
   void count_backward() { ++bwd_count; }

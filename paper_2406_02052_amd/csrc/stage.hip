@@ -218,7 +218,7 @@ hipError_t Stage::ensure_streams() {
   if ((e = hipEventCreateWithFlags(&ev_fwd, hipEventDisableTiming)) != hipSuccess) return e;
   if ((e = hipStreamCreateWithFlags(&s_wg, hipStreamNonBlocking)) != hipSuccess) return e;
   if ((e = hipStreamCreateWithFlags(&s_rec, hipStreamNonBlocking)) != hipSuccess) return e;
-  for (hipEvent_t* ev : {&ev_start, &ev_d, &ev_rec_end, &ev_rec[0], &ev_rec[1], &ev_gdone[0],
+  for (hipEvent_t* ev : {&ev_start, &ev_d, &ev_rec_end, &ev_side, &ev_rec[0], &ev_rec[1], &ev_gdone[0],
                          &ev_gdone[1], &ev_wgdone[0], &ev_wgdone[1]})
     if ((e = hipEventCreateWithFlags(ev, hipEventDisableTiming)) != hipSuccess) return e;
   return hipEventCreateWithFlags(&ev_bwd, hipEventDisableTiming);
@@ -506,7 +506,7 @@ void Stage::reconstruct(const void* y1, const void* y2, void* x1, void* x2, hipS
 }
 
 void Stage::backward(const void* y1, const void* y2, const void* dy1, const void* dy2, void* x1,
-                     void* x2, void* dx1, void* dx2, hipStream_t st) {
+                     void* x2, void* dx1, void* dx2, hipStream_t st, hipStream_t side) {
   // Residual functions in the order the backward visits them.
   pending_reduce.clear();
   pending_wgrad.clear();
@@ -581,6 +581,12 @@ void Stage::backward(const void* y1, const void* y2, const void* dy1, const void
       if (rb) (void)hipEventRecord(ev_rec[p ^ 1], rs);
     }
     fn_grad(fl[f], sc, nx, sn, st, wst, rs, f >= 1, p, 1, &dsrc);
+    if (defer && side != nullptr && ev_side != nullptr && nf >= 2 && f + 1 == nf / 2) {
+      // the first half's weight gradients on the idle side stream
+      (void)hipEventRecord(ev_side, st);
+      (void)hipStreamWaitEvent(side, ev_side, 0);
+      flush_deferred(side);
+    }
     if (has_next) {
       // reconstruction of the next function; it may overwrite this function's
       // input, which this function's weight gradients read
@@ -601,8 +607,13 @@ void Stage::backward(const void* y1, const void* y2, const void* dy1, const void
     (void)hipStreamWaitEvent(st, ev_rec_end, 0);
   }
   if (wb) (void)hipStreamWaitEvent(st, ev_wgdone[(nf - 1) & 1], 0);
-  // the deferred weight gradients, in one launch (their inputs are still intact:
-  // each function kept its scratch set and its block's buffers)
+  // the (remaining) deferred weight gradients and every layer's reduce: their
+  // inputs are still intact (each function kept its scratch set and its block's
+  // buffers)
+  flush_deferred(st);
+}
+
+void Stage::flush_deferred(hipStream_t st) {
   if (!pending_wgrad.empty()) {
     // one launch per kernel configuration (and per MAX_WG_GROUP layers)
     std::vector<std::pair<int, WgradArgs>> byplan;
