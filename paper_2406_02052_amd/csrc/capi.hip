@@ -354,8 +354,8 @@ petra_status petra_stage_step(petra_stage* st, const void* x1, const void* x2, v
   } else {
     if (s.defer_wgrad && s.bwd_streams == 1 && !s.prof.enabled) {
       // the forward stream is idle once the forward is done: the backward puts
-      // the first half of its deferred weight gradients there (after the
-      // forward's launches; the join below covers them)
+      // most of its deferred weight gradients there (after the forward's
+      // launches; the join below covers them)
       s.forward(x1, x2, y1, y2, s.s_fwd);
       s.backward(yb1, yb2, dyb1, dyb2, xb1, xb2, dxb1, dxb2, main, s.s_fwd);
     } else {

@@ -141,7 +141,8 @@ class Net {
   // Blocks + front backward of micro-batch mb given the block output (by) and
   // its gradient (bg), in variant `mode`; the message goes to parity `parity`.
   void backward_stage(NetStage& s, int64_t mb, int mode, int parity, hipStream_t q,
-                      const void* by1, const void* by2, const void* bg1, const void* bg2);
+                      const void* by1, const void* by2, const void* bg1, const void* bg2,
+                      hipStream_t side = nullptr);
   void backprop_pass(const void* images, const int32_t* labels, float* loss, bool update,
                      hipStream_t q);
   struct Redirect;

@@ -142,8 +142,9 @@ class Stage {
   void set_view(const float* th, const void* wf, const void* wd) { v_th = th; v_wf = wf; v_wd = wd; }
   void reset_view() { v_th = theta; v_wf = wfwd; v_wd = wdg; }
   // side (optional, single-stream deferred mode only): a stream that is idle
-  // during the second half of the backward; the first half's weight gradients
-  // run there, after one event, and the caller joins it before the update.
+  // during the second half of the backward; the weight gradients collected by
+  // the middle and by the last function run there (one event each), and the
+  // caller joins it before the update.
   void backward(const void* y1, const void* y2, const void* dy1, const void* dy2, void* x1,
                 void* x2, void* dx1, void* dx2, hipStream_t st, hipStream_t side = nullptr);
   void update_kernels(hipStream_t st);

@@ -581,8 +581,10 @@ void Stage::backward(const void* y1, const void* y2, const void* dy1, const void
       if (rb) (void)hipEventRecord(ev_rec[p ^ 1], rs);
     }
     fn_grad(fl[f], sc, nx, sn, st, wst, rs, f >= 1, p, 1, &dsrc);
-    if (defer && side != nullptr && ev_side != nullptr && nf >= 2 && f + 1 == nf / 2) {
-      // the first half's weight gradients on the idle side stream
+    if (defer && side != nullptr && ev_side != nullptr && nf >= 2 &&
+        (f + 1 == nf / 2 || f + 1 == nf - 1)) {
+      // the weight gradients collected so far on the idle side stream (after
+      // the first half and before the last function: one event each)
       (void)hipEventRecord(ev_side, st);
       (void)hipStreamWaitEvent(side, ev_side, 0);
       flush_deferred(side);
