@@ -102,13 +102,19 @@ def head_vjp(wfc, labels, cache):
 
 
 class NetStage:
-    """One stage: a non-reversible front layer, reversible blocks, optional head."""
+    """One stage: an optional non-reversible front layer (`front` = "stem" on the
+    images or "trans" for a downsampling, None for a purely reversible stage),
+    `blocks` reversible blocks (possibly none) and, for the last stage, the head.
+    Parameter order: front (w, gamma, beta), blocks, head (weight, bias)."""
 
     def __init__(self, params, names, first: bool, last: bool, blocks: int, eps: float,
-                 bn_momentum: float, dtype, weight_view, store=None):
+                 bn_momentum: float, dtype, weight_view, store=None, front="auto"):
         self.params = [np.array(p, dtype=dtype) for p in params]
         self.names = list(names)
+        self.front = ("stem" if first else "trans") if front == "auto" else front
         self.first, self.last, self.blocks = first, last, blocks
+        self.fo = 3 if self.front else 0     # first block parameter
+        self.ro = 1 if self.front else 0     # first block BN slot
         self.eps, self.bn_momentum, self.dtype = eps, bn_momentum, dtype
         self.weight_view = weight_view
         if store is None:
@@ -117,7 +123,7 @@ class NetStage:
             self.store = lambda a: np.asarray(store(np.asarray(a, np.float32)), dtype=dtype)
         self.accum = [np.zeros_like(p) for p in self.params]
         self.buf = [np.zeros_like(p) for p in self.params]
-        nbn = 1 + blocks * 4
+        nbn = self.ro + blocks * 4
         self.run_mean = [np.zeros(self.params[3 * i + 1].shape, dtype) for i in range(nbn)]
         self.run_var = [np.ones(self.params[3 * i + 1].shape, dtype) for i in range(nbn)]
         self.t = 0
@@ -133,23 +139,24 @@ class NetStage:
 
     def _layers(self, b, f, P=None):
         P = self.params if P is None else P
-        base = 3 + (2 * b + f) * 6
+        base = self.fo + (2 * b + f) * 6
         return [(self._w(base + 3 * l, P), P[base + 3 * l + 1], P[base + 3 * l + 2])
                 for l in range(2)]
 
     def _front(self, x1, x2, P=None):
         P = self.params if P is None else P
-        x = x1 if self.first else np.concatenate([x1, x2], axis=-1)
-        stride = 1 if self.first else 2
+        stem = self.front == "stem"
+        x = x1 if stem else np.concatenate([x1, x2], axis=-1)
+        stride = 1 if stem else 2
         a, graph = nonrev_forward(x, self._w(0, P), P[1], P[2], self.eps,
-                                  stride, relu=self.first, store=self.store)
+                                  stride, relu=stem, store=self.store)
         c = a.shape[-1] // 2
         return a[..., :c], a[..., c:], graph
 
     def forward(self, x1, x2, m=None):
         if m is not None:
             self.stash[m] = [p.copy() for p in self.params]
-        y1, y2, _ = self._front(x1, x2)
+        y1, y2 = self._front(x1, x2)[:2] if self.front else (x1, x2)
         if m is not None:
             self.inbuf[m] = (y1, y2)
         for b in range(self.blocks):
@@ -174,11 +181,11 @@ class NetStage:
 
         def take(b, r):
             for f, key in ((0, "dF"), (1, "dG")):
-                base = 3 + (2 * b + f) * 6
+                base = self.fo + (2 * b + f) * 6
                 stats = r["stats_F" if f == 0 else "stats_G"]
                 for l, (dw, dg, db) in enumerate(r[key]):
                     grads[base + 3 * l: base + 3 * l + 3] = [dw, dg, db]
-                    self._running((base + 3 * l) // 3, stats[l])
+                    self._running(self.ro + (base - self.fo + 3 * l) // 3, stats[l])
 
         if not use_inputs and not use_params:
             for b in reversed(range(self.blocks)):
@@ -206,11 +213,17 @@ class NetStage:
                                        self._layers(b, 1, P), self.eps, self.store)
                 take(b, r)
                 g1, g2 = r["dx1"], r["dx2"]
+        if not self.front:
+            # purely reversible stage: the input gradient is the blocks' one and
+            # the stage sends back the block input it used (reconstructed)
+            self.last_used["dx"] = np.concatenate([g1, g2], axis=-1)
+            return self.last_used["dx"], grads
         # non-reversible front: recompute from the buffered input
         _, _, graph = self._front(x1, x2, P)
-        stride = 1 if self.first else 2
+        stem = self.front == "stem"
+        stride = 1 if stem else 2
         dx, (dw, dg, db) = nonrev_vjp(np.concatenate([g1, g2], axis=-1), self._w(0, P),
-                                      P[1], graph, stride, relu=self.first,
+                                      P[1], graph, stride, relu=stem,
                                       store=self.store)
         grads[0:3] = [dw, dg, db]
         h = graph[1]
@@ -249,14 +262,35 @@ class PetraNet:
 
     def __init__(self, params, names, stages: int, blocks_per_stage: int, eps=1e-5,
                  bn_momentum=0.1, dtype=np.float64, weight_view=None, store=None,
-                 use_inputs=False, use_params=False):
-        self.J = stages
+                 use_inputs=False, use_params=False, split_fronts=False):
+        """`stages` levels of the network (widths); with split_fronts every front
+        layer (stem or downsampling) and every reversible block is a stage of
+        its own, the last block also owning the head, as in the paper's
+        per-layer splits (Table 6, App. B): J = levels x (1 + blocks), and a
+        reversible stage below another one reconstructs from the reconstruction
+        that stage sends back."""
         self.use_inputs, self.use_params = use_inputs, use_params
         self.record: Optional[dict] = None   # (stage, micro-batch) -> parameter gradients
         self.stages = []
-        for j, (ps, ns) in enumerate(split_params(names, params, stages)):
-            self.stages.append(NetStage(ps, ns, j == 0, j == stages - 1, blocks_per_stage,
-                                        eps, bn_momentum, dtype, weight_view, store))
+        groups = split_params(names, params, stages)
+        for lv, (ps, ns) in enumerate(groups):
+            last = lv == stages - 1
+            if not split_fronts:
+                self.stages.append(NetStage(ps, ns, lv == 0, last, blocks_per_stage, eps,
+                                            bn_momentum, dtype, weight_view, store))
+                continue
+            fr = [i for i, nm in enumerate(ns) if ".stem" in nm or ".trans" in nm]
+            self.stages.append(NetStage([ps[i] for i in fr], [ns[i] for i in fr], lv == 0, False,
+                                        0, eps, bn_momentum, dtype, weight_view, store,
+                                        front="stem" if lv == 0 else "trans"))
+            for b in range(blocks_per_stage):
+                lb = last and b == blocks_per_stage - 1
+                sel = [i for i, nm in enumerate(ns)
+                       if f".b{b}." in nm or (lb and ".fc." in nm)]
+                self.stages.append(NetStage([ps[i] for i in sel], [ns[i] for i in sel], False, lb,
+                                            1, eps, bn_momentum, dtype, weight_view, store,
+                                            front=None))
+        self.J = len(self.stages)
         self.dtype = dtype
         self.fwd_msg: List[Optional[tuple]] = [None] * stages
         self.bwd_msg: List[Optional[tuple]] = [None] * stages
@@ -284,7 +318,8 @@ class PetraNet:
                     x1, x2 = np.asarray(images(m), self.dtype), None
                 else:
                     x1, x2 = self.fwd_msg[j - 1]
-                    st.buffer[m] = (x1, x2)
+                    if st.front:
+                        st.buffer[m] = (x1, x2)
                 y1, y2 = st.forward(x1, x2, m)
                 if st.last:
                     last_out = (y1, y2)
@@ -303,8 +338,10 @@ class PetraNet:
                     y1, y2, g1, g2 = self.bwd_msg[j + 1]
                 if j == 0:
                     bx1, bx2 = np.asarray(images(mb), self.dtype), None
-                else:
+                elif st.front:
                     bx1, bx2 = st.buffer.pop(mb)
+                else:
+                    bx1 = bx2 = None
                 dx, grads = st.backward(y1, y2, g1, g2, bx1, bx2, k, mb, self.use_inputs,
                                         self.use_params)
                 if st.last:
@@ -315,8 +352,11 @@ class PetraNet:
                 st.accumulate(grads, k)
                 did_bwd[j] = True
                 if j > 0:
-                    c = bx1.shape[-1]
-                    new_bwd[j] = (bx1, bx2, dx[..., :c], dx[..., c:])
+                    # a stage with a front sends back its buffered input, a
+                    # reversible one the block input it used (reconstructed)
+                    sx1, sx2 = (bx1, bx2) if st.front else st.last_used["u"]
+                    c = sx1.shape[-1]
+                    new_bwd[j] = (sx1, sx2, dx[..., :c], dx[..., c:])
             self.trace.append((t, j, m if 0 <= m < n_micro else None,
                                mb if 0 <= mb < n_micro else None))
         for j, st in enumerate(self.stages):

@@ -308,3 +308,80 @@ def test_probes_leave_the_schedule_untouched_and_agree_at_the_last_stage():
     # stage 0 has a delay of 2(J-1) ticks with updates in between: the variants differ
     s0 = net.stages[0].names
     assert max(np.abs(probes[(False, False)][nm] - probes[(True, True)][nm]).max() for nm in s0) > 0
+
+
+def test_split_fronts_tick_table_and_exact_backprop_when_frozen():
+    # Paper-style split (each stem/downsampling and each block its own stage):
+    # J = 8 for 4 levels of one block; delays 2(J-1-j); with theta
+    # frozen the accumulated gradients are exact backprop even though the
+    # reversible stages rebuild their inputs from the reconstructions sent by
+    # the stage above (Eq. 4).
+    names, params, _ = build(TINY)
+    net = PetraNet(params, names, 4, 1, split_fronts=True)
+    assert net.J == 8
+    assert [st.front for st in net.stages] == ["stem", None, "trans", None, "trans", None, "trans", None]
+    assert [st.blocks for st in net.stages] == [0, 1, 0, 1, 0, 1, 0, 1]
+    imgs, labs = data(TINY, 3)
+    J = net.J
+    K = 1000
+    for t in range(3 + 2 * J):
+        net.tick(t, lambda m: imgs[m], lambda m: labs[m], 3, 0.0, 0.9, 0.0, k=K)
+    fwd_at, bwd_at = {}, {}
+    for (t, j, m, mb) in net.trace:
+        if m is not None:
+            fwd_at[(j, m)] = t
+        if mb is not None:
+            bwd_at[(j, mb)] = t
+    for j in range(J):
+        for m in range(3):
+            assert bwd_at[(j, m)] - fwd_at[(j, m)] == 2 * (J - 1 - j)
+    assert all(not st.buffer for st in net.stages)
+    leaves = [torch.tensor(p, requires_grad=True) for p in params]
+    total = 0
+    for m in range(3):
+        total = total + Fn.cross_entropy(revnet(imgs[m], leaves, names, 4, 1),
+                                         torch.tensor(labs[m]).long())
+    total.backward()
+    got = {nm: a * K for st in net.stages for nm, a in zip(st.names, st.accum)}
+    assert set(got) == set(names)
+    for nm, leaf in zip(names, leaves):
+        ref = leaf.grad.numpy()
+        err = np.linalg.norm(got[nm] - ref)
+        assert err <= 1e-9 * np.linalg.norm(ref) + 1e-12, (nm, err)
+
+
+def test_split_fronts_reversible_stage_reconstructs_from_received_reconstruction():
+    # Two blocks per level, each its own stage (J = 12): with updates between
+    # forward and backward, a reversible stage's block input is the inverse,
+    # under its current parameters, of what the stage above sent back, and when
+    # that stage is reversible too, what it sent is its own reconstruction.
+    wl = TINY.with_(blocks_per_stage=2)
+    names, params, _ = build(wl)
+    net = PetraNet(params, names, 4, 2, split_fronts=True)
+    assert net.J == 12
+    net.record = {}
+    imgs, labs = data(wl, 4)
+    for t in range(4 + 2 * net.J):
+        net.tick(t, lambda m: imgs[m], lambda m: labs[m], 4, 0.05, 0.9, 5e-4)
+    from oracle import revblock
+    checked = chained = 0
+    for (j, m), r in net.record.items():
+        st = net.stages[j]
+        if st.front or st.last:
+            continue
+        above = net.stages[j + 1]
+        if above.front is None and (j + 1, m) in net.record:
+            # the stage above is reversible: it sent back the input it used
+            np.testing.assert_array_equal(r["y"][0], net.record[(j + 1, m)]["u"][0])
+            np.testing.assert_array_equal(r["y"][1], net.record[(j + 1, m)]["u"][1])
+            chained += 1
+        # forward of the used input under the parameters of the backward gives
+        # back the received output
+        v1, v2 = r["u"]
+        P = r["P"]
+        for b in range(st.blocks):
+            v1, v2 = revblock.block_forward(v1, v2, st._layers(b, 0, P), st._layers(b, 1, P), st.eps)
+        np.testing.assert_allclose(v1, r["y"][0], rtol=1e-9, atol=1e-10)
+        np.testing.assert_allclose(v2, r["y"][1], rtol=1e-9, atol=1e-10)
+        checked += 1
+    assert checked >= 12 and chained >= 4
