@@ -231,6 +231,24 @@ def bench_schedule(args):
     torch.cuda.synchronize()
     el_bp = time.perf_counter() - t0
     bp_loss = float(net.loss.item())
+    del net
+    # The paper's per-layer split of the same network (every stem/downsampling
+    # and every block its own stage): more, smaller stages in the pipeline.
+    snet = Net(wl.n, wl.h, wl.w, wl.c_img, wl.widths, wl.blocks_per_stage, wl.classes, wl.dtype,
+               device="cuda:0", split_stages=True)
+    snet.set_params(synth.net_params(wl))
+    snet.set_optimizer(wl.lr, wl.momentum, wl.weight_decay, wl.nesterov, wl.accum_k)
+    SJ = snet.n_stages
+    swarm = max(args.warmup, 2 * SJ - 1)
+    for t in range(swarm):
+        snet.tick(imgs[t % D], labs[t % D])
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for t in range(swarm, swarm + args.steps):
+        snet.tick(imgs[t % D], labs[t % D])
+    torch.cuda.synchronize()
+    el_split = time.perf_counter() - t0
+    split_loss = float(snet.loss.item())
     out = {"metric": "images/sec per stage step (fwd+reconstruct+VJP+update)",
            "value": wl.n * args.steps / el, "unit": "images/s", "n_gpus": 1,
            "steps": args.steps, "warmup": warm, "ms_per_step": el / args.steps * 1e3,
@@ -246,7 +264,14 @@ def bench_schedule(args):
                "unit": "images/s",
                "step": "one micro-batch: all stages' forwards, head, all stages' backwards "
                        "(blocks rebuilt from outputs) and updates, one stream",
-               "iteration_time_ratio": (el_bp / args.steps) / (el / args.steps)}}
+               "iteration_time_ratio": (el_bp / args.steps) / (el / args.steps)},
+           "split_stages": {
+               "stages": SJ, "ms_per_tick": el_split / args.steps * 1e3,
+               "value": wl.n * args.steps / el_split, "unit": "images/s",
+               "last_loss": split_loss,
+               "step": "one tick of the per-layer split (stem, downsamplings and blocks as "
+                       "stages, delays 2(J-1-j))"}}
+    out["outputs_finite"] = out["outputs_finite"] and bool(np.isfinite(split_loss))
     print(json.dumps(out))
 
 

@@ -247,12 +247,21 @@ typedef struct {
    * buffer, a weight stash).  0 = PETRA's setting (neither). */
   int32_t input_buffer;
   int32_t param_buffer;
+  /* 0: one stage per level (front layer + its blocks).  1: the paper's
+   * per-layer split (Table 6, App. B): every front layer (stem, downsampling)
+   * and every reversible block is a stage of its own, the last block also
+   * owning the head, so num_stages x (1 + blocks_per_stage) stages; a
+   * reversible stage below another one rebuilds its input from the
+   * reconstruction that stage sends back.  num_stages then counts levels. */
+  int32_t split_stages;
 } petra_net_desc;
 
 typedef struct petra_net petra_net;
 
 petra_status petra_net_create(const petra_net_desc* desc, petra_net** out);
 petra_status petra_net_destroy(petra_net* net);
+/* Number of stages of the schedule (num_stages, or the per-layer split's count). */
+petra_status petra_net_num_stages(const petra_net* net, int32_t* stages);
 /* Sizes as for a stage.  Parameter tensors in canonical order: per stage j,
  * the front conv weight (KRSC, [w_j][3][3][c_img] or [w_j][1][1][w_{j-1}]), its
  * BN gamma and beta, the reversible blocks' tensors in the stage order, and

@@ -59,7 +59,8 @@ class NetDesc(ctypes.Structure):
                 ("widths", ctypes.c_int32 * MAX_STAGES), ("blocks_per_stage", ctypes.c_int32),
                 ("classes", ctypes.c_int32), ("dtype", ctypes.c_int32),
                 ("bn_eps", ctypes.c_float), ("bn_momentum", ctypes.c_float),
-                ("input_buffer", ctypes.c_int32), ("param_buffer", ctypes.c_int32)]
+                ("input_buffer", ctypes.c_int32), ("param_buffer", ctypes.c_int32),
+                ("split_stages", ctypes.c_int32)]
 
 
 class NetMem(ctypes.Structure):
@@ -94,6 +95,7 @@ _SIGS = {
     "petra_stage_step": (ctypes.c_int, [_VP] * 14 + [ctypes.POINTER(ctypes.c_int32)]),
     "petra_net_create": (ctypes.c_int, [ctypes.POINTER(NetDesc), ctypes.POINTER(_VP)]),
     "petra_net_destroy": (ctypes.c_int, [_VP]),
+    "petra_net_num_stages": (ctypes.c_int, [_VP, ctypes.POINTER(ctypes.c_int32)]),
     "petra_net_query": (ctypes.c_int, [_VP, ctypes.POINTER(ctypes.c_int64),
                                         ctypes.POINTER(ctypes.c_int32),
                                         ctypes.POINTER(ctypes.c_int64),
@@ -327,6 +329,12 @@ def petra_net_tick(handle, images, labels, loss=None, stream=None) -> bool:
 def petra_net_backprop_step(handle, images, labels, loss=None, stream=None) -> None:
     _check(load().petra_net_backprop_step(handle, _ptr(images), _ptr(labels), _ptr(loss),
                                           _stream(stream)), "petra_net_backprop_step")
+
+
+def petra_net_num_stages(handle) -> int:
+    j = ctypes.c_int32()
+    _check(load().petra_net_num_stages(handle, ctypes.byref(j)), "petra_net_num_stages")
+    return j.value
 
 
 def petra_net_set_backward(handle, mode: int) -> None:

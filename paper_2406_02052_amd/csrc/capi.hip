@@ -404,8 +404,9 @@ petra_status petra_net_create(const petra_net_desc* d, petra_net** out) {
   if (d->blocks_per_stage * 4 > petra::MAX_WEIGHT_SEGS)
     return fail(PETRA_ERR_SHAPE, "too many blocks per stage");
   if ((d->input_buffer != 0 && d->input_buffer != 1) ||
-      (d->param_buffer != 0 && d->param_buffer != 1))
-    return fail(PETRA_ERR_INVALID_ARG, "input_buffer and param_buffer must be 0 or 1");
+      (d->param_buffer != 0 && d->param_buffer != 1) ||
+      (d->split_stages != 0 && d->split_stages != 1))
+    return fail(PETRA_ERR_INVALID_ARG, "input_buffer, param_buffer and split_stages must be 0 or 1");
   petra_net* h = new (std::nothrow) petra_net;
   if (h == nullptr) return fail(PETRA_ERR_INVALID_ARG, "host allocation failed");
   h->impl = new (std::nothrow) petra::Net(*d);
@@ -414,6 +415,13 @@ petra_status petra_net_create(const petra_net_desc* d, petra_net** out) {
     return fail(PETRA_ERR_INVALID_ARG, "host allocation failed");
   }
   *out = h;
+  return ok();
+}
+
+petra_status petra_net_num_stages(const petra_net* net, int32_t* stages) {
+  if (net == nullptr || net->impl == nullptr || stages == nullptr)
+    return fail(PETRA_ERR_INVALID_ARG, "null argument");
+  *stages = net->impl->J;
   return ok();
 }
 
@@ -470,6 +478,7 @@ petra_status petra_net_set_optimizer(petra_net* net, const petra_sgd* opt) {
     return fail(PETRA_ERR_INVALID_ARG, "need lr >= 0, 0 <= momentum < 1, weight_decay >= 0, accum_k >= 1");
   net->impl->opt = *opt;
   for (petra::NetStage& s : net->impl->st) {
+    if (!s.has_blocks) continue;
     s.blocks->opt = *opt;
     s.blocks->graphs.clear();
   }
@@ -506,7 +515,7 @@ petra_status petra_net_tick(petra_net* net, const void* images, const int32_t* l
   const bool wrote = s.tick(images, labels, loss, static_cast<hipStream_t>(stream));
   if (loss_written) *loss_written = wrote ? 1 : 0;
   for (petra::NetStage& ns : s.st)
-    if ((r = launch_status(*ns.blocks, "petra_net_tick"))) return r;
+    if (ns.has_blocks && (r = launch_status(*ns.blocks, "petra_net_tick"))) return r;
   return check_hip("petra_net_tick");
 }
 
@@ -586,7 +595,7 @@ petra_status petra_net_probe_tick(petra_net* net, int32_t mode, float* grad_out,
   if (e != hipSuccess) return fail(PETRA_ERR_HIP, std::string("stream setup: ") + hipGetErrorString(e));
   s.probe_tick(mode, grad_out, static_cast<hipStream_t>(stream));
   for (petra::NetStage& ns : s.st)
-    if ((r = launch_status(*ns.blocks, "petra_net_probe_tick"))) return r;
+    if (ns.has_blocks && (r = launch_status(*ns.blocks, "petra_net_probe_tick"))) return r;
   return check_hip("petra_net_probe_tick");
 }
 
@@ -605,7 +614,7 @@ petra_status petra_net_probe_backprop(petra_net* net, const void* images, const 
   if (e != hipSuccess) return fail(PETRA_ERR_HIP, std::string("stream setup: ") + hipGetErrorString(e));
   s.probe_backprop(images, labels, grad_out, static_cast<hipStream_t>(stream));
   for (petra::NetStage& ns : s.st)
-    if ((r = launch_status(*ns.blocks, "petra_net_probe_backprop"))) return r;
+    if (ns.has_blocks && (r = launch_status(*ns.blocks, "petra_net_probe_backprop"))) return r;
   return check_hip("petra_net_probe_backprop");
 }
 
@@ -626,7 +635,7 @@ petra_status petra_net_backprop_step(petra_net* net, const void* images, const i
   if (e != hipSuccess) return fail(PETRA_ERR_HIP, std::string("stream setup: ") + hipGetErrorString(e));
   s.backprop_step(images, labels, loss, static_cast<hipStream_t>(stream));
   for (petra::NetStage& ns : s.st)
-    if ((r = launch_status(*ns.blocks, "petra_net_backprop_step"))) return r;
+    if (ns.has_blocks && (r = launch_status(*ns.blocks, "petra_net_backprop_step"))) return r;
   return check_hip("petra_net_backprop_step");
 }
 

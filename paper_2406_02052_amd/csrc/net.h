@@ -24,7 +24,11 @@ enum { MEM_PARAMS = 0, MEM_WEIGHT_COPIES, MEM_ACTIVATION_BUFFER, MEM_INPUT_BUFFE
 
 struct NetStage {
   int j = 0;
+  int level = 0;                    // network level (width index) the stage belongs to
   bool first = false, last = false;
+  bool has_front = true;            // opens with the stem / a downsampling layer
+  bool has_blocks = true;           // holds reversible blocks
+  int fseg = -1;                    // its front weight in front_segs
   int H = 0, W = 0, C = 0;          // block resolution and full width
   int Hin = 0, Win = 0, Cin = 0;    // front input (Cin padded to 8 for the images)
   int cin_real = 0;                 // front input channels in the master weight
@@ -45,6 +49,11 @@ struct NetStage {
   size_t o_xr1 = 0, o_xr2 = 0, o_dx1 = 0, o_dx2 = 0;                      // block backward outputs
   size_t o_msg[2][2] = {{0, 0}, {0, 0}};   // gradient message to stage j-1 [parity][half]
   size_t o_y1 = 0, o_y2 = 0, o_g1 = 0, o_g2 = 0;                          // last stage
+  // stage without front: forward input by micro-batch parity, the input it
+  // reconstructs for stage j - 1 by tick parity, and the backprop pass's input
+  size_t o_fin[2][2] = {{0, 0}, {0, 0}};
+  size_t o_xmsg[2][2] = {{0, 0}, {0, 0}};
+  size_t o_bpin = 0;
   size_t o_pooled = 0, o_dlogits = 0, o_lossn = 0, o_labels = 0;
   size_t ring_slot_bytes = 0;
   // buffer variants (Table 4): per micro-batch in flight, the blocks' input
@@ -59,6 +68,7 @@ struct NetStage {
   hipStream_t sf = nullptr, sb = nullptr;
   hipEvent_t ev_f = nullptr, ev_b = nullptr;
   int64_t mem[MEM_COUNT] = {0, 0, 0, 0, 0, 0};
+  int64_t bwd_count = 0;            // backward passes (stages without blocks)
 };
 
 // Parameters a front layer's backward reads: the live ones or a stashed copy.
@@ -77,7 +87,7 @@ class Net {
   petra_net_desc desc;
   int dt;
   size_t esz;
-  int J;
+  int J;            // stages (levels, or levels x (1 + blocks) with split_stages)
   std::vector<NetStage> st;
   std::vector<petra_param_info> infos;
   int64_t n_params = 0, n_bnch = 0;
@@ -133,8 +143,16 @@ class Net {
   FrontView front_view(const NetStage& s) const;
   FrontView stash_front_view(const NetStage& s, int64_t m) const;
   void stash_params(NetStage& s, int64_t m, hipStream_t q);
+  // The stage's forward input for micro-batch m (m < 0: the backprop pass),
+  // where its output goes, and the output / output gradient its backward gets.
+  void* fwd_in(const NetStage& s, int64_t m, int half) const;
+  void* fwd_dest(const NetStage& s, int64_t m, int half) const;
+  const void* bwd_y(const NetStage& s, int64_t m, int parity, int half) const;
+  const void* bwd_g(const NetStage& s, int parity, int half) const;
+  // Forward of one stage (front, blocks); buffers: keep the variant buffers.
+  void stage_forward(NetStage& s, int64_t m, hipStream_t q, bool keep, bool buffers);
   void front_forward(NetStage& s, const void* in1, const void* in2, hipStream_t q,
-                     bool keep = false);
+                     bool keep = false, void* out1 = nullptr, void* out2 = nullptr);
   void front_backward(NetStage& s, const void* in1, const void* in2, const void* d1,
                       const void* d2, int parity, hipStream_t q, bool recompute = true,
                       const FrontView* fv = nullptr);
@@ -142,9 +160,11 @@ class Net {
   // its gradient (bg), in variant `mode`; the message goes to parity `parity`.
   void backward_stage(NetStage& s, int64_t mb, int mode, int parity, hipStream_t q,
                       const void* by1, const void* by2, const void* bg1, const void* bg2,
-                      hipStream_t side = nullptr);
+                      hipStream_t side = nullptr, bool recompute = true);
   void backprop_pass(const void* images, const int32_t* labels, float* loss, bool update,
                      hipStream_t q);
+  // count one backward of the stage; does its update fire now?
+  bool count_and_due(NetStage& s);
   struct Redirect;
   void head(NetStage& s, const void* y1, const void* y2, const int32_t* labels, float* loss,
             hipStream_t q);

@@ -24,34 +24,59 @@ size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 Net::Net(const petra_net_desc& d) : desc(d) {
   dt = d.dtype == PETRA_BF16 ? DT_BF16 : DT_FP32;
   esz = dt == DT_BF16 ? 2 : 4;
-  J = d.num_stages;
+  // stage list: one per level, or the per-layer split
+  struct Spec { int level; bool front; int nblocks; };
+  std::vector<Spec> specs;
+  for (int l = 0; l < d.num_stages; ++l) {
+    if (!d.split_stages) {
+      specs.push_back({l, true, d.blocks_per_stage});
+      continue;
+    }
+    specs.push_back({l, true, 0});
+    for (int b = 0; b < d.blocks_per_stage; ++b) specs.push_back({l, false, 1});
+  }
+  J = static_cast<int>(specs.size());
   st.resize(J);
   const int k = d.classes;
   int64_t off = 0, run = 0;
+  int nfront = 0;
   for (int j = 0; j < J; ++j) {
     NetStage& s = st[j];
+    const Spec& sp = specs[j];
     s.j = j;
+    s.level = sp.level;
+    s.has_front = sp.front;
+    s.has_blocks = sp.nblocks > 0;
     s.first = j == 0;
     s.last = j == J - 1;
-    s.C = d.widths[j];
-    s.H = d.h >> j;
-    s.W = d.w >> j;
-    if (s.first) {
+    const int l = sp.level;
+    s.C = d.widths[l];
+    s.H = d.h >> l;
+    s.W = d.w >> l;
+    if (s.has_front && l == 0) {
       s.Hin = d.h; s.Win = d.w; s.Cin = 8; s.cin_real = d.c_img; s.R = 3; s.stride = 1; s.pad = 1;
+    } else if (s.has_front) {
+      s.Hin = d.h >> (l - 1); s.Win = d.w >> (l - 1); s.Cin = d.widths[l - 1];
+      s.cin_real = s.Cin; s.R = 1; s.stride = 2; s.pad = 0;
     } else {
-      s.Hin = st[j - 1].H; s.Win = st[j - 1].W; s.Cin = st[j - 1].C; s.cin_real = s.Cin;
-      s.R = 1; s.stride = 2; s.pad = 0;
+      s.Hin = s.H; s.Win = s.W; s.Cin = s.C; s.cin_real = s.C; s.R = 0; s.stride = 1; s.pad = 0;
     }
+    if (s.has_front) s.fseg = nfront++;
     s.M = static_cast<long>(d.n) * s.H * s.W;
     s.Min = static_cast<long>(d.n) * s.Hin * s.Win;
-    petra_stage_desc sd{};
-    sd.n = d.n; sd.h = s.H; sd.w = s.W; sd.c_half = s.C / 2; sd.c_mid = 0;
-    sd.num_blocks = d.blocks_per_stage; sd.kind = PETRA_BLOCK_BASIC; sd.dtype = d.dtype;
-    sd.bn_eps = d.bn_eps; sd.bn_momentum = d.bn_momentum;
-    s.blocks.reset(new Stage(sd));
+    if (s.has_blocks) {
+      petra_stage_desc sd{};
+      sd.n = d.n; sd.h = s.H; sd.w = s.W; sd.c_half = s.C / 2; sd.c_mid = 0;
+      sd.num_blocks = sp.nblocks; sd.kind = PETRA_BLOCK_BASIC; sd.dtype = d.dtype;
+      sd.bn_eps = d.bn_eps; sd.bn_momentum = d.bn_momentum;
+      s.blocks.reset(new Stage(sd));
+    }
+    const int64_t blk_params = s.has_blocks ? s.blocks->n_params : 0;
+    const int64_t blk_bnch = s.has_blocks ? s.blocks->n_bnch : 0;
+    const int cf = s.has_front ? s.C : 0;
     // flat layout: [front w][fc w] (decayed) [blocks] [front gamma][front beta][fc b]
     s.off_front_w = off;
-    s.n_front_w = static_cast<int64_t>(s.C) * s.R * s.R * s.cin_real;
+    s.n_front_w = s.has_front ? static_cast<int64_t>(s.C) * s.R * s.R * s.cin_real : 0;
     off += s.n_front_w;
     s.off_fc_w = off;
     s.n_fc_w = s.last ? static_cast<int64_t>(k) * s.C : 0;
@@ -59,37 +84,41 @@ Net::Net(const petra_net_desc& d) : desc(d) {
     s.off_decay = s.off_front_w;
     s.n_decay = s.n_front_w + s.n_fc_w;
     s.off_blocks = off;
-    off += s.blocks->n_params;
+    off += blk_params;
     s.off_front_g = off;
-    s.off_front_b = off + s.C;
-    off += 2 * s.C;
+    s.off_front_b = off + cf;
+    off += 2 * cf;
     s.off_fc_b = off;
     off += s.last ? k : 0;
     s.off_plain = s.off_front_g;
     s.n_plain = off - s.off_front_g;
     s.n_span = off - s.off_front_w;
     s.run_front = run;
-    run += s.C;
+    run += cf;
     s.run_blocks = run;
-    run += s.blocks->n_bnch;
+    run += blk_bnch;
 
     // canonical parameter order
-    petra_param_info wi{};
-    wi.offset = s.off_front_w; wi.numel = s.n_front_w; wi.role = PETRA_ROLE_CONV_WEIGHT; wi.ndim = 4;
-    wi.shape[0] = s.C; wi.shape[1] = s.R; wi.shape[2] = s.R; wi.shape[3] = s.cin_real;
-    wi.weight_decay = 1; wi.bn_index = -1;
-    infos.push_back(wi);
-    petra_param_info gi{};
-    gi.offset = s.off_front_g; gi.numel = s.C; gi.role = PETRA_ROLE_BN_GAMMA; gi.ndim = 1;
-    gi.shape[0] = s.C; gi.weight_decay = 0; gi.bn_index = -1;
-    infos.push_back(gi);
-    petra_param_info bi = gi;
-    bi.offset = s.off_front_b; bi.role = PETRA_ROLE_BN_BETA;
-    infos.push_back(bi);
-    for (petra_param_info p : s.blocks->infos) {
-      p.offset += s.off_blocks;
-      p.bn_index = -1;
-      infos.push_back(p);
+    if (s.has_front) {
+      petra_param_info wi{};
+      wi.offset = s.off_front_w; wi.numel = s.n_front_w; wi.role = PETRA_ROLE_CONV_WEIGHT;
+      wi.ndim = 4; wi.shape[0] = s.C; wi.shape[1] = s.R; wi.shape[2] = s.R; wi.shape[3] = s.cin_real;
+      wi.weight_decay = 1; wi.bn_index = -1;
+      infos.push_back(wi);
+      petra_param_info gi{};
+      gi.offset = s.off_front_g; gi.numel = s.C; gi.role = PETRA_ROLE_BN_GAMMA; gi.ndim = 1;
+      gi.shape[0] = s.C; gi.weight_decay = 0; gi.bn_index = -1;
+      infos.push_back(gi);
+      petra_param_info bi = gi;
+      bi.offset = s.off_front_b; bi.role = PETRA_ROLE_BN_BETA;
+      infos.push_back(bi);
+    }
+    if (s.has_blocks) {
+      for (petra_param_info p : s.blocks->infos) {
+        p.offset += s.off_blocks;
+        p.bn_index = -1;
+        infos.push_back(p);
+      }
     }
     if (s.last) {
       petra_param_info fw{};
@@ -107,10 +136,10 @@ Net::Net(const petra_net_desc& d) : desc(d) {
 
   // front weight copies
   int64_t fw_off = 0, dg_off = 0;
-  front_segs.nseg = J;
-  for (int j = 0; j < J; ++j) {
-    NetStage& s = st[j];
-    front_segs.seg[j] = WeightSeg{s.off_front_w, fw_off, dg_off, s.C, s.R, s.R, s.cin_real, s.Cin};
+  front_segs.nseg = nfront;
+  for (NetStage& s : st) {
+    if (!s.has_front) continue;
+    front_segs.seg[s.fseg] = WeightSeg{s.off_front_w, fw_off, dg_off, s.C, s.R, s.R, s.cin_real, s.Cin};
     const int64_t padded = static_cast<int64_t>(s.C) * s.R * s.R * s.Cin;
     front_max_numel = std::max(front_max_numel, padded);
     fw_off += padded;
@@ -134,24 +163,30 @@ Net::Net(const petra_net_desc& d) : desc(d) {
     NetStage& s = st[j];
     const size_t act = static_cast<size_t>(s.M) * s.C * esz;   // full-width block activation
     const size_t half = act / 2;
-    s.mem[MEM_WEIGHT_COPIES] += static_cast<int64_t>(
-        (static_cast<size_t>(s.C) * s.R * s.R * s.Cin + s.n_front_w) * esz +
-        2 * align_up(static_cast<size_t>(s.blocks->n_conv) * esz, 256));
-    s.mem[MEM_SCRATCH] -= static_cast<int64_t>(2 * align_up(static_cast<size_t>(s.blocks->n_conv) * esz, 256));
+    const size_t bconv = s.has_blocks ? align_up(static_cast<size_t>(s.blocks->n_conv) * esz, 256) : 0;
+    const size_t fpad = s.has_front ? static_cast<size_t>(s.C) * s.R * s.R * s.Cin : 0;
+    s.mem[MEM_WEIGHT_COPIES] += static_cast<int64_t>((fpad + s.n_front_w) * esz + 2 * bconv);
+    s.mem[MEM_SCRATCH] -= static_cast<int64_t>(2 * bconv);
     cur = &s.mem[MEM_SCRATCH];
-    s.o_blocks_ws = take(s.blocks->ws_need);
-    s.ring_depth = s.first ? 2 * J - 1 : 2 * (J - j) + 1;
-    s.ring_slot_bytes = align_up(static_cast<size_t>(s.Min) * s.Cin * esz, 256);
-    cur = &s.mem[MEM_ACTIVATION_BUFFER];
-    s.o_ring = take(s.ring_slot_bytes * (s.ring_depth + 1));   // + the backprop pass's slot
-    s.mem[MEM_ACTIVATION_BUFFER] -= static_cast<int64_t>(s.ring_slot_bytes);
-    s.mem[MEM_SCRATCH] += static_cast<int64_t>(s.ring_slot_bytes);
-    cur = &s.mem[MEM_SCRATCH];
+    if (s.has_blocks) s.o_blocks_ws = take(s.blocks->ws_need);
+    if (s.has_front) {
+      s.ring_depth = s.first ? 2 * J - 1 : 2 * (J - j) + 1;
+      s.ring_slot_bytes = align_up(static_cast<size_t>(s.Min) * s.Cin * esz, 256);
+      cur = &s.mem[MEM_ACTIVATION_BUFFER];
+      s.o_ring = take(s.ring_slot_bytes * (s.ring_depth + 1));   // + the backprop pass's slot
+      s.mem[MEM_ACTIVATION_BUFFER] -= static_cast<int64_t>(s.ring_slot_bytes);
+      s.mem[MEM_SCRATCH] += static_cast<int64_t>(s.ring_slot_bytes);
+      cur = &s.mem[MEM_SCRATCH];
+    } else {
+      for (int p = 0; p < 2; ++p)
+        for (int h = 0; h < 2; ++h) s.o_fin[p][h] = take(half);
+      s.o_bpin = take(act);
+    }
     if (!s.last && (d.input_buffer || d.param_buffer)) {
       // micro-batch m is kept from its forward (tick m + j) to its backward
       // (tick m + 2J - 2 - j)
       s.buf_depth = 2 * (J - 1 - j) + 1;
-      if (d.input_buffer) {
+      if (d.input_buffer && s.has_blocks) {
         s.ib_slot_bytes = align_up(act, 256);
         cur = &s.mem[MEM_INPUT_BUFFER];
         s.o_ib = take(s.ib_slot_bytes * s.buf_depth);
@@ -160,11 +195,11 @@ Net::Net(const petra_net_desc& d) : desc(d) {
       if (d.param_buffer) {
         size_t q = align_up(static_cast<size_t>(s.n_span) * sizeof(float), 256);
         s.ps_bwf = q;
-        q += align_up(static_cast<size_t>(s.blocks->n_conv) * esz, 256);
+        q += bconv;
         s.ps_bwd = q;
-        q += align_up(static_cast<size_t>(s.blocks->n_conv) * esz, 256);
+        q += bconv;
         s.ps_fwf = q;
-        q += align_up(static_cast<size_t>(s.C) * s.R * s.R * s.Cin * esz, 256);
+        q += align_up(fpad * esz, 256);
         s.ps_fwd = q;
         q += align_up(static_cast<size_t>(s.n_front_w) * esz, 256);
         s.ps_slot_bytes = q;
@@ -172,11 +207,14 @@ Net::Net(const petra_net_desc& d) : desc(d) {
         s.o_ps = take(s.ps_slot_bytes * s.buf_depth);
         cur = &s.mem[MEM_SCRATCH];
       }
-      s.o_rx1 = take(half);
-      s.o_rx2 = take(half);
-      s.o_ry1 = take(half);
-      s.o_ry2 = take(half);
+      if (s.has_blocks) {
+        s.o_rx1 = take(half);
+        s.o_rx2 = take(half);
+        s.o_ry1 = take(half);
+        s.o_ry2 = take(half);
+      }
     }
+    if (s.has_front) {
     // conv args of the front layer, for tile counts and weight-gradient splits
     ConvArgs f{};
     f.n = d.n; f.h = s.Hin; f.w = s.Win; f.c_in = s.Cin; f.p = s.H; f.q = s.W; f.c_out = s.C;
@@ -210,14 +248,20 @@ Net::Net(const petra_net_desc& d) : desc(d) {
       s.o_wpart = take(static_cast<size_t>(s.wsplits) * s.C * ktot * sizeof(float));
     }
     s.o_dtmp = s.first ? 0 : take(static_cast<size_t>(s.M) * s.Cin * esz);
-    s.o_xr1 = take(half);
-    s.o_xr2 = take(half);
-    s.o_dx1 = take(half);
-    s.o_dx2 = take(half);
+    }  // front scratch
+    if (s.has_blocks) {
+      s.o_xr1 = take(half);
+      s.o_xr2 = take(half);
+      s.o_dx1 = take(half);
+      s.o_dx2 = take(half);
+    }
     if (!s.first) {
       const size_t in_half = static_cast<size_t>(s.Min) * (s.Cin / 2) * esz;
       for (int p = 0; p < 2; ++p)
         for (int h = 0; h < 2; ++h) s.o_msg[p][h] = take(in_half);
+      if (!s.has_front)
+        for (int p = 0; p < 2; ++p)
+          for (int h = 0; h < 2; ++h) s.o_xmsg[p][h] = take(in_half);
     }
     if (s.last) {
       s.o_y1 = take(half);
@@ -239,7 +283,8 @@ Net::Net(const petra_net_desc& d) : desc(d) {
   int64_t counted = 0;
   for (NetStage& s : st) {
     s.mem[MEM_PARAMS] = 3 * s.n_span * static_cast<int64_t>(sizeof(float)) +
-                        2 * (s.C + s.blocks->n_bnch) * static_cast<int64_t>(sizeof(float));
+                        2 * ((s.has_front ? s.C : 0) + (s.has_blocks ? s.blocks->n_bnch : 0)) *
+                            static_cast<int64_t>(sizeof(float));
     for (int c = MEM_WEIGHT_COPIES; c < MEM_COUNT; ++c) counted += s.mem[c];
   }
   st[0].mem[MEM_SCRATCH] += static_cast<int64_t>(ws_need) - counted;
@@ -260,6 +305,7 @@ void Net::bind(float* th, float* gr, float* mo, float* rm, float* rv, void* w) {
   theta = th; grad = gr; mom = mo; rmean = rm; rvar = rv;
   ws = static_cast<char*>(w);
   for (NetStage& s : st) {
+    if (!s.has_blocks) continue;
     s.blocks->bind(th + s.off_blocks, gr + s.off_blocks, mo + s.off_blocks, rm + s.run_blocks,
                    rv + s.run_blocks, ws + s.o_blocks_ws);
     s.blocks->opt = opt;
@@ -275,14 +321,15 @@ hipError_t Net::ensure_streams() {
     if ((e = hipStreamCreateWithFlags(&s.sb, hipStreamNonBlocking)) != hipSuccess) return e;
     if ((e = hipEventCreateWithFlags(&s.ev_f, hipEventDisableTiming)) != hipSuccess) return e;
     if ((e = hipEventCreateWithFlags(&s.ev_b, hipEventDisableTiming)) != hipSuccess) return e;
-    if ((e = s.blocks->ensure_streams()) != hipSuccess) return e;
+    if (s.has_blocks && (e = s.blocks->ensure_streams()) != hipSuccess) return e;
   }
   return hipSuccess;
 }
 
 void Net::sync_weights(hipStream_t q) {
   refresh_weights(dt, theta, front_segs, front_max_numel, ws + o_front_wfwd, ws + o_front_wdg, q);
-  for (NetStage& s : st) s.blocks->sync_weights(q);
+  for (NetStage& s : st)
+    if (s.has_blocks) s.blocks->sync_weights(q);
 }
 
 void* Net::ring_slot(const NetStage& s, int64_t m, int half) const {
@@ -301,8 +348,33 @@ char* Net::ps_slot(const NetStage& s, int64_t m) const {
   return ws + s.o_ps + static_cast<size_t>(m % s.buf_depth) * s.ps_slot_bytes;
 }
 
+void* Net::fwd_in(const NetStage& s, int64_t m, int half) const {
+  if (s.has_front) return ring_slot(s, m, half);
+  const size_t hb = static_cast<size_t>(s.M) * (s.C / 2) * esz;
+  if (m < 0) return ws + s.o_bpin + (half ? hb : 0);
+  return ws + s.o_fin[m & 1][half];
+}
+
+void* Net::fwd_dest(const NetStage& s, int64_t m, int half) const {
+  if (s.last) return ws + (half ? s.o_y2 : s.o_y1);
+  return fwd_in(st[s.j + 1], m, half);
+}
+
+// y for stage j's backward: the next stage's buffered input (a front), the
+// reconstruction the next (reversible) stage sent back, or in the backprop
+// pass (m < 0) the exact input the forward left.
+const void* Net::bwd_y(const NetStage& s, int64_t m, int parity, int half) const {
+  const NetStage& nx = st[s.j + 1];
+  if (nx.has_front || m < 0) return fwd_in(nx, m, half);
+  return ws + nx.o_xmsg[parity][half];
+}
+
+const void* Net::bwd_g(const NetStage& s, int parity, int half) const {
+  return ws + st[s.j + 1].o_msg[parity][half];
+}
+
 FrontView Net::front_view(const NetStage& s) const {
-  const WeightSeg& g = front_segs.seg[s.j];
+  const WeightSeg& g = front_segs.seg[s.fseg];
   return FrontView{ws + o_front_wfwd + g.fwd_off * esz, ws + o_front_wdg + g.dg_off * esz,
                    theta + s.off_front_g, theta + s.off_front_b};
 }
@@ -318,28 +390,33 @@ FrontView Net::stash_front_view(const NetStage& s, int64_t m) const {
 // (fp32 parameters and the compute copies), ahead of it on its stream.
 void Net::stash_params(NetStage& s, int64_t m, hipStream_t q) {
   char* b = ps_slot(s, m);
-  const FrontView f = front_view(s);
-  const Stage& blk = *s.blocks;
-  const size_t cw = static_cast<size_t>(blk.n_conv) * esz;
   (void)hipMemcpyAsync(b, theta + s.off_front_w, static_cast<size_t>(s.n_span) * sizeof(float),
                        hipMemcpyDeviceToDevice, q);
-  (void)hipMemcpyAsync(b + s.ps_bwf, blk.wfwd, cw, hipMemcpyDeviceToDevice, q);
-  (void)hipMemcpyAsync(b + s.ps_bwd, blk.wdg, cw, hipMemcpyDeviceToDevice, q);
-  (void)hipMemcpyAsync(b + s.ps_fwf, f.wf, static_cast<size_t>(s.C) * s.R * s.R * s.Cin * esz,
-                       hipMemcpyDeviceToDevice, q);
-  (void)hipMemcpyAsync(b + s.ps_fwd, f.wd, static_cast<size_t>(s.n_front_w) * esz,
-                       hipMemcpyDeviceToDevice, q);
+  if (s.has_blocks) {
+    const Stage& blk = *s.blocks;
+    const size_t cw = static_cast<size_t>(blk.n_conv) * esz;
+    (void)hipMemcpyAsync(b + s.ps_bwf, blk.wfwd, cw, hipMemcpyDeviceToDevice, q);
+    (void)hipMemcpyAsync(b + s.ps_bwd, blk.wdg, cw, hipMemcpyDeviceToDevice, q);
+  }
+  if (s.has_front) {
+    const FrontView f = front_view(s);
+    (void)hipMemcpyAsync(b + s.ps_fwf, f.wf, static_cast<size_t>(s.C) * s.R * s.R * s.Cin * esz,
+                         hipMemcpyDeviceToDevice, q);
+    (void)hipMemcpyAsync(b + s.ps_fwd, f.wd, static_cast<size_t>(s.n_front_w) * esz,
+                         hipMemcpyDeviceToDevice, q);
+  }
 }
 
 // Front conv + BN (+ ReLU on the images) into the two half-tensors the blocks read.
 // keep: the conv output and its BN vectors go to the backward's buffers (and move
 // the running statistics) so that front_backward can skip the recompute.
-void Net::front_forward(NetStage& s, const void* in1, const void* in2, hipStream_t q, bool keep) {
+void Net::front_forward(NetStage& s, const void* in1, const void* in2, hipStream_t q, bool keep,
+                        void* out1, void* out2) {
   ConvArgs a{};
   a.src = in1;
   a.src2 = in2;
   a.c_split = in2 ? s.Cin / 2 : s.Cin;
-  a.wt = ws + o_front_wfwd + front_segs.seg[s.j].fwd_off * esz;
+  a.wt = ws + o_front_wfwd + front_segs.seg[s.fseg].fwd_off * esz;
   a.out = ws + (keep ? s.o_bh : s.o_fh);
   a.partials = at<float>(keep ? s.o_bpart : s.o_fpart);
   a.n = desc.n; a.h = s.Hin; a.w = s.Win; a.c_in = s.Cin; a.p = s.H; a.q = s.W; a.c_out = s.C;
@@ -351,7 +428,37 @@ void Net::front_forward(NetStage& s, const void* in1, const void* in2, hipStream
                     theta + s.off_front_g, theta + s.off_front_b, desc.bn_eps, v, v + s.C,
                     v + 2 * s.C, v + 3 * s.C, keep ? rmean + s.run_front : nullptr,
                     keep ? rvar + s.run_front : nullptr, desc.bn_momentum, q);
-  bn_apply_split(dt, a.out, v, v + s.C, s.first ? 1 : 0, ws + s.o_fx1, ws + s.o_fx2, s.M, s.C, q);
+  bn_apply_split(dt, a.out, v, v + s.C, s.first ? 1 : 0, out1 ? out1 : ws + s.o_fx1,
+                 out2 ? out2 : ws + s.o_fx2, s.M, s.C, q);
+}
+
+void Net::stage_forward(NetStage& s, int64_t m, hipStream_t q, bool keep, bool buffers) {
+  const void* in1 = fwd_in(s, m, 0);
+  const void* in2 = s.first ? nullptr : fwd_in(s, m, 1);
+  if (buffers && s.ps_slot_bytes) stash_params(s, m, q);
+  const void* b1 = in1;   // the blocks' input
+  const void* b2 = in2;
+  if (s.has_front) {
+    void* f1 = s.has_blocks ? ws + s.o_fx1 : fwd_dest(s, m, 0);
+    void* f2 = s.has_blocks ? ws + s.o_fx2 : fwd_dest(s, m, 1);
+    front_forward(s, in1, in2, q, keep, f1, f2);
+    b1 = f1;
+    b2 = f2;
+  }
+  if (!s.has_blocks) return;
+  if (buffers && s.ib_slot_bytes) {
+    const size_t hb = static_cast<size_t>(s.M) * (s.C / 2) * esz;
+    (void)hipMemcpyAsync(ib_slot(s, m, 0), b1, hb, hipMemcpyDeviceToDevice, q);
+    (void)hipMemcpyAsync(ib_slot(s, m, 1), b2, hb, hipMemcpyDeviceToDevice, q);
+  }
+  Stage& blk = *s.blocks;
+  void* y1 = fwd_dest(s, m, 0);
+  void* y2 = fwd_dest(s, m, 1);
+  if (blk.use_graphs)
+    (void)blk.graphs.run({1, reinterpret_cast<uintptr_t>(b1), reinterpret_cast<uintptr_t>(y1)}, q,
+                         [&](hipStream_t c) { blk.forward(b1, b2, y1, y2, c); }, 0);
+  else
+    blk.forward(b1, b2, y1, y2, q);
 }
 
 // Recompute the front layer from its buffered input (unless recompute is false:
@@ -429,14 +536,17 @@ void Net::front_backward(NetStage& s, const void* in1, const void* in2, const vo
 }
 
 void Net::stage_update(NetStage& s, hipStream_t q) {
-  sgd_update(theta + s.off_decay, grad + s.off_decay, mom + s.off_decay, s.n_decay, s.n_decay,
-             opt.lr, opt.momentum, opt.weight_decay, opt.nesterov, q);
-  s.blocks->update_kernels(q);
-  sgd_update(theta + s.off_plain, grad + s.off_plain, mom + s.off_plain, s.n_plain, 0, opt.lr,
-             opt.momentum, opt.weight_decay, opt.nesterov, q);
+  if (s.n_decay)
+    sgd_update(theta + s.off_decay, grad + s.off_decay, mom + s.off_decay, s.n_decay, s.n_decay,
+               opt.lr, opt.momentum, opt.weight_decay, opt.nesterov, q);
+  if (s.has_blocks) s.blocks->update_kernels(q);
+  if (s.n_plain)
+    sgd_update(theta + s.off_plain, grad + s.off_plain, mom + s.off_plain, s.n_plain, 0, opt.lr,
+               opt.momentum, opt.weight_decay, opt.nesterov, q);
+  if (!s.has_front) return;
   WeightSegTable one{};
   one.nseg = 1;
-  one.seg[0] = front_segs.seg[s.j];
+  one.seg[0] = front_segs.seg[s.fseg];
   refresh_weights(dt, theta, one, static_cast<int64_t>(s.C) * s.R * s.R * s.Cin, ws + o_front_wfwd,
                   ws + o_front_wdg, q);
 }
@@ -471,6 +581,7 @@ struct Net::Redirect {
     n.rvar = sink + n.n_bnch;
     n.opt.accum_k = 1;
     for (NetStage& s : n.st) {
+      if (!s.has_blocks) continue;
       s.blocks->grad = gout + s.off_blocks;
       s.blocks->rmean = sink + s.run_blocks;
       s.blocks->rvar = sink + n.n_bnch + s.run_blocks;
@@ -483,6 +594,7 @@ struct Net::Redirect {
     n.rvar = rv;
     n.opt.accum_k = k;
     for (NetStage& s : n.st) {
+      if (!s.has_blocks) continue;
       s.blocks->grad = g + s.off_blocks;
       s.blocks->rmean = rm + s.run_blocks;
       s.blocks->rvar = rv + s.run_blocks;
@@ -493,51 +605,62 @@ struct Net::Redirect {
 
 void Net::backward_stage(NetStage& s, int64_t mb, int mode, int parity, hipStream_t q,
                          const void* by1, const void* by2, const void* bg1, const void* bg2,
-                         hipStream_t side) {
-  Stage& blk = *s.blocks;
-  void* xr1 = ws + s.o_xr1;
-  void* xr2 = ws + s.o_xr2;
-  void* dx1 = ws + s.o_dx1;
-  void* dx2 = ws + s.o_dx2;
-  FrontView fv = front_view(s);
-  if (mode == 0) {
-    // PETRA: reconstruct the blocks' input from their output with the current
-    // parameters and take the VJP there
-    if (blk.use_graphs)
-      (void)blk.graphs.run({2, reinterpret_cast<uintptr_t>(by1), reinterpret_cast<uintptr_t>(bg1)}, q,
-                           [&](hipStream_t c) { blk.backward(by1, by2, bg1, bg2, xr1, xr2, dx1, dx2, c); },
-                           1);
-    else
-      blk.backward(by1, by2, bg1, bg2, xr1, xr2, dx1, dx2, q, side);
-  } else {
-    // Variants: the VJP at the stored input (bit 0) or at the input
-    // reconstructed with the current parameters, with the stashed parameters
-    // (bit 1) or the current ones.  The blocks' output at that point is
-    // recomputed, and the reversible backward runs from it.
-    const void* u1 = ib_slot(s, mb, 0);
-    const void* u2 = ib_slot(s, mb, 1);
-    if (!(mode & 1)) {
-      blk.reconstruct(by1, by2, ws + s.o_rx1, ws + s.o_rx2, q);
-      u1 = ws + s.o_rx1;
-      u2 = ws + s.o_rx2;
+                         hipStream_t side, bool recompute) {
+  FrontView fv = s.has_front ? front_view(s) : FrontView{};
+  const void* d1 = bg1;   // gradient of the front layer's output
+  const void* d2 = bg2;
+  if (s.has_blocks) {
+    Stage& blk = *s.blocks;
+    // a stage without front sends its reconstructed input and its input
+    // gradient straight to stage j - 1
+    void* xr1 = ws + (s.has_front ? s.o_xr1 : s.o_xmsg[parity][0]);
+    void* xr2 = ws + (s.has_front ? s.o_xr2 : s.o_xmsg[parity][1]);
+    void* dx1 = ws + (s.has_front ? s.o_dx1 : s.o_msg[parity][0]);
+    void* dx2 = ws + (s.has_front ? s.o_dx2 : s.o_msg[parity][1]);
+    if (mode == 0) {
+      // PETRA: reconstruct the blocks' input from their output with the current
+      // parameters and take the VJP there
+      if (blk.use_graphs)
+        (void)blk.graphs.run({2, reinterpret_cast<uintptr_t>(by1), reinterpret_cast<uintptr_t>(bg1)}, q,
+                             [&](hipStream_t c) { blk.backward(by1, by2, bg1, bg2, xr1, xr2, dx1, dx2, c); },
+                             1);
+      else
+        blk.backward(by1, by2, bg1, bg2, xr1, xr2, dx1, dx2, q, side);
+    } else {
+      // Variants: the VJP at the stored input (bit 0) or at the input
+      // reconstructed with the current parameters, with the stashed parameters
+      // (bit 1) or the current ones.  The blocks' output at that point is
+      // recomputed, and the reversible backward runs from it.
+      const void* u1 = s.ib_slot_bytes ? ib_slot(s, mb, 0) : nullptr;
+      const void* u2 = s.ib_slot_bytes ? ib_slot(s, mb, 1) : nullptr;
+      if (!(mode & 1)) {
+        blk.reconstruct(by1, by2, ws + s.o_rx1, ws + s.o_rx2, q);
+        u1 = ws + s.o_rx1;
+        u2 = ws + s.o_rx2;
+      }
+      if (mode & 2) {
+        char* b = ps_slot(s, mb);
+        blk.set_view(reinterpret_cast<const float*>(b) + (s.off_blocks - s.off_front_w),
+                     b + s.ps_bwf, b + s.ps_bwd);
+        if (s.has_front) fv = stash_front_view(s, mb);
+      }
+      blk.forward_with(u1, u2, ws + s.o_ry1, ws + s.o_ry2, blk.sb[0], q);
+      blk.backward(ws + s.o_ry1, ws + s.o_ry2, bg1, bg2, xr1, xr2, dx1, dx2, q);
+      blk.reset_view();
     }
-    if (mode & 2) {
-      char* b = ps_slot(s, mb);
-      blk.set_view(reinterpret_cast<const float*>(b) + (s.off_blocks - s.off_front_w),
-                   b + s.ps_bwf, b + s.ps_bwd);
-      fv = stash_front_view(s, mb);
-    }
-    blk.forward_with(u1, u2, ws + s.o_ry1, ws + s.o_ry2, blk.sb[0], q);
-    blk.backward(ws + s.o_ry1, ws + s.o_ry2, bg1, bg2, xr1, xr2, dx1, dx2, q);
-    blk.reset_view();
+    d1 = dx1;
+    d2 = dx2;
+  } else if (mode & 2) {
+    fv = stash_front_view(s, mb);
   }
+  if (!s.has_front) return;
   const void* in1 = ring_slot(s, mb, 0);
   const void* in2 = s.first ? nullptr : ring_slot(s, mb, 1);
-  front_backward(s, in1, in2, dx1, dx2, parity, q, true, &fv);
+  front_backward(s, in1, in2, d1, d2, parity, q, recompute, &fv);
 }
 
 // The reversible-backpropagation pass over one micro-batch on stream q, on the
-// extra input-ring slot of every stage, the extra label slot and the message
+// extra input slot of every stage, the extra label slot and the message
 // parity the next tick does not read.
 void Net::backprop_pass(const void* images, const int32_t* labels, float* loss, bool update,
                         hipStream_t q) {
@@ -546,37 +669,24 @@ void Net::backprop_pass(const void* images, const int32_t* labels, float* loss, 
   int32_t* lab = at<int32_t>(s0.o_labels) + static_cast<size_t>(J) * desc.n;
   pad_channels8(dt, images, desc.c_img, ring_slot(s0, -1, 0), s0.Min, q);
   copy_i32(labels, lab, desc.n, q);
-  for (NetStage& s : st) {
-    const void* in1 = ring_slot(s, -1, 0);
-    const void* in2 = s.first ? nullptr : ring_slot(s, -1, 1);
-    front_forward(s, in1, in2, q, /*keep=*/true);
-    void* y1 = s.last ? ws + s.o_y1 : ring_slot(st[s.j + 1], -1, 0);
-    void* y2 = s.last ? ws + s.o_y2 : ring_slot(st[s.j + 1], -1, 1);
-    s.blocks->forward(ws + s.o_fx1, ws + s.o_fx2, y1, y2, q);
-  }
+  for (NetStage& s : st) stage_forward(s, -1, q, /*keep=*/true, /*buffers=*/false);
   NetStage& sl = st[J - 1];
   head(sl, ws + sl.o_y1, ws + sl.o_y2, lab, loss, q);
   for (int j = J - 1; j >= 0; --j) {
     NetStage& s = st[j];
-    Stage& blk = *s.blocks;
     const void *by1, *by2, *bg1, *bg2;
     if (s.last) {
       by1 = ws + s.o_y1; by2 = ws + s.o_y2; bg1 = ws + s.o_g1; bg2 = ws + s.o_g2;
     } else {
-      const NetStage& nx = st[j + 1];
-      by1 = ring_slot(nx, -1, 0); by2 = ring_slot(nx, -1, 1);
-      bg1 = ws + nx.o_msg[par][0]; bg2 = ws + nx.o_msg[par][1];
+      by1 = bwd_y(s, -1, par, 0); by2 = bwd_y(s, -1, par, 1);
+      bg1 = bwd_g(s, par, 0); bg2 = bwd_g(s, par, 1);
     }
-    blk.backward(by1, by2, bg1, bg2, ws + s.o_xr1, ws + s.o_xr2, ws + s.o_dx1, ws + s.o_dx2, q);
-    const void* in1 = ring_slot(s, -1, 0);
-    const void* in2 = s.first ? nullptr : ring_slot(s, -1, 1);
-    front_backward(s, in1, in2, ws + s.o_dx1, ws + s.o_dx2, par, q, /*recompute=*/false);
+    backward_stage(s, -1, 0, par, q, by1, by2, bg1, bg2, nullptr, /*recompute=*/false);
     if (!update) continue;
-    blk.count_backward();
-    if (blk.update_due()) {
+    if (count_and_due(s)) {
       // stage j's gradient is complete; stages below read only its message
       stage_update(s, q);
-      blk.mark_updated();
+      if (s.has_blocks) s.blocks->mark_updated();
     }
   }
 }
@@ -602,21 +712,29 @@ void Net::probe_tick(int mode, float* gout, hipStream_t q) {
     const void *by1, *by2, *bg1, *bg2;
     if (s.last) {
       // the last stage runs the forward of its micro-batch in the same tick
-      const void* in1 = ring_slot(s, mb, 0);
-      const void* in2 = s.first ? nullptr : ring_slot(s, mb, 1);
-      front_forward(s, in1, in2, q);
-      s.blocks->forward(ws + s.o_fx1, ws + s.o_fx2, ws + s.o_y1, ws + s.o_y2, q);
+      stage_forward(s, mb, q, false, false);
       head(s, ws + s.o_y1, ws + s.o_y2, at<int32_t>(st[0].o_labels) + (mb % J) * desc.n, nullptr,
            q);
       by1 = ws + s.o_y1; by2 = ws + s.o_y2; bg1 = ws + s.o_g1; bg2 = ws + s.o_g2;
     } else {
-      const NetStage& nx = st[s.j + 1];
       const int pm = static_cast<int>((t - 1) & 1);
-      by1 = ring_slot(nx, mb, 0); by2 = ring_slot(nx, mb, 1);
-      bg1 = ws + nx.o_msg[pm][0]; bg2 = ws + nx.o_msg[pm][1];
+      by1 = bwd_y(s, mb, pm, 0); by2 = bwd_y(s, mb, pm, 1);
+      bg1 = bwd_g(s, pm, 0); bg2 = bwd_g(s, pm, 1);
     }
     backward_stage(s, mb, s.last ? 0 : mode, par, q, by1, by2, bg1, bg2);
   }
+}
+
+// Accumulation bookkeeping of a stage: a stage without blocks counts along
+// with the network's optimizer setting (its own counter).
+bool Net::count_and_due(NetStage& s) {
+  if (s.has_blocks) {
+    s.blocks->count_backward();
+    return s.blocks->update_due();
+  }
+  ++s.bwd_count;
+  const int k = std::max(1, opt.accum_k);
+  return s.bwd_count % k == 0;
 }
 
 bool Net::tick(const void* images, const int32_t* labels, float* loss, hipStream_t caller) {
@@ -629,48 +747,19 @@ bool Net::tick(const void* images, const int32_t* labels, float* loss, hipStream
     (void)hipStreamWaitEvent(s.sb, ev_tick, 0);
   }
   for (NetStage& s : st) {
-    Stage& blk = *s.blocks;
     const int64_t mf = t - s.j;
     const int64_t mb = t - (J2 - s.j);
     const bool do_f = mf >= 0 && mf < fed;
     const bool do_b = mb >= 0 && mb < fed;
-    void* y1 = nullptr;
-    void* y2 = nullptr;
     if (do_f) {
       hipStream_t q = s.sf;
-      const void* in1;
-      const void* in2 = nullptr;
       if (s.first) {
         pad_channels8(dt, images, desc.c_img, ring_slot(s, mf, 0), s.Min, q);
         copy_i32(labels, at<int32_t>(st[0].o_labels) + (mf % J) * desc.n, desc.n, q);
-        in1 = ring_slot(s, mf, 0);
-      } else {
-        in1 = ring_slot(s, mf, 0);
-        in2 = ring_slot(s, mf, 1);
       }
-      if (s.ps_slot_bytes) stash_params(s, mf, q);
-      front_forward(s, in1, in2, q);
-      if (s.ib_slot_bytes) {
-        const size_t hb = static_cast<size_t>(s.M) * (s.C / 2) * esz;
-        (void)hipMemcpyAsync(ib_slot(s, mf, 0), ws + s.o_fx1, hb, hipMemcpyDeviceToDevice, q);
-        (void)hipMemcpyAsync(ib_slot(s, mf, 1), ws + s.o_fx2, hb, hipMemcpyDeviceToDevice, q);
-      }
+      stage_forward(s, mf, q, /*keep=*/false, /*buffers=*/true);
       if (s.last) {
-        y1 = ws + s.o_y1;
-        y2 = ws + s.o_y2;
-      } else {
-        y1 = ring_slot(st[s.j + 1], mf, 0);
-        y2 = ring_slot(st[s.j + 1], mf, 1);
-      }
-      void* fx1 = ws + s.o_fx1;
-      void* fx2 = ws + s.o_fx2;
-      if (blk.use_graphs)
-        (void)blk.graphs.run({1, reinterpret_cast<uintptr_t>(fx1), reinterpret_cast<uintptr_t>(y1)}, q,
-                             [&](hipStream_t c) { blk.forward(fx1, fx2, y1, y2, c); }, 0);
-      else
-        blk.forward(fx1, fx2, y1, y2, q);
-      if (s.last) {
-        head(s, y1, y2, at<int32_t>(st[0].o_labels) + (mf % J) * desc.n, loss, q);
+        head(s, ws + s.o_y1, ws + s.o_y2, at<int32_t>(st[0].o_labels) + (mf % J) * desc.n, loss, q);
         wrote_loss = loss != nullptr;
       }
     }
@@ -681,18 +770,16 @@ bool Net::tick(const void* images, const int32_t* labels, float* loss, hipStream
       if (s.last) {
         by1 = ws + s.o_y1; by2 = ws + s.o_y2; bg1 = ws + s.o_g1; bg2 = ws + s.o_g2;
       } else {
-        const NetStage& nx = st[s.j + 1];
         const int par = static_cast<int>((t - 1) & 1);
-        by1 = ring_slot(nx, mb, 0); by2 = ring_slot(nx, mb, 1);
-        bg1 = ws + nx.o_msg[par][0]; bg2 = ws + nx.o_msg[par][1];
+        by1 = bwd_y(s, mb, par, 0); by2 = bwd_y(s, mb, par, 1);
+        bg1 = bwd_g(s, par, 0); bg2 = bwd_g(s, par, 1);
       }
       // the last stage has no delay: every variant is the PETRA backward there.
       // (Handing deferred weight gradients to the forward stream, as the
       // single-stage step does, measured slower here: 3.27 vs 3.09 ms per tick,
       // the stages' streams are busy with each other's work.)
       backward_stage(s, mb, s.last ? 0 : bwd_mode, static_cast<int>(t & 1), q, by1, by2, bg1, bg2);
-      blk.count_backward();
-      if (blk.update_due()) {
+      if (count_and_due(s)) {
         // the update follows this stage's forward and backward of the tick (Eq. 5)
         if (q != s.sb) {
           (void)hipEventRecord(s.ev_f, q);
@@ -702,7 +789,7 @@ bool Net::tick(const void* images, const int32_t* labels, float* loss, hipStream
           (void)hipStreamWaitEvent(s.sb, s.ev_f, 0);
         }
         stage_update(s, s.sb);
-        blk.mark_updated();
+        if (s.has_blocks) s.blocks->mark_updated();
       }
     }
   }

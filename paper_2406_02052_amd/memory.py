@@ -25,7 +25,7 @@ from . import _lib as L
 
 def net_memory(net) -> List[Dict[str, int]]:
     """Per-stage byte counts of an instantiated Net (see petra_net_mem)."""
-    return [L.petra_net_memory(net.handle, j) for j in range(len(net.widths))]
+    return [L.petra_net_memory(net.handle, j) for j in range(net.n_stages)]
 
 
 @dataclasses.dataclass(frozen=True)

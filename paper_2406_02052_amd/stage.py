@@ -120,7 +120,7 @@ class Net:
     def __init__(self, n: int, h: int, w: int, c_img: int, widths, blocks_per_stage: int,
                  classes: int, dtype: str = "bf16", bn_eps: float = 1e-5,
                  bn_momentum: float = 0.1, device: str = "cuda", input_buffer: bool = False,
-                 param_buffer: bool = False):
+                 param_buffer: bool = False, split_stages: bool = False):
         import torch
         self.torch = torch
         self.device = device
@@ -131,8 +131,9 @@ class Net:
         ws = (ctypes_int_array(widths))
         desc = L.NetDesc(n, h, w, c_img, len(widths), ws, blocks_per_stage, classes,
                          L.PETRA_BF16 if dtype == "bf16" else L.PETRA_FP32, bn_eps, bn_momentum,
-                         int(input_buffer), int(param_buffer))
+                         int(input_buffer), int(param_buffer), int(split_stages))
         self.handle = L.petra_net_create(desc)
+        self.n_stages = L.petra_net_num_stages(self.handle)
         self.n_params, self.n_tensors, self.n_bn, self.ws_bytes = L.petra_net_query(self.handle)
         self.infos = [L.petra_net_param_info(self.handle, i) for i in range(self.n_tensors)]
         f32 = dict(dtype=torch.float32, device=device)
@@ -199,7 +200,7 @@ class Net:
         L.petra_net_set_backward(self.handle, mode)
 
     def stage_spans(self):
-        return [L.petra_net_stage_params(self.handle, j) for j in range(len(self.widths))]
+        return [L.petra_net_stage_params(self.handle, j) for j in range(self.n_stages)]
 
     def probe_tick(self, mode: int, stream=None):
         """Unscaled gradients the next tick's backward passes would produce in

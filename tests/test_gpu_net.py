@@ -29,7 +29,7 @@ def affine_params(wl, seed=12):
     return names, params
 
 
-def run_both(wl, names, params, n_micro, ticks, store=None, gpu=True, mode=0):
+def run_both(wl, names, params, n_micro, ticks, store=None, gpu=True, mode=0, split=False):
     import torch
     from paper_2406_02052_amd import Net
 
@@ -41,7 +41,7 @@ def run_both(wl, names, params, n_micro, ticks, store=None, gpu=True, mode=0):
     ref = PetraNet([p.astype(np.float64) for p in params], names, len(wl.widths),
                    wl.blocks_per_stage, weight_view=synth.round_bf16 if bf else None,
                    store=store if store is not None else (synth.round_bf16 if bf else None),
-                   use_inputs=bool(mode & 1), use_params=bool(mode & 2))
+                   use_inputs=bool(mode & 1), use_params=bool(mode & 2), split_fronts=split)
     oloss = []
     for t in range(ticks):
         oloss.append(ref.tick(t, lambda m: imgs[m], lambda m: labs[m], n_micro, wl.lr,
@@ -49,7 +49,8 @@ def run_both(wl, names, params, n_micro, ticks, store=None, gpu=True, mode=0):
     if not gpu:
         return ref, oloss, None, None
     net = Net(wl.n, wl.h, wl.w, wl.c_img, wl.widths, wl.blocks_per_stage, wl.classes, wl.dtype,
-              input_buffer=bool(mode & 1), param_buffer=bool(mode & 2))
+              input_buffer=bool(mode & 1), param_buffer=bool(mode & 2), split_stages=split)
+    assert net.n_stages == ref.J
     net.set_params(params)
     net.set_optimizer(wl.lr, wl.momentum, wl.weight_decay, wl.nesterov, wl.accum_k)
     gloss = []
@@ -309,3 +310,53 @@ def test_tiny_net_fp32_accumulation_matches_oracle():
     ref, oloss, net, gloss = run_both(wl, names, params, n_micro, ticks)
     worst = compare(wl, names, params, ref, oloss, net, gloss, 1e-4, 1e-4)
     print("worst parameter increment error", worst, flush=True)
+
+
+@pytest.mark.parametrize("blocks", [1, 2])
+def test_split_stages_fp32_matches_oracle(blocks):
+    """The per-layer split (every stem/downsampling and every block its own
+    stage; J = 8 or 12): losses, parameters after every update and running
+    statistics against the oracle's split schedule.  With two blocks per level
+    the lower block stage rebuilds its input from the reconstruction the upper
+    one sends back."""
+    wl = TINY.with_(dtype="fp32", blocks_per_stage=blocks)
+    names, params = affine_params(wl)
+    J = len(wl.widths) * (1 + blocks)
+    n_micro, ticks = 3, 3 + 2 * J
+    ref, oloss, net, gloss = run_both(wl, names, params, n_micro, ticks, split=True)
+    print("J", J, "losses", gloss, oloss, flush=True)
+    worst = compare(wl, names, params, ref, oloss, net, gloss, 1e-4, 1e-4)
+    print("worst parameter increment error", worst, flush=True)
+    orm = np.concatenate([np.concatenate([m.reshape(-1) for m in st.run_mean]) for st in ref.stages])
+    np.testing.assert_allclose(net.run_mean.cpu().numpy(), orm, rtol=1e-4, atol=1e-5)
+    assert net.state() == (ticks, n_micro, 0)
+
+
+def test_split_stages_backprop_and_delayed_variant_match_oracle():
+    """Split schedule: the reversible-backprop step and the delayed-gradient
+    variant (both buffers) against the oracle."""
+    import torch
+    from paper_2406_02052_amd import Net
+
+    wl = TINY.with_(dtype="fp32", blocks_per_stage=2)
+    names, params = affine_params(wl)
+    rng = np.random.default_rng(8)
+    imgs = [rng.standard_normal((wl.n, wl.h, wl.w, wl.c_img), dtype=np.float32) for _ in range(2)]
+    labs = [rng.integers(0, wl.classes, wl.n).astype(np.int32) for _ in range(2)]
+    ref = PetraNet([p.astype(np.float64) for p in params], names, len(wl.widths),
+                   wl.blocks_per_stage, split_fronts=True)
+    oloss = [ref.backprop_step(imgs[i], labs[i], wl.lr, wl.momentum, wl.weight_decay, wl.nesterov,
+                               wl.accum_k) for i in range(2)]
+    net = Net(wl.n, wl.h, wl.w, wl.c_img, wl.widths, wl.blocks_per_stage, wl.classes, wl.dtype,
+              split_stages=True)
+    net.set_params(params)
+    net.set_optimizer(wl.lr, wl.momentum, wl.weight_decay, wl.nesterov, wl.accum_k)
+    gloss = []
+    for i in range(2):
+        net.backprop_step(net.images(imgs[i]), net.labels(labs[i]))
+        torch.cuda.synchronize()
+        gloss.append(float(net.loss.item()))
+    compare(wl, names, params, ref, oloss, net, gloss, 1e-4, 1e-4)
+    J = ref.J
+    ref2, oloss2, net2, gloss2 = run_both(wl, names, params, 3, 3 + 2 * J, mode=3, split=True)
+    compare(wl, names, params, ref2, oloss2, net2, gloss2, 1e-4, 1e-4)
