@@ -150,3 +150,33 @@ def test_net_backprop_step_validation_without_device_work():
         assert e.value.name == "PETRA_ERR_ALIGN"
     finally:
         L.petra_net_destroy(h)
+
+
+def test_net_split_stage_layout_and_validation():
+    """Per-layer split: same parameters in the same canonical order, one stage
+    per front layer and per block; bad flags are rejected."""
+    from paper_2406_02052_amd import _lib as L
+    from paper_2406_02052_amd.stage import ctypes_int_array
+    wl = synth.REVNET18_SCHEDULE
+    def desc(split, ib=0):
+        return L.NetDesc(wl.n, wl.h, wl.w, wl.c_img, len(wl.widths), ctypes_int_array(wl.widths),
+                         wl.blocks_per_stage, wl.classes, L.PETRA_BF16, wl.bn_eps, wl.bn_momentum,
+                         ib, 0, split)
+    infos = {}
+    for split in (0, 1):
+        h = L.petra_net_create(desc(split))
+        try:
+            n_params, nt, nbn, _ = L.petra_net_query(h)
+            J = L.petra_net_num_stages(h)
+            assert J == (len(wl.widths) * (1 + wl.blocks_per_stage) if split else len(wl.widths))
+            spans = [L.petra_net_stage_params(h, j) for j in range(J)]
+            assert spans[0][0] == 0 and sum(n for _, n in spans) == n_params
+            assert all(a[0] + a[1] == b[0] for a, b in zip(spans, spans[1:]))
+            infos[split] = [(L.petra_net_param_info(h, i).numel,
+                             tuple(L.petra_net_param_info(h, i).shape)) for i in range(nt)]
+        finally:
+            L.petra_net_destroy(h)
+    assert infos[0] == infos[1]
+    with pytest.raises(L.PetraError) as e:
+        L.petra_net_create(desc(2))
+    assert e.value.name == "PETRA_ERR_INVALID_ARG"

@@ -360,3 +360,25 @@ def test_split_stages_backprop_and_delayed_variant_match_oracle():
     J = ref.J
     ref2, oloss2, net2, gloss2 = run_both(wl, names, params, 3, 3 + 2 * J, mode=3, split=True)
     compare(wl, names, params, ref2, oloss2, net2, gloss2, 1e-4, 1e-4)
+
+
+def test_split_stages_bf16_matches_storage_oracle():
+    """bf16 per-layer split (J = 12) against the storage-precision oracle, with
+    per-tensor floors from two jittered-rounding oracle runs."""
+    wl = TINY.with_(blocks_per_stage=2)
+    names, params = affine_params(wl)
+    J = len(wl.widths) * 3
+    n_micro, ticks = 3, 3 + 2 * J
+    ref, oloss, net, gloss = run_both(wl, names, params, n_micro, ticks, split=True)
+    floors = {}
+    for seed in (1, 2):
+        tw, _, _, _ = run_both(wl, names, params, n_micro, ticks, store=jitter_store(seed),
+                               gpu=False, split=True)
+        tw_p = {nm: p for st in tw.stages for nm, p in zip(st.names, st.params)}
+        rf_p = {nm: p for st in ref.stages for nm, p in zip(st.names, st.params)}
+        p0 = dict(zip(names, params))
+        for nm in names:
+            floors[nm] = max(floors.get(nm, 0.0), rel(tw_p[nm] - p0[nm], rf_p[nm] - p0[nm]))
+    print("losses", gloss, oloss, flush=True)
+    worst = compare(wl, names, params, ref, oloss, net, gloss, 2e-2, 2e-2, floors)
+    print("worst parameter increment error", worst, flush=True)
