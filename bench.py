@@ -111,7 +111,7 @@ def gpu_inputs(st, wl):
     xb1, xb2 = synth.stage_input(wl, seed_offset=10)
     g1, g2 = synth.stage_output_grad(wl)
     t = dict(xa1=st.act(x1), xa2=st.act(x2), yb1=st.act(), yb2=st.act(),
-             db1=st.act(g1), db2=st.act(g2))
+             db1=st.act(g1), db2=st.act(g2), nb1=st.act(-g1), nb2=st.act(-g2), flip=0)
     # the backward micro-batch: the stage output of another micro-batch
     st.forward(st.act(xb1), st.act(xb2), t["yb1"], t["yb2"])
     for k in ("ya1", "ya2", "xr1", "xr2", "dx1", "dx2"):
@@ -119,15 +119,29 @@ def gpu_inputs(st, wl):
     return t
 
 
+def output_grad(t):
+    """The backward micro-batch's output gradient for the next step.
+
+    Its sign alternates from step to step.  A fixed synthetic gradient is not
+    the gradient of any loss: applied every step at the workload's learning
+    rate it pushes the weights the same way without end, and the activations
+    grow geometrically (non-finite after about a hundred steps).  With the sign
+    alternating, momentum SGD oscillates about the initial weights; every step
+    does the same work."""
+    t["flip"] ^= 1
+    return (t["db1"], t["db2"]) if t["flip"] else (t["nb1"], t["nb2"])
+
+
 def one_step(st, t):
-    return st.step(t["xa1"], t["xa2"], t["ya1"], t["ya2"], t["yb1"], t["yb2"], t["db1"], t["db2"],
+    d1, d2 = output_grad(t)
+    return st.step(t["xa1"], t["xa2"], t["ya1"], t["ya2"], t["yb1"], t["yb2"], d1, d2,
                    t["xr1"], t["xr2"], t["dx1"], t["dx2"])
 
 
 def one_step_serial(st, t):
+    d1, d2 = output_grad(t)
     st.forward(t["xa1"], t["xa2"], t["ya1"], t["ya2"])
-    st.reconstruct_backward(t["yb1"], t["yb2"], t["db1"], t["db2"], t["xr1"], t["xr2"],
-                            t["dx1"], t["dx2"])
+    st.reconstruct_backward(t["yb1"], t["yb2"], d1, d2, t["xr1"], t["xr2"], t["dx1"], t["dx2"])
     st.update()
 
 

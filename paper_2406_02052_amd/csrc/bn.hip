@@ -177,24 +177,6 @@ __global__ __launch_bounds__(256) void combine_rec_kernel(const T* v, const T* h
   }
 }
 
-template <typename T>
-__global__ __launch_bounds__(256) void bn_bwd_apply_kernel(const T* d, const T* h,
-                                                           const float* ca, const float* cb,
-                                                           const float* cc, const float* mean,
-                                                           T* out, long total8, int c8) {
-  for (long i = static_cast<long>(blockIdx.x) * 256 + threadIdx.x; i < total8;
-       i += static_cast<long>(gridDim.x) * 256) {
-    const int ch = static_cast<int>(i % c8) * 8;
-    float dv[8], hv[8], o[8];
-    Vec8<T>::load(d + i * 8, dv);
-    Vec8<T>::load(h + i * 8, hv);
-#pragma unroll
-    for (int j = 0; j < 8; ++j)
-      o[j] = fmaf(ca[ch + j], dv[j], fmaf(cb[ch + j], hv[j] - mean[ch + j], cc[ch + j]));
-    Vec8<T>::store(out + i * 8, o);
-  }
-}
-
 // Each block owns rows [tile*rows_per_tile, ...) and writes one partial row.
 template <typename T>
 __global__ __launch_bounds__(256) void combine_bwd_kernel(const T* v, const T* h, const T* d,
@@ -314,19 +296,6 @@ void combine_rec(int dtype, const void* v, const void* h, const float* scale, co
     PETRA_LAUNCH(combine_rec_kernel<float>, dim3(ew_grid(total8)), dim3(256), 0, st,
                        static_cast<const float*>(v), static_cast<const float*>(h), scale, shift,
                        static_cast<float*>(x), total8, c / 8);
-}
-
-void bn_bwd_apply(int dtype, const void* d, const void* h, const float* ca, const float* cb,
-                  const float* cc, const float* mean, void* out, long m, int c, hipStream_t st) {
-  const long total8 = m * c / 8;
-  if (dtype == DT_BF16)
-    PETRA_LAUNCH(bn_bwd_apply_kernel<bf16_t>, dim3(ew_grid(total8)), dim3(256), 0, st,
-                       static_cast<const bf16_t*>(d), static_cast<const bf16_t*>(h), ca, cb, cc,
-                       mean, static_cast<bf16_t*>(out), total8, c / 8);
-  else
-    PETRA_LAUNCH(bn_bwd_apply_kernel<float>, dim3(ew_grid(total8)), dim3(256), 0, st,
-                       static_cast<const float*>(d), static_cast<const float*>(h), ca, cb, cc,
-                       mean, static_cast<float*>(out), total8, c / 8);
 }
 
 void combine_bwd(int dtype, const void* v, const void* h, const void* d, const float* scale,

@@ -145,9 +145,6 @@ void combine_rec(int dtype, const void* v, const void* h, const float* scale, co
 void combine_bwd(int dtype, const void* v, const void* h, const void* d, const float* scale,
                  const float* shift, const float* mean, const float* rstd, void* x,
                  float* partials, long m, int c, hipStream_t st);
-// out = ca*d + cb*(h - mean) + cc  (BN input gradient); may run in place on d.
-void bn_bwd_apply(int dtype, const void* d, const void* h, const float* ca, const float* cb,
-                  const float* cc, const float* mean, void* out, long m, int c, hipStream_t st);
 
 // Conv weight tensors inside the flat parameter buffer, for the refresh of
 // the storage-type compute copies.

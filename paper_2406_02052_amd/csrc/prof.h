@@ -12,7 +12,7 @@ namespace petra {
 
 enum KernelClass {
   K_CONV_FPROP = 0, K_CONV_DGRAD, K_CONV_WGRAD, K_WGRAD_REDUCE, K_BN_FINALIZE, K_BN_BWD_FINALIZE,
-  K_COMBINE_FWD, K_COMBINE_BWD, K_BN_BWD_APPLY, K_SGD, K_REFRESH, K_NUM_CLASSES
+  K_COMBINE_FWD, K_COMBINE_BWD, K_SGD, K_REFRESH, K_NUM_CLASSES
 };
 
 const char* kernel_class_name(int k);

@@ -7,7 +7,7 @@ thread_local LaunchEvents g_launch_events;
 const char* kernel_class_name(int k) {
   static const char* names[K_NUM_CLASSES] = {
       "conv_fprop", "conv_dgrad", "conv_wgrad", "wgrad_reduce", "bn_finalize",
-      "bn_bwd_finalize", "combine_fwd", "combine_bwd", "bn_bwd_apply", "sgd_update",
+      "bn_bwd_finalize", "combine_fwd", "combine_bwd", "sgd_update",
       "refresh_weights"};
   return (k >= 0 && k < K_NUM_CLASSES) ? names[k] : "?";
 }

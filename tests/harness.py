@@ -1,7 +1,13 @@
 """Test-side helpers: drive a stage through the C ABI and the oracle on the
 same seeded inputs, and compare.  (Test infrastructure; not product code.)
 
-Tolerances.  fp32 workloads: normwise relative error <= 1e-4 on every tensor.
+Tolerances.  fp32 workloads: normwise relative error <= 1e-4 on every tensor,
+except where fp32 arithmetic itself cannot get there: for the same masked
+tensors as below the bar is max(1e-4, 3 x the distance between the oracle and
+the oracle run in fp32).  That floor stays far below 1e-4 at small sizes; at
+100k pixels per channel the BN-backward sums of the first layers cancel
+(the channel sums of an output gradient that the next BN backward has already
+centred), and the oracle's own fp32 run is ~5e-3 from its fp64 result there.
 bf16 workloads (bf16 storage, fp32 accumulation): <= 2e-2 on every tensor,
 where the oracle holds activations at bf16 wherever the method stores them.
 Tensors that come out of ReLU derivatives (input gradients, parameter
@@ -108,7 +114,7 @@ def run_step_parity(wl, bn_affine="random"):
     """Forward, reconstruct+VJP and update on both sides.
 
     Returns (errs, floors, info): per-tensor GPU-vs-oracle errors, per-tensor
-    bf16 noise floors (empty for fp32) and informational figures.
+    noise floors and informational figures.
     """
     import torch
     from paper_2406_02052_amd import to_host
@@ -152,6 +158,9 @@ def run_step_parity(wl, bn_affine="random"):
     info = {"drift_gpu": max(rel(got["x1"], x[0]), rel(got["x2"], x[1])),
             "drift_oracle": max(rel(want["x1"], x[0]), rel(want["x2"], x[1])),
             "accum_after_update": accum_after}
+    if wl.dtype == "fp32":
+        res = _oracle_step(oracle_state(wl, params, dtype=np.float32), wl, params, x, yin, g)
+        floors = {k: rel(res[k], want[k]) for k in want}
     if wl.dtype == "bf16":
         twins = [oracle_state(wl, params, dtype=np.float32),
                  oracle_state(wl, params, store=jitter_store(1)),
@@ -173,7 +182,7 @@ def check(errs, floors, info, wl):
     bad = {}
     for k, e in errs.items():
         bar = t
-        if wl.dtype == "bf16" and k.split(":")[0] in FLOORED:
+        if k.split(":")[0] in FLOORED:
             bar = max(t, 3.0 * floors.get(k, 0.0))
         if not e <= bar:
             bad[k] = (e, bar)

@@ -11,9 +11,15 @@ from tests.harness import check, gpu_stage, rel, run_step_parity
 pytestmark = pytest.mark.gpu
 
 
+# The last case is fp32 at 32x56x56 (100k pixels per channel, 49 MiB per half
+# tensor): fp32 kernels at a size where the BN-backward sums cancel, checked
+# under the fp32 floor rule of tests/harness.py.
 @pytest.mark.parametrize("wl", [synth.CIFAR_STAGE, synth.IMAGENET_BOTTLENECK_STAGE,
-                                synth.IMAGENET32_STAGE.with_(blocks=1)],
-                         ids=["cifar_stage", "imagenet_bottleneck_stage", "imagenet32_one_block"])
+                                synth.IMAGENET32_STAGE.with_(blocks=1),
+                                synth.IMAGENET_BOTTLENECK_STAGE.with_(dtype="fp32", n=32,
+                                                                      blocks=1)],
+                         ids=["cifar_stage", "imagenet_bottleneck_stage", "imagenet32_one_block",
+                              "imagenet_bottleneck_fp32_one_block"])
 def test_full_size_step_parity(wl):
     print(f"full-size case {wl}", flush=True)
     errs, floors, info = run_step_parity(wl, bn_affine="identity")
