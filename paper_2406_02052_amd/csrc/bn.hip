@@ -14,22 +14,11 @@ namespace {
 
 // Finalize kernels: one 256-thread block per channel.  Thread t takes tiles
 // t, t + 256, ... (loads of up to FIN_U tiles in flight), then the block's
-// values are combined in a fixed tree: xor-shuffle levels inside each wave,
+// sums are combined in a fixed tree: xor-shuffle levels inside each wave,
 // then the four wave results in order.  Deterministic run to run.
 constexpr int FIN_THREADS = 256;
 constexpr int FIN_U = 4;
-
-// Chan's pairwise combination of (count, mean, centred sum of squares).
-__device__ __forceinline__ void chan_combine(double& n, double& mean, double& m2, double nb,
-                                             double mb, double qb) {
-  if (nb <= 0.0) return;
-  const double nn = n + nb;
-  const double r = nb / nn;
-  const double d = mb - mean;
-  mean += d * r;
-  m2 += qb + d * d * n * r;
-  n = nn;
-}
+static_assert(FIN_THREADS == 256, "the wave results are combined as four");
 
 // Sum of (a, b) over partials[tile][2][c] for channel ch.
 __device__ void reduce_partials(const float* partials, int tiles, int c, int ch, double& s1,
@@ -65,12 +54,22 @@ __device__ void reduce_partials(const float* partials, int tiles, int c, int ch,
   s2 = (red[1][0] + red[1][1]) + (red[1][2] + red[1][3]);
 }
 
-// partials[tile][3][c] = (rows, sum, centred sum of squares) -> fp64 totals for ch.
+// partials[tile][3][c] = (rows n_t, sum S_t, centred sum of squares Q_t) ->
+// fp64 totals for ch.  Every tile is re-centred on one shift K, the first
+// tile's mean: sum_x (x - K)^2 = sum_t [Q_t + n_t (m_t - K)^2] and
+// sum_x (x - K) = sum_t n_t (m_t - K), with m_t = S_t / n_t.  Those are plain
+// sums (one fixed-order block reduction of three fp64 values), and
+// mean = K + B/N, M2 = A - B^2/N.  K lies within a tile's spread of the mean,
+// so the subtraction loses a few bits of fp64 at most.
 __device__ void reduce_stats(const float* partials, int tiles, int c, int ch, double& n,
                              double& mean, double& m2) {
   __shared__ double red[3][FIN_THREADS / 64];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  double na = 0.0, ma = 0.0, qa = 0.0;
+  const float n0 = tiles > 0 ? partials[ch] : 0.f;
+  const float s0 = tiles > 0 ? partials[c + ch] : 0.f;
+  double na = 0.0, aa = 0.0, ba = 0.0;
+  double k = 0.0;
+  bool have_k = false;
   for (int base = tid; base < tiles; base += FIN_THREADS * FIN_U) {
     float vn[FIN_U], vs[FIN_U], vq[FIN_U];
 #pragma unroll
@@ -82,25 +81,44 @@ __device__ void reduce_stats(const float* partials, int tiles, int c, int ch, do
       vs[u] = ok ? partials[(row + 1) * c + ch] : 0.f;
       vq[u] = ok ? partials[(row + 2) * c + ch] : 0.f;
     }
+    if (!have_k) {
+      k = n0 > 0.f ? static_cast<double>(s0) / n0 : 0.0;
+      have_k = true;
+    }
 #pragma unroll
-    for (int u = 0; u < FIN_U; ++u)
-      if (vn[u] > 0.f) chan_combine(na, ma, qa, vn[u], static_cast<double>(vs[u]) / vn[u], vq[u]);
+    for (int u = 0; u < FIN_U; ++u) {
+      if (vn[u] > 0.f) {
+        const double nt = vn[u];
+        const double d = static_cast<double>(vs[u]) / nt - k;
+        na += nt;
+        ba += nt * d;
+        aa += static_cast<double>(vq[u]) + nt * d * d;
+      }
+    }
   }
+  if (!have_k) k = n0 > 0.f ? static_cast<double>(s0) / n0 : 0.0;
+  // xor butterfly: every lane ends with the same (commutative) sums
   for (int off = 1; off < 64; off <<= 1) {
-    const double nb = __shfl_xor(na, off, 64), mb = __shfl_xor(ma, off, 64),
-                 qb = __shfl_xor(qa, off, 64);
-    chan_combine(na, ma, qa, nb, mb, qb);
+    na += __shfl_xor(na, off, 64);
+    aa += __shfl_xor(aa, off, 64);
+    ba += __shfl_xor(ba, off, 64);
   }
   if (lane == 0) {
     red[0][wave] = na;
-    red[1][wave] = ma;
-    red[2][wave] = qa;
+    red[1][wave] = aa;
+    red[2][wave] = ba;
   }
   __syncthreads();
-  n = red[0][0];
-  mean = red[1][0];
-  m2 = red[2][0];
-  for (int w = 1; w < FIN_THREADS / 64; ++w) chan_combine(n, mean, m2, red[0][w], red[1][w], red[2][w]);
+  n = (red[0][0] + red[0][1]) + (red[0][2] + red[0][3]);
+  const double A = (red[1][0] + red[1][1]) + (red[1][2] + red[1][3]);
+  const double B = (red[2][0] + red[2][1]) + (red[2][2] + red[2][3]);
+  if (n > 0.0) {
+    mean = k + B / n;
+    m2 = fmax(A - B * B / n, 0.0);
+  } else {
+    mean = 0.0;
+    m2 = 0.0;
+  }
 }
 
 __global__ __launch_bounds__(FIN_THREADS) void bn_stats_finalize_kernel(
