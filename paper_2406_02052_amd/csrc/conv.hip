@@ -1495,6 +1495,351 @@ __global__ __launch_bounds__(64 * NWM * NWN, 1) void conv_img_kernel(ConvArgs a)
   }
 }
 
+// 1x1 / stride 1 bf16 convolution with the BN-statistics epilogue, for the
+// HBM-bound bottleneck widths (C_in x C_out = 128 x 32 and 32 x 128).  There is
+// no LDS staging: a wave loads the 16 x K activation block of a 16-pixel unit
+// straight into MFMA operand registers (each lane 16 contiguous bytes of one
+// pixel), keeps every weight fragment in registers for the whole launch, and
+// issues D[cout][pixel] so that each lane stores 4 consecutive output channels
+// of one pixel (8 bytes).  Waves stream over units g, g + W, g + 2W, ... with
+// the next unit's loads in flight during the current unit's MFMAs and stores;
+// no barrier until the end.  BN moments are shifted sums in registers (shift:
+// the stored value of the wave's first pixel, per channel), combined over the
+// four waves once per workgroup: partial row = blockIdx.x.
+template <int K, int N, int PRO>
+__global__ __launch_bounds__(256) void conv1x1_kernel(ConvArgs a, int units) {
+  using T = bf16_t;
+  constexpr int KB = K / 32, NB = N / 16;
+  static_assert(K % 32 == 0 && N % 16 == 0 && PRO != PRO_BWD, "1x1 shape");
+  constexpr int PK = PRO == PRO_RELU ? KB : 1;
+  __shared__ float red[4][3][N];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int lr = lane & 15, lg = lane >> 4;
+  const long m = a.m;
+  const __amdgpu_buffer_rsrc_t r_src = make_rsrc(a.src, m * K * 2);
+  const __amdgpu_buffer_rsrc_t r_out = make_rsrc(a.out, m * N * 2);
+  const __amdgpu_buffer_rsrc_t r_wt = make_rsrc(a.wt, static_cast<long>(N) * K * 2);
+
+  auto load_unit = [&](int u, u32x4_t* x) {
+    const long pix = static_cast<long>(u) * 16 + lr;
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      const uint32_t off =
+          pix < m ? static_cast<uint32_t>((pix * K + kb * 32 + lg * 8) * 2) : BUF_OOB;
+      x[kb] = buf_load16(r_src, off);
+    }
+  };
+  const int W = gridDim.x * 4;
+  int u = blockIdx.x * 4 + wave;
+  u32x4_t xr[KB], xn[KB];
+  if (u < units) load_unit(u, xr);
+
+  // weight fragments: lane (lr, lg) holds W[nb*16 + lr][kb*32 + lg*8 .. +7]
+  Frag<T> wf[NB][KB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      Raw8<T> r;
+      r.set(buf_load16(r_wt, static_cast<uint32_t>(((nb * 16 + lr) * K + kb * 32 + lg * 8) * 2)));
+      wf[nb][kb].set(r);
+    }
+  // BN-apply + ReLU constants of this lane's input channels
+  float ps[PK][8], pt[PK][8];
+  if constexpr (PRO == PRO_RELU) {
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        ps[kb][j] = a.pro_scale[kb * 32 + lg * 8 + j];
+        pt[kb][j] = a.pro_shift[kb * 32 + lg * 8 + j];
+      }
+  }
+
+  float sa[NB][4], sb[NB][4], kk[NB][4];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) sa[nb][e] = sb[nb][e] = kk[nb][e] = 0.f;
+  float nv = 0.f;
+  bool first = true;
+  for (; u < units; u += W) {
+    const int un = u + W;
+    if (un < units) load_unit(un, xn);
+    Frag<T> xf[KB];
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      Raw8<T> r;
+      r.set(xr[kb]);
+      if constexpr (PRO == PRO_RELU) {
+        float v[8];
+        r.to_f32(v);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = fmaxf(fmaf(ps[kb][j], v[j], pt[kb][j]), 0.f);
+        r.from_f32(v);   // rounded to bf16, as the materialised activation
+      }
+      xf[kb].set(r);
+    }
+    const long pix = static_cast<long>(u) * 16 + lr;
+    const bool vm = pix < m;
+    nv += vm ? 1.f : 0.f;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) acc = mfma(wf[nb][kb], xf[kb], acc);
+      const uint32_t w0 = pack_bf16x2(acc[0], acc[1]), w1 = pack_bf16x2(acc[2], acc[3]);
+      const uint32_t off =
+          vm ? static_cast<uint32_t>((pix * N + nb * 16 + lg * 4) * 2) : BUF_OOB;
+      buf_store8(u32x2_t{w0, w1}, r_out, off);
+      // statistics of the stored values
+      float v[4];
+      v[0] = __uint_as_float(w0 << 16); v[1] = __uint_as_float(w0 & 0xffff0000u);
+      v[2] = __uint_as_float(w1 << 16); v[3] = __uint_as_float(w1 & 0xffff0000u);
+      if (first) {
+        // the unit's first pixel is inside the image (u < units)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) kk[nb][e] = __shfl(v[e], lane & 48, 64);
+      }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float d = vm ? v[e] - kk[nb][e] : 0.f;
+        sa[nb][e] += d;
+        sb[nb][e] = fmaf(d, d, sb[nb][e]);
+      }
+    }
+    first = false;
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) xr[kb] = xn[kb];
+  }
+  // per wave: (n, mean, centred M2) of every channel; then Chan over the waves
+  const float n16 = sum16(nv);
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float x = sum16(sa[nb][e]), y = sum16(sb[nb][e]);
+      if (lr == 0) {
+        const int c = nb * 16 + lg * 4 + e;
+        const float md = n16 > 0.f ? x / n16 : 0.f;
+        red[wave][0][c] = n16;
+        red[wave][1][c] = kk[nb][e] + md;
+        red[wave][2][c] = n16 > 0.f ? fmaxf(y - x * md, 0.f) : 0.f;
+      }
+    }
+  __syncthreads();
+  for (int c = tid; c < N; c += 256) {
+    float n = 0.f, mean = 0.f, m2 = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const float nb = red[w][0][c];
+      if (nb > 0.f) {
+        const float nn = n + nb, rb = nb / nn, d = red[w][1][c] - mean;
+        mean += d * rb;
+        m2 += red[w][2][c] + d * d * n * rb;
+        n = nn;
+      }
+    }
+    const long row = blockIdx.x;
+    a.partials[(row * 3 + 0) * N + c] = n;
+    a.partials[(row * 3 + 1) * N + c] = n * mean;
+    a.partials[(row * 3 + 2) * N + c] = m2;
+  }
+}
+
+// Input-gradient form of the streaming 1x1 kernel: out = conv(dh) with the
+// layer's transposed weights (here K and N are the layer's C_out and C_in).
+// Prologue: PRO_BWD forms the BN input gradient ca d + cb (h - mean) + cc of
+// the layer's BN as the output gradient d is loaded (h read at the same
+// position), rounded to bf16 as the materialised gradient.  Epilogues as in the
+// other conv kernels: EP_MASK (ReLU mask of the BN below plus its backward
+// partials), EP_RESID (residual add), EP_RESID_STATS (residual add plus the
+// BN-backward partials of the stored result against ep_h).  Every operand of
+// the next unit, the epilogue's included, is in flight during the current one.
+template <int K, int N, int EP, int PRO>
+__global__ __launch_bounds__(256) void conv1x1_bwd_kernel(ConvArgs a, int units) {
+  using T = bf16_t;
+  constexpr int KB = K / 32, NB = N / 16;
+  constexpr bool GRAD = EP == EP_MASK || EP == EP_RESID_STATS;
+  constexpr bool RES = EP == EP_RESID || EP == EP_RESID_STATS;
+  constexpr bool BWD = PRO == PRO_BWD;
+  static_assert(K % 32 == 0 && N % 16 == 0 && EP != EP_STATS && PRO != PRO_RELU, "1x1 shape");
+  constexpr int PK = BWD ? KB : 1;
+  constexpr int EN = GRAD ? NB : 1;
+  constexpr int RN = RES ? NB : 1;
+  __shared__ float red[4][2][N];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int lr = lane & 15, lg = lane >> 4;
+  const long m = a.m;
+  const long in_bytes = m * K * 2, out_bytes = m * N * 2;
+  const __amdgpu_buffer_rsrc_t r_src = make_rsrc(a.src, in_bytes);
+  const __amdgpu_buffer_rsrc_t r_h = make_rsrc(BWD ? a.pro_h : a.src, in_bytes);
+  const __amdgpu_buffer_rsrc_t r_out = make_rsrc(a.out, out_bytes);
+  const __amdgpu_buffer_rsrc_t r_eph = make_rsrc(a.ep_h != nullptr ? a.ep_h : a.out, out_bytes);
+  // a null residual reads zeros
+  const __amdgpu_buffer_rsrc_t r_res =
+      make_rsrc(a.resid != nullptr ? a.resid : a.out, a.resid != nullptr ? out_bytes : 0);
+  const __amdgpu_buffer_rsrc_t r_wt = make_rsrc(a.wt, static_cast<long>(N) * K * 2);
+
+  struct Unit {
+    u32x4_t x[KB], h[PK];
+    u32x2_t eh[EN], rs[RN];
+  };
+  auto load_unit = [&](int u, Unit& d) {
+    const long pix = static_cast<long>(u) * 16 + lr;
+    const bool in = pix < m;
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      const uint32_t off = in ? static_cast<uint32_t>((pix * K + kb * 32 + lg * 8) * 2) : BUF_OOB;
+      d.x[kb] = buf_load16(r_src, off);
+      if constexpr (BWD) d.h[kb] = buf_load16(r_h, off);
+    }
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const uint32_t off = in ? static_cast<uint32_t>((pix * N + nb * 16 + lg * 4) * 2) : BUF_OOB;
+      if constexpr (GRAD) d.eh[nb] = buf_load8(r_eph, off);
+      if constexpr (RES) d.rs[nb] = buf_load8(r_res, off);
+    }
+  };
+  const int W = gridDim.x * 4;
+  int u = blockIdx.x * 4 + wave;
+  Unit cur, nxt;
+  if (u < units) load_unit(u, cur);
+
+  Frag<T> wf[NB][KB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      Raw8<T> r;
+      r.set(buf_load16(r_wt, static_cast<uint32_t>(((nb * 16 + lr) * K + kb * 32 + lg * 8) * 2)));
+      wf[nb][kb].set(r);
+    }
+  // BN-backward constants of this lane's input channels, and the epilogue's
+  // per-output-channel constants
+  float pca[PK][8], pcb[PK][8], pcc[PK][8], pmu[PK][8];
+  if constexpr (BWD) {
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int c = kb * 32 + lg * 8 + j;
+        pca[kb][j] = a.pro_ca[c];
+        pcb[kb][j] = a.pro_cb[c];
+        pcc[kb][j] = a.pro_cc[c];
+        pmu[kb][j] = a.pro_mean[c];
+      }
+  }
+  float es[EN][4], esh[EN][4], emu[EN][4], ers[EN][4];
+  if constexpr (GRAD) {
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int c = nb * 16 + lg * 4 + e;
+        es[nb][e] = EP == EP_MASK ? a.ep_scale[c] : 0.f;
+        esh[nb][e] = EP == EP_MASK ? a.ep_shift[c] : 0.f;
+        emu[nb][e] = a.ep_mean[c];
+        ers[nb][e] = a.ep_rstd[c];
+      }
+  }
+
+  float sa[NB][4], sb[NB][4];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) sa[nb][e] = sb[nb][e] = 0.f;
+  for (; u < units; u += W) {
+    const int un = u + W;
+    if (un < units) load_unit(un, nxt);
+    Frag<T> xf[KB];
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      Raw8<T> r;
+      r.set(cur.x[kb]);
+      if constexpr (BWD) {
+        Raw8<T> hr;
+        hr.set(cur.h[kb]);
+        float v[8], h[8];
+        r.to_f32(v);
+        hr.to_f32(h);
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          v[j] = fmaf(pca[kb][j], v[j], fmaf(pcb[kb][j], h[j] - pmu[kb][j], pcc[kb][j]));
+        r.from_f32(v);   // rounded to bf16, as the materialised gradient
+      }
+      xf[kb].set(r);
+    }
+    const long pix = static_cast<long>(u) * 16 + lr;
+    const bool vm = pix < m;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) acc = mfma(wf[nb][kb], xf[kb], acc);
+      float v[4] = {acc[0], acc[1], acc[2], acc[3]};
+      if constexpr (RES) {
+        const u32x2_t rw = cur.rs[nb];
+        v[0] += __uint_as_float(rw.x << 16); v[1] += __uint_as_float(rw.x & 0xffff0000u);
+        v[2] += __uint_as_float(rw.y << 16); v[3] += __uint_as_float(rw.y & 0xffff0000u);
+      }
+      float hl[4] = {0.f, 0.f, 0.f, 0.f};
+      if constexpr (GRAD) {
+        const u32x2_t hw = cur.eh[nb];
+        hl[0] = __uint_as_float(hw.x << 16); hl[1] = __uint_as_float(hw.x & 0xffff0000u);
+        hl[2] = __uint_as_float(hw.y << 16); hl[3] = __uint_as_float(hw.y & 0xffff0000u);
+      }
+      if constexpr (EP == EP_MASK) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = fmaf(es[nb][e], hl[e], esh[nb][e]) > 0.f ? v[e] : 0.f;
+      }
+      const uint32_t w0 = pack_bf16x2(v[0], v[1]), w1 = pack_bf16x2(v[2], v[3]);
+      const uint32_t off =
+          vm ? static_cast<uint32_t>((pix * N + nb * 16 + lg * 4) * 2) : BUF_OOB;
+      buf_store8(u32x2_t{w0, w1}, r_out, off);
+      if constexpr (GRAD) {
+        // partials of the stored values
+        v[0] = __uint_as_float(w0 << 16); v[1] = __uint_as_float(w0 & 0xffff0000u);
+        v[2] = __uint_as_float(w1 << 16); v[3] = __uint_as_float(w1 & 0xffff0000u);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float g = vm ? v[e] : 0.f;
+          sa[nb][e] += g;
+          sb[nb][e] += g * ((hl[e] - emu[nb][e]) * ers[nb][e]);
+        }
+      }
+    }
+    cur = nxt;
+  }
+  if constexpr (GRAD) {
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float x = sum16(sa[nb][e]), y = sum16(sb[nb][e]);
+        if (lr == 0) {
+          const int c = nb * 16 + lg * 4 + e;
+          red[wave][0][c] = x;
+          red[wave][1][c] = y;
+        }
+      }
+    __syncthreads();
+    for (int c = tid; c < N; c += 256) {
+      float t1 = 0.f, t2 = 0.f;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        t1 += red[w][0][c];
+        t2 += red[w][1][c];
+      }
+      const long row = blockIdx.x;
+      a.partials[(row * 2 + 0) * N + c] = t1;
+      a.partials[(row * 2 + 1) * N + c] = t2;
+    }
+  }
+}
+
 // Persistent 3x3 / stride 1 / pad 1 conv for 32 -> 32 bf16 channels (the
 // HBM-bound shapes: C/2 = 32 at 32x32 and 56x56).  A workgroup takes tiles
 // g, g + G, g + 2G, ... of TH x TW output pixels; while the MFMAs of one tile
@@ -2844,6 +3189,64 @@ bool launch_conv32(const C32Shape& c, const ConvArgs& a, int ep, hipStream_t st)
   });
 }
 
+// Streaming 1x1 kernels (conv1x1_kernel, conv1x1_bwd_kernel): stride-1 1x1
+// bf16 convs of the bottleneck widths.  Grid: one workgroup per CU
+// (C1_GRID = the MI355X CU count) or fewer; the grid is also the number of
+// partial rows.  Measured per bottleneck stage step (64x56x56, 12544 units):
+// 256 workgroups 1.933 ms, 512: 1.949, 392: 1.962, 784: 1.985, 3136: 2.40;
+// with fewer workgroups than CU slots the kernels of the step's other streams
+// run beside it.
+constexpr int C1_GRID = 256;
+
+bool use_1x1(int dtype, const ConvArgs& a, int ep) {
+  // every epilogue; the prologue follows from the arguments (EP_STATS takes
+  // none or BN-apply + ReLU, the gradient epilogues none or the BN backward)
+  if (!(dtype == DT_BF16 && a.src2 == nullptr && a.r == 1 && a.s == 1 && a.stride == 1 &&
+        a.pad == 0 && a.p == a.h && a.q == a.w && a.k_tot == a.c_in))
+    return false;
+  if (ep == EP_STATS ? a.pro_h != nullptr : a.pro_scale != nullptr && a.pro_h == nullptr)
+    return false;
+  if (!((a.c_in == 128 && a.c_out == 32) || (a.c_in == 32 && a.c_out == 128))) return false;
+  // byte offsets of the buffer loads/stores are 32-bit
+  return static_cast<long>(a.m) * 128 * 2 < static_cast<long>(BUF_OOB);
+}
+
+int conv1x1_units(const ConvArgs& a) { return (a.m + 15) / 16; }
+
+int conv1x1_grid(const ConvArgs& a) {
+  return std::max(1, std::min(C1_GRID, (conv1x1_units(a) + 3) / 4));
+}
+
+template <int K, int N>
+void launch_1x1_kn(const ConvArgs& a, hipStream_t st) {
+  const dim3 grid(conv1x1_grid(a));
+  if (pro_mode(a) == PRO_RELU)
+    PETRA_LAUNCH((conv1x1_kernel<K, N, PRO_RELU>), grid, dim3(256), 0, st, a, conv1x1_units(a));
+  else
+    PETRA_LAUNCH((conv1x1_kernel<K, N, PRO_NONE>), grid, dim3(256), 0, st, a, conv1x1_units(a));
+}
+
+template <int K, int N>
+bool launch_1x1_bwd_kn(const ConvArgs& a, int ep, hipStream_t st) {
+  const dim3 grid(conv1x1_grid(a));
+  return dispatch_ep_pro(ep, pro_mode(a), [&](auto k) {
+    if constexpr (decltype(k)::ep != EP_STATS)
+      PETRA_LAUNCH((conv1x1_bwd_kernel<K, N, decltype(k)::ep, decltype(k)::pro>), grid,
+                   dim3(256), 0, st, a, conv1x1_units(a));
+  });
+}
+
+bool launch_1x1(const ConvArgs& a, int ep, hipStream_t st) {
+  if (ep != EP_STATS)
+    return a.c_in == 128 ? launch_1x1_bwd_kn<128, 32>(a, ep, st)
+                         : launch_1x1_bwd_kn<32, 128>(a, ep, st);
+  if (a.c_in == 128)
+    launch_1x1_kn<128, 32>(a, st);
+  else
+    launch_1x1_kn<32, 128>(a, st);
+  return true;
+}
+
 // Returns -1 when no halo kernel applies, else whether the launch was made.
 int launch_halo_any(int dtype, const ConvArgs& a, int ep, hipStream_t st) {
   if (use_img(dtype, a)) return launch_img<16, 16, 4>(a, ep, st) ? 1 : 0;
@@ -3113,7 +3516,8 @@ void wgrad_t(const WgradArgs& a, hipStream_t st) {
 
 }  // namespace
 
-int conv_row_tiles(int dtype, const ConvArgs& a) {
+int conv_row_tiles(int dtype, const ConvArgs& a, int ep) {
+  if (use_1x1(dtype, a, ep)) return conv1x1_grid(a);
   if (use_img(dtype, a)) return a.n;
   const C32Shape c32 = conv32_shape(dtype, a);
   if (c32.th != 0) return c32.grid;
@@ -3125,6 +3529,7 @@ int conv_row_tiles(int dtype, const ConvArgs& a) {
 }
 
 bool conv_gemm(int dtype, const ConvArgs& a, int ep, hipStream_t st) {
+  if (use_1x1(dtype, a, ep)) return launch_1x1(a, ep, st);
   const int h = launch_halo_any(dtype, a, ep, st);
   if (h >= 0) return h == 1;
   if (use_staged(dtype, a)) return launch_staged_tiles(a, ep, st);

@@ -68,8 +68,9 @@ constexpr int CONV_BM = 128;  // rows per conv output tile (= partial-sum tile)
 // prologue pair (EP_STATS takes PRO_NONE or PRO_RELU, the others PRO_NONE or
 // PRO_BWD).
 bool conv_gemm(int dtype, const ConvArgs& a, int ep, hipStream_t st);
-// Number of partial-sum rows (output row tiles) conv_gemm writes for these arguments.
-int conv_row_tiles(int dtype, const ConvArgs& a);
+// Number of partial-sum rows (output row tiles) conv_gemm writes for these
+// arguments and epilogue.
+int conv_row_tiles(int dtype, const ConvArgs& a, int ep);
 void conv_wgrad(int dtype, const WgradArgs& a, hipStream_t st);
 // Transposed-read weight-gradient kernel: configuration (0 = not applicable)
 // and its split count (partial rows) for these arguments; conv_wgrad uses it

@@ -222,7 +222,7 @@ Net::Net(const petra_net_desc& d) : desc(d) {
     f.m = static_cast<int>(s.M);
     f.c_split = s.first ? s.Cin : s.Cin / 2;
     f.src2 = s.first ? nullptr : reinterpret_cast<const void*>(16);  // marks the two-tensor input
-    const int tiles = std::max(std::max(conv_row_tiles(dt, f), split_tiles(s.M, s.C)), 1);
+    const int tiles = std::max(std::max(conv_row_tiles(dt, f, EP_STATS), split_tiles(s.M, s.C)), 1);
     const size_t part = static_cast<size_t>(tiles) * 3 * s.C * sizeof(float);
     const size_t bnp = static_cast<size_t>(8) * s.C * sizeof(float);
     s.o_fh = take(act);
@@ -424,7 +424,7 @@ void Net::front_forward(NetStage& s, const void* in1, const void* in2, hipStream
   a.m = static_cast<int>(s.M);
   conv_gemm(dt, a, EP_STATS, q);
   float* v = at<float>(keep ? s.o_bbnp : s.o_fbnp);
-  bn_stats_finalize(static_cast<const float*>(a.partials), conv_row_tiles(dt, a), s.C, s.M,
+  bn_stats_finalize(static_cast<const float*>(a.partials), conv_row_tiles(dt, a, EP_STATS), s.C, s.M,
                     theta + s.off_front_g, theta + s.off_front_b, desc.bn_eps, v, v + s.C,
                     v + 2 * s.C, v + 3 * s.C, keep ? rmean + s.run_front : nullptr,
                     keep ? rvar + s.run_front : nullptr, desc.bn_momentum, q);
@@ -490,7 +490,7 @@ void Net::front_backward(NetStage& s, const void* in1, const void* in2, const vo
   float* cc = v + 6 * s.C;
   if (recompute) {
     conv_gemm(dt, a, EP_STATS, q);
-    bn_stats_finalize(at<float>(s.o_bpart), conv_row_tiles(dt, a), s.C, s.M, fv.gamma,
+    bn_stats_finalize(at<float>(s.o_bpart), conv_row_tiles(dt, a, EP_STATS), s.C, s.M, fv.gamma,
                       fv.beta, desc.bn_eps, scale, shift, mean, rstd, rmean + s.run_front,
                       rvar + s.run_front, desc.bn_momentum, q);
   }

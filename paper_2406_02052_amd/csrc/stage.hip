@@ -113,10 +113,12 @@ Stage::Stage(const petra_stage_desc& d) : desc(d) {
   for (const ConvLayer& cv : convs) {
     ConvArgs f = conv_args(cv);
     f.c_in = cv.cin; f.c_out = cv.cout; f.k_tot = cv.r * cv.s * cv.cin;
-    tiles_max = std::max(tiles_max, conv_row_tiles(dt, f));
     ConvArgs g = conv_args(cv);
     g.c_in = cv.cout; g.c_out = cv.cin; g.k_tot = cv.r * cv.s * cv.cout;
-    tiles_max = std::max(tiles_max, conv_row_tiles(dt, g));
+    for (int ep : {EP_STATS, EP_MASK, EP_RESID_STATS}) {
+      tiles_max = std::max(tiles_max, conv_row_tiles(dt, f, ep));
+      tiles_max = std::max(tiles_max, conv_row_tiles(dt, g, ep));
+    }
   }
   // each conv layer has its own weight-gradient partials, so their reduces can
   // wait until the end of the backward and run as one launch
@@ -292,7 +294,7 @@ void Stage::fn_recompute(const ResidualFn& fn, const void* u, Scratch& s, bool r
     a.c_out = cv.cout;
     a.k_tot = cv.r * cv.s * cv.cin;
     a.partials = s.part;
-    const int tiles = conv_row_tiles(dt, a);
+    const int tiles = conv_row_tiles(dt, a, EP_STATS);
     prof.begin(st);
     conv(a, EP_STATS, st);
     prof.end(K_CONV_FPROP, st, 2.0 * M * cv.cout * a.k_tot,
@@ -381,7 +383,7 @@ void Stage::fn_grad(const BwdFn& f, Scratch& s, const BwdFn* next, Scratch* sn, 
       a.ep_mean = s.vec(l - 1, V_MEAN, cmax);
       a.ep_rstd = s.vec(l - 1, V_RSTD, cmax);
       a.partials = s.bpart;
-      const int tiles_conv = conv_row_tiles(dt, a);
+      const int tiles_conv = conv_row_tiles(dt, a, EP_MASK);
       prof.begin(st);
       conv(a, EP_MASK, st);
       prof.end(K_CONV_DGRAD, st, 2.0 * M * cv.cin * a.k_tot, dbytes);
@@ -405,7 +407,7 @@ void Stage::fn_grad(const BwdFn& f, Scratch& s, const BwdFn* next, Scratch* sn, 
         a.ep_mean = sn->vec(NL, V_MEAN, cmax);
         a.ep_rstd = sn->vec(NL, V_RSTD, cmax);
         a.partials = sn->gpart;
-        sn->gtiles = conv_row_tiles(dt, a);
+        sn->gtiles = conv_row_tiles(dt, a, EP_RESID_STATS);
         prof.begin(st);
         conv(a, EP_RESID_STATS, st);
         prof.end(K_CONV_DGRAD, st, 2.0 * M * cv.cin * a.k_tot, dbytes + 2.0 * esz * M * cv.cin);

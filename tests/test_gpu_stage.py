@@ -33,6 +33,13 @@ SMALL = {
     "bf16_halo_c64_2x9x16": synth.CIFAR_STAGE.with_(n=2, h=9, w=16, c_half=64, blocks=1),
     "bf16_halo_c128_1x9x16": synth.IMAGENET32_STAGE.with_(n=1, h=9, w=16, blocks=2),
     "bf16_halo_bottleneck_1x5x56": synth.IMAGENET_BOTTLENECK_STAGE.with_(n=1, h=5, w=56, blocks=1),
+    # streaming 1x1 convs (128 -> 32, 32 -> 128): 1587 pixels = 100 units of 16
+    # (the last one 3 pixels) over 25 workgroups; 18769 pixels = 1174 units (the
+    # last one a single pixel) over the full 256-workgroup grid, 1-2 units a wave
+    "bf16_bottleneck_1x1_3x23x23": synth.IMAGENET_BOTTLENECK_STAGE.with_(n=3, h=23, w=23,
+                                                                          blocks=1),
+    "bf16_bottleneck_1x1_1x137x137": synth.IMAGENET_BOTTLENECK_STAGE.with_(n=1, h=137, w=137,
+                                                                            blocks=1),
 }
 
 
