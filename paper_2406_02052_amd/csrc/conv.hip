@@ -1495,6 +1495,37 @@ __global__ __launch_bounds__(64 * NWM * NWN, 1) void conv_img_kernel(ConvArgs a)
   }
 }
 
+// Output tile of one 16-pixel unit of the 1x1 kernels, staged in a
+// wave-private LDS slice: the MFMA leaves each lane 4 channels (8 bytes) of one
+// pixel; read back row-major, every lane stores 16 contiguous bytes and one
+// store instruction covers 1 KB of consecutive output rows.  LDS operations of
+// a wave complete in order, so no barrier is needed between the writes and the
+// reads, nor before the next unit overwrites the slice.
+template <int N>
+struct UnitTile {
+  static constexpr int ROW = N / 2 + 2;        // 32-bit words per pixel row (+ pad)
+  static constexpr int CHUNKS = 16 * N / 8;    // 16-byte chunks per unit
+  static_assert(CHUNKS % 64 == 0, "whole chunks per lane");
+  uint32_t w[16 * ROW];
+  __device__ __forceinline__ void put(int lr, int lg, int nb, uint32_t w0, uint32_t w1) {
+    uint32_t* p = w + lr * ROW + (nb * 16 + lg * 4) / 2;
+    *reinterpret_cast<u32x2_t*>(p) = u32x2_t{w0, w1};
+  }
+  // stores the unit's valid rows (pixels u*16 .. u*16 + 15 below m) through r_out
+  __device__ __forceinline__ void store(__amdgpu_buffer_rsrc_t r_out, int u, long m, int lane) {
+#pragma unroll
+    for (int i = 0; i < CHUNKS / 64; ++i) {
+      const int q = lane + 64 * i;
+      const int px = q / (N / 8), ch = q - px * (N / 8);
+      const uint32_t* p = w + px * ROW + ch * 4;
+      const u32x4_t v = u32x4_t{p[0], p[1], p[2], p[3]};
+      const long pix = static_cast<long>(u) * 16 + px;
+      const uint32_t off = pix < m ? static_cast<uint32_t>((pix * N + ch * 8) * 2) : BUF_OOB;
+      buf_store16(v, r_out, off);
+    }
+  }
+};
+
 // 1x1 / stride 1 bf16 convolution with the BN-statistics epilogue, for the
 // HBM-bound bottleneck widths (C_in x C_out = 128 x 32 and 32 x 128).  There is
 // no LDS staging: a wave loads the 16 x K activation block of a 16-pixel unit
@@ -1513,6 +1544,7 @@ __global__ __launch_bounds__(256) void conv1x1_kernel(ConvArgs a, int units) {
   static_assert(K % 32 == 0 && N % 16 == 0 && PRO != PRO_BWD, "1x1 shape");
   constexpr int PK = PRO == PRO_RELU ? KB : 1;
   __shared__ float red[4][3][N];
+  __shared__ __attribute__((aligned(16))) UnitTile<N> otile[4];
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
@@ -1590,9 +1622,7 @@ __global__ __launch_bounds__(256) void conv1x1_kernel(ConvArgs a, int units) {
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb) acc = mfma(wf[nb][kb], xf[kb], acc);
       const uint32_t w0 = pack_bf16x2(acc[0], acc[1]), w1 = pack_bf16x2(acc[2], acc[3]);
-      const uint32_t off =
-          vm ? static_cast<uint32_t>((pix * N + nb * 16 + lg * 4) * 2) : BUF_OOB;
-      buf_store8(u32x2_t{w0, w1}, r_out, off);
+      otile[wave].put(lr, lg, nb, w0, w1);
       // statistics of the stored values
       float v[4];
       v[0] = __uint_as_float(w0 << 16); v[1] = __uint_as_float(w0 & 0xffff0000u);
@@ -1609,6 +1639,7 @@ __global__ __launch_bounds__(256) void conv1x1_kernel(ConvArgs a, int units) {
         sb[nb][e] = fmaf(d, d, sb[nb][e]);
       }
     }
+    otile[wave].store(r_out, u, m, lane);
     first = false;
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb) xr[kb] = xn[kb];
@@ -1669,6 +1700,7 @@ __global__ __launch_bounds__(256) void conv1x1_bwd_kernel(ConvArgs a, int units)
   constexpr int EN = GRAD ? NB : 1;
   constexpr int RN = RES ? NB : 1;
   __shared__ float red[4][2][N];
+  __shared__ __attribute__((aligned(16))) UnitTile<N> otile[4];
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
@@ -1796,9 +1828,7 @@ __global__ __launch_bounds__(256) void conv1x1_bwd_kernel(ConvArgs a, int units)
         for (int e = 0; e < 4; ++e) v[e] = fmaf(es[nb][e], hl[e], esh[nb][e]) > 0.f ? v[e] : 0.f;
       }
       const uint32_t w0 = pack_bf16x2(v[0], v[1]), w1 = pack_bf16x2(v[2], v[3]);
-      const uint32_t off =
-          vm ? static_cast<uint32_t>((pix * N + nb * 16 + lg * 4) * 2) : BUF_OOB;
-      buf_store8(u32x2_t{w0, w1}, r_out, off);
+      otile[wave].put(lr, lg, nb, w0, w1);
       if constexpr (GRAD) {
         // partials of the stored values
         v[0] = __uint_as_float(w0 << 16); v[1] = __uint_as_float(w0 & 0xffff0000u);
@@ -1811,6 +1841,7 @@ __global__ __launch_bounds__(256) void conv1x1_bwd_kernel(ConvArgs a, int units)
         }
       }
     }
+    otile[wave].store(r_out, u, m, lane);
     cur = nxt;
   }
   if constexpr (GRAD) {
