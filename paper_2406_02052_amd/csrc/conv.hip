@@ -1495,21 +1495,46 @@ __global__ __launch_bounds__(64 * NWM * NWN, 1) void conv_img_kernel(ConvArgs a)
   }
 }
 
-// Output tile of one 16-pixel unit of the 1x1 kernels, staged in a
-// wave-private LDS slice: the MFMA leaves each lane 4 channels (8 bytes) of one
-// pixel; read back row-major, every lane stores 16 contiguous bytes and one
-// store instruction covers 1 KB of consecutive output rows.  LDS operations of
-// a wave complete in order, so no barrier is needed between the writes and the
-// reads, nor before the next unit overwrites the slice.
+// [16 pixels][N] bf16 tile of one unit of the 1x1 kernels, in a wave-private
+// LDS slice.  The MFMA leaves each lane 4 channels (8 bytes) of one pixel; the
+// global side moves whole rows instead, every lane 16 contiguous bytes, so one
+// load or store instruction covers 1 KB of consecutive rows.  LDS operations of
+// a wave complete in order, so no barrier is needed between writes and reads,
+// nor before the next unit overwrites the slice.
 template <int N>
 struct UnitTile {
   static constexpr int ROW = N / 2 + 2;        // 32-bit words per pixel row (+ pad)
   static constexpr int CHUNKS = 16 * N / 8;    // 16-byte chunks per unit
   static_assert(CHUNKS % 64 == 0, "whole chunks per lane");
+  static constexpr int PER_LANE = CHUNKS / 64;
   uint32_t w[16 * ROW];
   __device__ __forceinline__ void put(int lr, int lg, int nb, uint32_t w0, uint32_t w1) {
     uint32_t* p = w + lr * ROW + (nb * 16 + lg * 4) / 2;
     *reinterpret_cast<u32x2_t*>(p) = u32x2_t{w0, w1};
+  }
+  __device__ __forceinline__ u32x2_t get(int lr, int lg, int nb) const {
+    return *reinterpret_cast<const u32x2_t*>(w + lr * ROW + (nb * 16 + lg * 4) / 2);
+  }
+  // row-major loads of the unit's rows of a [m][N] tensor (zeros past m)
+  static __device__ __forceinline__ void load_rows(__amdgpu_buffer_rsrc_t r, int u, long m,
+                                                   int lane, u32x4_t* q) {
+#pragma unroll
+    for (int i = 0; i < PER_LANE; ++i) {
+      const int c = lane + 64 * i;
+      const int px = c / (N / 8), ch = c - px * (N / 8);
+      const long pix = static_cast<long>(u) * 16 + px;
+      q[i] = buf_load16(r, pix < m ? static_cast<uint32_t>((pix * N + ch * 8) * 2) : BUF_OOB);
+    }
+  }
+  __device__ __forceinline__ void park_rows(const u32x4_t* q, int lane) {
+#pragma unroll
+    for (int i = 0; i < PER_LANE; ++i) {
+      const int c = lane + 64 * i;
+      const int px = c / (N / 8), ch = c - px * (N / 8);
+      uint32_t* p = w + px * ROW + ch * 4;
+      *reinterpret_cast<u32x2_t*>(p) = u32x2_t{q[i][0], q[i][1]};
+      *reinterpret_cast<u32x2_t*>(p + 2) = u32x2_t{q[i][2], q[i][3]};
+    }
   }
   // stores the unit's valid rows (pixels u*16 .. u*16 + 15 below m) through r_out
   __device__ __forceinline__ void store(__amdgpu_buffer_rsrc_t r_out, int u, long m, int lane) {
@@ -1698,9 +1723,9 @@ __global__ __launch_bounds__(256) void conv1x1_bwd_kernel(ConvArgs a, int units)
   static_assert(K % 32 == 0 && N % 16 == 0 && EP != EP_STATS && PRO != PRO_RELU, "1x1 shape");
   constexpr int PK = BWD ? KB : 1;
   constexpr int EN = GRAD ? NB : 1;
-  constexpr int RN = RES ? NB : 1;
   __shared__ float red[4][2][N];
-  __shared__ __attribute__((aligned(16))) UnitTile<N> otile[4];
+  __shared__ __attribute__((aligned(16))) UnitTile<N> otile[4];   // residual in, result out
+  __shared__ __attribute__((aligned(16))) UnitTile<N> etile[GRAD ? 4 : 1];
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
@@ -1715,9 +1740,11 @@ __global__ __launch_bounds__(256) void conv1x1_bwd_kernel(ConvArgs a, int units)
       make_rsrc(a.resid != nullptr ? a.resid : a.out, a.resid != nullptr ? out_bytes : 0);
   const __amdgpu_buffer_rsrc_t r_wt = make_rsrc(a.wt, static_cast<long>(N) * K * 2);
 
+  using Tile = UnitTile<N>;
+  constexpr int CH = Tile::PER_LANE;
   struct Unit {
     u32x4_t x[KB], h[PK];
-    u32x2_t eh[EN], rs[RN];
+    u32x4_t eh[GRAD ? CH : 1], rs[RES ? CH : 1];   // epilogue operands, row-major
   };
   auto load_unit = [&](int u, Unit& d) {
     const long pix = static_cast<long>(u) * 16 + lr;
@@ -1728,12 +1755,8 @@ __global__ __launch_bounds__(256) void conv1x1_bwd_kernel(ConvArgs a, int units)
       d.x[kb] = buf_load16(r_src, off);
       if constexpr (BWD) d.h[kb] = buf_load16(r_h, off);
     }
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      const uint32_t off = in ? static_cast<uint32_t>((pix * N + nb * 16 + lg * 4) * 2) : BUF_OOB;
-      if constexpr (GRAD) d.eh[nb] = buf_load8(r_eph, off);
-      if constexpr (RES) d.rs[nb] = buf_load8(r_res, off);
-    }
+    if constexpr (GRAD) Tile::load_rows(r_eph, u, m, lane, d.eh);
+    if constexpr (RES) Tile::load_rows(r_res, u, m, lane, d.rs);
   };
   const int W = gridDim.x * 4;
   int u = blockIdx.x * 4 + wave;
@@ -1806,6 +1829,9 @@ __global__ __launch_bounds__(256) void conv1x1_bwd_kernel(ConvArgs a, int units)
     }
     const long pix = static_cast<long>(u) * 16 + lr;
     const bool vm = pix < m;
+    // epilogue operands to the MFMA layout: each lane reads back 4 channels of its pixel
+    if constexpr (RES) otile[wave].park_rows(cur.rs, lane);
+    if constexpr (GRAD) etile[wave].park_rows(cur.eh, lane);
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
       f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
@@ -1813,13 +1839,13 @@ __global__ __launch_bounds__(256) void conv1x1_bwd_kernel(ConvArgs a, int units)
       for (int kb = 0; kb < KB; ++kb) acc = mfma(wf[nb][kb], xf[kb], acc);
       float v[4] = {acc[0], acc[1], acc[2], acc[3]};
       if constexpr (RES) {
-        const u32x2_t rw = cur.rs[nb];
+        const u32x2_t rw = otile[wave].get(lr, lg, nb);
         v[0] += __uint_as_float(rw.x << 16); v[1] += __uint_as_float(rw.x & 0xffff0000u);
         v[2] += __uint_as_float(rw.y << 16); v[3] += __uint_as_float(rw.y & 0xffff0000u);
       }
       float hl[4] = {0.f, 0.f, 0.f, 0.f};
       if constexpr (GRAD) {
-        const u32x2_t hw = cur.eh[nb];
+        const u32x2_t hw = etile[wave].get(lr, lg, nb);
         hl[0] = __uint_as_float(hw.x << 16); hl[1] = __uint_as_float(hw.x & 0xffff0000u);
         hl[2] = __uint_as_float(hw.y << 16); hl[3] = __uint_as_float(hw.y & 0xffff0000u);
       }
