@@ -637,6 +637,44 @@ __global__ __launch_bounds__(256) void conv_staged_kernel(ConvArgs a) {
   }
 }
 
+// Epilogue operands of one lane of epilogue_cp (the pre-BN tensor of the BN
+// below, the residual), loaded at the same offsets; a kernel that knows its
+// tile from the start issues them with its first operand loads, so their
+// latency hides behind the MFMAs instead of stalling the epilogue.
+template <int FM, int FN>
+struct EpiOps {
+  u32x2_t h[FM][FN], r[FM][FN];
+};
+
+template <int TW, int FM, int FN, int TM, int TN, int EP>
+__device__ __forceinline__ void epilogue_load(EpiOps<FM, FN>& o, const ConvArgs& a, int img,
+                                              int p0, int q0, int n0, int wm, int wn, int lane) {
+  constexpr bool GRAD = EP == EP_MASK || EP == EP_RESID_STATS;
+  constexpr bool RES = EP == EP_RESID || EP == EP_RESID_STATS;
+  if constexpr (GRAD || RES) {
+    const int lr = lane & 15, lg = lane >> 4;
+    const long out_bytes = static_cast<long>(a.m) * a.c_out * 2;
+    const __amdgpu_buffer_rsrc_t r_eph = make_rsrc(a.ep_h != nullptr ? a.ep_h : a.out, out_bytes);
+    const __amdgpu_buffer_rsrc_t r_res = make_rsrc(a.resid != nullptr ? a.resid : a.out,
+                                                   a.resid != nullptr ? out_bytes : 0);
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm) {
+      const int i = wm * TM + fm * 16 + lr;
+      const int ph = i / TW, pw = i - ph * TW;
+      const bool vm = p0 + ph < a.h && q0 + pw < a.w;
+      const long pix = (static_cast<long>(img) * a.h + p0 + ph) * a.w + q0 + pw;
+#pragma unroll
+      for (int fn = 0; fn < FN; ++fn) {
+        const int c0 = n0 + wn * TN + fn * 16 + lg * 4;
+        const uint32_t boff =
+            vm && c0 < a.c_out ? static_cast<uint32_t>((pix * a.c_out + c0) * 2) : BUF_OOB;
+        if constexpr (GRAD) o.h[fm][fn] = buf_load8(r_eph, boff);
+        if constexpr (RES) o.r[fm][fn] = buf_load8(r_res, boff);
+      }
+    }
+  }
+}
+
 // Epilogue for accumulators issued as D[cout][pixel] (the MFMA's A operand is
 // the weight fragment): lane (lr, lg) of fragment (fm, fn) holds output channels
 // n0 + wn*TN + fn*16 + lg*4 + e of tile pixel wm*TM + fm*16 + lr, pixel i of the
@@ -649,7 +687,8 @@ template <int TW, int FM, int FN, int WAVES_M, int TM, int TN, int BN, int EP>
 __device__ __forceinline__ void epilogue_cp(const f32x4_t (&acc)[FM][FN], const ConvArgs& a,
                                             int img, int p0, int q0, int n0, int wm, int wn,
                                             int lane, int tid, int nthreads,
-                                            float (*red)[3][BN]) {
+                                            float (*red)[3][BN],
+                                            const EpiOps<FM, FN>* pre = nullptr) {
   const int lr = lane & 15, lg = lane >> 4;
   const long out_bytes = static_cast<long>(a.m) * a.c_out * 2;
   const __amdgpu_buffer_rsrc_t r_out = make_rsrc(a.out, out_bytes);
@@ -698,12 +737,13 @@ __device__ __forceinline__ void epilogue_cp(const f32x4_t (&acc)[FM][FN], const 
       float v[4] = {acc[fm][fn][0], acc[fm][fn][1], acc[fm][fn][2], acc[fm][fn][3]};
       float hl[4] = {0.f, 0.f, 0.f, 0.f};
       if constexpr (GRAD) {
-        const u32x2_t hw = buf_load8(r_eph, boff);
+        const u32x2_t hw = pre != nullptr ? pre->h[fm][fn] : buf_load8(r_eph, boff);
         hl[0] = __uint_as_float(hw.x << 16); hl[1] = __uint_as_float(hw.x & 0xffff0000u);
         hl[2] = __uint_as_float(hw.y << 16); hl[3] = __uint_as_float(hw.y & 0xffff0000u);
       }
       if constexpr (EP == EP_RESID || EP == EP_RESID_STATS) {
-        const u32x2_t rw = buf_load8(r_res, boff);   // a null residual reads zeros
+        // a null residual reads zeros
+        const u32x2_t rw = pre != nullptr ? pre->r[fm][fn] : buf_load8(r_res, boff);
         v[0] += __uint_as_float(rw.x << 16); v[1] += __uint_as_float(rw.x & 0xffff0000u);
         v[2] += __uint_as_float(rw.y << 16); v[3] += __uint_as_float(rw.y & 0xffff0000u);
       }
@@ -935,9 +975,12 @@ __global__ __launch_bounds__(256) void conv_halo_kernel(ConvArgs a) {
 #pragma unroll
     for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  // Operand loads go out first; the prologue table is fetched while they fly.
+  // Operand loads go out first, then this tile's epilogue operands; the
+  // prologue table is fetched while they fly.
   load_patch(0);
   load_slab(0);
+  EpiOps<FM, FN> epi;
+  epilogue_load<TW, FM, FN, TM, TN, EP>(epi, a, img, p0, q0, n0, wm, wn, lane);
   if constexpr (PRO == PRO_RELU) {
     for (int i = tid; i < a.c_in; i += 256) {
       pro_tab[0][i] = a.pro_scale[i];
@@ -1009,7 +1052,7 @@ __global__ __launch_bounds__(256) void conv_halo_kernel(ConvArgs a) {
 
   // acc holds D[cout][pixel] (weights are the MFMA's A operand)
   epilogue_cp<TW, FM, FN, WAVES_M, TM, TN, BN, EP>(acc, a, img, p0, q0, n0, wm, wn, lane, tid, 256,
-                                                   red3);
+                                                   red3, &epi);
 }
 
 template <int TH, int TW, int BN, int WAVES_M, int CH, int EP, int PRO>
