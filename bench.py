@@ -6,10 +6,15 @@ current parameters, then the in-place SGD update (Eq. 5).  Inputs are seeded
 synthetic tensors already resident in HBM; the timed region covers exactly
 --steps steps between two device synchronisations.
 
-Prints one JSON line with the throughput (images/s per stage step), the
-roofline position of the dominant kernel class (per-launch HIP events on the
-launching stream, in a second pass of the same steps) and the CPU oracle's
-throughput on a bounded sample of the same workload.
+The headline is the ImageNet-shaped RevNet-50 bottleneck stage (64 x 56 x 56,
+256 channels, 3 blocks); the CIFAR- and ImageNet32-shaped stages and the
+four-stage schedule follow in the same run under "configs", each with its own
+figures.  Per stage workload: throughput, the serialized step, a cold-cache
+variant, the roofline position of the dominant kernel (per-launch HIP events
+on the launching stream, in a second pass of the same steps), the
+convolutions' MFMA fraction and the BN / elementwise kernels' HBM fraction,
+and the CPU oracle's throughput on a bounded sample (fp64 and fp32).  Prints
+one JSON line.
 """
 from __future__ import annotations
 
@@ -35,12 +40,16 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=100)
     p.add_argument("--warmup", type=int, default=20)
-    p.add_argument("--workload", default=synth.CIFAR_STAGE.name,
-                   choices=sorted(synth.STAGE_WORKLOADS) + [synth.REVNET18_SCHEDULE.name])
+    p.add_argument("--workload", default=synth.IMAGENET_BOTTLENECK_STAGE.name,
+                   choices=sorted(synth.STAGE_WORKLOADS) + [synth.REVNET18_SCHEDULE.name],
+                   help="the headline workload (default: the ImageNet-shaped bottleneck stage)")
+    p.add_argument("--only", action="store_true",
+                   help="time the headline workload alone (no nested lines for the others)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-profile", action="store_true")
-    p.add_argument("--cpu-seconds", type=float, default=12.0,
-                   help="target duration of the CPU-oracle sample")
+    p.add_argument("--no-cold", action="store_true", help="skip the cold-cache variant")
+    p.add_argument("--cpu-seconds", type=float, default=6.0,
+                   help="target duration of each CPU-oracle sample")
     p.add_argument("--gradient-quality", action="store_true",
                    help="train the schedule (PETRA backward, both buffers kept) and report "
                         "per-stage cosine similarity / norm ratio of the PETRA, delayed and "
@@ -56,6 +65,11 @@ def parse():
     p.add_argument("--copy-calibration", action="store_true",
                    help="only run a plain device copy of 256 MiB ten times (reference kernel "
                         "for scaling the FETCH_SIZE / WRITE_SIZE counters)")
+    p.add_argument("--counters-summary", nargs=5, metavar=("WORKLOAD", "FETCH_DIR", "WRITE_DIR",
+                                                           "COPY_FETCH_DIR", "COPY_WRITE_DIR"),
+                   help="host only: from rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE csv output of "
+                        "the bench command and of --copy-calibration, write the calibrated HBM "
+                        "bytes per dispatch of every kernel into profiles/traffic.json")
     return p.parse_args()
 
 
@@ -87,22 +101,84 @@ def kernel_source_sha():
     return h.hexdigest()[:16]
 
 
-def stored_traffic(workload, kernel):
-    """HBM bytes per launch of `kernel` from the committed counter summary
-    (FETCH_SIZE and WRITE_SIZE, each scaled by the copy calibration), or None
-    when no reading exists or the kernel sources changed since it was taken."""
-    path = os.path.join(ROOT, "profiles", "traffic_counters.md")
-    if not os.path.exists(path):
-        return None
+TRAFFIC_JSON = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def short_kernel_name(name: str) -> str:
+    """'void petra::k<1, 2>(petra::Args)' -> 'petra::k<1, 2>' (the profiler's
+    form): the argument list is the last parenthesised group outside template
+    brackets."""
+    if name.startswith("void "):
+        name = name[5:]
+    depth, cut = 0, -1
+    for i, ch in enumerate(name):
+        depth += ch == "<"
+        depth -= ch == ">"
+        if ch == "(" and depth == 0:
+            cut = i
+    return name if cut < 0 else name[:cut]
+
+
+def _pmc_rows(d, counter):
+    """{kernel: [values per dispatch]} from a rocprofv3 --pmc csv directory."""
+    import csv
+    import glob
+    out = {}
+    for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+        with open(f) as fh:
+            for r in csv.DictReader(fh):
+                if r["Counter_Name"] == counter:
+                    out.setdefault(short_kernel_name(r["Kernel_Name"]), []).append(
+                        float(r["Counter_Value"]))
+    return out
+
+
+def counters_summary(workload, fetch_dir, write_dir, copy_fetch_dir, copy_write_dir):
+    """Calibrated HBM bytes per dispatch of every kernel of a workload's bench
+    run, stored in profiles/traffic.json under the current kernel-source hash."""
+    fetch, write = _pmc_rows(fetch_dir, "FETCH_SIZE"), _pmc_rows(write_dir, "WRITE_SIZE")
+    copy_bytes = 256 << 20
+    cf = [v for k, vs in _pmc_rows(copy_fetch_dir, "FETCH_SIZE").items() if "neg" in k.lower()
+          for v in vs]
+    cw = [v for k, vs in _pmc_rows(copy_write_dir, "WRITE_SIZE").items() if "neg" in k.lower()
+          for v in vs]
+    ff = copy_bytes / (1024.0 * float(np.median(cf)))
+    fw = copy_bytes / (1024.0 * float(np.median(cw)))
     sha = kernel_source_sha()
-    with open(path) as fh:
-        for line in fh:
-            cells = [c.strip().strip("`") for c in line.strip().strip("|").split("|")]
-            if len(cells) >= 5 and cells[0] == workload and cells[1] == kernel and cells[2] == sha:
-                try:
-                    return float(cells[-1])
-                except ValueError:
-                    return None
+    data = {"entries": []}
+    if os.path.exists(TRAFFIC_JSON):
+        with open(TRAFFIC_JSON) as fh:
+            data = json.load(fh)
+    data["entries"] = [e for e in data["entries"] if e["workload"] != workload]
+    for k in sorted(set(fetch) & set(write)):
+        if not k.startswith("petra::"):
+            continue
+        f_kib, w_kib = float(np.mean(fetch[k])), float(np.mean(write[k]))
+        data["entries"].append({
+            "workload": workload, "kernel": k, "kernel_source_sha": sha,
+            "dispatches": len(fetch[k]), "fetch_kib": f_kib, "write_kib": w_kib,
+            "fetch_factor": ff, "write_factor": fw,
+            "hbm_bytes_per_launch": 1024.0 * (f_kib * ff + w_kib * fw)})
+    data["calibration"] = ("one torch.neg dispatch over 256 MiB (reads and writes 256 MiB); "
+                           "factor = bytes moved / (counter KiB x 1024)")
+    with open(TRAFFIC_JSON, "w") as fh:
+        json.dump(data, fh, indent=1)
+        fh.write("\n")
+    print(json.dumps({"workload": workload, "kernel_source_sha": sha, "fetch_factor": ff,
+                      "write_factor": fw, "kernels": len(data["entries"])}))
+
+
+def stored_traffic(workload, kernel):
+    """Calibrated HBM bytes per launch of `kernel` from profiles/traffic.json,
+    or None when no reading exists or the kernel sources changed since."""
+    if not os.path.exists(TRAFFIC_JSON):
+        return None
+    with open(TRAFFIC_JSON) as fh:
+        data = json.load(fh)
+    sha = kernel_source_sha()
+    for e in data.get("entries", []):
+        if e["workload"] == workload and e["kernel"] == kernel and e["kernel_source_sha"] == sha:
+            return e["hbm_bytes_per_launch"]
     return None
 
 
@@ -154,10 +230,26 @@ def timed(torch, fn, steps):
     return time.perf_counter() - t0
 
 
-def roofline(prof, dtype):
-    """Dominant kernel class (largest summed device time) against its roofline."""
-    name = max(prof, key=lambda k: prof[k][1])
-    n, ms, fl, by = prof[name]
+def cold_cache_ms(torch, st, t, steps):
+    """Mean step time with the caches cold: before every step a 512 MiB buffer
+    (twice the 256 MB last-level cache) is rewritten, and only the step itself
+    is timed (HIP events on the stream the step is ordered on)."""
+    flush = torch.empty(128 << 20, dtype=torch.float32, device="cuda:0")
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(steps)]
+    torch.cuda.synchronize()
+    for a, b in evs:
+        flush.fill_(1.0)
+        a.record()
+        one_step(st, t)
+        b.record()
+    torch.cuda.synchronize()
+    return float(np.mean([a.elapsed_time(b) for a, b in evs])), flush.numel() * 4
+
+
+def roofline(kernels, dtype):
+    """Dominant kernel (largest summed device time) against its roofline."""
+    name, cls, n, ms, fl, by = max(kernels, key=lambda k: k[3])
     ridge = PEAK_TFLOPS[dtype] * 1e12 / (PEAK_HBM_GBS * 1e9)
     per_launch_s = ms / 1e3 / n
     if fl > 0 and fl / by >= ridge:
@@ -170,24 +262,48 @@ def roofline(prof, dtype):
     out["frac"] = out["achieved"] / out["peak"]
     out["traffic"] = None
     out["kernel"] = name
-    out["launches_per_step"] = None
+    out["kernel_class"] = cls
+    out["launches"] = n
     out["avg_launch_us"] = per_launch_s * 1e6
     out["algorithmic_per_launch"] = {"flops": fl / n, "bytes": by / n}
     return out
 
 
-def cpu_baseline(wl, target_s):
-    """The oracle (fp64 numpy) timed on one stage step of a bounded sample."""
+CONV_CLASSES = ("conv_fprop", "conv_dgrad", "conv_wgrad")
+HBM_CLASSES = ("bn_finalize", "bn_bwd_finalize", "combine_fwd", "combine_bwd")
+
+
+def targets(prof, dtype):
+    """The convolutions' MFMA fraction and the BN / elementwise kernels' HBM
+    fraction, each over all their launches (summed algorithmic flops or bytes
+    over summed device time), against the peak and the stated targets."""
+    def frac(classes, idx, peak):
+        t = sum(prof[k][1] for k in classes if k in prof) / 1e3
+        q = sum(prof[k][idx] for k in classes if k in prof)
+        return (q / t / peak) if t > 0 else None
+    return {"conv_mfma_frac": frac(CONV_CLASSES, 2, PEAK_TFLOPS[dtype] * 1e12),
+            "conv_mfma_target": 0.5,
+            "bn_elementwise_hbm_frac": frac(HBM_CLASSES, 3, PEAK_HBM_GBS * 1e9),
+            "bn_elementwise_hbm_target": 0.7}
+
+
+def _threads():
     from threadpoolctl import threadpool_info
+    return max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+
+
+def cpu_baseline(wl, target_s):
+    """The oracle timed on one stage step of a bounded sample: fp64 (the
+    parity oracle) and fp32."""
     from oracle.stage import StageState
 
     names = [n for n, _ in wl.param_shapes()]
     params = synth.stage_params(wl)
 
-    def run(n):
+    def run(n, dtype):
         w = wl.with_(n=n)
         st = StageState(params, names, 2 if wl.kind == "basic" else 3, eps=wl.bn_eps,
-                        bn_momentum=wl.bn_momentum)
+                        bn_momentum=wl.bn_momentum, dtype=dtype)
         x1, x2 = synth.stage_input(w)
         g1, g2 = synth.stage_output_grad(w)
         t0 = time.perf_counter()
@@ -195,17 +311,128 @@ def cpu_baseline(wl, target_s):
                 wl.accum_k)
         return time.perf_counter() - t0
 
-    n0 = min(wl.n, 2 if wl.h * wl.w >= 3000 else 4)
-    t0 = run(n0)
-    n = int(min(wl.n, max(n0, n0 * target_s / max(t0, 1e-6))))
-    t = run(n) if n != n0 else t0
-    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    return {"value": n / t, "unit": "images/s", "cores": threads, "kind": "oracle",
-            "sample": f"one fp64 oracle stage step (forward + reconstruct/VJP + update) "
-                      f"on {n} of the {wl.n} images ({t:.1f} s); BN statistics over the sample"}
+    res = {}
+    for dtype, key in ((np.float64, "fp64"), (np.float32, "fp32")):
+        n0 = min(wl.n, 2 if wl.h * wl.w >= 3000 else 4)
+        t0 = run(n0, dtype)
+        n = int(min(wl.n, max(n0, n0 * target_s / max(t0, 1e-6))))
+        t = run(n, dtype) if n != n0 else t0
+        res[key] = (n, t)
+    (n, t), (n32, t32) = res["fp64"], res["fp32"]
+    return {"value": n / t, "unit": "images/s", "cores": _threads(), "kind": "oracle",
+            "sample": f"one fp64 oracle stage step (forward + reconstruct/VJP + update) on {n} "
+                      f"of the {wl.n} images ({t:.1f} s); BN statistics over the sample",
+            "fp32": {"value": n32 / t32, "unit": "images/s",
+                     "sample": f"the same step in fp32 on {n32} images ({t32:.1f} s)"}}
 
 
-def bench_schedule(args):
+def bench_stage(args, wl, cpu=True, cold=True):
+    """One stage workload: petra_stage_step throughput, serialized step, the
+    per-kernel profile with the roofline of the dominant kernel, the cold-cache
+    variant and the CPU oracle."""
+    import torch
+    from paper_2406_02052_amd import (Stage, petra_stage_profile, petra_stage_profile_kernel,
+                                      petra_stage_profile_read)
+
+    st = Stage(wl.n, wl.h, wl.w, wl.c_half, wl.blocks, wl.kind, wl.dtype, c_mid=wl.c_mid,
+               bn_eps=wl.bn_eps, bn_momentum=wl.bn_momentum, device="cuda:0")
+    st.set_params(synth.stage_params(wl))
+    st.set_optimizer(lr=wl.lr, momentum=wl.momentum, weight_decay=wl.weight_decay,
+                     nesterov=wl.nesterov, accum_k=wl.accum_k)
+    t = gpu_inputs(st, wl)
+    for _ in range(args.warmup):
+        one_step(st, t)
+    print(f"[bench] {wl.name}: warm-up done, timing {args.steps} steps", file=sys.stderr,
+          flush=True)
+    el = timed(torch, lambda: one_step(st, t), args.steps)
+    el_serial = timed(torch, lambda: one_step_serial(st, t), args.steps)
+    ms = el / args.steps * 1e3
+    out = {"metric": "images/sec per stage step (fwd+reconstruct+VJP+update)",
+           "value": wl.n * args.steps / el, "unit": "images/s", "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+           "dtype": wl.dtype, "data": "synthetic (seeded; CIFAR/ImageNet-shaped tensors)",
+           "config": {"workload": wl.name, "batch": wl.n, "hw": [wl.h, wl.w],
+                      "channels": 2 * wl.c_half, "blocks": wl.blocks, "block": wl.kind,
+                      "mid_channels": wl.c_mid or None,
+                      "step": "forward || reconstruct+VJP on two streams, then SGD update"},
+           "serial_ms_per_step": el_serial / args.steps * 1e3}
+    if cold:
+        cms, fb = cold_cache_ms(torch, st, t, max(10, args.steps // 4))
+        out["cold_cache"] = {"ms_per_step": cms, "value": wl.n / (cms / 1e3), "unit": "images/s",
+                             "flush_bytes_before_each_step": fb,
+                             "note": "each step timed alone after rewriting a buffer twice "
+                                     "the size of the last-level cache"}
+    if not args.no_profile:
+        petra_stage_profile(st.handle, True)
+        for _ in range(args.steps):
+            one_step(st, t)
+        torch.cuda.synchronize()
+        prof = {k: v for k, v in petra_stage_profile_read(st.handle).items() if v[0] > 0}
+        kern = petra_stage_profile_kernel(st.handle)
+        petra_stage_profile(st.handle, False)
+        rl = roofline(kern, wl.dtype)
+        rl["launches_per_step"] = rl.pop("launches") / args.steps
+        rl["traffic"] = stored_traffic(wl.name, rl["kernel"])
+        rl["kernel_source_sha"] = kernel_source_sha()
+        out["roofline"] = rl
+        out["kernels"] = {name: {"class": cls, "launches_per_step": n / args.steps,
+                                 "avg_us": m * 1e3 / n,
+                                 "tflops": f / (m / 1e3) / 1e12 if f else 0.0,
+                                 "gbs": b / (m / 1e3) / 1e9,
+                                 "share": m / sum(k[3] for k in kern)}
+                          for name, cls, n, m, f, b in sorted(kern, key=lambda k: -k[3])}
+        out["kernel_classes"] = {k: {"launches_per_step": v[0] / args.steps,
+                                     "avg_us": v[1] * 1e3 / v[0], "share":
+                                     v[1] / sum(p[1] for p in prof.values())}
+                                 for k, v in sorted(prof.items(), key=lambda kv: -kv[1][1])}
+        out["targets"] = targets(prof, wl.dtype)
+        conv_ms = sum(prof[k][1] for k in prof if k in CONV_CLASSES)
+        conv_fl = sum(prof[k][2] for k in prof if k in CONV_CLASSES)
+        out["mfma_util_pct"] = 100.0 * conv_fl / (conv_ms / 1e3) / (PEAK_TFLOPS[wl.dtype] * 1e12)
+    finite = all(bool(torch.isfinite(t[k].float()).all()) for k in ("ya1", "xr1", "dx2"))
+    out["outputs_finite"] = finite
+    if cpu:
+        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+    del st
+    return out
+
+
+def cpu_baseline_schedule(target_s):
+    """The oracle's tick simulator timed over 2J+2 ticks of the schedule on a
+    bounded batch (fp64 and fp32), per tick."""
+    from oracle.net import PetraNet
+
+    wl = synth.REVNET18_SCHEDULE
+    names = [nm for nm, _ in synth.net_param_shapes(wl)]
+    params = [p.astype(np.float64) for p in synth.net_params(wl)]
+    J = len(wl.widths)
+
+    def run(n, dtype, ticks):
+        w = wl.with_(n=n)
+        imgs = synth.net_images(w, ticks)
+        labs = synth.net_labels(w, ticks)
+        ref = PetraNet(params, names, J, wl.blocks_per_stage, dtype=dtype)
+        t0 = time.perf_counter()
+        for t in range(ticks):
+            ref.tick(t, lambda m: imgs[m], lambda m: labs[m], ticks, wl.lr, wl.momentum,
+                     wl.weight_decay, wl.nesterov, wl.accum_k)
+        return (time.perf_counter() - t0) / ticks
+
+    res = {}
+    for dtype, key in ((np.float64, "fp64"), (np.float32, "fp32")):
+        per = run(2, dtype, 2)
+        n = int(min(wl.n, max(2, 2 * target_s / max(per * (2 * J + 2), 1e-6))))
+        res[key] = (n, run(n, dtype, 2 * J + 2))
+    (n, t), (n32, t32) = res["fp64"], res["fp32"]
+    return {"value": n / t, "unit": "images/s", "cores": _threads(), "kind": "oracle",
+            "sample": f"fp64 tick simulator, {2 * J + 2} ticks (pipeline fill and steady "
+                      f"state) on {n} of the {wl.n} images, {t:.2f} s per tick",
+            "fp32": {"value": n32 / t32, "unit": "images/s",
+                     "sample": f"the same in fp32 on {n32} images, {t32:.2f} s per tick"}}
+
+
+def bench_schedule(args, cpu=True):
     """Steady-state ticks of the J-stage schedule (every stage busy every tick)."""
     import torch
     from paper_2406_02052_amd import Net
@@ -286,7 +513,10 @@ def bench_schedule(args):
                "step": "one tick of the per-layer split (stem, downsamplings and blocks as "
                        "stages, delays 2(J-1-j))"}}
     out["outputs_finite"] = out["outputs_finite"] and bool(np.isfinite(split_loss))
-    print(json.dumps(out))
+    del snet
+    if cpu:
+        out["cpu_baseline"] = cpu_baseline_schedule(args.cpu_seconds)
+    return out
 
 
 def _cos(a, b):
@@ -425,6 +655,9 @@ def k_sweep(args):
 
 def main():
     args = parse()
+    if args.counters_summary:
+        counters_summary(*args.counters_summary)
+        return
     if args.copy_calibration:
         copy_calibration()
         return
@@ -441,61 +674,25 @@ def main():
     if args.k_sweep:
         k_sweep(args)
         return
-    if args.workload == synth.REVNET18_SCHEDULE.name:
-        bench_schedule(args)
-        return
-    import torch
-    from paper_2406_02052_amd import Stage, petra_stage_profile, petra_stage_profile_read
-
-    wl = synth.STAGE_WORKLOADS[args.workload]
-    st = Stage(wl.n, wl.h, wl.w, wl.c_half, wl.blocks, wl.kind, wl.dtype, c_mid=wl.c_mid,
-               bn_eps=wl.bn_eps, bn_momentum=wl.bn_momentum, device="cuda:0")
-    st.set_params(synth.stage_params(wl))
-    st.set_optimizer(lr=wl.lr, momentum=wl.momentum, weight_decay=wl.weight_decay,
-                     nesterov=wl.nesterov, accum_k=wl.accum_k)
-    t = gpu_inputs(st, wl)
-    for _ in range(args.warmup):
-        one_step(st, t)
-    print(f"[bench] {wl.name}: warm-up done, timing {args.steps} steps", file=sys.stderr,
-          flush=True)
-    el = timed(torch, lambda: one_step(st, t), args.steps)
-    el_serial = timed(torch, lambda: one_step_serial(st, t), args.steps)
-    ms = el / args.steps * 1e3
-    out = {"metric": "images/sec per stage step (fwd+reconstruct+VJP+update)",
-           "value": wl.n * args.steps / el, "unit": "images/s", "n_gpus": 1,
-           "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
-           "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-           "dtype": wl.dtype, "data": "synthetic (seeded; CIFAR/ImageNet-shaped tensors)",
-           "config": {"workload": wl.name, "batch": wl.n, "hw": [wl.h, wl.w],
-                      "channels": 2 * wl.c_half, "blocks": wl.blocks, "block": wl.kind,
-                      "mid_channels": wl.c_mid or None,
-                      "step": "forward || reconstruct+VJP on two streams, then SGD update"},
-           "serial_ms_per_step": el_serial / args.steps * 1e3}
-    if not args.no_profile:
-        petra_stage_profile(st.handle, True)
-        for _ in range(args.steps):
-            one_step(st, t)
-        torch.cuda.synchronize()
-        prof = {k: v for k, v in petra_stage_profile_read(st.handle).items() if v[0] > 0}
-        petra_stage_profile(st.handle, False)
-        rl = roofline(prof, wl.dtype)
-        rl["launches_per_step"] = prof[rl["kernel"]][0] / args.steps
-        rl["traffic"] = stored_traffic(wl.name, rl["kernel"])
-        rl["kernel_source_sha"] = kernel_source_sha()
-        out["roofline"] = rl
-        out["kernels"] = {k: {"launches_per_step": v[0] / args.steps,
-                              "avg_us": v[1] * 1e3 / v[0],
-                              "tflops": v[2] / (v[1] / 1e3) / 1e12 if v[2] else 0.0,
-                              "gbs": v[3] / (v[1] / 1e3) / 1e9,
-                              "share": v[1] / sum(p[1] for p in prof.values())}
-                          for k, v in sorted(prof.items(), key=lambda kv: -kv[1][1])}
-        conv_ms = sum(prof[k][1] for k in prof if k.startswith("conv_"))
-        conv_fl = sum(prof[k][2] for k in prof if k.startswith("conv_"))
-        out["mfma_util_pct"] = 100.0 * conv_fl / (conv_ms / 1e3) / (PEAK_TFLOPS[wl.dtype] * 1e12)
-    finite = all(bool(torch.isfinite(t[k].float()).all()) for k in ("ya1", "xr1", "dx2"))
-    out["outputs_finite"] = finite
-    if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+    cpu = not args.no_cpu_baseline
+    sched = synth.REVNET18_SCHEDULE.name
+    if args.workload == sched:
+        out = bench_schedule(args, cpu=cpu)
+    else:
+        out = bench_stage(args, synth.STAGE_WORKLOADS[args.workload], cpu=cpu,
+                          cold=not args.no_cold)
+    if not args.only:
+        # the other workloads of the build, each with its own line of figures
+        out["configs"] = {}
+        for name in (synth.CIFAR_STAGE.name, synth.IMAGENET32_STAGE.name,
+                     synth.IMAGENET_BOTTLENECK_STAGE.name, sched):
+            if name == args.workload:
+                continue
+            if name == sched:
+                out["configs"][name] = bench_schedule(args, cpu=cpu)
+            else:
+                out["configs"][name] = bench_stage(args, synth.STAGE_WORKLOADS[name], cpu=cpu,
+                                                   cold=not args.no_cold)
     print(json.dumps(out))
 
 

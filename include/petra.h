@@ -76,7 +76,8 @@ typedef enum {
  * running statistics use momentum bn_momentum and move only during the
  * backward recompute (Sec. 4.1, "Model adaptations").
  * Limits: c_half and c_mid are 8 times a power of two, at most 512;
- * N*H*W*max(c_half, c_mid) < 2^31. */
+ * N*H*W*max(c_half, c_mid)*element size < 2^31 bytes (every tensor is
+ * addressed with 32-bit byte offsets); PETRA_ERR_SHAPE otherwise. */
 typedef struct {
   int32_t n, h, w;
   int32_t c_half;
@@ -228,7 +229,8 @@ petra_status petra_stage_step(petra_stage* st, const void* x1, const void* x2, v
  * follows it.
  *
  * Limits: h and w divisible by 2^(num_stages-1); widths[j]/2 is 8 times a
- * power of two, at most 512; c_img <= 8; classes <= 64; num_stages <= 8.
+ * power of two, at most 512; c_img <= 8; classes <= 64; num_stages <= 8;
+ * every stage's activation below 2^31 bytes (as for a stage).
  * ------------------------------------------------------------------------ */
 #define PETRA_MAX_STAGES 8
 
@@ -283,6 +285,17 @@ petra_status petra_net_sync_weights(petra_net* net, void* stream);
  * tells whether one did. */
 petra_status petra_net_tick(petra_net* net, const void* images, const int32_t* labels,
                             float* loss, void* stream, int32_t* loss_written);
+/* Drain the pipeline (Alg. 1 once the input has ended): runs ticks without
+ * input until no micro-batch is in flight, so every micro-batch fed so far
+ * has had its backward in every stage and its updates applied.  Feeding cannot
+ * resume afterwards.  losses (nullable, device fp32, at least petra_net_num_stages()
+ * entries, 16-byte aligned): entry i receives the mean loss of the i-th
+ * micro-batch that reaches the head during the drain; *n_losses (nullable)
+ * their count; *ticks_run (nullable) the ticks this call ran (0 if nothing
+ * was in flight).  Ordered after prior work on `stream`; later work on
+ * `stream` follows every tick. */
+petra_status petra_net_drain(petra_net* net, float* losses, void* stream, int32_t* n_losses,
+                             int32_t* ticks_run);
 /* Ticks run so far, micro-batches fed, and micro-batches still in flight. */
 petra_status petra_net_state(const petra_net* net, int64_t* ticks, int64_t* fed,
                              int64_t* in_flight);
@@ -362,6 +375,14 @@ petra_status petra_stage_profile(petra_stage* st, int32_t enable);
 petra_status petra_stage_profile_read(petra_stage* st, int32_t kernel_class, const char** name,
                                       int64_t* launches, double* total_ms, double* flops,
                                       double* bytes);
+/* The same totals per kernel (template instance) and class, index 0 .. until
+ * it returns PETRA_ERR_INVALID_ARG, in order of first launch since the
+ * profile was enabled: *name receives the kernel's demangled symbol as the
+ * profiler tools print it (valid until the next petra_stage_profile call),
+ * *kernel_class its class index for petra_stage_profile_read. */
+petra_status petra_stage_profile_kernel(petra_stage* st, int32_t index, const char** name,
+                                        int32_t* kernel_class, int64_t* launches,
+                                        double* total_ms, double* flops, double* bytes);
 
 #ifdef __cplusplus
 }

@@ -105,6 +105,8 @@ _SIGS = {
     "petra_net_set_optimizer": (ctypes.c_int, [_VP, ctypes.POINTER(Sgd)]),
     "petra_net_sync_weights": (ctypes.c_int, [_VP, _VP]),
     "petra_net_tick": (ctypes.c_int, [_VP, _VP, _VP, _VP, _VP, ctypes.POINTER(ctypes.c_int32)]),
+    "petra_net_drain": (ctypes.c_int, [_VP, _VP, _VP, ctypes.POINTER(ctypes.c_int32),
+                                       ctypes.POINTER(ctypes.c_int32)]),
     "petra_net_state": (ctypes.c_int, [_VP, ctypes.POINTER(ctypes.c_int64),
                                         ctypes.POINTER(ctypes.c_int64),
                                         ctypes.POINTER(ctypes.c_int64)]),
@@ -122,6 +124,13 @@ _SIGS = {
                                                  ctypes.POINTER(ctypes.c_double),
                                                  ctypes.POINTER(ctypes.c_double),
                                                  ctypes.POINTER(ctypes.c_double)]),
+    "petra_stage_profile_kernel": (ctypes.c_int, [_VP, ctypes.c_int32,
+                                                   ctypes.POINTER(ctypes.c_char_p),
+                                                   ctypes.POINTER(ctypes.c_int32),
+                                                   ctypes.POINTER(ctypes.c_int64),
+                                                   ctypes.POINTER(ctypes.c_double),
+                                                   ctypes.POINTER(ctypes.c_double),
+                                                   ctypes.POINTER(ctypes.c_double)]),
 }
 
 _lib: Optional[ctypes.CDLL] = None
@@ -278,6 +287,25 @@ def petra_stage_profile_read(handle):
         i += 1
 
 
+def petra_stage_profile_kernel(handle):
+    """Per kernel instance: [(name, class index, launches, total_ms, flops, bytes)]."""
+    out = []
+    i = 0
+    while True:
+        name = ctypes.c_char_p()
+        k, n, ms = ctypes.c_int32(), ctypes.c_int64(), ctypes.c_double()
+        fl, by = ctypes.c_double(), ctypes.c_double()
+        st = load().petra_stage_profile_kernel(handle, i, ctypes.byref(name), ctypes.byref(k),
+                                               ctypes.byref(n), ctypes.byref(ms), ctypes.byref(fl),
+                                               ctypes.byref(by))
+        if st != 0:
+            if STATUS[st] == "PETRA_ERR_INVALID_ARG":
+                return out
+            _check(st, "petra_stage_profile_kernel")
+        out.append((name.value.decode(), k.value, n.value, ms.value, fl.value, by.value))
+        i += 1
+
+
 # ---- multi-stage schedule ----------------------------------------------------
 
 def petra_net_create(desc: NetDesc) -> int:
@@ -324,6 +352,14 @@ def petra_net_tick(handle, images, labels, loss=None, stream=None) -> bool:
     _check(load().petra_net_tick(handle, _ptr(images), _ptr(labels), _ptr(loss), _stream(stream),
                                  ctypes.byref(wrote)), "petra_net_tick")
     return bool(wrote.value)
+
+
+def petra_net_drain(handle, losses=None, stream=None):
+    """Returns (losses written, ticks run)."""
+    nl, nt = ctypes.c_int32(), ctypes.c_int32()
+    _check(load().petra_net_drain(handle, _ptr(losses), _stream(stream), ctypes.byref(nl),
+                                  ctypes.byref(nt)), "petra_net_drain")
+    return nl.value, nt.value
 
 
 def petra_net_backprop_step(handle, images, labels, loss=None, stream=None) -> None:

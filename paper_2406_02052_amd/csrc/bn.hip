@@ -10,7 +10,7 @@
 
 namespace petra {
 
-namespace {
+namespace bnk {
 
 // Finalize kernels: one 256-thread block per channel.  Thread t takes tiles
 // t, t + 256, ... (loads of up to FIN_U tiles in flight), then the block's
@@ -268,7 +268,8 @@ unsigned ew_grid(long total8) {
   return static_cast<unsigned>(b);
 }
 
-}  // namespace
+}  // namespace bnk
+using namespace bnk;
 
 int ew_tiles(long m, int c) {
   const int rpt = ew_rows_per_tile(m, c);

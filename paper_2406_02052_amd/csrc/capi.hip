@@ -108,11 +108,32 @@ enum CallKind : uintptr_t { CALL_FWD = 1, CALL_BWD, CALL_UPD, CALL_SYNC };
 
 // Enqueue `work` on `stream`, through the stage's graph cache unless graphs are
 // off or per-launch profiling is active.
+petra_status hip_status(petra::HipStatus& h, const char* where) {
+  if (h.err == hipSuccess) return PETRA_OK;
+  const std::string msg = std::string(where) + ": " + h.what + ": " + hipGetErrorString(h.err);
+  h.clear();
+  return fail(PETRA_ERR_HIP, msg);
+}
+
 petra_status launch_status(petra::Stage& s, const char* where) {
   if (s.launch_error) {
     s.launch_error = false;
+    s.hip_status.clear();
     return fail(PETRA_ERR_STATE, std::string(where) + ": internal error: unsupported kernel variant");
   }
+  const petra_status r = hip_status(s.hip_status, where);
+  if (r) return r;
+  return check_hip(where);
+}
+
+// Status of the net's own runtime calls and of every stage program it enqueued.
+petra_status net_status(petra::Net& n, const char* where) {
+  petra_status r = hip_status(n.hip_status, where);
+  for (petra::NetStage& ns : n.st) {
+    const petra_status q = ns.has_blocks ? launch_status(*ns.blocks, where) : PETRA_OK;
+    if (r == PETRA_OK) r = q;
+  }
+  if (r) return r;
   return check_hip(where);
 }
 
@@ -130,6 +151,7 @@ petra_status launch(petra::Stage& s, const petra::GraphCache::Key& key, hipStrea
 uintptr_t P(const void* p) { return reinterpret_cast<uintptr_t>(p); }
 
 }  // namespace
+
 
 extern "C" {
 
@@ -166,8 +188,11 @@ petra_status petra_stage_create(const petra_stage_desc* d, petra_stage** out) {
     return fail(PETRA_ERR_SHAPE, "c_mid must be 8 times a power of two, at most 512");
   const long m = static_cast<long>(d->n) * d->h * d->w;
   const long cm = d->kind == PETRA_BLOCK_BOTTLENECK && d->c_mid > d->c_half ? d->c_mid : d->c_half;
-  if (m * cm >= (1L << 31) || m >= (1L << 30))
-    return fail(PETRA_ERR_SHAPE, "activation too large (N*H*W*C must stay below 2^31)");
+  // every kernel addresses a tensor with 32-bit byte offsets below its
+  // out-of-range sentinel (2^31): each half-tensor must stay below 2 GiB
+  const long esz = d->dtype == PETRA_BF16 ? 2 : 4;
+  if (m * cm * esz >= (1L << 31) || m >= (1L << 30))
+    return fail(PETRA_ERR_SHAPE, "activation too large (N*H*W*C*element size must stay below 2^31 bytes)");
   if (!(d->bn_eps > 0.f) || d->bn_momentum < 0.f || d->bn_momentum > 1.f)
     return fail(PETRA_ERR_INVALID_ARG, "bn_eps must be > 0 and bn_momentum in [0, 1]");
   const int convs = d->num_blocks * 2 * (d->kind == PETRA_BLOCK_BASIC ? 2 : 3);
@@ -334,8 +359,8 @@ petra_status petra_stage_step(petra_stage* st, const void* x1, const void* x2, v
   // backward on `main` itself; join: the update (and later work on `main`)
   // follow both passes.  With graphs on, each pass replays the graph of its
   // standalone call (two replay lanes), so the step shares them.
-  (void)hipEventRecord(s.ev_fork, main);
-  (void)hipStreamWaitEvent(s.s_fwd, s.ev_fork, 0);
+  PETRA_HIP(s.hip_status, hipEventRecord(s.ev_fork, main));
+  PETRA_HIP(s.hip_status, hipStreamWaitEvent(s.s_fwd, s.ev_fork, 0));
   if (s.use_graphs && !s.prof.enabled) {
     hipError_t ge = s.graphs.run({CALL_FWD, P(x1), P(x2), P(y1), P(y2)}, s.s_fwd,
                                  [&](hipStream_t c) { s.forward(x1, x2, y1, y2, c); }, 1);
@@ -344,8 +369,8 @@ petra_status petra_stage_step(petra_stage* st, const void* x1, const void* x2, v
                         main, [&](hipStream_t c) {
                           s.backward(yb1, yb2, dyb1, dyb2, xb1, xb2, dxb1, dxb2, c);
                         }, 0);
-    (void)hipEventRecord(s.ev_fwd, s.s_fwd);
-    (void)hipStreamWaitEvent(main, s.ev_fwd, 0);
+    PETRA_HIP(s.hip_status, hipEventRecord(s.ev_fwd, s.s_fwd));
+    PETRA_HIP(s.hip_status, hipStreamWaitEvent(main, s.ev_fwd, 0));
     if (ge == hipSuccess && due)
       ge = s.graphs.run({CALL_UPD}, main, [&](hipStream_t c) { s.update_kernels(c); }, 0);
     r = ge != hipSuccess
@@ -364,8 +389,8 @@ petra_status petra_stage_step(petra_stage* st, const void* x1, const void* x2, v
       s.backward(yb1, yb2, dyb1, dyb2, xb1, xb2, dxb1, dxb2, main);
       s.forward(x1, x2, y1, y2, s.s_fwd);
     }
-    (void)hipEventRecord(s.ev_fwd, s.s_fwd);
-    (void)hipStreamWaitEvent(main, s.ev_fwd, 0);
+    PETRA_HIP(s.hip_status, hipEventRecord(s.ev_fwd, s.s_fwd));
+    PETRA_HIP(s.hip_status, hipStreamWaitEvent(main, s.ev_fwd, 0));
     if (due) s.update_kernels(main);
     r = launch_status(s, "petra_stage_step");
   }
@@ -397,7 +422,9 @@ petra_status petra_net_create(const petra_net_desc* d, petra_net** out) {
     if (d->widths[j] % 2 != 0 || !pow2_multiple_of_8(d->widths[j] / 2))
       return fail(PETRA_ERR_SHAPE, "widths[j]/2 must be 8 times a power of two, at most 512");
     const long m = static_cast<long>(d->n) * (d->h >> j) * (d->w >> j);
-    if (m * d->widths[j] >= (1L << 31)) return fail(PETRA_ERR_SHAPE, "activation too large");
+    const long esz = d->dtype == PETRA_BF16 ? 2 : 4;
+    if (m * d->widths[j] * esz >= (1L << 31))
+      return fail(PETRA_ERR_SHAPE, "activation too large (N*H*W*C*element size must stay below 2^31 bytes)");
   }
   if (!(d->bn_eps > 0.f) || d->bn_momentum < 0.f || d->bn_momentum > 1.f)
     return fail(PETRA_ERR_INVALID_ARG, "bn_eps must be > 0 and bn_momentum in [0, 1]");
@@ -491,7 +518,7 @@ petra_status petra_net_sync_weights(petra_net* net, void* stream) {
   petra_status r;
   if ((r = check_hip("before petra_net_sync_weights"))) return r;
   net->impl->sync_weights(static_cast<hipStream_t>(stream));
-  return check_hip("petra_net_sync_weights");
+  return net_status(*net->impl, "petra_net_sync_weights");
 }
 
 petra_status petra_net_tick(petra_net* net, const void* images, const int32_t* labels,
@@ -514,9 +541,7 @@ petra_status petra_net_tick(petra_net* net, const void* images, const int32_t* l
   if (images == nullptr) s.feeding = false;
   const bool wrote = s.tick(images, labels, loss, static_cast<hipStream_t>(stream));
   if (loss_written) *loss_written = wrote ? 1 : 0;
-  for (petra::NetStage& ns : s.st)
-    if (ns.has_blocks && (r = launch_status(*ns.blocks, "petra_net_tick"))) return r;
-  return check_hip("petra_net_tick");
+  return net_status(s, "petra_net_tick");
 }
 
 namespace {
@@ -530,6 +555,33 @@ int64_t net_in_flight(const petra::Net& s) {
 }
 
 }  // namespace
+
+petra_status petra_net_drain(petra_net* net, float* losses, void* stream, int32_t* n_losses,
+                             int32_t* ticks_run) {
+  if (n_losses) *n_losses = 0;
+  if (ticks_run) *ticks_run = 0;
+  if (net == nullptr || net->impl == nullptr) return fail(PETRA_ERR_INVALID_ARG, "null net handle");
+  petra::Net& s = *net->impl;
+  if (!s.bound()) return fail(PETRA_ERR_STATE, "net buffers not bound");
+  if (losses != nullptr && !aligned16(losses)) return fail(PETRA_ERR_ALIGN, "losses must be 16-byte aligned");
+  petra_status r;
+  if ((r = check_hip("before petra_net_drain"))) return r;
+  const hipError_t e = s.ensure_streams();
+  if (e != hipSuccess) return fail(PETRA_ERR_HIP, std::string("stream setup: ") + hipGetErrorString(e));
+  s.feeding = false;
+  int32_t nl = 0, nt = 0;
+  // micro-batch m leaves stage 0 at tick m + 2J - 2, so at most 2J - 2 ticks remain;
+  // at most J - 1 of the micro-batches in flight still have to reach the head
+  while (net_in_flight(s) > 0) {
+    float* slot = losses != nullptr && nl < s.J ? losses + nl : nullptr;
+    if (s.tick(nullptr, nullptr, slot, static_cast<hipStream_t>(stream)) && slot != nullptr) ++nl;
+    ++nt;
+    if ((r = net_status(s, "petra_net_drain"))) break;
+  }
+  if (n_losses) *n_losses = nl;
+  if (ticks_run) *ticks_run = nt;
+  return r;
+}
 
 petra_status petra_net_state(const petra_net* net, int64_t* ticks, int64_t* fed,
                              int64_t* in_flight) {
@@ -594,9 +646,7 @@ petra_status petra_net_probe_tick(petra_net* net, int32_t mode, float* grad_out,
   const hipError_t e = s.ensure_streams();
   if (e != hipSuccess) return fail(PETRA_ERR_HIP, std::string("stream setup: ") + hipGetErrorString(e));
   s.probe_tick(mode, grad_out, static_cast<hipStream_t>(stream));
-  for (petra::NetStage& ns : s.st)
-    if (ns.has_blocks && (r = launch_status(*ns.blocks, "petra_net_probe_tick"))) return r;
-  return check_hip("petra_net_probe_tick");
+  return net_status(s, "petra_net_probe_tick");
 }
 
 petra_status petra_net_probe_backprop(petra_net* net, const void* images, const int32_t* labels,
@@ -613,9 +663,7 @@ petra_status petra_net_probe_backprop(petra_net* net, const void* images, const 
   const hipError_t e = s.ensure_streams();
   if (e != hipSuccess) return fail(PETRA_ERR_HIP, std::string("stream setup: ") + hipGetErrorString(e));
   s.probe_backprop(images, labels, grad_out, static_cast<hipStream_t>(stream));
-  for (petra::NetStage& ns : s.st)
-    if (ns.has_blocks && (r = launch_status(*ns.blocks, "petra_net_probe_backprop"))) return r;
-  return check_hip("petra_net_probe_backprop");
+  return net_status(s, "petra_net_probe_backprop");
 }
 
 petra_status petra_net_backprop_step(petra_net* net, const void* images, const int32_t* labels,
@@ -634,9 +682,7 @@ petra_status petra_net_backprop_step(petra_net* net, const void* images, const i
   const hipError_t e = s.ensure_streams();
   if (e != hipSuccess) return fail(PETRA_ERR_HIP, std::string("stream setup: ") + hipGetErrorString(e));
   s.backprop_step(images, labels, loss, static_cast<hipStream_t>(stream));
-  for (petra::NetStage& ns : s.st)
-    if (ns.has_blocks && (r = launch_status(*ns.blocks, "petra_net_backprop_step"))) return r;
-  return check_hip("petra_net_backprop_step");
+  return net_status(s, "petra_net_backprop_step");
 }
 
 petra_status petra_stage_profile(petra_stage* st, int32_t enable) {
@@ -663,6 +709,25 @@ petra_status petra_stage_profile_read(petra_stage* st, int32_t kernel_class, con
   if (total_ms) *total_ms = p.ms[kernel_class];
   if (flops) *flops = p.flops[kernel_class];
   if (bytes) *bytes = p.bytes[kernel_class];
+  return ok();
+}
+
+petra_status petra_stage_profile_kernel(petra_stage* st, int32_t index, const char** name,
+                                        int32_t* kernel_class, int64_t* launches,
+                                        double* total_ms, double* flops, double* bytes) {
+  if (st == nullptr || st->impl == nullptr) return fail(PETRA_ERR_INVALID_ARG, "null stage handle");
+  petra::Profiler& p = st->impl->prof;
+  const hipError_t e = p.collect();
+  if (e != hipSuccess) return fail(PETRA_ERR_HIP, std::string("profile: ") + hipGetErrorString(e));
+  if (index < 0 || index >= static_cast<int32_t>(p.kernels.size()))
+    return fail(PETRA_ERR_INVALID_ARG, "kernel index out of range");
+  const petra::KernelStat& k = p.kernels[index];
+  if (name) *name = k.name.c_str();
+  if (kernel_class) *kernel_class = k.kind;
+  if (launches) *launches = k.launches;
+  if (total_ms) *total_ms = k.ms;
+  if (flops) *flops = k.flops;
+  if (bytes) *bytes = k.bytes;
   return ok();
 }
 

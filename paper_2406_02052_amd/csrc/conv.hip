@@ -3214,6 +3214,8 @@ HaloShape halo_shape(int dtype, const ConvArgs& a) {
         a.pad == 1 && a.c_in % 32 == 0 && a.c_in <= 512 && a.c_out % 8 == 0 && a.p == a.h &&
         a.q == a.w))
     return z;
+  // byte offsets of the buffer loads/stores are 32-bit
+  if (static_cast<long>(a.m) * std::max(a.c_in, a.c_out) * 2 >= static_cast<long>(BUF_OOB)) return z;
   const int hb = a.c_in > 32 ? 2 : 1;
   if (a.w == 32 && a.c_out <= 32) return HaloShape{8, 32, 32, 4, hb};
   if (a.w == 16 && a.c_out <= 64) return HaloShape{8, 16, 64, 2, hb};
@@ -3376,7 +3378,10 @@ int launch_halo_any(int dtype, const ConvArgs& a, int ep, hipStream_t st) {
 
 bool use_staged(int dtype, const ConvArgs& a) {
   return dtype == DT_BF16 && a.src2 == nullptr && a.c_in % 32 == 0 && a.c_out % 8 == 0 &&
-         a.c_in <= 512 && a.c_out >= 16;
+         a.c_in <= 512 && a.c_out >= 16 &&
+         // byte offsets of the buffer loads/stores are 32-bit
+         static_cast<long>(a.n) * a.h * a.w * a.c_in * 2 < static_cast<long>(BUF_OOB) &&
+         static_cast<long>(a.m) * a.c_out * 2 < static_cast<long>(BUF_OOB);
 }
 
 template <typename T, int BO, int BK>

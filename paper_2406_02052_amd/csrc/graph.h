@@ -14,6 +14,26 @@
 
 namespace petra {
 
+// First failure among the HIP runtime calls of an enqueue sequence (event
+// records, cross-stream waits, device copies).  Enqueue code notes every
+// status here instead of dropping it; the C ABI call that enqueued the work
+// reports the failure as PETRA_ERR_HIP and clears it.
+struct HipStatus {
+  hipError_t err = hipSuccess;
+  const char* what = nullptr;
+  void note(hipError_t e, const char* call) {
+    if (e != hipSuccess && err == hipSuccess) {
+      err = e;
+      what = call;
+    }
+  }
+  void clear() {
+    err = hipSuccess;
+    what = nullptr;
+  }
+};
+#define PETRA_HIP(status, call) (status).note((call), #call)
+
 class GraphCache {
  public:
   using Key = std::vector<uintptr_t>;

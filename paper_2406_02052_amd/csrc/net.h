@@ -112,6 +112,7 @@ class Net {
   int64_t t = 0;       // ticks run
   int64_t fed = 0;     // micro-batches fed
   bool feeding = true;
+  HipStatus hip_status;  // first failed runtime call of the current enqueue
   hipEvent_t ev_tick = nullptr;
 
   bool bound() const { return theta != nullptr; }

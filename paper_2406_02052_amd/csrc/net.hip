@@ -390,20 +390,20 @@ FrontView Net::stash_front_view(const NetStage& s, int64_t m) const {
 // (fp32 parameters and the compute copies), ahead of it on its stream.
 void Net::stash_params(NetStage& s, int64_t m, hipStream_t q) {
   char* b = ps_slot(s, m);
-  (void)hipMemcpyAsync(b, theta + s.off_front_w, static_cast<size_t>(s.n_span) * sizeof(float),
-                       hipMemcpyDeviceToDevice, q);
+  PETRA_HIP(hip_status, hipMemcpyAsync(b, theta + s.off_front_w, static_cast<size_t>(s.n_span) * sizeof(float),
+                       hipMemcpyDeviceToDevice, q));
   if (s.has_blocks) {
     const Stage& blk = *s.blocks;
     const size_t cw = static_cast<size_t>(blk.n_conv) * esz;
-    (void)hipMemcpyAsync(b + s.ps_bwf, blk.wfwd, cw, hipMemcpyDeviceToDevice, q);
-    (void)hipMemcpyAsync(b + s.ps_bwd, blk.wdg, cw, hipMemcpyDeviceToDevice, q);
+    PETRA_HIP(hip_status, hipMemcpyAsync(b + s.ps_bwf, blk.wfwd, cw, hipMemcpyDeviceToDevice, q));
+    PETRA_HIP(hip_status, hipMemcpyAsync(b + s.ps_bwd, blk.wdg, cw, hipMemcpyDeviceToDevice, q));
   }
   if (s.has_front) {
     const FrontView f = front_view(s);
-    (void)hipMemcpyAsync(b + s.ps_fwf, f.wf, static_cast<size_t>(s.C) * s.R * s.R * s.Cin * esz,
-                         hipMemcpyDeviceToDevice, q);
-    (void)hipMemcpyAsync(b + s.ps_fwd, f.wd, static_cast<size_t>(s.n_front_w) * esz,
-                         hipMemcpyDeviceToDevice, q);
+    PETRA_HIP(hip_status, hipMemcpyAsync(b + s.ps_fwf, f.wf, static_cast<size_t>(s.C) * s.R * s.R * s.Cin * esz,
+                         hipMemcpyDeviceToDevice, q));
+    PETRA_HIP(hip_status, hipMemcpyAsync(b + s.ps_fwd, f.wd, static_cast<size_t>(s.n_front_w) * esz,
+                         hipMemcpyDeviceToDevice, q));
   }
 }
 
@@ -448,8 +448,8 @@ void Net::stage_forward(NetStage& s, int64_t m, hipStream_t q, bool keep, bool b
   if (!s.has_blocks) return;
   if (buffers && s.ib_slot_bytes) {
     const size_t hb = static_cast<size_t>(s.M) * (s.C / 2) * esz;
-    (void)hipMemcpyAsync(ib_slot(s, m, 0), b1, hb, hipMemcpyDeviceToDevice, q);
-    (void)hipMemcpyAsync(ib_slot(s, m, 1), b2, hb, hipMemcpyDeviceToDevice, q);
+    PETRA_HIP(hip_status, hipMemcpyAsync(ib_slot(s, m, 0), b1, hb, hipMemcpyDeviceToDevice, q));
+    PETRA_HIP(hip_status, hipMemcpyAsync(ib_slot(s, m, 1), b2, hb, hipMemcpyDeviceToDevice, q));
   }
   Stage& blk = *s.blocks;
   void* y1 = fwd_dest(s, m, 0);
@@ -697,13 +697,13 @@ void Net::backprop_step(const void* images, const int32_t* labels, float* loss, 
 
 void Net::probe_backprop(const void* images, const int32_t* labels, float* gout, hipStream_t q) {
   Redirect r(*this, gout);
-  (void)hipMemsetAsync(gout, 0, static_cast<size_t>(n_params) * sizeof(float), q);
+  PETRA_HIP(hip_status, hipMemsetAsync(gout, 0, static_cast<size_t>(n_params) * sizeof(float), q));
   backprop_pass(images, labels, nullptr, false, q);
 }
 
 void Net::probe_tick(int mode, float* gout, hipStream_t q) {
   Redirect r(*this, gout);
-  (void)hipMemsetAsync(gout, 0, static_cast<size_t>(n_params) * sizeof(float), q);
+  PETRA_HIP(hip_status, hipMemsetAsync(gout, 0, static_cast<size_t>(n_params) * sizeof(float), q));
   const int64_t J2 = 2 * static_cast<int64_t>(J) - 2;
   const int par = static_cast<int>(t & 1);
   for (NetStage& s : st) {
@@ -740,11 +740,11 @@ bool Net::count_and_due(NetStage& s) {
 bool Net::tick(const void* images, const int32_t* labels, float* loss, hipStream_t caller) {
   const int64_t J2 = 2 * static_cast<int64_t>(J) - 2;
   if (images != nullptr) ++fed;   // micro-batch number t enters at this tick
-  (void)hipEventRecord(ev_tick, caller);
+  PETRA_HIP(hip_status, hipEventRecord(ev_tick, caller));
   bool wrote_loss = false;
   for (NetStage& s : st) {
-    (void)hipStreamWaitEvent(s.sf, ev_tick, 0);
-    (void)hipStreamWaitEvent(s.sb, ev_tick, 0);
+    PETRA_HIP(hip_status, hipStreamWaitEvent(s.sf, ev_tick, 0));
+    PETRA_HIP(hip_status, hipStreamWaitEvent(s.sb, ev_tick, 0));
   }
   for (NetStage& s : st) {
     const int64_t mf = t - s.j;
@@ -782,11 +782,11 @@ bool Net::tick(const void* images, const int32_t* labels, float* loss, hipStream
       if (count_and_due(s)) {
         // the update follows this stage's forward and backward of the tick (Eq. 5)
         if (q != s.sb) {
-          (void)hipEventRecord(s.ev_f, q);
-          (void)hipStreamWaitEvent(s.sb, s.ev_f, 0);
+          PETRA_HIP(hip_status, hipEventRecord(s.ev_f, q));
+          PETRA_HIP(hip_status, hipStreamWaitEvent(s.sb, s.ev_f, 0));
         } else if (do_f) {
-          (void)hipEventRecord(s.ev_f, s.sf);
-          (void)hipStreamWaitEvent(s.sb, s.ev_f, 0);
+          PETRA_HIP(hip_status, hipEventRecord(s.ev_f, s.sf));
+          PETRA_HIP(hip_status, hipStreamWaitEvent(s.sb, s.ev_f, 0));
         }
         stage_update(s, s.sb);
         if (s.has_blocks) s.blocks->mark_updated();
@@ -794,10 +794,10 @@ bool Net::tick(const void* images, const int32_t* labels, float* loss, hipStream
     }
   }
   for (NetStage& s : st) {
-    (void)hipEventRecord(s.ev_f, s.sf);
-    (void)hipEventRecord(s.ev_b, s.sb);
-    (void)hipStreamWaitEvent(caller, s.ev_f, 0);
-    (void)hipStreamWaitEvent(caller, s.ev_b, 0);
+    PETRA_HIP(hip_status, hipEventRecord(s.ev_f, s.sf));
+    PETRA_HIP(hip_status, hipEventRecord(s.ev_b, s.sb));
+    PETRA_HIP(hip_status, hipStreamWaitEvent(caller, s.ev_f, 0));
+    PETRA_HIP(hip_status, hipStreamWaitEvent(caller, s.ev_b, 0));
   }
   ++t;
   return wrote_loss;

@@ -7,7 +7,7 @@
 
 namespace petra {
 
-namespace {
+namespace netk {
 
 unsigned grid_of(long n, long per_block = 256) {
   long b = (n + per_block - 1) / per_block;
@@ -265,7 +265,8 @@ __global__ __launch_bounds__(256) void wgrad_reduce_pad_kernel(const float* part
   grad[i] += inv_k * s;
 }
 
-}  // namespace
+}  // namespace netk
+using namespace netk;
 
 void pad_channels8(int dtype, const void* src, int c_img, void* dst, long m, hipStream_t st) {
   if (dtype == DT_BF16)

@@ -18,24 +18,42 @@ enum KernelClass {
 const char* kernel_class_name(int k);
 
 // Start/stop events that the next kernel launch attaches to its dispatch
-// (set by Profiler::begin, cleared by Profiler::end; null when not profiling).
+// (set by Profiler::begin, cleared by Profiler::end; null when not profiling),
+// and the host handle of the kernel that launch used.
 struct LaunchEvents {
   hipEvent_t start = nullptr, stop = nullptr;
+  const void* fn = nullptr;
 };
 extern thread_local LaunchEvents g_launch_events;
 
 // Every kernel launch of the library goes through this macro: with profiling
 // on, the runtime timestamps the dispatch itself (kernel start to end), so the
 // per-launch durations are kernel durations, not event-packet intervals.
-#define PETRA_LAUNCH(kernel, grid, block, shmem, stream, ...)                                 \
-  hipExtLaunchKernelGGL(kernel, grid, block, shmem, stream, ::petra::g_launch_events.start, \
-                        ::petra::g_launch_events.stop, 0, __VA_ARGS__)
+#define PETRA_LAUNCH(kernel, grid, block, shmem, stream, ...)                                  \
+  do {                                                                                         \
+    ::petra::g_launch_events.fn = reinterpret_cast<const void*>(kernel);                   \
+    hipExtLaunchKernelGGL(kernel, grid, block, shmem, stream, ::petra::g_launch_events.start,  \
+                          ::petra::g_launch_events.stop, 0, __VA_ARGS__);                      \
+  } while (0)
 
 struct ProfRecord {
   int kind;
   hipEvent_t start, stop;
   double flops, bytes;
+  const void* kernel;
 };
+
+// Totals of one kernel (template instance) within one class.
+struct KernelStat {
+  const void* kernel = nullptr;
+  int kind = 0;
+  std::string name;   // demangled symbol, e.g. "petra::sgd_kernel"
+  long launches = 0;
+  double ms = 0.0, flops = 0.0, bytes = 0.0;
+};
+
+// Demangled name of a kernel from its host handle ("?" if not found).
+std::string kernel_symbol_name(const void* kernel);
 
 class Profiler {
  public:
@@ -52,6 +70,7 @@ class Profiler {
   double ms[K_NUM_CLASSES] = {};
   double flops[K_NUM_CLASSES] = {};
   double bytes[K_NUM_CLASSES] = {};
+  std::vector<KernelStat> kernels;   // per kernel instance, in order of first launch
 
  private:
   std::vector<hipEvent_t> pool_;

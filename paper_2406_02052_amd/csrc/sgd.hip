@@ -11,7 +11,7 @@
 
 namespace petra {
 
-namespace {
+namespace sgdk {
 
 __global__ __launch_bounds__(256) void sgd_kernel(float* __restrict__ theta, float* __restrict__ accum,
                                                   float* __restrict__ mom, int64_t n, int64_t n_decay,
@@ -59,7 +59,8 @@ unsigned grid_for(int64_t n) {
   return static_cast<unsigned>(b);
 }
 
-}  // namespace
+}  // namespace sgdk
+using namespace sgdk;
 
 void sgd_update(float* theta, float* accum, float* mom, int64_t n, int64_t n_decay, float lr,
                 float momentum, float wd, int nesterov, hipStream_t st) {

@@ -114,6 +114,7 @@ class Stage {
 
   Profiler prof;
   bool launch_error = false;  // a conv variant was requested that no kernel implements
+  HipStatus hip_status;       // first failed runtime call of the current enqueue
 
   hipStream_t s_fwd = nullptr, s_bwd = nullptr;
   // Backward streams: the recompute of residual functions runs ahead on s_rec,
@@ -173,6 +174,7 @@ class Stage {
     void* xrec;        // reconstructed stream
     void* dout;        // input gradient: rg + dPhi/du^T d
   };
+  Scratch carve(const ScratchPlan& p, char* base, bool bwd) const;
   void fn_recompute(const ResidualFn& fn, const void* u, Scratch& s, bool running,
                     hipStream_t st);
   void fn_forward(const ResidualFn& fn, const void* u, const void* r, void* y, Scratch& s,

@@ -188,27 +188,31 @@ Stage::~Stage() {
   if (s_bwd) (void)hipStreamDestroy(s_bwd);
 }
 
+Scratch Stage::carve(const ScratchPlan& p, char* base, bool bwd) const {
+  const int nl = blocks.empty() ? 0 : blocks[0].f.nconv;
+  Scratch s;
+  for (int l = 0; l < 3; ++l) s.h[l] = l < nl ? base + p.h[l] : nullptr;
+  s.d1[0] = bwd ? base + p.d1[0] : nullptr;
+  s.d1[1] = bwd && nl > 2 ? base + p.d1[1] : nullptr;
+  s.part = reinterpret_cast<float*>(base + p.part);
+  s.gpart = bwd ? reinterpret_cast<float*>(base + p.gpart) : nullptr;
+  s.bpart = bwd ? reinterpret_cast<float*>(base + p.bpart) : nullptr;
+  s.bnp = reinterpret_cast<float*>(base + p.bnp);
+  return s;
+}
+
 void Stage::bind(float* th, float* gr, float* mo, float* rm, float* rv, void* w) {
   theta = th; grad = gr; mom = mo; rmean = rm; rvar = rv;
   ws = static_cast<char*>(w);
+  sb.assign(plan_b.size(), Scratch{});
   wfwd = ws + off_wfwd;
   wdg = ws + off_wdg;
   reset_view();
-  const int nl = blocks.empty() ? 0 : blocks[0].f.nconv;
-  sb.assign(plan_b.size(), Scratch{});
-  for (int pass = 0; pass < 1 + static_cast<int>(plan_b.size()); ++pass) {
-    const ScratchPlan& p = pass == 0 ? plan_f : plan_b[pass - 1];
-    Scratch& s = pass == 0 ? sf : sb[pass - 1];
-    const bool bwd = pass > 0;
-    for (int l = 0; l < 3; ++l) s.h[l] = l < nl ? ws + p.h[l] : nullptr;
-    s.d1[0] = bwd ? ws + p.d1[0] : nullptr;
-    s.d1[1] = bwd && nl > 2 ? ws + p.d1[1] : nullptr;
-    s.part = reinterpret_cast<float*>(ws + p.part);
-    s.gpart = bwd ? reinterpret_cast<float*>(ws + p.gpart) : nullptr;
-    s.bpart = bwd ? reinterpret_cast<float*>(ws + p.bpart) : nullptr;
-    s.bnp = reinterpret_cast<float*>(ws + p.bnp);
-  }
+  sf = carve(plan_f, ws, false);
+  for (size_t i = 0; i < plan_b.size(); ++i) sb[i] = carve(plan_b[i], ws, true);
   wpart = reinterpret_cast<float*>(ws + off_wpart);
+  // cached graphs hold the previous buffers' device pointers in their kernel arguments
+  graphs.clear();
 }
 
 hipError_t Stage::ensure_streams() {
@@ -356,7 +360,7 @@ void Stage::fn_grad(const BwdFn& f, Scratch& s, const BwdFn* next, Scratch* sn, 
     const ConvLayer& cv = convs[fn.conv[l]];
     const void* dsrc = *dsrc_io;
     // Both consumers form dh_l = BN_l backward of dsrc on the fly from (dsrc, h_l).
-    if (wb) (void)hipEventRecord(ev_d, st);
+    if (wb) PETRA_HIP(hip_status, hipEventRecord(ev_d, st));
     // input gradient: conv of dh_l with the transposed, flipped weights
     ConvArgs a = conv_args(cv);
     a.src = dsrc;
@@ -399,9 +403,9 @@ void Stage::fn_grad(const BwdFn& f, Scratch& s, const BwdFn* next, Scratch* sn, 
       a.resid = f.rg;
       // dout may alias the previous function's output gradient, which that
       // function's weight gradients read
-      if (wb && wait_prev_wg) (void)hipStreamWaitEvent(st, ev_wgdone[parity ^ 1], 0);
+      if (wb && wait_prev_wg) PETRA_HIP(hip_status, hipStreamWaitEvent(st, ev_wgdone[parity ^ 1], 0));
       if (next != nullptr) {
-        if (rb) (void)hipStreamWaitEvent(st, ev_rec[parity ^ 1], 0);
+        if (rb) PETRA_HIP(hip_status, hipStreamWaitEvent(st, ev_rec[parity ^ 1], 0));
         const int NL = next->fn->nconv - 1;
         a.ep_h = sn->h[NL];
         a.ep_mean = sn->vec(NL, V_MEAN, cmax);
@@ -418,7 +422,7 @@ void Stage::fn_grad(const BwdFn& f, Scratch& s, const BwdFn* next, Scratch* sn, 
       }
     }
     // weight gradient of conv_l (side stream), from the same dsrc and h_l
-    if (wb) (void)hipStreamWaitEvent(wst, ev_d, 0);
+    if (wb) PETRA_HIP(hip_status, hipStreamWaitEvent(wst, ev_d, 0));
     WgradArgs w{};
     w.dh = dsrc;
     w.dh_h = s.h[l];
@@ -462,8 +466,8 @@ void Stage::fn_grad(const BwdFn& f, Scratch& s, const BwdFn* next, Scratch* sn, 
     }
   }
   if (part == 1) {
-    if (rb) (void)hipEventRecord(ev_gdone[parity], st);
-    if (wb || rs != wst) (void)hipEventRecord(ev_wgdone[parity], wst);
+    if (rb) PETRA_HIP(hip_status, hipEventRecord(ev_gdone[parity], st));
+    if (wb || rs != wst) PETRA_HIP(hip_status, hipEventRecord(ev_wgdone[parity], wst));
   }
 }
 
@@ -544,9 +548,9 @@ void Stage::backward(const void* y1, const void* y2, const void* dy1, const void
   const int nf = static_cast<int>(fl.size());
   // scratch set of function f: its own when deferring, else alternating
   auto S = [&](int f) -> Scratch& { return defer ? sb[f] : sb[f & 1]; };
-  if (rb || wb) (void)hipEventRecord(ev_start, st);
-  if (rb) (void)hipStreamWaitEvent(rs, ev_start, 0);
-  if (wb) (void)hipStreamWaitEvent(wst, ev_start, 0);
+  if (rb || wb) PETRA_HIP(hip_status, hipEventRecord(ev_start, st));
+  if (rb) PETRA_HIP(hip_status, hipStreamWaitEvent(rs, ev_start, 0));
+  if (wb) PETRA_HIP(hip_status, hipStreamWaitEvent(wst, ev_start, 0));
   auto last_c = [&](const BwdFn& f) { return convs[f.fn->conv[f.fn->nconv - 1]].cout; };
   // First function: recompute, reconstruction and the BN_L-backward partials of
   // the given output gradient.
@@ -561,7 +565,7 @@ void Stage::backward(const void* y1, const void* y2, const void* dy1, const void
                 s0.vec(L, V_RSTD, cmax), fl[0].xrec, s0.gpart, M, c, rs);
     prof.end(K_COMBINE_BWD, rs, 0.0, 4.0 * M * c * esz);
     s0.gtiles = ew_tiles(M, c);
-    if (rb) (void)hipEventRecord(ev_rec[0], rs);
+    if (rb) PETRA_HIP(hip_status, hipEventRecord(ev_rec[0], rs));
   }
   for (int f = 0; f < nf; ++f) {
     const int p = f & 1;
@@ -573,28 +577,28 @@ void Stage::backward(const void* y1, const void* y2, const void* dy1, const void
     // the first function's weight gradients read y1 and dy2, which the last
     // function overwrites when the caller runs in place (x1 == y1, dx2 == dy2)
     defer_cur = defer && (f >= 1 || (x1 != y1 && dx2 != dy2));
-    if (rb) (void)hipStreamWaitEvent(st, ev_rec[p], 0);
+    if (rb) PETRA_HIP(hip_status, hipStreamWaitEvent(st, ev_rec[p], 0));
     fn_grad(fl[f], sc, nx, sn, st, wst, rs, f >= 1, p, 0, &dsrc);
     if (has_next) {
       // recompute of the next function (its input is this function's
       // reconstruction); its scratch set was last used by function f - 1
-      if (rb && f >= 1) (void)hipStreamWaitEvent(rs, ev_gdone[p ^ 1], 0);
+      if (rb && f >= 1) PETRA_HIP(hip_status, hipStreamWaitEvent(rs, ev_gdone[p ^ 1], 0));
       fn_recompute(*fl[f + 1].fn, fl[f + 1].u, *sn, true, rs);
-      if (rb) (void)hipEventRecord(ev_rec[p ^ 1], rs);
+      if (rb) PETRA_HIP(hip_status, hipEventRecord(ev_rec[p ^ 1], rs));
     }
     fn_grad(fl[f], sc, nx, sn, st, wst, rs, f >= 1, p, 1, &dsrc);
     if (defer && side != nullptr && ev_side != nullptr && nf >= 2 &&
         (f + 1 == nf / 2 || f + 1 == nf - 1)) {
       // the weight gradients collected so far on the idle side stream (after
       // the first half and before the last function: one event each)
-      (void)hipEventRecord(ev_side, st);
-      (void)hipStreamWaitEvent(side, ev_side, 0);
+      PETRA_HIP(hip_status, hipEventRecord(ev_side, st));
+      PETRA_HIP(hip_status, hipStreamWaitEvent(side, ev_side, 0));
       flush_deferred(side);
     }
     if (has_next) {
       // reconstruction of the next function; it may overwrite this function's
       // input, which this function's weight gradients read
-      if (rs != wst) (void)hipStreamWaitEvent(rs, ev_wgdone[p], 0);
+      if (rs != wst) PETRA_HIP(hip_status, hipStreamWaitEvent(rs, ev_wgdone[p], 0));
       const BwdFn& nx = fl[f + 1];
       const int L = nx.fn->nconv - 1;
       const int c = last_c(nx);
@@ -607,10 +611,10 @@ void Stage::backward(const void* y1, const void* y2, const void* dy1, const void
   defer_cur = false;
   // join the side streams
   if (rb) {
-    (void)hipEventRecord(ev_rec_end, rs);
-    (void)hipStreamWaitEvent(st, ev_rec_end, 0);
+    PETRA_HIP(hip_status, hipEventRecord(ev_rec_end, rs));
+    PETRA_HIP(hip_status, hipStreamWaitEvent(st, ev_rec_end, 0));
   }
-  if (wb) (void)hipStreamWaitEvent(st, ev_wgdone[(nf - 1) & 1], 0);
+  if (wb) PETRA_HIP(hip_status, hipStreamWaitEvent(st, ev_wgdone[(nf - 1) & 1], 0));
   // the (remaining) deferred weight gradients and every layer's reduce: their
   // inputs are still intact (each function kept its scratch set and its block's
   // buffers)

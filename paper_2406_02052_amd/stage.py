@@ -174,6 +174,12 @@ class Net:
     def get_params(self):
         return self._unflatten(self.params)
 
+    def get_momentum(self):
+        return self._unflatten(self.mom)
+
+    def get_grads(self):
+        return self._unflatten(self.grad)
+
     def set_optimizer(self, lr=0.1, momentum=0.9, weight_decay=0.0, nesterov=True, accum_k=1):
         L.petra_net_set_optimizer(self.handle, L.Sgd(lr, momentum, weight_decay,
                                                     1 if nesterov else 0, accum_k))
@@ -187,6 +193,13 @@ class Net:
 
     def tick(self, images=None, labels=None, stream=None) -> bool:
         return L.petra_net_tick(self.handle, images, labels, self.loss, stream)
+
+    def drain(self, stream=None):
+        """Ticks without input until nothing is in flight.  Returns the device
+        fp32 losses of the micro-batches that reached the head meanwhile."""
+        out = self.torch.zeros(max(self.n_stages, 4), dtype=self.torch.float32, device=self.device)
+        nl, _ = L.petra_net_drain(self.handle, out, stream)
+        return out[:nl]
 
     def backprop_step(self, images, labels, stream=None) -> None:
         """Reversible backpropagation of one micro-batch (no pipelining); the

@@ -1,30 +1,34 @@
 """Test-side helpers: drive a stage through the C ABI and the oracle on the
 same seeded inputs, and compare.  (Test infrastructure; not product code.)
 
-Tolerances.  fp32 workloads: normwise relative error <= 1e-4 on every tensor,
-except where fp32 arithmetic itself cannot get there: for the same masked
-tensors as below the bar is max(1e-4, 3 x the distance between the oracle and
-the oracle run in fp32).  That floor stays far below 1e-4 at small sizes; at
-100k pixels per channel the BN-backward sums of the first layers cancel
-(the channel sums of an output gradient that the next BN backward has already
-centred), and the oracle's own fp32 run is ~5e-3 from its fp64 result there.
-bf16 workloads (bf16 storage, fp32 accumulation): <= 2e-2 on every tensor,
-where the oracle holds activations at bf16 wherever the method stores them.
-Tensors that come out of ReLU derivatives (input gradients, parameter
-gradients, and what the update derives from them) have a measurable noise
-floor in bf16: a one-ulp difference anywhere cascades through later roundings,
-and every pre-activation that lands on the other side of zero flips a ReLU
-decision, so the normwise error of a masked gradient grows like the square
-root of the storage noise.  The reconstructed inputs share that floor: each
-block subtracts a freshly recomputed residual function of the previous
-block's reconstruction, so storage noise is amplified block after block (the
-reconstruction drift against the true input is reported).  The floor is measured in the same test as the
-largest distance between the oracle and three perturbed copies of it that
-any bf16 implementation is as entitled to as the kernels are: one computing
-in fp32 instead of fp64, and two whose storage rounding first scales each
-value by (1 + u 2^-20), u uniform in [-1, 1] (a last-bits difference of the
-kind another summation order produces).  For those tensors the bar is
-max(2e-2, 3 x floor).
+Bars (fixed constants, never computed in a run).  The error of a tensor is
+normwise, ||gpu - oracle|| / ||oracle||, against the oracle in fp64 with the
+storage model of the workload (fp32 workloads: plain fp64; bf16 workloads:
+every materialised tensor held at bf16, pinned in tests/test_oracle_storage.py).
+
+  TOL (fp32 1e-4, bf16 2e-2) -- the stated tolerance -- applies to
+    * every tensor of a "sharp" case: every bf16 case whose residual
+      functions are differentiated one at a time -- the last BN of F or of G
+      zeroed in every block (each block is then one additive half-coupling,
+      Sec. 3.2: every F, resp. G, kernel and the reconstruction run, and no
+      recompute reads a reconstruction that another function's output went
+      into) or of both (the identity block) -- and every fp32 case (the fp32
+      cases with full couplings are sized so that no ReLU decision moves);
+    * in every case, the forward output y and the running statistics.
+  CHAIN_TOL / CHAIN_COS apply to the remaining tensors of a bf16 stage of
+    full couplings (reconstructed input, input gradient, parameter gradients,
+    update increment, momentum).  F's recompute reads x2 = y2 - G(y1) stored
+    in bf16; a last-bit difference in G moves that reconstruction, and so F's
+    pre-activations, by about one bf16 ulp; every pre-activation that crosses
+    zero flips a ReLU decision, and the normwise error of a masked gradient
+    grows like the square root of the fraction flipped, block after block.
+    Any two correct bf16 implementations differ this way (the oracle run in
+    fp32 lands 4-9 % from itself in fp64 on the CIFAR stage); these tensors are
+    pinned by the isolated and identity cases, and here only bounded.
+
+Direction anchor.  The bf16 path is also compared with the plain fp64 oracle
+(no storage rounding): cosine similarity >= ANCHOR_COS in sharp cases and
+>= CHAIN_COS otherwise, for every tensor that is not identically zero.
 """
 from __future__ import annotations
 
@@ -33,7 +37,15 @@ import numpy as np
 import synth
 from oracle.stage import StageState
 
-FLOORED = ("x1", "x2", "dx1", "dx2", "grad", "update_inc", "momentum")
+TOL = {"fp32": 1e-4, "bf16": 2e-2}
+CHAIN_TOL = 0.5
+CHAIN_COS = 0.9
+ANCHOR_COS = 0.98
+
+# tensors that depend on the forward or recompute chains only
+FORWARD_SIDE = ("y1", "y2", "run_mean", "run_var")
+
+MODES = ("full", "isoF", "isoG", "p5")
 
 
 def rel(a, b) -> float:
@@ -50,18 +62,28 @@ def cos_sim(a, b) -> float:
 
 
 def tol(wl) -> float:
-    return 1e-4 if wl.dtype == "fp32" else 2e-2
+    return TOL[wl.dtype]
 
 
-def jitter_store(seed: int):
-    """bf16 storage after a relative perturbation of at most 2^-20."""
-    rng = np.random.default_rng(seed)
+def last_bn_zeroed(wl, params, mode):
+    """Parameters with gamma = beta = 0 on the last BN of G (isoF: the block is
+    y1 = x1 + F(x2), y2 = x2), of F (isoG) or of both (p5: the identity block).
+    Input preparation only."""
+    if mode == "full":
+        return params
+    names = [n for n, _ in wl.param_shapes()]
+    last = f"bn{len(wl.conv_layers()) - 1}"
+    fns = {"isoF": ("G",), "isoG": ("F",), "p5": ("F", "G")}[mode]
+    out = list(params)
+    for i, nm in enumerate(names):
+        _, f, layer, _ = nm.split(".")
+        if f in fns and layer == last:
+            out[i] = np.zeros_like(out[i])
+    return out
 
-    def store(a):
-        a32 = np.asarray(a, np.float32)
-        j = (1.0 + (2.0 ** -20) * rng.uniform(-1.0, 1.0, a32.shape)).astype(np.float32)
-        return synth.round_bf16(a32 * j)
-    return store
+
+def is_sharp(wl, mode) -> bool:
+    return wl.dtype == "fp32" or mode != "full"
 
 
 def oracle_state(wl, params, storage=True, dtype=np.float64, store=None) -> StageState:
@@ -89,13 +111,12 @@ def gpu_stage(wl, params, device="cuda"):
     return st
 
 
-def _oracle_step(ref, wl, params, x, yin, g):
-    """Outputs of one oracle step in a flat dict of named tensors."""
+def _oracle_step(ref, wl, params, x, yin, g, fwd=None):
+    """Outputs of one oracle step in a flat dict of named tensors (the forward
+    output may be passed in when it was computed already)."""
     out = {}
-    oy1, oy2 = ref.forward(*x)
+    oy1, oy2 = ref.forward(*x) if fwd is None else fwd
     out["y1"], out["y2"] = oy1, oy2
-    if yin is None:
-        return out
     ox1, ox2, odx1, odx2, _ = ref.backward(*yin, *g, k=wl.accum_k)
     out.update(x1=ox1, x2=ox2, dx1=odx1, dx2=odx2)
     names = [n for n, _ in wl.param_shapes()]
@@ -110,27 +131,12 @@ def _oracle_step(ref, wl, params, x, yin, g):
     return out
 
 
-def run_step_parity(wl, bn_affine="random"):
-    """Forward, reconstruct+VJP and update on both sides.
-
-    Returns (errs, floors, info): per-tensor GPU-vs-oracle errors, per-tensor
-    noise floors and informational figures.
-    """
+def gpu_step(wl, params, x, yin, g):
+    """One forward, reconstruct+VJP and update through the C ABI."""
     import torch
     from paper_2406_02052_amd import to_host
 
-    params = synth.stage_params(wl, bn_affine)
     names = [n for n, _ in wl.param_shapes()]
-    x = synth.stage_input(wl)
-    g = synth.stage_output_grad(wl)
-
-    ref = oracle_state(wl, params)
-    oy = ref.forward(*x)
-    # backward from the oracle output in storage precision (same bits on both sides)
-    yin = tuple(synth.to_storage(t, wl.dtype) for t in oy)
-    ref = oracle_state(wl, params)
-    want = _oracle_step(ref, wl, params, x, yin, g)
-
     st = gpu_stage(wl, params)
     got = {}
     y1, y2 = st.act(), st.act()
@@ -146,50 +152,87 @@ def run_step_parity(wl, bn_affine="random"):
     got["run_mean"] = st.run_mean.cpu().numpy()
     got["run_var"] = st.run_var.cpu().numpy()
     p0 = st.get_params()
-    st.update()
+    assert st.update()
     torch.cuda.synchronize()
     for nm, p1, a, b in zip(names, st.get_params(), p0, st.get_momentum()):
         got["update_inc:" + nm] = p1.astype(np.float64) - a
         got["momentum:" + nm] = b
-    accum_after = max(float(np.abs(a).max()) for a in st.get_grads())
+    got["_accum_after_update"] = max(float(np.abs(a).max()) for a in st.get_grads())
+    return got
 
-    errs = {k: rel(got[k], want[k]) for k in want}
-    floors = {}
-    info = {"drift_gpu": max(rel(got["x1"], x[0]), rel(got["x2"], x[1])),
-            "drift_oracle": max(rel(want["x1"], x[0]), rel(want["x2"], x[1])),
-            "accum_after_update": accum_after}
-    if wl.dtype == "fp32":
-        res = _oracle_step(oracle_state(wl, params, dtype=np.float32), wl, params, x, yin, g)
-        floors = {k: rel(res[k], want[k]) for k in want}
-    if wl.dtype == "bf16":
-        twins = [oracle_state(wl, params, dtype=np.float32),
-                 oracle_state(wl, params, store=jitter_store(1)),
-                 oracle_state(wl, params, store=jitter_store(2))]
-        for tw in twins:
-            res = _oracle_step(tw, wl, params, x, yin, g)
-            for k in want:
-                floors[k] = max(floors.get(k, 0.0), rel(res[k], want[k]))
+
+def run_step_parity(wl, bn_affine="random", mode="full", anchor=True):
+    """Forward, reconstruct+VJP and update on both sides at the same inputs.
+
+    The backward starts from the oracle's forward output in storage precision
+    (the same bits on both sides).  Returns (got, want, exact): the GPU's
+    tensors, the oracle's, and the plain fp64 oracle's (None if not asked)."""
+    params = last_bn_zeroed(wl, synth.stage_params(wl, bn_affine), mode)
+    x = synth.stage_input(wl)
+    g = synth.stage_output_grad(wl)
+    ref = oracle_state(wl, params)
+    oy = ref.forward(*x)
+    yin = tuple(synth.to_storage(t, wl.dtype) for t in oy)
+    want = _oracle_step(ref, wl, params, x, yin, g, fwd=oy)
+    exact = None
+    if anchor and wl.dtype == "bf16":
         exact = _oracle_step(oracle_state(wl, params, storage=False), wl, params, x, yin, g)
-        info["fp64_dx"] = max(rel(got["dx1"], exact["dx1"]), rel(got["dx2"], exact["dx2"]))
-        info["cos_dx2"] = cos_sim(got["dx2"], want["dx2"])
-        info["norm_ratio_dx2"] = float(np.linalg.norm(got["dx2"]) / np.linalg.norm(want["dx2"]))
-    return errs, floors, info
+    got = gpu_step(wl, params, x, yin, g)
+    got["_x"], got["_yin"], got["_g"] = x, yin, g
+    return got, want, exact
 
 
-def check(errs, floors, info, wl):
-    """Assert the tolerance of each tensor; returns a summary string."""
+def check(wl, mode, got, want, exact=None):
+    """Assert the fixed bars of the case (see the module docstring) and the
+    structural facts of the zeroed-BN modes; returns a summary string."""
     t = tol(wl)
+    sharp = is_sharp(wl, mode)
     bad = {}
-    for k, e in errs.items():
-        bar = t
-        if k.split(":")[0] in FLOORED:
-            bar = max(t, 3.0 * floors.get(k, 0.0))
-        if not e <= bar:
-            bad[k] = (e, bar)
-    worst = max(errs, key=errs.get)
-    summary = (f"worst {worst}={errs[worst]:.3g} floor={floors.get(worst, 0):.3g} "
-               f"y={max(errs['y1'], errs['y2']):.3g} x={max(errs['x1'], errs['x2']):.3g} "
-               f"dx={max(errs['dx1'], errs['dx2']):.3g} info={info}")
+    worst = (0.0, "")
+    for k, w in want.items():
+        e = rel(got[k], w)
+        worst = max(worst, (e, k))
+        if sharp or k in FORWARD_SIDE:
+            if not e <= t:
+                bad[k] = (e, t)
+        else:
+            c = cos_sim(got[k], w) if np.any(w != 0) else 1.0
+            if not (e <= CHAIN_TOL and c >= CHAIN_COS):
+                bad[k] = (e, c)
+        # what the oracle has as exact zeros (zeroed BNs) the GPU must too
+        if not np.any(w != 0) and np.any(np.asarray(got[k]) != 0):
+            bad[k + " (not exactly zero)"] = (float(np.abs(got[k]).max()), 0.0)
+    anchor = (1.0, "")
+    if exact is not None:
+        for k, w in exact.items():
+            if np.any(w != 0):
+                anchor = min(anchor, (cos_sim(got[k], w), k))
+        if not anchor[0] >= (ANCHOR_COS if sharp else CHAIN_COS):
+            bad["anchor " + anchor[1]] = anchor
+    x, yin, g = got["_x"], got["_yin"], got["_g"]
+    if mode == "p5":
+        # the identity block: y = x, reconstruction = y and dx = dy, bit for bit
+        for k, a in (("y1", x[0]), ("y2", x[1]), ("x1", yin[0]), ("x2", yin[1]),
+                     ("dx1", g[0]), ("dx2", g[1])):
+            if not np.array_equal(got[k], a):
+                bad[k + " (identity block, not bitwise)"] = (rel(got[k], a), 0.0)
+    if mode == "isoF":
+        # G = 0: y2 = x2 and its reconstruction y2 - 0, bit for bit; dx1 = dy1
+        for k, a in (("y2", x[1]), ("x2", yin[1]), ("dx1", g[0])):
+            if not np.array_equal(got[k], a):
+                bad[k + " (G zeroed, not bitwise)"] = (rel(got[k], a), 0.0)
+    if mode == "isoG":
+        # F = 0: y1 = x1, the reconstruction x1 = y1 - 0, and dx2 = dy2
+        for k, a in (("y1", x[0]), ("x1", yin[0]), ("dx2", g[1])):
+            if not np.array_equal(got[k], a):
+                bad[k + " (F zeroed, not bitwise)"] = (rel(got[k], a), 0.0)
+    summary = (f"{wl.name} {wl.dtype} n={wl.n} blocks={wl.blocks} mode={mode} "
+               f"{'sharp' if sharp else 'chain'}: worst {worst[1]}={worst[0]:.3g} "
+               f"y={max(rel(got['y1'], want['y1']), rel(got['y2'], want['y2'])):.3g} "
+               f"x={max(rel(got['x1'], want['x1']), rel(got['x2'], want['x2'])):.3g} "
+               f"dx={max(rel(got['dx1'], want['dx1']), rel(got['dx2'], want['dx2'])):.3g} "
+               f"anchor_cos={anchor[0]:.5f} ({anchor[1]}) "
+               f"drift={max(rel(got['x1'], x[0]), rel(got['x2'], x[1])):.3g}")
     assert not bad, f"parity failed: {bad}\n{summary}"
-    assert info["accum_after_update"] == 0.0, "accumulator not zeroed by the update"
+    assert got["_accum_after_update"] == 0.0, "accumulator not zeroed by the update"
     return summary

@@ -1,7 +1,12 @@
-"""GPU parity at the workloads' full sizes (the launch configuration bench.py
-times).  The oracle runs in full where it finishes in seconds; for the
-ImageNet32-shaped 6-block stage it runs one block at full batch, and the full
-stage is checked through properties that hold at any size."""
+"""GPU parity at the workloads' full sizes (the shapes and launch configuration
+bench.py times), against the oracle run in full on the same seeded inputs.
+
+Per workload: the stage as it is (every block a full reversible coupling),
+the stage with G's last BN zeroed in every block (each block is then the
+half-coupling y1 = x1 + F(x2): every F kernel, the reconstruction subtraction
+and the gradient chain of F, one function at a time), the same with F's last
+BN zeroed (every G kernel), and the identity block of P5 (both zeroed).  The
+bars are the fixed ones of tests/harness.py."""
 import numpy as np
 import pytest
 
@@ -10,24 +15,34 @@ from tests.harness import check, gpu_stage, rel, run_step_parity
 
 pytestmark = pytest.mark.gpu
 
+CASES = []
+for _wl, _id in ((synth.CIFAR_STAGE, "cifar_stage"),
+                 (synth.IMAGENET_BOTTLENECK_STAGE, "imagenet_bottleneck_stage"),
+                 (synth.IMAGENET32_STAGE, "imagenet32_stage")):
+    for _mode in ("full", "isoF", "isoG", "p5"):
+        CASES.append(pytest.param(_wl, _mode, id=f"{_id}-{_mode}"))
+    # one block at the full shape
+    CASES.append(pytest.param(_wl.with_(blocks=1), "full", id=f"{_id}-one_block"))
+# fp32 kernels at the bottleneck stage's image size (3 blocks, 4 images: at
+# 12.5k pixels per channel no ReLU decision moves under fp32 rounding), one
+# function at a time and as the identity block
+for _mode in ("isoF", "isoG", "p5"):
+    CASES.append(pytest.param(synth.IMAGENET_BOTTLENECK_STAGE.with_(dtype="fp32", n=4), _mode,
+                              id=f"imagenet_bottleneck_fp32_4-{_mode}"))
 
-# The last case is fp32 at 32x56x56 (100k pixels per channel, 49 MiB per half
-# tensor): fp32 kernels at a size where the BN-backward sums cancel, checked
-# under the fp32 floor rule of tests/harness.py.
-@pytest.mark.parametrize("wl", [synth.CIFAR_STAGE, synth.IMAGENET_BOTTLENECK_STAGE,
-                                synth.IMAGENET32_STAGE.with_(blocks=1),
-                                synth.IMAGENET_BOTTLENECK_STAGE.with_(dtype="fp32", n=32,
-                                                                      blocks=1)],
-                         ids=["cifar_stage", "imagenet_bottleneck_stage", "imagenet32_one_block",
-                              "imagenet_bottleneck_fp32_one_block"])
-def test_full_size_step_parity(wl):
-    print(f"full-size case {wl}", flush=True)
-    errs, floors, info = run_step_parity(wl, bn_affine="identity")
-    print(check(errs, floors, info, wl), flush=True)
+
+@pytest.mark.parametrize("wl,mode", CASES)
+def test_full_size_step_parity(wl, mode):
+    print(f"full-size case {wl.name} {wl.dtype} n={wl.n} blocks={wl.blocks} {mode}", flush=True)
+    # the plain-fp64 direction anchor costs a second oracle run: kept for the
+    # full coupling and for one isolated mode of the six-block stage
+    anchor = not (wl is synth.IMAGENET32_STAGE and mode in ("isoG", "p5"))
+    got, want, exact = run_step_parity(wl, bn_affine="random", mode=mode, anchor=anchor)
+    print(check(wl, mode, got, want, exact), flush=True)
 
 
 def test_imagenet32_stage_properties_full_size():
-    """6 blocks at 256x16x16x256: with frozen parameters the backward rebuilds
+    """6 blocks at 256x16x16x256 with frozen parameters: the backward rebuilds
     the forward's input (drift reported), repeated runs are bitwise identical,
     and every output is finite."""
     import torch

@@ -5,7 +5,7 @@ import pytest
 
 import synth
 from oracle.net import PetraNet
-from tests.harness import jitter_store, rel
+from tests.harness import CHAIN_TOL, TOL, rel
 
 pytestmark = pytest.mark.gpu
 
@@ -64,7 +64,7 @@ def run_both(wl, names, params, n_micro, ticks, store=None, gpu=True, mode=0, sp
     return ref, oloss, net, gloss
 
 
-def compare(wl, names, params, ref, oloss, net, gloss, tol_loss, tol_param, floors=None):
+def compare(wl, names, params, ref, oloss, net, gloss, tol_loss, tol_param, tol_stats=None):
     assert [l is None for l in oloss] == [l is None for l in gloss], (oloss, gloss)
     for a, b in zip(gloss, oloss):
         if b is not None:
@@ -84,13 +84,15 @@ def compare(wl, names, params, ref, oloss, net, gloss, tol_loss, tol_param, floo
         d_ref = np.asarray(want[nm], np.float64) - p0[nm]
         d_got = np.asarray(got[nm], np.float64) - p0[nm]
         e = float(np.linalg.norm(d_got - d_ref) / max(np.linalg.norm(d_ref), 1e-3 * total))
-        bar = max(tol_param, 3.0 * floors[nm]) if floors else tol_param
-        assert e <= bar, (nm, e, bar)
+        assert e <= tol_param, (nm, e, tol_param)
         worst = max(worst, (e, nm))
-    rm = net.run_mean.cpu().numpy()
-    orm = np.concatenate([np.concatenate([m.reshape(-1) for m in st.run_mean]) for st in ref.stages])
     # the net's running statistics are laid out per stage as [front, blocks...]
-    assert rm.shape == orm.shape
+    orm = np.concatenate([np.concatenate([m.reshape(-1) for m in st.run_mean]) for st in ref.stages])
+    orv = np.concatenate([np.concatenate([v.reshape(-1) for v in st.run_var]) for st in ref.stages])
+    ts = tol_loss if tol_stats is None else tol_stats
+    for a, b in ((net.run_mean.cpu().numpy(), orm), (net.run_var.cpu().numpy(), orv)):
+        assert a.shape == b.shape
+        assert rel(a, b) <= ts, ("running statistics", rel(a, b), ts)
     return worst
 
 
@@ -108,22 +110,43 @@ def test_tiny_net_fp32_matches_oracle_ticks():
 
 
 def test_tiny_net_bf16_matches_storage_oracle():
+    """bf16 schedule against the storage-precision oracle: losses and running
+    statistics (forward side) at the stated bar; the parameter increments come
+    out of gradients through several reconstructed bf16 blocks and are held to
+    the chain bound of tests/harness.py."""
     wl = TINY
     names, params = affine_params(wl)
     J = len(wl.widths)
     n_micro, ticks = 3, 3 + 2 * J
     ref, oloss, net, gloss = run_both(wl, names, params, n_micro, ticks)
-    floors = {}
-    for seed in (1, 2):
-        tw, _, _, _ = run_both(wl, names, params, n_micro, ticks, store=jitter_store(seed), gpu=False)
-        tw_p = {nm: p for st in tw.stages for nm, p in zip(st.names, st.params)}
-        rf_p = {nm: p for st in ref.stages for nm, p in zip(st.names, st.params)}
-        p0 = dict(zip(names, params))
-        for nm in names:
-            floors[nm] = max(floors.get(nm, 0.0), rel(tw_p[nm] - p0[nm], rf_p[nm] - p0[nm]))
     print("losses", gloss, oloss, flush=True)
-    worst = compare(wl, names, params, ref, oloss, net, gloss, 2e-2, 2e-2, floors)
+    worst = compare(wl, names, params, ref, oloss, net, gloss, TOL["bf16"], CHAIN_TOL)
     print("worst parameter increment error", worst, flush=True)
+
+
+def test_tiny_net_bf16_identity_blocks_at_stated_bar():
+    """The same schedule with identity blocks (last BN of every F and G zeroed)
+    and lr = 0: every backward is exact backprop through the front layers and
+    the head, one function deep; momentum buffers, losses and running
+    statistics at the stated bar."""
+    wl = TINY.with_(lr=0.0)
+    names, params = affine_params(wl)
+    for i, nm in enumerate(names):
+        parts = nm.split(".")
+        if len(parts) == 5 and parts[3] == "bn1":
+            params[i] = np.zeros_like(params[i])
+    J = len(wl.widths)
+    n_micro, ticks = 3, 3 + 2 * J
+    ref, oloss, net, gloss = run_both(wl, names, params, n_micro, ticks)
+    for a, b in zip(gloss, oloss):
+        if b is not None:
+            assert abs(a - b) <= TOL["bf16"] * abs(b), (a, b)
+    want = {nm: np.asarray(b, np.float64) for st in ref.stages for nm, b in zip(st.names, st.buf)}
+    for nm, g in zip(names, net.get_momentum()):
+        if not np.any(want[nm] != 0):
+            assert not np.any(g != 0), nm
+        else:
+            assert rel(g, want[nm]) <= TOL["bf16"], (nm, rel(g, want[nm]))
 
 
 def test_full_schedule_first_losses_and_finite_run():
@@ -363,22 +386,227 @@ def test_split_stages_backprop_and_delayed_variant_match_oracle():
 
 
 def test_split_stages_bf16_matches_storage_oracle():
-    """bf16 per-layer split (J = 12) against the storage-precision oracle, with
-    per-tensor floors from two jittered-rounding oracle runs."""
+    """bf16 per-layer split (J = 12) against the storage-precision oracle:
+    losses and running statistics at the stated bar, parameter increments at
+    the chain bound (several reconstructed bf16 blocks deep)."""
     wl = TINY.with_(blocks_per_stage=2)
     names, params = affine_params(wl)
     J = len(wl.widths) * 3
     n_micro, ticks = 3, 3 + 2 * J
     ref, oloss, net, gloss = run_both(wl, names, params, n_micro, ticks, split=True)
-    floors = {}
-    for seed in (1, 2):
-        tw, _, _, _ = run_both(wl, names, params, n_micro, ticks, store=jitter_store(seed),
-                               gpu=False, split=True)
-        tw_p = {nm: p for st in tw.stages for nm, p in zip(st.names, st.params)}
-        rf_p = {nm: p for st in ref.stages for nm, p in zip(st.names, st.params)}
-        p0 = dict(zip(names, params))
-        for nm in names:
-            floors[nm] = max(floors.get(nm, 0.0), rel(tw_p[nm] - p0[nm], rf_p[nm] - p0[nm]))
     print("losses", gloss, oloss, flush=True)
-    worst = compare(wl, names, params, ref, oloss, net, gloss, 2e-2, 2e-2, floors)
+    worst = compare(wl, names, params, ref, oloss, net, gloss, TOL["bf16"], CHAIN_TOL)
     print("worst parameter increment error", worst, flush=True)
+
+
+# ---------------------------------------------------------------------------
+# The RevNet-18-shaped schedule at its real shape (32 x 32 images, widths
+# 64/128/256/512, two blocks per stage: every kernel variant the benchmark
+# runs).  The batch is reduced to keep the oracle cheap; kernel selection
+# depends on H, W and C only.
+# ---------------------------------------------------------------------------
+
+REAL = synth.REVNET18_SCHEDULE.with_(n=32)
+
+
+def _identity_blocks(wl, params):
+    """gamma = beta = 0 on the last BN of every F and G: each reversible block
+    is the identity (Sec. 3.2), its reconstruction exact, and only those BNs'
+    parameters get a gradient inside the blocks."""
+    names = [n for n, _ in synth.net_param_shapes(wl)]
+    out = list(params)
+    for i, nm in enumerate(names):
+        parts = nm.split(".")
+        if len(parts) == 5 and parts[3] == "bn1":
+            out[i] = np.zeros_like(out[i])
+    return names, out
+
+
+def _drained_run(wl, names, params, n_micro):
+    """Feed n_micro micro-batches, then drain with petra_net_drain; the oracle
+    runs the same ticks.  Returns (ref, oracle losses, net, GPU losses)."""
+    import torch
+    from paper_2406_02052_amd import Net
+
+    J = len(wl.widths)
+    imgs = synth.net_images(wl, n_micro)
+    labs = synth.net_labels(wl, n_micro)
+    bf = wl.dtype == "bf16"
+    ref = PetraNet([p.astype(np.float64) for p in params], names, J, wl.blocks_per_stage,
+                   weight_view=synth.round_bf16 if bf else None,
+                   store=synth.round_bf16 if bf else None)
+    oloss = []
+    for t in range(n_micro + 2 * J - 2):
+        oloss.append(ref.tick(t, lambda m: imgs[m], lambda m: labs[m], n_micro, wl.lr,
+                              wl.momentum, wl.weight_decay, wl.nesterov, wl.accum_k))
+    oloss = [l for l in oloss if l is not None]
+    net = Net(wl.n, wl.h, wl.w, wl.c_img, wl.widths, wl.blocks_per_stage, wl.classes, wl.dtype)
+    net.set_params(params)
+    net.set_optimizer(wl.lr, wl.momentum, wl.weight_decay, wl.nesterov, wl.accum_k)
+    gloss = []
+    for t in range(n_micro):
+        if net.tick(net.images(imgs[t]), net.labels(labs[t])):
+            gloss.append(float(net.loss.item()))
+    tail = net.drain()
+    torch.cuda.synchronize()
+    gloss += [float(v) for v in tail.cpu().numpy()]
+    assert net.state() == (n_micro + 2 * J - 2, n_micro, 0)
+    return ref, oloss, net, gloss
+
+
+def _by_name(ref, attr):
+    return {nm: np.asarray(v, np.float64) for st in ref.stages
+            for nm, v in zip(st.names, getattr(st, attr))}
+
+
+def test_schedule_real_shape_identity_blocks_exact_gradients():
+    """Drained run of 2J + 2 micro-batches with lr = 0 (every backward is exact
+    backprop at the initial parameters, P8) and identity blocks: the losses,
+    every tensor's momentum buffer (the momentum sum of its gradients, weight
+    decay included) and the running statistics match the oracle's tick
+    simulator at the stated bf16 bar; the block parameters other than the
+    zeroed BNs get exactly no gradient."""
+    wl = REAL.with_(lr=0.0)
+    J = len(wl.widths)
+    names, params = _identity_blocks(wl, synth.net_params(wl))
+    ref, oloss, net, gloss = _drained_run(wl, names, params, 2 * J + 2)
+    print("losses", gloss, oloss, flush=True)
+    assert len(gloss) == len(oloss) == 2 * J + 2
+    for a, b in zip(gloss, oloss):
+        assert abs(a - b) <= TOL["bf16"] * abs(b), (a, b)
+    want = _by_name(ref, "buf")
+    got = dict(zip(names, net.get_momentum()))
+    # Some gradients vanish in exact arithmetic.  With identity blocks the
+    # gradient at the output of stage j < J-1 is the input gradient of stage
+    # j+1's 1x1 stride-2 downsampling of a BN-centred gradient, whose pixel sum
+    # is zero; it reaches unchanged the last BN of every block of stage j and,
+    # for j > 0, stage j's own downsampling BN, so those BNs' beta gradients
+    # vanish.  Stored in bf16 such a sum is rounding noise on both sides: both
+    # must stay below 1e-3 of the whole momentum vector.  The other tensors are
+    # compared normwise, relative to their own norm or to that 1e-3, whichever
+    # is larger.
+    total = np.sqrt(sum(float(np.sum(w ** 2)) for w in want.values()))
+    worst = (0.0, "")
+    for nm in names:
+        parts = nm.split(".")
+        if not np.any(want[nm] != 0):
+            assert not np.any(got[nm] != 0), f"{nm}: gradient must vanish"
+            continue
+        j = int(parts[0][1:])
+        if j < J - 1 and parts[-1] == "beta" and (
+                (len(parts) == 5 and parts[3] == "bn1") or (parts[1] == "trans_bn" and j > 0)):
+            assert np.linalg.norm(got[nm]) <= 1e-3 * total, (nm, np.linalg.norm(got[nm]) / total)
+            assert np.linalg.norm(want[nm]) <= 1e-3 * total, nm
+            continue
+        e = float(np.linalg.norm(got[nm] - want[nm]) / max(np.linalg.norm(want[nm]), 1e-3 * total))
+        worst = max(worst, (e, nm))
+        assert e <= TOL["bf16"], (nm, e)
+    print("worst momentum error", worst, flush=True)
+    for nm, p0, p1 in zip(names, params, net.get_params()):
+        assert np.array_equal(p0, p1), f"{nm} moved with lr = 0"
+    orm = np.concatenate([np.concatenate([m.reshape(-1) for m in st.run_mean]) for st in ref.stages])
+    orv = np.concatenate([np.concatenate([v.reshape(-1) for v in st.run_var]) for st in ref.stages])
+    assert rel(net.run_mean.cpu().numpy(), orm) <= TOL["bf16"]
+    assert rel(net.run_var.cpu().numpy(), orv) <= TOL["bf16"]
+
+
+def _stage_increments(names, params, got_params, ref):
+    """Per stage: (cosine, norm ratio) of the GPU's parameter increments
+    against the oracle's, over the stage's whole parameter vector."""
+    want = _by_name(ref, "params")
+    p0 = dict(zip(names, params))
+    acc = {}
+    for nm, p1 in zip(names, got_params):
+        s = nm.split(".")[0]
+        a = (np.asarray(p1, np.float64) - p0[nm]).ravel()
+        b = (want[nm] - p0[nm]).ravel()
+        r = acc.setdefault(s, [0.0, 0.0, 0.0])
+        r[0] += float(a @ b)
+        r[1] += float(a @ a)
+        r[2] += float(b @ b)
+    return {s: (r[0] / np.sqrt(r[1] * r[2]), np.sqrt(r[1] / r[2])) for s, r in acc.items()}
+
+
+# Fixed bounds for the trained schedule in bf16.  Training through J = 4
+# stages of reconstructed bf16 blocks is chaotic: the oracle itself run in
+# fp32 instead of fp64 (same storage model, batch 32) keeps the losses within
+# 1 % for the first ten ticks, within 10 % to tick 20 and diverges up to 2.6x
+# once the micro-batches are memorised; its per-stage increment cosine falls
+# from 0.95-0.98 at tick 9 to 0.65-0.84 at tick 99 while the increment norms
+# stay within 2 %.
+SCHED_LOSS_EARLY = 5e-2
+SCHED_COS_DRAINED = 0.8
+SCHED_COS_LONG = 0.5
+SCHED_NORM = 0.1
+
+
+def test_schedule_real_shape_drained_run_matches_oracle():
+    """The paper's setting (lr 0.1, Nesterov, weight decay 5e-4) at real shape,
+    2J + 2 micro-batches fed and the pipeline drained: every loss, each stage's
+    parameter increments (direction and size) and the running statistics
+    against the oracle's tick simulator."""
+    wl = REAL
+    J = len(wl.widths)
+    names = [n for n, _ in synth.net_param_shapes(wl)]
+    params = synth.net_params(wl)
+    ref, oloss, net, gloss = _drained_run(wl, names, params, 2 * J + 2)
+    print("losses", gloss, oloss, flush=True)
+    assert len(gloss) == len(oloss) == 2 * J + 2
+    for a, b in zip(gloss, oloss):
+        assert abs(a - b) <= SCHED_LOSS_EARLY * abs(b), (a, b)
+    inc = _stage_increments(names, params, net.get_params(), ref)
+    print("per-stage increment cosine, norm ratio", inc, flush=True)
+    for s, (c, r) in inc.items():
+        assert c >= SCHED_COS_DRAINED and abs(r - 1.0) <= SCHED_NORM, (s, c, r)
+    orm = np.concatenate([np.concatenate([m.reshape(-1) for m in st.run_mean]) for st in ref.stages])
+    orv = np.concatenate([np.concatenate([v.reshape(-1) for v in st.run_var]) for st in ref.stages])
+    assert rel(net.run_mean.cpu().numpy(), orm) <= TOL["bf16"]
+    assert rel(net.run_var.cpu().numpy(), orv) <= TOL["bf16"]
+
+
+def test_schedule_real_shape_hundred_ticks():
+    """100 ticks of the paper's setting at real shape over 8 synthetic
+    micro-batches fed in turn: the losses of the first 2J + 2 micro-batches
+    match the oracle; after that both runs train (the mean loss of the last 20
+    ticks is below half the first losses' mean) and each stage's increment
+    since the start points the oracle's way with the oracle's size."""
+    import torch
+    from paper_2406_02052_amd import Net
+
+    wl = REAL
+    J = len(wl.widths)
+    T, D = 100, 8
+    names = [n for n, _ in synth.net_param_shapes(wl)]
+    params = synth.net_params(wl)
+    imgs, labs = synth.net_images(wl, D), synth.net_labels(wl, D)
+    ref = PetraNet([p.astype(np.float64) for p in params], names, J, wl.blocks_per_stage,
+                   weight_view=synth.round_bf16, store=synth.round_bf16)
+    net = Net(wl.n, wl.h, wl.w, wl.c_img, wl.widths, wl.blocks_per_stage, wl.classes, wl.dtype)
+    net.set_params(params)
+    net.set_optimizer(wl.lr, wl.momentum, wl.weight_decay, wl.nesterov, wl.accum_k)
+    gi = [net.images(x) for x in imgs]
+    gl = [net.labels(l) for l in labs]
+    oloss, gloss = [], []
+    for t in range(T):
+        lo = ref.tick(t, lambda m: imgs[m % D], lambda m: labs[m % D], 10 ** 9, wl.lr,
+                      wl.momentum, wl.weight_decay, wl.nesterov, wl.accum_k)
+        if net.tick(gi[t % D], gl[t % D]):
+            gloss.append(float(net.loss.item()))
+        if lo is not None:
+            oloss.append(lo)
+        if t % 20 == 0:
+            print(f"tick {t}", flush=True)
+    torch.cuda.synchronize()
+    print("losses every 10:", [round(v, 4) for v in gloss[::10]], [round(v, 4) for v in oloss[::10]],
+          flush=True)
+    assert len(gloss) == len(oloss) == T - (J - 1)
+    for a, b in zip(gloss[:2 * J + 2], oloss[:2 * J + 2]):
+        assert abs(a - b) <= SCHED_LOSS_EARLY * abs(b), (a, b)
+    first = np.mean(oloss[:2 * J + 2])
+    for run in (gloss, oloss):
+        assert np.isfinite(run).all()
+        assert np.mean(run[-20:]) < 0.5 * first, (np.mean(run[-20:]), first)
+    inc = _stage_increments(names, params, net.get_params(), ref)
+    print("per-stage increment cosine, norm ratio", inc, flush=True)
+    for s, (c, r) in inc.items():
+        assert c >= SCHED_COS_LONG and abs(r - 1.0) <= SCHED_NORM, (s, c, r)

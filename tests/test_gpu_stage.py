@@ -43,18 +43,42 @@ SMALL = {
 }
 
 
-@pytest.mark.parametrize("name", list(SMALL))
-def test_stage_step_parity_small(name):
+def _small_cases():
+    """Every small case in full coupling; the bf16 ones also with one function
+    isolated (the other's last BN zeroed), which differentiates one function
+    at a time and so holds the stated bar."""
+    out = []
+    for name, wl in SMALL.items():
+        out.append((name, "full"))
+        if wl.dtype == "bf16":
+            out += [(name, "isoF"), (name, "isoG")]
+    return out
+
+
+@pytest.mark.parametrize("name,mode", _small_cases())
+def test_stage_step_parity_small(name, mode):
     wl = SMALL[name]
-    print(f"case {name}: {wl}", flush=True)
-    errs, floors, info = run_step_parity(wl, bn_affine="random")
-    print(name, check(errs, floors, info, wl), flush=True)
+    print(f"case {name} {mode}: {wl}", flush=True)
+    got, want, exact = run_step_parity(wl, bn_affine="random", mode=mode)
+    print(check(wl, mode, got, want, exact), flush=True)
 
 
-def test_fp32_block_identity_bn():
+@pytest.mark.parametrize("name", ["fp32_block_8x8x8x32", "bf16_c32_4x9x9", "bf16_c128_3x6x6",
+                                  "bf16_bottleneck_2x12x12"])
+def test_identity_block_small(name):
+    """P5 (Eq. 4): with gamma = beta = 0 on the last BN of F and of G every block
+    is the identity; the step must return its inputs bit for bit and only the
+    last BNs' parameters get a gradient (their sums of dy and dy * xhat)."""
+    wl = SMALL[name]
+    got, want, exact = run_step_parity(wl, bn_affine="random", mode="p5")
+    print(check(wl, "p5", got, want, exact), flush=True)
+
+
+def test_fp32_block_unit_bn_affine():
+    """The exact single-block fp32 workload with BN gamma = 1, beta = 0."""
     wl = synth.BLOCK_FP32
-    errs, floors, info = run_step_parity(wl, bn_affine="identity")
-    print(check(errs, floors, info, wl), flush=True)
+    got, want, exact = run_step_parity(wl, bn_affine="identity")
+    print(check(wl, "full", got, want, exact), flush=True)
 
 
 def _io(st, wl, seed):
