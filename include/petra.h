@@ -138,7 +138,8 @@ petra_status petra_stage_param_info(const petra_stage* st, int32_t index, petra_
  * run_var: BN running statistics; workspace: scratch of at least
  * workspace_bytes.  The caller initialises params, zeroes grad_accum and
  * momentum, and sets run_mean = 0, run_var = 1; then calls
- * petra_stage_sync_weights(). */
+ * petra_stage_sync_weights().  workspace = NULL with workspace_bytes = 0 binds
+ * a handle for petra_stage_forward_noalloc only. */
 petra_status petra_stage_bind(petra_stage* st, float* params, float* grad_accum, float* momentum,
                               float* run_mean, float* run_var, void* workspace,
                               size_t workspace_bytes);
@@ -174,6 +175,26 @@ petra_status petra_stage_sync_weights(petra_stage* st, void* stream);
  * leaves the running statistics untouched. */
 petra_status petra_stage_forward(petra_stage* st, const void* x1, const void* x2, void* y1,
                                  void* y2, void* stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the forward
+ * of petra_stage_forward, with the same arguments, aliasing rules and result
+ * bits, that needs no workspace.  Its scratch -- the compute copies of the
+ * conv weights, refreshed from params on every call, and one residual
+ * function's pre-BN tensors and BN partial sums -- lives in a static device
+ * array of PETRA_STATIC_SCRATCH_BYTES that the library holds on each device it
+ * runs on until the process ends.  The call allocates nothing and always
+ * launches directly (no graph cache, no timing events).  The handle may be
+ * bound with workspace = NULL and workspace_bytes = 0 (every other compute
+ * call then returns PETRA_ERR_WORKSPACE).  PETRA_ERR_WORKSPACE when the stage's
+ * forward needs more scratch than the array holds (about 2 bytes per conv
+ * weight plus N*H*W*(sum of one residual function's conv output widths)*element
+ * size).  Runs on the current device.  Every call on a device shares that
+ * device's array: calls that overlap in time on one device (other streams or
+ * threads) race and must be ordered by the caller. */
+#define PETRA_STATIC_SCRATCH_BYTES (64u << 20)
+petra_status petra_stage_forward_noalloc(petra_stage* st, const void* x1, const void* x2,
+                                         void* y1, void* y2, void* stream);
 
 /* Backward of the stage with the current parameters (Eq. 5, lines 2-4;
  * Alg. 1): blocks B..1, each rebuilding its input from its output

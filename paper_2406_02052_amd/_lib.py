@@ -117,6 +117,7 @@ _SIGS = {
     "petra_net_memory": (ctypes.c_int, [_VP, ctypes.c_int32, ctypes.POINTER(NetMem)]),
     "petra_net_probe_tick": (ctypes.c_int, [_VP, ctypes.c_int32, _VP, _VP]),
     "petra_net_probe_backprop": (ctypes.c_int, [_VP, _VP, _VP, _VP, _VP]),
+    "petra_stage_forward_noalloc": (ctypes.c_int, [_VP, _VP, _VP, _VP, _VP, _VP]),
     "petra_stage_profile": (ctypes.c_int, [_VP, ctypes.c_int32]),
     "petra_stage_profile_read": (ctypes.c_int, [_VP, ctypes.c_int32,
                                                  ctypes.POINTER(ctypes.c_char_p),
@@ -263,6 +264,11 @@ def petra_stage_step(handle, x1, x2, y1, y2, yb1, yb2, dyb1, dyb2, xb1, xb2, dxb
                                    _ptr(dxb1), _ptr(dxb2), _stream(stream), ctypes.byref(upd)),
            "petra_stage_step")
     return bool(upd.value)
+
+
+def petra_stage_forward_noalloc(handle, x1, x2, y1, y2, stream=None) -> None:
+    _check(load().petra_stage_forward_noalloc(handle, _ptr(x1), _ptr(x2), _ptr(y1), _ptr(y2),
+                                              _stream(stream)), "petra_stage_forward_noalloc")
 
 
 def petra_stage_profile(handle, enable: bool) -> None:

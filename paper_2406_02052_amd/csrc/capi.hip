@@ -3,6 +3,7 @@
 #include <cstdint>
 #include <cstdio>
 #include <functional>
+#include <mutex>
 #include <new>
 #include <string>
 
@@ -60,6 +61,9 @@ bool any_overlap(const void* a, const void* b, size_t n) {
 petra_status check_ready(const petra_stage* st) {
   if (st == nullptr || st->impl == nullptr) return fail(PETRA_ERR_INVALID_ARG, "null stage handle");
   if (!st->impl->bound()) return fail(PETRA_ERR_STATE, "stage buffers not bound");
+  if (!st->impl->has_workspace())
+    return fail(PETRA_ERR_WORKSPACE,
+                "no workspace bound (such a handle serves petra_stage_forward_noalloc only)");
   return PETRA_OK;
 }
 
@@ -152,6 +156,36 @@ uintptr_t P(const void* p) { return reinterpret_cast<uintptr_t>(p); }
 
 }  // namespace
 
+// Scratch of petra_stage_forward_noalloc: one array per device, held from the
+// library's code object load until the process ends.  Host code never uses
+// its name as an address: the device address comes from hipGetSymbolAddress,
+// once per device, and is kept in g_scratch below.
+static __device__ __align__(256) unsigned char scratch[PETRA_STATIC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices] = {};
+
+// Device address of the current device's copy of `scratch`.
+hipError_t static_scratch(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch[dev] == nullptr) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress((void**)&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch[dev] = ptr;
+  }
+  *out = g_scratch[dev];
+  return hipSuccess;
+}
+
+}  // namespace
 
 extern "C" {
 
@@ -243,7 +277,8 @@ petra_status petra_stage_bind(petra_stage* st, float* params, float* grad_accum,
   if (st == nullptr || st->impl == nullptr) return fail(PETRA_ERR_INVALID_ARG, "null stage handle");
   if (!params || !grad_accum || !momentum || !run_mean || !run_var)
     return fail(PETRA_ERR_INVALID_ARG, "null buffer");
-  if (workspace == nullptr || workspace_bytes < st->impl->ws_need)
+  const bool no_ws = workspace == nullptr && workspace_bytes == 0;
+  if (!no_ws && (workspace == nullptr || workspace_bytes < st->impl->ws_need))
     return fail(PETRA_ERR_WORKSPACE, "workspace missing or smaller than petra_stage_query()");
   const void* ptrs[6] = {params, grad_accum, momentum, run_mean, run_var, workspace};
   for (const void* p : ptrs)
@@ -298,6 +333,28 @@ petra_status petra_stage_forward(petra_stage* st, const void* x1, const void* x2
   petra::Stage& s = *st->impl;
   return launch(s, {CALL_FWD, P(x1), P(x2), P(y1), P(y2)}, static_cast<hipStream_t>(stream),
                 "petra_stage_forward", [&](hipStream_t q) { s.forward(x1, x2, y1, y2, q); });
+}
+
+petra_status petra_stage_forward_noalloc(petra_stage* st, const void* x1, const void* x2,
+                                         void* y1, void* y2, void* stream) {
+  if (st == nullptr || st->impl == nullptr) return fail(PETRA_ERR_INVALID_ARG, "null stage handle");
+  petra::Stage& s = *st->impl;
+  if (!s.bound()) return fail(PETRA_ERR_STATE, "stage buffers not bound");
+  petra_status r;
+  if ((r = check_fwd(s, x1, x2, y1, y2))) return r;
+  if (s.fwd_need > static_cast<size_t>(PETRA_STATIC_SCRATCH_BYTES))
+    return fail(PETRA_ERR_WORKSPACE,
+                "petra_stage_forward_noalloc: the stage's forward needs " +
+                    std::to_string(s.fwd_need) + " bytes of scratch; the static scratch holds " +
+                    std::to_string(static_cast<size_t>(PETRA_STATIC_SCRATCH_BYTES)));
+  if ((r = check_hip("before petra_stage_forward_noalloc"))) return r;
+  void* base = nullptr;
+  const hipError_t e = static_scratch(&base);
+  if (e != hipSuccess)
+    return fail(PETRA_ERR_HIP, std::string("petra_stage_forward_noalloc: scratch address: ") +
+                                   hipGetErrorString(e));
+  s.forward_on(static_cast<char*>(base), x1, x2, y1, y2, static_cast<hipStream_t>(stream));
+  return launch_status(s, "petra_stage_forward_noalloc");
 }
 
 petra_status petra_stage_reconstruct_backward(petra_stage* st, const void* y1, const void* y2,

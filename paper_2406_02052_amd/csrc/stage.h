@@ -71,6 +71,7 @@ class Stage {
 
   // Workspace plan (byte offsets).
   size_t ws_need = 0;
+  size_t fwd_need = 0;   // leading workspace bytes the forward uses (copies + scratch set)
   size_t off_wfwd = 0, off_wdg = 0;
   struct ScratchPlan {
     size_t h[3], d1[2], part, gpart, bpart, bnp;
@@ -127,10 +128,15 @@ class Stage {
   hipEvent_t ev_wgdone[2] = {nullptr, nullptr};  // weight gradients done with set p
 
   bool bound() const { return theta != nullptr; }
+  bool has_workspace() const { return ws != nullptr; }
   void bind(float* th, float* gr, float* mo, float* rm, float* rv, void* w);
   void sync_weights(hipStream_t st);
   // Kernel sequences (enqueue only; no host-side bookkeeping).
   void forward(const void* x1, const void* x2, void* y1, void* y2, hipStream_t st);
+  // The forward with its compute copies and scratch set laid out at `base` as in
+  // the first fwd_need bytes of the workspace (the copies refreshed first).
+  void forward_on(char* base, const void* x1, const void* x2, void* y1, void* y2,
+                  hipStream_t st);
   // The forward on a given scratch set (the backward's sb[0] for a recompute that
   // runs on the backward's stream while another forward may be in flight).
   void forward_with(const void* x1, const void* x2, void* y1, void* y2, Scratch& s,

@@ -166,6 +166,7 @@ Stage::Stage(const petra_stage_desc& d) : desc(d) {
     p->gpart = bwd ? take(static_cast<size_t>(tiles_max) * 2 * cmax * sizeof(float)) : 0;
     p->bpart = bwd ? take(static_cast<size_t>(tiles_max) * 2 * cmax * sizeof(float)) : 0;
     p->bnp = take(static_cast<size_t>(3) * 8 * cmax * sizeof(float));
+    if (p == &plan_f) fwd_need = off;   // compute copies + the forward's scratch set
   }
   off_wpart = take(static_cast<size_t>(wpart_floats) * sizeof(float));
   if (defer_wgrad && blocks.size() > 1)
@@ -205,6 +206,15 @@ void Stage::bind(float* th, float* gr, float* mo, float* rm, float* rv, void* w)
   theta = th; grad = gr; mom = mo; rmean = rm; rvar = rv;
   ws = static_cast<char*>(w);
   sb.assign(plan_b.size(), Scratch{});
+  if (ws == nullptr) {
+    // bound for the scratch-free forward only: no workspace-backed pointers
+    wfwd = wdg = nullptr;
+    sf = Scratch{};
+    wpart = nullptr;
+    reset_view();
+    graphs.clear();
+    return;
+  }
   wfwd = ws + off_wfwd;
   wdg = ws + off_wdg;
   reset_view();
@@ -473,6 +483,24 @@ void Stage::fn_grad(const BwdFn& f, Scratch& s, const BwdFn* next, Scratch* sn, 
 
 void Stage::forward(const void* x1, const void* x2, void* y1, void* y2, hipStream_t st) {
   forward_with(x1, x2, y1, y2, sf, st);
+}
+
+void Stage::forward_on(char* base, const void* x1, const void* x2, void* y1, void* y2,
+                       hipStream_t st) {
+  void* wf = base + off_wfwd;
+  void* wd = base + off_wdg;
+  // the compute copies of the current master parameters, then the forward
+  refresh_weights(dt, theta, segs, max_wnumel, wf, wd, st);
+  Scratch s = carve(plan_f, base, false);
+  const float* th0 = v_th;
+  const void* wf0 = v_wf;
+  const void* wd0 = v_wd;
+  const bool pe = prof.enabled;
+  prof.enabled = false;   // no timing events (they would be created on first use)
+  set_view(theta, wf, wd);
+  forward_with(x1, x2, y1, y2, s, st);
+  set_view(th0, wf0, wd0);
+  prof.enabled = pe;
 }
 
 void Stage::forward_with(const void* x1, const void* x2, void* y1, void* y2, Scratch& s,
