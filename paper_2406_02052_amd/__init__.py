@@ -5,8 +5,13 @@ of include/petra.h); this package holds its ctypes binding and a small
 buffer-owning helper.  Importing the package loads the library and fails if
 it has not been built.
 """
-from . import _lib
-from ._lib import *  # noqa: F401,F403  (the petra_* wrappers, same names as the C ABI)
+# torch first: it ships its own HIP runtime under the same soname as the
+# system one, and the library must bind to the runtime that owns the device
+# memory torch hands it
+import torch  # noqa: F401,E402
+
+from . import _lib  # noqa: E402
+from ._lib import *  # noqa: F401,F403,E402  (the petra_* wrappers, same names as the C ABI)
 
 _lib.load()
 

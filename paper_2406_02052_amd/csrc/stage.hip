@@ -115,9 +115,13 @@ Stage::Stage(const petra_stage_desc& d) : desc(d) {
     f.c_in = cv.cin; f.c_out = cv.cout; f.k_tot = cv.r * cv.s * cv.cin;
     ConvArgs g = conv_args(cv);
     g.c_in = cv.cout; g.c_out = cv.cin; g.k_tot = cv.r * cv.s * cv.cout;
+    // the input-gradient convs run with the BN-backward prologue
+    ConvArgs gb = g;
+    gb.pro_h = reinterpret_cast<const void*>(16);
     for (int ep : {EP_STATS, EP_MASK, EP_RESID_STATS}) {
       tiles_max = std::max(tiles_max, conv_row_tiles(dt, f, ep));
       tiles_max = std::max(tiles_max, conv_row_tiles(dt, g, ep));
+      if (ep != EP_STATS) tiles_max = std::max(tiles_max, conv_row_tiles(dt, gb, ep));
     }
   }
   // each conv layer has its own weight-gradient partials, so their reduces can
