@@ -364,9 +364,12 @@ def bench_stage(args, wl, cpu=True, cold=True):
                              "note": "each step timed alone after rewriting a buffer twice "
                                      "the size of the last-level cache"}
     if not args.no_profile:
+        # per-launch durations from a pass of the same steps with every launch
+        # on one stream (forward, backward, update in order), so each timed
+        # launch has the device to itself as in a kernel trace
         petra_stage_profile(st.handle, True)
         for _ in range(args.steps):
-            one_step(st, t)
+            one_step_serial(st, t)
         torch.cuda.synchronize()
         prof = {k: v for k, v in petra_stage_profile_read(st.handle).items() if v[0] > 0}
         kern = petra_stage_profile_kernel(st.handle)
