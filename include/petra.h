@@ -159,9 +159,10 @@ petra_status petra_stage_set_graphs(petra_stage* st, int32_t enable);
 /* Streams used by one backward call: 1 = every kernel on one stream; 2 = the
  * weight gradients on a second stream; 3 = in addition the recompute of the
  * next residual function on a third stream, overlapped with the input-gradient
- * chain of the current one.  Default: 1 for PETRA_BLOCK_BASIC stages (the
- * cross-stream event calls cost more host time than the overlap saves), 3 for
- * PETRA_BLOCK_BOTTLENECK stages.  Results are identical in every mode.
+ * chain of the current one.  Default: 1 for every block kind (with one stream
+ * the weight gradients wait for the end of the backward and run grouped, which
+ * fills the chip better than per-layer launches beside the chain).  Results
+ * are identical in every mode.
  * PETRA_ERR_INVALID_ARG outside [1, 3]. */
 petra_status petra_stage_set_streams(petra_stage* st, int32_t n);
 

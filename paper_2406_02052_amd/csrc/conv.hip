@@ -20,6 +20,7 @@
 // the reduction is split over row chunks whose fp32 partial sums are reduced
 // in a fixed order by wgrad_reduce (deterministic, no float atomics).
 #include <algorithm>
+#include <type_traits>
 
 #include "common.h"
 #include "kernels.h"
@@ -1604,8 +1605,10 @@ struct UnitTile {
 // the next unit's loads in flight during the current unit's MFMAs and stores;
 // no barrier until the end.  BN moments are shifted sums in registers (shift:
 // the stored value of the wave's first pixel, per channel), combined over the
-// four waves once per workgroup: partial row = blockIdx.x.
-template <int K, int N, int PRO>
+// four waves once per workgroup: partial row = blockIdx.x.  ST = false: the
+// statistics only (nothing stored; the coupling kernel below recomputes the
+// output where it is consumed).
+template <int K, int N, int PRO, bool ST = true>
 __global__ __launch_bounds__(256) void conv1x1_kernel(ConvArgs a, int units) {
   using T = bf16_t;
   constexpr int KB = K / 32, NB = N / 16;
@@ -1664,9 +1667,9 @@ __global__ __launch_bounds__(256) void conv1x1_kernel(ConvArgs a, int units) {
     for (int e = 0; e < 4; ++e) sa[nb][e] = sb[nb][e] = kk[nb][e] = 0.f;
   float nv = 0.f;
   bool first = true;
-  for (; u < units; u += W) {
-    const int un = u + W;
-    if (un < units) load_unit(un, xn);
+  // one unit; FULL: all 16 pixels inside the tensor (every unit but a ragged last one)
+  auto unit = [&](auto full_t) {
+    constexpr bool FULL = decltype(full_t)::value;
     Frag<T> xf[KB];
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb) {
@@ -1682,7 +1685,7 @@ __global__ __launch_bounds__(256) void conv1x1_kernel(ConvArgs a, int units) {
       xf[kb].set(r);
     }
     const long pix = static_cast<long>(u) * 16 + lr;
-    const bool vm = pix < m;
+    const bool vm = FULL || pix < m;
     nv += vm ? 1.f : 0.f;
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
@@ -1690,7 +1693,7 @@ __global__ __launch_bounds__(256) void conv1x1_kernel(ConvArgs a, int units) {
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb) acc = mfma(wf[nb][kb], xf[kb], acc);
       const uint32_t w0 = pack_bf16x2(acc[0], acc[1]), w1 = pack_bf16x2(acc[2], acc[3]);
-      otile[wave].put(lr, lg, nb, w0, w1);
+      if constexpr (ST) otile[wave].put(lr, lg, nb, w0, w1);
       // statistics of the stored values
       float v[4];
       v[0] = __uint_as_float(w0 << 16); v[1] = __uint_as_float(w0 & 0xffff0000u);
@@ -1707,7 +1710,15 @@ __global__ __launch_bounds__(256) void conv1x1_kernel(ConvArgs a, int units) {
         sb[nb][e] = fmaf(d, d, sb[nb][e]);
       }
     }
-    otile[wave].store(r_out, u, m, lane);
+    if constexpr (ST) otile[wave].store(r_out, u, m, lane);
+  };
+  for (; u < units; u += W) {
+    const int un = u + W;
+    if (un < units) load_unit(un, xn);
+    if ((static_cast<long>(u) + 1) * 16 <= m)
+      unit(std::true_type{});
+    else
+      unit(std::false_type{});
     first = false;
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb) xr[kb] = xn[kb];
@@ -1744,6 +1755,121 @@ __global__ __launch_bounds__(256) void conv1x1_kernel(ConvArgs a, int units) {
     a.partials[(row * 3 + 0) * N + c] = n;
     a.partials[(row * 3 + 1) * N + c] = n * mean;
     a.partials[(row * 3 + 2) * N + c] = m2;
+  }
+}
+
+// Coupling of a residual function whose last layer is a streaming 1x1 conv
+// (the forward add of Eq. 4, or the reconstruction's subtraction): out =
+// r + (scale h + shift), or r - (scale h + shift) with SUB, where h is that
+// conv's output as the statistics pass rounds it to bf16 (same operands, same
+// MFMA order, same rounding: the same bits) -- recomputed from the layer's
+// input (C_in = K channels, read once) instead of being stored at C_out = N
+// channels and read back.  The BN of h enters through ep_scale / ep_shift, the
+// layer's own BN-apply + ReLU prologue through pro_scale / pro_shift as in
+// conv1x1_kernel.  Each wave streams 16-pixel units with the input and
+// residual rows of the next unit in flight; the residual goes through the
+// wave's LDS tile into the MFMA layout and the result back out as whole rows.
+// out may alias resid: a unit's rows are read before they are written, by the
+// one wave that owns the unit.
+template <int K, int N, bool SUB>
+__global__ __launch_bounds__(256) void conv1x1_couple_kernel(ConvArgs a, int units) {
+  using T = bf16_t;
+  constexpr int KB = K / 32, NB = N / 16;
+  using Tile = UnitTile<N>;
+  constexpr int CH = Tile::PER_LANE;
+  __shared__ __attribute__((aligned(16))) Tile otile[4];   // residual in, result out
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int lr = lane & 15, lg = lane >> 4;
+  const long m = a.m;
+  const __amdgpu_buffer_rsrc_t r_src = make_rsrc(a.src, m * K * 2);
+  const __amdgpu_buffer_rsrc_t r_out = make_rsrc(a.out, m * N * 2);
+  const __amdgpu_buffer_rsrc_t r_res = make_rsrc(a.resid, m * N * 2);
+  const __amdgpu_buffer_rsrc_t r_wt = make_rsrc(a.wt, static_cast<long>(N) * K * 2);
+  struct Unit {
+    u32x4_t x[KB];
+    u32x4_t rs[CH];
+  };
+  auto load_unit = [&](int u, Unit& d) {
+    const long pix = static_cast<long>(u) * 16 + lr;
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      const uint32_t off =
+          pix < m ? static_cast<uint32_t>((pix * K + kb * 32 + lg * 8) * 2) : BUF_OOB;
+      d.x[kb] = buf_load16(r_src, off);
+    }
+    Tile::load_rows(r_res, u, m, lane, d.rs);
+  };
+  const int W = gridDim.x * 4;
+  int u = blockIdx.x * 4 + wave;
+  Unit cur, nxt;
+  if (u < units) load_unit(u, cur);
+
+  Frag<T> wf[NB][KB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      Raw8<T> r;
+      r.set(buf_load16(r_wt, static_cast<uint32_t>(((nb * 16 + lr) * K + kb * 32 + lg * 8) * 2)));
+      wf[nb][kb].set(r);
+    }
+  float ps[KB][8], pt[KB][8];
+#pragma unroll
+  for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      ps[kb][j] = a.pro_scale[kb * 32 + lg * 8 + j];
+      pt[kb][j] = a.pro_shift[kb * 32 + lg * 8 + j];
+    }
+  float cs[NB][4], csh[NB][4];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      cs[nb][e] = a.ep_scale[nb * 16 + lg * 4 + e];
+      csh[nb][e] = a.ep_shift[nb * 16 + lg * 4 + e];
+    }
+  for (; u < units; u += W) {
+    const int un = u + W;
+    if (un < units) load_unit(un, nxt);
+    Frag<T> xf[KB];
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      Raw8<T> r;
+      r.set(cur.x[kb]);
+      float v[8];
+      r.to_f32(v);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[j] = fmaxf(fmaf(ps[kb][j], v[j], pt[kb][j]), 0.f);
+      r.from_f32(v);   // rounded to bf16, as the materialised activation
+      xf[kb].set(r);
+    }
+    otile[wave].park_rows(cur.rs, lane);
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) acc = mfma(wf[nb][kb], xf[kb], acc);
+      // h as the statistics pass rounds it
+      const uint32_t h0 = pack_bf16x2(acc[0], acc[1]), h1 = pack_bf16x2(acc[2], acc[3]);
+      float h[4];
+      h[0] = __uint_as_float(h0 << 16); h[1] = __uint_as_float(h0 & 0xffff0000u);
+      h[2] = __uint_as_float(h1 << 16); h[3] = __uint_as_float(h1 & 0xffff0000u);
+      const u32x2_t rw = otile[wave].get(lr, lg, nb);
+      float r[4];
+      r[0] = __uint_as_float(rw.x << 16); r[1] = __uint_as_float(rw.x & 0xffff0000u);
+      r[2] = __uint_as_float(rw.y << 16); r[3] = __uint_as_float(rw.y & 0xffff0000u);
+      float o[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float f = fmaf(cs[nb][e], h[e], csh[nb][e]);
+        o[e] = SUB ? r[e] - f : r[e] + f;
+      }
+      otile[wave].put(lr, lg, nb, pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]));
+    }
+    otile[wave].store(r_out, u, m, lane);
+    cur = nxt;
   }
 }
 
@@ -3326,11 +3452,21 @@ int conv1x1_grid(const ConvArgs& a) {
 template <int K, int N>
 void launch_1x1_kn(const ConvArgs& a, hipStream_t st) {
   const dim3 grid(conv1x1_grid(a));
-  if (pro_mode(a) == PRO_RELU)
+  const bool relu = pro_mode(a) == PRO_RELU;
+  if (a.out == nullptr) {   // statistics only
+    if (relu)
+      PETRA_LAUNCH((conv1x1_kernel<K, N, PRO_RELU, false>), grid, dim3(256), 0, st, a,
+                   conv1x1_units(a));
+    else
+      PETRA_LAUNCH((conv1x1_kernel<K, N, PRO_NONE, false>), grid, dim3(256), 0, st, a,
+                   conv1x1_units(a));
+  } else if (relu) {
     PETRA_LAUNCH((conv1x1_kernel<K, N, PRO_RELU>), grid, dim3(256), 0, st, a, conv1x1_units(a));
-  else
+  } else {
     PETRA_LAUNCH((conv1x1_kernel<K, N, PRO_NONE>), grid, dim3(256), 0, st, a, conv1x1_units(a));
+  }
 }
+
 
 template <int K, int N>
 bool launch_1x1_bwd_kn(const ConvArgs& a, int ep, hipStream_t st) {
@@ -3624,6 +3760,28 @@ void wgrad_t(const WgradArgs& a, hipStream_t st) {
 }
 
 }  // namespace
+
+bool conv1x1_couple_ok(int dtype, const ConvArgs& a) {
+  return use_1x1(dtype, a, EP_STATS) && a.c_in == 32 && a.c_out == 128;
+}
+
+bool conv1x1_couple(int dtype, const ConvArgs& a, const float* scale, const float* shift,
+                    bool sub, hipStream_t st) {
+  if (!conv1x1_couple_ok(dtype, a) || pro_mode(a) != PRO_RELU || a.resid == nullptr ||
+      a.out == nullptr || scale == nullptr || shift == nullptr)
+    return false;
+  ConvArgs b = a;
+  b.ep_scale = scale;
+  b.ep_shift = shift;
+  const dim3 grid(conv1x1_grid(b));
+  if (sub)
+    PETRA_LAUNCH((conv1x1_couple_kernel<32, 128, true>), grid, dim3(256), 0, st, b,
+                 conv1x1_units(b));
+  else
+    PETRA_LAUNCH((conv1x1_couple_kernel<32, 128, false>), grid, dim3(256), 0, st, b,
+                 conv1x1_units(b));
+  return true;
+}
 
 int conv_row_tiles(int dtype, const ConvArgs& a, int ep) {
   if (use_1x1(dtype, a, ep)) return conv1x1_grid(a);

@@ -71,6 +71,15 @@ bool conv_gemm(int dtype, const ConvArgs& a, int ep, hipStream_t st);
 // Number of partial-sum rows (output row tiles) conv_gemm writes for these
 // arguments and epilogue.
 int conv_row_tiles(int dtype, const ConvArgs& a, int ep);
+// With a.out == nullptr, conv_gemm's streaming 1x1 forward (EP_STATS) writes
+// the BN partials only.  conv1x1_couple then forms the coupling output
+// a.out = a.resid +/- (scale h + shift) with h = that conv of
+// relu(pro_scale * a.src + pro_shift), recomputed bit for bit as the
+// statistics pass rounded it (a.out may alias a.resid); false, with nothing
+// launched, where it does not apply (conv1x1_couple_ok: bf16 1x1 32 -> 128).
+bool conv1x1_couple_ok(int dtype, const ConvArgs& a);
+bool conv1x1_couple(int dtype, const ConvArgs& a, const float* scale, const float* shift,
+                    bool sub, hipStream_t st);
 void conv_wgrad(int dtype, const WgradArgs& a, hipStream_t st);
 // Transposed-read weight-gradient kernel: configuration (0 = not applicable)
 // and its split count (partial rows) for these arguments; conv_wgrad uses it

@@ -76,6 +76,12 @@ class Stage {
   struct ScratchPlan {
     size_t h[3], d1[2], part, gpart, bpart, bnp;
   };
+  static constexpr size_t NO_BUF = ~static_cast<size_t>(0);   // a buffer the set does not hold
+  // Residual functions whose last conv is the bf16 1x1 32 -> 128: every
+  // coupling (forward add and reconstruction) recomputes that conv's output
+  // from the layer's input; in the forward the conv writes its BN statistics
+  // only (the forward set holds no buffer for it).
+  bool couple_fwd = false;
   ScratchPlan plan_f{};
   std::vector<ScratchPlan> plan_b;   // 2 sets, or one per residual function (defer_wgrad)
   // Weight gradients wait until the end of a single-stream backward and run as
@@ -181,13 +187,20 @@ class Stage {
     void* dout;        // input gradient: rg + dPhi/du^T d
   };
   Scratch carve(const ScratchPlan& p, char* base, bool bwd) const;
+  // stats_only_last: the last conv writes its BN partials only (the forward's
+  // coupling recomputes its output; see couple_fwd)
   void fn_recompute(const ResidualFn& fn, const void* u, Scratch& s, bool running,
-                    hipStream_t st);
+                    hipStream_t st, bool stats_only_last = false);
   void fn_forward(const ResidualFn& fn, const void* u, const void* r, void* y, Scratch& s,
                   hipStream_t st);
   void fn_grad(const BwdFn& f, Scratch& s, const BwdFn* next, Scratch* sn, hipStream_t st,
                hipStream_t wst, hipStream_t rs, bool wait_prev_wg, int parity, int part,
                const void** dsrc_io);
+  // Coupling output of a residual function whose convs s holds (recomputed):
+  // out = r + BN_L(h_L), or r - BN_L(h_L) with sub (the reconstruction); with
+  // couple_fwd h_L is recomputed from h_{L-1}, else read from s.h[L].
+  void coupling(const ResidualFn& fn, Scratch& s, const void* r, void* out, bool sub,
+                hipStream_t st);
   bool conv(const ConvArgs& a, int ep, hipStream_t st);
   ConvArgs conv_args(const ConvLayer& cv) const;
   void wgrad_splits(const ConvLayer& cv, int* splits, int* rows_per_split) const;

@@ -35,7 +35,10 @@ size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 Stage::Stage(const petra_stage_desc& d) : desc(d) {
   dt = d.dtype == PETRA_BF16 ? DT_BF16 : DT_FP32;
-  bwd_streams = d.kind == PETRA_BLOCK_BOTTLENECK ? 3 : 1;
+  // one backward stream: the weight gradients are deferred and grouped (with
+  // three streams they run layer by layer beside the chain; measured slower
+  // for every block kind)
+  bwd_streams = 1;
   esz = dt == DT_BF16 ? 2 : 4;
   M = static_cast<long>(d.n) * d.h * d.w;
   const int c = d.c_half, cm = d.c_mid;
@@ -154,6 +157,13 @@ Stage::Stage(const petra_stage_desc& d) : desc(d) {
       if (wgrad_tr_plan(dt, w, &sp) == 0) defer_wgrad = false;
     }
   }
+  couple_fwd = false;
+  if (!blocks.empty() && blocks[0].f.nconv == 3) {
+    const ConvLayer& cv = convs[blocks[0].f.conv[2]];
+    ConvArgs a = conv_args(cv);
+    a.c_in = cv.cin; a.c_out = cv.cout; a.k_tot = cv.r * cv.s * cv.cin;
+    couple_fwd = conv1x1_couple_ok(dt, a);
+  }
   const int nfn = 2 * static_cast<int>(blocks.size());
   plan_b.assign(defer_wgrad ? std::max(2, nfn) : 2, ScratchPlan{});
   off_wfwd = take(static_cast<size_t>(n_conv) * esz);
@@ -162,7 +172,9 @@ Stage::Stage(const petra_stage_desc& d) : desc(d) {
   for (ScratchPlan& pb : plan_b) plans.push_back(&pb);
   for (ScratchPlan* p : plans) {
     for (size_t l = 0; l < 3; ++l)
-      p->h[l] = l < fn_shapes.size() ? take(static_cast<size_t>(M) * fn_shapes[l].cout * esz) : 0;
+      p->h[l] = l >= fn_shapes.size()                        ? 0
+                : p == &plan_f && couple_fwd && l == 2       ? NO_BUF
+                : take(static_cast<size_t>(M) * fn_shapes[l].cout * esz);
     const bool bwd = p != &plan_f;
     p->d1[0] = bwd ? take(static_cast<size_t>(M) * cmax * esz) : 0;
     p->d1[1] = bwd && fn_shapes.size() > 2 ? take(static_cast<size_t>(M) * cmax * esz) : 0;
@@ -196,7 +208,7 @@ Stage::~Stage() {
 Scratch Stage::carve(const ScratchPlan& p, char* base, bool bwd) const {
   const int nl = blocks.empty() ? 0 : blocks[0].f.nconv;
   Scratch s;
-  for (int l = 0; l < 3; ++l) s.h[l] = l < nl ? base + p.h[l] : nullptr;
+  for (int l = 0; l < 3; ++l) s.h[l] = l < nl && p.h[l] != NO_BUF ? base + p.h[l] : nullptr;
   s.d1[0] = bwd ? base + p.d1[0] : nullptr;
   s.d1[1] = bwd && nl > 2 ? base + p.d1[1] : nullptr;
   s.part = reinterpret_cast<float*>(base + p.part);
@@ -295,8 +307,9 @@ void Stage::wgrad_splits(const ConvLayer& cv, int* splits, int* rows_per_split) 
 }
 
 void Stage::fn_recompute(const ResidualFn& fn, const void* u, Scratch& s, bool running,
-                         hipStream_t st) {
+                         hipStream_t st, bool stats_only_last) {
   for (int l = 0; l < fn.nconv; ++l) {
+    const bool stats_only = stats_only_last && l == fn.nconv - 1;
     const ConvLayer& cv = convs[fn.conv[l]];
     const BnLayer& bn = bns[cv.bn];
     ConvArgs a = conv_args(cv);
@@ -308,15 +321,19 @@ void Stage::fn_recompute(const ResidualFn& fn, const void* u, Scratch& s, bool r
       a.pro_shift = s.vec(l - 1, V_SHIFT, cmax);
     }
     a.wt = static_cast<const char*>(v_wf) + cv.w_off * esz;
-    a.out = s.h[l];
+    a.out = stats_only ? nullptr : s.h[l];
     a.c_out = cv.cout;
     a.k_tot = cv.r * cv.s * cv.cin;
     a.partials = s.part;
+    if (a.out == nullptr && !(stats_only && conv1x1_couple_ok(dt, a))) {
+      launch_error = true;   // no buffer for this output (not reached by the library's calls)
+      return;
+    }
     const int tiles = conv_row_tiles(dt, a, EP_STATS);
     prof.begin(st);
     conv(a, EP_STATS, st);
     prof.end(K_CONV_FPROP, st, 2.0 * M * cv.cout * a.k_tot,
-             static_cast<double>(esz) * (static_cast<double>(M) * (cv.cin + cv.cout) +
+             static_cast<double>(esz) * (static_cast<double>(M) * (cv.cin + (stats_only ? 0 : cv.cout)) +
                                          static_cast<double>(cv.cout) * a.k_tot));
     prof.begin(st);
     bn_stats_finalize(s.part, tiles, cv.cout, M, v_th + bn.g_off, v_th + bn.b_off, desc.bn_eps,
@@ -329,12 +346,43 @@ void Stage::fn_recompute(const ResidualFn& fn, const void* u, Scratch& s, bool r
 
 void Stage::fn_forward(const ResidualFn& fn, const void* u, const void* r, void* y, Scratch& s,
                        hipStream_t st) {
-  fn_recompute(fn, u, s, false, st);
+  // with couple_fwd the last conv writes its statistics only
+  fn_recompute(fn, u, s, false, st, couple_fwd);
+  coupling(fn, s, r, y, false, st);
+}
+
+void Stage::coupling(const ResidualFn& fn, Scratch& s, const void* r, void* out, bool sub,
+                     hipStream_t st) {
   const int L = fn.nconv - 1;
-  const int c = convs[fn.conv[L]].cout;
+  const ConvLayer& cv = convs[fn.conv[L]];
+  const int c = cv.cout;
+  if (couple_fwd) {
+    // h_L recomputed from the layer's input (the same bits as the statistics pass)
+    ConvArgs a = conv_args(cv);
+    a.src = s.h[L - 1];
+    a.c_in = cv.cin;
+    a.c_split = cv.cin;
+    a.pro_scale = s.vec(L - 1, V_SCALE, cmax);
+    a.pro_shift = s.vec(L - 1, V_SHIFT, cmax);
+    a.wt = static_cast<const char*>(v_wf) + cv.w_off * esz;
+    a.out = out;
+    a.resid = r;
+    a.c_out = c;
+    a.k_tot = cv.r * cv.s * cv.cin;
+    prof.begin(st);
+    if (!conv1x1_couple(dt, a, s.vec(L, V_SCALE, cmax), s.vec(L, V_SHIFT, cmax), sub, st))
+      launch_error = true;
+    prof.end(K_CONV_FPROP, st, 2.0 * M * c * a.k_tot,
+             static_cast<double>(esz) * (static_cast<double>(M) * (cv.cin + 2.0 * c) +
+                                         static_cast<double>(c) * a.k_tot));
+    return;
+  }
   prof.begin(st);
-  combine_fwd(dt, r, s.h[L], s.vec(L, V_SCALE, cmax), s.vec(L, V_SHIFT, cmax), y, M, c, st);
-  prof.end(K_COMBINE_FWD, st, 0.0, 3.0 * M * c * esz);
+  if (sub)
+    combine_rec(dt, r, s.h[L], s.vec(L, V_SCALE, cmax), s.vec(L, V_SHIFT, cmax), out, M, c, st);
+  else
+    combine_fwd(dt, r, s.h[L], s.vec(L, V_SCALE, cmax), s.vec(L, V_SHIFT, cmax), out, M, c, st);
+  prof.end(sub ? K_COMBINE_BWD : K_COMBINE_FWD, st, 0.0, 3.0 * M * c * esz);
 }
 
 bool Stage::conv(const ConvArgs& a, int ep, hipStream_t st) {
@@ -532,11 +580,7 @@ void Stage::reconstruct(const void* y1, const void* y2, void* x1, void* x2, hipS
       const void* v = f == 0 ? c2 : c1;
       void* out = f == 0 ? x2 : x1;
       fn_recompute(fn, u, s, false, st);
-      const int L = fn.nconv - 1;
-      const int c = convs[fn.conv[L]].cout;
-      prof.begin(st);
-      combine_rec(dt, v, s.h[L], s.vec(L, V_SCALE, cmax), s.vec(L, V_SHIFT, cmax), out, M, c, st);
-      prof.end(K_COMBINE_BWD, st, 0.0, 3.0 * M * c * esz);
+      coupling(fn, s, v, out, true, st);
     }
     c1 = x1;
     c2 = x2;
@@ -632,12 +676,7 @@ void Stage::backward(const void* y1, const void* y2, const void* dy1, const void
       // input, which this function's weight gradients read
       if (rs != wst) PETRA_HIP(hip_status, hipStreamWaitEvent(rs, ev_wgdone[p], 0));
       const BwdFn& nx = fl[f + 1];
-      const int L = nx.fn->nconv - 1;
-      const int c = last_c(nx);
-      prof.begin(rs);
-      combine_rec(dt, nx.v, sn->h[L], sn->vec(L, V_SCALE, cmax), sn->vec(L, V_SHIFT, cmax),
-                  nx.xrec, M, c, rs);
-      prof.end(K_COMBINE_BWD, rs, 0.0, 3.0 * M * c * esz);
+      coupling(*nx.fn, *sn, nx.v, nx.xrec, true, rs);
     }
   }
   defer_cur = false;

@@ -49,6 +49,17 @@ def test_forward_noalloc_matches_forward_two_calls_second_smaller():
             assert np.array_equal(a, b)
 
 
+def test_forward_noalloc_matches_forward_bottleneck_full_size():
+    """The bottleneck stage at its full batch (its forward keeps the two
+    32-channel pre-BN tensors only: the 128-channel one is recomputed where the
+    coupling consumes it, so the working set fits the static array)."""
+    wl = synth.IMAGENET_BOTTLENECK_STAGE
+    print(f"noalloc case {wl.name} n={wl.n}", flush=True)
+    want, got = _forward_both(wl)
+    for a, b in zip(want, got):
+        assert np.array_equal(a, b)
+
+
 def test_forward_noalloc_on_a_handle_without_workspace():
     import torch
     from paper_2406_02052_amd import PetraError, Stage, to_host
@@ -78,9 +89,9 @@ def test_forward_noalloc_rejects_a_stage_beyond_the_scratch():
     from paper_2406_02052_amd import _lib as L
 
     _, fwd_noalloc = _lib()
-    # the bottleneck stage's forward holds 77 MB of pre-BN tensors
+    # at batch 192 the bottleneck stage's forward holds two 38.5 MB pre-BN tensors
     wl = synth.IMAGENET_BOTTLENECK_STAGE
-    st = gpu_stage(wl.with_(n=64), synth.stage_params(wl, "random"))
+    st = gpu_stage(wl.with_(n=192), synth.stage_params(wl, "random"))
     a = [st.act() for _ in range(4)]
     rc = fwd_noalloc(st.handle, *(t.data_ptr() for t in a), None)
     assert L.STATUS[rc] == "PETRA_ERR_WORKSPACE"
