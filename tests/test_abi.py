@@ -84,6 +84,26 @@ def test_create_rejects_bad_descriptions(field, value, status):
     assert L.petra_last_error() != ""
 
 
+def test_create_enforces_the_32_bit_buffer_offset_limit():
+    """Every kernel addresses activations through buffer resources with 32-bit
+    byte offsets and 2^31 as the out-of-range sentinel, so a stage whose
+    half-tensor reaches 2^31 bytes is refused at creation (PETRA_ERR_SHAPE);
+    one just below is accepted.  Host only: creation allocates nothing."""
+    from paper_2406_02052_amd import _lib as L
+    wl = synth.CIFAR_STAGE            # 32 x 32 x 32 bf16: 65536 bytes per image
+    per_image = wl.h * wl.w * wl.c_half * 2
+    limit_n = (1 << 31) // per_image  # first batch at the limit
+    d = _desc(wl)
+    d.n = limit_n
+    with pytest.raises(L.PetraError) as e:
+        L.petra_stage_create(d)
+    assert e.value.name == "PETRA_ERR_SHAPE"
+    assert "2^31" in L.petra_last_error()
+    d.n = limit_n - 1
+    h = L.petra_stage_create(d)
+    L.petra_stage_destroy(h)
+
+
 def test_bind_and_call_validation_without_device_work():
     from paper_2406_02052_amd import _lib as L
     wl = synth.CIFAR_STAGE.with_(n=2, h=4, w=4)
