@@ -1771,13 +1771,25 @@ __global__ __launch_bounds__(256) void conv1x1_kernel(ConvArgs a, int units) {
 // wave's LDS tile into the MFMA layout and the result back out as whole rows.
 // out may alias resid: a unit's rows are read before they are written, by the
 // one wave that owns the unit.
-template <int K, int N, bool SUB>
-__global__ __launch_bounds__(256) void conv1x1_couple_kernel(ConvArgs a, int units) {
+// NX: the coupling output is also the input of the next residual function,
+// whose first layer is the 1x1 N -> K conv: the unit's output rows, still in
+// the LDS tile, feed that conv's MFMAs directly, and its output (stored at
+// nx.out) and BN partials (nx.partials, row = blockIdx.x) are exactly what
+// conv1x1_kernel<N, K, PRO_NONE> would produce from the stored output: the
+// same grid, units per wave, operands, MFMA order, rounding and statistics.
+
+template <int K, int N, bool SUB, bool NX>
+__global__ __launch_bounds__(256) void conv1x1_couple_kernel(ConvArgs a, int units, NextConv nx) {
   using T = bf16_t;
   constexpr int KB = K / 32, NB = N / 16;
+  constexpr int KB2 = N / 32, NB2 = K / 16;   // the next conv: N -> K
   using Tile = UnitTile<N>;
+  using Tile2 = UnitTile<K>;
   constexpr int CH = Tile::PER_LANE;
   __shared__ __attribute__((aligned(16))) Tile otile[4];   // residual in, result out
+  __shared__ __attribute__((aligned(16))) Tile2 ntile[NX ? 4 : 1];
+  __shared__ float red[NX ? 4 : 1][3][K];
+  __shared__ float cst[2][NX ? N : 1];   // BN of h (scale, shift) when registers are short
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
@@ -1786,6 +1798,15 @@ __global__ __launch_bounds__(256) void conv1x1_couple_kernel(ConvArgs a, int uni
   const __amdgpu_buffer_rsrc_t r_out = make_rsrc(a.out, m * N * 2);
   const __amdgpu_buffer_rsrc_t r_res = make_rsrc(a.resid, m * N * 2);
   const __amdgpu_buffer_rsrc_t r_wt = make_rsrc(a.wt, static_cast<long>(N) * K * 2);
+  const __amdgpu_buffer_rsrc_t r_nout = make_rsrc(NX ? nx.out : a.out, NX ? m * K * 2 : 0);
+  const __amdgpu_buffer_rsrc_t r_nwt =
+      make_rsrc(NX ? nx.wt : a.wt, NX ? static_cast<long>(K) * N * 2 : 0);
+  if constexpr (NX) {
+    for (int c = tid; c < N; c += 256) {
+      cst[0][c] = a.ep_scale[c];
+      cst[1][c] = a.ep_shift[c];
+    }
+  }
   struct Unit {
     u32x4_t x[KB];
     u32x4_t rs[CH];
@@ -1814,6 +1835,19 @@ __global__ __launch_bounds__(256) void conv1x1_couple_kernel(ConvArgs a, int uni
       r.set(buf_load16(r_wt, static_cast<uint32_t>(((nb * 16 + lr) * K + kb * 32 + lg * 8) * 2)));
       wf[nb][kb].set(r);
     }
+  // the next conv's weight fragments (as conv1x1_kernel<N, K> holds them)
+  Frag<T> wf2[NX ? NB2 : 1][NX ? KB2 : 1];
+  if constexpr (NX) {
+#pragma unroll
+    for (int nb = 0; nb < NB2; ++nb)
+#pragma unroll
+      for (int kb = 0; kb < KB2; ++kb) {
+        Raw8<T> r;
+        r.set(buf_load16(r_nwt,
+                         static_cast<uint32_t>(((nb * 16 + lr) * N + kb * 32 + lg * 8) * 2)));
+        wf2[nb][kb].set(r);
+      }
+  }
   float ps[KB][8], pt[KB][8];
 #pragma unroll
   for (int kb = 0; kb < KB; ++kb)
@@ -1822,17 +1856,27 @@ __global__ __launch_bounds__(256) void conv1x1_couple_kernel(ConvArgs a, int uni
       ps[kb][j] = a.pro_scale[kb * 32 + lg * 8 + j];
       pt[kb][j] = a.pro_shift[kb * 32 + lg * 8 + j];
     }
-  float cs[NB][4], csh[NB][4];
+  float cs[NX ? 1 : NB][4], csh[NX ? 1 : NB][4];
+  if constexpr (!NX) {
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb)
+    for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      cs[nb][e] = a.ep_scale[nb * 16 + lg * 4 + e];
-      csh[nb][e] = a.ep_shift[nb * 16 + lg * 4 + e];
-    }
-  for (; u < units; u += W) {
-    const int un = u + W;
-    if (un < units) load_unit(un, nxt);
+      for (int e = 0; e < 4; ++e) {
+        cs[nb][e] = a.ep_scale[nb * 16 + lg * 4 + e];
+        csh[nb][e] = a.ep_shift[nb * 16 + lg * 4 + e];
+      }
+  }
+  // the next conv's BN moments: shifted sums per lane, as in conv1x1_kernel
+  float sa[NX ? NB2 : 1][4], sb[NX ? NB2 : 1][4], kk[NX ? NB2 : 1][4];
+#pragma unroll
+  for (int nb = 0; nb < (NX ? NB2 : 1); ++nb)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) sa[nb][e] = sb[nb][e] = kk[nb][e] = 0.f;
+  float nv = 0.f;
+  bool first = true;
+  if constexpr (NX) __syncthreads();   // cst
+  auto unit = [&](auto full_t) {
+    constexpr bool FULL = decltype(full_t)::value;
     Frag<T> xf[KB];
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb) {
@@ -1863,13 +1907,99 @@ __global__ __launch_bounds__(256) void conv1x1_couple_kernel(ConvArgs a, int uni
       float o[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const float f = fmaf(cs[nb][e], h[e], csh[nb][e]);
+        const int c = nb * 16 + lg * 4 + e;
+        const float f = NX ? fmaf(cst[0][c], h[e], cst[1][c])
+                           : fmaf(cs[NX ? 0 : nb][e], h[e], csh[NX ? 0 : nb][e]);
         o[e] = SUB ? r[e] - f : r[e] + f;
       }
       otile[wave].put(lr, lg, nb, pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]));
     }
     otile[wave].store(r_out, u, m, lane);
+    if constexpr (NX) {
+      // the next conv on the unit's output rows: lane (lr, lg) takes channels
+      // kb * 32 + lg * 8 .. + 7 of pixel lr, as a row load of the stored tensor would
+      Frag<T> yf[KB2];
+#pragma unroll
+      for (int kb = 0; kb < KB2; ++kb) {
+        const uint32_t* p = otile[wave].w + lr * Tile::ROW + (kb * 32 + lg * 8) / 2;
+        const u32x2_t lo = *reinterpret_cast<const u32x2_t*>(p);
+        const u32x2_t hi = *reinterpret_cast<const u32x2_t*>(p + 2);
+        Raw8<T> rr;
+        rr.set(u32x4_t{lo.x, lo.y, hi.x, hi.y});
+        yf[kb].set(rr);
+      }
+      const long pix = static_cast<long>(u) * 16 + lr;
+      const bool vm = FULL || pix < m;
+      nv += vm ? 1.f : 0.f;
+#pragma unroll
+      for (int nb = 0; nb < NB2; ++nb) {
+        f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kb = 0; kb < KB2; ++kb) acc = mfma(wf2[nb][kb], yf[kb], acc);
+        const uint32_t w0 = pack_bf16x2(acc[0], acc[1]), w1 = pack_bf16x2(acc[2], acc[3]);
+        ntile[wave].put(lr, lg, nb, w0, w1);
+        float v[4];
+        v[0] = __uint_as_float(w0 << 16); v[1] = __uint_as_float(w0 & 0xffff0000u);
+        v[2] = __uint_as_float(w1 << 16); v[3] = __uint_as_float(w1 & 0xffff0000u);
+        if (first) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) kk[nb][e] = __shfl(v[e], lane & 48, 64);
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float d = vm ? v[e] - kk[nb][e] : 0.f;
+          sa[nb][e] += d;
+          sb[nb][e] = fmaf(d, d, sb[nb][e]);
+        }
+      }
+      ntile[wave].store(r_nout, u, m, lane);
+    }
+  };
+  for (; u < units; u += W) {
+    const int un = u + W;
+    if (un < units) load_unit(un, nxt);
+    if ((static_cast<long>(u) + 1) * 16 <= m)
+      unit(std::true_type{});
+    else
+      unit(std::false_type{});
+    first = false;
     cur = nxt;
+  }
+  if constexpr (NX) {
+    // per wave: (n, mean, centred M2) of every channel; then Chan over the
+    // waves (the reduction of conv1x1_kernel)
+    const float n16 = sum16(nv);
+#pragma unroll
+    for (int nb = 0; nb < NB2; ++nb)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float x = sum16(sa[nb][e]), y = sum16(sb[nb][e]);
+        if (lr == 0) {
+          const int c = nb * 16 + lg * 4 + e;
+          const float md = n16 > 0.f ? x / n16 : 0.f;
+          red[wave][0][c] = n16;
+          red[wave][1][c] = kk[nb][e] + md;
+          red[wave][2][c] = n16 > 0.f ? fmaxf(y - x * md, 0.f) : 0.f;
+        }
+      }
+    __syncthreads();
+    for (int c = tid; c < K; c += 256) {
+      float n = 0.f, mean = 0.f, m2 = 0.f;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const float nb = red[w][0][c];
+        if (nb > 0.f) {
+          const float nn = n + nb, rb = nb / nn, d = red[w][1][c] - mean;
+          mean += d * rb;
+          m2 += red[w][2][c] + d * d * n * rb;
+          n = nn;
+        }
+      }
+      const long row = blockIdx.x;
+      nx.partials[(row * 3 + 0) * K + c] = n;
+      nx.partials[(row * 3 + 1) * K + c] = n * mean;
+      nx.partials[(row * 3 + 2) * K + c] = m2;
+    }
   }
 }
 
@@ -3765,21 +3895,37 @@ bool conv1x1_couple_ok(int dtype, const ConvArgs& a) {
   return use_1x1(dtype, a, EP_STATS) && a.c_in == 32 && a.c_out == 128;
 }
 
+bool conv1x1_couple_next_ok(int dtype, const ConvArgs& a, const ConvArgs& next) {
+  return conv1x1_couple_ok(dtype, a) && use_1x1(dtype, next, EP_STATS) && next.c_in == 128 &&
+         next.c_out == 32 && next.m == a.m && next.pro_scale == nullptr &&
+         conv_row_tiles(dtype, next, EP_STATS) == conv1x1_grid(a);
+}
+
 bool conv1x1_couple(int dtype, const ConvArgs& a, const float* scale, const float* shift,
-                    bool sub, hipStream_t st) {
+                    bool sub, hipStream_t st, const NextConv* next) {
   if (!conv1x1_couple_ok(dtype, a) || pro_mode(a) != PRO_RELU || a.resid == nullptr ||
       a.out == nullptr || scale == nullptr || shift == nullptr)
+    return false;
+  if (next != nullptr &&
+      (next->wt == nullptr || next->out == nullptr || next->partials == nullptr))
     return false;
   ConvArgs b = a;
   b.ep_scale = scale;
   b.ep_shift = shift;
   const dim3 grid(conv1x1_grid(b));
-  if (sub)
-    PETRA_LAUNCH((conv1x1_couple_kernel<32, 128, true>), grid, dim3(256), 0, st, b,
-                 conv1x1_units(b));
+  const NextConv nx = next != nullptr ? *next : NextConv{};
+  if (next != nullptr && sub)
+    PETRA_LAUNCH((conv1x1_couple_kernel<32, 128, true, true>), grid, dim3(256), 0, st, b,
+                 conv1x1_units(b), nx);
+  else if (next != nullptr)
+    PETRA_LAUNCH((conv1x1_couple_kernel<32, 128, false, true>), grid, dim3(256), 0, st, b,
+                 conv1x1_units(b), nx);
+  else if (sub)
+    PETRA_LAUNCH((conv1x1_couple_kernel<32, 128, true, false>), grid, dim3(256), 0, st, b,
+                 conv1x1_units(b), nx);
   else
-    PETRA_LAUNCH((conv1x1_couple_kernel<32, 128, false>), grid, dim3(256), 0, st, b,
-                 conv1x1_units(b));
+    PETRA_LAUNCH((conv1x1_couple_kernel<32, 128, false, false>), grid, dim3(256), 0, st, b,
+                 conv1x1_units(b), nx);
   return true;
 }
 

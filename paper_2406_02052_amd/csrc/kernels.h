@@ -77,9 +77,21 @@ int conv_row_tiles(int dtype, const ConvArgs& a, int ep);
 // relu(pro_scale * a.src + pro_shift), recomputed bit for bit as the
 // statistics pass rounded it (a.out may alias a.resid); false, with nothing
 // launched, where it does not apply (conv1x1_couple_ok: bf16 1x1 32 -> 128).
+// With next, the coupling output (sum or reconstruction) is also fed to the next
+// residual function's first conv, the 1x1 128 -> 32 (weights next->wt): its
+// pre-BN output goes to next->out and its BN partials to next->partials,
+// exactly as conv_gemm (EP_STATS, no prologue) would write them from the
+// stored coupling output (the same partial rows: conv_row_tiles of that conv).
+struct NextConv {
+  const void* wt;   // [K][N] weights of the next function's first conv
+  void* out;        // [m][K] its pre-BN output
+  float* partials;  // [grid][3][K] its BN partials
+};
 bool conv1x1_couple_ok(int dtype, const ConvArgs& a);
+// Whether the coupling of `a` can also run `next` (that first conv, EP_STATS).
+bool conv1x1_couple_next_ok(int dtype, const ConvArgs& a, const ConvArgs& next);
 bool conv1x1_couple(int dtype, const ConvArgs& a, const float* scale, const float* shift,
-                    bool sub, hipStream_t st);
+                    bool sub, hipStream_t st, const NextConv* next = nullptr);
 void conv_wgrad(int dtype, const WgradArgs& a, hipStream_t st);
 // Transposed-read weight-gradient kernel: configuration (0 = not applicable)
 // and its split count (partial rows) for these arguments; conv_wgrad uses it

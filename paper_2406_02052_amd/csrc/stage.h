@@ -82,6 +82,8 @@ class Stage {
   // from the layer's input; in the forward the conv writes its BN statistics
   // only (the forward set holds no buffer for it).
   bool couple_fwd = false;
+  // ... and the coupling also runs the next function's first conv (1x1 128 -> 32)
+  bool couple_next = false;
   ScratchPlan plan_f{};
   std::vector<ScratchPlan> plan_b;   // 2 sets, or one per residual function (defer_wgrad)
   // Weight gradients wait until the end of a single-stream backward and run as
@@ -189,18 +191,27 @@ class Stage {
   Scratch carve(const ScratchPlan& p, char* base, bool bwd) const;
   // stats_only_last: the last conv writes its BN partials only (the forward's
   // coupling recomputes its output; see couple_fwd)
+  // first_done: the first conv already ran (its output in s.h[0], its BN
+  // partials in s.part, written by the previous function's coupling); only its
+  // finalize is enqueued.
   void fn_recompute(const ResidualFn& fn, const void* u, Scratch& s, bool running,
-                    hipStream_t st, bool stats_only_last = false);
-  void fn_forward(const ResidualFn& fn, const void* u, const void* r, void* y, Scratch& s,
-                  hipStream_t st);
+                    hipStream_t st, bool stats_only_last = false, bool first_done = false);
+  // Forward of one residual function (y = r + fn(u)).  With next set and
+  // couple_next, the coupling also runs next's first conv on y; returns
+  // whether it did (then next's forward passes first_done).
+  bool fn_forward(const ResidualFn& fn, const void* u, const void* r, void* y, Scratch& s,
+                  hipStream_t st, bool first_done = false, const ResidualFn* next = nullptr);
   void fn_grad(const BwdFn& f, Scratch& s, const BwdFn* next, Scratch* sn, hipStream_t st,
                hipStream_t wst, hipStream_t rs, bool wait_prev_wg, int parity, int part,
                const void** dsrc_io);
   // Coupling output of a residual function whose convs s holds (recomputed):
   // out = r + BN_L(h_L), or r - BN_L(h_L) with sub (the reconstruction); with
   // couple_fwd h_L is recomputed from h_{L-1}, else read from s.h[L].
-  void coupling(const ResidualFn& fn, Scratch& s, const void* r, void* out, bool sub,
-                hipStream_t st);
+  // With next / ns (and couple_next), the same launch also runs next's first
+  // conv on out, into ns->h[0] and ns->part (then next's recompute passes
+  // first_done); returns whether it did.
+  bool coupling(const ResidualFn& fn, Scratch& s, const void* r, void* out, bool sub,
+                hipStream_t st, const ResidualFn* next = nullptr, Scratch* ns = nullptr);
   bool conv(const ConvArgs& a, int ep, hipStream_t st);
   ConvArgs conv_args(const ConvLayer& cv) const;
   void wgrad_splits(const ConvLayer& cv, int* splits, int* rows_per_split) const;

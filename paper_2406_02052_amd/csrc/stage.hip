@@ -163,6 +163,10 @@ Stage::Stage(const petra_stage_desc& d) : desc(d) {
     ConvArgs a = conv_args(cv);
     a.c_in = cv.cin; a.c_out = cv.cout; a.k_tot = cv.r * cv.s * cv.cin;
     couple_fwd = conv1x1_couple_ok(dt, a);
+    const ConvLayer& c0 = convs[blocks[0].g.conv[0]];
+    ConvArgs b = conv_args(c0);
+    b.c_in = c0.cin; b.c_out = c0.cout; b.k_tot = c0.r * c0.s * c0.cin;
+    couple_next = couple_fwd && conv1x1_couple_next_ok(dt, a, b);
   }
   const int nfn = 2 * static_cast<int>(blocks.size());
   plan_b.assign(defer_wgrad ? std::max(2, nfn) : 2, ScratchPlan{});
@@ -307,9 +311,10 @@ void Stage::wgrad_splits(const ConvLayer& cv, int* splits, int* rows_per_split) 
 }
 
 void Stage::fn_recompute(const ResidualFn& fn, const void* u, Scratch& s, bool running,
-                         hipStream_t st, bool stats_only_last) {
+                         hipStream_t st, bool stats_only_last, bool first_done) {
   for (int l = 0; l < fn.nconv; ++l) {
     const bool stats_only = stats_only_last && l == fn.nconv - 1;
+    const bool done = first_done && l == 0;
     const ConvLayer& cv = convs[fn.conv[l]];
     const BnLayer& bn = bns[cv.bn];
     ConvArgs a = conv_args(cv);
@@ -330,11 +335,14 @@ void Stage::fn_recompute(const ResidualFn& fn, const void* u, Scratch& s, bool r
       return;
     }
     const int tiles = conv_row_tiles(dt, a, EP_STATS);
-    prof.begin(st);
-    conv(a, EP_STATS, st);
-    prof.end(K_CONV_FPROP, st, 2.0 * M * cv.cout * a.k_tot,
-             static_cast<double>(esz) * (static_cast<double>(M) * (cv.cin + (stats_only ? 0 : cv.cout)) +
-                                         static_cast<double>(cv.cout) * a.k_tot));
+    if (!done) {
+      prof.begin(st);
+      conv(a, EP_STATS, st);
+      prof.end(K_CONV_FPROP, st, 2.0 * M * cv.cout * a.k_tot,
+               static_cast<double>(esz) *
+                   (static_cast<double>(M) * (cv.cin + (stats_only ? 0 : cv.cout)) +
+                    static_cast<double>(cv.cout) * a.k_tot));
+    }
     prof.begin(st);
     bn_stats_finalize(s.part, tiles, cv.cout, M, v_th + bn.g_off, v_th + bn.b_off, desc.bn_eps,
                       s.vec(l, V_SCALE, cmax), s.vec(l, V_SHIFT, cmax), s.vec(l, V_MEAN, cmax),
@@ -344,18 +352,43 @@ void Stage::fn_recompute(const ResidualFn& fn, const void* u, Scratch& s, bool r
   }
 }
 
-void Stage::fn_forward(const ResidualFn& fn, const void* u, const void* r, void* y, Scratch& s,
-                       hipStream_t st) {
+bool Stage::fn_forward(const ResidualFn& fn, const void* u, const void* r, void* y, Scratch& s,
+                       hipStream_t st, bool first_done, const ResidualFn* next) {
   // with couple_fwd the last conv writes its statistics only
-  fn_recompute(fn, u, s, false, st, couple_fwd);
-  coupling(fn, s, r, y, false, st);
+  fn_recompute(fn, u, s, false, st, couple_fwd, first_done);
+  // y = r + BN_L(h_L), and (couple_next) the next function's first conv on y,
+  // into the same scratch set
+  return coupling(fn, s, r, y, false, st, next, &s);
 }
 
-void Stage::coupling(const ResidualFn& fn, Scratch& s, const void* r, void* out, bool sub,
-                     hipStream_t st) {
+bool Stage::coupling(const ResidualFn& fn, Scratch& s, const void* r, void* out, bool sub,
+                     hipStream_t st, const ResidualFn* next, Scratch* ns) {
   const int L = fn.nconv - 1;
   const ConvLayer& cv = convs[fn.conv[L]];
   const int c = cv.cout;
+  if (couple_next && next != nullptr && ns != nullptr) {
+    const ConvLayer& c0 = convs[next->conv[0]];
+    ConvArgs a = conv_args(cv);
+    a.src = s.h[L - 1];
+    a.c_in = cv.cin;
+    a.c_split = cv.cin;
+    a.pro_scale = s.vec(L - 1, V_SCALE, cmax);
+    a.pro_shift = s.vec(L - 1, V_SHIFT, cmax);
+    a.wt = static_cast<const char*>(v_wf) + cv.w_off * esz;
+    a.out = out;
+    a.resid = r;
+    a.c_out = c;
+    a.k_tot = cv.r * cv.s * cv.cin;
+    const NextConv nx{static_cast<const char*>(v_wf) + c0.w_off * esz, ns->h[0], ns->part};
+    prof.begin(st);
+    if (!conv1x1_couple(dt, a, s.vec(L, V_SCALE, cmax), s.vec(L, V_SHIFT, cmax), sub, st, &nx))
+      launch_error = true;
+    prof.end(K_CONV_FPROP, st, 2.0 * M * (c * a.k_tot + c0.cout * c0.cin),
+             static_cast<double>(esz) *
+                 (static_cast<double>(M) * (cv.cin + 2.0 * c + c0.cout) +
+                  static_cast<double>(c) * a.k_tot + static_cast<double>(c0.cout) * c0.cin));
+    return true;
+  }
   if (couple_fwd) {
     // h_L recomputed from the layer's input (the same bits as the statistics pass)
     ConvArgs a = conv_args(cv);
@@ -375,7 +408,7 @@ void Stage::coupling(const ResidualFn& fn, Scratch& s, const void* r, void* out,
     prof.end(K_CONV_FPROP, st, 2.0 * M * c * a.k_tot,
              static_cast<double>(esz) * (static_cast<double>(M) * (cv.cin + 2.0 * c) +
                                          static_cast<double>(c) * a.k_tot));
-    return;
+    return false;
   }
   prof.begin(st);
   if (sub)
@@ -383,6 +416,7 @@ void Stage::coupling(const ResidualFn& fn, Scratch& s, const void* r, void* out,
   else
     combine_fwd(dt, r, s.h[L], s.vec(L, V_SCALE, cmax), s.vec(L, V_SHIFT, cmax), out, M, c, st);
   prof.end(sub ? K_COMBINE_BWD : K_COMBINE_FWD, st, 0.0, 3.0 * M * c * esz);
+  return false;
 }
 
 bool Stage::conv(const ConvArgs& a, int ep, hipStream_t st) {
@@ -559,9 +593,12 @@ void Stage::forward_with(const void* x1, const void* x2, void* y1, void* y2, Scr
                          hipStream_t st) {
   const void* a1 = x1;
   const void* a2 = x2;
-  for (const Block& b : blocks) {
-    fn_forward(b.f, a2, a1, y1, s, st);   // y1 = x1 + F(x2)
-    fn_forward(b.g, y1, a2, y2, s, st);   // y2 = x2 + G(y1)
+  bool done = false;   // the next function's first conv ran inside a coupling
+  for (size_t bi = 0; bi < blocks.size(); ++bi) {
+    const Block& b = blocks[bi];
+    const ResidualFn* after = bi + 1 < blocks.size() ? &blocks[bi + 1].f : nullptr;
+    done = fn_forward(b.f, a2, a1, y1, s, st, done, &b.g);    // y1 = x1 + F(x2)
+    done = fn_forward(b.g, y1, a2, y2, s, st, done, after);   // y2 = x2 + G(y1)
     a1 = y1;
     a2 = y2;
   }
@@ -622,6 +659,7 @@ void Stage::backward(const void* y1, const void* y2, const void* dy1, const void
     c1 = bx1; c2 = bx2; g1 = bdx1; g2 = bdx2;
   }
   const int nf = static_cast<int>(fl.size());
+  std::vector<char> first_done(static_cast<size_t>(nf), 0);   // first conv run by a coupling
   // scratch set of function f: its own when deferring, else alternating
   auto S = [&](int f) -> Scratch& { return defer ? sb[f] : sb[f & 1]; };
   if (rb || wb) PETRA_HIP(hip_status, hipEventRecord(ev_start, st));
@@ -659,7 +697,7 @@ void Stage::backward(const void* y1, const void* y2, const void* dy1, const void
       // recompute of the next function (its input is this function's
       // reconstruction); its scratch set was last used by function f - 1
       if (rb && f >= 1) PETRA_HIP(hip_status, hipStreamWaitEvent(rs, ev_gdone[p ^ 1], 0));
-      fn_recompute(*fl[f + 1].fn, fl[f + 1].u, *sn, true, rs);
+      fn_recompute(*fl[f + 1].fn, fl[f + 1].u, *sn, true, rs, false, first_done[f + 1] != 0);
       if (rb) PETRA_HIP(hip_status, hipEventRecord(ev_rec[p ^ 1], rs));
     }
     fn_grad(fl[f], sc, nx, sn, st, wst, rs, f >= 1, p, 1, &dsrc);
@@ -676,7 +714,12 @@ void Stage::backward(const void* y1, const void* y2, const void* dy1, const void
       // input, which this function's weight gradients read
       if (rs != wst) PETRA_HIP(hip_status, hipStreamWaitEvent(rs, ev_wgdone[p], 0));
       const BwdFn& nx = fl[f + 1];
-      coupling(*nx.fn, *sn, nx.v, nx.xrec, true, rs);
+      // with one scratch set per function (one stream), the reconstruction also
+      // runs the first conv of the function after next, whose input it is
+      const bool fuse = defer && !rb && f + 2 < nf && fl[f + 2].u == nx.xrec;
+      const bool ran = coupling(*nx.fn, *sn, nx.v, nx.xrec, true, rs,
+                                fuse ? fl[f + 2].fn : nullptr, fuse ? &S(f + 2) : nullptr);
+      if (fuse && ran) first_done[f + 2] = 1;
     }
   }
   defer_cur = false;
