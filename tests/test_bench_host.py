@@ -72,3 +72,15 @@ def test_roofline_picks_the_kernel_with_most_device_time():
     assert abs(rl["achieved"] - 200.0) < 1e-9 and abs(rl["frac"] - 200.0 / 8000.0) < 1e-12
     rl = bench.roofline([("c", 0, 1, 1.0, 1e12, 1e9)], "bf16")
     assert rl["bound"] == "mfma" and abs(rl["achieved"] - 1000.0) < 1e-9
+
+
+def test_roofline_skips_launch_bound_finalize_kernels():
+    """A BN finalize (class 4 or 5) with the largest summed time does not
+    become the roofline kernel: it is launch-latency bound, and the kernel with
+    the most time among the others is taken (only finalizes: the largest)."""
+    kernels = [("conv", 0, 12, 2.0, 1e9, 6.0e8), ("fin", 4, 36, 3.0, 0.0, 5.0e6),
+               ("bfin", 5, 18, 1.0, 0.0, 2.0e6)]
+    rl = bench.roofline(kernels, "bf16")
+    assert rl["kernel"] == "conv"
+    rl = bench.roofline([("fin", 4, 36, 3.0, 0.0, 5.0e6), ("bfin", 5, 18, 1.0, 0.0, 2.0e6)], "bf16")
+    assert rl["kernel"] == "fin"
