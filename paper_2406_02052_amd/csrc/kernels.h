@@ -83,9 +83,9 @@ int conv_row_tiles(int dtype, const ConvArgs& a, int ep);
 // exactly as conv_gemm (EP_STATS, no prologue) would write them from the
 // stored coupling output (the same partial rows: conv_row_tiles of that conv).
 struct NextConv {
-  const void* wt;   // [K][N] weights of the next function's first conv
-  void* out;        // [m][K] its pre-BN output
-  float* partials;  // [grid][3][K] its BN partials
+  const void* wt;   // [32][128] weights (c_out x c_in) of the next function's first conv
+  void* out;        // [m][32] its pre-BN output
+  float* partials;  // [tiles][3][32] its BN partials (tiles = conv_row_tiles of that conv)
 };
 bool conv1x1_couple_ok(int dtype, const ConvArgs& a);
 // Whether the coupling of `a` can also run `next` (that first conv, EP_STATS).
