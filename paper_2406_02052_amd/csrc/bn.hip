@@ -15,9 +15,14 @@ namespace bnk {
 // Finalize kernels: one 256-thread block per channel.  Thread t takes tiles
 // t, t + 256, ... (loads of up to FIN_U tiles in flight), then the block's
 // sums are combined in a fixed tree: xor-shuffle levels inside each wave,
-// then the four wave results in order.  Deterministic run to run.
+// then the four wave results in order.  Deterministic run to run.  The
+// summation order does not depend on FIN_U; FIN_U = 2 keeps the statistics
+// finalize at 44 VGPRs, so that one of its waves fits on a SIMD beside two
+// waves of the whole-image conv (up to 232 VGPRs each).  With FIN_U = 4 (64
+// VGPRs) it waited for a CU that conv did not hold (ImageNet32-shaped stage
+// step 3.131 -> 3.117 ms).
 constexpr int FIN_THREADS = 256;
-constexpr int FIN_U = 4;
+constexpr int FIN_U = 2;
 static_assert(FIN_THREADS == 256, "the wave results are combined as four");
 
 // Sum of (a, b) over partials[tile][2][c] for channel ch.

@@ -1223,17 +1223,25 @@ __global__ __launch_bounds__(256, 2) void conv_fp_kernel(ConvArgs a) {
 }
 
 // Whole-image 3x3 / stride 1 / pad 1 conv for the MFMA-bound shapes: one
-// 512-thread workgroup per TH x TW image, C_in = 32 * CH, C_out = 128.
-//  * The (TH+2) x (TW+2) input patch of every input chunk is loaded into LDS
-//    once (prologue applied there, chunk c + 1 in flight while chunk c parks).
-//  * The reduction runs in k order (k = tap * C_in + c), so two consecutive
-//    32-wide steps are one contiguous 128-byte run of every weight row: the
-//    workgroup stages weight slabs of two steps through a double-buffered LDS
-//    slab with full-line loads issued one slab ahead, one barrier per slab.
+// 512-thread workgroup per TH x TW image (TW = 16: a 16-pixel MFMA fragment is
+// one image row), C_in = 32 * CH, C_out = 128.
+//  * The reduction runs chunk-major (k step s = c * 9 + tap over the 32-channel
+//    input chunks c), so the MFMAs start as soon as chunk 0 of the (TH+2) x
+//    (TW+2) input patch is in LDS; the later chunks are loaded meanwhile
+//    (prologue applied while parking) and parked one slab before their first
+//    use.
+//  * Weights go through double-buffered LDS slabs of one tap row (3 k steps of
+//    32 channels, 64 bytes of every weight row each), loaded two slabs ahead,
+//    one barrier per slab.
+//  * LDS rows are 64 bytes (32 bf16) with the four 16-byte chunks of a row
+//    permuted by bits 1-2 of the row index: the 16 consecutive rows a fragment
+//    read touches then fall in distinct banks (ds_read_b128 measured at full
+//    LDS bandwidth, against half of it for 80- or 144-byte padded rows).
 //  * The MFMA is issued as D[cout][pixel] = W x patch^T: each lane ends with 4
 //    consecutive output channels of one pixel, stored directly (8 bytes), and
 //    the BN statistics are shifted sums in registers reduced once at the end.
-// Partial row of the statistics = blockIdx.x (the image).
+// The tile is the whole image (the launcher checks h = TH, w = TW), so every
+// output pixel is valid.  Partial row of the statistics = blockIdx.x (the image).
 template <int TH, int TW, int CH, int EP, int PRO, int NWM, int NWN>
 __global__ __launch_bounds__(64 * NWM * NWN, 1) void conv_img_kernel(ConvArgs a) {
   using T = bf16_t;
@@ -1242,19 +1250,17 @@ __global__ __launch_bounds__(64 * NWM * NWN, 1) void conv_img_kernel(ConvArgs a)
   constexpr int BN = 128, BM = TH * TW;
   constexpr int TM = BM / WAVES_M, TN = BN / WAVES_N;
   constexpr int FM = TM / 16, FN = TN / 16;
-  static_assert(TM % 16 == 0 && BM % 64 == 0, "tile");
+  static_assert(TW == 16 && TM % 16 == 0 && TN % 16 == 0, "fragments are image rows");
+  static_assert(NT == BN * 4, "one 16-byte weight load per thread and k step");
   constexpr int HTH = TH + 2, HTW = TW + 2, HPIX = HTH * HTW;
-  constexpr int HP = 40;                             // bf16 per patch pixel and chunk (32 + pad)
-  constexpr int PLANE = HPIX * HP;
-  constexpr int P_CHUNKS = (HPIX * 4 + NT - 1) / NT;
-  constexpr int STEPS = CH * 9;                      // 32-wide k steps
-  static_assert(STEPS % 2 == 0, "two steps per slab");
-  constexpr int SLABS = STEPS / 2;
-  constexpr int SP = 72;                             // bf16 per weight row of a slab (64 + pad)
-  constexpr int SLAB = BN * SP;
-  constexpr int S_CHUNKS = BN * 8 / NT;              // 16-byte weight loads per thread and slab
+  constexpr int PLANE = HPIX * 32;                   // bf16 per input chunk (64 bytes per pixel)
+  constexpr int P_CHUNKS = (HPIX * 4 + NT - 1) / NT; // 16-byte patch loads per thread and chunk
+  constexpr int WPLANE = BN * 32;                    // bf16 per k step of a weight slab
+  constexpr int SLAB = 3 * WPLANE;                   // one tap row: 3 k steps
+  constexpr int SLABS = CH * 3;                      // slab j: chunk j / 3, tap row j % 3
   constexpr bool BWD = PRO == PRO_BWD;
   constexpr bool STATS = EP == EP_STATS;
+  constexpr int NCS = 1;                             // input chunks in flight in registers
   __shared__ __attribute__((aligned(16))) T lds[CH * PLANE + 2 * SLAB];
   __shared__ float pro_tab[BWD ? 4 : 2][PRO == PRO_NONE ? 1 : CH * 32];
   __shared__ float red[WAVES_M][3][BN];
@@ -1277,31 +1283,26 @@ __global__ __launch_bounds__(64 * NWM * NWN, 1) void conv_img_kernel(ConvArgs a)
   const __amdgpu_buffer_rsrc_t r_res = make_rsrc(a.resid != nullptr ? a.resid : a.out,
                                                  a.resid != nullptr ? out_bytes : 0);
 
-  // Weight slab j holds k = 64 j .. 64 j + 63 of every output channel; thread
-  // q loads 16 bytes of row q / 8, so 8 neighbouring threads read one row's
-  // 128 bytes.
-  // Two register sets: slab j + 1 is loaded one iteration before it is parked,
-  // so its L2 latency hides behind two slabs of MFMA work.
-  Raw8<T> rs0[S_CHUNKS], rs1[S_CHUNKS];
-  auto load_slab = [&](Raw8<T>* rs, int j) {
+  // Weight slab j (chunk c = j / 3, tap row dy = j % 3), k step u = dx: input
+  // channels c*32 .. c*32+31 of tap 3 dy + dx.  Thread t loads 16 bytes of row
+  // t / 4 per k step, so 4 neighbouring threads read one 64-byte run.
+  const int s_row = tid >> 2, s_sub = tid & 3;
+  const uint32_t s_gl = static_cast<uint32_t>((s_row * a.k_tot + s_sub * 8) * 2);
+  const int s_lds = s_row * 32 + ((s_sub ^ ((s_row >> 1) & 3)) * 8);
+  u32x4_t rs[2][3];
+  auto load_slab = [&](u32x4_t* r, int j) {
+    const int c = j / 3, dy = j - c * 3;
 #pragma unroll
-    for (int i = 0; i < S_CHUNKS; ++i) {
-      const int q = tid + NT * i;
-      const int row = q >> 3, sub = q & 7;
-      rs[i].set(buf_load16(r_wt, static_cast<uint32_t>((row * a.k_tot + j * 64 + sub * 8) * 2)));
-    }
+    for (int u = 0; u < 3; ++u)
+      r[u] = buf_load16(r_wt, s_gl + static_cast<uint32_t>(((3 * dy + u) * a.c_in + c * 32) * 2));
   };
-  auto park_slab = [&](const Raw8<T>* rs, int buf) {
+  auto park_slab = [&](const u32x4_t* r, int buf) {
 #pragma unroll
-    for (int i = 0; i < S_CHUNKS; ++i) {
-      const int q = tid + NT * i;
-      const int row = q >> 3, sub = q & 7;
-      *reinterpret_cast<uint4*>(slabs + buf * SLAB + row * SP + sub * 8) =
-          make_uint4(rs[i].w[0], rs[i].w[1], rs[i].w[2], rs[i].w[3]);
-    }
+    for (int u = 0; u < 3; ++u)
+      *reinterpret_cast<u32x4_t*>(slabs + buf * SLAB + u * WPLANE + s_lds) = r[u];
   };
-  load_slab(rs0, 0);
-  load_slab(rs1, SLABS > 1 ? 1 : 0);
+  load_slab(rs[0], 0);
+  if (SLABS > 1) load_slab(rs[1], 1);
 
   if constexpr (PRO == PRO_RELU) {
     for (int i = tid; i < a.c_in; i += NT) {
@@ -1317,7 +1318,8 @@ __global__ __launch_bounds__(64 * NWM * NWN, 1) void conv_img_kernel(ConvArgs a)
     }
   }
 
-  // Patch fill, one chunk at a time with the next chunk's loads in flight.
+  // Input patch: thread t takes 16-byte pieces q = t + NT i (patch pixel q / 4,
+  // channels (q % 4) * 8 .. + 7 of a chunk).
   int p_off[P_CHUNKS];
   uint32_t pvalid = 0;
 #pragma unroll
@@ -1330,8 +1332,9 @@ __global__ __launch_bounds__(64 * NWM * NWN, 1) void conv_img_kernel(ConvArgs a)
     p_off[i] = ok ? static_cast<int>(((img_base + static_cast<long>(ih) * a.w + iw) * a.c_in + sub * 8) * 2) : -1;
     pvalid |= ok ? 1u << i : 0u;
   }
-  Raw8<T> ph[2][P_CHUNKS], phh[2][BWD ? P_CHUNKS : 1];
-  auto load_chunk = [&](int c, int slot) {
+  Raw8<T> ph[NCS][P_CHUNKS], phh[NCS][BWD ? P_CHUNKS : 1];
+  auto load_chunk = [&](int c) {
+    const int slot = c % NCS;
 #pragma unroll
     for (int i = 0; i < P_CHUNKS; ++i) {
       const uint32_t off = p_off[i] >= 0 ? static_cast<uint32_t>(p_off[i] + c * 64) : BUF_OOB;
@@ -1339,7 +1342,8 @@ __global__ __launch_bounds__(64 * NWM * NWN, 1) void conv_img_kernel(ConvArgs a)
       if constexpr (BWD) phh[slot][i].set(buf_load16(r_proh, off));
     }
   };
-  auto park_chunk = [&](int c, int slot) {
+  auto park_chunk = [&](int c) {
+    const int slot = c % NCS;
     T* dst = patch + c * PLANE;
 #pragma unroll
     for (int i = 0; i < P_CHUNKS; ++i) {
@@ -1352,63 +1356,67 @@ __global__ __launch_bounds__(64 * NWM * NWN, 1) void conv_img_kernel(ConvArgs a)
                      pro_tab[BWD ? 3 : 0], c * 32 + sub * 8);
         if (!((pvalid >> i) & 1u)) r.zero();
       }
-      *reinterpret_cast<uint4*>(dst + hp * HP + sub * 8) = make_uint4(r.w[0], r.w[1], r.w[2], r.w[3]);
+      *reinterpret_cast<uint4*>(dst + hp * 32 + ((sub ^ ((hp >> 1) & 3)) * 8)) =
+          make_uint4(r.w[0], r.w[1], r.w[2], r.w[3]);
     }
   };
-  load_chunk(0, 0);
-  if constexpr (PRO != PRO_NONE) __syncthreads();   // prologue table
 #pragma unroll
-  for (int c = 0; c < CH; ++c) {
-    if (c + 1 < CH) load_chunk(c + 1, (c + 1) & 1);
-    park_chunk(c, c & 1);
-  }
-  park_slab(rs0, 0);
+  for (int c = 0; c < NCS && c < CH; ++c) load_chunk(c);
+  if constexpr (PRO != PRO_NONE) __syncthreads();   // prologue table
+  park_chunk(0);
+  if (NCS < CH) load_chunk(NCS);
+  park_slab(rs[0], 0);
   __syncthreads();
 
-  int rowpix[FM];
+  // Fragment addresses.  Weights: row wn*TN + fn*16 + lr of a k-step plane,
+  // whose chunk permutation is (lr >> 1) & 3.  Patch: fragment fm of tap
+  // (dy, dx) reads pixel (rb + fm + dy) * HTW + dx + lr of a chunk plane (rb =
+  // wm * FM, the wave's first image row); bits 1-2 of that index are
+  // (rb + fm + dy + ((dx + lr) >> 1)) & 3, so the lane's offsets for the 3
+  // values of dx and the 4 values of (fm + dy) & 3 are computed once here.
+  const int rb = wm * FM;
+  const int w_off = (wn * TN + lr) * 32 + ((lg ^ ((lr >> 1) & 3)) * 8);
+  int p_tab[3][4];
 #pragma unroll
-  for (int fm = 0; fm < FM; ++fm) {
-    const int i = wm * TM + fm * 16 + lr;
-    const int ph_ = i / TW, pw = i - ph_ * TW;
-    rowpix[fm] = ph_ * HTW + pw;
-  }
+  for (int dx = 0; dx < 3; ++dx)
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      p_tab[dx][k] = (rb * HTW + dx + lr) * 32 + ((lg ^ ((k + rb + ((dx + lr) >> 1)) & 3)) * 8);
+
   f32x4_t acc[FM][FN];
 #pragma unroll
   for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
     for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  // Iteration j: slab j + 2 into the set that held slab j, MFMAs on slab j from
-  // LDS, then slab j + 1 (loaded an iteration earlier) parked into the other
-  // LDS buffer.  Loads past the end re-read the last slab (never parked), so
-  // the number of loads in flight is the same every iteration.
-  auto slab_iter = [&](int j, Raw8<T>* rs_load, const Raw8<T>* rs_park) {
-    const int buf = j & 1;
-    load_slab(rs_load, min(j + 2, SLABS - 1));
+  // Slab j: slab j + 2 into the register set that held slab j, MFMAs on slab j
+  // from LDS buffer j % 2, slab j + 1 (loaded an iteration earlier) parked into
+  // the other buffer, and before the last slab of a chunk the next chunk parked.
+#pragma unroll
+  for (int j = 0; j < SLABS; ++j) {
+    const int c = j / 3, dy = j - c * 3, buf = j & 1;
+    if (j + 2 < SLABS) load_slab(rs[j & 1], j + 2);
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int s = 2 * j + u;              // k = 32 s .. 32 s + 31
-      const int tap = s / CH, chunk = s - tap * CH;
-      const T* pt = patch + chunk * PLANE + ((tap / 3) * HTW + (tap % 3)) * HP + lg * 8;
-      const T* sb = slabs + buf * SLAB + (wn * TN + lr) * SP + u * 32 + lg * 8;
+    for (int dx = 0; dx < 3; ++dx) {
       Frag<T> wf[FN], pf[FM];
 #pragma unroll
-      for (int fn = 0; fn < FN; ++fn) wf[fn].load(sb + fn * 16 * SP);
+      for (int fn = 0; fn < FN; ++fn) wf[fn].load(slabs + buf * SLAB + dx * WPLANE + fn * 16 * 32 + w_off);
 #pragma unroll
-      for (int fm = 0; fm < FM; ++fm) pf[fm].load(pt + rowpix[fm] * HP);
+      for (int fm = 0; fm < FM; ++fm)
+        pf[fm].load(patch + c * PLANE + (fm + dy) * HTW * 32 + p_tab[dx][(fm + dy) & 3]);
 #pragma unroll
       for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
         for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma(wf[fn], pf[fm], acc[fm][fn]);
     }
     __builtin_amdgcn_sched_barrier(0);
-    if (j + 1 < SLABS) park_slab(rs_park, buf ^ 1);
+    if (dy == 2 && c + 1 < CH) {
+      park_chunk(c + 1);
+      if (c + 1 + NCS < CH) load_chunk(c + 1 + NCS);
+    }
+    if (j + 1 < SLABS) park_slab(rs[(j + 1) & 1], buf ^ 1);
     __syncthreads();
-  };
-  for (int j = 0; j < SLABS; j += 2) {
-    slab_iter(j, rs0, rs1);
-    if (j + 1 < SLABS) slab_iter(j + 1, rs1, rs0);
   }
 
   // Epilogue: lane (lr, lg) holds channels wn*TN + fn*16 + lg*4 + e of pixel
@@ -1434,11 +1442,11 @@ __global__ __launch_bounds__(64 * NWM * NWN, 1) void conv_img_kernel(ConvArgs a)
   float nv = 0.f;
 #pragma unroll
   for (int fm = 0; fm < FM; ++fm) {
-    const int i = wm * TM + fm * 16 + lr;
-    const int ph_ = i / TW, pw = i - ph_ * TW;
-    const bool vm = ph_ < a.h && pw < a.w;
-    nv += vm ? 1.f : 0.f;
-    const uint32_t pixoff = vm ? static_cast<uint32_t>(((img_base + static_cast<long>(ph_) * a.w + pw) * BN) * 2) : BUF_OOB;
+    // image row rb + fm, column lr: every pixel of the tile is in the image
+    constexpr bool vm = true;
+    nv += 1.f;
+    const uint32_t pixoff =
+        static_cast<uint32_t>(((img_base + static_cast<long>(rb + fm) * TW + lr) * BN) * 2);
 #pragma unroll
     for (int fn = 0; fn < FN; ++fn) {
       const uint32_t boff = vm ? pixoff + (wn * TN + fn * 16 + lg * 4) * 2 : BUF_OOB;
@@ -3496,6 +3504,9 @@ bool launch_halo(const ConvArgs& a, int ep, hipStream_t st) {
 constexpr int IMG_WM = 4, IMG_WN = 2;
 template <int TH, int TW, int CH>
 bool launch_img(const ConvArgs& a, int ep, hipStream_t st) {
+  // the tile is the whole image, and every weight row is c_in * 9 long
+  if (a.h != TH || a.w != TW || a.c_in != 32 * CH || a.c_out != 128 || a.k_tot != 9 * a.c_in)
+    return false;
   return dispatch_ep_pro(ep, pro_mode(a), [&](auto k) {
     PETRA_LAUNCH((conv_img_kernel<TH, TW, CH, decltype(k)::ep, decltype(k)::pro, IMG_WM, IMG_WN>),
                  dim3(a.n), dim3(64 * IMG_WM * IMG_WN), 0, st, a);
