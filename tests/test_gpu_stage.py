@@ -33,6 +33,11 @@ SMALL = {
     "bf16_halo_c64_2x9x16": synth.CIFAR_STAGE.with_(n=2, h=9, w=16, c_half=64, blocks=1),
     "bf16_halo_c128_1x9x16": synth.IMAGENET32_STAGE.with_(n=1, h=9, w=16, blocks=2),
     "bf16_halo_bottleneck_1x5x56": synth.IMAGENET_BOTTLENECK_STAGE.with_(n=1, h=5, w=56, blocks=1),
+    # whole-image conv (16x16, 128 channels: one workgroup per image) and the
+    # weight gradient that splits the 9 taps over three waves, at batches of
+    # one and two images (the weight gradient then has as many splits as tiles)
+    "bf16_img_c128_2x16x16": synth.IMAGENET32_STAGE.with_(n=2, h=16, w=16, blocks=2),
+    "bf16_img_c128_1x16x16": synth.IMAGENET32_STAGE.with_(n=1, h=16, w=16, blocks=1),
     # streaming 1x1 convs (128 -> 32, 32 -> 128): 1587 pixels = 100 units of 16
     # (the last one 3 pixels) over 25 workgroups; 18769 pixels = 1174 units (the
     # last one a single pixel) over the full 256-workgroup grid, 1-2 units a wave
