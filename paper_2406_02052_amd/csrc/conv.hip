@@ -3704,8 +3704,13 @@ int wgrad_tr_plan(int dtype, const WgradArgs& a, int* splits) {
                               : ((a.w + tw - 1) / tw) * ((a.h + th - 1) / th) * a.n;
   const int per = (a.c_out / bo) * (a.c_in / bc);
   // about half a workgroup per CU and layer: the backward launches the weight
-  // gradients of all but one layer together, so fewer, longer splits win
-  if (splits) *splits = std::max(1, std::min(ntiles, 128 / per));
+  // gradients of all but one layer together, so fewer, longer splits win.  The
+  // bottleneck plans (2, 5, 6), whose grouped launches run beside the backward
+  // chain on the forward stream, take three quarters (measured at 64x56x56:
+  // 32 / 64 / 128 / 192 / 256 splits per layer, step 1.737 / 1.620 / 1.562 /
+  // 1.554 / 1.560 ms; CIFAR and ImageNet32 shapes are slower at 192).
+  const int budget = (cfg == 2 || cfg == 5 || cfg == 6) ? 192 : 128;
+  if (splits) *splits = std::max(1, std::min(ntiles, budget / per));
   return cfg;
 }
 
