@@ -3708,8 +3708,11 @@ int wgrad_tr_plan(int dtype, const WgradArgs& a, int* splits) {
   // bottleneck plans (2, 5, 6), whose grouped launches run beside the backward
   // chain on the forward stream, take three quarters (measured at 64x56x56:
   // 32 / 64 / 128 / 192 / 256 splits per layer, step 1.737 / 1.620 / 1.562 /
-  // 1.554 / 1.560 ms; CIFAR and ImageNet32 shapes are slower at 192).
-  const int budget = (cfg == 2 || cfg == 5 || cfg == 6) ? 192 : 128;
+  // 1.554 / 1.560 ms); the 16x16 plan (3) a little less (ImageNet32-shaped
+  // stage with 16 / 24 / 32 splits per layer: 3.065 / 3.056 / 3.078 ms; 48
+  // splits on another box 3.20 against 3.09 ms with 32).  CIFAR-shaped: 64 /
+  // 96 / 128 splits 0.414 / 0.412 / 0.412 ms, 192 on another box 0.420 ms.
+  const int budget = (cfg == 2 || cfg == 5 || cfg == 6) ? 192 : cfg == 3 ? 96 : 128;
   if (splits) *splits = std::max(1, std::min(ntiles, budget / per));
   return cfg;
 }
