@@ -3712,7 +3712,9 @@ int wgrad_tr_plan(int dtype, const WgradArgs& a, int* splits) {
   // stage with 16 / 24 / 32 splits per layer: 3.065 / 3.056 / 3.078 ms; 48
   // splits on another box 3.20 against 3.09 ms with 32).  CIFAR-shaped: 64 /
   // 96 / 128 splits 0.414 / 0.412 / 0.412 ms, 192 on another box 0.420 ms.
-  const int budget = (cfg == 2 || cfg == 5 || cfg == 6) ? 192 : cfg == 3 ? 96 : 128;
+  // The 8x8 plan (4) in the 4-stage schedule: budget 32 / 48 / 64 / 128 / 192,
+  // tick 3.047 / 3.045 / 3.044 / 3.065 / 3.081 ms.
+  const int budget = (cfg == 2 || cfg == 5 || cfg == 6) ? 192 : cfg == 3 ? 96 : cfg == 4 ? 64 : 128;
   if (splits) *splits = std::max(1, std::min(ntiles, budget / per));
   return cfg;
 }
