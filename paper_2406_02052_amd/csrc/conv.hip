@@ -858,9 +858,10 @@ __global__ __launch_bounds__(256) void conv_halo_kernel(ConvArgs a) {
   constexpr int NSLAB = FB ? 9 : 2;
   constexpr int H_CHUNKS = (HPIX * 4 + 255) / 256;    // 16-byte patch chunks per thread
   constexpr int B_CHUNKS = ((FB ? 9 : 1) * BN * 4 + 255) / 256;
-  constexpr int BPITCH = 40;
+  // weight slab rows of 64 bytes (32 bf16), the four 16-byte chunks permuted
+  // by bits 1-2 of the row: conflict-free fragment reads
   constexpr int PATCH = HPIX * HP;
-  constexpr int SLAB = BN * BPITCH;
+  constexpr int SLAB = BN * 32;
   constexpr int MAIN_BYTES = (HB * PATCH + NSLAB * SLAB) * 2;
   constexpr int LDS_BYTES = MAIN_BYTES;
   __shared__ __attribute__((aligned(16))) unsigned char lds[LDS_BYTES];
@@ -873,6 +874,7 @@ __global__ __launch_bounds__(256) void conv_halo_kernel(ConvArgs a) {
   const int lane = tid & 63, wave = tid >> 6;
   const int wm = wave % WAVES_M, wn = wave / WAVES_M;
   const int lr = lane & 15, lg = lane >> 4;
+  const int w_off = lr * 32 + ((lg ^ ((lr >> 1) & 3)) * 8);   // weight fragment rows
   const int tiles_x = (a.w + TW - 1) / TW, tiles_y = (a.h + TH - 1) / TH;
   const int tx = blockIdx.x % tiles_x;
   const int ty = (blockIdx.x / tiles_x) % tiles_y;
@@ -957,7 +959,9 @@ __global__ __launch_bounds__(256) void conv_halo_kernel(ConvArgs a) {
       const int tap = FB ? q / (BN * 4) : 0;
       const int rem = q - tap * (BN * 4);
       T* dst = slab_base + (FB ? tap : buf) * SLAB;
-      *reinterpret_cast<uint4*>(dst + (rem >> 2) * BPITCH + (rem & 3) * 8) = make_uint4(rb[i].w[0], rb[i].w[1], rb[i].w[2], rb[i].w[3]);
+      const int row = rem >> 2, sub = rem & 3;
+      *reinterpret_cast<uint4*>(dst + row * 32 + ((sub ^ ((row >> 1) & 3)) * 8)) =
+          make_uint4(rb[i].w[0], rb[i].w[1], rb[i].w[2], rb[i].w[3]);
     }
   };
 
@@ -1011,7 +1015,7 @@ __global__ __launch_bounds__(256) void conv_halo_kernel(ConvArgs a) {
 #pragma unroll
       for (int fm = 0; fm < FM; ++fm) af[fm].load(patch_base + (rowpix[fm] + toff) * HP + lg * 8);
 #pragma unroll
-      for (int fn = 0; fn < FN; ++fn) bfr[fn].load(sb + (wn * TN + fn * 16 + lr) * BPITCH + lg * 8);
+      for (int fn = 0; fn < FN; ++fn) bfr[fn].load(sb + (wn * TN + fn * 16) * 32 + w_off);
 #pragma unroll
       for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
@@ -1035,7 +1039,7 @@ __global__ __launch_bounds__(256) void conv_halo_kernel(ConvArgs a) {
 #pragma unroll
       for (int fm = 0; fm < FM; ++fm) af[fm].load(pt + (rowpix[fm] + toff) * HP + lg * 8);
 #pragma unroll
-      for (int fn = 0; fn < FN; ++fn) bfr[fn].load(sb + (wn * TN + fn * 16 + lr) * BPITCH + lg * 8);
+      for (int fn = 0; fn < FN; ++fn) bfr[fn].load(sb + (wn * TN + fn * 16) * 32 + w_off);
 #pragma unroll
       for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
